@@ -1,0 +1,135 @@
+"""CPU oracle for region attribution over marker traces.
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` may import this package.  The product library
+(``paper_2609_12299_amd``) never imports, links or calls it; the two share no
+code.  See ``argus_oracle.cpp`` for the definitions and the paper passages
+each step follows.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "argus_oracle.cpp")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+NUM_COUNTERS = 32
+RS_WIDTH = 142
+COUNTER_NAMES = [
+    "n_records", "n_valid", "n_bad_kind", "n_bad_region", "n_begin", "n_end",
+    "ts_min", "ts_max", "n_ctx", "n_matched", "n_mismatched", "n_unclosed",
+    "n_orphan_end", "n_self_nested", "max_level", "n_overlap_skipped",
+    "ctx_min", "ctx_max",
+]
+RS = dict(count=0, incl_sum=1, excl_sum=2, incl_min=3, incl_max=4, excl_min=5,
+          excl_max=6, unclosed=7, orphan_end=8, mism_as_begin=9, mism_as_end=10,
+          self_nested=11, hist_incl=12, hist_excl=77)
+
+INSTANCE_DTYPE = np.dtype([
+    ("t_begin", "<u8"), ("t_end", "<u8"), ("ctx_key", "<u4"), ("parent", "<u4"),
+    ("level", "<u4"), ("region_id", "<u2"), ("end_region_id", "<u2"),
+])
+assert INSTANCE_DTYPE.itemsize == 32
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with g++ (single-threaded, -O2)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(["g++", "-O2", "-std=c++17", "-Wall", "-shared", "-fPIC",
+                               _SRC, "-o", tmp])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def _open(path: str):
+    lib = ctypes.CDLL(path)
+    f = lib.argus_oracle_run
+    f.restype = ctypes.c_int
+    f.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint32,
+                  ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint32,
+                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64]
+    return lib
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        _lib = _open(_LIB)
+    return _lib
+
+
+class OracleLib:
+    """The oracle entry point bound to a specific shared library (tests use
+    this to run the pins against deliberately mutated builds)."""
+
+    def __init__(self, path: str):
+        self._lib = _open(path)
+
+    def run(self, *args, **kw):
+        return run(*args, _lib=self._lib, **kw)
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+def run(records: np.ndarray, num_regions: int, num_classes: int = 0, region_class=None,
+        group_shift: int = 0, num_groups: int = 0, instances: bool = True, _lib=None) -> dict:
+    """Run the oracle on host records (uint8 [N,16] or any 16-byte-itemsize array).
+
+    Returns a dict of numpy arrays: counters [32] u64, region_stats [R,142] u64,
+    overlap_group [G,2,K,K] u64 and overlap_global [2,K,K] u64 (K > 0 only),
+    instances [n_begin] (INSTANCE_DTYPE) and instance_excl [n_begin] u64.
+    """
+    rec = np.ascontiguousarray(records)
+    nbytes = rec.nbytes
+    assert nbytes % 16 == 0, "records are 16 bytes each"
+    n = nbytes // 16
+    R, K, G = int(num_regions), int(num_classes), int(num_groups)
+    cls = None
+    if K > 0:
+        cls = np.ascontiguousarray(np.asarray(region_class, dtype=np.uint8))
+        assert cls.shape == (R,)
+    counters = np.zeros(NUM_COUNTERS, np.uint64)
+    rstats = np.zeros((R, RS_WIDTH), np.uint64)
+    og = np.zeros((G, 2, K, K), np.uint64) if K > 0 else None
+    ogl = np.zeros((2, K, K), np.uint64) if K > 0 else None
+    if instances:
+        # n_begin is at most the number of records.
+        kinds = rec.reshape(-1).view(np.uint8).reshape(n, 16)[:, 14] if n else np.zeros(0, np.uint8)
+        cap = int(np.count_nonzero(kinds == 1))
+        inst = np.zeros(cap, INSTANCE_DTYPE)
+        excl = np.zeros(cap, np.uint64)
+    else:
+        cap, inst, excl = 0, None, None
+    lib = _lib if _lib is not None else _load()
+    rc = lib.argus_oracle_run(_ptr(rec) if n else None, n, R, K, _ptr(cls), int(group_shift),
+                                  G, _ptr(counters), _ptr(rstats), _ptr(og), _ptr(ogl),
+                                  _ptr(inst), _ptr(excl), cap)
+    if rc != 0:
+        raise ValueError(f"argus_oracle_run failed with {rc}")
+    out = dict(counters=counters, region_stats=rstats)
+    if K > 0:
+        out["overlap_group"] = og
+        out["overlap_global"] = ogl
+    if instances:
+        nb = int(counters[4])
+        out["instances"] = inst[:nb]
+        out["instance_excl"] = excl[:nb]
+    return out
+
+
+def counters_dict(counters: np.ndarray) -> dict:
+    return {name: int(counters[i]) for i, name in enumerate(COUNTER_NAMES)}

@@ -1,0 +1,109 @@
+/*
+ * argus_oracle.h -- CPU reference ("oracle") for region attribution over
+ * begin/end marker traces.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This library exists so that tests, the smoke
+ * check and the benchmark's CPU-baseline leg can check the GPU library
+ * against a plain, slow, single-threaded implementation of the same
+ * definitions.  The product path never links, loads or calls it, and it
+ * shares no header, helper, table or kernel with the GPU library.
+ *
+ * What it computes follows the paper's Section 3.2 (regions are delimited
+ * by begin(id)/end(id) transitions; temporal traces recover region-labelled
+ * intervals; a per-warp nested region-context stack decides which region
+ * is innermost), Section 3.3 (the duration signal is read from a reference
+ * region trace), Section 3.5 (observed fields; reports expose attribution
+ * ambiguity) and Section 4.3 (compute/communication overlap).  Where the
+ * paper is silent the readings are the ones listed with each function in
+ * argus_oracle.cpp.
+ *
+ * Byte layouts (little-endian):
+ *   record   (16 B): u64 ts @0, u32 ctx_key @8, u16 region_id @12,
+ *                    u8 kind @14 (1 = BEGIN, 2 = END), u8 pad @15.
+ *   instance (32 B): u64 t_begin @0, u64 t_end @8, u32 ctx_key @16,
+ *                    u32 parent @20, u32 level @24, u16 region_id @28,
+ *                    u16 end_region_id @30.
+ */
+#ifndef ARGUS_ORACLE_H
+#define ARGUS_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Indices into the counters array. */
+enum {
+  ORC_N_RECORDS = 0,
+  ORC_N_VALID = 1,
+  ORC_N_BAD_KIND = 2,
+  ORC_N_BAD_REGION = 3,
+  ORC_N_BEGIN = 4,
+  ORC_N_END = 5,
+  ORC_TS_MIN = 6,
+  ORC_TS_MAX = 7,
+  ORC_N_CTX = 8,
+  ORC_N_MATCHED = 9,
+  ORC_N_MISMATCHED = 10,
+  ORC_N_UNCLOSED = 11,
+  ORC_N_ORPHAN_END = 12,
+  ORC_N_SELF_NESTED = 13,
+  ORC_MAX_LEVEL = 14,
+  ORC_N_OVERLAP_SKIPPED = 15,
+  ORC_CTX_MIN = 16,
+  ORC_CTX_MAX = 17,
+  ORC_NUM_COUNTERS = 32 /* 18..31 are always zero */
+};
+
+/* Columns of one row of the per-region statistics ([num_regions][142]). */
+enum {
+  ORC_RS_COUNT = 0,
+  ORC_RS_INCL_SUM = 1,
+  ORC_RS_EXCL_SUM = 2,
+  ORC_RS_INCL_MIN = 3,
+  ORC_RS_INCL_MAX = 4,
+  ORC_RS_EXCL_MIN = 5,
+  ORC_RS_EXCL_MAX = 6,
+  ORC_RS_UNCLOSED = 7,
+  ORC_RS_ORPHAN_END = 8,
+  ORC_RS_MISM_AS_BEGIN = 9,
+  ORC_RS_MISM_AS_END = 10,
+  ORC_RS_SELF_NESTED = 11,
+  ORC_RS_HIST_INCL = 12, /* 65 bins */
+  ORC_RS_HIST_EXCL = 77, /* 65 bins */
+  ORC_RS_WIDTH = 142
+};
+
+/*
+ * Runs the whole definition on host memory.
+ *   records        n records (16 B each).
+ *   num_regions    R, 1..65535; region_id >= R makes a record invalid.
+ *   num_classes    K, 0..8; 0 disables overlap.
+ *   region_class   [R] class of each region (>= K means unclassified);
+ *                  may be NULL when K == 0.
+ *   group_shift    group = ctx_key >> group_shift (0..32; 32 puts every
+ *                  context in group 0).
+ *   num_groups     G; contexts whose group is >= G are left out of overlap.
+ *   counters       [ORC_NUM_COUNTERS]
+ *   region_stats   [R * ORC_RS_WIDTH]
+ *   overlap_group  [G * 2 * K * K] (U matrix then Q matrix per group) or NULL
+ *   overlap_global [2 * K * K] or NULL
+ *   instances      [inst_cap] 32-byte instances or NULL
+ *   instance_excl  [inst_cap] or NULL
+ * Returns 0, -1 for bad arguments, -2 if n_begin exceeds inst_cap while an
+ * instance output was requested.
+ */
+int argus_oracle_run(const void* records, uint64_t n, uint32_t num_regions,
+                     uint32_t num_classes, const uint8_t* region_class,
+                     uint32_t group_shift, uint32_t num_groups,
+                     uint64_t* counters, uint64_t* region_stats,
+                     uint64_t* overlap_group, uint64_t* overlap_global,
+                     void* instances, uint64_t* instance_excl,
+                     uint64_t inst_cap);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif

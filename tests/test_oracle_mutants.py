@@ -1,0 +1,129 @@
+"""The pins must catch plausible mistakes in the oracle.
+
+Each mutant is a one-line textual change to a COPY of oracle/argus_oracle.cpp
+(a dropped term, a wrong sign, index or comparison), compiled into a temporary
+library.  The pin checks (hand-built traces, the depth-scan derivation, the
+brute-force overlap, generator ground truth and invariants) are run against
+it and at least one of them must fail.  The real oracle is never modified.
+"""
+from __future__ import annotations
+
+import os
+import subprocess
+
+import numpy as np
+import pytest
+
+from golden_util import (case_params, expected_counters, expected_instances,
+                         expected_region_stats, load_cases, random_malformed,
+                         random_wellformed, records_from_rows)
+from test_oracle_pins import brute_force_overlap, check_invariants, scan_derivation
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "argus_oracle.cpp")
+
+MUTANTS = {
+    "parent_dropped": ("x.parent = stack.empty() ? kNone : stack.back();", "x.parent = kNone;"),
+    "level_off_by_one": ("x.level = static_cast<uint32_t>(stack.size());",
+                         "x.level = static_cast<uint32_t>(stack.size()) + 1;"),
+    "excl_wrong_sign": ("excl[id] = (x.t_end - x.t_begin) - child_sum[id];",
+                        "excl[id] = (x.t_end - x.t_begin) + child_sum[id];"),
+    "excl_only_matched_children": ("if (is_closed(x) && x.parent != kNone)",
+                                   "if (is_matched(x) && x.parent != kNone)"),
+    "sort_ignores_time": ("return a.ts < b.ts;", "return false;"),
+    "mismatch_counted_as_match": ("return x.end_region != kNoEnd && x.end_region == x.region;",
+                                  "return x.end_region != kNoEnd;"),
+    "hist_bin_shifted": ("row[ORC_RS_HIST_INCL + bit_width(d)] += 1;",
+                         "row[ORC_RS_HIST_INCL + bit_width(d / 2)] += 1;"),
+    "u_is_or": ("if (ca > 0 && cb > 0) U[a * K + b] += gap;",
+                "if (ca > 0 || cb > 0) U[a * K + b] += gap;"),
+    "q_same_class_pairs": ("Q[a * K + b] += gap * (ca * (ca - 1) / 2);",
+                           "Q[a * K + b] += gap * (ca * ca / 2);"),
+    "min_sentinel_zero": ("row[ORC_RS_INCL_MIN] = kNoTime;", "row[ORC_RS_INCL_MIN] = 0;"),
+    "self_nested_by_end_region": ("inst[x.parent].region == x.region",
+                                  "inst[x.parent].end_region == x.region"),
+    "orphan_region_wrong": ("region_stats[uint64_t(r.region) * ORC_RS_WIDTH + ORC_RS_ORPHAN_END] += 1;",
+                            "region_stats[ORC_RS_ORPHAN_END] += 1;"),
+    "bad_region_inclusive": ("if (r.region >= num_regions) {", "if (r.region > num_regions) {"),
+    "group_shift_ignored": ("(x.ctx >> group_shift)", "(x.ctx)"),
+}
+
+
+def run_pins(orc) -> list[str]:
+    """Return the names of the pin checks that fail for oracle `orc`."""
+    failures = []
+
+    def attempt(name, fn):
+        try:
+            fn()
+        except Exception:  # noqa: BLE001 - any failure kills the mutant
+            failures.append(name)
+
+    def hand():
+        for case in load_cases():
+            p = case_params(case)
+            out = orc.run(records_from_rows(case["records"]), p["num_regions"],
+                          p["num_classes"], p["region_class"], p["group_shift"],
+                          p["num_groups"])
+            np.testing.assert_array_equal(out["counters"], expected_counters(case))
+            if "region_stats" in case:
+                np.testing.assert_array_equal(out["region_stats"], expected_region_stats(case))
+            if "instances" in case:
+                assert out["instances"].tobytes() == expected_instances(case).tobytes()
+                np.testing.assert_array_equal(out["instance_excl"],
+                                              np.array(case["excl"], np.uint64))
+            if "overlap_group" in case:
+                np.testing.assert_array_equal(out["overlap_group"],
+                                              np.array(case["overlap_group"], np.uint64))
+
+    def scan():
+        for seed in range(150):
+            rng = np.random.default_rng(seed)
+            R = 1 + seed % 5
+            rec = random_malformed(rng, 48, 1 + seed % 4, R, [3, 10, 1000][seed % 3])
+            out = orc.run(rec, R)
+            inst, excl = scan_derivation(rec, R)
+            assert out["instances"].tobytes() == inst.tobytes()
+            np.testing.assert_array_equal(out["instance_excl"], excl)
+            check_invariants(out, R)
+
+    def overlap():
+        for seed in range(60):
+            rng = np.random.default_rng(1000 + seed)
+            K, R, shift, G = 1 + seed % 3, 4, seed % 3, 1 + seed % 2
+            cls = rng.integers(0, K + 1, size=R).astype(np.uint8)
+            rec, ivs = random_wellformed(rng, 4, 6, R, max_depth=2, t_spread=20)
+            out = orc.run(rec, R, K, cls, shift, G)
+            U, Q = brute_force_overlap(ivs, K, cls, shift, G)
+            np.testing.assert_array_equal(out["overlap_group"][:, 0].astype(object), U)
+            np.testing.assert_array_equal(out["overlap_group"][:, 1].astype(object), Q)
+
+    attempt("hand_traces", hand)
+    attempt("depth_scan_derivation", scan)
+    attempt("brute_force_overlap", overlap)
+    return failures
+
+
+@pytest.fixture(scope="module")
+def mutant_dir(tmp_path_factory):
+    return tmp_path_factory.mktemp("oracle_mutants")
+
+
+def test_unmutated_oracle_passes_all_pins(oracle_mod):
+    assert run_pins(oracle_mod) == []
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(oracle_mod, mutant_dir, name):
+    old, new = MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation site for {name} not unique"
+    path = os.path.join(str(mutant_dir), f"{name}.cpp")
+    with open(path, "w") as f:
+        f.write(src.replace(old, new))
+    inc = os.path.join(ROOT, "oracle")
+    lib = os.path.join(str(mutant_dir), f"lib{name}.so")
+    subprocess.check_call(["g++", "-O1", "-std=c++17", "-shared", "-fPIC", "-I", inc, path,
+                           "-o", lib])
+    orc = oracle_mod.OracleLib(lib)
+    assert run_pins(orc), f"mutant {name} survived every pin"

@@ -1,0 +1,140 @@
+"""Seeded synthetic marker traces (input generation only).
+
+Five workload shapes, after the paper's evaluation (Section 4):
+
+====  ==========================================================  ==========
+cfg   shape                                                       records
+====  ==========================================================  ==========
+1     tiny well-formed: 8 SMs x 4 warps, depth <= 3, 8 regions,  2^16
+      shuffled within 4 KiB chunks
+2     persistent GEMM (Section 4.1): 256 blocks x 8 warps,        2^24
+      producer/consumer stage regions inside per-tile regions
+3     decode megakernel (Section 4.2): 256 blocks x 16 warps,    2^26 - 33554
+      22 layers x 8 operators + a per-token region, 0.1% of ENDs
+      dropped
+4     compute/communication overlap (Section 4.3): 256 x 8,       2^25
+      flat compute and comm regions on disjoint warps
+5     large skewed stress trace: 2048 x 16 warps, Zipf(1.2)       2^28
+      records per warp, 1024 regions, depth <= 8, 1% malformed
+====  ==========================================================  ==========
+
+This package holds no attribution arithmetic; it is shared by the tests, the
+benchmark and the smoke check only as an input source.  Ground-truth instance
+lists (configs 1, 2 and 4) are what the generator itself emitted.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "tracegen.c")
+_LIB = os.path.join(_HERE, "libtracegen.so")
+
+RECORD_DTYPE = np.dtype([("ts", "<u8"), ("ctx_key", "<u4"), ("region_id", "<u2"),
+                         ("kind", "u1"), ("pad", "u1")])
+INSTANCE_DTYPE = np.dtype([
+    ("t_begin", "<u8"), ("t_end", "<u8"), ("ctx_key", "<u4"), ("parent", "<u4"),
+    ("level", "<u4"), ("region_id", "<u2"), ("end_region_id", "<u2"),
+])
+assert RECORD_DTYPE.itemsize == 16 and INSTANCE_DTYPE.itemsize == 32
+
+DEFAULTS = {1: (8, 4, 2048), 2: (256, 8, 8192), 3: (256, 16, 16384),
+            4: (256, 8, 16384), 5: (2048, 16, 1 << 28)}
+SEEDS = {1: 0, 2: 1, 3: 2, 4: 3, 5: 4}
+
+
+def build(force: bool = True) -> str:
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call(["gcc", "-O2", "-std=c11", "-Wall", "-fopenmp", "-shared",
+                               "-fPIC", _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        lib = ctypes.CDLL(_LIB)
+        lib.tg_size.restype = ctypes.c_int64
+        lib.tg_size.argtypes = [ctypes.c_int, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint64]
+        lib.tg_truth_size.restype = ctypes.c_int64
+        lib.tg_truth_size.argtypes = lib.tg_size.argtypes
+        lib.tg_regions.restype = ctypes.c_int
+        lib.tg_regions.argtypes = [ctypes.c_int, ctypes.c_void_p, ctypes.POINTER(ctypes.c_int)]
+        lib.tg_generate.restype = ctypes.c_int64
+        lib.tg_generate.argtypes = [ctypes.c_int, ctypes.c_uint64, ctypes.c_uint32,
+                                    ctypes.c_uint32, ctypes.c_uint64, ctypes.c_void_p,
+                                    ctypes.c_uint64, ctypes.c_void_p, ctypes.c_uint64,
+                                    ctypes.c_int]
+        _lib = lib
+    return _lib
+
+
+def _log2(v: int) -> int:
+    assert v > 0 and v & (v - 1) == 0, "warps per block must be a power of two"
+    return v.bit_length() - 1
+
+
+def generate(cfg: int, seed: int | None = None, blocks: int = 0, warps: int = 0,
+             size: int = 0, truth: bool = False, threads: int = 0, out=None) -> dict:
+    """Generate configuration `cfg` (1..5).
+
+    blocks / warps / size default to the full configuration when 0; `size`
+    is records per warp for configs 1-4 and the total record count for 5.
+    `out` may be a preallocated uint8 buffer (e.g. pinned) of at least
+    16 * N bytes.  Returns a dict with the records (uint8 [N, 16]) and the
+    attribution parameters of the shape (num_regions, num_classes,
+    region_class, group_shift, num_groups), plus `truth` for configs
+    1, 2 and 4 when asked.
+    """
+    lib = _load()
+    if seed is None:
+        seed = SEEDS[cfg]
+    b0, w0, _ = DEFAULTS[cfg]
+    B = blocks or b0
+    W = warps or w0
+    n = lib.tg_size(cfg, B, W, size)
+    if n < 0:
+        raise ValueError("bad configuration")
+    if out is None:
+        rec = np.empty((n, 16), np.uint8)
+    else:
+        rec = out.reshape(-1)[: n * 16].reshape(n, 16)
+    tn = lib.tg_truth_size(cfg, B, W, size) if truth else 0
+    tr = np.empty(tn, INSTANCE_DTYPE) if tn > 0 else None
+    got = lib.tg_generate(cfg, seed, B, W, size, rec.ctypes.data, n,
+                          tr.ctypes.data if tr is not None else None, tn, threads)
+    if got != n:
+        raise RuntimeError(f"tg_generate returned {got}, expected {n}")
+    cls = np.zeros(65536, np.uint8)
+    k = ctypes.c_int(0)
+    R = lib.tg_regions(cfg, cls.ctypes.data, ctypes.byref(k))
+    out_d = dict(records=rec, num_regions=R, num_classes=k.value,
+                 region_class=cls[:R].copy(), group_shift=_log2(W), num_groups=B,
+                 cfg=cfg, seed=seed, blocks=B, warps=W)
+    if tr is not None:
+        out_d["truth"] = tr
+    return out_d
+
+
+def as_records(rec_u8: np.ndarray) -> np.ndarray:
+    """View uint8 [N,16] records as the structured record dtype."""
+    return rec_u8.reshape(-1).view(RECORD_DTYPE)
+
+
+def make_records(rows) -> np.ndarray:
+    """Build uint8 [N,16] records from (ts, ctx, region, kind) tuples."""
+    a = np.zeros(len(rows), RECORD_DTYPE)
+    for i, (ts, ctx, region, kind) in enumerate(rows):
+        a[i] = (ts, ctx, region, kind, 0)
+    return a.view(np.uint8).reshape(len(rows), 16)
