@@ -1,0 +1,213 @@
+/*
+ * argus_attr.h -- region attribution over begin/end marker traces on one
+ * MI355X (gfx950) GPU.  C ABI, version 1, little-endian.
+ *
+ * What the library computes (the paper's Section 3.2: code regions are
+ * delimited by begin(id)/end(id) transitions; temporal traces recover
+ * region-labelled intervals; each warp keeps a nested region-context stack
+ * and the innermost active region owns the work.  Section 3.3: the duration
+ * signal is read from a reference region trace.  Section 3.5: observed fields
+ * and explicit attribution ambiguity.  Section 4.3: compute/communication
+ * overlap.):
+ *
+ *   1. Validate each record: kind must be BEGIN (1) or END (2) (else
+ *      "bad kind"), then region_id must be < num_regions (else "bad region").
+ *      Invalid records take no further part.
+ *   2. Order the valid records by (ctx_key, ts, input index).
+ *   3. Per execution context, replay a nested stack: a BEGIN opens an
+ *      instance (numbered by its position in that order, level = stack
+ *      depth, parent = the instance on top of the stack); an END closes the
+ *      instance on top of the stack whatever its region (MATCHED when the
+ *      regions agree, MISMATCHED otherwise); an END on an empty stack is an
+ *      orphan; instances still open when the context ends are UNCLOSED.
+ *   4. Exclusive duration of a closed instance = its inclusive duration
+ *      (t_end - t_begin) minus the inclusive durations of its closed direct
+ *      children.  Unclosed instances have exclusive duration 0.
+ *   5. Per region, over MATCHED instances: count, sums, min/max of inclusive
+ *      and exclusive duration, and 65-bin log2 histograms (bin = bit width of
+ *      the duration: 0 for 0, floor(log2 d) + 1 otherwise); plus ambiguity
+ *      counts: unclosed, orphan END, mismatched (by begin and by end region)
+ *      and self-nested (matched instance whose parent has the same region).
+ *   6. If num_classes > 0: per group (ctx_key >> group_shift, groups below
+ *      num_groups), over MATCHED instances whose region has a class below
+ *      num_classes, with half-open intervals [t_begin, t_end):
+ *      U[A][B] = time during which some class-A and some class-B instance
+ *      are active; Q[A][B] = sum over pairs of distinct instances (one of
+ *      class A, one of class B; unordered pairs for A == B) of their
+ *      intersection length.  The global matrices are sums over groups.
+ *
+ * All results are exact integers; sums wrap modulo 2^64.
+ */
+#ifndef ARGUS_ATTR_H
+#define ARGUS_ATTR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ARGUS_ATTR_ABI_VERSION 1u
+
+/* ---------------------------------------------------------------- records */
+enum { ARGUS_KIND_BEGIN = 1, ARGUS_KIND_END = 2 };
+
+/* One marker record, 16 bytes, 16-byte aligned in device memory.  `pad` is
+ * ignored. */
+typedef struct argus_record {
+  uint64_t ts;        /* timestamp in cycles of the context's clock */
+  uint32_t ctx_key;   /* execution context (e.g. block * warps + warp) */
+  uint16_t region_id; /* stable region id, < num_regions */
+  uint8_t kind;       /* ARGUS_KIND_BEGIN or ARGUS_KIND_END */
+  uint8_t pad;
+} argus_record;
+
+/* One region instance, 32 bytes.  Instances are numbered by the position of
+ * their BEGIN in (ctx_key, ts, input index) order. */
+typedef struct argus_instance {
+  uint64_t t_begin;
+  uint64_t t_end;         /* UINT64_MAX if UNCLOSED */
+  uint32_t ctx_key;
+  uint32_t parent;        /* instance index of the parent, ARGUS_NO_PARENT */
+  uint32_t level;         /* stack depth at the BEGIN; 0 = top level */
+  uint16_t region_id;     /* region of the BEGIN */
+  uint16_t end_region_id; /* region of the closing END; ARGUS_UNCLOSED if none.
+                             MISMATCHED iff != region_id (and not UNCLOSED) */
+} argus_instance;
+
+#define ARGUS_NO_PARENT 0xFFFFFFFFu
+#define ARGUS_UNCLOSED 0xFFFFu
+
+/* ------------------------------------------------------ counters (u64 each) */
+enum {
+  ARGUS_C_N_RECORDS = 0,
+  ARGUS_C_N_VALID = 1,
+  ARGUS_C_N_BAD_KIND = 2,
+  ARGUS_C_N_BAD_REGION = 3,
+  ARGUS_C_N_BEGIN = 4,
+  ARGUS_C_N_END = 5,
+  ARGUS_C_TS_MIN = 6,          /* over valid records; UINT64_MAX if none */
+  ARGUS_C_TS_MAX = 7,          /* 0 if none */
+  ARGUS_C_N_CTX = 8,           /* distinct ctx_key among valid records */
+  ARGUS_C_N_MATCHED = 9,
+  ARGUS_C_N_MISMATCHED = 10,
+  ARGUS_C_N_UNCLOSED = 11,
+  ARGUS_C_N_ORPHAN_END = 12,
+  ARGUS_C_N_SELF_NESTED = 13,
+  ARGUS_C_MAX_LEVEL = 14,      /* max level over BEGINs; 0 if none */
+  ARGUS_C_N_OVERLAP_SKIPPED = 15, /* matched classified, group >= num_groups */
+  ARGUS_C_CTX_MIN = 16,        /* UINT64_MAX if none */
+  ARGUS_C_CTX_MAX = 17,
+  ARGUS_C_INTERNAL_ERROR = 31, /* 0; nonzero only if the library detected an
+                                  internal inconsistency (a bug) */
+  ARGUS_NUM_COUNTERS = 32      /* 18..30 are zero */
+};
+
+/* ------------------------------------- per-region statistics, u64 [R][142] */
+enum {
+  ARGUS_RS_COUNT = 0,      /* matched instances */
+  ARGUS_RS_INCL_SUM = 1,
+  ARGUS_RS_EXCL_SUM = 2,
+  ARGUS_RS_INCL_MIN = 3,   /* UINT64_MAX when count == 0 */
+  ARGUS_RS_INCL_MAX = 4,
+  ARGUS_RS_EXCL_MIN = 5,   /* UINT64_MAX when count == 0 */
+  ARGUS_RS_EXCL_MAX = 6,
+  ARGUS_RS_UNCLOSED = 7,
+  ARGUS_RS_ORPHAN_END = 8,
+  ARGUS_RS_MISM_AS_BEGIN = 9,
+  ARGUS_RS_MISM_AS_END = 10,
+  ARGUS_RS_SELF_NESTED = 11,
+  ARGUS_RS_HIST_INCL = 12, /* 65 bins */
+  ARGUS_RS_HIST_EXCL = 77, /* 65 bins */
+  ARGUS_RS_WIDTH = 142
+};
+
+/* ------------------------------------------------------------------ config */
+enum {
+  ARGUS_OUT_INSTANCES = 1u,     /* write out->d_instances */
+  ARGUS_OUT_INSTANCE_EXCL = 2u, /* write out->d_instance_excl */
+  ARGUS_FORCE_FULL_SORT = 4u    /* always sort on every timestamp digit, even
+                                   when each context is already in time order
+                                   in the input (results are identical; for
+                                   measurement and testing) */
+};
+
+typedef struct argus_attr_config {
+  uint32_t abi_version;   /* must equal ARGUS_ATTR_ABI_VERSION */
+  uint32_t num_regions;   /* R: 1..65535 */
+  uint32_t num_classes;   /* K: 0..8; 0 disables the overlap step */
+  uint32_t group_shift;   /* group = ctx_key >> group_shift; 0..32 (32: one group) */
+  uint32_t num_groups;    /* G: rows of the per-group overlap output; 1..2^20 if K > 0 */
+  uint32_t flags;         /* ARGUS_OUT_* / ARGUS_FORCE_FULL_SORT */
+  uint64_t max_records;   /* capacity this handle is planned for, < 2^31 */
+  const uint8_t* d_region_class; /* device [R]; class of each region, >= K means
+                                    unclassified; caller-owned; may be NULL iff K == 0 */
+} argus_attr_config;
+
+/* Output buffers, all device memory, all caller-owned.  `run` initialises
+ * every one of them. */
+typedef struct argus_attr_outputs {
+  uint64_t* d_counters;        /* [ARGUS_NUM_COUNTERS] */
+  uint64_t* d_region_stats;    /* [R][ARGUS_RS_WIDTH] */
+  uint64_t* d_overlap_group;   /* [G][2][K][K]: U then Q; required iff K > 0 */
+  uint64_t* d_overlap_global;  /* [2][K][K]; required iff K > 0 */
+  argus_instance* d_instances; /* [n_begin <= n_records]; required iff flag 1 */
+  uint64_t* d_instance_excl;   /* [n_begin]; required iff flag 2 */
+} argus_attr_outputs;
+
+/* ------------------------------------------------------------ error codes */
+enum {
+  ARGUS_OK = 0,
+  ARGUS_E_INVAL = -1,    /* NULL pointer, bad R/K/G/shift, missing buffer */
+  ARGUS_E_ABI = -2,      /* abi_version mismatch */
+  ARGUS_E_ALIGN = -3,    /* records not 16-B aligned or workspace not 256-B aligned */
+  ARGUS_E_CAPACITY = -4, /* n_records > max_records, or workspace too small */
+  ARGUS_E_DEVICE = -5,   /* current device is not gfx950 */
+  ARGUS_E_HIP = -6       /* a HIP call failed; see argus_attr_last_error */
+};
+
+typedef struct argus_attr argus_attr; /* opaque host-side handle */
+
+/* Create a handle from a copy of *cfg.  Checks the configuration only (no
+ * GPU call).  On success writes *out and returns ARGUS_OK; on failure *out
+ * is set to NULL and a negative code is returned. */
+int argus_attr_create(const argus_attr_config* cfg, argus_attr** out);
+
+/* Device workspace `run` needs for n_records records (bytes; callers pass a
+ * buffer at least this large, 256-byte aligned).  0 if h is NULL or
+ * n_records exceeds the handle's capacity. */
+size_t argus_attr_workspace_bytes(const argus_attr* h, uint64_t n_records);
+
+/* Enqueue the whole computation on `stream` (a hipStream_t; NULL = the
+ * default stream) and return without synchronising.  `d_records` points to
+ * n_records device records (16-byte aligned, caller-owned, not modified).
+ * The library allocates no memory and makes no host<->device copies; every
+ * output is initialised on the stream.  Results are valid once the stream
+ * has completed.  Argument errors are reported before any GPU call.  Data
+ * anomalies never fail the call: they are counted.  A handle must not run
+ * on two streams at once; distinct handles are independent. */
+int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n_records,
+                   void* d_workspace, size_t workspace_bytes,
+                   const argus_attr_outputs* out, void* stream);
+
+/* Destroy a handle; NULL is a no-op. */
+void argus_attr_destroy(argus_attr* h);
+
+/* Message for the last non-zero return on this handle ("" if none). */
+const char* argus_attr_last_error(const argus_attr* h);
+
+/* ---------------------------------------------------------------- timing */
+/* Per-kernel timing for measurement.  When enabled, `run` records a HIP
+ * event after each kernel launch on its stream.  argus_attr_kernel_times
+ * then fills up to `cap` entries of names[] (static strings) and ms[] with
+ * the elapsed time of each launch of the last run (it synchronises on the
+ * last event); returns the number of launches, or a negative code. */
+int argus_attr_set_timing(argus_attr* h, int enable);
+int argus_attr_kernel_times(argus_attr* h, const char** names, float* ms, int cap);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ARGUS_ATTR_H */

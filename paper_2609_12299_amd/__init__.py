@@ -1,0 +1,22 @@
+"""MI355X-native region attribution over begin/end marker traces.
+
+The data-parallel core of the evidence join of "Argus: Orchestrating
+Cross-Layer GPU Performance Measurements around Semantic Regions"
+(arxiv 2609.12299): marker records become region instances with nesting,
+per-region duration statistics, class overlap and ambiguity counts, computed
+by hand-written HIP kernels for gfx950 behind a C ABI (include/argus_attr.h).
+"""
+from .attr import (ABI_VERSION, COUNTER_NAMES, FORCE_FULL_SORT, INSTANCE_DTYPE, NUM_COUNTERS,
+                   OUT_INSTANCE_EXCL, OUT_INSTANCES, RS_WIDTH, ArgusError, RegionAttribution,
+                   argus_attr_config, argus_attr_create, argus_attr_destroy,
+                   argus_attr_kernel_times, argus_attr_last_error, argus_attr_outputs,
+                   argus_attr_run, argus_attr_set_timing, argus_attr_workspace_bytes,
+                   load_library, to_host)
+
+__all__ = [
+    "ABI_VERSION", "COUNTER_NAMES", "FORCE_FULL_SORT", "INSTANCE_DTYPE", "NUM_COUNTERS",
+    "OUT_INSTANCE_EXCL", "OUT_INSTANCES", "RS_WIDTH", "ArgusError", "RegionAttribution",
+    "argus_attr_config", "argus_attr_create", "argus_attr_destroy", "argus_attr_kernel_times",
+    "argus_attr_last_error", "argus_attr_outputs", "argus_attr_run", "argus_attr_set_timing",
+    "argus_attr_workspace_bytes", "load_library", "to_host",
+]

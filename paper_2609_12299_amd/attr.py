@@ -1,0 +1,251 @@
+"""Python binding of the region-attribution C ABI (include/argus_attr.h).
+
+The functions named ``argus_attr_*`` are one-to-one wrappers (argument
+marshalling only).  :class:`RegionAttribution` adds what a PyTorch caller
+needs: it allocates outputs and the workspace as torch tensors on the current
+device and runs on the current torch stream.  Every step of the computation
+runs in the HIP kernels of libargus_attr.so; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libargus_attr.so")
+
+ABI_VERSION = 1
+KIND_BEGIN, KIND_END = 1, 2
+OUT_INSTANCES, OUT_INSTANCE_EXCL, FORCE_FULL_SORT = 1, 2, 4
+NUM_COUNTERS = 32
+RS_WIDTH = 142
+NO_PARENT = 0xFFFFFFFF
+UNCLOSED = 0xFFFF
+ERRORS = {0: "OK", -1: "ARGUS_E_INVAL", -2: "ARGUS_E_ABI", -3: "ARGUS_E_ALIGN",
+          -4: "ARGUS_E_CAPACITY", -5: "ARGUS_E_DEVICE", -6: "ARGUS_E_HIP"}
+COUNTER_NAMES = [
+    "n_records", "n_valid", "n_bad_kind", "n_bad_region", "n_begin", "n_end",
+    "ts_min", "ts_max", "n_ctx", "n_matched", "n_mismatched", "n_unclosed",
+    "n_orphan_end", "n_self_nested", "max_level", "n_overlap_skipped",
+    "ctx_min", "ctx_max",
+]
+INSTANCE_DTYPE = np.dtype([
+    ("t_begin", "<u8"), ("t_end", "<u8"), ("ctx_key", "<u4"), ("parent", "<u4"),
+    ("level", "<u4"), ("region_id", "<u2"), ("end_region_id", "<u2"),
+])
+
+
+class argus_attr_config(ctypes.Structure):
+    _fields_ = [("abi_version", ctypes.c_uint32), ("num_regions", ctypes.c_uint32),
+                ("num_classes", ctypes.c_uint32), ("group_shift", ctypes.c_uint32),
+                ("num_groups", ctypes.c_uint32), ("flags", ctypes.c_uint32),
+                ("max_records", ctypes.c_uint64), ("d_region_class", ctypes.c_void_p)]
+
+
+class argus_attr_outputs(ctypes.Structure):
+    _fields_ = [("d_counters", ctypes.c_void_p), ("d_region_stats", ctypes.c_void_p),
+                ("d_overlap_group", ctypes.c_void_p), ("d_overlap_global", ctypes.c_void_p),
+                ("d_instances", ctypes.c_void_p), ("d_instance_excl", ctypes.c_void_p)]
+
+
+assert ctypes.sizeof(argus_attr_config) == 40
+assert ctypes.sizeof(argus_attr_outputs) == 48
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libargus_attr.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2609_12299_amd.build`"
+                           " (the HIP library is required; there is no CPU fallback)")
+    lib = ctypes.CDLL(path)
+    vp, u64, i32 = ctypes.c_void_p, ctypes.c_uint64, ctypes.c_int
+    lib.argus_attr_create.argtypes = [ctypes.POINTER(argus_attr_config), ctypes.POINTER(vp)]
+    lib.argus_attr_create.restype = i32
+    lib.argus_attr_workspace_bytes.argtypes = [vp, u64]
+    lib.argus_attr_workspace_bytes.restype = ctypes.c_size_t
+    lib.argus_attr_run.argtypes = [vp, vp, u64, vp, ctypes.c_size_t,
+                                   ctypes.POINTER(argus_attr_outputs), vp]
+    lib.argus_attr_run.restype = i32
+    lib.argus_attr_destroy.argtypes = [vp]
+    lib.argus_attr_destroy.restype = None
+    lib.argus_attr_last_error.argtypes = [vp]
+    lib.argus_attr_last_error.restype = ctypes.c_char_p
+    lib.argus_attr_set_timing.argtypes = [vp, i32]
+    lib.argus_attr_set_timing.restype = i32
+    lib.argus_attr_kernel_times.argtypes = [vp, ctypes.POINTER(ctypes.c_char_p),
+                                            ctypes.POINTER(ctypes.c_float), i32]
+    lib.argus_attr_kernel_times.restype = i32
+    _lib = lib
+    return lib
+
+
+# ------------------------------------------------------------ C ABI, 1:1
+
+def argus_attr_create(cfg: argus_attr_config):
+    """Returns (code, handle)."""
+    h = ctypes.c_void_p()
+    rc = load_library().argus_attr_create(ctypes.byref(cfg), ctypes.byref(h))
+    return rc, h
+
+
+def argus_attr_workspace_bytes(h, n_records: int) -> int:
+    return load_library().argus_attr_workspace_bytes(h, n_records)
+
+
+def argus_attr_run(h, d_records: int, n_records: int, d_workspace: int, workspace_bytes: int,
+                   out: argus_attr_outputs, stream: int) -> int:
+    return load_library().argus_attr_run(h, d_records, n_records, d_workspace, workspace_bytes,
+                                         ctypes.byref(out), stream)
+
+
+def argus_attr_destroy(h) -> None:
+    load_library().argus_attr_destroy(h)
+
+
+def argus_attr_last_error(h) -> str:
+    s = load_library().argus_attr_last_error(h)
+    return s.decode() if s else ""
+
+
+def argus_attr_set_timing(h, enable: bool) -> int:
+    return load_library().argus_attr_set_timing(h, 1 if enable else 0)
+
+
+def argus_attr_kernel_times(h, cap: int = 128):
+    """[(name, ms)] for every launch of the last timed run."""
+    names = (ctypes.c_char_p * cap)()
+    ms = (ctypes.c_float * cap)()
+    n = load_library().argus_attr_kernel_times(h, names, ms, cap)
+    if n < 0:
+        raise RuntimeError(f"argus_attr_kernel_times failed: {ERRORS.get(n, n)}")
+    return [(names[i].decode(), float(ms[i])) for i in range(min(n, cap))]
+
+
+class ArgusError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{ERRORS.get(code, code)}: {msg}")
+        self.code = code
+
+
+# ------------------------------------------------------------ torch wrapper
+
+class RegionAttribution:
+    """Region attribution on one GPU.
+
+    records: a CUDA tensor of uint8 [N, 16] (or any dtype whose bytes are the
+    16-byte records), 16-byte aligned.  region_class: sequence or tensor of R
+    class ids (>= num_classes: unclassified).
+    """
+
+    def __init__(self, num_regions: int, num_classes: int = 0, region_class=None,
+                 group_shift: int = 0, num_groups: int = 0, max_records: int = 1 << 20,
+                 instances: bool = True, instance_excl: bool = True,
+                 force_full_sort: bool = False, device=None):
+        import torch
+        self.torch = torch
+        self.device = torch.device(device if device is not None else "cuda")
+        self.R, self.K, self.G = int(num_regions), int(num_classes), int(num_groups)
+        if self.K > 0:
+            rc = torch.as_tensor(np.asarray(region_class, dtype=np.uint8), device=self.device)
+            self.region_class = rc.contiguous()
+            rc_ptr = self.region_class.data_ptr()
+        else:
+            self.region_class, rc_ptr = None, None
+        flags = (OUT_INSTANCES if instances else 0) | (OUT_INSTANCE_EXCL if instance_excl else 0)
+        flags |= FORCE_FULL_SORT if force_full_sort else 0
+        self.flags = flags
+        self.cfg = argus_attr_config(ABI_VERSION, self.R, self.K, int(group_shift),
+                                     self.G if self.K else 0, flags, int(max_records), rc_ptr)
+        rc, self.h = argus_attr_create(self.cfg)
+        if rc != 0:
+            raise ArgusError(rc, "argus_attr_create rejected the configuration")
+        self._ws = None
+
+    def close(self):
+        if getattr(self, "h", None):
+            argus_attr_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:  # noqa: BLE001 - interpreter shutdown
+            pass
+
+    def alloc(self, n: int) -> dict:
+        """Output tensors for up to n records."""
+        t = self.torch
+        d = self.device
+        out = dict(
+            counters=t.zeros(NUM_COUNTERS, dtype=t.uint64, device=d),
+            region_stats=t.zeros((self.R, RS_WIDTH), dtype=t.uint64, device=d),
+        )
+        if self.K:
+            out["overlap_group"] = t.zeros((self.G, 2, self.K, self.K), dtype=t.uint64, device=d)
+            out["overlap_global"] = t.zeros((2, self.K, self.K), dtype=t.uint64, device=d)
+        if self.flags & OUT_INSTANCES:
+            out["instances"] = t.zeros((max(n, 1), 32), dtype=t.uint8, device=d)
+        if self.flags & OUT_INSTANCE_EXCL:
+            out["instance_excl"] = t.zeros(max(n, 1), dtype=t.uint64, device=d)
+        return out
+
+    def workspace(self, n: int):
+        need = argus_attr_workspace_bytes(self.h, n)
+        if need == 0:
+            raise ArgusError(-4, "n exceeds max_records")
+        if self._ws is None or self._ws.numel() < need + 256:
+            self._ws = None
+            self._ws = self.torch.empty(need + 256, dtype=self.torch.uint8, device=self.device)
+        base = self._ws.data_ptr()
+        aligned = (base + 255) & ~255
+        return aligned, need
+
+    def run(self, records, out: dict | None = None, stream=None) -> dict:
+        """Enqueue on `stream` (default: the current torch stream); returns the
+        output tensors (valid once the stream has completed)."""
+        t = self.torch
+        n = records.numel() * records.element_size() // 16
+        if out is None:
+            out = self.alloc(n)
+        ws, ws_bytes = self.workspace(n)
+        o = argus_attr_outputs(
+            out["counters"].data_ptr(), out["region_stats"].data_ptr(),
+            out["overlap_group"].data_ptr() if self.K else None,
+            out["overlap_global"].data_ptr() if self.K else None,
+            out["instances"].data_ptr() if "instances" in out else None,
+            out["instance_excl"].data_ptr() if "instance_excl" in out else None)
+        s = stream if stream is not None else t.cuda.current_stream(self.device)
+        rc = argus_attr_run(self.h, records.data_ptr() if n else None, n, ws, ws_bytes, o,
+                            s.cuda_stream)
+        if rc != 0:
+            raise ArgusError(rc, argus_attr_last_error(self.h))
+        return out
+
+    def set_timing(self, on: bool):
+        rc = argus_attr_set_timing(self.h, on)
+        if rc != 0:
+            raise ArgusError(rc, argus_attr_last_error(self.h))
+
+    def kernel_times(self):
+        return argus_attr_kernel_times(self.h)
+
+
+def to_host(out: dict) -> dict:
+    """Copy results to numpy; instances become structured arrays trimmed to n_begin."""
+    res = {}
+    for k, v in out.items():
+        a = v.cpu().numpy()
+        res[k] = a
+    nb = int(res["counters"][4])
+    if "instances" in res:
+        res["instances"] = res["instances"].reshape(-1).view(INSTANCE_DTYPE)[:nb]
+    if "instance_excl" in res:
+        res["instance_excl"] = res["instance_excl"][:nb]
+    return res

@@ -1,0 +1,307 @@
+// attr_host.hip -- the C ABI: handle, argument checks, workspace layout and
+// the launch sequence of one run.  Every argument check happens before the
+// first HIP call, so error paths can be exercised without a GPU.
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+using namespace argus;
+
+struct argus_attr {
+  argus_attr_config cfg;
+  std::string err;
+  int device_checked = -1;  // device ordinal verified to be gfx950
+  bool timing = false;
+  std::vector<hipEvent_t> events;
+  std::vector<const char*> names;
+  int n_launches = 0;
+};
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t v) { return (v + kAlign - 1) & ~(kAlign - 1); }
+
+// Workspace layout for n records.  Offsets only; the base is added in run.
+struct Layout {
+  size_t plan, rec_hist, rec_off, ev_hist, ev_off, tile_ctr;
+  size_t key[2], pay[2], ctxw[2], lb[2], mlb, slb, tiles, tree;
+  size_t pop_ts, pop_reg, pushes, op_parent, op_sum;
+  size_t inst, child_sum, hist_key, ov_mask, ov_q;
+  size_t total;
+  uint64_t lb_words, tree_leaves, match_tiles, pool_cap;
+};
+
+Layout make_layout(const argus_attr_config& c, uint64_t n, bool own_instances) {
+  Layout L{};
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o = align_up(o + (bytes ? bytes : 1));
+    return at;
+  };
+  const uint64_t nn = n ? n : 1;
+  L.plan = take(sizeof(DevPlan));
+  L.rec_hist = take(sizeof(uint32_t) * kDigitPositions * kRadixBins);
+  L.rec_off = take(sizeof(uint32_t) * kDigitPositions * kRadixBins);
+  L.ev_hist = take(sizeof(uint32_t) * kDigitPositions * kRadixBins);
+  L.ev_off = take(sizeof(uint32_t) * kDigitPositions * kRadixBins);
+  L.tile_ctr = take(sizeof(uint32_t) * kCtrCount);
+  for (int b = 0; b < 2; ++b) {
+    L.key[b] = take(sizeof(uint64_t) * nn);
+    L.pay[b] = take(sizeof(uint32_t) * nn);
+    L.ctxw[b] = take(sizeof(uint32_t) * nn);
+  }
+  // The first event pass reads 2 * n_begin <= 2 * n slots.
+  L.lb_words = ceil_div(2 * nn, kSortTile) * kRadixBins;
+  for (int b = 0; b < 2; ++b) L.lb[b] = take(sizeof(uint64_t) * L.lb_words);
+  L.match_tiles = ceil_div(nn, kMatchTile);
+  L.mlb = take(sizeof(uint64_t) * 4 * L.match_tiles);
+  L.slb = take(sizeof(uint64_t) * 8 * ceil_div(nn, kSweepTile));
+  L.tiles = take(sizeof(TileDesc) * L.match_tiles);
+  uint64_t leaves = 1;
+  while (leaves < L.match_tiles) leaves <<= 1;
+  L.tree_leaves = leaves;
+  L.tree = take(sizeof(int64_t) * 2 * leaves);
+  L.pool_cap = L.match_tiles * (uint64_t)kMatchTile;
+  L.pop_ts = take(sizeof(uint64_t) * L.pool_cap);
+  L.pop_reg = take(sizeof(uint32_t) * L.pool_cap);
+  L.pushes = take(sizeof(uint32_t) * L.pool_cap);
+  L.op_parent = take(sizeof(uint32_t) * L.pool_cap);
+  L.op_sum = take(sizeof(uint64_t) * L.pool_cap);
+  L.inst = own_instances ? take(sizeof(argus_instance) * nn) : 0;
+  L.child_sum = take(sizeof(uint64_t) * nn);
+  L.hist_key = take(sizeof(uint32_t) * nn);
+  const uint64_t G = c.num_classes ? c.num_groups : 0;
+  L.ov_mask = take(sizeof(uint64_t) * kMasks * (G ? G : 1));
+  L.ov_q = take(sizeof(uint64_t) * kQPairs * (G ? G : 1));
+  L.total = o;
+  return L;
+}
+
+int fail(argus_attr* h, int code, const char* fmt, const char* detail = "") {
+  if (h) {
+    char buf[512];
+    snprintf(buf, sizeof buf, fmt, detail);
+    h->err = buf;
+  }
+  return code;
+}
+
+int check_config(const argus_attr_config* c, std::string* why) {
+  if (!c) { *why = "config is NULL"; return ARGUS_E_INVAL; }
+  if (c->abi_version != ARGUS_ATTR_ABI_VERSION) { *why = "abi_version mismatch"; return ARGUS_E_ABI; }
+  if (c->num_regions < 1 || c->num_regions > 65535) { *why = "num_regions must be 1..65535"; return ARGUS_E_INVAL; }
+  if (c->num_classes > 8) { *why = "num_classes must be 0..8"; return ARGUS_E_INVAL; }
+  if (c->group_shift > 32) { *why = "group_shift must be 0..32"; return ARGUS_E_INVAL; }
+  if (c->num_classes > 0) {
+    if (c->num_groups < 1 || c->num_groups > (1u << 20)) { *why = "num_groups must be 1..2^20 when num_classes > 0"; return ARGUS_E_INVAL; }
+    if (!c->d_region_class) { *why = "d_region_class is NULL while num_classes > 0"; return ARGUS_E_INVAL; }
+  }
+  if (c->flags & ~7u) { *why = "unknown flag bits"; return ARGUS_E_INVAL; }
+  if (c->max_records >= (1ull << 31)) { *why = "max_records must be < 2^31"; return ARGUS_E_CAPACITY; }
+  return ARGUS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int argus_attr_create(const argus_attr_config* cfg, argus_attr** out) {
+  if (!out) return ARGUS_E_INVAL;
+  *out = nullptr;
+  std::string why;
+  int rc = check_config(cfg, &why);
+  if (rc != ARGUS_OK) return rc;
+  argus_attr* h = new (std::nothrow) argus_attr();
+  if (!h) return ARGUS_E_INVAL;
+  h->cfg = *cfg;
+  *out = h;
+  return ARGUS_OK;
+}
+
+size_t argus_attr_workspace_bytes(const argus_attr* h, uint64_t n_records) {
+  if (!h || n_records > h->cfg.max_records) return 0;
+  return make_layout(h->cfg, n_records, true).total;
+}
+
+void argus_attr_destroy(argus_attr* h) {
+  if (!h) return;
+  for (hipEvent_t e : h->events) (void)hipEventDestroy(e);
+  delete h;
+}
+
+const char* argus_attr_last_error(const argus_attr* h) { return h ? h->err.c_str() : "handle is NULL"; }
+
+int argus_attr_set_timing(argus_attr* h, int enable) {
+  if (!h) return ARGUS_E_INVAL;
+  h->timing = enable != 0;
+  return ARGUS_OK;
+}
+
+int argus_attr_kernel_times(argus_attr* h, const char** names, float* ms, int cap) {
+  if (!h) return ARGUS_E_INVAL;
+  if (!h->timing || h->n_launches == 0) return 0;
+  if (hipEventSynchronize(h->events[h->n_launches]) != hipSuccess)
+    return fail(h, ARGUS_E_HIP, "%s", "hipEventSynchronize failed");
+  int k = 0;
+  for (; k < h->n_launches && k < cap; ++k) {
+    float t = 0;
+    if (hipEventElapsedTime(&t, h->events[k], h->events[k + 1]) != hipSuccess)
+      return fail(h, ARGUS_E_HIP, "%s", "hipEventElapsedTime failed");
+    if (names) names[k] = h->names[k];
+    if (ms) ms[k] = t;
+  }
+  return h->n_launches;
+}
+
+int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
+                   void* d_workspace, size_t workspace_bytes,
+                   const argus_attr_outputs* out, void* stream_v) {
+  if (!h) return ARGUS_E_INVAL;
+  h->err.clear();
+  const argus_attr_config& c = h->cfg;
+  if (!out) return fail(h, ARGUS_E_INVAL, "%s", "outputs is NULL");
+  if (n > c.max_records) return fail(h, ARGUS_E_CAPACITY, "%s", "n_records exceeds max_records");
+  if (n > 0 && !d_records) return fail(h, ARGUS_E_INVAL, "%s", "d_records is NULL");
+  if (!out->d_counters || !out->d_region_stats)
+    return fail(h, ARGUS_E_INVAL, "%s", "d_counters and d_region_stats are required");
+  if (c.num_classes > 0 && (!out->d_overlap_group || !out->d_overlap_global))
+    return fail(h, ARGUS_E_INVAL, "%s", "overlap outputs are required when num_classes > 0");
+  if ((c.flags & ARGUS_OUT_INSTANCES) && !out->d_instances)
+    return fail(h, ARGUS_E_INVAL, "%s", "ARGUS_OUT_INSTANCES set but d_instances is NULL");
+  if ((c.flags & ARGUS_OUT_INSTANCE_EXCL) && !out->d_instance_excl)
+    return fail(h, ARGUS_E_INVAL, "%s", "ARGUS_OUT_INSTANCE_EXCL set but d_instance_excl is NULL");
+  if (((uintptr_t)d_records & 15) != 0) return fail(h, ARGUS_E_ALIGN, "%s", "records must be 16-byte aligned");
+  if (!d_workspace) return fail(h, ARGUS_E_INVAL, "%s", "d_workspace is NULL");
+  if (((uintptr_t)d_workspace & (kAlign - 1)) != 0)
+    return fail(h, ARGUS_E_ALIGN, "%s", "workspace must be 256-byte aligned");
+  const bool own_inst = !(c.flags & ARGUS_OUT_INSTANCES);
+  const Layout L = make_layout(c, n, own_inst);
+  if (workspace_bytes < L.total) return fail(h, ARGUS_E_CAPACITY, "%s", "workspace too small");
+
+  // Device check (lazily, once per device).
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(h, ARGUS_E_HIP, "%s", "hipGetDevice failed");
+  if (h->device_checked != dev) {
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess)
+      return fail(h, ARGUS_E_HIP, "%s", "hipGetDeviceProperties failed");
+    if (strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+      return fail(h, ARGUS_E_DEVICE, "device is %s, this library is built for gfx950", prop.gcnArchName);
+    h->device_checked = dev;
+  }
+
+  hipStream_t s = (hipStream_t)stream_v;
+  char* base = (char*)d_workspace;
+  RunArgs a{};
+  a.rec = d_records;
+  a.n = n;
+  a.R = c.num_regions;
+  a.K = c.num_classes;
+  a.G = c.num_classes ? c.num_groups : 0;
+  a.shift = c.group_shift;
+  a.flags = c.flags;
+  a.region_class = c.d_region_class;
+  a.out = *out;
+  Work& w = a.w;
+  w.plan = (DevPlan*)(base + L.plan);
+  w.rec_hist = (uint32_t*)(base + L.rec_hist);
+  w.rec_off = (uint32_t*)(base + L.rec_off);
+  w.ev_hist = (uint32_t*)(base + L.ev_hist);
+  w.ev_off = (uint32_t*)(base + L.ev_off);
+  w.tile_ctr = (uint32_t*)(base + L.tile_ctr);
+  for (int b = 0; b < 2; ++b) {
+    w.key[b] = (uint64_t*)(base + L.key[b]);
+    w.pay[b] = (uint32_t*)(base + L.pay[b]);
+    w.ctxw[b] = (uint32_t*)(base + L.ctxw[b]);
+    w.lb[b] = (uint64_t*)(base + L.lb[b]);
+  }
+  w.mlb = (uint64_t*)(base + L.mlb);
+  w.slb = (uint64_t*)(base + L.slb);
+  w.tiles = (TileDesc*)(base + L.tiles);
+  w.tree = (int64_t*)(base + L.tree);
+  w.pop_ts = (uint64_t*)(base + L.pop_ts);
+  w.pop_reg = (uint32_t*)(base + L.pop_reg);
+  w.pushes = (uint32_t*)(base + L.pushes);
+  w.op_parent = (uint32_t*)(base + L.op_parent);
+  w.op_sum = (uint64_t*)(base + L.op_sum);
+  w.inst = own_inst ? (argus_instance*)(base + L.inst) : out->d_instances;
+  w.child_sum = (uint64_t*)(base + L.child_sum);
+  w.hist_key = (uint32_t*)(base + L.hist_key);
+  w.ov_mask = (uint64_t*)(base + L.ov_mask);
+  w.ov_q = (uint64_t*)(base + L.ov_q);
+  w.lb_words = L.lb_words;
+  w.tree_leaves = L.tree_leaves;
+  w.match_tiles = L.match_tiles;
+  w.pool_cap = L.pool_cap;
+
+  // Timing events.
+  h->n_launches = 0;
+  h->names.clear();
+  if (h->timing) {
+    while (h->events.size() < 96) {
+      hipEvent_t e;
+      if (hipEventCreate(&e) != hipSuccess) return fail(h, ARGUS_E_HIP, "%s", "hipEventCreate failed");
+      h->events.push_back(e);
+    }
+    if (hipEventRecord(h->events[0], s) != hipSuccess)
+      return fail(h, ARGUS_E_HIP, "%s", "hipEventRecord failed");
+  }
+  auto step = [&](const char* name, hipError_t e) -> bool {
+    if (e == hipSuccess) e = hipGetLastError();
+    if (e != hipSuccess) {
+      fail(h, ARGUS_E_HIP, "launch failed: %s", name);
+      h->err += std::string(" (") + hipGetErrorString(e) + ")";
+      return false;
+    }
+    if (h->timing && h->n_launches + 1 < (int)h->events.size()) {
+      h->names.push_back(name);
+      h->n_launches++;
+      if (hipEventRecord(h->events[h->n_launches], s) != hipSuccess) return false;
+    }
+    return true;
+  };
+
+  if (!step("init", launch_init(a, s))) return ARGUS_E_HIP;
+  if (n == 0) return ARGUS_OK;
+  if (!step("ingest", launch_ingest(a, s))) return ARGUS_E_HIP;
+  if (!step("plan", launch_plan(a, s))) return ARGUS_E_HIP;
+  static const char* rnames[kSlots] = {
+      "radix_ctx0", "radix_ctx1", "radix_ctx2", "radix_ctx3", "radix_ts0", "radix_ts1",
+      "radix_ts2", "radix_ts3", "radix_ts4", "radix_ts5", "radix_ts6", "radix_ts7",
+      "radix_ctx0b", "radix_ctx1b", "radix_ctx2b", "radix_ctx3b"};
+  for (int sl = 0; sl < kPhase2Slot; ++sl)
+    if (!step(rnames[sl], launch_radix_pass(a, 0, sl, n, s))) return ARGUS_E_HIP;
+  if (!step("check_sorted", launch_check_sorted(a, s))) return ARGUS_E_HIP;
+  if (!step("ts_hist", launch_ts_hist(a, s))) return ARGUS_E_HIP;
+  if (!step("plan2", launch_plan2(a, s))) return ARGUS_E_HIP;
+  for (int sl = kPhase2Slot; sl < kSlots; ++sl)
+    if (!step(rnames[sl], launch_radix_pass(a, 0, sl, n, s))) return ARGUS_E_HIP;
+  if (!step("match", launch_match(a, s))) return ARGUS_E_HIP;
+  if (!step("tree", launch_tree(a, s))) return ARGUS_E_HIP;
+  if (!step("resolve", launch_resolve(a, s))) return ARGUS_E_HIP;
+  if (!step("agg", launch_agg(a, s))) return ARGUS_E_HIP;
+  if (!step("hist", launch_hist(a, s))) return ARGUS_E_HIP;
+  if (a.K > 0) {
+    static const char* enames[kSlots] = {
+        "ev_radix_ts0", "ev_radix_ts1", "ev_radix_ts2", "ev_radix_ts3", "ev_radix_ts4",
+        "ev_radix_ts5", "ev_radix_ts6", "ev_radix_ts7", "ev_radix_g0", "ev_radix_g1",
+        "ev_radix_g2", "ev_radix_g3", "ev_unused12", "ev_unused13", "ev_unused14", "ev_unused15"};
+    if (!step("ev_hist", launch_ev_hist(a, s))) return ARGUS_E_HIP;
+    if (!step("ev_plan", launch_ev_plan(a, s))) return ARGUS_E_HIP;
+    if (!step("ev_clear", launch_ev_clear(a, s))) return ARGUS_E_HIP;
+    for (int sl = 0; sl < 12; ++sl)
+      if (!step(enames[sl], launch_radix_pass(a, 1, sl, 2 * n, s))) return ARGUS_E_HIP;
+    if (!step("sweep", launch_sweep(a, s))) return ARGUS_E_HIP;
+    if (!step("ov_final", launch_ov_final(a, s))) return ARGUS_E_HIP;
+  }
+  return ARGUS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,218 @@
+// internal.h -- shared definitions of the HIP implementation (not part of the
+// public ABI).  Every kernel of the library runs on gfx950: 64-lane
+// wavefronts, 160 KiB of LDS per CU, 8 XCDs with private L2 caches (so all
+// cross-workgroup communication inside a kernel goes through agent-scope
+// atomics).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/argus_attr.h"
+
+namespace argus {
+
+// ------------------------------------------------------------------ sizes
+constexpr int kSortThreads = 256;
+constexpr int kSortItems = 16;
+constexpr int kSortTile = kSortThreads * kSortItems;  // 4096 elements
+constexpr int kRadixBins = 256;
+constexpr int kDigitPositions = 12;  // 4 context digits, then 8 timestamp digits
+constexpr int kSlots = 16;           // sort passes planned per sort
+constexpr int kPhase2Slot = 4;       // first slot of the full-sort phase
+
+constexpr int kMatchThreads = 256;
+constexpr int kMatchItems = 8;
+constexpr int kMatchTile = kMatchThreads * kMatchItems;  // 2048 elements
+
+constexpr int kSweepThreads = 256;
+constexpr int kSweepItems = 8;
+constexpr int kSweepTile = kSweepThreads * kSweepItems;  // 2048 events
+constexpr int kSweepSlots = 8;  // groups of one tile aggregated in LDS
+
+constexpr int kMaxClasses = 8;
+constexpr int kQPairs = kMaxClasses * (kMaxClasses + 1) / 2;  // 36
+constexpr int kMasks = 1 << kMaxClasses;                      // 256
+
+constexpr uint32_t kNoParent = 0xFFFFFFFFu;
+constexpr uint32_t kParentPending = 0x80000000u;  // | tile: parent lies in an earlier tile
+constexpr uint16_t kNoEnd = 0xFFFF;
+constexpr uint64_t kU64Max = ~0ull;
+
+// Source of the elements read by a sort pass.
+enum SrcKind : uint32_t { kSrcPacked = 0, kSrcRecords = 1, kSrcInstances = 2 };
+
+// How packed sort keys are laid out.  key = (ctx_rel << ts_bits) | ts_off
+// when ctx_bits + ts_bits <= 64, else ("wide") key = ts_off and ctx_rel lives
+// in a separate 32-bit array.  ts_off = ts - ts_min, ctx_rel = ctx - ctx_min.
+struct KeySpace {
+  uint64_t ts_min;
+  uint64_t ts_mask;  // (1 << ts_bits) - 1, all ones for 64
+  uint64_t ctx_min;
+  uint32_t ts_bits;
+  uint32_t ctx_bits;
+  uint32_t wide;
+  uint32_t pad;
+};
+
+struct SlotPlan {
+  uint32_t active;
+  uint32_t pos;    // digit position: 0..3 context digit, 4..11 timestamp digit
+  uint32_t src;    // buffer index 0/1, or 2 = raw source
+  uint32_t dst;    // buffer index 0/1
+  uint32_t lb;     // look-back status array used (0/1)
+  uint32_t n_out;  // valid elements written (destination bound)
+  uint64_t n_elems;  // elements read (raw sources include the invalid ones)
+  uint64_t tiles;
+};
+
+// Written on the device by the planning kernels; read by everything else.
+struct DevPlan {
+  // ingest
+  uint64_t n_records;
+  uint64_t n_valid;
+  uint64_t n_begin;
+  KeySpace rec;   // record sort keys
+  KeySpace ev;    // overlap event keys (context = group)
+  uint32_t unsorted;     // the context-only sort left some context out of time order
+  uint32_t force_full;   // ARGUS_FORCE_FULL_SORT
+  uint32_t rec_final;    // buffer holding the sorted records
+  uint32_t ev_final;     // buffer holding the sorted events
+  uint32_t rec_active;   // active record passes so far (look-back parity)
+  uint32_t pad0;
+  uint64_t n_ev;         // valid overlap events
+  uint64_t ev_slots;     // 2 * n_begin
+  SlotPlan rs[kSlots];   // record sort
+  SlotPlan es[kSlots];   // event sort
+  // matching
+  uint64_t match_tiles;
+};
+
+// Per-tile summary written by the matching kernel, read by the resolver.
+struct TileDesc {
+  int64_t key;       // -1 if the tile holds a context start, else lowest depth seen
+  uint32_t s_in;     // depth before the tile's first element (0 if it starts a context)
+  uint32_t lo_head;  // lowest depth in the part before the first context start
+  uint32_t s_out;    // depth after the last element
+  uint32_t lo_tail;  // lowest depth in the part after the last context start
+  uint32_t op_lo;    // lowest level of an enclosing instance referenced from this tile
+  uint32_t pop_base;
+  uint32_t push_base;
+  uint32_t op_base;
+  uint32_t n_pop;    // s_in - lo_head
+  uint32_t n_push;   // s_out - lo_tail
+  uint32_t n_op;     // s_in - op_lo (if s_in > op_lo)
+  uint32_t pad;
+};
+
+// Device pointers of one run (workspace carved on the host).
+struct Work {
+  DevPlan* plan;
+  uint32_t* rec_hist;   // [12][256]
+  uint32_t* rec_off;    // [12][256]
+  uint32_t* ev_hist;    // [12][256]
+  uint32_t* ev_off;     // [12][256]
+  uint32_t* tile_ctr;   // [64] dynamic tile counters (one per launch that needs one)
+  uint64_t* key[2];
+  uint32_t* pay[2];
+  uint32_t* ctxw[2];
+  uint64_t* lb[2];      // radix look-back status, [tiles][256]
+  uint64_t* mlb;        // matching look-back status, [tiles][4]
+  uint64_t* slb;        // sweep look-back status, [tiles][8]
+  TileDesc* tiles;      // [match tiles]
+  int64_t* tree;        // [2 * tree_leaves]
+  uint64_t* pop_ts;     // per matching tile, kMatchTile entries each
+  uint32_t* pop_reg;
+  uint32_t* pushes;
+  uint32_t* op_parent;
+  uint64_t* op_sum;
+  argus_instance* inst;
+  uint64_t* child_sum;  // [n_begin]
+  uint32_t* hist_key;   // [n_begin]
+  uint64_t* ov_mask;    // [G][256]
+  uint64_t* ov_q;       // [G][36]
+  uint64_t lb_words;    // capacity of each lb array in words
+  uint64_t tree_leaves; // power of two >= max match tiles
+  uint64_t match_tiles; // upper bound (from n_records)
+  uint64_t pool_cap;
+};
+
+// Run parameters shared by all launches.
+struct RunArgs {
+  const argus_record* rec;
+  uint64_t n;
+  uint32_t R, K, G, shift;
+  uint32_t flags;
+  const uint8_t* region_class;
+  argus_attr_outputs out;
+  Work w;
+};
+
+// Tile counter slots.
+enum CtrSlot {
+  kCtrRec = 0,     // 16 record passes
+  kCtrEv = 16,     // 16 event passes
+  kCtrMatch = 32,
+  kCtrSweep = 33,
+  kCtrCount = 64
+};
+
+// ------------------------------------------------------- device helpers
+#if defined(__HIP_DEVICE_COMPILE__)
+#define ARGUS_DEV __device__ __forceinline__
+#else
+#define ARGUS_DEV __device__ inline
+#endif
+
+ARGUS_DEV uint64_t ld_agent(const uint64_t* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+ARGUS_DEV void st_agent(uint64_t* p, uint64_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+ARGUS_DEV void backoff() { __builtin_amdgcn_s_sleep(1); }
+
+// Look-back waits are bounded: a predecessor tile always publishes within
+// microseconds, so running out of spins means an internal error.  The wait
+// then gives up (the kernel finishes, results are wrong) and the error is
+// reported in counter ARGUS_C_INTERNAL_ERROR instead of hanging the GPU.
+constexpr uint32_t kMaxSpins = 1u << 24;
+ARGUS_DEV void flag_internal_error(uint64_t* counters, uint64_t code) {
+  atomicOr((unsigned long long*)&counters[31], (unsigned long long)code);
+}
+
+ARGUS_DEV unsigned lane_id() { return __lane_id(); }
+ARGUS_DEV uint64_t lanemask_lt() { return (1ull << lane_id()) - 1ull; }
+
+ARGUS_DEV uint32_t bit_width64(uint64_t v) { return v ? 64u - (uint32_t)__clzll(v) : 0u; }
+
+// Look-back status words: bits 62..63 hold the state, bits 0..61 the value.
+constexpr uint64_t kFlagAgg = 1ull << 62;
+constexpr uint64_t kFlagIncl = 2ull << 62;
+constexpr uint64_t kValMask = (1ull << 62) - 1;
+
+// ------------------------------------------------------------- launchers
+// Each returns hipSuccess or the launch error.
+hipError_t launch_init(const RunArgs& a, hipStream_t s);
+hipError_t launch_ingest(const RunArgs& a, hipStream_t s);
+hipError_t launch_plan(const RunArgs& a, hipStream_t s);
+hipError_t launch_radix_pass(const RunArgs& a, int which /*0 rec, 1 ev*/, int slot,
+                             uint64_t max_elems, hipStream_t s);
+hipError_t launch_check_sorted(const RunArgs& a, hipStream_t s);
+hipError_t launch_ts_hist(const RunArgs& a, hipStream_t s);
+hipError_t launch_plan2(const RunArgs& a, hipStream_t s);
+hipError_t launch_match(const RunArgs& a, hipStream_t s);
+hipError_t launch_tree(const RunArgs& a, hipStream_t s);
+hipError_t launch_resolve(const RunArgs& a, hipStream_t s);
+hipError_t launch_agg(const RunArgs& a, hipStream_t s);
+hipError_t launch_hist(const RunArgs& a, hipStream_t s);
+hipError_t launch_ev_hist(const RunArgs& a, hipStream_t s);
+hipError_t launch_ev_plan(const RunArgs& a, hipStream_t s);
+hipError_t launch_ev_clear(const RunArgs& a, hipStream_t s);
+hipError_t launch_sweep(const RunArgs& a, hipStream_t s);
+hipError_t launch_ov_final(const RunArgs& a, hipStream_t s);
+
+// Launch geometry helpers shared by host code.
+__host__ __device__ inline uint64_t ceil_div(uint64_t a, uint64_t b) { return (a + b - 1) / b; }
+
+}  // namespace argus

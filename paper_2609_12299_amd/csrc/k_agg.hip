@@ -1,0 +1,497 @@
+// k_agg.hip -- per-region observed statistics and ambiguity counts, and the
+// planning of the overlap events.
+//
+// Section 3.5 of the paper: duration is an observed field of a region
+// report, and reports expose attribution ambiguity.  Statistics are taken
+// over matched instances; unclosed, mismatched and self-nested instances are
+// counted per region.  Per-block partial results live in LDS and are flushed
+// once per block with global atomics (all integer: the result does not
+// depend on the order).
+#include "internal.h"
+
+namespace argus {
+
+constexpr uint32_t kAggLdsBytes = 96 * 1024;  // per-block statistics budget
+constexpr uint32_t kStatBytes = 6 * 8 + 5 * 4;  // per region
+constexpr uint32_t kHistBytes = 130 * 4;         // per region
+
+__device__ __forceinline__ uint32_t agg_parent(const argus_instance& x, const TileDesc* tiles,
+                                               const uint32_t* op_parent) {
+  uint32_t pf = x.parent;
+  if (pf == kNoParent || !(pf & kParentPending)) return pf;
+  const uint64_t t = pf & ~kParentPending;
+  const TileDesc d = tiles[t];
+  const uint32_t L = x.level - 1;
+  if (x.level == 0 || L < d.op_lo || L - d.op_lo >= d.n_op) return kNoParent;  // not reached
+  return op_parent[t * kMatchTile + (L - d.op_lo)];
+}
+
+struct AggArgs {
+  const DevPlan* plan;
+  argus_instance* inst;
+  const uint64_t* child_sum;
+  const TileDesc* tiles;
+  const uint32_t* op_parent;
+  uint64_t* excl_out;  // NULL unless requested
+  uint32_t* hist_key;  // NULL when histograms are done here
+  uint64_t* counters;
+  uint64_t* rstats;
+  uint32_t R;
+  uint32_t lds_regions;  // R if statistics fit in LDS, else 0
+  uint32_t hist_lds;     // histograms in LDS too
+};
+
+template <typename T>
+__device__ __forceinline__ T wsum(T v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__global__ __launch_bounds__(256) void k_agg(AggArgs a) {
+  extern __shared__ __align__(16) uint8_t smem[];
+  const uint32_t RL = a.lds_regions;
+  uint64_t* s_isum = (uint64_t*)smem;
+  uint64_t* s_esum = s_isum + RL;
+  uint64_t* s_imin = s_esum + RL;
+  uint64_t* s_imax = s_imin + RL;
+  uint64_t* s_emin = s_imax + RL;
+  uint64_t* s_emax = s_emin + RL;
+  uint32_t* s_cnt = (uint32_t*)(s_emax + RL);
+  uint32_t* s_unc = s_cnt + RL;
+  uint32_t* s_mab = s_unc + RL;
+  uint32_t* s_mae = s_mab + RL;
+  uint32_t* s_sn = s_mae + RL;
+  uint32_t* s_hist = s_sn + RL;  // [RL][130] when hist_lds
+  __shared__ uint64_t s_red[4][4];
+  for (uint32_t r = threadIdx.x; r < RL; r += 256) {
+    s_isum[r] = 0;
+    s_esum[r] = 0;
+    s_imin[r] = kU64Max;
+    s_imax[r] = 0;
+    s_emin[r] = kU64Max;
+    s_emax[r] = 0;
+    s_cnt[r] = 0;
+    s_unc[r] = 0;
+    s_mab[r] = 0;
+    s_mae[r] = 0;
+    s_sn[r] = 0;
+  }
+  if (a.hist_lds)
+    for (uint32_t i = threadIdx.x; i < RL * 130; i += 256) s_hist[i] = 0;
+  __syncthreads();
+
+  const uint64_t nb = a.plan->n_begin;
+  uint64_t n_m = 0, n_mm = 0, n_u = 0, n_sn = 0;
+  unsigned long long* rs = (unsigned long long*)a.rstats;
+  const uint64_t stride = (uint64_t)gridDim.x * 256;
+  for (uint64_t id = (uint64_t)blockIdx.x * 256 + threadIdx.x; id < nb; id += stride) {
+    argus_instance x = a.inst[id];
+    uint32_t par = agg_parent(x, a.tiles, a.op_parent);
+    if (par != kNoParent && par >= nb) {
+      flag_internal_error(a.counters, 4);
+      par = kNoParent;
+    }
+    if (par != x.parent) a.inst[id].parent = par;
+    const uint32_t region = x.region_id, ereg = x.end_region_id;
+    const bool closed = ereg != kNoEnd;
+    const bool matched = closed && ereg == region;
+    const uint64_t incl = closed ? x.t_end - x.t_begin : 0;
+    const uint64_t excl = closed ? incl - a.child_sum[id] : 0;
+    if (a.excl_out) a.excl_out[id] = excl;
+    uint32_t hk = 0xFFFFFFFFu;
+    if (matched) {
+      n_m++;
+      const bool sn = par != kNoParent && a.inst[par].region_id == region;
+      n_sn += sn;
+      const uint32_t bi = bit_width64(incl), be = bit_width64(excl);
+      hk = (region << 16) | (bi << 8) | be;
+      if (RL) {
+        atomicAdd(&s_cnt[region], 1u);
+        atomicAdd((unsigned long long*)&s_isum[region], (unsigned long long)incl);
+        atomicAdd((unsigned long long*)&s_esum[region], (unsigned long long)excl);
+        atomicMin((unsigned long long*)&s_imin[region], (unsigned long long)incl);
+        atomicMax((unsigned long long*)&s_imax[region], (unsigned long long)incl);
+        atomicMin((unsigned long long*)&s_emin[region], (unsigned long long)excl);
+        atomicMax((unsigned long long*)&s_emax[region], (unsigned long long)excl);
+        if (sn) atomicAdd(&s_sn[region], 1u);
+        if (a.hist_lds) {
+          atomicAdd(&s_hist[region * 130 + bi], 1u);
+          atomicAdd(&s_hist[region * 130 + 65 + be], 1u);
+        }
+      } else {
+        unsigned long long* row = rs + (uint64_t)region * ARGUS_RS_WIDTH;
+        atomicAdd(&row[ARGUS_RS_COUNT], 1ull);
+        atomicAdd(&row[ARGUS_RS_INCL_SUM], (unsigned long long)incl);
+        atomicAdd(&row[ARGUS_RS_EXCL_SUM], (unsigned long long)excl);
+        atomicMin(&row[ARGUS_RS_INCL_MIN], (unsigned long long)incl);
+        atomicMax(&row[ARGUS_RS_INCL_MAX], (unsigned long long)incl);
+        atomicMin(&row[ARGUS_RS_EXCL_MIN], (unsigned long long)excl);
+        atomicMax(&row[ARGUS_RS_EXCL_MAX], (unsigned long long)excl);
+        if (sn) atomicAdd(&row[ARGUS_RS_SELF_NESTED], 1ull);
+      }
+    } else if (closed) {
+      n_mm++;
+      if (RL) {
+        atomicAdd(&s_mab[region], 1u);
+        atomicAdd(&s_mae[ereg], 1u);
+      } else {
+        atomicAdd(&rs[(uint64_t)region * ARGUS_RS_WIDTH + ARGUS_RS_MISM_AS_BEGIN], 1ull);
+        atomicAdd(&rs[(uint64_t)ereg * ARGUS_RS_WIDTH + ARGUS_RS_MISM_AS_END], 1ull);
+      }
+    } else {
+      n_u++;
+      if (RL) atomicAdd(&s_unc[region], 1u);
+      else atomicAdd(&rs[(uint64_t)region * ARGUS_RS_WIDTH + ARGUS_RS_UNCLOSED], 1ull);
+    }
+    if (a.hist_key) a.hist_key[id] = hk;
+  }
+  n_m = wsum(n_m);
+  n_mm = wsum(n_mm);
+  n_u = wsum(n_u);
+  n_sn = wsum(n_sn);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    s_red[w][0] = n_m;
+    s_red[w][1] = n_mm;
+    s_red[w][2] = n_u;
+    s_red[w][3] = n_sn;
+  }
+  __syncthreads();
+  if (threadIdx.x < 4) {
+    const uint64_t v = s_red[0][threadIdx.x] + s_red[1][threadIdx.x] + s_red[2][threadIdx.x] +
+                       s_red[3][threadIdx.x];
+    const int idx = threadIdx.x == 0   ? ARGUS_C_N_MATCHED
+                    : threadIdx.x == 1 ? ARGUS_C_N_MISMATCHED
+                    : threadIdx.x == 2 ? ARGUS_C_N_UNCLOSED
+                                       : ARGUS_C_N_SELF_NESTED;
+    if (v) atomicAdd((unsigned long long*)&a.counters[idx], (unsigned long long)v);
+  }
+  for (uint32_t r = threadIdx.x; r < RL; r += 256) {
+    unsigned long long* row = rs + (uint64_t)r * ARGUS_RS_WIDTH;
+    if (s_cnt[r]) {
+      atomicAdd(&row[ARGUS_RS_COUNT], (unsigned long long)s_cnt[r]);
+      atomicAdd(&row[ARGUS_RS_INCL_SUM], (unsigned long long)s_isum[r]);
+      atomicAdd(&row[ARGUS_RS_EXCL_SUM], (unsigned long long)s_esum[r]);
+      atomicMin(&row[ARGUS_RS_INCL_MIN], (unsigned long long)s_imin[r]);
+      atomicMax(&row[ARGUS_RS_INCL_MAX], (unsigned long long)s_imax[r]);
+      atomicMin(&row[ARGUS_RS_EXCL_MIN], (unsigned long long)s_emin[r]);
+      atomicMax(&row[ARGUS_RS_EXCL_MAX], (unsigned long long)s_emax[r]);
+    }
+    if (s_unc[r]) atomicAdd(&row[ARGUS_RS_UNCLOSED], (unsigned long long)s_unc[r]);
+    if (s_mab[r]) atomicAdd(&row[ARGUS_RS_MISM_AS_BEGIN], (unsigned long long)s_mab[r]);
+    if (s_mae[r]) atomicAdd(&row[ARGUS_RS_MISM_AS_END], (unsigned long long)s_mae[r]);
+    if (s_sn[r]) atomicAdd(&row[ARGUS_RS_SELF_NESTED], (unsigned long long)s_sn[r]);
+  }
+  if (a.hist_lds) {
+    for (uint32_t i = threadIdx.x; i < RL * 130; i += 256) {
+      const uint32_t h = s_hist[i];
+      if (h) {
+        const uint32_t r = i / 130, b = i % 130;
+        atomicAdd(&rs[(uint64_t)r * ARGUS_RS_WIDTH + ARGUS_RS_HIST_INCL + b], (unsigned long long)h);
+      }
+    }
+  }
+}
+
+static void agg_sizes(uint32_t R, uint32_t* rl, uint32_t* hist_lds, size_t* bytes) {
+  if ((uint64_t)R * (kStatBytes + kHistBytes) <= kAggLdsBytes) {
+    *rl = R;
+    *hist_lds = 1;
+    *bytes = (size_t)R * (kStatBytes + kHistBytes);
+  } else if ((uint64_t)R * kStatBytes <= kAggLdsBytes) {
+    *rl = R;
+    *hist_lds = 0;
+    *bytes = (size_t)R * kStatBytes;
+  } else {
+    *rl = 0;
+    *hist_lds = 0;
+    *bytes = 0;
+  }
+}
+
+hipError_t launch_agg(const RunArgs& a, hipStream_t s) {
+  uint32_t rl, hl;
+  size_t bytes;
+  agg_sizes(a.R, &rl, &hl, &bytes);
+  AggArgs g{};
+  g.plan = a.w.plan;
+  g.inst = a.w.inst;
+  g.child_sum = a.w.child_sum;
+  g.tiles = a.w.tiles;
+  g.op_parent = a.w.op_parent;
+  g.excl_out = (a.flags & ARGUS_OUT_INSTANCE_EXCL) ? a.out.d_instance_excl : nullptr;
+  g.hist_key = hl ? nullptr : a.w.hist_key;
+  g.counters = a.out.d_counters;
+  g.rstats = a.out.d_region_stats;
+  g.R = a.R;
+  g.lds_regions = rl;
+  g.hist_lds = hl;
+  uint64_t blocks = ceil_div(a.n ? a.n : 1, 256 * 16);
+  if (blocks > 512) blocks = 512;
+  if (bytes > 64 * 1024)
+    (void)hipFuncSetAttribute((const void*)k_agg, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+  hipLaunchKernelGGL(k_agg, dim3((uint32_t)blocks), dim3(256), bytes, s, g);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------ histograms
+
+struct HistArgs {
+  const DevPlan* plan;
+  const uint32_t* hist_key;
+  uint64_t* rstats;
+  uint32_t R;
+  uint32_t slice;  // regions per slice
+};
+
+// Log2 histograms when they do not fit next to the statistics: each
+// blockIdx.y covers one slice of regions in LDS.
+__global__ __launch_bounds__(256) void k_hist(HistArgs a) {
+  extern __shared__ __align__(16) uint8_t smem[];
+  uint32_t* s_h = (uint32_t*)smem;
+  const uint32_t r0 = blockIdx.y * a.slice;
+  const uint32_t r1 = r0 + a.slice < a.R ? r0 + a.slice : a.R;
+  const uint32_t nr = r1 - r0;
+  for (uint32_t i = threadIdx.x; i < nr * 130; i += 256) s_h[i] = 0;
+  __syncthreads();
+  const uint64_t nb = a.plan->n_begin;
+  const uint64_t stride = (uint64_t)gridDim.x * 256;
+  for (uint64_t id = (uint64_t)blockIdx.x * 256 + threadIdx.x; id < nb; id += stride) {
+    const uint32_t k = a.hist_key[id];
+    if (k == 0xFFFFFFFFu) continue;
+    const uint32_t r = k >> 16;
+    if (r < r0 || r >= r1) continue;
+    atomicAdd(&s_h[(r - r0) * 130 + ((k >> 8) & 0xFFu)], 1u);
+    atomicAdd(&s_h[(r - r0) * 130 + 65 + (k & 0xFFu)], 1u);
+  }
+  __syncthreads();
+  unsigned long long* rs = (unsigned long long*)a.rstats;
+  for (uint32_t i = threadIdx.x; i < nr * 130; i += 256) {
+    const uint32_t h = s_h[i];
+    if (h) {
+      const uint32_t r = r0 + i / 130, b = i % 130;
+      atomicAdd(&rs[(uint64_t)r * ARGUS_RS_WIDTH + ARGUS_RS_HIST_INCL + b], (unsigned long long)h);
+    }
+  }
+}
+
+hipError_t launch_hist(const RunArgs& a, hipStream_t s) {
+  uint32_t rl, hl;
+  size_t bytes;
+  agg_sizes(a.R, &rl, &hl, &bytes);
+  if (hl) return hipSuccess;
+  const uint32_t slice = kAggLdsBytes / kHistBytes;
+  const uint32_t slices = (uint32_t)ceil_div(a.R, slice);
+  HistArgs h{a.w.plan, a.w.hist_key, a.out.d_region_stats, a.R, slice};
+  uint64_t blocks = ceil_div(a.n ? a.n : 1, 256 * 32);
+  if (blocks > 256) blocks = 256;
+  const size_t hb = (size_t)slice * kHistBytes;
+  (void)hipFuncSetAttribute((const void*)k_hist, hipFuncAttributeMaxDynamicSharedMemorySize, (int)hb);
+  hipLaunchKernelGGL(k_hist, dim3((uint32_t)blocks, slices), dim3(256), hb, s, h);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------- overlap events
+
+__device__ __forceinline__ uint64_t peers8b(uint32_t d, uint64_t valid) {
+  uint64_t m = valid;
+#pragma unroll
+  for (int b = 0; b < 8; ++b) {
+    const uint32_t bit = (d >> b) & 1u;
+    const uint64_t v = __ballot(bit);
+    m &= bit ? v : ~v;
+  }
+  return m;
+}
+__device__ __forceinline__ void whist(uint32_t* hist, uint32_t d, bool valid) {
+  const uint64_t vm = __ballot(valid);
+  if (vm == 0) return;
+  const uint64_t peers = peers8b(d, vm);
+  if (valid && (peers >> lane_id()) == 1ull) atomicAdd(&hist[d], (uint32_t)__popcll(peers));
+}
+
+struct EvHistArgs {
+  DevPlan* plan;
+  const argus_instance* inst;
+  const uint8_t* region_class;
+  uint32_t K, G, shift;
+  uint32_t* hist;  // ev_hist [12][256]
+  uint64_t* counters;
+};
+
+// Counts the overlap events (begin and end of each matched, classified
+// instance of a group below G) and builds the histograms of their sort
+// digits: group digits (positions 0..3) and timestamp digits (4..11), only
+// for positions that can vary.
+__global__ __launch_bounds__(256) void k_ev_hist(EvHistArgs a) {
+  __shared__ uint32_t s_hist[kDigitPositions][kRadixBins];
+  __shared__ uint64_t s_red[4][2];
+  for (int i = threadIdx.x; i < kDigitPositions * kRadixBins; i += 256) (&s_hist[0][0])[i] = 0;
+  __syncthreads();
+  const DevPlan* p = a.plan;
+  const uint64_t nb = p->n_begin;
+  const uint64_t ts_lo = p->rec.ts_min;
+  // a digit can vary only if the range of values spans a change above it
+  const bool full_ts = p->rec.ts_bits >= 64;
+  const uint64_t ts_hi = ts_lo + p->rec.ts_mask;  // upper bound of every timestamp
+  uint32_t vary = 0;
+  for (int d = 0; d < 4; ++d)
+    if (d == 0 || ((uint64_t)(a.G - 1) >> (8 * d)) != 0) vary |= 1u << d;
+  for (int d = 0; d < 8; ++d)
+    if (full_ts || ts_hi < ts_lo || (ts_lo >> (8 * d)) != (ts_hi >> (8 * d))) vary |= 1u << (4 + d);
+  uint64_t n_ev = 0, n_skip = 0;
+  const uint64_t stride = (uint64_t)gridDim.x * 256;
+  const uint64_t first = (uint64_t)blockIdx.x * 256 + (threadIdx.x & ~63u);
+  for (uint64_t b = first; b < nb; b += stride) {
+    const uint64_t id = b + (threadIdx.x & 63);
+    bool valid = false;
+    uint64_t g = 0, t0 = 0, t1 = 0;
+    if (id < nb) {
+      const argus_instance x = a.inst[id];
+      if (x.end_region_id == x.region_id) {
+        const uint32_t cls = a.region_class[x.region_id];
+        if (cls < a.K) {
+          g = a.shift >= 32 ? 0 : (x.ctx_key >> a.shift);
+          if (g < a.G) {
+            valid = true;
+            t0 = x.t_begin;
+            t1 = x.t_end;
+            n_ev += 2;
+          } else {
+            n_skip++;
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+      if ((vary >> d) & 1u) {
+        const uint32_t dg = (uint32_t)(g >> (8 * d)) & 0xFFu;
+        whist(s_hist[d], dg, valid);
+        whist(s_hist[d], dg, valid);
+      }
+#pragma unroll
+    for (int d = 0; d < 8; ++d)
+      if ((vary >> (4 + d)) & 1u) {
+        whist(s_hist[4 + d], (uint32_t)(t0 >> (8 * d)) & 0xFFu, valid);
+        whist(s_hist[4 + d], (uint32_t)(t1 >> (8 * d)) & 0xFFu, valid);
+      }
+  }
+  n_ev = wsum(n_ev);
+  n_skip = wsum(n_skip);
+  if ((threadIdx.x & 63) == 0) {
+    s_red[threadIdx.x >> 6][0] = n_ev;
+    s_red[threadIdx.x >> 6][1] = n_skip;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const uint64_t e = s_red[0][0] + s_red[1][0] + s_red[2][0] + s_red[3][0];
+    const uint64_t k = s_red[0][1] + s_red[1][1] + s_red[2][1] + s_red[3][1];
+    if (e) atomicAdd((unsigned long long*)&a.plan->n_ev, (unsigned long long)e);
+    if (k) atomicAdd((unsigned long long*)&a.counters[ARGUS_C_N_OVERLAP_SKIPPED], (unsigned long long)k);
+  }
+  for (int i = threadIdx.x; i < kDigitPositions * kRadixBins; i += 256) {
+    const uint32_t h = (&s_hist[0][0])[i];
+    if (h) atomicAdd(&a.hist[i], h);
+  }
+}
+
+hipError_t launch_ev_hist(const RunArgs& a, hipStream_t s) {
+  EvHistArgs e{a.w.plan, a.w.inst, a.region_class, a.K, a.G, a.shift, a.w.ev_hist,
+               a.out.d_counters};
+  uint64_t blocks = ceil_div(a.n ? a.n : 1, 256 * 16);
+  if (blocks > 1024) blocks = 1024;
+  hipLaunchKernelGGL(k_ev_hist, dim3((uint32_t)blocks), dim3(256), 0, s, e);
+  return hipGetLastError();
+}
+
+struct EvPlanArgs {
+  DevPlan* plan;
+  const uint32_t* hist;
+  uint32_t* off;
+  uint32_t G;
+};
+
+__global__ __launch_bounds__(256) void k_ev_plan(EvPlanArgs a) {
+  __shared__ uint32_t s_scr[4];
+  __shared__ uint32_t s_active[kDigitPositions];
+  DevPlan* p = a.plan;
+  const int t = threadIdx.x;
+  for (int pos = 0; pos < kDigitPositions; ++pos) {
+    const uint32_t h = a.hist[pos * kRadixBins + t];
+    const int used = __syncthreads_count(h != 0);
+    uint32_t x = h;
+    const int lane = t & 63, w = t >> 6;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      uint32_t y = __shfl_up(x, o);
+      if (lane >= o) x += y;
+    }
+    if (lane == 63) s_scr[w] = x;
+    __syncthreads();
+    uint32_t pre = 0;
+    for (int k = 0; k < w; ++k) pre += s_scr[k];
+    a.off[pos * kRadixBins + t] = pre + x - h;
+    if (t == 0) s_active[pos] = used > 1;
+    __syncthreads();
+  }
+  if (t != 0) return;
+  KeySpace k = p->rec;
+  k.ctx_min = 0;
+  k.ctx_bits = bit_width64(a.G > 0 ? a.G - 1 : 0);
+  k.wide = (k.ts_bits + k.ctx_bits > 64) ? 1u : 0u;
+  p->ev = k;
+  p->ev_slots = 2 * p->n_begin;
+  // LSD order: timestamp digits, then group digits.
+  uint32_t nact = 0;
+  for (int pos = 0; pos < kDigitPositions; ++pos) nact += s_active[pos];
+  uint32_t j = 0;
+  for (int sl = 0; sl < kSlots; ++sl) {
+    SlotPlan& sp = p->es[sl];
+    sp.active = 0;
+    if (sl >= 12) continue;
+    const uint32_t pos = sl < 8 ? (uint32_t)(4 + sl) : (uint32_t)(sl - 8);
+    sp.pos = pos;
+    const bool act = s_active[pos] || (nact == 0 && sl == 0 && p->n_ev > 0);
+    if (!act) continue;
+    sp.active = 1;
+    sp.src = j == 0 ? 2u : ((j - 1) & 1u);
+    sp.dst = j & 1u;
+    sp.lb = j & 1u;
+    sp.n_elems = j == 0 ? p->ev_slots : p->n_ev;
+    sp.n_out = (uint32_t)p->n_ev;
+    sp.tiles = ceil_div(sp.n_elems, kSortTile);
+    p->ev_final = sp.dst;
+    ++j;
+  }
+}
+
+hipError_t launch_ev_plan(const RunArgs& a, hipStream_t s) {
+  EvPlanArgs e{a.w.plan, a.w.ev_hist, a.w.ev_off, a.G};
+  hipLaunchKernelGGL(k_ev_plan, dim3(1), dim3(256), 0, s, e);
+  return hipGetLastError();
+}
+
+struct EvClearArgs {
+  const DevPlan* plan;
+  uint64_t* lb0;
+};
+
+// Clears the look-back status the first event pass uses.
+__global__ __launch_bounds__(256) void k_ev_clear(EvClearArgs a) {
+  const uint64_t words = ceil_div(a.plan->ev_slots, kSortTile) * kRadixBins;
+  const uint64_t stride = (uint64_t)gridDim.x * 256;
+  for (uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x; i < words; i += stride) a.lb0[i] = 0;
+}
+
+hipError_t launch_ev_clear(const RunArgs& a, hipStream_t s) {
+  EvClearArgs e{a.w.plan, a.w.lb[0]};
+  uint64_t blocks = ceil_div(ceil_div(2 * (a.n ? a.n : 1), kSortTile) * kRadixBins, 256 * 4);
+  if (blocks > 2048) blocks = 2048;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_ev_clear, dim3((uint32_t)blocks), dim3(256), 0, s, e);
+  return hipGetLastError();
+}
+
+}  // namespace argus

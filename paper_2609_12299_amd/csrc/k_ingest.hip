@@ -1,0 +1,482 @@
+// k_ingest.hip -- run initialisation, record validation and the sort plans.
+//
+// Validation follows the definition of a marker record: only BEGIN (1) and
+// END (2) transitions of known regions (id < R) carry region identity (the
+// paper's Section 3.2); anything else is counted and dropped.
+#include "internal.h"
+
+namespace argus {
+
+// ---------------------------------------------------------------- helpers
+
+// Lanes of the wave whose 8-bit value equals this lane's (restricted to
+// `valid`): eight ballots, one per bit.
+__device__ __forceinline__ uint64_t peers8(uint32_t d, uint64_t valid) {
+  uint64_t m = valid;
+#pragma unroll
+  for (int b = 0; b < 8; ++b) {
+    const uint32_t bit = (d >> b) & 1u;
+    const uint64_t v = __ballot(bit);
+    m &= bit ? v : ~v;
+  }
+  return m;
+}
+
+// Add this wave's values of digit `d` (for lanes in `valid`) into an LDS
+// histogram with one atomic per distinct digit.
+__device__ __forceinline__ void wave_hist_add(uint32_t* hist, uint32_t d, bool valid) {
+  const uint64_t vm = __ballot(valid);
+  if (vm == 0) return;
+  const uint64_t peers = peers8(d, vm);
+  if (valid && (peers >> lane_id()) == 1ull) atomicAdd(&hist[d], (uint32_t)__popcll(peers));
+}
+
+template <typename T>
+__device__ __forceinline__ T wave_sum(T v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+template <typename T>
+__device__ __forceinline__ T wave_min(T v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    T u = __shfl_xor(v, o);
+    v = u < v ? u : v;
+  }
+  return v;
+}
+template <typename T>
+__device__ __forceinline__ T wave_max(T v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    T u = __shfl_xor(v, o);
+    v = u > v ? u : v;
+  }
+  return v;
+}
+
+// Exclusive prefix sum over 256 values held one per thread of a 256-thread
+// block; returns the exclusive prefix, writes the total to *total.
+__device__ __forceinline__ uint32_t block_excl_scan256(uint32_t v, uint32_t* scratch4,
+                                                       uint32_t* total) {
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  uint32_t x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    uint32_t y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) scratch4[w] = x;
+  __syncthreads();
+  uint32_t pre = 0, tot = 0;
+  for (int k = 0; k < 4; ++k) {
+    if (k < w) pre += scratch4[k];
+    tot += scratch4[k];
+  }
+  __syncthreads();
+  *total = tot;
+  return pre + x - v;
+}
+
+// ------------------------------------------------------------------ init
+
+struct Fill {
+  uint64_t* p;
+  uint64_t n;
+  uint64_t v;
+};
+constexpr int kMaxFill = 16;
+struct FillList {
+  Fill f[kMaxFill];
+  int count;
+  uint64_t n_records;
+  uint32_t R;
+  uint32_t force_full;
+  uint64_t* counters;
+  uint64_t* rstats;
+  DevPlan* plan;
+};
+
+// Initialises every output and the parts of the workspace that a run needs
+// zeroed.  A fill kernel rather than hipMemsetAsync keeps the run
+// capturable into a HIP graph.
+__global__ __launch_bounds__(256) void k_init(FillList fl) {
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  const uint64_t tid = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  for (int s = 0; s < fl.count; ++s) {
+    const Fill f = fl.f[s];
+    for (uint64_t i = tid; i < f.n; i += stride) f.p[i] = f.v;
+  }
+  // counters
+  if (tid < ARGUS_NUM_COUNTERS) {
+    uint64_t v = 0;
+    if (tid == ARGUS_C_N_RECORDS) v = fl.n_records;
+    if (tid == ARGUS_C_TS_MIN || tid == ARGUS_C_CTX_MIN) v = kU64Max;
+    fl.counters[tid] = v;
+  }
+  // region statistics: zero, except the minima
+  const uint64_t nrs = (uint64_t)fl.R * ARGUS_RS_WIDTH;
+  for (uint64_t i = tid; i < nrs; i += stride) {
+    const uint32_t col = (uint32_t)(i % ARGUS_RS_WIDTH);
+    fl.rstats[i] = (col == ARGUS_RS_INCL_MIN || col == ARGUS_RS_EXCL_MIN) ? kU64Max : 0;
+  }
+  if (tid == 0) {
+    fl.plan->n_records = fl.n_records;
+    fl.plan->force_full = fl.force_full;
+  }
+}
+
+hipError_t launch_init(const RunArgs& a, hipStream_t s) {
+  FillList fl{};
+  const Work& w = a.w;
+  auto add = [&](void* p, uint64_t bytes, uint64_t v) {
+    if (fl.count < kMaxFill && bytes >= 8) fl.f[fl.count++] = Fill{(uint64_t*)p, bytes / 8, v};
+  };
+  add(w.plan, sizeof(DevPlan), 0);
+  add(w.rec_hist, sizeof(uint32_t) * kDigitPositions * kRadixBins, 0);
+  add(w.ev_hist, sizeof(uint32_t) * kDigitPositions * kRadixBins, 0);
+  add(w.tile_ctr, sizeof(uint32_t) * kCtrCount, 0);
+  // look-back status of the first record pass (its tiles cover every record)
+  add(w.lb[0], sizeof(uint64_t) * ceil_div(a.n ? a.n : 1, kSortTile) * kRadixBins, 0);
+  add(w.mlb, sizeof(uint64_t) * 4 * w.match_tiles, 0);
+  add(w.slb, sizeof(uint64_t) * 8 * ceil_div(a.n ? a.n : 1, kSweepTile), 0);
+  if (a.K > 0) {
+    add(w.ov_mask, sizeof(uint64_t) * kMasks * a.G, 0);
+    add(w.ov_q, sizeof(uint64_t) * kQPairs * a.G, 0);
+    add(a.out.d_overlap_group, sizeof(uint64_t) * 2ull * a.K * a.K * a.G, 0);
+    add(a.out.d_overlap_global, sizeof(uint64_t) * 2ull * a.K * a.K, 0);
+  }
+  fl.n_records = a.n;
+  fl.R = a.R;
+  fl.force_full = (a.flags & ARGUS_FORCE_FULL_SORT) ? 1u : 0u;
+  fl.counters = a.out.d_counters;
+  fl.rstats = a.out.d_region_stats;
+  fl.plan = w.plan;
+  uint64_t most = (uint64_t)a.R * ARGUS_RS_WIDTH;
+  for (int i = 0; i < fl.count; ++i) most = most > fl.f[i].n ? most : fl.f[i].n;
+  uint64_t blocks = ceil_div(most, 256 * 4);
+  if (blocks < 1) blocks = 1;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(k_init, dim3((uint32_t)blocks), dim3(256), 0, s, fl);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- ingest
+
+struct IngestArgs {
+  const uint4* rec;
+  uint64_t n;
+  uint32_t R;
+  uint64_t* counters;
+  uint32_t* hist;  // rec_hist: positions 0..3 (raw context digits)
+};
+
+// One coalesced 16-byte load per record.  Counts kinds and regions, reduces
+// the timestamp and context ranges of valid records, and builds the 256-bin
+// histograms of the four raw context digits (used by the context passes of
+// the sort).
+__global__ __launch_bounds__(256) void k_ingest(IngestArgs a) {
+  __shared__ uint32_t s_hist[4][kRadixBins];
+  __shared__ uint64_t s_red[4][8];
+  for (int i = threadIdx.x; i < 4 * kRadixBins; i += 256) (&s_hist[0][0])[i] = 0;
+  __syncthreads();
+
+  uint64_t n_valid = 0, n_badk = 0, n_badr = 0, n_begin = 0;
+  uint64_t ts_min = kU64Max, ts_max = 0, ctx_min = kU64Max, ctx_max = 0;
+  const uint64_t stride = (uint64_t)gridDim.x * 256;
+  // Every lane of a wave iterates the same number of times (ballots below).
+  const uint64_t first = (uint64_t)blockIdx.x * 256 + (threadIdx.x & ~63u);
+  for (uint64_t base = first; base < a.n; base += stride) {
+    const uint64_t i = base + (threadIdx.x & 63);
+    bool valid = false;
+    uint32_t ctx = 0;
+    if (i < a.n) {
+      const uint4 r = a.rec[i];
+      const uint64_t ts = (uint64_t)r.x | ((uint64_t)r.y << 32);
+      ctx = r.z;
+      const uint32_t region = r.w & 0xFFFFu;
+      const uint32_t kind = (r.w >> 16) & 0xFFu;
+      if (kind != 1 && kind != 2) {
+        n_badk++;
+      } else if (region >= a.R) {
+        n_badr++;
+      } else {
+        valid = true;
+        n_valid++;
+        n_begin += (kind == 1);
+        ts_min = ts < ts_min ? ts : ts_min;
+        ts_max = ts > ts_max ? ts : ts_max;
+        ctx_min = ctx < ctx_min ? ctx : ctx_min;
+        ctx_max = ctx > ctx_max ? ctx : ctx_max;
+      }
+    }
+#pragma unroll
+    for (int d = 0; d < 4; ++d) wave_hist_add(s_hist[d], (ctx >> (8 * d)) & 0xFFu, valid);
+  }
+  n_valid = wave_sum(n_valid);
+  n_badk = wave_sum(n_badk);
+  n_badr = wave_sum(n_badr);
+  n_begin = wave_sum(n_begin);
+  ts_min = wave_min(ts_min);
+  ts_max = wave_max(ts_max);
+  ctx_min = wave_min(ctx_min);
+  ctx_max = wave_max(ctx_max);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    s_red[w][0] = n_valid;
+    s_red[w][1] = n_badk;
+    s_red[w][2] = n_badr;
+    s_red[w][3] = n_begin;
+    s_red[w][4] = ts_min;
+    s_red[w][5] = ts_max;
+    s_red[w][6] = ctx_min;
+    s_red[w][7] = ctx_max;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t v[8];
+    for (int k = 0; k < 8; ++k) v[k] = s_red[0][k];
+    for (int q = 1; q < 4; ++q) {
+      for (int k = 0; k < 4; ++k) v[k] += s_red[q][k];
+      v[4] = s_red[q][4] < v[4] ? s_red[q][4] : v[4];
+      v[5] = s_red[q][5] > v[5] ? s_red[q][5] : v[5];
+      v[6] = s_red[q][6] < v[6] ? s_red[q][6] : v[6];
+      v[7] = s_red[q][7] > v[7] ? s_red[q][7] : v[7];
+    }
+    unsigned long long* c = (unsigned long long*)a.counters;
+    if (v[0]) atomicAdd(&c[ARGUS_C_N_VALID], v[0]);
+    if (v[1]) atomicAdd(&c[ARGUS_C_N_BAD_KIND], v[1]);
+    if (v[2]) atomicAdd(&c[ARGUS_C_N_BAD_REGION], v[2]);
+    if (v[3]) atomicAdd(&c[ARGUS_C_N_BEGIN], v[3]);
+    if (v[0] - v[3]) atomicAdd(&c[ARGUS_C_N_END], v[0] - v[3]);
+    if (v[0]) {
+      atomicMin(&c[ARGUS_C_TS_MIN], v[4]);
+      atomicMax(&c[ARGUS_C_TS_MAX], v[5]);
+      atomicMin(&c[ARGUS_C_CTX_MIN], v[6]);
+      atomicMax(&c[ARGUS_C_CTX_MAX], v[7]);
+    }
+  }
+  for (int i = threadIdx.x; i < 4 * kRadixBins; i += 256) {
+    const uint32_t h = (&s_hist[0][0])[i];
+    if (h) atomicAdd(&a.hist[i], h);
+  }
+}
+
+hipError_t launch_ingest(const RunArgs& a, hipStream_t s) {
+  IngestArgs ia{(const uint4*)a.rec, a.n, a.R, a.out.d_counters, a.w.rec_hist};
+  uint64_t blocks = ceil_div(a.n, 256 * 8);
+  if (blocks > 2048) blocks = 2048;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_ingest, dim3((uint32_t)blocks), dim3(256), 0, s, ia);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ plan
+
+struct PlanArgs {
+  DevPlan* plan;
+  const uint64_t* counters;
+  const uint32_t* hist;  // rec_hist
+  uint32_t* off;         // rec_off
+  uint32_t phase;        // 1: context passes; 2: full sort (if needed)
+};
+
+__device__ __forceinline__ uint64_t mask_bits(uint32_t bits) {
+  return bits >= 64 ? kU64Max : ((1ull << bits) - 1);
+}
+
+// Plans the passes of one sort phase on the device (no host round trip).
+// A digit position is active if more than one bin of its histogram is used;
+// active passes ping-pong between the two buffers and the two look-back
+// status arrays; the first pass of the record sort reads the raw records.
+__global__ __launch_bounds__(256) void k_plan(PlanArgs a) {
+  __shared__ uint32_t s_scr[4];
+  __shared__ uint32_t s_active[kDigitPositions];
+  DevPlan* p = a.plan;
+  const int t = threadIdx.x;
+  if (a.phase == 2 && !p->unsorted) return;
+  const uint64_t n_valid = a.counters[ARGUS_C_N_VALID];
+  if (a.phase == 1 && t == 0) {
+    p->n_valid = n_valid;
+    p->n_begin = a.counters[ARGUS_C_N_BEGIN];
+    KeySpace k{};
+    if (n_valid) {
+      const uint64_t ts_min = a.counters[ARGUS_C_TS_MIN], ts_max = a.counters[ARGUS_C_TS_MAX];
+      const uint64_t c_min = a.counters[ARGUS_C_CTX_MIN], c_max = a.counters[ARGUS_C_CTX_MAX];
+      k.ts_min = ts_min;
+      k.ts_bits = bit_width64(ts_max - ts_min);
+      k.ctx_min = c_min;
+      k.ctx_bits = bit_width64(c_max - c_min);
+    }
+    k.ts_mask = mask_bits(k.ts_bits);
+    k.wide = (k.ts_bits + k.ctx_bits > 64) ? 1u : 0u;
+    p->rec = k;
+    p->match_tiles = ceil_div(n_valid, kMatchTile);
+  }
+  // Histogram triviality and exclusive offsets for the positions of this phase.
+  const int pos_lo = 0, pos_hi = a.phase == 1 ? 4 : kDigitPositions;
+  for (int pos = pos_lo; pos < pos_hi; ++pos) {
+    const uint32_t h = a.hist[pos * kRadixBins + t];
+    const int used = __syncthreads_count(h != 0);
+    uint32_t total;
+    const uint32_t ex = block_excl_scan256(h, s_scr, &total);
+    a.off[pos * kRadixBins + t] = ex;
+    if (t == 0) s_active[pos] = used > 1 ? 1u : 0u;
+  }
+  __syncthreads();
+  if (t != 0) return;
+  if (a.phase == 1) {
+    // Context digits only: when every context is already in time order in the
+    // input, a stable sort on the context alone gives (ctx, ts, input) order.
+    uint32_t nact = 0;
+    for (int pos = 0; pos < 4; ++pos) nact += s_active[pos];
+    uint32_t j = 0;
+    for (int sl = 0; sl < 4; ++sl) {
+      SlotPlan& sp = p->rs[sl];
+      const uint32_t act = s_active[sl] || (nact == 0 && sl == 0);
+      sp.active = act;
+      sp.pos = (uint32_t)sl;
+      if (!act) continue;
+      sp.src = j == 0 ? 2u : ((j - 1) & 1u);
+      sp.dst = j & 1u;
+      sp.lb = j & 1u;
+      sp.n_elems = j == 0 ? p->n_records : n_valid;
+      sp.n_out = (uint32_t)n_valid;
+      sp.tiles = ceil_div(sp.n_elems, kSortTile);
+      p->rec_final = sp.dst;
+      ++j;
+    }
+    p->rec_active = j;
+  } else {
+    // Full sort: every varying timestamp digit, then every varying context
+    // digit, continuing the ping-pong from the context-sorted buffer.
+    uint32_t j = p->rec_active;
+    uint32_t cur = p->rec_final;
+    for (int sl = kPhase2Slot; sl < kSlots; ++sl) {
+      const uint32_t pos = sl < 12 ? (uint32_t)sl : (uint32_t)(sl - 12);
+      SlotPlan& sp = p->rs[sl];
+      const uint32_t act = s_active[pos] ? 1u : 0u;
+      sp.active = act;
+      sp.pos = pos;
+      if (!act) continue;
+      sp.src = cur;
+      sp.dst = cur ^ 1u;
+      sp.lb = j & 1u;
+      sp.n_elems = n_valid;
+      sp.n_out = (uint32_t)n_valid;
+      sp.tiles = ceil_div(n_valid, kSortTile);
+      cur ^= 1u;
+      ++j;
+    }
+    p->rec_final = cur;
+    p->rec_active = j;
+  }
+}
+
+hipError_t launch_plan(const RunArgs& a, hipStream_t s) {
+  PlanArgs pa{a.w.plan, a.out.d_counters, a.w.rec_hist, a.w.rec_off, 1};
+  hipLaunchKernelGGL(k_plan, dim3(1), dim3(256), 0, s, pa);
+  return hipGetLastError();
+}
+
+hipError_t launch_plan2(const RunArgs& a, hipStream_t s) {
+  PlanArgs pa{a.w.plan, a.out.d_counters, a.w.rec_hist, a.w.rec_off, 2};
+  hipLaunchKernelGGL(k_plan, dim3(1), dim3(256), 0, s, pa);
+  return hipGetLastError();
+}
+
+// ----------------------------------------------------------- sortedness
+
+struct CheckArgs {
+  DevPlan* plan;
+  const uint64_t* key[2];
+  const uint32_t* ctxw[2];
+};
+
+// After the context-only passes: is the (ctx, ts) order non-decreasing?  If
+// not (some context was out of time order in the input), the full sort runs.
+__global__ __launch_bounds__(256) void k_check_sorted(CheckArgs a) {
+  DevPlan* p = a.plan;
+  if (p->force_full) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) p->unsorted = 1;
+    return;
+  }
+  const uint64_t n = p->n_valid;
+  if (n < 2) return;
+  const uint32_t b = p->rec_final;
+  const uint64_t* key = a.key[b];
+  const uint32_t* cw = a.ctxw[b];
+  const bool wide = p->rec.wide != 0;
+  bool bad = false;
+  const uint64_t stride = (uint64_t)gridDim.x * 256;
+  for (uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x; i + 1 < n; i += stride) {
+    const uint64_t k0 = key[i], k1 = key[i + 1];
+    if (!wide) {
+      bad |= k0 > k1;
+    } else {
+      const uint32_t c0 = cw[i], c1 = cw[i + 1];
+      bad |= (c0 > c1) || (c0 == c1 && k0 > k1);
+    }
+  }
+  if (__syncthreads_or(bad) && threadIdx.x == 0) p->unsorted = 1;
+}
+
+hipError_t launch_check_sorted(const RunArgs& a, hipStream_t s) {
+  CheckArgs ca{a.w.plan, {a.w.key[0], a.w.key[1]}, {a.w.ctxw[0], a.w.ctxw[1]}};
+  uint64_t blocks = ceil_div(a.n, 256 * 16);
+  if (blocks > 2048) blocks = 2048;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_check_sorted, dim3((uint32_t)blocks), dim3(256), 0, s, ca);
+  return hipGetLastError();
+}
+
+// -------------------------------------------------- timestamp histograms
+
+struct TsHistArgs {
+  DevPlan* plan;
+  const uint64_t* key[2];
+  uint32_t* hist;  // rec_hist positions 4..11
+};
+
+// Only when the full sort is needed: histograms of the eight raw timestamp
+// digits of the (packed) records.
+__global__ __launch_bounds__(256) void k_ts_hist(TsHistArgs a) {
+  const DevPlan* p = a.plan;
+  if (!p->unsorted) return;
+  __shared__ uint32_t s_hist[8][kRadixBins];
+  for (int i = threadIdx.x; i < 8 * kRadixBins; i += 256) (&s_hist[0][0])[i] = 0;
+  __syncthreads();
+  const uint64_t n = p->n_valid;
+  const KeySpace ks = p->rec;
+  const uint64_t* key = a.key[p->rec_final];
+  const uint64_t stride = (uint64_t)gridDim.x * 256;
+  const uint64_t first = (uint64_t)blockIdx.x * 256 + (threadIdx.x & ~63u);
+  for (uint64_t base = first; base < n; base += stride) {
+    const uint64_t i = base + (threadIdx.x & 63);
+    const bool valid = i < n;
+    uint64_t ts = 0;
+    if (valid) {
+      const uint64_t k = key[i];
+      ts = ks.ts_min + (ks.wide ? k : (k & ks.ts_mask));
+    }
+#pragma unroll
+    for (int d = 0; d < 8; ++d) wave_hist_add(s_hist[d], (uint32_t)(ts >> (8 * d)) & 0xFFu, valid);
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < 8 * kRadixBins; i += 256) {
+    const uint32_t h = (&s_hist[0][0])[i];
+    if (h) atomicAdd(&a.hist[4 * kRadixBins + i], h);
+  }
+}
+
+hipError_t launch_ts_hist(const RunArgs& a, hipStream_t s) {
+  TsHistArgs ta{a.w.plan, {a.w.key[0], a.w.key[1]}, a.w.rec_hist};
+  uint64_t blocks = ceil_div(a.n, 256 * 8);
+  if (blocks > 2048) blocks = 2048;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_ts_hist, dim3((uint32_t)blocks), dim3(256), 0, s, ta);
+  return hipGetLastError();
+}
+
+}  // namespace argus

@@ -1,0 +1,509 @@
+// k_match.hip -- replay of the per-context nested region stack, in parallel.
+//
+// The paper's Section 3.2 attributes work to regions through a nested
+// region-context stack per warp: begin(id) pushes, end(id) closes the
+// innermost active region.  Over records sorted by (ctx, ts, input index)
+// the stack size after record i of a context is the clamped depth
+//   s_i = max(0, s_{i-1} + delta_i),  delta = +1 for BEGIN, -1 for END,
+// reset to 0 at the start of each context; an END with s_{i-1} = 0 is an
+// orphan.  With x_i = s_{i-1} (the depth before record i, -1 at the start of
+// a context):
+//   * the BEGIN closed by a (non-orphan) END at position j with s_j = L is the
+//     last position q < j with x_q <= L;
+//   * the parent of a BEGIN at position k with level L >= 1 is the last
+//     position q < k with x_q <= L - 1.
+// Both are previous-smaller-value searches, answered here on a min-tree over
+// x held in LDS.  The map s -> max(c, s + a) (or a constant after a context
+// start) composes associatively, so the depth entering each tile comes from
+// a decoupled look-back over tiles.  What a tile cannot resolve locally --
+// ENDs that pop a level open at the tile start, BEGINs still open at its end,
+// parents opened in an earlier tile -- is summarised per tile and resolved
+// by k_resolve.
+//
+// Exclusive time needs the sum of the inclusive durations of each instance's
+// closed children; children closed inside the tile are summed in LDS.
+#include "internal.h"
+
+namespace argus {
+
+struct Fn {
+  uint32_t reset;  // 1: output is the constant c (a context starts inside)
+  int64_t a;
+  int64_t c;       // else output is max(c, s + a)
+};
+
+__device__ __forceinline__ Fn fn_id() { return Fn{0u, 0, 0}; }
+// g after f
+__device__ __forceinline__ Fn compose(const Fn& f, const Fn& g) {
+  if (g.reset) return g;
+  Fn r;
+  r.reset = f.reset;
+  r.a = f.reset ? 0 : f.a + g.a;
+  r.c = f.c + g.a > g.c ? f.c + g.a : g.c;
+  return r;
+}
+__device__ __forceinline__ int64_t apply(const Fn& f, int64_t s) {
+  if (f.reset) return f.c;
+  return s + f.a > f.c ? s + f.a : f.c;
+}
+__device__ __forceinline__ Fn shfl_up_fn(const Fn& f, int o) {
+  Fn r;
+  r.reset = __shfl_up(f.reset, o);
+  r.a = __shfl_up(f.a, o);
+  r.c = __shfl_up(f.c, o);
+  return r;
+}
+
+// Tile aggregate in one status word: reset (1 bit), a + 2048 (13 bits),
+// c (12 bits), number of BEGINs (12 bits).
+__device__ __forceinline__ uint64_t pack_agg(const Fn& f, uint32_t nb) {
+  return kFlagAgg | ((uint64_t)f.reset << 40) | ((uint64_t)(f.a + 2048) << 24) |
+         ((uint64_t)f.c << 12) | (uint64_t)nb;
+}
+__device__ __forceinline__ void unpack_agg(uint64_t v, Fn* f, uint32_t* nb) {
+  f->reset = (uint32_t)(v >> 40) & 1u;
+  f->a = (int64_t)((v >> 24) & 0x1FFFull) - 2048;
+  f->c = (int64_t)((v >> 12) & 0xFFFull);
+  *nb = (uint32_t)(v & 0xFFFull);
+}
+
+// Last q < qpos whose leaf value is <= v, or -1 (heap-ordered min tree, leaves
+// at [kMatchTile, 2 * kMatchTile)).
+__device__ __forceinline__ int psv(const uint32_t* tree, int qpos, uint32_t v) {
+  int node = qpos + kMatchTile;
+  while (node > 1) {
+    if ((node & 1) && tree[node - 1] <= v) {
+      node = node - 1;
+      while (node < kMatchTile) node = (tree[2 * node + 1] <= v) ? 2 * node + 1 : 2 * node;
+      return node - kMatchTile;
+    }
+    node >>= 1;
+  }
+  return -1;
+}
+
+struct MatchArgs {
+  const DevPlan* plan;
+  const uint64_t* key[2];
+  const uint32_t* pay[2];
+  const uint32_t* ctxw[2];
+  argus_instance* inst;
+  uint64_t* child_sum;
+  TileDesc* tiles;
+  uint64_t* mlb;
+  uint64_t* pop_ts;
+  uint32_t* pop_reg;
+  uint32_t* pushes;
+  uint64_t* op_sum;
+  uint64_t* counters;
+  uint64_t* rstats;
+  uint32_t* tile_ctr;
+};
+
+constexpr uint32_t kParNone = 0xFFFFFFFFu;
+constexpr uint32_t kParOut = 0xFFFFFFFEu;
+
+__global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
+  const DevPlan* P = a.plan;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+
+  __shared__ uint32_t s_tile;
+  __shared__ uint64_t s_key[kMatchTile];
+  __shared__ uint32_t s_pay[kMatchTile];
+  __shared__ uint64_t s_cs[kMatchTile];     // wide contexts while loading, then child sums
+  __shared__ uint32_t s_tree[2 * kMatchTile];  // min tree, then out-of-tile child sums
+  __shared__ uint16_t s_lbr[kMatchTile];    // local BEGIN rank of each position
+  __shared__ uint16_t s_partner[kMatchTile];  // closing END of each local BEGIN
+  __shared__ Fn s_wfn[4];
+  __shared__ uint32_t s_wnb[4];
+  __shared__ uint32_t s_prevctx, s_hasprev;
+  __shared__ uint32_t s_first, s_lastp1, s_heads, s_lo, s_sout, s_maxlvl, s_orph;
+  __shared__ uint32_t s_sin, s_nbpre_lo, s_nbpre_hi;
+
+  if (tid == 0) s_tile = atomicAdd(&a.tile_ctr[kCtrMatch], 1u);
+  __syncthreads();
+  const uint64_t tile = s_tile;
+  if (tile >= P->match_tiles) return;
+
+  const KeySpace ks = P->rec;
+  const bool wide = ks.wide != 0;
+  const uint64_t nv = P->n_valid;
+  const uint64_t base = tile * kMatchTile;
+  const uint32_t cnt = nv - base < (uint64_t)kMatchTile ? (uint32_t)(nv - base) : (uint32_t)kMatchTile;
+  const uint32_t buf = P->rec_final;
+  const uint64_t* gk = a.key[buf];
+  const uint32_t* gp = a.pay[buf];
+  const uint32_t* gc = a.ctxw[buf];
+  uint32_t* s_cw = (uint32_t*)s_cs;
+  uint64_t* s_oc = (uint64_t*)s_tree;
+
+  auto ctx_of_key = [&](uint64_t k) -> uint32_t {
+    return ks.ts_bits >= 64 ? 0u : (uint32_t)(k >> ks.ts_bits);
+  };
+
+  // ---- load (coalesced, striped)
+  for (int j = 0; j < kMatchItems; ++j) {
+    const uint32_t i = (uint32_t)j * kMatchThreads + tid;
+    if (i < cnt) {
+      s_key[i] = gk[base + i];
+      s_pay[i] = gp[base + i];
+      if (wide) s_cw[i] = gc[base + i];
+    }
+  }
+  if (tid == 0) {
+    s_hasprev = base > 0;
+    s_prevctx = base > 0 ? (wide ? gc[base - 1] : ctx_of_key(gk[base - 1])) : 0u;
+    s_first = kMatchTile;
+    s_lastp1 = 0;
+    s_heads = 0;
+    s_lo = 0xFFFFFFFFu;
+    s_maxlvl = 0;
+    s_orph = 0;
+  }
+  __syncthreads();
+
+  // ---- per-thread elements (blocked: positions 8*tid .. 8*tid+7)
+  uint64_t ts[kMatchItems];
+  uint32_t ctxr[kMatchItems], reg[kMatchItems];
+  uint32_t fb = 0, fh = 0, fv = 0;  // bit i: BEGIN / context start / valid
+  Fn f = fn_id();
+  uint32_t nb = 0;
+  uint32_t first_head = kMatchTile, last_p1 = 0, nheads = 0;
+#pragma unroll
+  for (int i = 0; i < kMatchItems; ++i) {
+    const uint32_t p = (uint32_t)tid * kMatchItems + i;
+    ts[i] = 0;
+    ctxr[i] = 0;
+    reg[i] = 0;
+    if (p < cnt) {
+      const uint64_t k = s_key[p];
+      const uint32_t py = s_pay[p];
+      ctxr[i] = wide ? s_cw[p] : ctx_of_key(k);
+      ts[i] = ks.ts_min + (wide ? k : (k & ks.ts_mask));
+      reg[i] = py & 0xFFFFu;
+      const bool isb = ((py >> 16) & 1u) == 0;
+      uint32_t prev;
+      bool has_prev;
+      if (i > 0) {
+        prev = ctxr[i - 1];
+        has_prev = true;
+      } else if (p > 0) {
+        prev = wide ? s_cw[p - 1] : ctx_of_key(s_key[p - 1]);
+        has_prev = true;
+      } else {
+        prev = s_prevctx;
+        has_prev = s_hasprev != 0;
+      }
+      const bool head = !has_prev || prev != ctxr[i];
+      fv |= 1u << i;
+      if (isb) fb |= 1u << i;
+      if (head) {
+        fh |= 1u << i;
+        first_head = p < first_head ? p : first_head;
+        last_p1 = p + 1;
+        nheads++;
+      }
+      Fn e;
+      if (head) {
+        e = Fn{1u, 0, isb ? 1 : 0};
+      } else {
+        e = Fn{0u, isb ? 1 : -1, 0};
+      }
+      f = compose(f, e);
+      nb += isb;
+    }
+  }
+  if (nheads) {
+    atomicMin(&s_first, first_head);
+    atomicMax(&s_lastp1, last_p1);
+    atomicAdd(&s_heads, nheads);
+  }
+
+  // ---- block exclusive scan of the per-thread maps and BEGIN counts
+  Fn x = f;
+  uint32_t nbx = nb;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const Fn y = shfl_up_fn(x, o);
+    const uint32_t ny = __shfl_up(nbx, o);
+    if (lane >= o) {
+      x = compose(y, x);
+      nbx += ny;
+    }
+  }
+  Fn ex = shfl_up_fn(x, 1);
+  uint32_t nbex = __shfl_up(nbx, 1);
+  if (lane == 0) {
+    ex = fn_id();
+    nbex = 0;
+  }
+  if (lane == 63) {
+    s_wfn[w] = x;
+    s_wnb[w] = nbx;
+  }
+  __syncthreads();
+  Fn pre = fn_id();
+  uint32_t pnb = 0;
+  for (int k = 0; k < w; ++k) {
+    pre = compose(pre, s_wfn[k]);
+    pnb += s_wnb[k];
+  }
+  const Fn tfn = compose(pre, ex);  // map from tile input to this thread's input
+  const uint32_t tnb = pnb + nbex;  // BEGINs of the tile before this thread
+
+  // ---- decoupled look-back: depth entering the tile, BEGINs before it
+  if (tid == 0) {
+    Fn all = fn_id();
+    uint32_t nball = 0;
+    for (int k = 0; k < 4; ++k) {
+      all = compose(all, s_wfn[k]);
+      nball += s_wnb[k];
+    }
+    uint64_t s_in = 0, nbpre = 0;
+    uint64_t* lb = a.mlb;
+    if (tile > 0) {
+      st_agent(&lb[tile * 4], pack_agg(all, nball));
+      Fn acc = fn_id();
+      uint64_t nb_acc = 0;
+      int64_t tt = (int64_t)tile - 1;
+      uint32_t spins = 0;
+      while (tt >= 0) {
+        const uint64_t w1 = ld_agent(&lb[tt * 4 + 1]);
+        const uint64_t w2 = ld_agent(&lb[tt * 4 + 2]);
+        if ((w1 & ~kValMask) == kFlagIncl && (w2 & ~kValMask) == kFlagIncl) {
+          s_in = (uint64_t)apply(acc, (int64_t)(w1 & kValMask));
+          nbpre = (w2 & kValMask) + nb_acc;
+          break;
+        }
+        const uint64_t w0 = ld_agent(&lb[tt * 4]);
+        if ((w0 & ~kValMask) == kFlagAgg) {
+          Fn fa;
+          uint32_t na;
+          unpack_agg(w0, &fa, &na);
+          acc = compose(fa, acc);
+          nb_acc += na;
+          --tt;
+          continue;
+        }
+        if (++spins > kMaxSpins) {
+          flag_internal_error(a.counters, 8);
+          break;
+        }
+        backoff();
+      }
+    }
+    const uint64_t s_out = (uint64_t)apply(all, (int64_t)s_in);
+    st_agent(&lb[tile * 4 + 1], kFlagIncl | s_out);
+    st_agent(&lb[tile * 4 + 2], kFlagIncl | (nbpre + nball));
+    s_sin = (uint32_t)s_in;
+    s_nbpre_lo = (uint32_t)nbpre;
+    s_nbpre_hi = (uint32_t)(nbpre >> 32);
+  }
+  __syncthreads();
+
+  const uint32_t s_in = s_sin;
+  const uint64_t nbpre = (uint64_t)s_nbpre_lo | ((uint64_t)s_nbpre_hi << 32);
+  const uint32_t first = s_first, lastp1 = s_lastp1;
+  const bool first_is_head = first == 0;
+
+  // ---- depths, tree leaves, local BEGIN ranks
+  uint32_t sb[kMatchItems], sa[kMatchItems];
+  uint32_t cur = (uint32_t)apply(tfn, (int64_t)s_in);
+  uint32_t lb_rank = tnb;
+  uint32_t lo = 0xFFFFFFFFu, maxlvl = 0, norph = 0;
+  if (tid == 0 && !first_is_head) lo = s_in;
+#pragma unroll
+  for (int i = 0; i < kMatchItems; ++i) {
+    const uint32_t p = (uint32_t)tid * kMatchItems + i;
+    sb[i] = 0;
+    sa[i] = 0;
+    uint32_t leaf = 0xFFFFFFFFu;
+    if ((fv >> i) & 1u) {
+      const bool head = (fh >> i) & 1u;
+      const bool isb = (fb >> i) & 1u;
+      const uint32_t before = head ? 0u : cur;
+      uint32_t after;
+      if (isb) {
+        after = before + 1;
+        maxlvl = before > maxlvl ? before : maxlvl;
+        s_lbr[p] = (uint16_t)lb_rank;
+        lb_rank++;
+      } else if (before == 0) {
+        after = 0;  // orphan END
+        norph++;
+        atomicAdd((unsigned long long*)&a.rstats[(uint64_t)reg[i] * ARGUS_RS_WIDTH + ARGUS_RS_ORPHAN_END], 1ull);
+      } else {
+        after = before - 1;
+      }
+      sb[i] = before;
+      sa[i] = after;
+      leaf = head ? 0u : before + 1;  // x + 1, so that a context start is 0
+      if (p < first) lo = after < lo ? after : lo;
+      cur = after;
+      if (p + 1 == cnt) s_sout = after;
+    }
+    s_tree[kMatchTile + p] = leaf;
+  }
+  if (lo != 0xFFFFFFFFu) atomicMin(&s_lo, lo);
+  if (maxlvl) atomicMax(&s_maxlvl, maxlvl);
+  if (norph) atomicAdd(&s_orph, norph);
+  // s_cs (which aliased the wide contexts) becomes the child-sum array.
+  __syncthreads();
+  for (int k = tid; k < kMatchTile; k += kMatchThreads) {
+    s_cs[k] = 0;
+    s_partner[k] = 0xFFFF;
+  }
+  // min tree, bottom-up
+  for (int width = kMatchTile / 2; width >= 1; width >>= 1) {
+    for (int k = tid; k < width; k += kMatchThreads) {
+      const int node = width + k;
+      const uint32_t l = s_tree[2 * node], r = s_tree[2 * node + 1];
+      s_tree[node] = l < r ? l : r;
+    }
+    __syncthreads();
+  }
+
+  const uint32_t lo_head = first_is_head ? 0u : s_lo;
+  const uint32_t sin_eff = first_is_head ? 0u : s_in;
+  const uint32_t op_lo = lo_head >= 1 ? lo_head - 1 : 0;
+  const bool has_head = lastp1 > 0;
+  const uint32_t lo_tail = has_head ? 0u : lo_head;
+  const uint64_t pool = tile * kMatchTile;
+
+  // ---- searches: ENDs find their BEGIN, BEGINs find their parent
+  uint32_t par[kMatchItems];
+#pragma unroll
+  for (int i = 0; i < kMatchItems; ++i) {
+    const uint32_t p = (uint32_t)tid * kMatchItems + i;
+    par[i] = kParNone;
+    if (!((fv >> i) & 1u)) continue;
+    const bool isb = (fb >> i) & 1u;
+    if (!isb) {
+      if (sb[i] == 0) continue;  // orphan
+      const uint32_t L = sa[i];
+      const int q = psv(s_tree, (int)p, L + 1);
+      if (q >= 0) {
+        s_partner[s_lbr[q]] = (uint16_t)p;
+      } else {
+        // pops a level that was open when the tile started
+        const uint32_t idx = L - lo_head;
+        if (L >= lo_head && idx < (uint32_t)kMatchTile) {
+          a.pop_ts[pool + idx] = ts[i];
+          a.pop_reg[pool + idx] = reg[i];
+        } else {
+          flag_internal_error(a.counters, 16);
+        }
+      }
+    } else {
+      const uint32_t L = sb[i];
+      if (L >= 1) {
+        const int q = psv(s_tree, (int)p, L);
+        par[i] = q >= 0 ? (uint32_t)s_lbr[q] : kParOut;
+      }
+    }
+  }
+  __syncthreads();
+  for (int k = tid; k < kMatchTile; k += kMatchThreads) s_oc[k] = 0;
+  __syncthreads();
+
+  // ---- instances and child sums
+#pragma unroll
+  for (int i = 0; i < kMatchItems; ++i) {
+    const uint32_t p = (uint32_t)tid * kMatchItems + i;
+    if (!((fv >> i) & 1u) || !((fb >> i) & 1u)) continue;
+    const uint32_t k = s_lbr[p];
+    const uint64_t id = nbpre + k;
+    const uint32_t L = sb[i];
+    const uint32_t j = s_partner[k];
+    uint64_t t_end = kU64Max;
+    uint32_t ereg = kNoEnd;
+    if (j != 0xFFFF) {
+      const uint64_t kj = s_key[j];
+      t_end = ks.ts_min + (wide ? kj : (kj & ks.ts_mask));
+      ereg = s_pay[j] & 0xFFFFu;
+      const uint64_t incl = t_end - ts[i];
+      if (par[i] == kParOut) {
+        const uint32_t oi = (L - 1) - op_lo;
+        if (L >= 1 + op_lo && oi < (uint32_t)kMatchTile)
+          atomicAdd((unsigned long long*)&s_oc[oi], (unsigned long long)incl);
+        else
+          flag_internal_error(a.counters, 16);
+      } else if (par[i] != kParNone) {
+        atomicAdd((unsigned long long*)&s_cs[par[i]], (unsigned long long)incl);
+      }
+    } else if (lastp1 <= p + 1) {
+      // still open when the tile ends, in a context that may continue
+      if (L >= lo_tail && L - lo_tail < (uint32_t)kMatchTile)
+        a.pushes[pool + (L - lo_tail)] = (uint32_t)id;
+      else
+        flag_internal_error(a.counters, 16);
+    }
+    uint32_t pf;
+    if (par[i] == kParNone) pf = kNoParent;
+    else if (par[i] == kParOut) pf = kParentPending | (uint32_t)tile;
+    else pf = (uint32_t)(nbpre + par[i]);
+    uint4* dst = (uint4*)(a.inst + id);
+    dst[0] = make_uint4((uint32_t)ts[i], (uint32_t)(ts[i] >> 32), (uint32_t)t_end,
+                        (uint32_t)(t_end >> 32));
+    dst[1] = make_uint4(ctxr[i] + (uint32_t)ks.ctx_min, pf, L, reg[i] | (ereg << 16));
+  }
+  __syncthreads();
+
+  // ---- per-tile outputs
+  const uint32_t tile_nb = s_wnb[0] + s_wnb[1] + s_wnb[2] + s_wnb[3];
+  for (uint32_t k = tid; k < tile_nb; k += kMatchThreads) a.child_sum[nbpre + k] = s_cs[k];
+  const uint32_t n_op = (sin_eff > op_lo) ? ((sin_eff - op_lo) < (uint32_t)kMatchTile ? sin_eff - op_lo : (uint32_t)kMatchTile) : 0u;
+  for (uint32_t k = tid; k < n_op; k += kMatchThreads) a.op_sum[pool + k] = s_oc[k];
+  if (tid == 0) {
+    const uint32_t s_out = cnt ? s_sout : 0u;
+    TileDesc d;
+    d.key = has_head ? -1 : (int64_t)lo_head;
+    d.s_in = sin_eff;
+    d.lo_head = lo_head;
+    d.s_out = s_out;
+    d.lo_tail = lo_tail;
+    d.op_lo = op_lo;
+    d.pop_base = 0;
+    d.push_base = 0;
+    d.op_base = 0;
+    d.n_pop = sin_eff - lo_head;
+    d.n_push = s_out - lo_tail;
+    if (d.n_pop > (uint32_t)kMatchTile || d.n_push > (uint32_t)kMatchTile) {
+      flag_internal_error(a.counters, 32);
+      d.n_pop = d.n_pop > (uint32_t)kMatchTile ? 0u : d.n_pop;
+      d.n_push = d.n_push > (uint32_t)kMatchTile ? 0u : d.n_push;
+    }
+    d.n_op = n_op;
+    d.pad = 0;
+    a.tiles[tile] = d;
+    unsigned long long* c = (unsigned long long*)a.counters;
+    if (s_heads) atomicAdd(&c[ARGUS_C_N_CTX], (unsigned long long)s_heads);
+    if (s_maxlvl) atomicMax(&c[ARGUS_C_MAX_LEVEL], (unsigned long long)s_maxlvl);
+    if (s_orph) atomicAdd(&c[ARGUS_C_N_ORPHAN_END], (unsigned long long)s_orph);
+  }
+}
+
+hipError_t launch_match(const RunArgs& a, hipStream_t s) {
+  MatchArgs m{};
+  m.plan = a.w.plan;
+  for (int b = 0; b < 2; ++b) {
+    m.key[b] = a.w.key[b];
+    m.pay[b] = a.w.pay[b];
+    m.ctxw[b] = a.w.ctxw[b];
+  }
+  m.inst = a.w.inst;
+  m.child_sum = a.w.child_sum;
+  m.tiles = a.w.tiles;
+  m.mlb = a.w.mlb;
+  m.pop_ts = a.w.pop_ts;
+  m.pop_reg = a.w.pop_reg;
+  m.pushes = a.w.pushes;
+  m.op_sum = a.w.op_sum;
+  m.counters = a.out.d_counters;
+  m.rstats = a.out.d_region_stats;
+  m.tile_ctr = a.w.tile_ctr;
+  hipLaunchKernelGGL(k_match, dim3((uint32_t)a.w.match_tiles), dim3(kMatchThreads), 0, s, m);
+  return hipGetLastError();
+}
+
+}  // namespace argus

@@ -1,0 +1,284 @@
+// k_radix.hip -- one stable LSD radix pass over 8-bit digits.
+//
+// Stable sorting is how the records of every execution context are put in
+// execution order before the per-context stack is replayed (the paper's
+// Section 3.2 keeps one nested region-context stack per warp); the same
+// pass orders the overlap events by (group, time).
+//
+// One pass, per tile of 4096 elements (4 waves x 16 rounds x 64 lanes):
+//   * rank: each wave finds, with eight ballots, the lanes holding the same
+//     digit and counts them in per-wave LDS digit counters (stable order is
+//     wave, round, lane = element order);
+//   * the tile's 256 digit counts are published for decoupled look-back
+//     (Merrill & Garland 2016) with tile ids taken in launch order from an
+//     atomic counter, so every predecessor tile is already running;
+//   * elements are staged in LDS in digit order and written out so that a
+//     run of equal digits goes to consecutive addresses.
+// The first pass of a sort reads its raw source (records or instances),
+// drops invalid elements (they are never written) and packs the key.
+#include "internal.h"
+
+namespace argus {
+
+struct RadixArgs {
+  const DevPlan* plan;
+  int which;  // 0: records, 1: overlap events
+  int slot;
+  const uint4* rec;
+  const argus_instance* inst;
+  const uint8_t* region_class;
+  uint32_t R, K, G, shift;
+  uint64_t* key[2];
+  uint32_t* pay[2];
+  uint32_t* ctxw[2];
+  uint64_t* lb[2];
+  const uint32_t* off;  // [12][256] exclusive digit offsets
+  uint32_t* tile_ctr;
+  uint64_t* counters;
+};
+
+__device__ __forceinline__ uint32_t digit_of(uint32_t pos, uint64_t raw_ctx, uint64_t raw_ts) {
+  return pos < 4 ? (uint32_t)(raw_ctx >> (8 * pos)) & 0xFFu
+                 : (uint32_t)(raw_ts >> (8 * (pos - 4))) & 0xFFu;
+}
+
+__global__ __launch_bounds__(kSortThreads) void k_radix_pass(RadixArgs a) {
+  const SlotPlan sp = a.which ? a.plan->es[a.slot] : a.plan->rs[a.slot];
+  if (!sp.active) return;
+  const KeySpace ks = a.which ? a.plan->ev : a.plan->rec;
+
+  __shared__ uint32_t s_tile;
+  __shared__ uint32_t s_wave[4][kRadixBins];  // per-wave counts, then wave prefixes
+  __shared__ uint32_t s_start[kRadixBins];    // tile-local start of each digit
+  __shared__ uint32_t s_gbase[kRadixBins];    // global start of this tile's digit run
+  __shared__ uint32_t s_scr[4];
+  __shared__ uint32_t s_total;
+  __shared__ uint64_t s_key[kSortTile];
+  __shared__ uint32_t s_pay[kSortTile];
+  __shared__ uint32_t s_cw[kSortTile];
+  __shared__ uint8_t s_dig[kSortTile];
+
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  if (tid == 0) s_tile = atomicAdd(&a.tile_ctr[(a.which ? kCtrEv : kCtrRec) + a.slot], 1u);
+  for (int i = tid; i < 4 * kRadixBins; i += kSortThreads) (&s_wave[0][0])[i] = 0;
+  __syncthreads();
+  const uint64_t tile = s_tile;
+  if (tile >= sp.tiles) return;
+
+  const uint64_t base = tile * kSortTile;
+  const uint64_t left = sp.n_elems - base;
+  const uint32_t cnt = left < (uint64_t)kSortTile ? (uint32_t)left : (uint32_t)kSortTile;
+  const bool wide = ks.wide != 0;
+  const uint32_t pos = sp.pos;
+
+  uint64_t key[kSortItems];
+  uint32_t pay[kSortItems], cw[kSortItems], dig[kSortItems], rank[kSortItems];
+
+  const uint64_t* ksrc = sp.src < 2 ? a.key[sp.src] : nullptr;
+  const uint32_t* psrc = sp.src < 2 ? a.pay[sp.src] : nullptr;
+  const uint32_t* csrc = sp.src < 2 ? a.ctxw[sp.src] : nullptr;
+
+#pragma unroll
+  for (int r = 0; r < kSortItems; ++r) {
+    const uint32_t el = (uint32_t)w * (kSortItems * 64) + (uint32_t)r * 64 + lane;
+    uint32_t d = 256;  // 256: no element / invalid (never written)
+    key[r] = 0;
+    pay[r] = 0;
+    cw[r] = 0;
+    if (el < cnt) {
+      const uint64_t e = base + el;
+      if (sp.src < 2) {
+        const uint64_t k = ksrc[e];
+        key[r] = k;
+        pay[r] = psrc[e];
+        uint64_t ctx_rel, ts_off;
+        if (wide) {
+          cw[r] = csrc[e];
+          ctx_rel = cw[r];
+          ts_off = k;
+        } else {
+          ctx_rel = ks.ts_bits >= 64 ? 0 : (k >> ks.ts_bits);
+          ts_off = k & ks.ts_mask;
+        }
+        d = digit_of(pos, ks.ctx_min + ctx_rel, ks.ts_min + ts_off);
+      } else if (a.which == 0) {
+        const uint4 rr = a.rec[e];
+        const uint64_t ts = (uint64_t)rr.x | ((uint64_t)rr.y << 32);
+        const uint32_t ctx = rr.z;
+        const uint32_t region = rr.w & 0xFFFFu;
+        const uint32_t kind = (rr.w >> 16) & 0xFFu;
+        if ((kind == 1 || kind == 2) && region < a.R) {
+          const uint64_t ts_off = ts - ks.ts_min;
+          const uint64_t ctx_rel = (uint64_t)ctx - ks.ctx_min;
+          key[r] = wide ? ts_off : ((ks.ts_bits >= 64 ? 0 : (ctx_rel << ks.ts_bits)) | ts_off);
+          cw[r] = (uint32_t)ctx_rel;
+          pay[r] = region | ((kind - 1u) << 16);
+          d = digit_of(pos, ctx, ts);
+        }
+      } else {
+        // Overlap events: element e is the begin (even) or end (odd) of
+        // instance e / 2; only matched, classified instances of a group < G.
+        const argus_instance* ip = a.inst + (e >> 1);
+        const uint32_t is_end = (uint32_t)(e & 1);
+        const uint64_t t = is_end ? ip->t_end : ip->t_begin;
+        const uint32_t ctx = ip->ctx_key;
+        const uint32_t regs = *(const uint32_t*)&ip->region_id;  // region | end_region << 16
+        const uint32_t region = regs & 0xFFFFu, eregion = regs >> 16;
+        if (region == eregion) {
+          const uint32_t cls = a.region_class[region];
+          const uint64_t g = a.shift >= 32 ? 0 : (ctx >> a.shift);
+          if (cls < a.K && g < a.G) {
+            const uint64_t ts_off = t - ks.ts_min;
+            key[r] = wide ? ts_off : ((ks.ts_bits >= 64 ? 0 : (g << ks.ts_bits)) | ts_off);
+            cw[r] = (uint32_t)g;
+            pay[r] = cls | (is_end << 8);
+            d = digit_of(pos, g, t);
+          }
+        }
+      }
+    }
+    dig[r] = d;
+    // Rank among this wave's elements with the same digit (stable).
+    const bool part = d < 256;
+    const uint64_t vm = __ballot(part);
+    uint64_t peers = vm;
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      const uint32_t bit = (d >> b) & 1u;
+      const uint64_t m = __ballot(bit);
+      peers &= bit ? m : ~m;
+    }
+    uint32_t rk = 0;
+    if (part) {
+      const uint32_t before = (uint32_t)__popcll(peers & lanemask_lt());
+      const uint32_t old = s_wave[w][d];
+      rk = old + before;
+      __builtin_amdgcn_wave_barrier();
+      if ((peers >> lane) == 1ull) s_wave[w][d] = old + (uint32_t)__popcll(peers);
+    }
+    __builtin_amdgcn_wave_barrier();
+    rank[r] = rk;
+  }
+  __syncthreads();
+
+  // Digit totals of the tile, per-wave prefixes and tile-local starts.
+  const int dgt = tid;
+  uint32_t c0 = s_wave[0][dgt], c1 = s_wave[1][dgt], c2 = s_wave[2][dgt], c3 = s_wave[3][dgt];
+  const uint32_t tot = c0 + c1 + c2 + c3;
+  uint32_t lane_total;
+  {
+    uint32_t x = tot;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      uint32_t y = __shfl_up(x, o);
+      if (lane >= o) x += y;
+    }
+    if (lane == 63) s_scr[w] = x;
+    __syncthreads();
+    uint32_t pre = 0, all = 0;
+    for (int k = 0; k < 4; ++k) {
+      if (k < w) pre += s_scr[k];
+      all += s_scr[k];
+    }
+    s_start[dgt] = pre + x - tot;
+    lane_total = all;
+  }
+  s_wave[0][dgt] = 0;
+  s_wave[1][dgt] = c0;
+  s_wave[2][dgt] = c0 + c1;
+  s_wave[3][dgt] = c0 + c1 + c2;
+  if (tid == 0) s_total = lane_total;
+
+  // Decoupled look-back on the count of this digit in earlier tiles.
+  uint64_t* lb = a.lb[sp.lb];
+  uint64_t excl = 0;
+  if (tile == 0) {
+    st_agent(&lb[dgt], kFlagIncl | tot);
+  } else {
+    st_agent(&lb[tile * kRadixBins + dgt], kFlagAgg | tot);
+    int64_t tt = (int64_t)tile - 1;
+    uint32_t spins = 0;
+    while (tt >= 0) {
+      const uint64_t v = ld_agent(&lb[(uint64_t)tt * kRadixBins + dgt]);
+      const uint64_t f = v & ~kValMask;
+      if (f == 0) {
+        if (++spins > kMaxSpins) {
+          flag_internal_error(a.counters, 1);
+          break;
+        }
+        backoff();
+        continue;
+      }
+      excl += v & kValMask;
+      if (f == kFlagIncl) break;
+      --tt;
+    }
+    st_agent(&lb[tile * kRadixBins + dgt], kFlagIncl | (excl + tot));
+  }
+  s_gbase[dgt] = a.off[pos * kRadixBins + dgt] + (uint32_t)excl;
+  // The other status array is the one the next pass uses: clear our slots.
+  a.lb[sp.lb ^ 1u][tile * kRadixBins + dgt] = 0;
+  __syncthreads();
+
+  // Stage in LDS in digit order.
+#pragma unroll
+  for (int r = 0; r < kSortItems; ++r) {
+    const uint32_t d = dig[r];
+    if (d < 256) {
+      const uint32_t lp = s_start[d] + s_wave[w][d] + rank[r];
+      s_key[lp] = key[r];
+      s_pay[lp] = pay[r];
+      s_cw[lp] = cw[r];
+      s_dig[lp] = (uint8_t)d;
+    }
+  }
+  __syncthreads();
+
+  // Write out: consecutive staged elements of one digit go to consecutive
+  // global positions.
+  const uint32_t total = s_total;
+  uint64_t* kd = a.key[sp.dst];
+  uint32_t* pd = a.pay[sp.dst];
+  uint32_t* cd = a.ctxw[sp.dst];
+  const uint32_t n_out = sp.n_out;
+  for (uint32_t i = tid; i < total; i += kSortThreads) {
+    const uint32_t d = s_dig[i];
+    const uint32_t gp = s_gbase[d] + (i - s_start[d]);
+    if (gp >= n_out) {
+      flag_internal_error(a.counters, 2);
+      continue;
+    }
+    kd[gp] = s_key[i];
+    pd[gp] = s_pay[i];
+    if (wide) cd[gp] = s_cw[i];
+  }
+}
+
+hipError_t launch_radix_pass(const RunArgs& a, int which, int slot, uint64_t max_elems,
+                             hipStream_t s) {
+  RadixArgs ra{};
+  ra.plan = a.w.plan;
+  ra.which = which;
+  ra.slot = slot;
+  ra.rec = (const uint4*)a.rec;
+  ra.inst = a.w.inst;
+  ra.region_class = a.region_class;
+  ra.R = a.R;
+  ra.K = a.K;
+  ra.G = a.G;
+  ra.shift = a.shift;
+  for (int b = 0; b < 2; ++b) {
+    ra.key[b] = a.w.key[b];
+    ra.pay[b] = a.w.pay[b];
+    ra.ctxw[b] = a.w.ctxw[b];
+    ra.lb[b] = a.w.lb[b];
+  }
+  ra.off = which ? a.w.ev_off : a.w.rec_off;
+  ra.tile_ctr = a.w.tile_ctr;
+  ra.counters = a.out.d_counters;
+  uint64_t blocks = ceil_div(max_elems ? max_elems : 1, kSortTile);
+  hipLaunchKernelGGL(k_radix_pass, dim3((uint32_t)blocks), dim3(kSortThreads), 0, s, ra);
+  return hipGetLastError();
+}
+
+}  // namespace argus

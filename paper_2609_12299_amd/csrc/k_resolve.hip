@@ -1,0 +1,194 @@
+// k_resolve.hip -- stack pairs that cross tile boundaries.
+//
+// After k_match, each tile t has summarised what it could not resolve:
+//   * pops: ENDs that close levels [lo_head, s_in) open when t started;
+//   * pushes: BEGINs at levels [lo_tail, s_out) still open when t ends;
+//   * references to enclosing instances at levels [op_lo, s_in) (parents of
+//     BEGINs opened in t, and the durations of their children closed in t).
+// With key(t) = -1 if t holds a context start, else the lowest depth seen in
+// t, the END closing a push at level L of tile t is the pop at level L of the
+// first later tile with key <= L (if that tile continues the context and
+// pops L; otherwise the BEGIN is unclosed), and the instance open at level L
+// when tile t starts is the push at level L of the last earlier tile with
+// key <= L.  Both searches run on a min-tree over the tile keys.
+#include "internal.h"
+
+namespace argus {
+
+constexpr int64_t kInf = 0x7FFFFFFFFFFFFFFFll;
+
+// ------------------------------------------------------------ tile tree
+
+struct TreeArgs {
+  const DevPlan* plan;
+  const TileDesc* tiles;
+  int64_t* tree;
+  uint64_t leaves;
+};
+
+// Leaves and the bottom levels (subtrees of up to 1024 leaves per block).
+__global__ __launch_bounds__(256) void k_tree_lo(TreeArgs a) {
+  __shared__ int64_t s[2048];
+  const uint64_t ntiles = a.plan->match_tiles;
+  const uint64_t sub = a.leaves < 1024 ? a.leaves : 1024;
+  const uint64_t first = (uint64_t)blockIdx.x * sub;
+  for (uint64_t i = threadIdx.x; i < sub; i += 256) {
+    const uint64_t t = first + i;
+    const int64_t v = t < ntiles ? a.tiles[t].key : kInf;
+    s[sub + i] = v;
+    a.tree[a.leaves + t] = v;
+  }
+  __syncthreads();
+  // local heap: node j (1 <= j < sub) covers global node (leaves + first) / sub ... ;
+  // global index of local node j at depth d is (a.leaves / sub) * ... computed below.
+  for (uint64_t width = sub / 2; width >= 1; width >>= 1) {
+    for (uint64_t k = threadIdx.x; k < width; k += 256) {
+      const uint64_t node = width + k;
+      const int64_t l = s[2 * node], r = s[2 * node + 1];
+      const int64_t m = l < r ? l : r;
+      s[node] = m;
+      // global node: level with `width` local nodes corresponds to global
+      // level with width * gridDim.x nodes; offset by this block's share.
+      const uint64_t gwidth = width * gridDim.x;
+      a.tree[gwidth + (uint64_t)blockIdx.x * width + k] = m;
+    }
+    __syncthreads();
+    if (width == 1) break;
+  }
+}
+
+// Upper levels above the per-block subtrees (one block).
+__global__ __launch_bounds__(1024) void k_tree_hi(TreeArgs a, uint64_t roots) {
+  for (uint64_t width = roots / 2; width >= 1; width >>= 1) {
+    for (uint64_t k = threadIdx.x; k < width; k += 1024) {
+      const uint64_t node = width + k;
+      const int64_t l = a.tree[2 * node], r = a.tree[2 * node + 1];
+      a.tree[node] = l < r ? l : r;
+    }
+    __syncthreads();
+    if (width == 1) break;
+  }
+}
+
+hipError_t launch_tree(const RunArgs& a, hipStream_t s) {
+  TreeArgs ta{a.w.plan, a.w.tiles, a.w.tree, a.w.tree_leaves};
+  const uint64_t sub = a.w.tree_leaves < 1024 ? a.w.tree_leaves : 1024;
+  const uint64_t blocks = a.w.tree_leaves / sub;
+  hipLaunchKernelGGL(k_tree_lo, dim3((uint32_t)blocks), dim3(256), 0, s, ta);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || blocks == 1) return e;
+  hipLaunchKernelGGL(k_tree_hi, dim3(1), dim3(1024), 0, s, ta, blocks);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------- searches
+
+// First tile index > t with key <= v, or -1.
+__device__ __forceinline__ int64_t first_le(const int64_t* tree, uint64_t leaves, uint64_t t,
+                                            int64_t v) {
+  uint64_t node = t + leaves;
+  while (node > 1) {
+    if (!(node & 1) && tree[node + 1] <= v) {
+      node = node + 1;
+      while (node < leaves) node = (tree[2 * node] <= v) ? 2 * node : 2 * node + 1;
+      return (int64_t)(node - leaves);
+    }
+    node >>= 1;
+  }
+  return -1;
+}
+
+// Last tile index < t with key <= v, or -1.
+__device__ __forceinline__ int64_t last_le(const int64_t* tree, uint64_t leaves, uint64_t t,
+                                           int64_t v) {
+  uint64_t node = t + leaves;
+  while (node > 1) {
+    if ((node & 1) && tree[node - 1] <= v) {
+      node = node - 1;
+      while (node < leaves) node = (tree[2 * node + 1] <= v) ? 2 * node + 1 : 2 * node;
+      return (int64_t)(node - leaves);
+    }
+    node >>= 1;
+  }
+  return -1;
+}
+
+struct ResolveArgs {
+  const DevPlan* plan;
+  const TileDesc* tiles;
+  const int64_t* tree;
+  uint64_t leaves;
+  const uint64_t* pop_ts;
+  const uint32_t* pop_reg;
+  const uint32_t* pushes;
+  uint32_t* op_parent;
+  const uint64_t* op_sum;
+  argus_instance* inst;
+  uint64_t* child_sum;
+  uint64_t* counters;
+};
+
+// Instance open at level L when tile t starts.  (Such a tile always exists
+// for the levels k_match refers to; the checks only keep every access in
+// bounds.)
+__device__ __forceinline__ uint32_t enclosing(const ResolveArgs& a, uint64_t t, uint32_t L) {
+  const int64_t tp = last_le(a.tree, a.leaves, t, (int64_t)L);
+  if (tp < 0) return kNoParent;
+  const TileDesc d = a.tiles[tp];
+  if (L < d.lo_tail || L - d.lo_tail >= d.n_push) return kNoParent;
+  return a.pushes[(uint64_t)tp * kMatchTile + (L - d.lo_tail)];
+}
+
+// One wave per tile.
+__global__ __launch_bounds__(256) void k_resolve(ResolveArgs a) {
+  const uint64_t t = (uint64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const uint32_t lane = threadIdx.x & 63;
+  if (t >= a.plan->match_tiles) return;
+  const TileDesc d = a.tiles[t];
+  const uint64_t pool = t * kMatchTile;
+  const uint64_t nb = a.plan->n_begin;
+  // BEGINs still open at the end of tile t.
+  for (uint32_t i = lane; i < d.n_push; i += 64) {
+    const uint32_t L = d.lo_tail + i;
+    const uint32_t id = a.pushes[pool + i];
+    if (id >= nb) {
+      flag_internal_error(a.counters, 64);
+      continue;
+    }
+    const int64_t t2 = first_le(a.tree, a.leaves, t, (int64_t)L);
+    if (t2 < 0) continue;  // context ends with the data: unclosed
+    const TileDesc d2 = a.tiles[t2];
+    if (L < d2.lo_head || L - d2.lo_head >= d2.n_pop) continue;  // context ended: unclosed
+    const uint64_t q = (uint64_t)t2 * kMatchTile + (L - d2.lo_head);
+    const uint64_t t_end = a.pop_ts[q];
+    const uint32_t ereg = a.pop_reg[q];
+    argus_instance* x = a.inst + id;
+    x->t_end = t_end;
+    x->end_region_id = (uint16_t)ereg;
+    const uint64_t incl = t_end - x->t_begin;
+    uint32_t pf = x->parent;
+    if (pf == kNoParent) continue;
+    if (pf & kParentPending) pf = L >= 1 ? enclosing(a, t, L - 1) : kNoParent;
+    if (pf == kNoParent || pf >= nb) continue;
+    atomicAdd((unsigned long long*)&a.child_sum[pf], (unsigned long long)incl);
+  }
+  // Instances open when tile t starts that tile t refers to.
+  for (uint32_t i = lane; i < d.n_op; i += 64) {
+    const uint32_t L = d.op_lo + i;
+    const uint32_t pid = enclosing(a, t, L);
+    a.op_parent[pool + i] = pid;
+    const uint64_t sum = a.op_sum[pool + i];
+    if (sum && pid < nb) atomicAdd((unsigned long long*)&a.child_sum[pid], (unsigned long long)sum);
+  }
+}
+
+hipError_t launch_resolve(const RunArgs& a, hipStream_t s) {
+  ResolveArgs r{a.w.plan, a.w.tiles, a.w.tree, a.w.tree_leaves, a.w.pop_ts, a.w.pop_reg,
+                a.w.pushes, a.w.op_parent, a.w.op_sum, a.w.inst, a.w.child_sum,
+                a.out.d_counters};
+  const uint64_t blocks = ceil_div(a.w.match_tiles, 4);
+  hipLaunchKernelGGL(k_resolve, dim3((uint32_t)blocks), dim3(256), 0, s, r);
+  return hipGetLastError();
+}
+
+}  // namespace argus

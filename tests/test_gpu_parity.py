@@ -1,0 +1,169 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle, element by
+element and bit-exact: counters, per-region statistics, overlap matrices,
+instances and exclusive durations.
+
+Sizes span several sort tiles (4096) and matching tiles (2048) with ragged
+tails; edge cases cover empty and all-invalid inputs, ties, orphans, unclosed
+and mismatched markers, nesting deeper than a tile, contexts spanning many
+tiles, keys wider than 64 bits and inputs that are out of time order inside
+a context (the full sort)."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from golden_util import (case_params, expected_counters, expected_instances,
+                         expected_region_stats, load_cases, random_malformed,
+                         random_wellformed, records_from_rows)
+from gpu_util import assert_parity, gpu_run, log, oracle_run
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU in this container")
+    from paper_2609_12299_amd import load_library
+    load_library()  # fails loudly if the HIP library is missing
+    return torch
+
+
+CASES = load_cases()
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c["name"] for c in CASES])
+def test_hand_traces(oracle_mod, case):
+    log(f"[gpu] hand trace {case['name']}")
+    rec = records_from_rows(case["records"])
+    p = case_params(case)
+    g = gpu_run(rec, p)
+    np.testing.assert_array_equal(g["counters"], expected_counters(case))
+    if "region_stats" in case:
+        np.testing.assert_array_equal(g["region_stats"], expected_region_stats(case))
+    if "instances" in case:
+        assert g["instances"].tobytes() == expected_instances(case).tobytes()
+        np.testing.assert_array_equal(g["instance_excl"], np.array(case["excl"], np.uint64))
+    if "overlap_group" in case:
+        np.testing.assert_array_equal(g["overlap_group"], np.array(case["overlap_group"], np.uint64))
+    assert_parity(g, oracle_run(oracle_mod, rec, p), what=case["name"])
+
+
+SIZES = [0, 1, 2, 63, 64, 65, 2047, 2048, 2049, 4095, 4096, 4097, 10007, 30001]
+
+
+@pytest.mark.parametrize("n", SIZES)
+@pytest.mark.parametrize("n_ctx,ts_range", [(1, 1 << 40), (3, 40), (50, 1 << 20)])
+def test_random_malformed(oracle_mod, n, n_ctx, ts_range):
+    rng = np.random.default_rng(n * 131 + n_ctx)
+    R = 7
+    rec = random_malformed(rng, n, n_ctx, R, ts_range)
+    cls = rng.integers(0, 4, size=R).astype(np.uint8)
+    p = dict(num_regions=R, num_classes=3, region_class=cls, group_shift=1, num_groups=20)
+    log(f"[gpu] random malformed n={n} ctx={n_ctx} ts_range={ts_range}")
+    assert_parity(gpu_run(rec, p), oracle_run(oracle_mod, rec, p), what=f"n={n}")
+
+
+@pytest.mark.parametrize("force_full", [False, True])
+@pytest.mark.parametrize("seed", [0, 1])
+def test_random_wellformed(oracle_mod, seed, force_full):
+    rng = np.random.default_rng(100 + seed)
+    rec, _ = random_wellformed(rng, 40, 300, 6, max_depth=5, t_spread=9)
+    cls = np.array([0, 1, 2, 0, 255, 1], np.uint8)
+    p = dict(num_regions=6, num_classes=3, region_class=cls, group_shift=3, num_groups=5)
+    log(f"[gpu] random wellformed seed={seed} force_full={force_full} n={len(rec)}")
+    assert_parity(gpu_run(rec, p, force_full=force_full), oracle_run(oracle_mod, rec, p))
+
+
+def test_nesting_deeper_than_a_tile(oracle_mod):
+    rows, t = [], 0
+    for ctx in (5, 6):
+        for k in range(5000):
+            rows.append((t, ctx, k % 9, 1))
+            t += 1
+        for k in reversed(range(5000)):
+            rows.append((t, ctx, k % 9 if k % 97 else (k + 1) % 9, 2))
+            t += 1
+    rows.append((t, 6, 3, 2))  # an orphan after the context unwinds
+    rec = records_from_rows(rows)
+    p = dict(num_regions=9, num_classes=2, region_class=np.array([0, 1] * 4 + [9], np.uint8),
+             group_shift=0, num_groups=8)
+    log("[gpu] nesting deeper than a tile")
+    assert_parity(gpu_run(rec, p), oracle_run(oracle_mod, rec, p))
+
+
+@pytest.mark.parametrize("drift", ["up", "down", "balanced"])
+def test_long_context_with_drift(oracle_mod, drift):
+    """One context over ~25 tiles whose depth drifts (duplicate BEGINs or orphan
+    ENDs), so pairs, parents and child sums cross many tiles."""
+    rng = np.random.default_rng({"up": 1, "down": 2, "balanced": 3}[drift])
+    p_begin = {"up": 0.52, "down": 0.48, "balanced": 0.5}[drift]
+    n = 50000
+    kinds = np.where(rng.random(n) < p_begin, 1, 2)
+    ts = np.cumsum(rng.integers(0, 4, size=n))  # zero gaps give ties
+    regs = rng.integers(0, 5, size=n)
+    ctx = np.full(n, 11)
+    ctx[rng.random(n) < 0.01] = 12
+    rows = list(zip(ts.tolist(), ctx.tolist(), regs.tolist(), kinds.tolist()))
+    rec = records_from_rows(rows)
+    p = dict(num_regions=5, num_classes=2, region_class=np.array([0, 1, 0, 1, 0], np.uint8),
+             group_shift=1, num_groups=7)
+    log(f"[gpu] long context drift={drift}")
+    assert_parity(gpu_run(rec, p), oracle_run(oracle_mod, rec, p))
+
+
+def test_wide_keys(oracle_mod):
+    """Context keys spread over 32 bits and a 40-bit time span: the packed
+    (ctx, ts) key needs more than 64 bits."""
+    rng = np.random.default_rng(5)
+    rows = []
+    for c in rng.integers(0, 1 << 32, size=64, dtype=np.uint64).tolist():
+        t = int(rng.integers(0, 1 << 40))
+        depth, stack = 0, []
+        for k in range(120):
+            if depth == 0 or (depth < 4 and rng.random() < 0.5):
+                r = int(rng.integers(0, 6))
+                stack.append(r)
+                rows.append((t, c, r, 1))
+                depth += 1
+            else:
+                rows.append((t, c, stack.pop(), 2))
+                depth -= 1
+            t += int(rng.integers(1, 1 << 20))
+    rng.shuffle(rows)
+    rec = records_from_rows(rows)
+    p = dict(num_regions=6, num_classes=2, region_class=np.array([0, 1, 0, 1, 0, 1], np.uint8),
+             group_shift=24, num_groups=256)
+    log("[gpu] wide keys")
+    assert_parity(gpu_run(rec, p), oracle_run(oracle_mod, rec, p))
+
+
+@pytest.mark.parametrize("force_full", [False, True])
+@pytest.mark.parametrize("cfg,kw", [(1, {}), (2, dict(blocks=4)), (3, dict(blocks=2)),
+                                    (4, dict(blocks=4)), (5, dict(blocks=16, size=1 << 20))])
+def test_workload_shapes_scaled(oracle_mod, tracegen_mod, cfg, kw, force_full):
+    d = tracegen_mod.generate(cfg, **kw)
+    p = {k: d[k] for k in ("num_regions", "num_classes", "region_class", "group_shift", "num_groups")}
+    log(f"[gpu] config {cfg} {kw} force_full={force_full} n={len(d['records'])}")
+    assert_parity(gpu_run(d["records"], p, force_full=force_full),
+                  oracle_run(oracle_mod, d["records"], p), what=f"cfg{cfg}")
+
+
+def test_determinism_and_stream(oracle_mod, tracegen_mod, gpu):
+    d = tracegen_mod.generate(5, blocks=8, size=1 << 18)
+    p = {k: d[k] for k in ("num_regions", "num_classes", "region_class", "group_shift", "num_groups")}
+    log("[gpu] determinism, non-default stream")
+    s = gpu.cuda.Stream()
+    a, b = gpu_run(d["records"], p, stream=s, repeat=2)
+    for k in a:
+        np.testing.assert_array_equal(a[k], b[k])
+    assert_parity(a, oracle_run(oracle_mod, d["records"], p))
+
+
+def test_without_instance_outputs(oracle_mod, tracegen_mod):
+    d = tracegen_mod.generate(3, blocks=1)
+    p = {k: d[k] for k in ("num_regions", "num_classes", "region_class", "group_shift", "num_groups")}
+    log("[gpu] statistics only (instances in the workspace)")
+    g = gpu_run(d["records"], p, instances=False)
+    assert_parity(g, oracle_run(oracle_mod, d["records"], p, instances=False), instances=False)
