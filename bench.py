@@ -1,0 +1,253 @@
+#!/usr/bin/env python3
+"""Benchmark of region attribution over marker traces on one MI355X.
+
+Workload: the large skewed trace -- 2^28 records of 16 B (4 GiB), 2048 blocks
+x 16 warps = 32768 contexts with Zipf(1.2) record counts, 1024 regions, depth
+<= 8, 1% malformed markers, 40-bit timestamps, 4 region classes over 2048
+groups -- generated with a fixed seed, resident in HBM before timing.
+
+One step = one call of the whole path (argus_attr_run): validate, sort,
+match, exclusive times, per-region statistics, ambiguity counts and the
+class-overlap sweep, with instance and exclusive-time outputs written.
+`value` = records attributed per second over the timed steps.
+
+Also reported: per-launch timing (HIP events on the run's stream, recorded
+during the timed steps), the roofline of the dominant kernel (algorithmic
+bytes per launch / average launch time vs 8 TB/s HBM), the whole pipeline's
+algorithmic bytes per record and GB/s, and the CPU oracle timed on a bounded
+sample of the same trace (1 core).
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "marker records attributed/sec (sort+match+aggregate) + achieved HBM GB/s"
+WORKLOADS = {
+    5: "large skewed trace: 2^28 x 16 B records, 2048x16 warps (32768 contexts, Zipf 1.2), "
+       "1024 regions, depth<=8, 1% malformed, 4 classes x 2048 groups",
+    4: "compute/comm overlap trace: 2^25 records, 256x8 warps, 2 classes x 256 groups",
+    3: "decode-megakernel trace: 2^26 records less 0.1% dropped ENDs, 256x16 warps, 177 regions",
+    2: "persistent-GEMM trace: 2^24 records, 256x8 warps, 12 regions",
+    1: "tiny well-formed trace: 2^16 records, 8x4 warps",
+}
+
+
+def err(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def byte_model(name: str, c: dict, plan: dict, R: int, K: int, G: int, flags: int) -> float:
+    """Algorithmic bytes moved by one launch (element data read and written;
+    look-back status and histogram traffic excluded)."""
+    n, nv, nb, nev = c["n"], c["nv"], c["nb"], plan["n_ev"]
+    wide = plan["rec_wide"]
+    if name == "ingest":
+        return 16.0 * n
+    if name.startswith("radix_") or name.startswith("ev_radix_"):
+        ev = name.startswith("ev_")
+        slots = plan["ev_slots"] if ev else plan["rec_slots"]
+        idx = {"ctx0": 0, "ctx1": 1, "ctx2": 2, "ctx3": 3, "ts0": 4, "ts1": 5, "ts2": 6, "ts3": 7,
+               "ts4": 8, "ts5": 9, "ts6": 10, "ts7": 11, "ctx0b": 12, "ctx1b": 13, "ctx2b": 14,
+               "ctx3b": 15}
+        if ev:
+            tail = name[len("ev_radix_"):]
+            slot = int(tail[2:]) if tail.startswith("ts") else (8 + int(tail[1:]) if tail.startswith("g") else 99)
+        else:
+            slot = idx[name[len("radix_"):]]
+        if slot >= 16 or not slots[slot]["active"]:
+            return 0.0
+        out_n = nev if ev else nv
+        elem = 12.0 + (4.0 if (wide and not ev) else 0.0)
+        src = int(slots[slot]["src"])
+        if src == 2:  # first pass: raw records / instances
+            return (16.0 * n if not ev else 32.0 * nb) + elem * out_n
+        return 2.0 * elem * out_n
+    if name == "check_sorted":
+        return 8.0 * nv
+    if name == "ts_hist":
+        return 8.0 * nv if plan["unsorted"] else 0.0
+    if name == "match":
+        return (12.0 + (4.0 if wide else 0.0)) * nv + 40.0 * nb
+    if name == "agg":
+        return 40.0 * nb + (8.0 * nb if flags & 2 else 0.0) + (4.0 * nb if R > 167 else 0.0)
+    if name == "hist":
+        return 4.0 * nb * max(1, -(-R // 189)) if R > 167 else 0.0
+    if name == "ev_hist":
+        return 32.0 * nb
+    if name == "sweep":
+        return 12.0 * nev
+    if name == "init":
+        return 8.0 * (R * 142 + (-(-n // 4096)) * 256 + (-(-nv // 2048)) * 4 + (-(-n // 2048)) * 8)
+    if name == "ev_clear":
+        return 8.0 * (-(-2 * nb // 4096)) * 256
+    return 0.0
+
+
+def traffic_for(kernel: str):
+    """HBM bytes per launch measured by rocprofv3 counters, if the committed
+    measurement is for the current source of that kernel."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path)).get(kernel)
+        if not rec:
+            return None
+        src = os.path.join(ROOT, "paper_2609_12299_amd", "csrc", rec["source"])
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        if sha != rec["source_sha256"]:
+            return None
+        return float(rec["bytes_per_launch"])
+    except Exception:  # noqa: BLE001
+        return None
+
+
+def cpu_baseline(records: np.ndarray, d: dict, sample: int) -> dict:
+    import oracle
+    sub = np.ascontiguousarray(records[:sample])
+    t0 = time.perf_counter()
+    oracle.run(sub, d["num_regions"], d["num_classes"], d["region_class"], d["group_shift"],
+               d["num_groups"], instances=True)
+    t = time.perf_counter() - t0
+    return {"value": sample / t, "unit": "records/s", "cores": 1, "kind": "oracle",
+            "seconds": round(t, 3),
+            "sample": f"first {sample} records ({sample * 16 >> 20} MiB) of the same trace, "
+                      "single-threaded C++ oracle (validate, stable sort, stack replay, sums, sweep)"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=5, choices=sorted(WORKLOADS))
+    ap.add_argument("--force-full-sort", action="store_true")
+    ap.add_argument("--cpu-sample", type=int, default=1 << 25)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--kernels", action="store_true", help="print per-launch timing to stderr")
+    ap.add_argument("--copy-calibrate", action="store_true",
+                    help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        err("bench.py measures one GPU: this build has no multi-GPU path (the path would shard by "
+            "context group with one all-reduce of the aggregates; see DESIGN.md). Use --gpus 1.")
+        return 2
+
+    import torch
+
+    import tracegen
+    from paper_2609_12299_amd import RegionAttribution, load_library
+    load_library()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+
+    t0 = time.perf_counter()
+    d = tracegen.generate(args.config, threads=int(os.environ.get("OMP_NUM_THREADS", "16")))
+    rec_np = d["records"]
+    n = rec_np.shape[0]
+    err(f"generated config {args.config}: {n} records in {time.perf_counter() - t0:.1f}s")
+    rec = torch.from_numpy(rec_np.reshape(-1)).to(dev)
+    torch.cuda.synchronize()
+    ra = RegionAttribution(d["num_regions"], d["num_classes"], d["region_class"], d["group_shift"],
+                           d["num_groups"], max_records=n, instances=True, instance_excl=True,
+                           force_full_sort=args.force_full_sort, device=dev)
+    out = ra.alloc(n)
+    for _ in range(max(args.warmup, 1)):
+        ra.run(rec, out)
+    torch.cuda.synchronize()
+    cnt = out["counters"].cpu().numpy()
+    assert int(cnt[31]) == 0, "internal error flag set"
+    assert int(cnt[0]) == n
+    err(f"warm: n_valid={int(cnt[1])} n_begin={int(cnt[4])} matched={int(cnt[9])} "
+        f"max_level={int(cnt[14])}")
+
+    if args.copy_calibrate:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    ra.set_timing(True)
+    ra.kernel_times()  # discard
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        ra.run(rec, out)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    times = ra.kernel_times()
+    ra.set_timing(False)
+    plan = ra.plan()
+
+    c = dict(n=n, nv=int(cnt[1]), nb=int(cnt[4]))
+    per = {}
+    for name, ms in times:
+        per.setdefault(name, []).append(ms)
+    avg = {k: float(np.mean(v)) for k, v in per.items()}
+    flags = ra.flags
+    R, K, G = d["num_regions"], d["num_classes"], d["num_groups"]
+    bytes_per = {k: byte_model(k, c, plan, R, K, G, flags) for k in avg}
+    step_ms = elapsed * 1e3 / args.steps
+    total_bytes = sum(bytes_per.values())
+    dom = max(avg, key=lambda k: avg[k])
+    achieved = bytes_per[dom] / (avg[dom] * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": traffic_for(dom), "avg_launch_ms": round(avg[dom], 4),
+                "bytes_per_launch": bytes_per[dom]}
+    if args.kernels:
+        for k in sorted(avg, key=lambda k: -avg[k]):
+            gbs = bytes_per[k] / (avg[k] * 1e-3) / 1e9 if avg[k] > 0 else 0.0
+            err(f"  {k:16s} {avg[k]:8.4f} ms  {bytes_per[k] / 2**20:10.1f} MiB  {gbs:8.1f} GB/s")
+        err(f"plan: unsorted={plan['unsorted']} n_ev={plan['n_ev']} "
+            f"rec_active={[int(s['pos']) for s in plan['rec_slots'] if s['active']]} "
+            f"ev_active={[int(s['pos']) for s in plan['ev_slots'] if s['active']]}")
+
+    result = {
+        "metric": METRIC,
+        "value": n * args.steps / elapsed,
+        "unit": "records/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(step_ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u64",
+        "data": "synthetic",
+        "config": {"workload": WORKLOADS[args.config], "records": n, "record_bytes": 16,
+                   "contexts": int(d["blocks"]) * int(d["warps"]), "regions": R, "classes": K,
+                   "groups": G, "force_full_sort": bool(args.force_full_sort)},
+        "pipeline": {"bytes_per_record": round(total_bytes / n, 2),
+                     "achieved_gbs": round(total_bytes / (step_ms * 1e-3) / 1e9, 1),
+                     "frac_of_peak": round(total_bytes / (step_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "full_sort": bool(plan["unsorted"])},
+        "roofline": roofline,
+        "kernels_ms": {k: round(v, 4) for k, v in sorted(avg.items(), key=lambda kv: -kv[1])
+                       if v >= 0.01},
+    }
+    if not args.no_cpu_baseline:
+        sample = min(args.cpu_sample, n)
+        err(f"cpu baseline: oracle on {sample} records ...")
+        result["cpu_baseline"] = cpu_baseline(rec_np, d, sample)
+    print(json.dumps(result), flush=True)
+    ra.close()
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -198,11 +198,13 @@ void argus_attr_destroy(argus_attr* h);
 const char* argus_attr_last_error(const argus_attr* h);
 
 /* ---------------------------------------------------------------- timing */
-/* Per-kernel timing for measurement.  When enabled, `run` records a HIP
- * event after each kernel launch on its stream.  argus_attr_kernel_times
- * then fills up to `cap` entries of names[] (static strings) and ms[] with
- * the elapsed time of each launch of the last run (it synchronises on the
- * last event); returns the number of launches, or a negative code. */
+/* Per-kernel timing for measurement.  While enabled, every `run` records a
+ * HIP event before its first launch and after each kernel launch, on its
+ * stream (no host synchronisation).  argus_attr_kernel_times synchronises on
+ * those events, fills up to `cap` entries of names[] (static strings) and
+ * ms[] with the elapsed time of each launch of every run since the previous
+ * call, in launch order, forgets them, and returns how many launches there
+ * were (which may exceed cap), or a negative code. */
 int argus_attr_set_timing(argus_attr* h, int enable);
 int argus_attr_kernel_times(argus_attr* h, const char** names, float* ms, int cap);
 

@@ -118,8 +118,8 @@ def argus_attr_set_timing(h, enable: bool) -> int:
     return load_library().argus_attr_set_timing(h, 1 if enable else 0)
 
 
-def argus_attr_kernel_times(h, cap: int = 128):
-    """[(name, ms)] for every launch of the last timed run."""
+def argus_attr_kernel_times(h, cap: int = 1 << 16):
+    """[(name, ms)] for every launch of every timed run since the last call."""
     names = (ctypes.c_char_p * cap)()
     ms = (ctypes.c_float * cap)()
     n = load_library().argus_attr_kernel_times(h, names, ms, cap)
@@ -227,6 +227,26 @@ class RegionAttribution:
         if rc != 0:
             raise ArgusError(rc, argus_attr_last_error(self.h))
         return out
+
+    def plan(self) -> dict:
+        """The device-side plan of the last run (read back for measurement:
+        which sort passes ran, whether the full sort was needed, the number
+        of overlap events).  Synchronises the device."""
+        if self._ws is None:
+            raise RuntimeError("no run yet")
+        t = self.torch
+        t.cuda.synchronize(self.device)
+        off = ((self._ws.data_ptr() + 255) & ~255) - self._ws.data_ptr()
+        raw = self._ws[off:off + 1432].cpu().numpy()
+        slot = np.dtype([("active", "<u4"), ("pos", "<u4"), ("src", "<u4"), ("dst", "<u4"),
+                         ("lb", "<u4"), ("n_out", "<u4"), ("n_elems", "<u8"), ("tiles", "<u8")])
+        u64 = raw.view(np.uint64)
+        u32 = raw.view(np.uint32)
+        return dict(n_records=int(u64[0]), n_valid=int(u64[1]), n_begin=int(u64[2]),
+                    rec_ts_bits=int(u32[48 // 4]), rec_ctx_bits=int(u32[52 // 4]),
+                    rec_wide=int(u32[56 // 4]), unsorted=int(u32[104 // 4]),
+                    n_ev=int(u64[128 // 8]),
+                    rec_slots=raw[144:784].view(slot).copy(), ev_slots=raw[784:1424].view(slot).copy())
 
     def set_timing(self, on: bool):
         rc = argus_attr_set_timing(self.h, on)

@@ -16,10 +16,28 @@ struct argus_attr {
   std::string err;
   int device_checked = -1;  // device ordinal verified to be gfx950
   bool timing = false;
-  std::vector<hipEvent_t> events;
-  std::vector<const char*> names;
-  int n_launches = 0;
+  // Timing: for every timed run, a start event and one event per launch.
+  struct TimedRun {
+    std::vector<hipEvent_t> ev;
+    std::vector<const char*> names;
+  };
+  std::vector<TimedRun> runs;
+  std::vector<hipEvent_t> pool;  // recycled events
 };
+
+namespace argus {
+
+uint64_t persistent_blocks(const void* kernel, int threads) {
+  int dev = 0, cus = 256, per_cu = 1;
+  if (hipGetDevice(&dev) == hipSuccess)
+    (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess ||
+      per_cu < 1)
+    per_cu = 1;
+  return (uint64_t)cus * (uint64_t)per_cu;
+}
+
+}  // namespace argus
 
 namespace {
 
@@ -132,7 +150,9 @@ size_t argus_attr_workspace_bytes(const argus_attr* h, uint64_t n_records) {
 
 void argus_attr_destroy(argus_attr* h) {
   if (!h) return;
-  for (hipEvent_t e : h->events) (void)hipEventDestroy(e);
+  for (auto& r : h->runs)
+    for (hipEvent_t e : r.ev) (void)hipEventDestroy(e);
+  for (hipEvent_t e : h->pool) (void)hipEventDestroy(e);
   delete h;
 }
 
@@ -146,18 +166,25 @@ int argus_attr_set_timing(argus_attr* h, int enable) {
 
 int argus_attr_kernel_times(argus_attr* h, const char** names, float* ms, int cap) {
   if (!h) return ARGUS_E_INVAL;
-  if (!h->timing || h->n_launches == 0) return 0;
-  if (hipEventSynchronize(h->events[h->n_launches]) != hipSuccess)
-    return fail(h, ARGUS_E_HIP, "%s", "hipEventSynchronize failed");
-  int k = 0;
-  for (; k < h->n_launches && k < cap; ++k) {
-    float t = 0;
-    if (hipEventElapsedTime(&t, h->events[k], h->events[k + 1]) != hipSuccess)
-      return fail(h, ARGUS_E_HIP, "%s", "hipEventElapsedTime failed");
-    if (names) names[k] = h->names[k];
-    if (ms) ms[k] = t;
+  int total = 0, k = 0;
+  for (auto& r : h->runs) {
+    if (r.ev.size() < 2) continue;
+    if (hipEventSynchronize(r.ev.back()) != hipSuccess)
+      return fail(h, ARGUS_E_HIP, "%s", "hipEventSynchronize failed");
+    for (size_t j = 0; j + 1 < r.ev.size(); ++j, ++total) {
+      if (k >= cap) continue;
+      float t = 0;
+      if (hipEventElapsedTime(&t, r.ev[j], r.ev[j + 1]) != hipSuccess)
+        return fail(h, ARGUS_E_HIP, "%s", "hipEventElapsedTime failed");
+      if (names) names[k] = r.names[j];
+      if (ms) ms[k] = t;
+      ++k;
+    }
   }
-  return h->n_launches;
+  for (auto& r : h->runs)
+    for (hipEvent_t e : r.ev) h->pool.push_back(e);
+  h->runs.clear();
+  return total;
 }
 
 int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
@@ -241,17 +268,23 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
   w.match_tiles = L.match_tiles;
   w.pool_cap = L.pool_cap;
 
-  // Timing events.
-  h->n_launches = 0;
-  h->names.clear();
-  if (h->timing) {
-    while (h->events.size() < 96) {
-      hipEvent_t e;
-      if (hipEventCreate(&e) != hipSuccess) return fail(h, ARGUS_E_HIP, "%s", "hipEventCreate failed");
-      h->events.push_back(e);
+  // Timing events (one per launch, recorded on the run's stream).
+  argus_attr::TimedRun* tr = nullptr;
+  auto new_event = [&](hipEvent_t* e) -> bool {
+    if (!h->pool.empty()) {
+      *e = h->pool.back();
+      h->pool.pop_back();
+      return true;
     }
-    if (hipEventRecord(h->events[0], s) != hipSuccess)
-      return fail(h, ARGUS_E_HIP, "%s", "hipEventRecord failed");
+    return hipEventCreate(e) == hipSuccess;
+  };
+  if (h->timing) {
+    h->runs.emplace_back();
+    tr = &h->runs.back();
+    hipEvent_t e;
+    if (!new_event(&e) || hipEventRecord(e, s) != hipSuccess)
+      return fail(h, ARGUS_E_HIP, "%s", "timing event failed");
+    tr->ev.push_back(e);
   }
   auto step = [&](const char* name, hipError_t e) -> bool {
     if (e == hipSuccess) e = hipGetLastError();
@@ -260,10 +293,11 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
       h->err += std::string(" (") + hipGetErrorString(e) + ")";
       return false;
     }
-    if (h->timing && h->n_launches + 1 < (int)h->events.size()) {
-      h->names.push_back(name);
-      h->n_launches++;
-      if (hipEventRecord(h->events[h->n_launches], s) != hipSuccess) return false;
+    if (tr) {
+      hipEvent_t ev;
+      if (!new_event(&ev) || hipEventRecord(ev, s) != hipSuccess) return false;
+      tr->ev.push_back(ev);
+      tr->names.push_back(name);
     }
     return true;
   };
@@ -293,7 +327,6 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
         "ev_radix_ts0", "ev_radix_ts1", "ev_radix_ts2", "ev_radix_ts3", "ev_radix_ts4",
         "ev_radix_ts5", "ev_radix_ts6", "ev_radix_ts7", "ev_radix_g0", "ev_radix_g1",
         "ev_radix_g2", "ev_radix_g3", "ev_unused12", "ev_unused13", "ev_unused14", "ev_unused15"};
-    if (!step("ev_hist", launch_ev_hist(a, s))) return ARGUS_E_HIP;
     if (!step("ev_plan", launch_ev_plan(a, s))) return ARGUS_E_HIP;
     if (!step("ev_clear", launch_ev_clear(a, s))) return ARGUS_E_HIP;
     for (int sl = 0; sl < 12; ++sl)

@@ -6,6 +6,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <stddef.h>
 #include <stdint.h>
 
 #include "../../include/argus_attr.h"
@@ -87,6 +88,15 @@ struct DevPlan {
   // matching
   uint64_t match_tiles;
 };
+
+// The Python binding reads the plan back for measurement; keep its layout.
+static_assert(sizeof(KeySpace) == 40, "KeySpace layout");
+static_assert(sizeof(SlotPlan) == 40, "SlotPlan layout");
+static_assert(offsetof(DevPlan, unsorted) == 104, "DevPlan layout");
+static_assert(offsetof(DevPlan, n_ev) == 128, "DevPlan layout");
+static_assert(offsetof(DevPlan, rs) == 144, "DevPlan layout");
+static_assert(offsetof(DevPlan, es) == 784, "DevPlan layout");
+static_assert(sizeof(DevPlan) == 1432, "DevPlan layout");
 
 // Per-tile summary written by the matching kernel, read by the resolver.
 struct TileDesc {
@@ -206,11 +216,14 @@ hipError_t launch_tree(const RunArgs& a, hipStream_t s);
 hipError_t launch_resolve(const RunArgs& a, hipStream_t s);
 hipError_t launch_agg(const RunArgs& a, hipStream_t s);
 hipError_t launch_hist(const RunArgs& a, hipStream_t s);
-hipError_t launch_ev_hist(const RunArgs& a, hipStream_t s);
 hipError_t launch_ev_plan(const RunArgs& a, hipStream_t s);
 hipError_t launch_ev_clear(const RunArgs& a, hipStream_t s);
 hipError_t launch_sweep(const RunArgs& a, hipStream_t s);
 hipError_t launch_ov_final(const RunArgs& a, hipStream_t s);
+
+// Number of blocks of `kernel` that fit on the device at once (all CUs at
+// the kernel's occupancy): the grid of a persistent kernel.
+uint64_t persistent_blocks(const void* kernel, int threads);
 
 // Launch geometry helpers shared by host code.
 __host__ __device__ inline uint64_t ceil_div(uint64_t a, uint64_t b) { return (a + b - 1) / b; }

@@ -39,6 +39,11 @@ struct AggArgs {
   uint32_t R;
   uint32_t lds_regions;  // R if statistics fit in LDS, else 0
   uint32_t hist_lds;     // histograms in LDS too
+  // overlap events (K > 0): digit histograms of the events' sort keys
+  const uint8_t* region_class;
+  uint32_t K, G, shift;
+  uint32_t* ev_hist;  // [12][256]
+  DevPlan* wplan;
 };
 
 template <typename T>
@@ -48,7 +53,24 @@ __device__ __forceinline__ T wsum(T v) {
   return v;
 }
 
-__global__ __launch_bounds__(256) void k_agg(AggArgs a) {
+// Adds this wave's digits (lanes in `valid`) to an LDS histogram: one atomic
+// when every valid lane holds the same digit (high digits of nearby
+// timestamps, groups of one context), else one per lane (low digits, which
+// rarely collide).
+__device__ __forceinline__ void whist(uint32_t* hist, uint32_t d, bool valid) {
+  const uint64_t vm = __ballot(valid);
+  if (vm == 0) return;
+  const int first = __ffsll((long long)vm) - 1;
+  const uint32_t d0 = __shfl(d, first);
+  const uint64_t same = __ballot(valid && d == d0);
+  if (same == vm) {
+    if ((int)lane_id() == first) atomicAdd(&hist[d0], (uint32_t)__popcll(vm));
+    return;
+  }
+  if (valid) atomicAdd(&hist[d], 1u);
+}
+
+__global__ __launch_bounds__(512) void k_agg(AggArgs a) {
   extern __shared__ __align__(16) uint8_t smem[];
   const uint32_t RL = a.lds_regions;
   uint64_t* s_isum = (uint64_t*)smem;
@@ -63,8 +85,10 @@ __global__ __launch_bounds__(256) void k_agg(AggArgs a) {
   uint32_t* s_mae = s_mab + RL;
   uint32_t* s_sn = s_mae + RL;
   uint32_t* s_hist = s_sn + RL;  // [RL][130] when hist_lds
-  __shared__ uint64_t s_red[4][4];
-  for (uint32_t r = threadIdx.x; r < RL; r += 256) {
+  uint32_t* s_evh = s_hist + (a.hist_lds ? RL * 130 : 0);  // [12][256] when K > 0
+  __shared__ uint64_t s_red[8][6];
+  constexpr uint32_t NT = 512;
+  for (uint32_t r = threadIdx.x; r < RL; r += NT) {
     s_isum[r] = 0;
     s_esum[r] = 0;
     s_imin[r] = kU64Max;
@@ -78,14 +102,33 @@ __global__ __launch_bounds__(256) void k_agg(AggArgs a) {
     s_sn[r] = 0;
   }
   if (a.hist_lds)
-    for (uint32_t i = threadIdx.x; i < RL * 130; i += 256) s_hist[i] = 0;
+    for (uint32_t i = threadIdx.x; i < RL * 130; i += NT) s_hist[i] = 0;
+  if (a.K)
+    for (uint32_t i = threadIdx.x; i < kDigitPositions * kRadixBins; i += NT) s_evh[i] = 0;
   __syncthreads();
 
   const uint64_t nb = a.plan->n_begin;
-  uint64_t n_m = 0, n_mm = 0, n_u = 0, n_sn = 0;
+  // Overlap-event digits that can vary: group digits below the width of
+  // G - 1, timestamp digits above which ts_min and ts_max differ.
+  uint32_t vary = 0;
+  if (a.K) {
+    const uint64_t ts_lo = a.plan->rec.ts_min;
+    const uint64_t ts_hi = ts_lo + a.plan->rec.ts_mask;
+    const bool full_ts = a.plan->rec.ts_bits >= 64 || ts_hi < ts_lo;
+    for (int d = 0; d < 4; ++d)
+      if (d == 0 || ((uint64_t)(a.G - 1) >> (8 * d)) != 0) vary |= 1u << d;
+    for (int d = 0; d < 8; ++d)
+      if (full_ts || (ts_lo >> (8 * d)) != (ts_hi >> (8 * d))) vary |= 1u << (4 + d);
+  }
+  uint64_t n_m = 0, n_mm = 0, n_u = 0, n_sn = 0, n_ev = 0, n_skip = 0;
   unsigned long long* rs = (unsigned long long*)a.rstats;
-  const uint64_t stride = (uint64_t)gridDim.x * 256;
-  for (uint64_t id = (uint64_t)blockIdx.x * 256 + threadIdx.x; id < nb; id += stride) {
+  const uint64_t stride = (uint64_t)gridDim.x * NT;
+  // Wave-uniform trip count (the event histograms use ballots).
+  for (uint64_t wb = (uint64_t)blockIdx.x * NT + (threadIdx.x & ~63u); wb < nb; wb += stride) {
+    const uint64_t id = wb + (threadIdx.x & 63);
+    bool ev = false;
+    uint64_t eg = 0, et0 = 0, et1 = 0;
+    if (id < nb) {
     argus_instance x = a.inst[id];
     uint32_t par = agg_parent(x, a.tiles, a.op_parent);
     if (par != kNoParent && par >= nb) {
@@ -102,6 +145,20 @@ __global__ __launch_bounds__(256) void k_agg(AggArgs a) {
     uint32_t hk = 0xFFFFFFFFu;
     if (matched) {
       n_m++;
+      if (a.K) {
+        const uint32_t cls = a.region_class[region];
+        if (cls < a.K) {
+          eg = a.shift >= 32 ? 0 : (x.ctx_key >> a.shift);
+          if (eg < a.G) {
+            ev = true;
+            et0 = x.t_begin;
+            et1 = x.t_end;
+            n_ev += 2;
+          } else {
+            n_skip++;
+          }
+        }
+      }
       const bool sn = par != kNoParent && a.inst[par].region_id == region;
       n_sn += sn;
       const uint32_t bi = bit_width64(incl), be = bit_width64(excl);
@@ -145,29 +202,54 @@ __global__ __launch_bounds__(256) void k_agg(AggArgs a) {
       else atomicAdd(&rs[(uint64_t)region * ARGUS_RS_WIDTH + ARGUS_RS_UNCLOSED], 1ull);
     }
     if (a.hist_key) a.hist_key[id] = hk;
+    }
+    if (a.K) {
+#pragma unroll
+      for (int d = 0; d < 4; ++d)
+        if ((vary >> d) & 1u) {
+          const uint32_t dg = (uint32_t)(eg >> (8 * d)) & 0xFFu;
+          whist(s_evh + d * kRadixBins, dg, ev);
+          whist(s_evh + d * kRadixBins, dg, ev);
+        }
+#pragma unroll
+      for (int d = 0; d < 8; ++d)
+        if ((vary >> (4 + d)) & 1u) {
+          whist(s_evh + (4 + d) * kRadixBins, (uint32_t)(et0 >> (8 * d)) & 0xFFu, ev);
+          whist(s_evh + (4 + d) * kRadixBins, (uint32_t)(et1 >> (8 * d)) & 0xFFu, ev);
+        }
+    }
   }
   n_m = wsum(n_m);
   n_mm = wsum(n_mm);
   n_u = wsum(n_u);
   n_sn = wsum(n_sn);
+  n_ev = wsum(n_ev);
+  n_skip = wsum(n_skip);
   const int w = threadIdx.x >> 6;
   if ((threadIdx.x & 63) == 0) {
     s_red[w][0] = n_m;
     s_red[w][1] = n_mm;
     s_red[w][2] = n_u;
     s_red[w][3] = n_sn;
+    s_red[w][4] = n_skip;
+    s_red[w][5] = n_ev;
   }
   __syncthreads();
-  if (threadIdx.x < 4) {
-    const uint64_t v = s_red[0][threadIdx.x] + s_red[1][threadIdx.x] + s_red[2][threadIdx.x] +
-                       s_red[3][threadIdx.x];
+  if (threadIdx.x < 6) {
+    uint64_t v = 0;
+    for (int q = 0; q < (int)(NT / 64); ++q) v += s_red[q][threadIdx.x];
     const int idx = threadIdx.x == 0   ? ARGUS_C_N_MATCHED
                     : threadIdx.x == 1 ? ARGUS_C_N_MISMATCHED
                     : threadIdx.x == 2 ? ARGUS_C_N_UNCLOSED
-                                       : ARGUS_C_N_SELF_NESTED;
-    if (v) atomicAdd((unsigned long long*)&a.counters[idx], (unsigned long long)v);
+                    : threadIdx.x == 3 ? ARGUS_C_N_SELF_NESTED
+                                       : ARGUS_C_N_OVERLAP_SKIPPED;
+    if (v && threadIdx.x < 5) atomicAdd((unsigned long long*)&a.counters[idx], (unsigned long long)v);
+    if (v && threadIdx.x == 5) atomicAdd((unsigned long long*)&a.wplan->n_ev, (unsigned long long)v);
   }
-  for (uint32_t r = threadIdx.x; r < RL; r += 256) {
+  if (a.K)
+    for (uint32_t i = threadIdx.x; i < kDigitPositions * kRadixBins; i += NT)
+      if (s_evh[i]) atomicAdd(&a.ev_hist[i], s_evh[i]);
+  for (uint32_t r = threadIdx.x; r < RL; r += NT) {
     unsigned long long* row = rs + (uint64_t)r * ARGUS_RS_WIDTH;
     if (s_cnt[r]) {
       atomicAdd(&row[ARGUS_RS_COUNT], (unsigned long long)s_cnt[r]);
@@ -184,7 +266,7 @@ __global__ __launch_bounds__(256) void k_agg(AggArgs a) {
     if (s_sn[r]) atomicAdd(&row[ARGUS_RS_SELF_NESTED], (unsigned long long)s_sn[r]);
   }
   if (a.hist_lds) {
-    for (uint32_t i = threadIdx.x; i < RL * 130; i += 256) {
+    for (uint32_t i = threadIdx.x; i < RL * 130; i += NT) {
       const uint32_t h = s_hist[i];
       if (h) {
         const uint32_t r = i / 130, b = i % 130;
@@ -214,6 +296,7 @@ hipError_t launch_agg(const RunArgs& a, hipStream_t s) {
   uint32_t rl, hl;
   size_t bytes;
   agg_sizes(a.R, &rl, &hl, &bytes);
+  if (a.K) bytes += sizeof(uint32_t) * kDigitPositions * kRadixBins;
   AggArgs g{};
   g.plan = a.w.plan;
   g.inst = a.w.inst;
@@ -227,11 +310,17 @@ hipError_t launch_agg(const RunArgs& a, hipStream_t s) {
   g.R = a.R;
   g.lds_regions = rl;
   g.hist_lds = hl;
-  uint64_t blocks = ceil_div(a.n ? a.n : 1, 256 * 16);
+  g.region_class = a.region_class;
+  g.K = a.K;
+  g.G = a.G;
+  g.shift = a.shift;
+  g.ev_hist = a.w.ev_hist;
+  g.wplan = a.w.plan;
+  uint64_t blocks = ceil_div(a.n ? a.n : 1, 512 * 16);
   if (blocks > 512) blocks = 512;
   if (bytes > 64 * 1024)
     (void)hipFuncSetAttribute((const void*)k_agg, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-  hipLaunchKernelGGL(k_agg, dim3((uint32_t)blocks), dim3(256), bytes, s, g);
+  hipLaunchKernelGGL(k_agg, dim3((uint32_t)blocks), dim3(512), bytes, s, g);
   return hipGetLastError();
 }
 
@@ -247,27 +336,37 @@ struct HistArgs {
 
 // Log2 histograms when they do not fit next to the statistics: each
 // blockIdx.y covers one slice of regions in LDS.
-__global__ __launch_bounds__(256) void k_hist(HistArgs a) {
+__global__ __launch_bounds__(1024) void k_hist(HistArgs a) {
   extern __shared__ __align__(16) uint8_t smem[];
+  constexpr uint32_t NT = 1024;
   uint32_t* s_h = (uint32_t*)smem;
   const uint32_t r0 = blockIdx.y * a.slice;
   const uint32_t r1 = r0 + a.slice < a.R ? r0 + a.slice : a.R;
   const uint32_t nr = r1 - r0;
-  for (uint32_t i = threadIdx.x; i < nr * 130; i += 256) s_h[i] = 0;
+  for (uint32_t i = threadIdx.x; i < nr * 130; i += NT) s_h[i] = 0;
   __syncthreads();
   const uint64_t nb = a.plan->n_begin;
-  const uint64_t stride = (uint64_t)gridDim.x * 256;
-  for (uint64_t id = (uint64_t)blockIdx.x * 256 + threadIdx.x; id < nb; id += stride) {
-    const uint32_t k = a.hist_key[id];
-    if (k == 0xFFFFFFFFu) continue;
+  auto add = [&](uint32_t k) {
     const uint32_t r = k >> 16;
-    if (r < r0 || r >= r1) continue;
+    if (k == 0xFFFFFFFFu || r < r0 || r >= r1) return;
     atomicAdd(&s_h[(r - r0) * 130 + ((k >> 8) & 0xFFu)], 1u);
     atomicAdd(&s_h[(r - r0) * 130 + 65 + (k & 0xFFu)], 1u);
+  };
+  // four keys per load (the key array is 256-byte aligned)
+  const uint64_t n4 = nb / 4;
+  const uint4* k4 = (const uint4*)a.hist_key;
+  const uint64_t stride = (uint64_t)gridDim.x * NT;
+  for (uint64_t q = (uint64_t)blockIdx.x * NT + threadIdx.x; q < n4; q += stride) {
+    const uint4 v = k4[q];
+    add(v.x);
+    add(v.y);
+    add(v.z);
+    add(v.w);
   }
+  if (blockIdx.x == 0 && threadIdx.x < nb - n4 * 4) add(a.hist_key[n4 * 4 + threadIdx.x]);
   __syncthreads();
   unsigned long long* rs = (unsigned long long*)a.rstats;
-  for (uint32_t i = threadIdx.x; i < nr * 130; i += 256) {
+  for (uint32_t i = threadIdx.x; i < nr * 130; i += NT) {
     const uint32_t h = s_h[i];
     if (h) {
       const uint32_t r = r0 + i / 130, b = i % 130;
@@ -284,127 +383,16 @@ hipError_t launch_hist(const RunArgs& a, hipStream_t s) {
   const uint32_t slice = kAggLdsBytes / kHistBytes;
   const uint32_t slices = (uint32_t)ceil_div(a.R, slice);
   HistArgs h{a.w.plan, a.w.hist_key, a.out.d_region_stats, a.R, slice};
-  uint64_t blocks = ceil_div(a.n ? a.n : 1, 256 * 32);
+  uint64_t blocks = ceil_div(a.n ? a.n : 1, 1024 * 64);
   if (blocks > 256) blocks = 256;
+  if (blocks < 1) blocks = 1;
   const size_t hb = (size_t)slice * kHistBytes;
   (void)hipFuncSetAttribute((const void*)k_hist, hipFuncAttributeMaxDynamicSharedMemorySize, (int)hb);
-  hipLaunchKernelGGL(k_hist, dim3((uint32_t)blocks, slices), dim3(256), hb, s, h);
+  hipLaunchKernelGGL(k_hist, dim3((uint32_t)blocks, slices), dim3(1024), hb, s, h);
   return hipGetLastError();
 }
 
 // ------------------------------------------------------- overlap events
-
-__device__ __forceinline__ uint64_t peers8b(uint32_t d, uint64_t valid) {
-  uint64_t m = valid;
-#pragma unroll
-  for (int b = 0; b < 8; ++b) {
-    const uint32_t bit = (d >> b) & 1u;
-    const uint64_t v = __ballot(bit);
-    m &= bit ? v : ~v;
-  }
-  return m;
-}
-__device__ __forceinline__ void whist(uint32_t* hist, uint32_t d, bool valid) {
-  const uint64_t vm = __ballot(valid);
-  if (vm == 0) return;
-  const uint64_t peers = peers8b(d, vm);
-  if (valid && (peers >> lane_id()) == 1ull) atomicAdd(&hist[d], (uint32_t)__popcll(peers));
-}
-
-struct EvHistArgs {
-  DevPlan* plan;
-  const argus_instance* inst;
-  const uint8_t* region_class;
-  uint32_t K, G, shift;
-  uint32_t* hist;  // ev_hist [12][256]
-  uint64_t* counters;
-};
-
-// Counts the overlap events (begin and end of each matched, classified
-// instance of a group below G) and builds the histograms of their sort
-// digits: group digits (positions 0..3) and timestamp digits (4..11), only
-// for positions that can vary.
-__global__ __launch_bounds__(256) void k_ev_hist(EvHistArgs a) {
-  __shared__ uint32_t s_hist[kDigitPositions][kRadixBins];
-  __shared__ uint64_t s_red[4][2];
-  for (int i = threadIdx.x; i < kDigitPositions * kRadixBins; i += 256) (&s_hist[0][0])[i] = 0;
-  __syncthreads();
-  const DevPlan* p = a.plan;
-  const uint64_t nb = p->n_begin;
-  const uint64_t ts_lo = p->rec.ts_min;
-  // a digit can vary only if the range of values spans a change above it
-  const bool full_ts = p->rec.ts_bits >= 64;
-  const uint64_t ts_hi = ts_lo + p->rec.ts_mask;  // upper bound of every timestamp
-  uint32_t vary = 0;
-  for (int d = 0; d < 4; ++d)
-    if (d == 0 || ((uint64_t)(a.G - 1) >> (8 * d)) != 0) vary |= 1u << d;
-  for (int d = 0; d < 8; ++d)
-    if (full_ts || ts_hi < ts_lo || (ts_lo >> (8 * d)) != (ts_hi >> (8 * d))) vary |= 1u << (4 + d);
-  uint64_t n_ev = 0, n_skip = 0;
-  const uint64_t stride = (uint64_t)gridDim.x * 256;
-  const uint64_t first = (uint64_t)blockIdx.x * 256 + (threadIdx.x & ~63u);
-  for (uint64_t b = first; b < nb; b += stride) {
-    const uint64_t id = b + (threadIdx.x & 63);
-    bool valid = false;
-    uint64_t g = 0, t0 = 0, t1 = 0;
-    if (id < nb) {
-      const argus_instance x = a.inst[id];
-      if (x.end_region_id == x.region_id) {
-        const uint32_t cls = a.region_class[x.region_id];
-        if (cls < a.K) {
-          g = a.shift >= 32 ? 0 : (x.ctx_key >> a.shift);
-          if (g < a.G) {
-            valid = true;
-            t0 = x.t_begin;
-            t1 = x.t_end;
-            n_ev += 2;
-          } else {
-            n_skip++;
-          }
-        }
-      }
-    }
-#pragma unroll
-    for (int d = 0; d < 4; ++d)
-      if ((vary >> d) & 1u) {
-        const uint32_t dg = (uint32_t)(g >> (8 * d)) & 0xFFu;
-        whist(s_hist[d], dg, valid);
-        whist(s_hist[d], dg, valid);
-      }
-#pragma unroll
-    for (int d = 0; d < 8; ++d)
-      if ((vary >> (4 + d)) & 1u) {
-        whist(s_hist[4 + d], (uint32_t)(t0 >> (8 * d)) & 0xFFu, valid);
-        whist(s_hist[4 + d], (uint32_t)(t1 >> (8 * d)) & 0xFFu, valid);
-      }
-  }
-  n_ev = wsum(n_ev);
-  n_skip = wsum(n_skip);
-  if ((threadIdx.x & 63) == 0) {
-    s_red[threadIdx.x >> 6][0] = n_ev;
-    s_red[threadIdx.x >> 6][1] = n_skip;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const uint64_t e = s_red[0][0] + s_red[1][0] + s_red[2][0] + s_red[3][0];
-    const uint64_t k = s_red[0][1] + s_red[1][1] + s_red[2][1] + s_red[3][1];
-    if (e) atomicAdd((unsigned long long*)&a.plan->n_ev, (unsigned long long)e);
-    if (k) atomicAdd((unsigned long long*)&a.counters[ARGUS_C_N_OVERLAP_SKIPPED], (unsigned long long)k);
-  }
-  for (int i = threadIdx.x; i < kDigitPositions * kRadixBins; i += 256) {
-    const uint32_t h = (&s_hist[0][0])[i];
-    if (h) atomicAdd(&a.hist[i], h);
-  }
-}
-
-hipError_t launch_ev_hist(const RunArgs& a, hipStream_t s) {
-  EvHistArgs e{a.w.plan, a.w.inst, a.region_class, a.K, a.G, a.shift, a.w.ev_hist,
-               a.out.d_counters};
-  uint64_t blocks = ceil_div(a.n ? a.n : 1, 256 * 16);
-  if (blocks > 1024) blocks = 1024;
-  hipLaunchKernelGGL(k_ev_hist, dim3((uint32_t)blocks), dim3(256), 0, s, e);
-  return hipGetLastError();
-}
 
 struct EvPlanArgs {
   DevPlan* plan;

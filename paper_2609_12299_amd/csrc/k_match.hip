@@ -106,53 +106,36 @@ constexpr uint32_t kParOut = 0xFFFFFFFEu;
 __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   const DevPlan* P = a.plan;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  constexpr int IT = kMatchItems;
 
   __shared__ uint32_t s_tile;
-  __shared__ uint64_t s_key[kMatchTile];
-  __shared__ uint32_t s_pay[kMatchTile];
-  __shared__ uint64_t s_cs[kMatchTile];     // wide contexts while loading, then child sums
-  __shared__ uint32_t s_tree[2 * kMatchTile];  // min tree, then out-of-tile child sums
-  __shared__ uint16_t s_lbr[kMatchTile];    // local BEGIN rank of each position
-  __shared__ uint16_t s_partner[kMatchTile];  // closing END of each local BEGIN
+  __shared__ uint32_t s_tree[2 * kMatchTile];  // min tree over x + 1, then out-of-tile child sums
+  __shared__ uint64_t s_tend[kMatchTile];      // t_end of each local BEGIN closed in the tile
+  __shared__ uint64_t s_cs[kMatchTile];        // child sums of each local BEGIN
+  __shared__ uint16_t s_lbr[kMatchTile];       // local BEGIN rank of each position
+  __shared__ uint16_t s_ereg[kMatchTile];      // end region of each local BEGIN (0xFFFF: open)
+  __shared__ uint32_t s_lastctx[kMatchThreads];
   __shared__ Fn s_wfn[4];
   __shared__ uint32_t s_wnb[4];
   __shared__ uint32_t s_prevctx, s_hasprev;
   __shared__ uint32_t s_first, s_lastp1, s_heads, s_lo, s_sout, s_maxlvl, s_orph;
   __shared__ uint32_t s_sin, s_nbpre_lo, s_nbpre_hi;
-
-  if (tid == 0) s_tile = atomicAdd(&a.tile_ctr[kCtrMatch], 1u);
-  __syncthreads();
-  const uint64_t tile = s_tile;
-  if (tile >= P->match_tiles) return;
+  uint64_t* s_oc = (uint64_t*)s_tree;
 
   const KeySpace ks = P->rec;
   const bool wide = ks.wide != 0;
   const uint64_t nv = P->n_valid;
-  const uint64_t base = tile * kMatchTile;
-  const uint32_t cnt = nv - base < (uint64_t)kMatchTile ? (uint32_t)(nv - base) : (uint32_t)kMatchTile;
   const uint32_t buf = P->rec_final;
   const uint64_t* gk = a.key[buf];
   const uint32_t* gp = a.pay[buf];
   const uint32_t* gc = a.ctxw[buf];
-  uint32_t* s_cw = (uint32_t*)s_cs;
-  uint64_t* s_oc = (uint64_t*)s_tree;
-
   auto ctx_of_key = [&](uint64_t k) -> uint32_t {
     return ks.ts_bits >= 64 ? 0u : (uint32_t)(k >> ks.ts_bits);
   };
 
-  // ---- load (coalesced, striped)
-  for (int j = 0; j < kMatchItems; ++j) {
-    const uint32_t i = (uint32_t)j * kMatchThreads + tid;
-    if (i < cnt) {
-      s_key[i] = gk[base + i];
-      s_pay[i] = gp[base + i];
-      if (wide) s_cw[i] = gc[base + i];
-    }
-  }
+  for (;;) {
   if (tid == 0) {
-    s_hasprev = base > 0;
-    s_prevctx = base > 0 ? (wide ? gc[base - 1] : ctx_of_key(gk[base - 1])) : 0u;
+    s_tile = atomicAdd(&a.tile_ctr[kCtrMatch], 1u);
     s_first = kMatchTile;
     s_lastp1 = 0;
     s_heads = 0;
@@ -161,40 +144,80 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
     s_orph = 0;
   }
   __syncthreads();
+  const uint64_t tile = s_tile;
+  if (tile >= P->match_tiles) break;
+  const uint64_t base = tile * kMatchTile;
+  const uint32_t cnt = nv - base < (uint64_t)kMatchTile ? (uint32_t)(nv - base) : (uint32_t)kMatchTile;
+  const uint32_t p0 = (uint32_t)tid * IT;
 
-  // ---- per-thread elements (blocked: positions 8*tid .. 8*tid+7)
-  uint64_t ts[kMatchItems];
-  uint32_t ctxr[kMatchItems], reg[kMatchItems];
+  // ---- blocked load: this thread's 8 consecutive records, 16-byte loads
+  uint64_t key[IT];
+  uint32_t pay[IT], ctxr[IT];
+  if (p0 + IT <= cnt) {
+    const uint4* k4 = (const uint4*)(gk + base + p0);
+#pragma unroll
+    for (int q = 0; q < IT / 2; ++q) {
+      const uint4 v = k4[q];
+      key[2 * q] = (uint64_t)v.x | ((uint64_t)v.y << 32);
+      key[2 * q + 1] = (uint64_t)v.z | ((uint64_t)v.w << 32);
+    }
+    const uint4* p4 = (const uint4*)(gp + base + p0);
+#pragma unroll
+    for (int q = 0; q < IT / 4; ++q) {
+      const uint4 v = p4[q];
+      pay[4 * q] = v.x;
+      pay[4 * q + 1] = v.y;
+      pay[4 * q + 2] = v.z;
+      pay[4 * q + 3] = v.w;
+    }
+    if (wide) {
+      const uint4* c4 = (const uint4*)(gc + base + p0);
+#pragma unroll
+      for (int q = 0; q < IT / 4; ++q) {
+        const uint4 v = c4[q];
+        ctxr[4 * q] = v.x;
+        ctxr[4 * q + 1] = v.y;
+        ctxr[4 * q + 2] = v.z;
+        ctxr[4 * q + 3] = v.w;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < IT; ++i) {
+      const uint32_t p = p0 + i;
+      key[i] = p < cnt ? gk[base + p] : 0;
+      pay[i] = p < cnt ? gp[base + p] : 0;
+      if (wide) ctxr[i] = p < cnt ? gc[base + p] : 0;
+    }
+  }
+  uint64_t ts[IT];
+  uint32_t reg[IT];
+#pragma unroll
+  for (int i = 0; i < IT; ++i) {
+    if (!wide) ctxr[i] = ctx_of_key(key[i]);
+    ts[i] = ks.ts_min + (wide ? key[i] : (key[i] & ks.ts_mask));
+    reg[i] = pay[i] & 0xFFFFu;
+  }
+  // context of the record before this thread's first one
+  s_lastctx[tid] = ctxr[IT - 1];
+  if (tid == 0) {
+    s_hasprev = base > 0;
+    s_prevctx = base > 0 ? (wide ? gc[base - 1] : ctx_of_key(gk[base - 1])) : 0u;
+  }
+  __syncthreads();
+  const bool has_prev0 = tid > 0 || s_hasprev != 0;
+  const uint32_t prev0 = tid > 0 ? s_lastctx[tid - 1] : s_prevctx;
+
   uint32_t fb = 0, fh = 0, fv = 0;  // bit i: BEGIN / context start / valid
   Fn f = fn_id();
   uint32_t nb = 0;
   uint32_t first_head = kMatchTile, last_p1 = 0, nheads = 0;
 #pragma unroll
-  for (int i = 0; i < kMatchItems; ++i) {
-    const uint32_t p = (uint32_t)tid * kMatchItems + i;
-    ts[i] = 0;
-    ctxr[i] = 0;
-    reg[i] = 0;
+  for (int i = 0; i < IT; ++i) {
+    const uint32_t p = p0 + i;
     if (p < cnt) {
-      const uint64_t k = s_key[p];
-      const uint32_t py = s_pay[p];
-      ctxr[i] = wide ? s_cw[p] : ctx_of_key(k);
-      ts[i] = ks.ts_min + (wide ? k : (k & ks.ts_mask));
-      reg[i] = py & 0xFFFFu;
-      const bool isb = ((py >> 16) & 1u) == 0;
-      uint32_t prev;
-      bool has_prev;
-      if (i > 0) {
-        prev = ctxr[i - 1];
-        has_prev = true;
-      } else if (p > 0) {
-        prev = wide ? s_cw[p - 1] : ctx_of_key(s_key[p - 1]);
-        has_prev = true;
-      } else {
-        prev = s_prevctx;
-        has_prev = s_hasprev != 0;
-      }
-      const bool head = !has_prev || prev != ctxr[i];
+      const bool isb = ((pay[i] >> 16) & 1u) == 0;
+      const bool head = i > 0 ? ctxr[i - 1] != ctxr[i] : (!has_prev0 || prev0 != ctxr[i]);
       fv |= 1u << i;
       if (isb) fb |= 1u << i;
       if (head) {
@@ -203,12 +226,7 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
         last_p1 = p + 1;
         nheads++;
       }
-      Fn e;
-      if (head) {
-        e = Fn{1u, 0, isb ? 1 : 0};
-      } else {
-        e = Fn{0u, isb ? 1 : -1, 0};
-      }
+      const Fn e = head ? Fn{1u, 0, isb ? 1 : 0} : Fn{0u, isb ? 1 : -1, 0};
       f = compose(f, e);
       nb += isb;
     }
@@ -306,18 +324,17 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   const uint32_t first = s_first, lastp1 = s_lastp1;
   const bool first_is_head = first == 0;
 
-  // ---- depths, tree leaves, local BEGIN ranks
-  uint32_t sb[kMatchItems], sa[kMatchItems];
+  // ---- depths (before: sb, after: sa), leaves x + 1 and the lower tree levels
+  uint32_t sb[IT], sa[IT], xp[IT];
   uint32_t cur = (uint32_t)apply(tfn, (int64_t)s_in);
-  uint32_t lb_rank = tnb;
   uint32_t lo = 0xFFFFFFFFu, maxlvl = 0, norph = 0;
   if (tid == 0 && !first_is_head) lo = s_in;
 #pragma unroll
-  for (int i = 0; i < kMatchItems; ++i) {
-    const uint32_t p = (uint32_t)tid * kMatchItems + i;
+  for (int i = 0; i < IT; ++i) {
+    const uint32_t p = p0 + i;
     sb[i] = 0;
     sa[i] = 0;
-    uint32_t leaf = 0xFFFFFFFFu;
+    xp[i] = 0xFFFFFFFFu;
     if ((fv >> i) & 1u) {
       const bool head = (fh >> i) & 1u;
       const bool isb = (fb >> i) & 1u;
@@ -326,8 +343,6 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
       if (isb) {
         after = before + 1;
         maxlvl = before > maxlvl ? before : maxlvl;
-        s_lbr[p] = (uint16_t)lb_rank;
-        lb_rank++;
       } else if (before == 0) {
         after = 0;  // orphan END
         norph++;
@@ -337,31 +352,57 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
       }
       sb[i] = before;
       sa[i] = after;
-      leaf = head ? 0u : before + 1;  // x + 1, so that a context start is 0
+      xp[i] = head ? 0u : before + 1;  // x + 1, so that a context start is 0
       if (p < first) lo = after < lo ? after : lo;
       cur = after;
       if (p + 1 == cnt) s_sout = after;
     }
-    s_tree[kMatchTile + p] = leaf;
   }
+  // local BEGIN ranks
+  uint32_t lbr[IT];
+  {
+    uint32_t r = tnb;
+#pragma unroll
+    for (int i = 0; i < IT; ++i) {
+      lbr[i] = r;
+      r += (fb >> i) & 1u;
+    }
+  }
+  {
+    uint4* leaf4 = (uint4*)&s_tree[kMatchTile + p0];
+    leaf4[0] = make_uint4(xp[0], xp[1], xp[2], xp[3]);
+    leaf4[1] = make_uint4(xp[4], xp[5], xp[6], xp[7]);
+    const uint32_t m01 = min(xp[0], xp[1]), m23 = min(xp[2], xp[3]);
+    const uint32_t m45 = min(xp[4], xp[5]), m67 = min(xp[6], xp[7]);
+    *(uint4*)&s_tree[kMatchTile / 2 + 4 * tid] = make_uint4(m01, m23, m45, m67);
+    const uint32_t q0 = min(m01, m23), q1 = min(m45, m67);
+    *(uint2*)&s_tree[kMatchTile / 4 + 2 * tid] = make_uint2(q0, q1);
+    s_tree[kMatchTile / 8 + tid] = min(q0, q1);
+  }
+#pragma unroll
+  for (int i = 0; i < IT; ++i)
+    if ((fb >> i) & 1u) s_lbr[p0 + i] = (uint16_t)lbr[i];
   if (lo != 0xFFFFFFFFu) atomicMin(&s_lo, lo);
   if (maxlvl) atomicMax(&s_maxlvl, maxlvl);
   if (norph) atomicAdd(&s_orph, norph);
-  // s_cs (which aliased the wide contexts) becomes the child-sum array.
-  __syncthreads();
   for (int k = tid; k < kMatchTile; k += kMatchThreads) {
     s_cs[k] = 0;
-    s_partner[k] = 0xFFFF;
+    s_ereg[k] = 0xFFFF;
   }
-  // min tree, bottom-up
-  for (int width = kMatchTile / 2; width >= 1; width >>= 1) {
-    for (int k = tid; k < width; k += kMatchThreads) {
-      const int node = width + k;
-      const uint32_t l = s_tree[2 * node], r = s_tree[2 * node + 1];
-      s_tree[node] = l < r ? l : r;
+  __syncthreads();
+  // upper tree levels (256 nodes and above) by one wave
+  if (w == 0) {
+    for (int width = kMatchTile / 16; width >= 1; width >>= 1) {
+      for (int k = lane; k < width; k += 64) {
+        const int node = width + k;
+        s_tree[node] = min(s_tree[2 * node], s_tree[2 * node + 1]);
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
-    __syncthreads();
   }
+  __syncthreads();
 
   const uint32_t lo_head = first_is_head ? 0u : s_lo;
   const uint32_t sin_eff = first_is_head ? 0u : s_in;
@@ -370,22 +411,45 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   const uint32_t lo_tail = has_head ? 0u : lo_head;
   const uint64_t pool = tile * kMatchTile;
 
-  // ---- searches: ENDs find their BEGIN, BEGINs find their parent
-  uint32_t par[kMatchItems];
+  // ---- searches.  An END at p closing level L needs the last q < p with
+  // x + 1 <= L + 1; a BEGIN at level L >= 1 needs the last q < p with
+  // x + 1 <= L (its parent).  This thread's own records are scanned in
+  // registers first; the tree is climbed from the thread's first record only
+  // when the answer lies further back.
+  uint32_t par[IT];
 #pragma unroll
-  for (int i = 0; i < kMatchItems; ++i) {
-    const uint32_t p = (uint32_t)tid * kMatchItems + i;
+  for (int i = 0; i < IT; ++i) {
     par[i] = kParNone;
     if (!((fv >> i) & 1u)) continue;
     const bool isb = (fb >> i) & 1u;
+    if (!isb && sb[i] == 0) continue;  // orphan END: no search
+    if (isb && sb[i] == 0) continue;   // top-level BEGIN: no parent
+    const uint32_t v = isb ? sb[i] : sa[i] + 1;
+    int qi = -1;
+#pragma unroll
+    for (int j = i - 1; j >= 0; --j)
+      if (qi < 0 && xp[j] <= v) qi = j;
+    uint32_t qrank;
+    bool found = qi >= 0;
+    if (found) {
+      // in-thread: rank from registers (the hit is always a BEGIN)
+      uint32_t rr = lbr[0];
+#pragma unroll
+      for (int j = 0; j < IT; ++j)
+        if (j == qi) rr = lbr[j];
+      qrank = rr;
+    } else {
+      const int q = psv(s_tree, (int)p0, v);
+      found = q >= 0;
+      qrank = found ? (uint32_t)s_lbr[q] : 0u;
+    }
     if (!isb) {
-      if (sb[i] == 0) continue;  // orphan
-      const uint32_t L = sa[i];
-      const int q = psv(s_tree, (int)p, L + 1);
-      if (q >= 0) {
-        s_partner[s_lbr[q]] = (uint16_t)p;
+      if (found) {
+        s_tend[qrank] = ts[i];
+        s_ereg[qrank] = (uint16_t)reg[i];
       } else {
         // pops a level that was open when the tile started
+        const uint32_t L = sa[i];
         const uint32_t idx = L - lo_head;
         if (L >= lo_head && idx < (uint32_t)kMatchTile) {
           a.pop_ts[pool + idx] = ts[i];
@@ -395,11 +459,7 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
         }
       }
     } else {
-      const uint32_t L = sb[i];
-      if (L >= 1) {
-        const int q = psv(s_tree, (int)p, L);
-        par[i] = q >= 0 ? (uint32_t)s_lbr[q] : kParOut;
-      }
+      par[i] = found ? qrank : kParOut;
     }
   }
   __syncthreads();
@@ -408,19 +468,16 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
 
   // ---- instances and child sums
 #pragma unroll
-  for (int i = 0; i < kMatchItems; ++i) {
-    const uint32_t p = (uint32_t)tid * kMatchItems + i;
+  for (int i = 0; i < IT; ++i) {
+    const uint32_t p = p0 + i;
     if (!((fv >> i) & 1u) || !((fb >> i) & 1u)) continue;
-    const uint32_t k = s_lbr[p];
+    const uint32_t k = lbr[i];
     const uint64_t id = nbpre + k;
     const uint32_t L = sb[i];
-    const uint32_t j = s_partner[k];
+    uint32_t ereg = s_ereg[k];
     uint64_t t_end = kU64Max;
-    uint32_t ereg = kNoEnd;
-    if (j != 0xFFFF) {
-      const uint64_t kj = s_key[j];
-      t_end = ks.ts_min + (wide ? kj : (kj & ks.ts_mask));
-      ereg = s_pay[j] & 0xFFFFu;
+    if (ereg != kNoEnd) {
+      t_end = s_tend[k];
       const uint64_t incl = t_end - ts[i];
       if (par[i] == kParOut) {
         const uint32_t oi = (L - 1) - op_lo;
@@ -481,6 +538,8 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
     if (s_maxlvl) atomicMax(&c[ARGUS_C_MAX_LEVEL], (unsigned long long)s_maxlvl);
     if (s_orph) atomicAdd(&c[ARGUS_C_N_ORPHAN_END], (unsigned long long)s_orph);
   }
+  __syncthreads();
+  }  // tiles
 }
 
 hipError_t launch_match(const RunArgs& a, hipStream_t s) {
@@ -502,7 +561,10 @@ hipError_t launch_match(const RunArgs& a, hipStream_t s) {
   m.counters = a.out.d_counters;
   m.rstats = a.out.d_region_stats;
   m.tile_ctr = a.w.tile_ctr;
-  hipLaunchKernelGGL(k_match, dim3((uint32_t)a.w.match_tiles), dim3(kMatchThreads), 0, s, m);
+  uint64_t blocks = a.w.match_tiles;
+  const uint64_t resident = persistent_blocks((const void*)k_match, kMatchThreads);
+  if (blocks > resident) blocks = resident;
+  hipLaunchKernelGGL(k_match, dim3((uint32_t)blocks), dim3(kMatchThreads), 0, s, m);
   return hipGetLastError();
 }
 

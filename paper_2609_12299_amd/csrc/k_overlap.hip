@@ -61,12 +61,13 @@ __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
   __shared__ uint32_t s_prev_g, s_has_prev, s_next_g, s_has_next;
   __shared__ uint64_t s_next_t;
 
-  if (tid == 0) s_tile = atomicAdd(&a.tile_ctr[kCtrSweep], 1u);
-  __syncthreads();
   const uint64_t n = P->n_ev;
   const uint64_t tiles = ceil_div(n, kSweepTile);
+  for (;;) {
+  if (tid == 0) s_tile = atomicAdd(&a.tile_ctr[kCtrSweep], 1u);
+  __syncthreads();
   const uint64_t tile = s_tile;
-  if (tile >= tiles) return;
+  if (tile >= tiles) break;
   const KeySpace ks = P->ev;
   const bool wide = ks.wide != 0;
   const uint32_t buf = P->ev_final;
@@ -351,6 +352,8 @@ __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
     if (s_u[slot][k]) atomicAdd((unsigned long long*)&a.ov_u[gg * kSweepQWords + k], (unsigned long long)s_u[slot][k]);
     if (s_q[slot][k]) atomicAdd((unsigned long long*)&a.ov_q[gg * kSweepQWords + k], (unsigned long long)s_q[slot][k]);
   }
+  __syncthreads();
+  }  // tiles
 }
 
 hipError_t launch_sweep(const RunArgs& a, hipStream_t s) {
@@ -368,7 +371,10 @@ hipError_t launch_sweep(const RunArgs& a, hipStream_t s) {
   sa.G = a.G;
   sa.tile_ctr = a.w.tile_ctr;
   sa.counters = a.out.d_counters;
-  const uint64_t blocks = ceil_div(a.n ? a.n : 1, kSweepTile);
+  uint64_t blocks = ceil_div(a.n ? a.n : 1, kSweepTile);
+  const void* kern = a.K <= 2 ? (const void*)k_sweep<2> : a.K <= 4 ? (const void*)k_sweep<4> : (const void*)k_sweep<8>;
+  const uint64_t resident = persistent_blocks(kern, kSweepThreads);
+  if (blocks > resident) blocks = resident;
   if (a.K <= 2)
     hipLaunchKernelGGL(k_sweep<2>, dim3((uint32_t)blocks), dim3(kSweepThreads), 0, s, sa);
   else if (a.K <= 4)

@@ -42,7 +42,12 @@ __device__ __forceinline__ uint32_t digit_of(uint32_t pos, uint64_t raw_ctx, uin
                  : (uint32_t)(raw_ts >> (8 * (pos - 4))) & 0xFFu;
 }
 
+// WHICH (records / events) and SLOT are template parameters so that every
+// pass of a sort is a distinct kernel in profiles.
+template <int WHICH, int SLOT>
 __global__ __launch_bounds__(kSortThreads) void k_radix_pass(RadixArgs a) {
+  a.which = WHICH;
+  a.slot = SLOT;
   const SlotPlan sp = a.which ? a.plan->es[a.slot] : a.plan->rs[a.slot];
   if (!sp.active) return;
   const KeySpace ks = a.which ? a.plan->ev : a.plan->rec;
@@ -59,11 +64,14 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(RadixArgs a) {
   __shared__ uint8_t s_dig[kSortTile];
 
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  // Persistent blocks: tiles are taken in order from an atomic counter, so a
+  // tile's predecessors always belong to blocks that are already running.
+  for (;;) {
   if (tid == 0) s_tile = atomicAdd(&a.tile_ctr[(a.which ? kCtrEv : kCtrRec) + a.slot], 1u);
   for (int i = tid; i < 4 * kRadixBins; i += kSortThreads) (&s_wave[0][0])[i] = 0;
   __syncthreads();
   const uint64_t tile = s_tile;
-  if (tile >= sp.tiles) return;
+  if (tile >= sp.tiles) break;
 
   const uint64_t base = tile * kSortTile;
   const uint64_t left = sp.n_elems - base;
@@ -252,6 +260,8 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(RadixArgs a) {
     pd[gp] = s_pay[i];
     if (wide) cd[gp] = s_cw[i];
   }
+  __syncthreads();
+  }  // tiles
 }
 
 hipError_t launch_radix_pass(const RunArgs& a, int which, int slot, uint64_t max_elems,
@@ -277,7 +287,17 @@ hipError_t launch_radix_pass(const RunArgs& a, int which, int slot, uint64_t max
   ra.tile_ctr = a.w.tile_ctr;
   ra.counters = a.out.d_counters;
   uint64_t blocks = ceil_div(max_elems ? max_elems : 1, kSortTile);
-  hipLaunchKernelGGL(k_radix_pass, dim3((uint32_t)blocks), dim3(kSortThreads), 0, s, ra);
+  const uint64_t resident = persistent_blocks((const void*)k_radix_pass<0, 0>, kSortThreads);
+  if (blocks > resident) blocks = resident;
+  using K = void (*)(RadixArgs);
+#define ARGUS_SLOTS(W) \
+  k_radix_pass<W, 0>, k_radix_pass<W, 1>, k_radix_pass<W, 2>, k_radix_pass<W, 3>, \
+  k_radix_pass<W, 4>, k_radix_pass<W, 5>, k_radix_pass<W, 6>, k_radix_pass<W, 7>, \
+  k_radix_pass<W, 8>, k_radix_pass<W, 9>, k_radix_pass<W, 10>, k_radix_pass<W, 11>, \
+  k_radix_pass<W, 12>, k_radix_pass<W, 13>, k_radix_pass<W, 14>, k_radix_pass<W, 15>
+  static const K table[2][kSlots] = {{ARGUS_SLOTS(0)}, {ARGUS_SLOTS(1)}};
+#undef ARGUS_SLOTS
+  hipLaunchKernelGGL(table[which][slot], dim3((uint32_t)blocks), dim3(kSortThreads), 0, s, ra);
   return hipGetLastError();
 }
 
