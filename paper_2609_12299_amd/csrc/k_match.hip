@@ -54,6 +54,21 @@ __device__ __forceinline__ Fn shfl_up_fn(const Fn& f, int o) {
   return r;
 }
 
+__device__ __forceinline__ Fn shfl_down_fn(const Fn& f, int o) {
+  Fn r;
+  r.reset = __shfl_down(f.reset, o);
+  r.a = __shfl_down(f.a, o);
+  r.c = __shfl_down(f.c, o);
+  return r;
+}
+__device__ __forceinline__ Fn shfl_fn(const Fn& f, int src) {
+  Fn r;
+  r.reset = __shfl(f.reset, src);
+  r.a = __shfl(f.a, src);
+  r.c = __shfl(f.c, src);
+  return r;
+}
+
 // Tile aggregate in one status word: reset (1 bit), a + 2048 (13 bits),
 // c (12 bits), number of BEGINs (12 bits).
 __device__ __forceinline__ uint64_t pack_agg(const Fn& f, uint32_t nb) {
@@ -67,19 +82,46 @@ __device__ __forceinline__ void unpack_agg(uint64_t v, Fn* f, uint32_t* nb) {
   *nb = (uint32_t)(v & 0xFFFull);
 }
 
-// Last q < qpos whose leaf value is <= v, or -1 (heap-ordered min tree, leaves
-// at [kMatchTile, 2 * kMatchTile)).
-__device__ __forceinline__ int psv(const uint32_t* tree, int qpos, uint32_t v) {
-  int node = qpos + kMatchTile;
-  while (node > 1) {
-    if ((node & 1) && tree[node - 1] <= v) {
-      node = node - 1;
-      while (node < kMatchTile) node = (tree[2 * node + 1] <= v) ? 2 * node + 1 : 2 * node;
-      return node - kMatchTile;
+// Min tree over the tile's 2048 leaves with fan-out 8, in LDS:
+//   level 0: leaves [0, 2048), level 1: 256 nodes at 2048, level 2: 32 nodes
+//   at 2304, level 3: 4 nodes at 2336 (padded to 8).  Every group of 8
+//   siblings is 32-byte aligned and read with two 16-byte loads.
+constexpr int kT1 = kMatchTile;
+constexpr int kT2 = kT1 + kMatchTile / 8;
+constexpr int kT3 = kT2 + kMatchTile / 64;
+static_assert(kMatchTile == 2048, "tree levels assume 2048 leaves");
+
+// Last j < lim of the 8 siblings at g whose value is <= v, or -1.
+__device__ __forceinline__ int last_le8(const uint32_t* g, uint32_t lim, uint32_t v) {
+  const uint4 a = *(const uint4*)g, b = *(const uint4*)(g + 4);
+  const uint32_t x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+  int r = -1;
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+    if ((uint32_t)j < lim && x[j] <= v) r = j;
+  return r;
+}
+
+// Last leaf q < 8 * chunk whose value is <= v, or -1: climb from the
+// chunk's level-1 node through left siblings, then descend to the leaf.
+__device__ __forceinline__ int psv8(const uint32_t* t, uint32_t chunk, uint32_t v) {
+  const uint32_t i1 = chunk, i2 = chunk >> 3, i3 = chunk >> 6;
+  int n1 = -1, n2 = -1;
+  int j = last_le8(t + kT1 + (i1 & ~7u), i1 & 7u, v);
+  if (j >= 0) {
+    n1 = (int)(i1 & ~7u) + j;
+  } else {
+    j = last_le8(t + kT2 + (i2 & ~7u), i2 & 7u, v);
+    if (j >= 0) {
+      n2 = (int)(i2 & ~7u) + j;
+    } else {
+      j = last_le8(t + kT3, i3, v);
+      if (j < 0) return -1;
+      n2 = j * 8 + last_le8(t + kT2 + j * 8, 8u, v);
     }
-    node >>= 1;
+    n1 = n2 * 8 + last_le8(t + kT1 + n2 * 8, 8u, v);
   }
-  return -1;
+  return n1 * 8 + last_le8(t + n1 * 8, 8u, v);
 }
 
 struct MatchArgs {
@@ -269,8 +311,11 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   const Fn tfn = compose(pre, ex);  // map from tile input to this thread's input
   const uint32_t tnb = pnb + nbex;  // BEGINs of the tile before this thread
 
-  // ---- decoupled look-back: depth entering the tile, BEGINs before it
-  if (tid == 0) {
+  // ---- decoupled look-back: depth entering the tile, BEGINs before it.
+  // Wave 0 inspects 64 predecessor tiles per round trip (lane j: the j-th
+  // nearest not yet folded in) and folds the aggregates up to the nearest
+  // inclusive value, or up to the nearest tile that has published nothing.
+  if (w == 0) {
     Fn all = fn_id();
     uint32_t nball = 0;
     for (int k = 0; k < 4; ++k) {
@@ -280,42 +325,65 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
     uint64_t s_in = 0, nbpre = 0;
     uint64_t* lb = a.mlb;
     if (tile > 0) {
-      st_agent(&lb[tile * 4], pack_agg(all, nball));
+      if (lane == 0) st_agent(&lb[tile * 4], pack_agg(all, nball));
       Fn acc = fn_id();
       uint64_t nb_acc = 0;
-      int64_t tt = (int64_t)tile - 1;
+      int64_t top = (int64_t)tile - 1;  // nearest tile not yet folded in
       uint32_t spins = 0;
-      while (tt >= 0) {
-        const uint64_t w1 = ld_agent(&lb[tt * 4 + 1]);
-        const uint64_t w2 = ld_agent(&lb[tt * 4 + 2]);
-        if ((w1 & ~kValMask) == kFlagIncl && (w2 & ~kValMask) == kFlagIncl) {
-          s_in = (uint64_t)apply(acc, (int64_t)(w1 & kValMask));
-          nbpre = (w2 & kValMask) + nb_acc;
+      for (;;) {
+        const int64_t tt = top - lane;
+        uint64_t w0 = 0, w1 = 0, w2 = 0;
+        if (tt >= 0) {
+          w1 = ld_agent(&lb[tt * 4 + 1]);
+          w2 = ld_agent(&lb[tt * 4 + 2]);
+          w0 = ld_agent(&lb[tt * 4]);
+        }
+        const bool incl = (w1 & ~kValMask) == kFlagIncl && (w2 & ~kValMask) == kFlagIncl;
+        const bool agg = (w0 & ~kValMask) == kFlagAgg;
+        const uint64_t mi = __ballot(incl), mn = __ballot(!incl && !agg);
+        const int ji = mi ? __ffsll((unsigned long long)mi) - 1 : 64;
+        const int jn = mn ? __ffsll((unsigned long long)mn) - 1 : 64;
+        const bool done = ji < jn;
+        const int k = done ? ji : jn;  // lanes [0, k) hold aggregates to fold in
+        Fn x = fn_id();
+        uint32_t nx = 0;
+        if (lane < k) unpack_agg(w0, &x, &nx);
+        // reduce towards lane 0; a higher lane is an earlier tile
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const Fn y = shfl_down_fn(x, o);
+          const uint32_t ny = __shfl_down(nx, o);
+          if (lane + o < 64) {
+            x = compose(y, x);
+            nx += ny;
+          }
+        }
+        acc = compose(shfl_fn(x, 0), acc);
+        nb_acc += (uint32_t)__shfl(nx, 0);
+        if (done) {
+          const uint64_t v1 = __shfl(w1, ji), v2 = __shfl(w2, ji);
+          s_in = (uint64_t)apply(acc, (int64_t)(v1 & kValMask));
+          nbpre = (v2 & kValMask) + nb_acc;
           break;
         }
-        const uint64_t w0 = ld_agent(&lb[tt * 4]);
-        if ((w0 & ~kValMask) == kFlagAgg) {
-          Fn fa;
-          uint32_t na;
-          unpack_agg(w0, &fa, &na);
-          acc = compose(fa, acc);
-          nb_acc += na;
-          --tt;
-          continue;
+        top -= k;
+        if (k == 0) {
+          if (++spins > kMaxSpins) {
+            if (lane == 0) flag_internal_error(a.counters, 8);
+            break;
+          }
+          backoff();
         }
-        if (++spins > kMaxSpins) {
-          flag_internal_error(a.counters, 8);
-          break;
-        }
-        backoff();
       }
     }
-    const uint64_t s_out = (uint64_t)apply(all, (int64_t)s_in);
-    st_agent(&lb[tile * 4 + 1], kFlagIncl | s_out);
-    st_agent(&lb[tile * 4 + 2], kFlagIncl | (nbpre + nball));
-    s_sin = (uint32_t)s_in;
-    s_nbpre_lo = (uint32_t)nbpre;
-    s_nbpre_hi = (uint32_t)(nbpre >> 32);
+    if (lane == 0) {
+      const uint64_t s_out = (uint64_t)apply(all, (int64_t)s_in);
+      st_agent(&lb[tile * 4 + 1], kFlagIncl | s_out);
+      st_agent(&lb[tile * 4 + 2], kFlagIncl | (nbpre + nball));
+      s_sin = (uint32_t)s_in;
+      s_nbpre_lo = (uint32_t)nbpre;
+      s_nbpre_hi = (uint32_t)(nbpre >> 32);
+    }
   }
   __syncthreads();
 
@@ -369,15 +437,24 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
     }
   }
   {
-    uint4* leaf4 = (uint4*)&s_tree[kMatchTile + p0];
+    uint4* leaf4 = (uint4*)&s_tree[p0];
     leaf4[0] = make_uint4(xp[0], xp[1], xp[2], xp[3]);
     leaf4[1] = make_uint4(xp[4], xp[5], xp[6], xp[7]);
-    const uint32_t m01 = min(xp[0], xp[1]), m23 = min(xp[2], xp[3]);
-    const uint32_t m45 = min(xp[4], xp[5]), m67 = min(xp[6], xp[7]);
-    *(uint4*)&s_tree[kMatchTile / 2 + 4 * tid] = make_uint4(m01, m23, m45, m67);
-    const uint32_t q0 = min(m01, m23), q1 = min(m45, m67);
-    *(uint2*)&s_tree[kMatchTile / 4 + 2 * tid] = make_uint2(q0, q1);
-    s_tree[kMatchTile / 8 + tid] = min(q0, q1);
+    uint32_t m = xp[0];
+#pragma unroll
+    for (int i = 1; i < IT; ++i) m = min(m, xp[i]);
+    s_tree[kT1 + tid] = m;
+    m = min(m, (uint32_t)__shfl_xor(m, 1));
+    m = min(m, (uint32_t)__shfl_xor(m, 2));
+    m = min(m, (uint32_t)__shfl_xor(m, 4));
+    if ((lane & 7) == 0) s_tree[kT2 + (tid >> 3)] = m;
+    m = min(m, (uint32_t)__shfl_xor(m, 8));
+    m = min(m, (uint32_t)__shfl_xor(m, 16));
+    m = min(m, (uint32_t)__shfl_xor(m, 32));
+    if (lane == 0) {
+      s_tree[kT3 + w] = m;
+      s_tree[kT3 + 4 + w] = 0xFFFFFFFFu;
+    }
   }
 #pragma unroll
   for (int i = 0; i < IT; ++i)
@@ -390,20 +467,6 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
     s_ereg[k] = 0xFFFF;
   }
   __syncthreads();
-  // upper tree levels (256 nodes and above) by one wave
-  if (w == 0) {
-    for (int width = kMatchTile / 16; width >= 1; width >>= 1) {
-      for (int k = lane; k < width; k += 64) {
-        const int node = width + k;
-        s_tree[node] = min(s_tree[2 * node], s_tree[2 * node + 1]);
-      }
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    }
-  }
-  __syncthreads();
-
   const uint32_t lo_head = first_is_head ? 0u : s_lo;
   const uint32_t sin_eff = first_is_head ? 0u : s_in;
   const uint32_t op_lo = lo_head >= 1 ? lo_head - 1 : 0;
@@ -439,7 +502,7 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
         if (j == qi) rr = lbr[j];
       qrank = rr;
     } else {
-      const int q = psv(s_tree, (int)p0, v);
+      const int q = psv8(s_tree, (uint32_t)tid, v);
       found = q >= 0;
       qrank = found ? (uint32_t)s_lbr[q] : 0u;
     }

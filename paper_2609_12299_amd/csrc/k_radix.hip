@@ -146,7 +146,12 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(RadixArgs a) {
       }
     }
     dig[r] = d;
-    // Rank among this wave's elements with the same digit (stable).
+  }
+  // Rank among this wave's elements with the same digit (stable order is
+  // wave, round, lane).  All loads above are already in flight.
+#pragma unroll
+  for (int r = 0; r < kSortItems; ++r) {
+    const uint32_t d = dig[r];
     const bool part = d < 256;
     const uint64_t vm = __ballot(part);
     uint64_t peers = vm;
@@ -204,22 +209,33 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(RadixArgs a) {
     st_agent(&lb[dgt], kFlagIncl | tot);
   } else {
     st_agent(&lb[tile * kRadixBins + dgt], kFlagAgg | tot);
+    // Four predecessors per round trip; consume them nearest first.
     int64_t tt = (int64_t)tile - 1;
     uint32_t spins = 0;
-    while (tt >= 0) {
-      const uint64_t v = ld_agent(&lb[(uint64_t)tt * kRadixBins + dgt]);
-      const uint64_t f = v & ~kValMask;
-      if (f == 0) {
+    bool done = false;
+    while (!done && tt >= 0) {
+      uint64_t v[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        v[q] = tt - q >= 0 ? ld_agent(&lb[(uint64_t)(tt - q) * kRadixBins + dgt]) : kFlagIncl;
+      int used = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (done || used != q) break;
+        const uint64_t f = v[q] & ~kValMask;
+        if (f == 0) break;  // not published yet: reload from here
+        excl += v[q] & kValMask;
+        ++used;
+        if (f == kFlagIncl) done = true;
+      }
+      tt -= used;
+      if (used == 0) {
         if (++spins > kMaxSpins) {
           flag_internal_error(a.counters, 1);
           break;
         }
         backoff();
-        continue;
       }
-      excl += v & kValMask;
-      if (f == kFlagIncl) break;
-      --tt;
     }
     st_agent(&lb[tile * kRadixBins + dgt], kFlagIncl | (excl + tot));
   }
