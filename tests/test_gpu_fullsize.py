@@ -1,0 +1,172 @@
+"""Parity at the full workload sizes, in the launch configuration the benchmark
+times (instances and exclusive times written, default sort path).
+
+* The four smaller workloads (2^16 .. 2^26 records) are compared whole with
+  the oracle, bit for bit.
+* The 2^28-record trace (4 GiB) is run whole on the GPU.  Its outputs are
+  checked (a) on sampled context groups -- the largest groups and a seeded
+  random choice -- against the oracle run on just those groups' records: the
+  instances, their exclusive times and the groups' overlap matrices must be
+  identical; and (b) through properties that hold at any size: counter
+  identities, per-region statistics recomputed from the instance array, and
+  the global overlap as the sum over groups.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from golden_util import RS_FIELDS, RS_HIST_EXCL, RS_HIST_INCL
+from gpu_util import assert_parity, gpu_run, log, oracle_run
+
+pytestmark = pytest.mark.gpu
+
+U64_MAX = np.uint64(0xFFFFFFFFFFFFFFFF)
+NO_PARENT = 0xFFFFFFFF
+NO_END = 0xFFFF
+
+
+def _params(d):
+    return {k: d[k] for k in ("num_regions", "num_classes", "region_class", "group_shift", "num_groups")}
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 4, 3])
+def test_full_size_whole(oracle_mod, tracegen_mod, cfg):
+    d = tracegen_mod.generate(cfg, threads=16)
+    p = _params(d)
+    log(f"[gpu] full-size config {cfg}: n={len(d['records'])}")
+    assert_parity(gpu_run(d["records"], p), oracle_run(oracle_mod, d["records"], p),
+                  what=f"full cfg{cfg}")
+
+
+def _bit_width(x: np.ndarray) -> np.ndarray:
+    """Number of significant bits of each u64 (0 for 0), exactly."""
+    x = x.astype(np.uint64)
+    bw = np.zeros(x.shape, np.int64)
+    for s in (32, 16, 8, 4, 2, 1):
+        big = (x >> np.uint64(s)) != 0
+        bw += np.where(big, s, 0)
+        x = np.where(big, x >> np.uint64(s), x)
+    return bw + (x != 0)
+
+
+def _region_stats_from_instances(inst: np.ndarray, excl: np.ndarray, R: int) -> dict:
+    """Per-region statistics of the matched instances, from the instance array."""
+    closed = inst["end_region_id"] != NO_END
+    matched = closed & (inst["end_region_id"] == inst["region_id"])
+    reg = inst["region_id"][matched].astype(np.int64)
+    d = (inst["t_end"][matched] - inst["t_begin"][matched]).astype(np.uint64)
+    e = excl[matched].astype(np.uint64)
+    out = {}
+    out["count"] = np.bincount(reg, minlength=R).astype(np.uint64)
+    # u64 sums that wrap: split into 32-bit halves, sum exactly in u64 per half
+    for name, v in (("incl_sum", d), ("excl_sum", e)):
+        lo = np.zeros(R, np.uint64)
+        hi = np.zeros(R, np.uint64)
+        np.add.at(lo, reg, v & np.uint64(0xFFFFFFFF))
+        np.add.at(hi, reg, v >> np.uint64(32))
+        out[name] = lo + (hi << np.uint64(32))
+    for name, v, fn, init in (("incl_min", d, np.minimum, U64_MAX), ("incl_max", d, np.maximum, 0),
+                              ("excl_min", e, np.minimum, U64_MAX), ("excl_max", e, np.maximum, 0)):
+        a = np.full(R, init, np.uint64)
+        fn.at(a, reg, v)
+        out[name] = a
+    for name, v in (("hist_incl", d), ("hist_excl", e)):
+        h = np.zeros(R * 65, np.uint64)
+        np.add.at(h, reg * 65 + _bit_width(v), 1)
+        out[name] = h.reshape(R, 65)
+    # ambiguity counts that the instance array determines
+    unc = ~closed
+    out["unclosed"] = np.bincount(inst["region_id"][unc].astype(np.int64), minlength=R).astype(np.uint64)
+    mism = closed & ~matched
+    out["mism_as_begin"] = np.bincount(inst["region_id"][mism].astype(np.int64), minlength=R).astype(np.uint64)
+    out["mism_as_end"] = np.bincount(inst["end_region_id"][mism].astype(np.int64), minlength=R).astype(np.uint64)
+    par = inst["parent"]
+    has_par = matched & (par != NO_PARENT)
+    idx = np.nonzero(has_par)[0]
+    selfn = idx[inst["region_id"][par[idx]] == inst["region_id"][idx]]
+    out["self_nested"] = np.bincount(inst["region_id"][selfn].astype(np.int64), minlength=R).astype(np.uint64)
+    return out
+
+
+def test_full_size_large_trace_sampled(oracle_mod, tracegen_mod):
+    d = tracegen_mod.generate(5, threads=16)
+    p = _params(d)
+    rec = d["records"]
+    n = len(rec)
+    R, K, G, shift = p["num_regions"], p["num_classes"], p["num_groups"], p["group_shift"]
+    log(f"[gpu] full-size large trace: n={n}")
+    g = gpu_run(rec, p)
+    c = g["counters"].astype(np.uint64)
+    assert int(c[31]) == 0, f"internal error flag {int(c[31])}"
+    inst, excl = g["instances"], g["instance_excl"]
+
+    # ---- (b) properties at full size
+    log("[gpu] full-size large trace: properties")
+    rv = rec.view(np.uint8).reshape(n, 16)
+    kind = rv[:, 14]
+    region = rv[:, 12].astype(np.uint32) | (rv[:, 13].astype(np.uint32) << 8)
+    ctx = np.ascontiguousarray(rv[:, 8:12]).view(np.uint32).reshape(n)
+    bad_kind = (kind != 1) & (kind != 2)
+    bad_region = ~bad_kind & (region >= R)
+    valid = ~bad_kind & ~bad_region
+    assert int(c[0]) == n
+    assert int(c[2]) == int(bad_kind.sum()) and int(c[3]) == int(bad_region.sum())
+    assert int(c[1]) == int(valid.sum())
+    assert int(c[4]) == int((valid & (kind == 1)).sum()) and int(c[5]) == int((valid & (kind == 2)).sum())
+    assert len(inst) == int(c[4])
+    assert int(c[9]) + int(c[10]) + int(c[11]) == int(c[4])  # matched + mismatched + unclosed = begins
+    # every END is either an orphan or closes exactly one instance
+    closed = inst["end_region_id"] != NO_END
+    assert int(c[12]) + int(closed.sum()) == int(c[5])
+    vctx = ctx[valid]
+    assert int(c[8]) == len(np.unique(vctx))
+    assert int(c[16]) == int(vctx.min()) and int(c[17]) == int(vctx.max())
+    ts = np.ascontiguousarray(rv[:, 0:8]).view(np.uint64).reshape(n)[valid]
+    assert int(c[6]) == int(ts.min()) and int(c[7]) == int(ts.max())
+    assert int(c[14]) == int(inst["level"].max())
+    # instances sorted by (ctx, t_begin); durations and exclusive times sane
+    assert np.all(np.diff(inst["ctx_key"].astype(np.int64)) >= 0)
+    same = inst["ctx_key"][1:] == inst["ctx_key"][:-1]
+    assert np.all(inst["t_begin"][1:][same] >= inst["t_begin"][:-1][same])
+    assert np.all(inst["t_end"][closed] >= inst["t_begin"][closed])
+    assert np.all(excl[closed] <= (inst["t_end"][closed] - inst["t_begin"][closed]))
+    assert np.all(excl[~closed] == 0)
+    rs = g["region_stats"].reshape(R, -1)
+    ref = _region_stats_from_instances(inst, excl, R)
+    for name, col in RS_FIELDS.items():
+        if name == "orphan_end":
+            continue  # needs the records, not the instances
+        np.testing.assert_array_equal(rs[:, col], ref[name], err_msg=f"region stats {name}")
+    np.testing.assert_array_equal(rs[:, RS_HIST_INCL:RS_HIST_INCL + 65], ref["hist_incl"])
+    np.testing.assert_array_equal(rs[:, RS_HIST_EXCL:RS_HIST_EXCL + 65], ref["hist_excl"])
+    assert int(c[9]) == int(ref["count"].sum())
+    ov = g["overlap_group"].reshape(G, 2 * K * K)
+    np.testing.assert_array_equal(ov.sum(axis=0, dtype=np.uint64), g["overlap_global"].reshape(-1))
+
+    # ---- (a) sampled groups against the oracle
+    grp = ctx >> np.uint32(shift) if shift < 32 else np.zeros(n, np.uint32)
+    sizes = np.bincount(grp.astype(np.int64), minlength=G)
+    rng = np.random.default_rng(12299)
+    largest = np.argsort(-sizes[:G], kind="stable")[:3]
+    rest = np.setdiff1d(np.arange(G), largest)
+    pick = np.concatenate([largest, rng.choice(rest, size=29, replace=False)])
+    sel = np.isin(grp, pick)
+    sub = np.ascontiguousarray(rec[sel])
+    log(f"[gpu] full-size large trace: oracle on {len(pick)} groups, {len(sub)} records")
+    o = oracle_run(oracle_mod, sub, p)
+    oi = o["instances"]
+    keep = np.isin(inst["ctx_key"] >> np.uint32(shift), pick)
+    gi = inst[keep]
+    assert len(gi) == len(oi), f"{len(gi)} sampled instances vs {len(oi)}"
+    for f in ("t_begin", "t_end", "ctx_key", "level", "region_id", "end_region_id"):
+        np.testing.assert_array_equal(gi[f], oi[f], err_msg=f"sampled instances: {f}")
+    gid = np.nonzero(keep)[0]
+    remap = np.full(len(inst), NO_PARENT, np.int64)
+    remap[gid] = np.arange(len(gid))
+    gp = gi["parent"].astype(np.int64)
+    gp_sub = np.where(gp == NO_PARENT, NO_PARENT, remap[np.minimum(gp, len(inst) - 1)])
+    np.testing.assert_array_equal(gp_sub, oi["parent"].astype(np.int64), err_msg="sampled parents")
+    np.testing.assert_array_equal(excl[keep], o["instance_excl"], err_msg="sampled exclusive times")
+    og = o["overlap_group"].reshape(G, 2 * K * K)
+    np.testing.assert_array_equal(ov[pick], og[pick], err_msg="sampled group overlap")
