@@ -77,8 +77,12 @@ def byte_model(name: str, c: dict, plan: dict, R: int, K: int, G: int, flags: in
         return 8.0 * nv
     if name == "ts_hist":
         return 8.0 * nv if plan["unsorted"] else 0.0
+    ev_words = K > 0 and plan["rec_ts_bits"] + (max(G - 1, 0)).bit_length() + 5 <= 64
     if name == "match":
-        return (12.0 + (4.0 if wide else 0.0)) * nv + 40.0 * nb
+        # sorted keys (+ context words) in; instances and one event word per record out
+        return (12.0 + (4.0 if wide else 0.0) + (8.0 if ev_words else 0.0)) * nv + 40.0 * nb
+    if name.startswith("merge") and name[5:].isdigit():
+        return 16.0 * plan["merge_end"] if int(name[5:]) < plan["merge_rounds"] and plan["ev_merge"] else 0.0
     if name == "agg":
         return 40.0 * nb + (8.0 * nb if flags & 2 else 0.0) + (4.0 * nb if R > 167 else 0.0)
     if name == "hist":
@@ -86,7 +90,7 @@ def byte_model(name: str, c: dict, plan: dict, R: int, K: int, G: int, flags: in
     if name == "ev_hist":
         return 32.0 * nb
     if name == "sweep":
-        return 12.0 * nev
+        return 8.0 * plan["merge_end"] if plan["ev_merge"] else 12.0 * nev
     if name == "init":
         return 8.0 * (R * 142 + (-(-n // 4096)) * 256 + (-(-nv // 2048)) * 4 + (-(-n // 2048)) * 8)
     if name == "ev_clear":
@@ -133,6 +137,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=5, choices=sorted(WORKLOADS))
     ap.add_argument("--force-full-sort", action="store_true")
+    ap.add_argument("--force-event-sort", action="store_true",
+                    help="order overlap events with the radix sort instead of merging")
     ap.add_argument("--cpu-sample", type=int, default=1 << 25)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernels", action="store_true", help="print per-launch timing to stderr")
@@ -161,7 +167,8 @@ def main() -> int:
     torch.cuda.synchronize()
     ra = RegionAttribution(d["num_regions"], d["num_classes"], d["region_class"], d["group_shift"],
                            d["num_groups"], max_records=n, instances=True, instance_excl=True,
-                           force_full_sort=args.force_full_sort, device=dev)
+                           force_full_sort=args.force_full_sort,
+                           force_event_sort=args.force_event_sort, device=dev)
     out = ra.alloc(n)
     for _ in range(max(args.warmup, 1)):
         ra.run(rec, out)
@@ -212,7 +219,8 @@ def main() -> int:
         for k in sorted(avg, key=lambda k: -avg[k]):
             gbs = bytes_per[k] / (avg[k] * 1e-3) / 1e9 if avg[k] > 0 else 0.0
             err(f"  {k:16s} {avg[k]:8.4f} ms  {bytes_per[k] / 2**20:10.1f} MiB  {gbs:8.1f} GB/s")
-        err(f"plan: unsorted={plan['unsorted']} n_ev={plan['n_ev']} "
+        err(f"plan: unsorted={plan['unsorted']} n_ev={plan['n_ev']} ev_merge={plan['ev_merge']} "
+            f"merge_rounds={plan['merge_rounds']} "
             f"rec_active={[int(s['pos']) for s in plan['rec_slots'] if s['active']]} "
             f"ev_active={[int(s['pos']) for s in plan['ev_slots'] if s['active']]}")
 
@@ -231,11 +239,13 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": WORKLOADS[args.config], "records": n, "record_bytes": 16,
                    "contexts": int(d["blocks"]) * int(d["warps"]), "regions": R, "classes": K,
-                   "groups": G, "force_full_sort": bool(args.force_full_sort)},
+                   "groups": G, "force_full_sort": bool(args.force_full_sort),
+                   "force_event_sort": bool(args.force_event_sort)},
         "pipeline": {"bytes_per_record": round(total_bytes / n, 2),
                      "achieved_gbs": round(total_bytes / (step_ms * 1e-3) / 1e9, 1),
                      "frac_of_peak": round(total_bytes / (step_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-                     "full_sort": bool(plan["unsorted"])},
+                     "full_sort": bool(plan["unsorted"]),
+                     "events": f"merged in {plan['merge_rounds']} rounds" if plan["ev_merge"] else "radix sort"},
         "roofline": roofline,
         "kernels_ms": {k: round(v, 4) for k, v in sorted(avg.items(), key=lambda kv: -kv[1])
                        if v >= 0.01},

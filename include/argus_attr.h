@@ -127,10 +127,14 @@ enum {
 enum {
   ARGUS_OUT_INSTANCES = 1u,     /* write out->d_instances */
   ARGUS_OUT_INSTANCE_EXCL = 2u, /* write out->d_instance_excl */
-  ARGUS_FORCE_FULL_SORT = 4u    /* always sort on every timestamp digit, even
+  ARGUS_FORCE_FULL_SORT = 4u,   /* always sort on every timestamp digit, even
                                    when each context is already in time order
                                    in the input (results are identical; for
                                    measurement and testing) */
+  ARGUS_FORCE_EVENT_SORT = 8u   /* order the overlap events with a radix sort
+                                   of (group, time) even where merging the
+                                   per-context runs applies (results are
+                                   identical; for measurement and testing) */
 };
 
 typedef struct argus_attr_config {
@@ -139,7 +143,7 @@ typedef struct argus_attr_config {
   uint32_t num_classes;   /* K: 0..8; 0 disables the overlap step */
   uint32_t group_shift;   /* group = ctx_key >> group_shift; 0..32 (32: one group) */
   uint32_t num_groups;    /* G: rows of the per-group overlap output; 1..2^20 if K > 0 */
-  uint32_t flags;         /* ARGUS_OUT_* / ARGUS_FORCE_FULL_SORT */
+  uint32_t flags;         /* ARGUS_OUT_* / ARGUS_FORCE_* */
   uint64_t max_records;   /* capacity this handle is planned for, < 2^31 */
   const uint8_t* d_region_class; /* device [R]; class of each region, >= K means
                                     unclassified; caller-owned; may be NULL iff K == 0 */

@@ -15,7 +15,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libargus_attr.so")
-SOURCES = ["attr_host.hip", "k_ingest.hip", "k_radix.hip", "k_match.hip", "k_resolve.hip",
+SOURCES = ["attr_host.hip", "k_ingest.hip", "k_radix.hip", "k_match.hip", "k_resolve.hip", "k_merge.hip",
            "k_agg.hip", "k_overlap.hip"]
 ARCH = "gfx950"
 

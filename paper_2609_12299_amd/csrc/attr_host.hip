@@ -51,8 +51,9 @@ struct Layout {
   size_t key[2], pay[2], ctxw[2], lb[2], mlb, slb, tiles, tree;
   size_t pop_ts, pop_reg, pushes, op_parent, op_sum;
   size_t inst, child_sum, hist_key, ov_mask, ov_q;
+  size_t push_pos, pop_pos, ctx_list, ctx_seg, seg_start, seg_split, seg_tile0, part, part_seg;
   size_t total;
-  uint64_t lb_words, tree_leaves, match_tiles, pool_cap;
+  uint64_t lb_words, tree_leaves, match_tiles, pool_cap, ctx_cap, tiles_cap;
 };
 
 Layout make_layout(const argus_attr_config& c, uint64_t n, bool own_instances) {
@@ -98,6 +99,19 @@ Layout make_layout(const argus_attr_config& c, uint64_t n, bool own_instances) {
   const uint64_t G = c.num_classes ? c.num_groups : 0;
   L.ov_mask = take(sizeof(uint64_t) * kMasks * (G ? G : 1));
   L.ov_q = take(sizeof(uint64_t) * kQPairs * (G ? G : 1));
+  // merge path of the overlap events
+  const bool ev = c.num_classes > 0;
+  L.ctx_cap = ev ? (nn < kCtxCap ? nn : kCtxCap) : 0;
+  L.tiles_cap = ev ? ceil_div(nn, kMergeTile) + L.ctx_cap : 0;
+  L.push_pos = take(ev ? sizeof(uint32_t) * L.pool_cap : 0);
+  L.pop_pos = take(ev ? sizeof(uint32_t) * L.pool_cap : 0);
+  L.ctx_list = take(sizeof(uint2) * L.ctx_cap);
+  L.ctx_seg = take(sizeof(uint32_t) * L.ctx_cap);
+  L.seg_start = take(sizeof(uint32_t) * (L.ctx_cap + 1));
+  L.seg_split = take(sizeof(uint32_t) * (L.ctx_cap + 1));
+  L.seg_tile0 = take(sizeof(uint32_t) * (L.ctx_cap + 1));
+  L.part = take(sizeof(uint32_t) * (L.tiles_cap + 1));
+  L.part_seg = take(sizeof(uint32_t) * (L.tiles_cap + 1));
   L.total = o;
   return L;
 }
@@ -121,7 +135,7 @@ int check_config(const argus_attr_config* c, std::string* why) {
     if (c->num_groups < 1 || c->num_groups > (1u << 20)) { *why = "num_groups must be 1..2^20 when num_classes > 0"; return ARGUS_E_INVAL; }
     if (!c->d_region_class) { *why = "d_region_class is NULL while num_classes > 0"; return ARGUS_E_INVAL; }
   }
-  if (c->flags & ~7u) { *why = "unknown flag bits"; return ARGUS_E_INVAL; }
+  if (c->flags & ~15u) { *why = "unknown flag bits"; return ARGUS_E_INVAL; }
   if (c->max_records >= (1ull << 31)) { *why = "max_records must be < 2^31"; return ARGUS_E_CAPACITY; }
   return ARGUS_OK;
 }
@@ -263,6 +277,17 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
   w.hist_key = (uint32_t*)(base + L.hist_key);
   w.ov_mask = (uint64_t*)(base + L.ov_mask);
   w.ov_q = (uint64_t*)(base + L.ov_q);
+  w.push_pos = (uint32_t*)(base + L.push_pos);
+  w.pop_pos = (uint32_t*)(base + L.pop_pos);
+  w.ctx_list = (uint2*)(base + L.ctx_list);
+  w.ctx_seg = (uint32_t*)(base + L.ctx_seg);
+  w.seg_start = (uint32_t*)(base + L.seg_start);
+  w.seg_split = (uint32_t*)(base + L.seg_split);
+  w.seg_tile0 = (uint32_t*)(base + L.seg_tile0);
+  w.part = (uint32_t*)(base + L.part);
+  w.part_seg = (uint32_t*)(base + L.part_seg);
+  w.ctx_cap = L.ctx_cap;
+  w.tiles_cap = L.tiles_cap;
   w.lb_words = L.lb_words;
   w.tree_leaves = L.tree_leaves;
   w.match_tiles = L.match_tiles;
@@ -320,6 +345,7 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
   if (!step("match", launch_match(a, s))) return ARGUS_E_HIP;
   if (!step("tree", launch_tree(a, s))) return ARGUS_E_HIP;
   if (!step("resolve", launch_resolve(a, s))) return ARGUS_E_HIP;
+  if (a.K > 0 && !step("merge_plan", launch_mplan(a, s))) return ARGUS_E_HIP;
   if (!step("agg", launch_agg(a, s))) return ARGUS_E_HIP;
   if (!step("hist", launch_hist(a, s))) return ARGUS_E_HIP;
   if (a.K > 0) {
@@ -331,6 +357,18 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
     if (!step("ev_clear", launch_ev_clear(a, s))) return ARGUS_E_HIP;
     for (int sl = 0; sl < 12; ++sl)
       if (!step(enames[sl], launch_radix_pass(a, 1, sl, 2 * n, s))) return ARGUS_E_HIP;
+    // Merge rounds (device-planned; a round beyond the plan returns at once).
+    static const char* mnames[kMaxMergeRounds][3] = {
+        {"mseg0", "mpart0", "merge0"}, {"mseg1", "mpart1", "merge1"},
+        {"mseg2", "mpart2", "merge2"}, {"mseg3", "mpart3", "merge3"},
+        {"mseg4", "mpart4", "merge4"}, {"mseg5", "mpart5", "merge5"},
+        {"mseg6", "mpart6", "merge6"}, {"mseg7", "mpart7", "merge7"}};
+    const int rounds = a.shift < (uint32_t)kMaxMergeRounds ? (int)a.shift : kMaxMergeRounds;
+    for (int r = 0; r < rounds; ++r) {
+      if (!step(mnames[r][0], launch_mseg(a, r, s))) return ARGUS_E_HIP;
+      if (!step(mnames[r][1], launch_mpart(a, r, s))) return ARGUS_E_HIP;
+      if (!step(mnames[r][2], launch_merge(a, r, s))) return ARGUS_E_HIP;
+    }
     if (!step("sweep", launch_sweep(a, s))) return ARGUS_E_HIP;
     if (!step("ov_final", launch_ov_final(a, s))) return ARGUS_E_HIP;
   }

@@ -31,6 +31,14 @@ constexpr int kSweepItems = 8;
 constexpr int kSweepTile = kSweepThreads * kSweepItems;  // 2048 events
 constexpr int kSweepSlots = 8;  // groups of one tile aggregated in LDS
 
+// Ordering overlap events by merging per-context runs (see k_merge.hip).
+constexpr int kMergeThreads = 512;
+constexpr int kMergeItems = 8;
+constexpr int kMergeTile = kMergeThreads * kMergeItems;  // 4096 events
+constexpr int kMaxMergeRounds = 8;
+constexpr uint64_t kCtxCap = 1ull << 20;  // contexts the merge path handles
+constexpr int kEvCodeBits = 5;           // event code: 0 none, 1 + 2 * class + is_end
+
 constexpr int kMaxClasses = 8;
 constexpr int kQPairs = kMaxClasses * (kMaxClasses + 1) / 2;  // 36
 constexpr int kMasks = 1 << kMaxClasses;                      // 256
@@ -67,6 +75,15 @@ struct SlotPlan {
   uint64_t tiles;
 };
 
+struct MergeRound {
+  uint32_t bit;  // context bit merged in this round
+  uint32_t src;  // event buffer read (0/1)
+  uint32_t dst;  // event buffer written
+  uint32_t pad;
+  uint64_t n_segs;
+  uint64_t n_tiles;
+};
+
 // Written on the device by the planning kernels; read by everything else.
 struct DevPlan {
   // ingest
@@ -87,6 +104,13 @@ struct DevPlan {
   SlotPlan es[kSlots];   // event sort
   // matching
   uint64_t match_tiles;
+  // overlap events ordered by merging per-context runs
+  uint32_t ev_merge;   // 1: merge path chosen (else the event radix sort)
+  uint32_t m_need;     // bit b: two contexts of one group first differ in bit b
+  uint32_t m_rounds;   // merge rounds (set bits of m_need)
+  uint32_t m_nctx;     // contexts of groups < G (a prefix of the context list)
+  uint64_t m_end;      // sorted position where groups >= G start (or n_valid)
+  MergeRound mr[kMaxMergeRounds];
 };
 
 // The Python binding reads the plan back for measurement; keep its layout.
@@ -96,7 +120,11 @@ static_assert(offsetof(DevPlan, unsorted) == 104, "DevPlan layout");
 static_assert(offsetof(DevPlan, n_ev) == 128, "DevPlan layout");
 static_assert(offsetof(DevPlan, rs) == 144, "DevPlan layout");
 static_assert(offsetof(DevPlan, es) == 784, "DevPlan layout");
-static_assert(sizeof(DevPlan) == 1432, "DevPlan layout");
+static_assert(offsetof(DevPlan, ev_merge) == 1432, "DevPlan layout");
+static_assert(offsetof(DevPlan, m_end) == 1448, "DevPlan layout");
+static_assert(sizeof(MergeRound) == 32, "MergeRound layout");
+static_assert(offsetof(DevPlan, mr) == 1456, "DevPlan layout");
+static_assert(sizeof(DevPlan) == 1712, "DevPlan layout");
 
 // Per-tile summary written by the matching kernel, read by the resolver.
 struct TileDesc {
@@ -141,6 +169,17 @@ struct Work {
   uint32_t* hist_key;   // [n_begin]
   uint64_t* ov_mask;    // [G][256]
   uint64_t* ov_q;       // [G][36]
+  uint32_t* push_pos;   // sorted position of each pushed BEGIN (pool layout)
+  uint32_t* pop_pos;    // sorted position of each popping END (pool layout)
+  uint2* ctx_list;      // [ctx_cap] (context key, first sorted position)
+  uint32_t* ctx_seg;    // [ctx_cap] segment of each context (merge round)
+  uint32_t* seg_start;  // [ctx_cap + 1]
+  uint32_t* seg_split;  // [ctx_cap + 1]
+  uint32_t* seg_tile0;  // [ctx_cap + 1] first merge tile of each segment
+  uint32_t* part;       // [tiles_cap + 1] events taken from the first run before each tile
+  uint32_t* part_seg;   // [tiles_cap] segment of each tile
+  uint64_t ctx_cap;
+  uint64_t tiles_cap;
   uint64_t lb_words;    // capacity of each lb array in words
   uint64_t tree_leaves; // power of two >= max match tiles
   uint64_t match_tiles; // upper bound (from n_records)
@@ -164,6 +203,7 @@ enum CtrSlot {
   kCtrEv = 16,     // 16 event passes
   kCtrMatch = 32,
   kCtrSweep = 33,
+  kCtrMerge = 34,  // 8 merge rounds
   kCtrCount = 64
 };
 
@@ -218,6 +258,10 @@ hipError_t launch_agg(const RunArgs& a, hipStream_t s);
 hipError_t launch_hist(const RunArgs& a, hipStream_t s);
 hipError_t launch_ev_plan(const RunArgs& a, hipStream_t s);
 hipError_t launch_ev_clear(const RunArgs& a, hipStream_t s);
+hipError_t launch_mplan(const RunArgs& a, hipStream_t s);
+hipError_t launch_mseg(const RunArgs& a, int round, hipStream_t s);
+hipError_t launch_mpart(const RunArgs& a, int round, hipStream_t s);
+hipError_t launch_merge(const RunArgs& a, int round, hipStream_t s);
 hipError_t launch_sweep(const RunArgs& a, hipStream_t s);
 hipError_t launch_ov_final(const RunArgs& a, hipStream_t s);
 

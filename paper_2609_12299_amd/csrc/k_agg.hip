@@ -103,7 +103,9 @@ __global__ __launch_bounds__(512) void k_agg(AggArgs a) {
   }
   if (a.hist_lds)
     for (uint32_t i = threadIdx.x; i < RL * 130; i += NT) s_hist[i] = 0;
-  if (a.K)
+  // Events for the radix sort only: the merge path needs no histograms.
+  const bool evk = a.K && !a.plan->ev_merge;
+  if (evk)
     for (uint32_t i = threadIdx.x; i < kDigitPositions * kRadixBins; i += NT) s_evh[i] = 0;
   __syncthreads();
 
@@ -111,7 +113,7 @@ __global__ __launch_bounds__(512) void k_agg(AggArgs a) {
   // Overlap-event digits that can vary: group digits below the width of
   // G - 1, timestamp digits above which ts_min and ts_max differ.
   uint32_t vary = 0;
-  if (a.K) {
+  if (evk) {
     const uint64_t ts_lo = a.plan->rec.ts_min;
     const uint64_t ts_hi = ts_lo + a.plan->rec.ts_mask;
     const bool full_ts = a.plan->rec.ts_bits >= 64 || ts_hi < ts_lo;
@@ -203,7 +205,7 @@ __global__ __launch_bounds__(512) void k_agg(AggArgs a) {
     }
     if (a.hist_key) a.hist_key[id] = hk;
     }
-    if (a.K) {
+    if (evk) {
 #pragma unroll
       for (int d = 0; d < 4; ++d)
         if ((vary >> d) & 1u) {
@@ -244,9 +246,9 @@ __global__ __launch_bounds__(512) void k_agg(AggArgs a) {
                     : threadIdx.x == 3 ? ARGUS_C_N_SELF_NESTED
                                        : ARGUS_C_N_OVERLAP_SKIPPED;
     if (v && threadIdx.x < 5) atomicAdd((unsigned long long*)&a.counters[idx], (unsigned long long)v);
-    if (v && threadIdx.x == 5) atomicAdd((unsigned long long*)&a.wplan->n_ev, (unsigned long long)v);
+    if (v && threadIdx.x == 5 && evk) atomicAdd((unsigned long long*)&a.wplan->n_ev, (unsigned long long)v);
   }
-  if (a.K)
+  if (evk)
     for (uint32_t i = threadIdx.x; i < kDigitPositions * kRadixBins; i += NT)
       if (s_evh[i]) atomicAdd(&a.ev_hist[i], s_evh[i]);
   for (uint32_t r = threadIdx.x; r < RL; r += NT) {
@@ -406,6 +408,7 @@ __global__ __launch_bounds__(256) void k_ev_plan(EvPlanArgs a) {
   __shared__ uint32_t s_active[kDigitPositions];
   DevPlan* p = a.plan;
   const int t = threadIdx.x;
+  if (p->ev_merge) return;  // events are merged, not sorted (all slots stay inactive)
   for (int pos = 0; pos < kDigitPositions; ++pos) {
     const uint32_t h = a.hist[pos * kRadixBins + t];
     const int used = __syncthreads_count(h != 0);
@@ -468,6 +471,7 @@ struct EvClearArgs {
 
 // Clears the look-back status the first event pass uses.
 __global__ __launch_bounds__(256) void k_ev_clear(EvClearArgs a) {
+  if (a.plan->ev_merge) return;
   const uint64_t words = ceil_div(a.plan->ev_slots, kSortTile) * kRadixBins;
   const uint64_t stride = (uint64_t)gridDim.x * 256;
   for (uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x; i < words; i += stride) a.lb0[i] = 0;

@@ -69,17 +69,18 @@ __device__ __forceinline__ Fn shfl_fn(const Fn& f, int src) {
   return r;
 }
 
-// Tile aggregate in one status word: reset (1 bit), a + 2048 (13 bits),
-// c (12 bits), number of BEGINs (12 bits).
-__device__ __forceinline__ uint64_t pack_agg(const Fn& f, uint32_t nb) {
-  return kFlagAgg | ((uint64_t)f.reset << 40) | ((uint64_t)(f.a + 2048) << 24) |
-         ((uint64_t)f.c << 12) | (uint64_t)nb;
+// Tile aggregate in one status word: number of BEGINs (12 bits), c (12
+// bits), a + 2048 (13 bits), reset (1 bit), number of context starts (12
+// bits).  BEGIN and start counts travel packed as nb | starts << 16.
+__device__ __forceinline__ uint64_t pack_agg(const Fn& f, uint32_t nbh) {
+  return kFlagAgg | ((uint64_t)(nbh >> 16) << 41) | ((uint64_t)f.reset << 40) |
+         ((uint64_t)(f.a + 2048) << 24) | ((uint64_t)f.c << 12) | (uint64_t)(nbh & 0xFFFFu);
 }
-__device__ __forceinline__ void unpack_agg(uint64_t v, Fn* f, uint32_t* nb) {
+__device__ __forceinline__ void unpack_agg(uint64_t v, Fn* f, uint32_t* nbh) {
   f->reset = (uint32_t)(v >> 40) & 1u;
   f->a = (int64_t)((v >> 24) & 0x1FFFull) - 2048;
   f->c = (int64_t)((v >> 12) & 0xFFFull);
-  *nb = (uint32_t)(v & 0xFFFull);
+  *nbh = (uint32_t)(v & 0xFFFull) | ((uint32_t)((v >> 41) & 0xFFFull) << 16);
 }
 
 // Min tree over the tile's 2048 leaves with fan-out 8, in LDS:
@@ -126,6 +127,7 @@ __device__ __forceinline__ int psv8(const uint32_t* t, uint32_t chunk, uint32_t 
 
 struct MatchArgs {
   const DevPlan* plan;
+  DevPlan* wplan;
   const uint64_t* key[2];
   const uint32_t* pay[2];
   const uint32_t* ctxw[2];
@@ -140,6 +142,14 @@ struct MatchArgs {
   uint64_t* counters;
   uint64_t* rstats;
   uint32_t* tile_ctr;
+  // overlap events in sorted-record order (merge path)
+  uint64_t* ev[2];
+  const uint8_t* region_class;
+  uint32_t K, G, shift;
+  uint32_t* push_pos;
+  uint32_t* pop_pos;
+  uint2* ctx_list;
+  uint64_t ctx_cap;
 };
 
 constexpr uint32_t kParNone = 0xFFFFFFFFu;
@@ -156,12 +166,13 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   __shared__ uint64_t s_cs[kMatchTile];        // child sums of each local BEGIN
   __shared__ uint16_t s_lbr[kMatchTile];       // local BEGIN rank of each position
   __shared__ uint16_t s_ereg[kMatchTile];      // end region of each local BEGIN (0xFFFF: open)
+  __shared__ uint16_t s_breg[kMatchTile];      // region of each local BEGIN
   __shared__ uint32_t s_lastctx[kMatchThreads];
   __shared__ Fn s_wfn[4];
   __shared__ uint32_t s_wnb[4];
   __shared__ uint32_t s_prevctx, s_hasprev;
   __shared__ uint32_t s_first, s_lastp1, s_heads, s_lo, s_sout, s_maxlvl, s_orph;
-  __shared__ uint32_t s_sin, s_nbpre_lo, s_nbpre_hi;
+  __shared__ uint32_t s_sin, s_nbpre_lo, s_nbpre_hi, s_hpre, s_need;
   uint64_t* s_oc = (uint64_t*)s_tree;
 
   const KeySpace ks = P->rec;
@@ -174,6 +185,20 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   auto ctx_of_key = [&](uint64_t k) -> uint32_t {
     return ks.ts_bits >= 64 ? 0u : (uint32_t)(k >> ks.ts_bits);
   };
+  // Overlap events in sorted-record order: one word per record,
+  // group << (ts_bits + 5) | ts_off << 5 | code, code = 0 for a record that
+  // is no event, else 1 + 2 * class + is_end.
+  const uint32_t g_bits = a.G > 1 ? bit_width64(a.G - 1) : 0u;
+  const bool ev_on = a.K > 0 && ks.ts_bits + g_bits + kEvCodeBits <= 64;
+  const uint32_t es = ks.ts_bits + kEvCodeBits;
+  uint64_t* evo = a.ev[buf ^ 1u];
+  auto group_of = [&](uint32_t raw_ctx) -> uint32_t {
+    return a.shift >= 32 ? 0u : (raw_ctx >> a.shift);
+  };
+  auto ev_code = [&](uint32_t region, uint32_t raw_ctx, uint32_t is_end) -> uint32_t {
+    const uint32_t cls = a.region_class[region];
+    return (cls < a.K && group_of(raw_ctx) < a.G) ? 1u + 2u * cls + is_end : 0u;
+  };
 
   for (;;) {
   if (tid == 0) {
@@ -184,6 +209,7 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
     s_lo = 0xFFFFFFFFu;
     s_maxlvl = 0;
     s_orph = 0;
+    s_need = 0;
   }
   __syncthreads();
   const uint64_t tile = s_tile;
@@ -279,9 +305,10 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
     atomicAdd(&s_heads, nheads);
   }
 
-  // ---- block exclusive scan of the per-thread maps and BEGIN counts
+  // ---- block exclusive scan of the per-thread maps, BEGIN counts and
+  // context-start counts (packed as nb | starts << 16)
   Fn x = f;
-  uint32_t nbx = nb;
+  uint32_t nbx = nb | (nheads << 16);
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) {
     const Fn y = shfl_up_fn(x, o);
@@ -309,7 +336,9 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
     pnb += s_wnb[k];
   }
   const Fn tfn = compose(pre, ex);  // map from tile input to this thread's input
-  const uint32_t tnb = pnb + nbex;  // BEGINs of the tile before this thread
+  const uint32_t tnbh = pnb + nbex;
+  const uint32_t tnb = tnbh & 0xFFFFu;  // BEGINs of the tile before this thread
+  const uint32_t thd = tnbh >> 16;      // context starts of the tile before this thread
 
   // ---- decoupled look-back: depth entering the tile, BEGINs before it.
   // Wave 0 inspects 64 predecessor tiles per round trip (lane j: the j-th
@@ -322,23 +351,25 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
       all = compose(all, s_wfn[k]);
       nball += s_wnb[k];
     }
-    uint64_t s_in = 0, nbpre = 0;
+    uint64_t s_in = 0, nbpre = 0, hpre = 0;
     uint64_t* lb = a.mlb;
     if (tile > 0) {
       if (lane == 0) st_agent(&lb[tile * 4], pack_agg(all, nball));
       Fn acc = fn_id();
-      uint64_t nb_acc = 0;
+      uint64_t nb_acc = 0, h_acc = 0;
       int64_t top = (int64_t)tile - 1;  // nearest tile not yet folded in
       uint32_t spins = 0;
       for (;;) {
         const int64_t tt = top - lane;
-        uint64_t w0 = 0, w1 = 0, w2 = 0;
+        uint64_t w0 = 0, w1 = 0, w2 = 0, w3 = 0;
         if (tt >= 0) {
           w1 = ld_agent(&lb[tt * 4 + 1]);
           w2 = ld_agent(&lb[tt * 4 + 2]);
+          w3 = ld_agent(&lb[tt * 4 + 3]);
           w0 = ld_agent(&lb[tt * 4]);
         }
-        const bool incl = (w1 & ~kValMask) == kFlagIncl && (w2 & ~kValMask) == kFlagIncl;
+        const bool incl = (w1 & ~kValMask) == kFlagIncl && (w2 & ~kValMask) == kFlagIncl &&
+                          (w3 & ~kValMask) == kFlagIncl;
         const bool agg = (w0 & ~kValMask) == kFlagAgg;
         const uint64_t mi = __ballot(incl), mn = __ballot(!incl && !agg);
         const int ji = mi ? __ffsll((unsigned long long)mi) - 1 : 64;
@@ -346,24 +377,32 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
         const bool done = ji < jn;
         const int k = done ? ji : jn;  // lanes [0, k) hold aggregates to fold in
         Fn x = fn_id();
-        uint32_t nx = 0;
-        if (lane < k) unpack_agg(w0, &x, &nx);
+        uint32_t nx = 0, hx = 0;  // BEGINs, context starts
+        if (lane < k) {
+          uint32_t nbh;
+          unpack_agg(w0, &x, &nbh);
+          nx = nbh & 0xFFFFu;
+          hx = nbh >> 16;
+        }
         // reduce towards lane 0; a higher lane is an earlier tile
 #pragma unroll
         for (int o = 1; o < 64; o <<= 1) {
           const Fn y = shfl_down_fn(x, o);
-          const uint32_t ny = __shfl_down(nx, o);
+          const uint32_t ny = __shfl_down(nx, o), hy = __shfl_down(hx, o);
           if (lane + o < 64) {
             x = compose(y, x);
             nx += ny;
+            hx += hy;
           }
         }
         acc = compose(shfl_fn(x, 0), acc);
         nb_acc += (uint32_t)__shfl(nx, 0);
+        h_acc += (uint32_t)__shfl(hx, 0);
         if (done) {
-          const uint64_t v1 = __shfl(w1, ji), v2 = __shfl(w2, ji);
+          const uint64_t v1 = __shfl(w1, ji), v2 = __shfl(w2, ji), v3 = __shfl(w3, ji);
           s_in = (uint64_t)apply(acc, (int64_t)(v1 & kValMask));
           nbpre = (v2 & kValMask) + nb_acc;
+          hpre = (v3 & kValMask) + h_acc;
           break;
         }
         top -= k;
@@ -379,8 +418,10 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
     if (lane == 0) {
       const uint64_t s_out = (uint64_t)apply(all, (int64_t)s_in);
       st_agent(&lb[tile * 4 + 1], kFlagIncl | s_out);
-      st_agent(&lb[tile * 4 + 2], kFlagIncl | (nbpre + nball));
+      st_agent(&lb[tile * 4 + 2], kFlagIncl | (nbpre + (nball & 0xFFFFu)));
+      st_agent(&lb[tile * 4 + 3], kFlagIncl | (hpre + (nball >> 16)));
       s_sin = (uint32_t)s_in;
+      s_hpre = (uint32_t)hpre;
       s_nbpre_lo = (uint32_t)nbpre;
       s_nbpre_hi = (uint32_t)(nbpre >> 32);
     }
@@ -391,6 +432,26 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   const uint64_t nbpre = (uint64_t)s_nbpre_lo | ((uint64_t)s_nbpre_hi << 32);
   const uint32_t first = s_first, lastp1 = s_lastp1;
   const bool first_is_head = first == 0;
+
+  // ---- context list (key and first sorted position of every context, in
+  // order) and the bits in which neighbouring contexts of one group first
+  // differ: the merge rounds that ordering the overlap events needs
+  if (ev_on && fh) {
+    uint32_t ord = s_hpre + thd, need = 0;
+#pragma unroll
+    for (int i = 0; i < IT; ++i) {
+      if (!((fh >> i) & 1u)) continue;
+      const uint32_t c1 = ctxr[i] + (uint32_t)ks.ctx_min;
+      if (ord < a.ctx_cap) a.ctx_list[ord] = make_uint2(c1, (uint32_t)(base + p0 + i));
+      ++ord;
+      if (i > 0 || has_prev0) {
+        const uint32_t c0 = (i > 0 ? ctxr[i - 1] : prev0) + (uint32_t)ks.ctx_min;
+        const uint32_t hb = 31u - (uint32_t)__clz(c0 ^ c1);
+        if (hb < a.shift && group_of(c1) < a.G) need |= 1u << hb;
+      }
+    }
+    if (need) atomicOr(&s_need, need);
+  }
 
   // ---- depths (before: sb, after: sa), leaves x + 1 and the lower tree levels
   uint32_t sb[IT], sa[IT], xp[IT];
@@ -458,7 +519,10 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   }
 #pragma unroll
   for (int i = 0; i < IT; ++i)
-    if ((fb >> i) & 1u) s_lbr[p0 + i] = (uint16_t)lbr[i];
+    if ((fb >> i) & 1u) {
+      s_lbr[p0 + i] = (uint16_t)lbr[i];
+      s_breg[lbr[i]] = (uint16_t)reg[i];
+    }
   if (lo != 0xFFFFFFFFu) atomicMin(&s_lo, lo);
   if (maxlvl) atomicMax(&s_maxlvl, maxlvl);
   if (norph) atomicAdd(&s_orph, norph);
@@ -479,10 +543,11 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   // x + 1 <= L (its parent).  This thread's own records are scanned in
   // registers first; the tree is climbed from the thread's first record only
   // when the answer lies further back.
-  uint32_t par[IT];
+  uint32_t par[IT], code[IT];
 #pragma unroll
   for (int i = 0; i < IT; ++i) {
     par[i] = kParNone;
+    code[i] = 0;
     if (!((fv >> i) & 1u)) continue;
     const bool isb = (fb >> i) & 1u;
     if (!isb && sb[i] == 0) continue;  // orphan END: no search
@@ -510,6 +575,8 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
       if (found) {
         s_tend[qrank] = ts[i];
         s_ereg[qrank] = (uint16_t)reg[i];
+        if (ev_on && s_breg[qrank] == reg[i])
+          code[i] = ev_code(reg[i], ctxr[i] + (uint32_t)ks.ctx_min, 1u);
       } else {
         // pops a level that was open when the tile started
         const uint32_t L = sa[i];
@@ -517,6 +584,7 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
         if (L >= lo_head && idx < (uint32_t)kMatchTile) {
           a.pop_ts[pool + idx] = ts[i];
           a.pop_reg[pool + idx] = reg[i];
+          if (ev_on) a.pop_pos[pool + idx] = (uint32_t)(base + p0 + i);
         } else {
           flag_internal_error(a.counters, 16);
         }
@@ -541,6 +609,7 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
     uint64_t t_end = kU64Max;
     if (ereg != kNoEnd) {
       t_end = s_tend[k];
+      if (ev_on && ereg == reg[i]) code[i] = ev_code(reg[i], ctxr[i] + (uint32_t)ks.ctx_min, 0u);
       const uint64_t incl = t_end - ts[i];
       if (par[i] == kParOut) {
         const uint32_t oi = (L - 1) - op_lo;
@@ -553,9 +622,10 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
       }
     } else if (lastp1 <= p + 1) {
       // still open when the tile ends, in a context that may continue
-      if (L >= lo_tail && L - lo_tail < (uint32_t)kMatchTile)
+      if (L >= lo_tail && L - lo_tail < (uint32_t)kMatchTile) {
         a.pushes[pool + (L - lo_tail)] = (uint32_t)id;
-      else
+        if (ev_on) a.push_pos[pool + (L - lo_tail)] = (uint32_t)p + (uint32_t)base;
+      } else
         flag_internal_error(a.counters, 16);
     }
     uint32_t pf;
@@ -567,10 +637,29 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
                         (uint32_t)(t_end >> 32));
     dst[1] = make_uint4(ctxr[i] + (uint32_t)ks.ctx_min, pf, L, reg[i] | (ereg << 16));
   }
+  if (ev_on) {
+    uint64_t e[IT];
+#pragma unroll
+    for (int i = 0; i < IT; ++i) {
+      const uint64_t g = group_of(ctxr[i] + (uint32_t)ks.ctx_min);
+      e[i] = (es < 64 ? (g << es) : 0ull) | ((ts[i] - ks.ts_min) << kEvCodeBits) | code[i];
+    }
+    if (p0 + IT <= cnt) {
+      uint4* e4 = (uint4*)(evo + base + p0);
+#pragma unroll
+      for (int q = 0; q < IT / 2; ++q)
+        e4[q] = make_uint4((uint32_t)e[2 * q], (uint32_t)(e[2 * q] >> 32), (uint32_t)e[2 * q + 1],
+                           (uint32_t)(e[2 * q + 1] >> 32));
+    } else {
+#pragma unroll
+      for (int i = 0; i < IT; ++i)
+        if (p0 + i < cnt) evo[base + p0 + i] = e[i];
+    }
+  }
   __syncthreads();
 
   // ---- per-tile outputs
-  const uint32_t tile_nb = s_wnb[0] + s_wnb[1] + s_wnb[2] + s_wnb[3];
+  const uint32_t tile_nb = (s_wnb[0] + s_wnb[1] + s_wnb[2] + s_wnb[3]) & 0xFFFFu;
   for (uint32_t k = tid; k < tile_nb; k += kMatchThreads) a.child_sum[nbpre + k] = s_cs[k];
   const uint32_t n_op = (sin_eff > op_lo) ? ((sin_eff - op_lo) < (uint32_t)kMatchTile ? sin_eff - op_lo : (uint32_t)kMatchTile) : 0u;
   for (uint32_t k = tid; k < n_op; k += kMatchThreads) a.op_sum[pool + k] = s_oc[k];
@@ -597,6 +686,7 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
     d.pad = 0;
     a.tiles[tile] = d;
     unsigned long long* c = (unsigned long long*)a.counters;
+    if (s_need) atomicOr(&a.wplan->m_need, s_need);
     if (s_heads) atomicAdd(&c[ARGUS_C_N_CTX], (unsigned long long)s_heads);
     if (s_maxlvl) atomicMax(&c[ARGUS_C_MAX_LEVEL], (unsigned long long)s_maxlvl);
     if (s_orph) atomicAdd(&c[ARGUS_C_N_ORPHAN_END], (unsigned long long)s_orph);
@@ -608,6 +698,16 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
 hipError_t launch_match(const RunArgs& a, hipStream_t s) {
   MatchArgs m{};
   m.plan = a.w.plan;
+  m.wplan = a.w.plan;
+  for (int b = 0; b < 2; ++b) m.ev[b] = a.w.key[b];
+  m.region_class = a.region_class;
+  m.K = a.K;
+  m.G = a.G;
+  m.shift = a.shift;
+  m.push_pos = a.w.push_pos;
+  m.pop_pos = a.w.pop_pos;
+  m.ctx_list = a.w.ctx_list;
+  m.ctx_cap = a.w.ctx_cap;
   for (int b = 0; b < 2; ++b) {
     m.key[b] = a.w.key[b];
     m.pay[b] = a.w.pay[b];

@@ -8,7 +8,10 @@
 //   Q[A][B] = sum over pairs of distinct instances, one of class A and one
 //             of class B (unordered pairs when A == B), of their intersection.
 // Events (t_begin, +1, class) and (t_end, -1, class) of matched, classified
-// instances are sorted by (group, time) beforehand (k_radix).  This kernel
+// instances are put in (group, time) order beforehand, either by merging the
+// per-context runs of the sorted records (k_merge: one word per record,
+// group | time | code) or by a radix sort of (group, time) keys with a class
+// payload (k_radix).  This kernel
 // scans the per-class active counts c (segmented by group, decoupled
 // look-back across tiles) and, for each gap between consecutive events of a
 // group, adds gap * [c_A > 0 and c_B > 0] to U and gap * c_A * c_B (or
@@ -80,14 +83,23 @@ __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
     return wide ? cw : (ks.ts_bits >= 64 ? 0u : (uint32_t)(k >> ks.ts_bits));
   };
   auto tof = [&](uint64_t k) -> uint64_t { return wide ? k : (k & ks.ts_mask); };
+  // Merged event words: key = word >> 5; code 0 (no event) gets a class
+  // that matches no counter.
+  const bool mfmt = P->ev_merge != 0;
+  auto key_at = [&](uint64_t i) -> uint64_t { return mfmt ? gk[i] >> kEvCodeBits : gk[i]; };
+  auto pay_at = [&](uint64_t i) -> uint32_t {
+    if (!mfmt) return gp[i];
+    const uint32_t c = (uint32_t)(gk[i] & ((1u << kEvCodeBits) - 1u));
+    return c ? ((c - 1u) >> 1) | (((c - 1u) & 1u) << 8) : 0xFFu;
+  };
 
   for (int j = 0; j < kSweepItems; ++j) {
     const uint32_t i = (uint32_t)j * kSweepThreads + tid;
     if (i < cnt) {
-      const uint64_t k = gk[base + i];
+      const uint64_t k = key_at(base + i);
       s_t[i] = tof(k);
       s_g[i] = grp(k, wide ? gc[base + i] : 0u);
-      s_pay[i] = gp[base + i];
+      s_pay[i] = pay_at(base + i);
     }
   }
   for (int i = tid; i < kSweepSlots * NP; i += kSweepThreads) {
@@ -96,10 +108,10 @@ __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
   }
   if (tid == 0) {
     s_has_prev = base > 0;
-    s_prev_g = base > 0 ? grp(gk[base - 1], wide ? gc[base - 1] : 0u) : 0u;
+    s_prev_g = base > 0 ? grp(key_at(base - 1), wide ? gc[base - 1] : 0u) : 0u;
     s_has_next = base + cnt < n;
     if (base + cnt < n) {
-      const uint64_t k = gk[base + cnt];
+      const uint64_t k = key_at(base + cnt);
       s_next_g = grp(k, wide ? gc[base + cnt] : 0u);
       s_next_t = tof(k);
     }

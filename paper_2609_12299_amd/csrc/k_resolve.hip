@@ -126,6 +126,12 @@ struct ResolveArgs {
   argus_instance* inst;
   uint64_t* child_sum;
   uint64_t* counters;
+  // overlap events of pairs matched across tiles (merge path)
+  uint64_t* ev[2];
+  const uint32_t* push_pos;
+  const uint32_t* pop_pos;
+  const uint8_t* region_class;
+  uint32_t K, G, shift;
 };
 
 // Instance open at level L when tile t starts.  (Such a tile always exists
@@ -147,6 +153,12 @@ __global__ __launch_bounds__(256) void k_resolve(ResolveArgs a) {
   const TileDesc d = a.tiles[t];
   const uint64_t pool = t * kMatchTile;
   const uint64_t nb = a.plan->n_begin;
+  const uint64_t nv = a.plan->n_valid;
+  const KeySpace ks = a.plan->rec;
+  const uint32_t g_bits = a.G > 1 ? bit_width64(a.G - 1) : 0u;
+  const bool ev_on = a.K > 0 && ks.ts_bits + g_bits + kEvCodeBits <= 64;
+  const uint32_t es = ks.ts_bits + kEvCodeBits;
+  uint64_t* evo = a.ev[a.plan->rec_final ^ 1u];
   // BEGINs still open at the end of tile t.
   for (uint32_t i = lane; i < d.n_push; i += 64) {
     const uint32_t L = d.lo_tail + i;
@@ -165,7 +177,23 @@ __global__ __launch_bounds__(256) void k_resolve(ResolveArgs a) {
     argus_instance* x = a.inst + id;
     x->t_end = t_end;
     x->end_region_id = (uint16_t)ereg;
-    const uint64_t incl = t_end - x->t_begin;
+    const uint64_t t_begin = x->t_begin;
+    const uint64_t incl = t_end - t_begin;
+    if (ev_on && ereg == x->region_id) {
+      // both events of a classified instance of a group < G
+      const uint32_t cls = a.region_class[ereg];
+      const uint64_t g = a.shift >= 32 ? 0u : (x->ctx_key >> a.shift);
+      const uint32_t pb = a.push_pos[pool + i], pe = a.pop_pos[q];
+      if (cls < a.K && g < a.G) {
+        if (pb < nv && pe < nv) {
+          const uint64_t hi = es < 64 ? (g << es) : 0ull;
+          evo[pb] = hi | ((t_begin - ks.ts_min) << kEvCodeBits) | (1u + 2u * cls);
+          evo[pe] = hi | ((t_end - ks.ts_min) << kEvCodeBits) | (2u + 2u * cls);
+        } else {
+          flag_internal_error(a.counters, 64);
+        }
+      }
+    }
     uint32_t pf = x->parent;
     if (pf == kNoParent) continue;
     if (pf & kParentPending) pf = L >= 1 ? enclosing(a, t, L - 1) : kNoParent;
@@ -186,6 +214,13 @@ hipError_t launch_resolve(const RunArgs& a, hipStream_t s) {
   ResolveArgs r{a.w.plan, a.w.tiles, a.w.tree, a.w.tree_leaves, a.w.pop_ts, a.w.pop_reg,
                 a.w.pushes, a.w.op_parent, a.w.op_sum, a.w.inst, a.w.child_sum,
                 a.out.d_counters};
+  for (int b = 0; b < 2; ++b) r.ev[b] = a.w.key[b];
+  r.push_pos = a.w.push_pos;
+  r.pop_pos = a.w.pop_pos;
+  r.region_class = a.region_class;
+  r.K = a.K;
+  r.G = a.G;
+  r.shift = a.shift;
   const uint64_t blocks = ceil_div(a.w.match_tiles, 4);
   hipLaunchKernelGGL(k_resolve, dim3((uint32_t)blocks), dim3(256), 0, s, r);
   return hipGetLastError();

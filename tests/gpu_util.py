@@ -13,7 +13,7 @@ def log(msg: str) -> None:
 
 
 def gpu_run(rec_u8: np.ndarray, p: dict, force_full: bool = False, instances: bool = True,
-            stream=None, repeat: int = 1) -> dict:
+            stream=None, repeat: int = 1, force_event: bool = False, with_plan: bool = False) -> dict:
     import torch
 
     from paper_2609_12299_amd import RegionAttribution, to_host
@@ -21,7 +21,7 @@ def gpu_run(rec_u8: np.ndarray, p: dict, force_full: bool = False, instances: bo
     ra = RegionAttribution(p["num_regions"], p.get("num_classes", 0), p.get("region_class"),
                            p.get("group_shift", 0), p.get("num_groups", 0),
                            max_records=max(n, 1), instances=instances, instance_excl=instances,
-                           force_full_sort=force_full)
+                           force_full_sort=force_full, force_event_sort=force_event)
     rec = torch.from_numpy(np.ascontiguousarray(rec_u8).reshape(-1)).to("cuda")
     outs = []
     for _ in range(repeat):
@@ -32,7 +32,10 @@ def gpu_run(rec_u8: np.ndarray, p: dict, force_full: bool = False, instances: bo
         else:
             out = ra.run(rec)
             torch.cuda.synchronize()
-        outs.append(to_host(out))
+        res = to_host(out)
+        if with_plan and n > 0:
+            res["_plan"] = ra.plan()
+        outs.append(res)
     ra.close()
     return outs[0] if repeat == 1 else outs
 

@@ -53,16 +53,92 @@ def test_hand_traces(oracle_mod, case):
 SIZES = [0, 1, 2, 63, 64, 65, 2047, 2048, 2049, 4095, 4096, 4097, 10007, 30001]
 
 
+@pytest.mark.parametrize("ev", ["merge", "radix"])
 @pytest.mark.parametrize("n", SIZES)
 @pytest.mark.parametrize("n_ctx,ts_range", [(1, 1 << 40), (3, 40), (50, 1 << 20)])
-def test_random_malformed(oracle_mod, n, n_ctx, ts_range):
+def test_random_malformed(oracle_mod, n, n_ctx, ts_range, ev):
     rng = np.random.default_rng(n * 131 + n_ctx)
     R = 7
     rec = random_malformed(rng, n, n_ctx, R, ts_range)
     cls = rng.integers(0, 4, size=R).astype(np.uint8)
     p = dict(num_regions=R, num_classes=3, region_class=cls, group_shift=1, num_groups=20)
-    log(f"[gpu] random malformed n={n} ctx={n_ctx} ts_range={ts_range}")
-    assert_parity(gpu_run(rec, p), oracle_run(oracle_mod, rec, p), what=f"n={n}")
+    log(f"[gpu] random malformed n={n} ctx={n_ctx} ts_range={ts_range} events={ev}")
+    g = gpu_run(rec, p, force_event=ev == "radix", with_plan=True)
+    if int(g["counters"][1]) > 0:
+        assert g["_plan"]["ev_merge"] == (1 if ev == "merge" else 0)
+    assert_parity(g, oracle_run(oracle_mod, rec, p), what=f"n={n}")
+
+
+def _nested_contexts(rng, ctx_sizes, R, t_spread, ts_base=0):
+    """Well-formed nested regions in each context, `size` records each (even),
+    timestamps overlapping across contexts, rows shuffled."""
+    rows = []
+    for c, size in ctx_sizes:
+        t = ts_base + int(rng.integers(0, t_spread))
+        stack, left = [], size
+        while left > 0:
+            if stack and (len(stack) >= left or len(stack) >= 6 or rng.random() < 0.45):
+                rows.append((t, c, stack.pop(), 2))
+            else:
+                r = int(rng.integers(0, R))
+                stack.append(r)
+                rows.append((t, c, r, 1))
+            left -= 1
+            t += int(rng.integers(0, 3 * t_spread // max(size, 1) + 2))
+    order = rng.permutation(len(rows))
+    return records_from_rows([rows[i] for i in order])
+
+
+@pytest.mark.parametrize("shift,G", [(5, 3), (3, 100), (32, 1)])
+def test_merge_many_small_contexts(oracle_mod, shift, G):
+    """Hundreds of tiny contexts per group (segments far smaller than a merge
+    tile, many segments per round), groups beyond G present."""
+    rng = np.random.default_rng(shift * 7 + G)
+    ctxs = sorted(rng.choice(1 << 8, size=150, replace=False).tolist())
+    rec = _nested_contexts(rng, [(c, int(rng.integers(1, 6)) * 2) for c in ctxs], 5, 1 << 40)
+    p = dict(num_regions=5, num_classes=3, region_class=np.array([0, 1, 2, 1, 7], np.uint8),
+             group_shift=shift, num_groups=G)
+    log(f"[gpu] merge: many small contexts shift={shift} G={G} n={len(rec)}")
+    g = gpu_run(rec, p, with_plan=True)
+    assert g["_plan"]["ev_merge"] == 1
+    assert_parity(g, oracle_run(oracle_mod, rec, p))
+
+
+def test_merge_skewed_contexts(oracle_mod):
+    """One group: a context spanning many merge tiles next to contexts of a
+    few records, and eight merge rounds (contexts differ in bits 0..7)."""
+    rng = np.random.default_rng(77)
+    sizes = [(0, 40000), (1, 2), (2, 4), (4, 30000), (8, 6), (16, 9000), (32, 2), (64, 12),
+             (128, 5000)]
+    rec = _nested_contexts(rng, sizes, 6, 1 << 56)
+    p = dict(num_regions=6, num_classes=2, region_class=np.array([0, 1, 0, 1, 5, 0], np.uint8),
+             group_shift=32, num_groups=1)
+    log(f"[gpu] merge: skewed contexts n={len(rec)}")
+    g = gpu_run(rec, p, with_plan=True)
+    assert g["_plan"]["ev_merge"] == 1 and g["_plan"]["merge_rounds"] == 8
+    assert_parity(g, oracle_run(oracle_mod, rec, p))
+
+
+@pytest.mark.parametrize("why", ["bits", "rounds"])
+def test_event_radix_fallback(oracle_mod, why):
+    """Where merging does not apply the radix sort orders the events: the
+    event word would need more than 64 bits, or merging would take more
+    rounds than the sort takes passes."""
+    rng = np.random.default_rng(9)
+    if why == "bits":
+        sizes = [(c, 400) for c in range(0, 64, 3)]
+        rec = _nested_contexts(rng, sizes, 4, 1 << 61)
+        p = dict(num_regions=4, num_classes=2, region_class=np.array([0, 1, 1, 0], np.uint8),
+                 group_shift=2, num_groups=1 << 12)
+    else:
+        sizes = [(c, 40) for c in rng.choice(1 << 12, size=300, replace=False).tolist()]
+        rec = _nested_contexts(rng, sizes, 4, 200)
+        p = dict(num_regions=4, num_classes=2, region_class=np.array([0, 1, 1, 0], np.uint8),
+                 group_shift=12, num_groups=1)
+    log(f"[gpu] event radix fallback ({why}) n={len(rec)}")
+    g = gpu_run(rec, p, with_plan=True)
+    assert g["_plan"]["ev_merge"] == 0
+    assert_parity(g, oracle_run(oracle_mod, rec, p))
 
 
 @pytest.mark.parametrize("force_full", [False, True])
@@ -148,6 +224,18 @@ def test_workload_shapes_scaled(oracle_mod, tracegen_mod, cfg, kw, force_full):
     log(f"[gpu] config {cfg} {kw} force_full={force_full} n={len(d['records'])}")
     assert_parity(gpu_run(d["records"], p, force_full=force_full),
                   oracle_run(oracle_mod, d["records"], p), what=f"cfg{cfg}")
+
+
+@pytest.mark.parametrize("cfg,kw", [(2, dict(blocks=4)), (3, dict(blocks=2)), (4, dict(blocks=4)),
+                                    (5, dict(blocks=16, size=1 << 20))])
+def test_workload_shapes_event_radix(oracle_mod, tracegen_mod, cfg, kw):
+    """The event radix sort on the workload shapes (merging is the default)."""
+    d = tracegen_mod.generate(cfg, **kw)
+    p = {k: d[k] for k in ("num_regions", "num_classes", "region_class", "group_shift", "num_groups")}
+    log(f"[gpu] config {cfg} {kw} event radix n={len(d['records'])}")
+    g = gpu_run(d["records"], p, force_event=True, with_plan=True)
+    assert g["_plan"]["ev_merge"] == 0
+    assert_parity(g, oracle_run(oracle_mod, d["records"], p), what=f"cfg{cfg}")
 
 
 def test_determinism_and_stream(oracle_mod, tracegen_mod, gpu):
