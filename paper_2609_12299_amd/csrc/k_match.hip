@@ -195,9 +195,9 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   auto group_of = [&](uint32_t raw_ctx) -> uint32_t {
     return a.shift >= 32 ? 0u : (raw_ctx >> a.shift);
   };
-  auto ev_code = [&](uint32_t region, uint32_t raw_ctx, uint32_t is_end) -> uint32_t {
-    const uint32_t cls = a.region_class[region];
-    return (cls < a.K && group_of(raw_ctx) < a.G) ? 1u + 2u * cls + is_end : 0u;
+  // cls: the record's region class, or 0xFF when its events do not count
+  auto ev_code = [&](uint32_t cls, uint32_t is_end) -> uint32_t {
+    return cls < a.K ? 1u + 2u * cls + is_end : 0u;
   };
 
   for (;;) {
@@ -265,6 +265,15 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
     if (!wide) ctxr[i] = ctx_of_key(key[i]);
     ts[i] = ks.ts_min + (wide ? key[i] : (key[i] & ks.ts_mask));
     reg[i] = pay[i] & 0xFFFFu;
+  }
+  // Region classes of the records, fetched now so that their latency hides
+  // behind the scan and the look-back.
+  uint32_t cls[IT];
+#pragma unroll
+  for (int i = 0; i < IT; ++i) {
+    cls[i] = 0xFFu;
+    if (ev_on && p0 + i < cnt && group_of(ctxr[i] + (uint32_t)ks.ctx_min) < a.G)
+      cls[i] = a.region_class[reg[i]];
   }
   // context of the record before this thread's first one
   s_lastctx[tid] = ctxr[IT - 1];
@@ -576,7 +585,7 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
         s_tend[qrank] = ts[i];
         s_ereg[qrank] = (uint16_t)reg[i];
         if (ev_on && s_breg[qrank] == reg[i])
-          code[i] = ev_code(reg[i], ctxr[i] + (uint32_t)ks.ctx_min, 1u);
+          code[i] = ev_code(cls[i], 1u);
       } else {
         // pops a level that was open when the tile started
         const uint32_t L = sa[i];
@@ -609,7 +618,7 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
     uint64_t t_end = kU64Max;
     if (ereg != kNoEnd) {
       t_end = s_tend[k];
-      if (ev_on && ereg == reg[i]) code[i] = ev_code(reg[i], ctxr[i] + (uint32_t)ks.ctx_min, 0u);
+      if (ev_on && ereg == reg[i]) code[i] = ev_code(cls[i], 0u);
       const uint64_t incl = t_end - ts[i];
       if (par[i] == kParOut) {
         const uint32_t oi = (L - 1) - op_lo;

@@ -47,98 +47,128 @@ __host__ __device__ constexpr int pair_index(int a, int b) {
   return a * KM - a * (a - 1) / 2 + (b - a);
 }
 
+// a * b mod 2^64 for a 32-bit b
+__device__ __forceinline__ uint64_t mul64x32(uint64_t a, uint32_t b) {
+  return (uint64_t)(uint32_t)a * b + ((uint64_t)((uint32_t)(a >> 32) * b) << 32);
+}
+
 template <int KM>
 __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
   constexpr int NP = KM * (KM + 1) / 2;
+  constexpr int IT = kSweepItems;
   const DevPlan* P = a.plan;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   __shared__ uint32_t s_tile;
-  __shared__ uint64_t s_t[kSweepTile];
-  __shared__ uint32_t s_g[kSweepTile];
-  __shared__ uint32_t s_pay[kSweepTile];
   __shared__ uint64_t s_u[kSweepSlots][NP];
   __shared__ uint64_t s_q[kSweepSlots][NP];
   __shared__ int32_t s_wd[4][KM];
   __shared__ uint32_t s_wr[4];
   __shared__ int32_t s_cin[KM];
-  __shared__ uint32_t s_prev_g, s_has_prev, s_next_g, s_has_next;
-  __shared__ uint64_t s_next_t;
+  __shared__ uint32_t s_g0;
 
   const uint64_t n = P->n_ev;
   const uint64_t tiles = ceil_div(n, kSweepTile);
-  for (;;) {
-  if (tid == 0) s_tile = atomicAdd(&a.tile_ctr[kCtrSweep], 1u);
-  __syncthreads();
-  const uint64_t tile = s_tile;
-  if (tile >= tiles) break;
   const KeySpace ks = P->ev;
   const bool wide = ks.wide != 0;
+  const bool mfmt = P->ev_merge != 0;
   const uint32_t buf = P->ev_final;
   const uint64_t* gk = a.key[buf];
   const uint32_t* gp = a.pay[buf];
   const uint32_t* gc = a.ctxw[buf];
-  const uint64_t base = tile * kSweepTile;
-  const uint32_t cnt = n - base < (uint64_t)kSweepTile ? (uint32_t)(n - base) : (uint32_t)kSweepTile;
-  auto grp = [&](uint64_t k, uint32_t cw) -> uint32_t {
-    return wide ? cw : (ks.ts_bits >= 64 ? 0u : (uint32_t)(k >> ks.ts_bits));
+  constexpr uint32_t kNoGroup = 0xFFFFFFFFu;
+  // (group, time, class | is_end << 8) of event i; class 0xFF changes no count
+  auto decode = [&](uint64_t raw, uint32_t pay, uint32_t cw, uint32_t* g, uint64_t* t,
+                    uint32_t* py) {
+    uint64_t k = raw;
+    if (mfmt) {
+      k = raw >> kEvCodeBits;
+      const uint32_t c = (uint32_t)(raw & ((1u << kEvCodeBits) - 1u));
+      pay = c ? ((c - 1u) >> 1) | (((c - 1u) & 1u) << 8) : 0xFFu;
+    }
+    *g = wide ? cw : (ks.ts_bits >= 64 ? 0u : (uint32_t)(k >> ks.ts_bits));
+    *t = wide ? k : (k & ks.ts_mask);
+    *py = pay;
   };
-  auto tof = [&](uint64_t k) -> uint64_t { return wide ? k : (k & ks.ts_mask); };
-  // Merged event words: key = word >> 5; code 0 (no event) gets a class
-  // that matches no counter.
-  const bool mfmt = P->ev_merge != 0;
-  auto key_at = [&](uint64_t i) -> uint64_t { return mfmt ? gk[i] >> kEvCodeBits : gk[i]; };
-  auto pay_at = [&](uint64_t i) -> uint32_t {
-    if (!mfmt) return gp[i];
-    const uint32_t c = (uint32_t)(gk[i] & ((1u << kEvCodeBits) - 1u));
-    return c ? ((c - 1u) >> 1) | (((c - 1u) & 1u) << 8) : 0xFFu;
+  auto load_one = [&](uint64_t i, uint32_t* g, uint64_t* t, uint32_t* py) {
+    decode(gk[i], mfmt ? 0u : gp[i], wide ? gc[i] : 0u, g, t, py);
   };
 
-  for (int j = 0; j < kSweepItems; ++j) {
-    const uint32_t i = (uint32_t)j * kSweepThreads + tid;
-    if (i < cnt) {
-      const uint64_t k = key_at(base + i);
-      s_t[i] = tof(k);
-      s_g[i] = grp(k, wide ? gc[base + i] : 0u);
-      s_pay[i] = pay_at(base + i);
-    }
-  }
+  for (;;) {
+  if (tid == 0) s_tile = atomicAdd(&a.tile_ctr[kCtrSweep], 1u);
   for (int i = tid; i < kSweepSlots * NP; i += kSweepThreads) {
     (&s_u[0][0])[i] = 0;
     (&s_q[0][0])[i] = 0;
   }
-  if (tid == 0) {
-    s_has_prev = base > 0;
-    s_prev_g = base > 0 ? grp(key_at(base - 1), wide ? gc[base - 1] : 0u) : 0u;
-    s_has_next = base + cnt < n;
-    if (base + cnt < n) {
-      const uint64_t k = key_at(base + cnt);
-      s_next_g = grp(k, wide ? gc[base + cnt] : 0u);
-      s_next_t = tof(k);
+  __syncthreads();
+  const uint64_t tile = s_tile;
+  if (tile >= tiles) break;
+  const uint64_t base = tile * kSweepTile;
+  const uint32_t cnt = n - base < (uint64_t)kSweepTile ? (uint32_t)(n - base) : (uint32_t)kSweepTile;
+  const uint32_t p0 = (uint32_t)tid * IT;
+
+  // ---- this thread's 8 consecutive events, the one before and the one after
+  uint32_t g[IT], py[IT];
+  uint64_t t[IT];
+  if (p0 + IT <= cnt && mfmt) {
+    const uint4* e4 = (const uint4*)(gk + base + p0);
+#pragma unroll
+    for (int q = 0; q < IT / 2; ++q) {
+      const uint4 v = e4[q];
+      decode((uint64_t)v.x | ((uint64_t)v.y << 32), 0u, 0u, &g[2 * q], &t[2 * q], &py[2 * q]);
+      decode((uint64_t)v.z | ((uint64_t)v.w << 32), 0u, 0u, &g[2 * q + 1], &t[2 * q + 1],
+             &py[2 * q + 1]);
+    }
+  } else if (p0 + IT <= cnt && !wide) {
+    const uint4* k4 = (const uint4*)(gk + base + p0);
+    const uint4* q4 = (const uint4*)(gp + base + p0);
+    uint32_t pw[IT];
+#pragma unroll
+    for (int q = 0; q < IT / 4; ++q) {
+      const uint4 v = q4[q];
+      pw[4 * q] = v.x;
+      pw[4 * q + 1] = v.y;
+      pw[4 * q + 2] = v.z;
+      pw[4 * q + 3] = v.w;
+    }
+#pragma unroll
+    for (int q = 0; q < IT / 2; ++q) {
+      const uint4 v = k4[q];
+      decode((uint64_t)v.x | ((uint64_t)v.y << 32), pw[2 * q], 0u, &g[2 * q], &t[2 * q], &py[2 * q]);
+      decode((uint64_t)v.z | ((uint64_t)v.w << 32), pw[2 * q + 1], 0u, &g[2 * q + 1],
+             &t[2 * q + 1], &py[2 * q + 1]);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < IT; ++i) {
+      g[i] = kNoGroup;
+      t[i] = 0;
+      py[i] = 0xFFu;
+      if (p0 + i < cnt) load_one(base + p0 + i, &g[i], &t[i], &py[i]);
     }
   }
-  __syncthreads();
+  uint32_t g_prev = kNoGroup, g_next = kNoGroup, pdummy;
+  uint64_t t_next = 0, tdummy;
+  if (p0 < cnt && base + p0 > 0) load_one(base + p0 - 1, &g_prev, &tdummy, &pdummy);
+  if (base + p0 + IT < n && p0 + IT <= cnt) load_one(base + p0 + IT, &g_next, &t_next, &pdummy);
+  if (tid == 0) s_g0 = g[0];
 
   // ---- per-thread aggregate: reset flag and count deltas since the last start
-  const uint32_t p0 = (uint32_t)tid * kSweepItems;
   uint32_t reset = 0;
   int32_t d[KM];
 #pragma unroll
   for (int k = 0; k < KM; ++k) d[k] = 0;
 #pragma unroll
-  for (int i = 0; i < kSweepItems; ++i) {
-    const uint32_t p = p0 + i;
-    if (p >= cnt) break;
-    const uint32_t g = s_g[p];
-    const bool head = p == 0 ? (!s_has_prev || s_prev_g != g) : s_g[p - 1] != g;
-    if (head) {
+  for (int i = 0; i < IT; ++i) {
+    if (g[i] == kNoGroup) continue;
+    const uint32_t gb = i > 0 ? g[i - 1] : g_prev;
+    if (gb != g[i]) {
       reset = 1;
 #pragma unroll
       for (int k = 0; k < KM; ++k) d[k] = 0;
     }
-    const uint32_t py = s_pay[p];
-    const int32_t delta = ((py >> 8) & 1u) ? -1 : 1;
+    const int32_t delta = ((py[i] >> 8) & 1u) ? -1 : 1;
 #pragma unroll
-    for (int k = 0; k < KM; ++k) d[k] += ((py & 0xFFu) == (uint32_t)k) ? delta : 0;
+    for (int k = 0; k < KM; ++k) d[k] += ((py[i] & 0xFFu) == (uint32_t)k) ? delta : 0;
   }
   // wave inclusive scan (g after f: g.reset ? g : f + g)
   uint32_t xr = reset;
@@ -196,72 +226,124 @@ __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
     for (int k = 0; k < KM; ++k) pd[k] += ed[k];
   }
 
-  // ---- look-back for the counts entering the tile
-  if (tid == 0) {
+  // ---- look-back for the counts entering the tile.  Wave 0 inspects 64
+  // predecessor tiles per round trip (lane j: the j-th nearest not yet
+  // folded in).  A tile's aggregate is (reset, deltas): reset when a group
+  // starts inside it, deltas since that start; folding keeps the nearer
+  // aggregate whole when it resets.
+  if (w == 0) {
     uint32_t tr = 0;
     int32_t td[KM];
 #pragma unroll
     for (int k = 0; k < KM; ++k) td[k] = 0;
-    for (int q = 0; q < 4; ++q) {
-      if (s_wr[q]) {
+    for (int qq = 0; qq < 4; ++qq) {
+      if (s_wr[qq]) {
         tr = 1;
 #pragma unroll
-        for (int k = 0; k < KM; ++k) td[k] = s_wd[q][k];
+        for (int k = 0; k < KM; ++k) td[k] = s_wd[qq][k];
       } else {
 #pragma unroll
-        for (int k = 0; k < KM; ++k) td[k] += s_wd[q][k];
+        for (int k = 0; k < KM; ++k) td[k] += s_wd[qq][k];
       }
     }
-    int64_t cin[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    int64_t cin[KM];
+#pragma unroll
+    for (int k = 0; k < KM; ++k) cin[k] = 0;
     uint64_t* lb = a.slb + tile * 8;
     if (tile > 0) {
-      uint64_t w0 = kFlagAgg | ((uint64_t)tr << 61), w1 = kFlagAgg;
-      for (int k = 0; k < 4 && k < KM; ++k) w0 |= (uint64_t)(td[k] + 2048) << (13 * k);
-      for (int k = 4; k < KM; ++k) w1 |= (uint64_t)(td[k] + 2048) << (13 * (k - 4));
-      st_agent(&lb[0], w0);
-      st_agent(&lb[1], w1);
-      int64_t acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-      int64_t tt = (int64_t)tile - 1;
+      if (lane == 0) {
+        uint64_t w0 = kFlagAgg | ((uint64_t)tr << 61), w1 = kFlagAgg;
+        for (int k = 0; k < 4 && k < KM; ++k) w0 |= (uint64_t)(td[k] + 2048) << (13 * k);
+        for (int k = 4; k < KM; ++k) w1 |= (uint64_t)(td[k] + 2048) << (13 * (k - 4));
+        st_agent(&lb[0], w0);
+        st_agent(&lb[1], w1);
+      }
+      uint32_t acc_r = 0;  // fold of the tiles between the found one and this tile
+      int64_t acc[KM];
+#pragma unroll
+      for (int k = 0; k < KM; ++k) acc[k] = 0;
+      int64_t top = (int64_t)tile - 1;
       uint32_t spins = 0;
-      while (tt >= 0) {
-        const uint64_t* l = a.slb + (uint64_t)tt * 8;
-        uint64_t iw[4];
-        bool incl = true;
-        for (int q = 0; q < 4; ++q) {
-          iw[q] = ld_agent(&l[2 + q]);
-          incl &= (iw[q] & ~kValMask) == kFlagIncl;
+      for (;;) {
+        const int64_t tt = top - lane;
+        uint64_t aw0 = 0, aw1 = 0, iw[4] = {0, 0, 0, 0};
+        if (tt >= 0) {
+          const uint64_t* l = a.slb + (uint64_t)tt * 8;
+#pragma unroll
+          for (int qq = 0; qq < 4; ++qq) iw[qq] = ld_agent(&l[2 + qq]);
+          aw0 = ld_agent(&l[0]);
+          aw1 = ld_agent(&l[1]);
         }
-        if (incl) {
-          for (int k = 0; k < 8; ++k) {
-            const uint64_t v = (iw[k >> 1] >> (31 * (k & 1))) & 0x7FFFFFFFull;
+        bool incl = true;
+#pragma unroll
+        for (int qq = 0; qq < 4; ++qq) incl &= (iw[qq] & ~kValMask) == kFlagIncl;
+        const bool agg = (aw0 & ~kValMask) == kFlagAgg && (aw1 & ~kValMask) == kFlagAgg;
+        const uint64_t mi = __ballot(incl), mn = __ballot(!incl && !agg);
+        const int ji = mi ? __ffsll((unsigned long long)mi) - 1 : 64;
+        const int jn = mn ? __ffsll((unsigned long long)mn) - 1 : 64;
+        const bool done = ji < jn;
+        const int kk = done ? ji : jn;  // lanes [0, kk) hold aggregates to fold in
+        uint32_t xr = 0;
+        int32_t xd[KM];
+#pragma unroll
+        for (int k = 0; k < KM; ++k) xd[k] = 0;
+        if (lane < kk) {
+          xr = (uint32_t)(aw0 >> 61) & 1u;
+#pragma unroll
+          for (int k = 0; k < KM; ++k)
+            xd[k] = (int32_t)(((k < 4 ? aw0 >> (13 * k) : aw1 >> (13 * (k - 4)))) & 0x1FFFull) - 2048;
+        }
+        // reduce towards lane 0 (a higher lane is an earlier tile)
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const uint32_t yr = __shfl_down(xr, o);
+          int32_t yd[KM];
+#pragma unroll
+          for (int k = 0; k < KM; ++k) yd[k] = __shfl_down(xd[k], o);
+          if (lane + o < 64 && !xr) {
+            xr = yr;
+#pragma unroll
+            for (int k = 0; k < KM; ++k) xd[k] += yd[k];
+          }
+        }
+        // acc = fold(lanes [0, kk)) then acc
+        const uint32_t fr = (uint32_t)__shfl(xr, 0);
+        if (!acc_r) {
+          acc_r = fr;
+#pragma unroll
+          for (int k = 0; k < KM; ++k) acc[k] += __shfl(xd[k], 0);
+        }
+        if (acc_r) {
+#pragma unroll
+          for (int k = 0; k < KM; ++k) cin[k] = acc[k];
+          break;
+        }
+        if (done) {
+#pragma unroll
+          for (int k = 0; k < KM; ++k) {
+            const uint64_t v = (__shfl(iw[k >> 1], ji) >> (31 * (k & 1))) & 0x7FFFFFFFull;
             cin[k] = (int64_t)v + acc[k];
           }
           break;
         }
-        const uint64_t a0 = ld_agent(&l[0]), a1 = ld_agent(&l[1]);
-        if ((a0 & ~kValMask) == kFlagAgg && (a1 & ~kValMask) == kFlagAgg) {
-          for (int k = 0; k < 4; ++k) acc[k] += (int64_t)((a0 >> (13 * k)) & 0x1FFFull) - 2048;
-          for (int k = 4; k < 8; ++k) acc[k] += (int64_t)((a1 >> (13 * (k - 4))) & 0x1FFFull) - 2048;
-          if ((a0 >> 61) & 1ull) {
-            for (int k = 0; k < 8; ++k) cin[k] = acc[k];
+        top -= kk;
+        if (kk == 0) {
+          if (++spins > kMaxSpins) {
+            if (lane == 0) flag_internal_error(a.counters, 128);
             break;
           }
-          --tt;
-          continue;
+          backoff();
         }
-        if (++spins > kMaxSpins) {
-          flag_internal_error(a.counters, 128);
-          break;
-        }
-        backoff();
       }
     }
-    int64_t cout[8];
-    for (int k = 0; k < 8; ++k) cout[k] = (k < KM) ? (tr ? td[k] : cin[k] + td[k]) : 0;
-    for (int q = 0; q < 4; ++q)
-      st_agent(&lb[2 + q], kFlagIncl | (uint64_t)cout[2 * q] | ((uint64_t)cout[2 * q + 1] << 31));
+    if (lane == 0) {
+      int64_t cout[8];
+      for (int k = 0; k < 8; ++k) cout[k] = (k < KM) ? (tr ? td[k] : cin[k] + td[k]) : 0;
+      for (int qq = 0; qq < 4; ++qq)
+        st_agent(&lb[2 + qq], kFlagIncl | (uint64_t)cout[2 * qq] | ((uint64_t)cout[2 * qq + 1] << 31));
 #pragma unroll
-    for (int k = 0; k < KM; ++k) s_cin[k] = (int32_t)cin[k];
+      for (int k = 0; k < KM; ++k) s_cin[k] = (int32_t)cin[k];
+    }
   }
   __syncthreads();
 
@@ -269,27 +351,27 @@ __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
   int32_t c[KM];
 #pragma unroll
   for (int k = 0; k < KM; ++k) c[k] = pr ? pd[k] : s_cin[k] + pd[k];
-  const uint32_t g0 = s_g[0];
+  const uint32_t g0 = s_g0;
   uint64_t u[NP], q[NP];
 #pragma unroll
   for (int k = 0; k < NP; ++k) {
     u[k] = 0;
     q[k] = 0;
   }
-  uint32_t qg = p0 < cnt ? s_g[p0] : g0;
+  uint32_t qg = g[0] != kNoGroup ? g[0] : g0;
   const uint32_t K = a.K;
-  auto flush = [&](uint32_t g) {
-    const uint32_t slot = g - g0;
-    if (g >= a.G) return;
+  auto flush = [&](uint32_t gg) {
+    const uint32_t slot = gg - g0;
+    if (gg >= a.G) return;
 #pragma unroll
     for (int k = 0; k < NP; ++k) {
       if (u[k]) {
         if (slot < kSweepSlots) atomicAdd((unsigned long long*)&s_u[slot][k], (unsigned long long)u[k]);
-        else atomicAdd((unsigned long long*)&a.ov_u[(uint64_t)g * kSweepQWords + k], (unsigned long long)u[k]);
+        else atomicAdd((unsigned long long*)&a.ov_u[(uint64_t)gg * kSweepQWords + k], (unsigned long long)u[k]);
       }
       if (q[k]) {
         if (slot < kSweepSlots) atomicAdd((unsigned long long*)&s_q[slot][k], (unsigned long long)q[k]);
-        else atomicAdd((unsigned long long*)&a.ov_q[(uint64_t)g * kSweepQWords + k], (unsigned long long)q[k]);
+        else atomicAdd((unsigned long long*)&a.ov_q[(uint64_t)gg * kSweepQWords + k], (unsigned long long)q[k]);
       }
       u[k] = 0;
       q[k] = 0;
@@ -297,41 +379,46 @@ __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
   };
   bool flushed_early = false;
 #pragma unroll
-  for (int i = 0; i < kSweepItems; ++i) {
-    const uint32_t p = p0 + i;
-    if (p >= cnt) break;
-    const uint32_t g = s_g[p];
-    const bool head = p == 0 ? (!s_has_prev || s_prev_g != g) : s_g[p - 1] != g;
-    if (head) {
+  for (int i = 0; i < IT; ++i) {
+    if (g[i] == kNoGroup) break;
+    const uint32_t gb = i > 0 ? g[i - 1] : g_prev;
+    if (gb != g[i]) {
 #pragma unroll
       for (int k = 0; k < KM; ++k) c[k] = 0;
     }
-    if (g != qg) {
+    if (g[i] != qg) {
       flush(qg);
       flushed_early = true;
-      qg = g;
+      qg = g[i];
     }
-    const uint32_t py = s_pay[p];
-    const int32_t delta = ((py >> 8) & 1u) ? -1 : 1;
+    const int32_t delta = ((py[i] >> 8) & 1u) ? -1 : 1;
 #pragma unroll
-    for (int k = 0; k < KM; ++k) c[k] += ((py & 0xFFu) == (uint32_t)k) ? delta : 0;
-    uint64_t gap = 0;
-    if (p + 1 < cnt) {
-      if (s_g[p + 1] == g) gap = s_t[p + 1] - s_t[p];
-    } else if (s_has_next && s_next_g == g) {
-      gap = s_next_t - s_t[p];
-    }
+    for (int k = 0; k < KM; ++k) c[k] += ((py[i] & 0xFFu) == (uint32_t)k) ? delta : 0;
+    const uint32_t gn = i + 1 < IT ? g[i + 1] : g_next;
+    const uint64_t tn = i + 1 < IT ? t[i + 1] : t_next;
+    if (gn != g[i]) continue;  // last event of its group (or of the data)
+    const uint64_t gap = tn - t[i];
     if (gap == 0) continue;
+    uint32_t cc[KM];
+    uint64_t gx[KM];
+#pragma unroll
+    for (int x = 0; x < KM; ++x) {
+      cc[x] = c[x] > 0 ? (uint32_t)c[x] : 0u;
+      gx[x] = mul64x32(gap, cc[x]);
+    }
 #pragma unroll
     for (int x = 0; x < KM; ++x) {
 #pragma unroll
       for (int y = x; y < KM; ++y) {
         if ((uint32_t)y >= K) continue;
         const int pi = pair_index<KM>(x, y);
-        const uint64_t cx = (uint64_t)(c[x] > 0 ? c[x] : 0), cy = (uint64_t)(c[y] > 0 ? c[y] : 0);
-        if (cx > 0 && cy > 0) u[pi] += gap;
-        if (x != y) q[pi] += gap * cx * cy;
-        else if (cx > 1) q[pi] += gap * (cx * (cx - 1) / 2);
+        if (cc[x] && cc[y]) u[pi] += gap;
+        if (x != y) {
+          q[pi] += mul64x32(gx[x], cc[y]);
+        } else if (cc[x] > 1) {
+          const uint64_t pairs = (uint64_t)cc[x] * (cc[x] - 1) / 2;
+          q[pi] += gap * pairs;
+        }
       }
     }
   }
@@ -354,12 +441,10 @@ __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
   }
   flush(qg);
   __syncthreads();
-  // ---- tile flush of the LDS slots
-  const uint32_t last_g = s_g[cnt - 1];
-  const uint32_t nslots = (last_g - g0 + 1) < (uint32_t)kSweepSlots ? last_g - g0 + 1 : (uint32_t)kSweepSlots;
-  for (uint32_t i = tid; i < nslots * NP; i += kSweepThreads) {
+  // ---- tile flush of the LDS slots (slot j: group g0 + j)
+  for (uint32_t i = tid; i < (uint32_t)(kSweepSlots * NP); i += kSweepThreads) {
     const uint32_t slot = i / NP, k = i % NP;
-    const uint64_t gg = (uint64_t)(g0 + slot);
+    const uint64_t gg = (uint64_t)g0 + slot;
     if (gg >= a.G) continue;
     if (s_u[slot][k]) atomicAdd((unsigned long long*)&a.ov_u[gg * kSweepQWords + k], (unsigned long long)s_u[slot][k]);
     if (s_q[slot][k]) atomicAdd((unsigned long long*)&a.ov_q[gg * kSweepQWords + k], (unsigned long long)s_q[slot][k]);

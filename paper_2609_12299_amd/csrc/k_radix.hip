@@ -46,11 +46,9 @@ __device__ __forceinline__ uint32_t digit_of(uint32_t pos, uint64_t raw_ctx, uin
 // pass of a sort is a distinct kernel in profiles.
 template <int WHICH, int SLOT>
 __global__ __launch_bounds__(kSortThreads) void k_radix_pass(RadixArgs a) {
-  a.which = WHICH;
-  a.slot = SLOT;
-  const SlotPlan sp = a.which ? a.plan->es[a.slot] : a.plan->rs[a.slot];
+  const SlotPlan sp = WHICH ? a.plan->es[SLOT] : a.plan->rs[SLOT];
   if (!sp.active) return;
-  const KeySpace ks = a.which ? a.plan->ev : a.plan->rec;
+  const KeySpace ks = WHICH ? a.plan->ev : a.plan->rec;
 
   __shared__ uint32_t s_tile;
   __shared__ uint32_t s_wave[4][kRadixBins];  // per-wave counts, then wave prefixes
@@ -67,7 +65,7 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(RadixArgs a) {
   // Persistent blocks: tiles are taken in order from an atomic counter, so a
   // tile's predecessors always belong to blocks that are already running.
   for (;;) {
-  if (tid == 0) s_tile = atomicAdd(&a.tile_ctr[(a.which ? kCtrEv : kCtrRec) + a.slot], 1u);
+  if (tid == 0) s_tile = atomicAdd(&a.tile_ctr[(WHICH ? kCtrEv : kCtrRec) + SLOT], 1u);
   for (int i = tid; i < 4 * kRadixBins; i += kSortThreads) (&s_wave[0][0])[i] = 0;
   __syncthreads();
   const uint64_t tile = s_tile;
@@ -82,70 +80,90 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(RadixArgs a) {
   uint64_t key[kSortItems];
   uint32_t pay[kSortItems], cw[kSortItems], dig[kSortItems], rank[kSortItems];
 
-  const uint64_t* ksrc = sp.src < 2 ? a.key[sp.src] : nullptr;
-  const uint32_t* psrc = sp.src < 2 ? a.pay[sp.src] : nullptr;
-  const uint32_t* csrc = sp.src < 2 ? a.ctxw[sp.src] : nullptr;
-
+  // Loads first, all of them unconditional (an index past the tile's end is
+  // clamped to its last element, whose digit is then discarded), so that
+  // every load of the tile is in flight before the first one is used.
+  auto elem = [&](int r) -> uint32_t {
+    return (uint32_t)w * (kSortItems * 64) + (uint32_t)r * 64 + lane;
+  };
+  auto clamp = [&](uint32_t el) -> uint64_t { return base + (el < cnt ? el : cnt - 1); };
+  if (sp.src < 2) {
+    const uint64_t* ksrc = sp.src ? a.key[1] : a.key[0];
+    const uint32_t* psrc = sp.src ? a.pay[1] : a.pay[0];
+    const uint32_t* csrc = sp.src ? a.ctxw[1] : a.ctxw[0];
 #pragma unroll
-  for (int r = 0; r < kSortItems; ++r) {
-    const uint32_t el = (uint32_t)w * (kSortItems * 64) + (uint32_t)r * 64 + lane;
-    uint32_t d = 256;  // 256: no element / invalid (never written)
-    key[r] = 0;
-    pay[r] = 0;
-    cw[r] = 0;
-    if (el < cnt) {
-      const uint64_t e = base + el;
-      if (sp.src < 2) {
-        const uint64_t k = ksrc[e];
-        key[r] = k;
-        pay[r] = psrc[e];
-        uint64_t ctx_rel, ts_off;
-        if (wide) {
-          cw[r] = csrc[e];
-          ctx_rel = cw[r];
-          ts_off = k;
-        } else {
-          ctx_rel = ks.ts_bits >= 64 ? 0 : (k >> ks.ts_bits);
-          ts_off = k & ks.ts_mask;
-        }
-        d = digit_of(pos, ks.ctx_min + ctx_rel, ks.ts_min + ts_off);
-      } else if (a.which == 0) {
-        const uint4 rr = a.rec[e];
-        const uint64_t ts = (uint64_t)rr.x | ((uint64_t)rr.y << 32);
-        const uint32_t ctx = rr.z;
-        const uint32_t region = rr.w & 0xFFFFu;
-        const uint32_t kind = (rr.w >> 16) & 0xFFu;
-        if ((kind == 1 || kind == 2) && region < a.R) {
-          const uint64_t ts_off = ts - ks.ts_min;
-          const uint64_t ctx_rel = (uint64_t)ctx - ks.ctx_min;
-          key[r] = wide ? ts_off : ((ks.ts_bits >= 64 ? 0 : (ctx_rel << ks.ts_bits)) | ts_off);
-          cw[r] = (uint32_t)ctx_rel;
-          pay[r] = region | ((kind - 1u) << 16);
-          d = digit_of(pos, ctx, ts);
-        }
-      } else {
-        // Overlap events: element e is the begin (even) or end (odd) of
-        // instance e / 2; only matched, classified instances of a group < G.
-        const argus_instance* ip = a.inst + (e >> 1);
-        const uint32_t is_end = (uint32_t)(e & 1);
-        const uint64_t t = is_end ? ip->t_end : ip->t_begin;
-        const uint32_t ctx = ip->ctx_key;
-        const uint32_t regs = *(const uint32_t*)&ip->region_id;  // region | end_region << 16
-        const uint32_t region = regs & 0xFFFFu, eregion = regs >> 16;
-        if (region == eregion) {
-          const uint32_t cls = a.region_class[region];
-          const uint64_t g = a.shift >= 32 ? 0 : (ctx >> a.shift);
-          if (cls < a.K && g < a.G) {
-            const uint64_t ts_off = t - ks.ts_min;
-            key[r] = wide ? ts_off : ((ks.ts_bits >= 64 ? 0 : (g << ks.ts_bits)) | ts_off);
-            cw[r] = (uint32_t)g;
-            pay[r] = cls | (is_end << 8);
-            d = digit_of(pos, g, t);
-          }
-        }
-      }
+    for (int r = 0; r < kSortItems; ++r) {
+      const uint64_t e = clamp(elem(r));
+      key[r] = ksrc[e];
+      pay[r] = psrc[e];
+      cw[r] = wide ? csrc[e] : 0u;
     }
-    dig[r] = d;
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) {
+      uint64_t ctx_rel, ts_off;
+      if (wide) {
+        ctx_rel = cw[r];
+        ts_off = key[r];
+      } else {
+        ctx_rel = ks.ts_bits >= 64 ? 0 : (key[r] >> ks.ts_bits);
+        ts_off = key[r] & ks.ts_mask;
+      }
+      dig[r] = elem(r) < cnt ? digit_of(pos, ks.ctx_min + ctx_rel, ks.ts_min + ts_off) : 256u;
+    }
+  } else if (WHICH == 0) {
+    uint4 rr[kSortItems];
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) rr[r] = a.rec[clamp(elem(r))];
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) {
+      // branch-free, so that the whole 16-byte record is loaded up front
+      const uint64_t ts = (uint64_t)rr[r].x | ((uint64_t)rr[r].y << 32);
+      const uint32_t ctx = rr[r].z;
+      const uint32_t region = rr[r].w & 0xFFFFu;
+      const uint32_t kind = (rr[r].w >> 16) & 0xFFu;
+      const bool ok = elem(r) < cnt && (kind == 1 || kind == 2) && region < a.R;
+      const uint64_t ts_off = ts - ks.ts_min;
+      const uint64_t ctx_rel = (uint64_t)ctx - ks.ctx_min;
+      const uint64_t k = wide ? ts_off : ((ks.ts_bits >= 64 ? 0 : (ctx_rel << ks.ts_bits)) | ts_off);
+      key[r] = ok ? k : 0;
+      cw[r] = ok ? (uint32_t)ctx_rel : 0u;
+      pay[r] = ok ? region | ((kind - 1u) << 16) : 0u;
+      dig[r] = ok ? digit_of(pos, ctx, ts) : 256u;  // 256: invalid (never written)
+    }
+  } else {
+    // Overlap events: element e is the begin (even) or end (odd) of instance
+    // e / 2; only matched, classified instances of a group < G.
+    uint64_t tv[kSortItems];
+    uint32_t cv[kSortItems], rv[kSortItems], cl[kSortItems];
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) {
+      const uint64_t e = clamp(elem(r));
+      const argus_instance* ip = a.inst + (e >> 1);
+      tv[r] = (e & 1) ? ip->t_end : ip->t_begin;
+      cv[r] = ip->ctx_key;
+      rv[r] = *(const uint32_t*)&ip->region_id;  // region | end_region << 16
+    }
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) cl[r] = a.region_class[rv[r] & 0xFFFFu];
+#pragma unroll
+    for (int r = 0; r < kSortItems; ++r) {
+      uint32_t d = 256;
+      const uint32_t el = elem(r);
+      const uint32_t is_end = (uint32_t)((base + el) & 1);
+      const uint32_t region = rv[r] & 0xFFFFu, eregion = rv[r] >> 16;
+      const uint64_t g = a.shift >= 32 ? 0 : (cv[r] >> a.shift);
+      key[r] = 0;
+      pay[r] = 0;
+      cw[r] = 0;
+      if (el < cnt && region == eregion && cl[r] < a.K && g < a.G) {
+        const uint64_t ts_off = tv[r] - ks.ts_min;
+        key[r] = wide ? ts_off : ((ks.ts_bits >= 64 ? 0 : (g << ks.ts_bits)) | ts_off);
+        cw[r] = (uint32_t)g;
+        pay[r] = cl[r] | (is_end << 8);
+        d = digit_of(pos, g, tv[r]);
+      }
+      dig[r] = d;
+    }
   }
   // Rank among this wave's elements with the same digit (stable order is
   // wave, round, lane).  All loads above are already in flight.
