@@ -124,25 +124,52 @@ __global__ __launch_bounds__(512) void k_agg(AggArgs a) {
   }
   uint64_t n_m = 0, n_mm = 0, n_u = 0, n_sn = 0, n_ev = 0, n_skip = 0;
   unsigned long long* rs = (unsigned long long*)a.rstats;
-  const uint64_t stride = (uint64_t)gridDim.x * NT;
-  // Wave-uniform trip count (the event histograms use ballots).
-  for (uint64_t wb = (uint64_t)blockIdx.x * NT + (threadIdx.x & ~63u); wb < nb; wb += stride) {
-    const uint64_t id = wb + (threadIdx.x & 63);
+  // Each wave takes 4 x 64 consecutive instances per step, with their loads
+  // (and then the parents' regions) in flight together; every lane of a
+  // wave iterates the same number of times (the event histograms use
+  // ballots).
+  constexpr int B = 4;
+  const uint32_t lane = threadIdx.x & 63;
+  const uint64_t stride = (uint64_t)gridDim.x * NT * B;
+  for (uint64_t wb = ((uint64_t)blockIdx.x * (NT / 64) + (threadIdx.x >> 6)) * (64 * B); wb < nb;
+       wb += stride) {
+    argus_instance xs[B];
+    uint64_t cs[B];
+    uint32_t par[B];
+    uint16_t preg[B];
+#pragma unroll
+    for (int j = 0; j < B; ++j) {
+      const uint64_t id = wb + (uint64_t)j * 64 + lane;
+      const uint64_t ic = id < nb ? id : nb - 1;
+      xs[j] = a.inst[ic];
+      cs[j] = a.child_sum[ic];
+    }
+#pragma unroll
+    for (int j = 0; j < B; ++j) {
+      par[j] = agg_parent(xs[j], a.tiles, a.op_parent);
+      if (par[j] != kNoParent && par[j] >= nb) {
+        flag_internal_error(a.counters, 4);
+        par[j] = kNoParent;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < B; ++j) {
+      const bool matched = xs[j].end_region_id != kNoEnd && xs[j].end_region_id == xs[j].region_id;
+      preg[j] = (matched && par[j] != kNoParent) ? a.inst[par[j]].region_id : (uint16_t)kNoEnd;
+    }
+#pragma unroll
+    for (int j = 0; j < B; ++j) {
+    const uint64_t id = wb + (uint64_t)j * 64 + lane;
     bool ev = false;
     uint64_t eg = 0, et0 = 0, et1 = 0;
     if (id < nb) {
-    argus_instance x = a.inst[id];
-    uint32_t par = agg_parent(x, a.tiles, a.op_parent);
-    if (par != kNoParent && par >= nb) {
-      flag_internal_error(a.counters, 4);
-      par = kNoParent;
-    }
-    if (par != x.parent) a.inst[id].parent = par;
+    const argus_instance& x = xs[j];
+    if (par[j] != x.parent) a.inst[id].parent = par[j];
     const uint32_t region = x.region_id, ereg = x.end_region_id;
     const bool closed = ereg != kNoEnd;
     const bool matched = closed && ereg == region;
     const uint64_t incl = closed ? x.t_end - x.t_begin : 0;
-    const uint64_t excl = closed ? incl - a.child_sum[id] : 0;
+    const uint64_t excl = closed ? incl - cs[j] : 0;
     if (a.excl_out) a.excl_out[id] = excl;
     uint32_t hk = 0xFFFFFFFFu;
     if (matched) {
@@ -161,7 +188,7 @@ __global__ __launch_bounds__(512) void k_agg(AggArgs a) {
           }
         }
       }
-      const bool sn = par != kNoParent && a.inst[par].region_id == region;
+      const bool sn = preg[j] == region;
       n_sn += sn;
       const uint32_t bi = bit_width64(incl), be = bit_width64(excl);
       hk = (region << 16) | (bi << 8) | be;
@@ -220,7 +247,9 @@ __global__ __launch_bounds__(512) void k_agg(AggArgs a) {
           whist(s_evh + (4 + d) * kRadixBins, (uint32_t)(et1 >> (8 * d)) & 0xFFu, ev);
         }
     }
+  }  // j
   }
+
   n_m = wsum(n_m);
   n_mm = wsum(n_mm);
   n_u = wsum(n_u);

@@ -184,35 +184,54 @@ __global__ __launch_bounds__(256) void k_ingest(IngestArgs a) {
 
   uint64_t n_valid = 0, n_badk = 0, n_badr = 0, n_begin = 0;
   uint64_t ts_min = kU64Max, ts_max = 0, ctx_min = kU64Max, ctx_max = 0;
-  const uint64_t stride = (uint64_t)gridDim.x * 256;
-  // Every lane of a wave iterates the same number of times (ballots below).
-  const uint64_t first = (uint64_t)blockIdx.x * 256 + (threadIdx.x & ~63u);
+  // Each wave takes 4 x 64 consecutive records per step (4 loads in flight
+  // per lane); every lane of a wave iterates the same number of times.
+  constexpr int kPer = 4;
+  const uint64_t stride = (uint64_t)gridDim.x * 256 * kPer;
+  const uint32_t lane = threadIdx.x & 63;
+  const uint64_t first = ((uint64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * (64 * kPer);
   for (uint64_t base = first; base < a.n; base += stride) {
-    const uint64_t i = base + (threadIdx.x & 63);
-    bool valid = false;
-    uint32_t ctx = 0;
-    if (i < a.n) {
-      const uint4 r = a.rec[i];
-      const uint64_t ts = (uint64_t)r.x | ((uint64_t)r.y << 32);
-      ctx = r.z;
-      const uint32_t region = r.w & 0xFFFFu;
-      const uint32_t kind = (r.w >> 16) & 0xFFu;
-      if (kind != 1 && kind != 2) {
-        n_badk++;
-      } else if (region >= a.R) {
-        n_badr++;
-      } else {
-        valid = true;
-        n_valid++;
-        n_begin += (kind == 1);
-        ts_min = ts < ts_min ? ts : ts_min;
-        ts_max = ts > ts_max ? ts : ts_max;
-        ctx_min = ctx < ctx_min ? ctx : ctx_min;
-        ctx_max = ctx > ctx_max ? ctx : ctx_max;
-      }
+    uint4 r[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const uint64_t i = base + (uint64_t)j * 64 + lane;
+      r[j] = a.rec[i < a.n ? i : a.n - 1];
     }
 #pragma unroll
-    for (int d = 0; d < 4; ++d) wave_hist_add(s_hist[d], (ctx >> (8 * d)) & 0xFFu, valid);
+    for (int j = 0; j < kPer; ++j) {
+      const uint64_t i = base + (uint64_t)j * 64 + lane;
+      const uint64_t ts = (uint64_t)r[j].x | ((uint64_t)r[j].y << 32);
+      const uint32_t ctx = r[j].z;
+      const uint32_t region = r[j].w & 0xFFFFu;
+      const uint32_t kind = (r[j].w >> 16) & 0xFFu;
+      const bool in = i < a.n;
+      const bool kind_ok = kind == 1 || kind == 2;
+      const bool valid = in && kind_ok && region < a.R;
+      n_badk += in && !kind_ok;
+      n_badr += in && kind_ok && region >= a.R;
+      n_valid += valid;
+      n_begin += valid && kind == 1;
+      ts_min = valid && ts < ts_min ? ts : ts_min;
+      ts_max = valid && ts > ts_max ? ts : ts_max;
+      ctx_min = valid && ctx < ctx_min ? ctx : ctx_min;
+      ctx_max = valid && ctx > ctx_max ? ctx : ctx_max;
+      // Context digit histograms.  Trace buffers hold runs of one context,
+      // so a wave whose valid records share a context adds with one atomic
+      // per digit; otherwise lanes with equal digits are found by ballots.
+      const uint64_t vm = __ballot(valid);
+      if (vm == 0) continue;
+      const uint32_t c0 = __shfl(ctx, __ffsll((unsigned long long)vm) - 1);
+      if (__ballot(valid && ctx != c0) == 0) {
+        if (lane == 0) {
+          const uint32_t nv = (uint32_t)__popcll(vm);
+#pragma unroll
+          for (int d = 0; d < 4; ++d) atomicAdd(&s_hist[d][(c0 >> (8 * d)) & 0xFFu], nv);
+        }
+      } else {
+#pragma unroll
+        for (int d = 0; d < 4; ++d) wave_hist_add(s_hist[d], (ctx >> (8 * d)) & 0xFFu, valid);
+      }
+    }
   }
   n_valid = wave_sum(n_valid);
   n_badk = wave_sum(n_badk);
@@ -265,7 +284,7 @@ __global__ __launch_bounds__(256) void k_ingest(IngestArgs a) {
 
 hipError_t launch_ingest(const RunArgs& a, hipStream_t s) {
   IngestArgs ia{(const uint4*)a.rec, a.n, a.R, a.out.d_counters, a.w.rec_hist};
-  uint64_t blocks = ceil_div(a.n, 256 * 8);
+  uint64_t blocks = ceil_div(a.n, 256 * 4 * 4);
   if (blocks > 2048) blocks = 2048;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(k_ingest, dim3((uint32_t)blocks), dim3(256), 0, s, ia);
@@ -472,7 +491,7 @@ __global__ __launch_bounds__(256) void k_ts_hist(TsHistArgs a) {
 
 hipError_t launch_ts_hist(const RunArgs& a, hipStream_t s) {
   TsHistArgs ta{a.w.plan, {a.w.key[0], a.w.key[1]}, a.w.rec_hist};
-  uint64_t blocks = ceil_div(a.n, 256 * 8);
+  uint64_t blocks = ceil_div(a.n, 256 * 4 * 4);
   if (blocks > 2048) blocks = 2048;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(k_ts_hist, dim3((uint32_t)blocks), dim3(256), 0, s, ta);

@@ -351,8 +351,22 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(MergeArgs a) {
     }
     const uint32_t b0 = o0 - a0, b1 = o1 - a1;
     const uint32_t na = a1 - a0, nb = b1 - b0, cnt = o1 - o0;
-    for (uint32_t i = t; i < cnt; i += kMergeThreads)
-      s_e[i] = i < na ? src[s0 + a0 + i] : src[sp + b0 + (i - na)];
+    {
+      // all loads in flight before the first LDS store (indexes past the
+      // tile's end are clamped to its last element)
+      uint64_t v[kMergeItems];
+#pragma unroll
+      for (int j = 0; j < kMergeItems; ++j) {
+        const uint32_t i0 = t + (uint32_t)j * kMergeThreads;
+        const uint32_t i = i0 < cnt ? i0 : cnt - 1;
+        v[j] = i < na ? src[s0 + a0 + i] : src[sp + b0 + (i - na)];
+      }
+#pragma unroll
+      for (int j = 0; j < kMergeItems; ++j) {
+        const uint32_t i = t + (uint32_t)j * kMergeThreads;
+        if (i < cnt) s_e[i] = v[j];
+      }
+    }
     __syncthreads();
     const uint32_t d = t * kMergeItems;
     if (d < cnt) {
