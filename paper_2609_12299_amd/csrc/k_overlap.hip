@@ -400,24 +400,45 @@ __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
     const uint64_t gap = tn - t[i];
     if (gap == 0) continue;
     uint32_t cc[KM];
-    uint64_t gx[KM];
+    bool small = (gap >> 32) == 0;
 #pragma unroll
     for (int x = 0; x < KM; ++x) {
       cc[x] = c[x] > 0 ? (uint32_t)c[x] : 0u;
-      gx[x] = mul64x32(gap, cc[x]);
+      small = small && cc[x] < 65536u;
     }
+    if (small) {
+      // gap < 2^32 and counts < 2^16: each term is one 32 x 32 -> 64-bit
+      // multiply-add (pair products and pair counts fit 32 bits)
+      const uint32_t g32 = (uint32_t)gap;
 #pragma unroll
-    for (int x = 0; x < KM; ++x) {
+      for (int x = 0; x < KM; ++x) {
 #pragma unroll
-      for (int y = x; y < KM; ++y) {
-        if ((uint32_t)y >= K) continue;
-        const int pi = pair_index<KM>(x, y);
-        if (cc[x] && cc[y]) u[pi] += gap;
-        if (x != y) {
-          q[pi] += mul64x32(gx[x], cc[y]);
-        } else if (cc[x] > 1) {
-          const uint64_t pairs = (uint64_t)cc[x] * (cc[x] - 1) / 2;
-          q[pi] += gap * pairs;
+        for (int y = x; y < KM; ++y) {
+          if ((uint32_t)y >= K) continue;
+          const int pi = pair_index<KM>(x, y);
+          u[pi] += (cc[x] && cc[y]) ? (uint64_t)g32 : 0ull;
+          const uint32_t w = x != y ? __umul24(cc[x], cc[y])
+                                    : __umul24(cc[x], cc[x] - (cc[x] > 0)) >> 1;
+          q[pi] += (uint64_t)g32 * w;
+        }
+      }
+    } else {
+      uint64_t gx[KM];
+#pragma unroll
+      for (int x = 0; x < KM; ++x) gx[x] = mul64x32(gap, cc[x]);
+#pragma unroll
+      for (int x = 0; x < KM; ++x) {
+#pragma unroll
+        for (int y = x; y < KM; ++y) {
+          if ((uint32_t)y >= K) continue;
+          const int pi = pair_index<KM>(x, y);
+          if (cc[x] && cc[y]) u[pi] += gap;
+          if (x != y) {
+            q[pi] += mul64x32(gx[x], cc[y]);
+          } else if (cc[x] > 1) {
+            const uint64_t pairs = (uint64_t)cc[x] * (cc[x] - 1) / 2;
+            q[pi] += gap * pairs;
+          }
         }
       }
     }
