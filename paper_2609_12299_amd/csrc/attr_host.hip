@@ -51,7 +51,7 @@ struct Layout {
   size_t key[2], pay[2], ctxw[2], lb[2], mlb, slb, tiles, tree;
   size_t pop_ts, pop_reg, pushes, op_parent, op_sum;
   size_t inst, child_sum, hist_key, ov_mask, ov_q;
-  size_t push_pos, pop_pos, ctx_list, ctx_seg, seg_start, seg_split, seg_tile0, part, part_seg;
+  size_t push_pos, pop_pos, ctx_list, ctx_seg, seg_start, seg_split, seg_tile0, part;
   size_t total;
   uint64_t lb_words, tree_leaves, match_tiles, pool_cap, ctx_cap, tiles_cap;
 };
@@ -110,8 +110,7 @@ Layout make_layout(const argus_attr_config& c, uint64_t n, bool own_instances) {
   L.seg_start = take(sizeof(uint32_t) * (L.ctx_cap + 1));
   L.seg_split = take(sizeof(uint32_t) * (L.ctx_cap + 1));
   L.seg_tile0 = take(sizeof(uint32_t) * (L.ctx_cap + 1));
-  L.part = take(sizeof(uint32_t) * (L.tiles_cap + 1));
-  L.part_seg = take(sizeof(uint32_t) * (L.tiles_cap + 1));
+  L.part = take(32 * L.tiles_cap);
   L.total = o;
   return L;
 }
@@ -285,7 +284,6 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
   w.seg_split = (uint32_t*)(base + L.seg_split);
   w.seg_tile0 = (uint32_t*)(base + L.seg_tile0);
   w.part = (uint32_t*)(base + L.part);
-  w.part_seg = (uint32_t*)(base + L.part_seg);
   w.ctx_cap = L.ctx_cap;
   w.tiles_cap = L.tiles_cap;
   w.lb_words = L.lb_words;

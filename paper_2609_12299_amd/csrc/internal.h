@@ -176,8 +176,7 @@ struct Work {
   uint32_t* seg_start;  // [ctx_cap + 1]
   uint32_t* seg_split;  // [ctx_cap + 1]
   uint32_t* seg_tile0;  // [ctx_cap + 1] first merge tile of each segment
-  uint32_t* part;       // [tiles_cap + 1] events taken from the first run before each tile
-  uint32_t* part_seg;   // [tiles_cap] segment of each tile
+  uint32_t* part;       // [tiles_cap] merge tasks, 32 B each (k_merge.hip)
   uint64_t ctx_cap;
   uint64_t tiles_cap;
   uint64_t lb_words;    // capacity of each lb array in words

@@ -235,14 +235,19 @@ __device__ __forceinline__ uint32_t corank(const uint64_t* A, uint32_t la, const
   return lo;
 }
 
+// One merge tile: where its slices of the two runs start, their lengths,
+// and where its output starts (absolute sorted positions).
+struct MergeTask {
+  uint32_t a_pos, na, b_pos, nb, out_pos, pad0, pad1, pad2;
+};
+
 struct MPartArgs {
   const DevPlan* plan;
   const uint64_t* ev[2];
   const uint32_t* seg_start;
   const uint32_t* seg_split;
   const uint32_t* seg_tile0;
-  uint32_t* part;
-  uint32_t* part_seg;
+  MergeTask* task;
   uint64_t* counters;
   int round;
 };
@@ -266,17 +271,24 @@ __global__ __launch_bounds__(256) void k_mpart(MPartArgs a) {
     }
     const uint32_t s0 = a.seg_start[lo], sp = a.seg_split[lo];
     const uint32_t s1 = lo + 1 < n_segs ? a.seg_start[lo + 1] : end;
-    if (!(s0 <= sp && sp <= s1 && s1 <= end)) {
+    MergeTask tk{0, 0, 0, 0, 0, 0, 0, 0};
+    if (s0 <= sp && sp <= s1 && s1 <= end) {
+      const uint32_t L = s1 - s0, la = sp - s0, lb = s1 - sp;
+      const uint64_t d0w = (k - a.seg_tile0[lo]) * (uint64_t)kMergeTile;
+      const uint32_t d0 = d0w < L ? (uint32_t)d0w : L;
+      const uint32_t d1 = d0 + kMergeTile < L ? d0 + kMergeTile : L;
+      const uint64_t* A = src + s0;
+      const uint64_t* B = src + sp;
+      const uint32_t a0 = corank(A, la, B, lb, d0), a1 = corank(A, la, B, lb, d1);
+      tk.a_pos = s0 + a0;
+      tk.na = a1 - a0;
+      tk.b_pos = sp + (d0 - a0);
+      tk.nb = (d1 - a1) - (d0 - a0);
+      tk.out_pos = s0 + d0;
+    } else {
       flag_internal_error(a.counters, 256);
-      a.part[k] = 0;
-      a.part_seg[k] = lo;
-      continue;
     }
-    const uint32_t d = (uint32_t)(k - a.seg_tile0[lo]) * (uint32_t)kMergeTile;
-    const uint64_t* A = src + s0;
-    const uint64_t* B = src + sp;
-    a.part[k] = corank(A, sp - s0, B, s1 - sp, d < s1 - s0 ? d : s1 - s0);
-    a.part_seg[k] = lo;
+    a.task[k] = tk;
   }
 }
 
@@ -287,8 +299,7 @@ hipError_t launch_mpart(const RunArgs& a, int round, hipStream_t s) {
   m.seg_start = a.w.seg_start;
   m.seg_split = a.w.seg_split;
   m.seg_tile0 = a.w.seg_tile0;
-  m.part = a.w.part;
-  m.part_seg = a.w.part_seg;
+  m.task = (MergeTask*)a.w.part;
   m.counters = a.out.d_counters;
   m.round = round;
   uint64_t blocks = ceil_div(a.w.tiles_cap, 256);
@@ -303,89 +314,102 @@ hipError_t launch_mpart(const RunArgs& a, int round, hipStream_t s) {
 struct MergeArgs {
   const DevPlan* plan;
   uint64_t* ev[2];
-  const uint32_t* seg_start;
-  const uint32_t* seg_split;
-  const uint32_t* seg_tile0;
-  const uint32_t* part;
-  const uint32_t* part_seg;
-  uint32_t* tile_ctr;
+  const MergeTask* task;
   uint64_t* counters;
   int round;
 };
 
-// One output tile of 4096 events per iteration: its slices of the two runs
-// are read into LDS (two contiguous ranges), each thread finds its own split
-// in LDS and merges 8 outputs.
+// A task is usable if its slices and output lie inside the merged range.
+__device__ __forceinline__ bool task_ok(const MergeTask& t, uint32_t end) {
+  return t.na + t.nb <= (uint32_t)kMergeTile && t.na + t.nb > 0 && t.a_pos + t.na <= end &&
+         t.b_pos + t.nb <= end && t.out_pos + t.na + t.nb <= end;
+}
+
+// Loads this thread's share of a tile's inputs (element t + 512 j; past the
+// end: the last element again, never stored).
+__device__ __forceinline__ void load_task(const uint64_t* src, const MergeTask& tk, uint32_t t,
+                                          uint64_t* v) {
+  const uint32_t cnt = tk.na + tk.nb;
+#pragma unroll
+  for (int j = 0; j < kMergeItems; ++j) {
+    const uint32_t i0 = t + (uint32_t)j * kMergeThreads;
+    const uint32_t i = i0 < cnt ? i0 : cnt - 1;
+    v[j] = i < tk.na ? src[tk.a_pos + i] : src[tk.b_pos + (i - tk.na)];
+  }
+}
+
+// Static tiles (tile = block + k * grid; there is no dependency between
+// tiles).  Each tile's two input slices go through LDS; each thread finds
+// its own split and merges 8 outputs, which are staged in LDS again so that
+// the stores are contiguous.  The next tile's task and inputs are loaded
+// while the current one is merged.
 __global__ __launch_bounds__(kMergeThreads) void k_merge(MergeArgs a) {
   const DevPlan* p = a.plan;
   if (!p->ev_merge || (uint32_t)a.round >= p->m_rounds) return;
-  __shared__ uint64_t s_e[kMergeTile];
-  __shared__ uint32_t s_tile;
+  __shared__ uint64_t s_e[kMergeTile + 1];  // + 1: reads past a run stay inside
   const MergeRound mr = p->mr[a.round];
-  const uint32_t n_segs = (uint32_t)mr.n_segs;
   const uint64_t n_tiles = mr.n_tiles;
   const uint32_t end = (uint32_t)p->m_end;
   const uint64_t* src = a.ev[mr.src];
   uint64_t* dst = a.ev[mr.dst];
   const uint32_t t = threadIdx.x;
-  for (;;) {
-    if (t == 0) s_tile = atomicAdd(&a.tile_ctr[kCtrMerge + a.round], 1u);
-    __syncthreads();
-    const uint64_t k = s_tile;
-    if (k >= n_tiles) break;
-    const uint32_t sg = a.part_seg[k];
-    const uint32_t s0 = a.seg_start[sg], sp = a.seg_split[sg];
-    const uint32_t s1 = sg + 1 < n_segs ? a.seg_start[sg + 1] : end;
-    const uint32_t L = s1 - s0, la = sp - s0;
-    const uint32_t o0 = (uint32_t)(k - a.seg_tile0[sg]) * (uint32_t)kMergeTile;
-    const uint32_t o1 = o0 + kMergeTile < L ? o0 + kMergeTile : L;
-    const uint32_t a0 = a.part[k];
-    const uint32_t a1 = o1 == L ? la : a.part[k + 1];
-    const bool ok = sg < n_segs && s0 <= sp && sp <= s1 && s1 <= end && o0 < o1 && a0 <= a1 &&
-                    a1 <= la && a0 <= o0 && a1 <= o1 && o1 - a1 >= o0 - a0 &&
-                    o1 - a1 <= L - la;
+  uint64_t k = blockIdx.x;
+  if (k >= n_tiles) return;
+  MergeTask tk = a.task[k];
+  bool ok = task_ok(tk, end);
+  uint64_t v[kMergeItems];
+  if (ok) load_task(src, tk, t, v);
+  for (; k < n_tiles; k += gridDim.x) {
+    const uint64_t kn = k + gridDim.x;
+    MergeTask tn{0, 0, 0, 0, 0, 0, 0, 0};
+    if (kn < n_tiles) tn = a.task[kn];
     if (!ok) {
       if (t == 0) flag_internal_error(a.counters, 256);
-      __syncthreads();
-      continue;
-    }
-    const uint32_t b0 = o0 - a0, b1 = o1 - a1;
-    const uint32_t na = a1 - a0, nb = b1 - b0, cnt = o1 - o0;
-    {
-      // all loads in flight before the first LDS store (indexes past the
-      // tile's end are clamped to its last element)
-      uint64_t v[kMergeItems];
-#pragma unroll
-      for (int j = 0; j < kMergeItems; ++j) {
-        const uint32_t i0 = t + (uint32_t)j * kMergeThreads;
-        const uint32_t i = i0 < cnt ? i0 : cnt - 1;
-        v[j] = i < na ? src[s0 + a0 + i] : src[sp + b0 + (i - na)];
-      }
+    } else {
+      const uint32_t na = tk.na, nb = tk.nb, cnt = na + nb;
 #pragma unroll
       for (int j = 0; j < kMergeItems; ++j) {
         const uint32_t i = t + (uint32_t)j * kMergeThreads;
         if (i < cnt) s_e[i] = v[j];
       }
-    }
-    __syncthreads();
-    const uint32_t d = t * kMergeItems;
-    if (d < cnt) {
-      const uint64_t* A = s_e;
-      const uint64_t* B = s_e + na;
-      uint32_t ia = corank(A, na, B, nb, d), ib = d - ia;
-      uint64_t* out = dst + s0 + o0 + d;
-      const uint32_t m = cnt - d < (uint32_t)kMergeItems ? cnt - d : (uint32_t)kMergeItems;
+      __syncthreads();
+      // the next tile's inputs, in flight during this merge
+      const bool okn = kn < n_tiles && task_ok(tn, end);
+      if (okn) load_task(src, tn, t, v);
+      uint64_t o[kMergeItems];
+      const uint32_t d = t * kMergeItems;
+      if (d < cnt) {
+        const uint64_t* A = s_e;
+        const uint64_t* B = s_e + na;
+        uint32_t ia = corank(A, na, B, nb, d), ib = d - ia;
+#pragma unroll
+        for (int j = 0; j < kMergeItems; ++j) {
+          const bool take_a = ia < na && (ib >= nb || mkey(A[ia]) <= mkey(B[ib]));
+          o[j] = take_a ? A[ia] : B[ib < nb ? ib : nb];
+          ia += take_a;
+          ib += !take_a;
+        }
+      }
+      __syncthreads();
+      if (d < cnt) {
+#pragma unroll
+        for (int j = 0; j < kMergeItems; ++j)
+          if (d + j < cnt) s_e[d + j] = o[j];
+      }
+      __syncthreads();
 #pragma unroll
       for (int j = 0; j < kMergeItems; ++j) {
-        if ((uint32_t)j >= m) break;
-        const bool take_a = ia < na && (ib >= nb || mkey(A[ia]) <= mkey(B[ib]));
-        const uint64_t v = take_a ? A[ia] : B[ib];
-        ia += take_a;
-        ib += !take_a;
-        out[j] = v;
+        const uint32_t i = t + (uint32_t)j * kMergeThreads;
+        if (i < cnt) dst[tk.out_pos + i] = s_e[i];
       }
+      __syncthreads();
+      ok = okn;
     }
-    __syncthreads();
+    tk = tn;
+    if (kn < n_tiles && !ok && task_ok(tn, end)) {
+      ok = true;
+      load_task(src, tn, t, v);
+    }
   }
 }
 
@@ -393,12 +417,7 @@ hipError_t launch_merge(const RunArgs& a, int round, hipStream_t s) {
   MergeArgs m{};
   m.plan = a.w.plan;
   for (int b = 0; b < 2; ++b) m.ev[b] = a.w.key[b];
-  m.seg_start = a.w.seg_start;
-  m.seg_split = a.w.seg_split;
-  m.seg_tile0 = a.w.seg_tile0;
-  m.part = a.w.part;
-  m.part_seg = a.w.part_seg;
-  m.tile_ctr = a.w.tile_ctr;
+  m.task = (const MergeTask*)a.w.part;
   m.counters = a.out.d_counters;
   m.round = round;
   uint64_t blocks = a.w.tiles_cap ? a.w.tiles_cap : 1;
