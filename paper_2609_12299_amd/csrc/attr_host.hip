@@ -106,10 +106,12 @@ Layout make_layout(const argus_attr_config& c, uint64_t n, bool own_instances) {
   L.push_pos = take(ev ? sizeof(uint32_t) * L.pool_cap : 0);
   L.pop_pos = take(ev ? sizeof(uint32_t) * L.pool_cap : 0);
   L.ctx_list = take(sizeof(uint2) * L.ctx_cap);
-  L.ctx_seg = take(sizeof(uint32_t) * L.ctx_cap);
-  L.seg_start = take(sizeof(uint32_t) * (L.ctx_cap + 1));
-  L.seg_split = take(sizeof(uint32_t) * (L.ctx_cap + 1));
-  L.seg_tile0 = take(sizeof(uint32_t) * (L.ctx_cap + 1));
+  // segment arrays of every merge round, ctx_cap + 1 entries per round
+  const uint64_t segs = ev ? kMaxMergeRounds * (L.ctx_cap + 1) : 0;
+  L.ctx_seg = take(sizeof(uint32_t) * segs);
+  L.seg_start = take(sizeof(uint32_t) * segs);
+  L.seg_split = take(sizeof(uint32_t) * segs);
+  L.seg_tile0 = take(sizeof(uint32_t) * segs);
   L.part = take(32 * L.tiles_cap);
   L.total = o;
   return L;
@@ -362,8 +364,8 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
         {"mseg4", "mpart4", "merge4"}, {"mseg5", "mpart5", "merge5"},
         {"mseg6", "mpart6", "merge6"}, {"mseg7", "mpart7", "merge7"}};
     const int rounds = a.shift < (uint32_t)kMaxMergeRounds ? (int)a.shift : kMaxMergeRounds;
+    if (rounds > 0 && !step("mseg", launch_mseg(a, rounds, s))) return ARGUS_E_HIP;
     for (int r = 0; r < rounds; ++r) {
-      if (!step(mnames[r][0], launch_mseg(a, r, s))) return ARGUS_E_HIP;
       if (!step(mnames[r][1], launch_mpart(a, r, s))) return ARGUS_E_HIP;
       if (!step(mnames[r][2], launch_merge(a, r, s))) return ARGUS_E_HIP;
     }

@@ -172,10 +172,10 @@ struct Work {
   uint32_t* push_pos;   // sorted position of each pushed BEGIN (pool layout)
   uint32_t* pop_pos;    // sorted position of each popping END (pool layout)
   uint2* ctx_list;      // [ctx_cap] (context key, first sorted position)
-  uint32_t* ctx_seg;    // [ctx_cap] segment of each context (merge round)
-  uint32_t* seg_start;  // [ctx_cap + 1]
-  uint32_t* seg_split;  // [ctx_cap + 1]
-  uint32_t* seg_tile0;  // [ctx_cap + 1] first merge tile of each segment
+  uint32_t* ctx_seg;    // [rounds][ctx_cap + 1] segment of each context
+  uint32_t* seg_start;  // [rounds][ctx_cap + 1]
+  uint32_t* seg_split;  // [rounds][ctx_cap + 1]
+  uint32_t* seg_tile0;  // [rounds][ctx_cap + 1] first merge tile of each segment
   uint32_t* part;       // [tiles_cap] merge tasks, 32 B each (k_merge.hip)
   uint64_t ctx_cap;
   uint64_t tiles_cap;
@@ -258,7 +258,7 @@ hipError_t launch_hist(const RunArgs& a, hipStream_t s);
 hipError_t launch_ev_plan(const RunArgs& a, hipStream_t s);
 hipError_t launch_ev_clear(const RunArgs& a, hipStream_t s);
 hipError_t launch_mplan(const RunArgs& a, hipStream_t s);
-hipError_t launch_mseg(const RunArgs& a, int round, hipStream_t s);
+hipError_t launch_mseg(const RunArgs& a, int rounds, hipStream_t s);
 hipError_t launch_mpart(const RunArgs& a, int round, hipStream_t s);
 hipError_t launch_merge(const RunArgs& a, int round, hipStream_t s);
 hipError_t launch_sweep(const RunArgs& a, hipStream_t s);

@@ -133,16 +133,22 @@ struct MSegArgs {
   uint32_t* seg_start;
   uint32_t* seg_split;
   uint32_t* seg_tile0;
-  int round;
+  uint64_t stride;  // per-round stride of the segment arrays
 };
 
-// Segments of a round: maximal runs of contexts with equal ctx >> (bit + 1);
-// the split is where bit `bit` becomes 1.  One block.
+// Segments of every round (block r: round r): maximal runs of contexts with
+// equal ctx >> (bit + 1); the split is where bit `bit` becomes 1.  They
+// depend on the context list only, so all rounds are planned at once.
 __global__ __launch_bounds__(1024) void k_mseg(MSegArgs a) {
   DevPlan* p = a.plan;
-  if (!p->ev_merge || (uint32_t)a.round >= p->m_rounds) return;
+  const int round = blockIdx.x;
+  if (!p->ev_merge || (uint32_t)round >= p->m_rounds) return;
+  a.ctx_seg += round * a.stride;
+  a.seg_start += round * a.stride;
+  a.seg_split += round * a.stride;
+  a.seg_tile0 += round * a.stride;
   __shared__ uint32_t s_w[16];
-  const uint32_t bit = p->mr[a.round].bit;
+  const uint32_t bit = p->mr[round].bit;
   const uint32_t nc = p->m_nctx;
   const uint32_t end = (uint32_t)p->m_end;
   const uint32_t t = threadIdx.x;
@@ -203,15 +209,15 @@ __global__ __launch_bounds__(1024) void k_mseg(MSegArgs a) {
   }
   if (t == 0) {
     a.seg_tile0[n_segs] = carry;
-    p->mr[a.round].n_segs = n_segs;
-    p->mr[a.round].n_tiles = carry;
+    p->mr[round].n_segs = n_segs;
+    p->mr[round].n_tiles = carry;
   }
 }
 
-hipError_t launch_mseg(const RunArgs& a, int round, hipStream_t s) {
+hipError_t launch_mseg(const RunArgs& a, int rounds, hipStream_t s) {
   MSegArgs m{a.w.plan, a.w.ctx_list, a.w.ctx_seg, a.w.seg_start, a.w.seg_split, a.w.seg_tile0,
-             round};
-  hipLaunchKernelGGL(k_mseg, dim3(1), dim3(1024), 0, s, m);
+             a.w.ctx_cap + 1};
+  hipLaunchKernelGGL(k_mseg, dim3((uint32_t)(rounds > 0 ? rounds : 1)), dim3(1024), 0, s, m);
   return hipGetLastError();
 }
 
@@ -250,6 +256,7 @@ struct MPartArgs {
   MergeTask* task;
   uint64_t* counters;
   int round;
+  uint64_t stride;
 };
 
 __global__ __launch_bounds__(256) void k_mpart(MPartArgs a) {
@@ -260,21 +267,25 @@ __global__ __launch_bounds__(256) void k_mpart(MPartArgs a) {
   const uint64_t n_tiles = mr.n_tiles;
   const uint32_t end = (uint32_t)p->m_end;
   const uint64_t* src = a.ev[mr.src];
+  const uint64_t off = (uint64_t)a.round * a.stride;
+  const uint32_t* seg_start = a.seg_start + off;
+  const uint32_t* seg_split = a.seg_split + off;
+  const uint32_t* seg_tile0 = a.seg_tile0 + off;
   for (uint64_t k = (uint64_t)blockIdx.x * 256 + threadIdx.x; k < n_tiles;
        k += (uint64_t)gridDim.x * 256) {
     // segment of tile k: the last one whose first tile is <= k
     uint32_t lo = 0, hi = n_segs;
     while (hi - lo > 1) {
       const uint32_t mid = (lo + hi) >> 1;
-      if (a.seg_tile0[mid] <= k) lo = mid;
+      if (seg_tile0[mid] <= k) lo = mid;
       else hi = mid;
     }
-    const uint32_t s0 = a.seg_start[lo], sp = a.seg_split[lo];
-    const uint32_t s1 = lo + 1 < n_segs ? a.seg_start[lo + 1] : end;
+    const uint32_t s0 = seg_start[lo], sp = seg_split[lo];
+    const uint32_t s1 = lo + 1 < n_segs ? seg_start[lo + 1] : end;
     MergeTask tk{0, 0, 0, 0, 0, 0, 0, 0};
     if (s0 <= sp && sp <= s1 && s1 <= end) {
       const uint32_t L = s1 - s0, la = sp - s0, lb = s1 - sp;
-      const uint64_t d0w = (k - a.seg_tile0[lo]) * (uint64_t)kMergeTile;
+      const uint64_t d0w = (k - seg_tile0[lo]) * (uint64_t)kMergeTile;
       const uint32_t d0 = d0w < L ? (uint32_t)d0w : L;
       const uint32_t d1 = d0 + kMergeTile < L ? d0 + kMergeTile : L;
       const uint64_t* A = src + s0;
@@ -302,6 +313,7 @@ hipError_t launch_mpart(const RunArgs& a, int round, hipStream_t s) {
   m.task = (MergeTask*)a.w.part;
   m.counters = a.out.d_counters;
   m.round = round;
+  m.stride = a.w.ctx_cap + 1;
   uint64_t blocks = ceil_div(a.w.tiles_cap, 256);
   if (blocks > 1024) blocks = 1024;
   if (blocks < 1) blocks = 1;
