@@ -32,6 +32,9 @@ def flags() -> list[str]:
         "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
         # no packed-FP32 instructions anywhere in the device code
         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+        # uniform-address atomics: reduce across the wave with DPP, not with a
+        # scalar loop over the active lanes
+        "-mllvm", "-amdgpu-atomic-optimizer-strategy=DPP",
         "-Wall", "-Wno-unused-function", "-Wno-unused-variable",
         "-I", os.path.join(HERE, "..", "include"),
     ]

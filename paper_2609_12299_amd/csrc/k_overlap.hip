@@ -17,11 +17,9 @@
 // group, adds gap * [c_A > 0 and c_B > 0] to U and gap * c_A * c_B (or
 // gap * c_A (c_A - 1) / 2 for A == B) to Q.  Equal times give zero gaps, so
 // the order among ties does not matter.
-#include "internal.h"
+#include "sweep_common.h"
 
 namespace argus {
-
-constexpr int kSweepQWords = 36;  // stride of the per-group U and Q rows
 
 template <int KM>
 struct Counts {
@@ -41,16 +39,6 @@ struct SweepArgs {
   uint32_t* tile_ctr;
   uint64_t* counters;
 };
-
-template <int KM>
-__host__ __device__ constexpr int pair_index(int a, int b) {
-  return a * KM - a * (a - 1) / 2 + (b - a);
-}
-
-// a * b mod 2^64 for a 32-bit b
-__device__ __forceinline__ uint64_t mul64x32(uint64_t a, uint32_t b) {
-  return (uint64_t)(uint32_t)a * b + ((uint64_t)((uint32_t)(a >> 32) * b) << 32);
-}
 
 template <int KM>
 __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
@@ -82,8 +70,7 @@ __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
     uint64_t k = raw;
     if (mfmt) {
       k = raw >> kEvCodeBits;
-      const uint32_t c = (uint32_t)(raw & ((1u << kEvCodeBits) - 1u));
-      pay = c ? ((c - 1u) >> 1) | (((c - 1u) & 1u) << 8) : 0xFFu;
+      pay = ev_word_pay(raw);
     }
     *g = wide ? cw : (ks.ts_bits >= 64 ? 0u : (uint32_t)(k >> ks.ts_bits));
     *t = wide ? k : (k & ks.ts_mask);
@@ -399,49 +386,7 @@ __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
     if (gn != g[i]) continue;  // last event of its group (or of the data)
     const uint64_t gap = tn - t[i];
     if (gap == 0) continue;
-    uint32_t cc[KM];
-    bool small = (gap >> 32) == 0;
-#pragma unroll
-    for (int x = 0; x < KM; ++x) {
-      cc[x] = c[x] > 0 ? (uint32_t)c[x] : 0u;
-      small = small && cc[x] < 65536u;
-    }
-    if (small) {
-      // gap < 2^32 and counts < 2^16: each term is one 32 x 32 -> 64-bit
-      // multiply-add (pair products and pair counts fit 32 bits)
-      const uint32_t g32 = (uint32_t)gap;
-#pragma unroll
-      for (int x = 0; x < KM; ++x) {
-#pragma unroll
-        for (int y = x; y < KM; ++y) {
-          if ((uint32_t)y >= K) continue;
-          const int pi = pair_index<KM>(x, y);
-          u[pi] += (cc[x] && cc[y]) ? (uint64_t)g32 : 0ull;
-          const uint32_t w = x != y ? __umul24(cc[x], cc[y])
-                                    : __umul24(cc[x], cc[x] - (cc[x] > 0)) >> 1;
-          q[pi] += (uint64_t)g32 * w;
-        }
-      }
-    } else {
-      uint64_t gx[KM];
-#pragma unroll
-      for (int x = 0; x < KM; ++x) gx[x] = mul64x32(gap, cc[x]);
-#pragma unroll
-      for (int x = 0; x < KM; ++x) {
-#pragma unroll
-        for (int y = x; y < KM; ++y) {
-          if ((uint32_t)y >= K) continue;
-          const int pi = pair_index<KM>(x, y);
-          if (cc[x] && cc[y]) u[pi] += gap;
-          if (x != y) {
-            q[pi] += mul64x32(gx[x], cc[y]);
-          } else if (cc[x] > 1) {
-            const uint64_t pairs = (uint64_t)cc[x] * (cc[x] - 1) / 2;
-            q[pi] += gap * pairs;
-          }
-        }
-      }
-    }
+    sweep_gap<KM>(u, q, c, gap, K);
   }
   // Whole waves in one group reduce in registers; everything else goes
   // through LDS atomics.
