@@ -83,13 +83,15 @@ __device__ __forceinline__ void unpack_agg(uint64_t v, Fn* f, uint32_t* nbh) {
   *nbh = (uint32_t)(v & 0xFFFull) | ((uint32_t)((v >> 41) & 0xFFFull) << 16);
 }
 
-// Min tree over the tile's 2048 leaves with fan-out 8, in LDS:
-//   level 0: leaves [0, 2048), level 1: 256 nodes at 2048, level 2: 32 nodes
-//   at 2304, level 3: 4 nodes at 2336 (padded to 8).  Every group of 8
-//   siblings is 32-byte aligned and read with two 16-byte loads.
-constexpr int kT1 = kMatchTile;
-constexpr int kT2 = kT1 + kMatchTile / 8;
-constexpr int kT3 = kT2 + kMatchTile / 64;
+// Min tree over the tile's 2048 leaves with fan-out 8, in LDS.  A leaf is
+// the pair (x + 1, rank | region << 11): the local BEGIN rank and the region
+// of the record (meaningful for BEGINs, the only records a search can hit),
+// so that one read of a leaf group answers a search.  The upper levels live
+// in their own array: level 1 (256 nodes) at 0, level 2 (32) at 256,
+// level 3 (4, padded to 8) at 288.  Every group of 8 siblings is 32-byte
+// aligned.
+constexpr int kU1 = 0, kU2 = 256, kU3 = 288, kUpSize = 296;
+constexpr uint32_t kNoHit = 0xFFFFFFFFu;
 static_assert(kMatchTile == 2048, "tree levels assume 2048 leaves");
 
 // Last j < lim of the 8 siblings at g whose value is <= v, or -1.
@@ -103,26 +105,44 @@ __device__ __forceinline__ int last_le8(const uint32_t* g, uint32_t lim, uint32_
   return r;
 }
 
-// Last leaf q < 8 * chunk whose value is <= v, or -1: climb from the
-// chunk's level-1 node through left siblings, then descend to the leaf.
-__device__ __forceinline__ int psv8(const uint32_t* t, uint32_t chunk, uint32_t v) {
-  const uint32_t i1 = chunk, i2 = chunk >> 3, i3 = chunk >> 6;
-  int n1 = -1, n2 = -1;
-  int j = last_le8(t + kT1 + (i1 & ~7u), i1 & 7u, v);
+// The last of 8 leaves whose x + 1 is <= v (one exists): its second word.
+__device__ __forceinline__ uint32_t leaf_hit8(const uint2* g, uint32_t v) {
+  const uint4 a = *(const uint4*)g, b = *(const uint4*)(g + 2);
+  const uint4 c = *(const uint4*)(g + 4), d = *(const uint4*)(g + 6);
+  const uint32_t x[8] = {a.x, a.z, b.x, b.z, c.x, c.z, d.x, d.z};
+  const uint32_t y[8] = {a.y, a.w, b.y, b.w, c.y, c.w, d.y, d.w};
+  uint32_t r = kNoHit;
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+    if (x[j] <= v) r = y[j];
+  return r;
+}
+
+// Second word of the last leaf q < 8 * chunk with x + 1 <= v, or kNoHit.
+// g1 holds the chunk's level-1 sibling group (read once per thread).
+__device__ __forceinline__ uint32_t psv_hit(const uint2* leaf, const uint32_t* up,
+                                            const uint32_t (&g1)[8], uint32_t chunk, uint32_t v) {
+  int j = -1;
+#pragma unroll
+  for (int k = 0; k < 8; ++k)
+    if ((uint32_t)k < (chunk & 7u) && g1[k] <= v) j = k;
+  int n1;
   if (j >= 0) {
-    n1 = (int)(i1 & ~7u) + j;
+    n1 = (int)(chunk & ~7u) + j;
   } else {
-    j = last_le8(t + kT2 + (i2 & ~7u), i2 & 7u, v);
+    const uint32_t i2 = chunk >> 3, i3 = chunk >> 6;
+    int n2;
+    j = last_le8(up + kU2 + (i2 & ~7u), i2 & 7u, v);
     if (j >= 0) {
       n2 = (int)(i2 & ~7u) + j;
     } else {
-      j = last_le8(t + kT3, i3, v);
-      if (j < 0) return -1;
-      n2 = j * 8 + last_le8(t + kT2 + j * 8, 8u, v);
+      j = last_le8(up + kU3, i3, v);
+      if (j < 0) return kNoHit;
+      n2 = j * 8 + last_le8(up + kU2 + j * 8, 8u, v);
     }
-    n1 = n2 * 8 + last_le8(t + kT1 + n2 * 8, 8u, v);
+    n1 = n2 * 8 + last_le8(up + kU1 + n2 * 8, 8u, v);
   }
-  return n1 * 8 + last_le8(t + n1 * 8, 8u, v);
+  return leaf_hit8(leaf + n1 * 8, v);
 }
 
 struct MatchArgs {
@@ -161,19 +181,18 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   constexpr int IT = kMatchItems;
 
   __shared__ uint32_t s_tile;
-  __shared__ uint32_t s_tree[2 * kMatchTile];  // min tree over x + 1, then out-of-tile child sums
+  __shared__ uint2 s_leaf[kMatchTile];         // tree leaves, then out-of-tile child sums
+  __shared__ uint32_t s_up[kUpSize];           // upper tree levels
   __shared__ uint64_t s_tend[kMatchTile];      // t_end of each local BEGIN closed in the tile
   __shared__ uint64_t s_cs[kMatchTile];        // child sums of each local BEGIN
-  __shared__ uint16_t s_lbr[kMatchTile];       // local BEGIN rank of each position
   __shared__ uint16_t s_ereg[kMatchTile];      // end region of each local BEGIN (0xFFFF: open)
-  __shared__ uint16_t s_breg[kMatchTile];      // region of each local BEGIN
   __shared__ uint32_t s_lastctx[kMatchThreads];
   __shared__ Fn s_wfn[4];
   __shared__ uint32_t s_wnb[4];
   __shared__ uint32_t s_prevctx, s_hasprev;
   __shared__ uint32_t s_first, s_lastp1, s_heads, s_lo, s_sout, s_maxlvl, s_orph;
   __shared__ uint32_t s_sin, s_nbpre_lo, s_nbpre_hi, s_hpre, s_need;
-  uint64_t* s_oc = (uint64_t*)s_tree;
+  uint64_t* s_oc = (uint64_t*)s_leaf;
 
   const KeySpace ks = P->rec;
   const bool wide = ks.wide != 0;
@@ -507,31 +526,27 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
     }
   }
   {
-    uint4* leaf4 = (uint4*)&s_tree[p0];
-    leaf4[0] = make_uint4(xp[0], xp[1], xp[2], xp[3]);
-    leaf4[1] = make_uint4(xp[4], xp[5], xp[6], xp[7]);
+    uint4* leaf4 = (uint4*)&s_leaf[p0];
+#pragma unroll
+    for (int q = 0; q < IT / 2; ++q)
+      leaf4[q] = make_uint4(xp[2 * q], lbr[2 * q] | (reg[2 * q] << 11), xp[2 * q + 1],
+                            lbr[2 * q + 1] | (reg[2 * q + 1] << 11));
     uint32_t m = xp[0];
 #pragma unroll
     for (int i = 1; i < IT; ++i) m = min(m, xp[i]);
-    s_tree[kT1 + tid] = m;
+    s_up[kU1 + tid] = m;
     m = min(m, (uint32_t)__shfl_xor(m, 1));
     m = min(m, (uint32_t)__shfl_xor(m, 2));
     m = min(m, (uint32_t)__shfl_xor(m, 4));
-    if ((lane & 7) == 0) s_tree[kT2 + (tid >> 3)] = m;
+    if ((lane & 7) == 0) s_up[kU2 + (tid >> 3)] = m;
     m = min(m, (uint32_t)__shfl_xor(m, 8));
     m = min(m, (uint32_t)__shfl_xor(m, 16));
     m = min(m, (uint32_t)__shfl_xor(m, 32));
     if (lane == 0) {
-      s_tree[kT3 + w] = m;
-      s_tree[kT3 + 4 + w] = 0xFFFFFFFFu;
+      s_up[kU3 + w] = m;
+      s_up[kU3 + 4 + w] = 0xFFFFFFFFu;
     }
   }
-#pragma unroll
-  for (int i = 0; i < IT; ++i)
-    if ((fb >> i) & 1u) {
-      s_lbr[p0 + i] = (uint16_t)lbr[i];
-      s_breg[lbr[i]] = (uint16_t)reg[i];
-    }
   if (lo != 0xFFFFFFFFu) atomicMin(&s_lo, lo);
   if (maxlvl) atomicMax(&s_maxlvl, maxlvl);
   if (norph) atomicAdd(&s_orph, norph);
@@ -552,6 +567,13 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   // x + 1 <= L (its parent).  This thread's own records are scanned in
   // registers first; the tree is climbed from the thread's first record only
   // when the answer lies further back.
+  uint32_t g1[8];  // level-1 siblings of this thread's chunk
+  {
+    const uint4 ga = *(const uint4*)&s_up[kU1 + (tid & ~7)];
+    const uint4 gb = *(const uint4*)&s_up[kU1 + (tid & ~7) + 4];
+    g1[0] = ga.x; g1[1] = ga.y; g1[2] = ga.z; g1[3] = ga.w;
+    g1[4] = gb.x; g1[5] = gb.y; g1[6] = gb.z; g1[7] = gb.w;
+  }
   uint32_t par[IT], code[IT];
 #pragma unroll
   for (int i = 0; i < IT; ++i) {
@@ -566,25 +588,30 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
 #pragma unroll
     for (int j = i - 1; j >= 0; --j)
       if (qi < 0 && xp[j] <= v) qi = j;
-    uint32_t qrank;
+    uint32_t qrank, qreg;
     bool found = qi >= 0;
     if (found) {
-      // in-thread: rank from registers (the hit is always a BEGIN)
-      uint32_t rr = lbr[0];
+      // in-thread: rank and region from registers (the hit is always a BEGIN)
+      uint32_t rr = lbr[0], rg = reg[0];
 #pragma unroll
       for (int j = 0; j < IT; ++j)
-        if (j == qi) rr = lbr[j];
+        if (j == qi) {
+          rr = lbr[j];
+          rg = reg[j];
+        }
       qrank = rr;
+      qreg = rg;
     } else {
-      const int q = psv8(s_tree, (uint32_t)tid, v);
-      found = q >= 0;
-      qrank = found ? (uint32_t)s_lbr[q] : 0u;
+      const uint32_t h = psv_hit(s_leaf, s_up, g1, (uint32_t)tid, v);
+      found = h != kNoHit;
+      qrank = h & 0x7FFu;
+      qreg = h >> 11;
     }
     if (!isb) {
       if (found) {
         s_tend[qrank] = ts[i];
         s_ereg[qrank] = (uint16_t)reg[i];
-        if (ev_on && s_breg[qrank] == reg[i])
+        if (ev_on && qreg == reg[i])
           code[i] = ev_code(cls[i], 1u);
       } else {
         // pops a level that was open when the tile started
