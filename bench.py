@@ -82,7 +82,11 @@ def byte_model(name: str, c: dict, plan: dict, R: int, K: int, G: int, flags: in
         # sorted keys (+ context words) in; instances and one event word per record out
         return (12.0 + (4.0 if wide else 0.0) + (8.0 if ev_words else 0.0)) * nv + 40.0 * nb
     if name.startswith("merge") and name[5:].isdigit():
-        return 16.0 * plan["merge_end"] if int(name[5:]) < plan["merge_rounds"] and plan["ev_merge"] else 0.0
+        # rounds before the last: read and write one word per event
+        return 16.0 * plan["merge_end"] if int(name[5:]) + 1 < plan["merge_rounds"] and plan["ev_merge"] else 0.0
+    if name == "merge_sweep":
+        # last round: reads one word per event, merges and sweeps without storing
+        return 8.0 * plan["merge_end"] if plan["ev_merge"] else 0.0
     if name == "agg":
         return 40.0 * nb + (8.0 * nb if flags & 2 else 0.0) + (4.0 * nb if R > 167 else 0.0)
     if name == "hist":
@@ -90,7 +94,7 @@ def byte_model(name: str, c: dict, plan: dict, R: int, K: int, G: int, flags: in
     if name == "ev_hist":
         return 32.0 * nb
     if name == "sweep":
-        return 8.0 * plan["merge_end"] if plan["ev_merge"] else 12.0 * nev
+        return 0.0 if plan["ev_merge"] else 12.0 * nev
     if name == "init":
         return 8.0 * (R * 142 + (-(-n // 4096)) * 256 + (-(-nv // 2048)) * 4 + (-(-n // 2048)) * 8)
     if name == "ev_clear":

@@ -48,7 +48,7 @@ size_t align_up(size_t v) { return (v + kAlign - 1) & ~(kAlign - 1); }
 // Workspace layout for n records.  Offsets only; the base is added in run.
 struct Layout {
   size_t plan, rec_hist, rec_off, ev_hist, ev_off, tile_ctr;
-  size_t key[2], pay[2], ctxw[2], lb[2], mlb, slb, tiles, tree;
+  size_t key[2], pay[2], ctxw[2], lb[2], mlb, slb, mslb, tiles, tree;
   size_t pop_ts, pop_reg, pushes, op_parent, op_sum;
   size_t inst, child_sum, hist_key, ov_mask, ov_q;
   size_t push_pos, pop_pos, ctx_list, ctx_seg, seg_start, seg_split, seg_tile0, part;
@@ -113,6 +113,9 @@ Layout make_layout(const argus_attr_config& c, uint64_t n, bool own_instances) {
   L.seg_split = take(sizeof(uint32_t) * segs);
   L.seg_tile0 = take(sizeof(uint32_t) * segs);
   L.part = take(32 * L.tiles_cap);
+  // tile records of the last merge round (2 + 2K + K(K + 1) words each)
+  const uint64_t kc = c.num_classes;
+  L.mslb = take(sizeof(uint64_t) * (2 + 2 * kc + kc * (kc + 1)) * L.tiles_cap);
   L.total = o;
   return L;
 }
@@ -266,6 +269,7 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
   }
   w.mlb = (uint64_t*)(base + L.mlb);
   w.slb = (uint64_t*)(base + L.slb);
+  w.mslb = (uint64_t*)(base + L.mslb);
   w.tiles = (TileDesc*)(base + L.tiles);
   w.tree = (int64_t*)(base + L.tree);
   w.pop_ts = (uint64_t*)(base + L.pop_ts);
@@ -358,17 +362,19 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
     for (int sl = 0; sl < 12; ++sl)
       if (!step(enames[sl], launch_radix_pass(a, 1, sl, 2 * n, s))) return ARGUS_E_HIP;
     // Merge rounds (device-planned; a round beyond the plan returns at once).
-    static const char* mnames[kMaxMergeRounds][3] = {
-        {"mseg0", "mpart0", "merge0"}, {"mseg1", "mpart1", "merge1"},
-        {"mseg2", "mpart2", "merge2"}, {"mseg3", "mpart3", "merge3"},
-        {"mseg4", "mpart4", "merge4"}, {"mseg5", "mpart5", "merge5"},
-        {"mseg6", "mpart6", "merge6"}, {"mseg7", "mpart7", "merge7"}};
-    const int rounds = a.shift < (uint32_t)kMaxMergeRounds ? (int)a.shift : kMaxMergeRounds;
-    if (rounds > 0 && !step("mseg", launch_mseg(a, rounds, s))) return ARGUS_E_HIP;
+    // The last round is merged and swept by one kernel; there is always at
+    // least one round (a group of one context is a run by itself).
+    static const char* mnames[kMaxMergeRounds][2] = {
+        {"mpart0", "merge0"}, {"mpart1", "merge1"}, {"mpart2", "merge2"}, {"mpart3", "merge3"},
+        {"mpart4", "merge4"}, {"mpart5", "merge5"}, {"mpart6", "merge6"}, {"mpart7", "merge7"}};
+    int rounds = a.shift < (uint32_t)kMaxMergeRounds ? (int)a.shift : kMaxMergeRounds;
+    if (rounds < 1) rounds = 1;
+    if (!step("mseg", launch_mseg(a, rounds, s))) return ARGUS_E_HIP;
     for (int r = 0; r < rounds; ++r) {
-      if (!step(mnames[r][1], launch_mpart(a, r, s))) return ARGUS_E_HIP;
-      if (!step(mnames[r][2], launch_merge(a, r, s))) return ARGUS_E_HIP;
+      if (!step(mnames[r][0], launch_mpart(a, r, s))) return ARGUS_E_HIP;
+      if (r + 1 < rounds && !step(mnames[r][1], launch_merge(a, r, s))) return ARGUS_E_HIP;
     }
+    if (!step("merge_sweep", launch_merge_sweep(a, s))) return ARGUS_E_HIP;
     if (!step("sweep", launch_sweep(a, s))) return ARGUS_E_HIP;
     if (!step("ov_final", launch_ov_final(a, s))) return ARGUS_E_HIP;
   }

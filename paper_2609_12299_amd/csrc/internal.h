@@ -36,6 +36,9 @@ constexpr int kMergeThreads = 512;
 constexpr int kMergeItems = 8;
 constexpr int kMergeTile = kMergeThreads * kMergeItems;  // 4096 events
 constexpr int kMaxMergeRounds = 8;
+// Bit of a round that merges nothing: every group holds one context, so the
+// last (only) round takes each group as one run (segments = groups).
+constexpr uint32_t kSegByGroup = 0xFFFFFFFFu;
 constexpr uint64_t kCtxCap = 1ull << 20;  // contexts the merge path handles
 constexpr int kEvCodeBits = 5;           // event code: 0 none, 1 + 2 * class + is_end
 
@@ -157,6 +160,7 @@ struct Work {
   uint64_t* lb[2];      // radix look-back status, [tiles][256]
   uint64_t* mlb;        // matching look-back status, [tiles][4]
   uint64_t* slb;        // sweep look-back status, [tiles][8]
+  uint64_t* mslb;       // last merge round tile records, [tiles_cap][2 + 2K + K(K + 1)]
   TileDesc* tiles;      // [match tiles]
   int64_t* tree;        // [2 * tree_leaves]
   uint64_t* pop_ts;     // per matching tile, kMatchTile entries each
@@ -235,6 +239,87 @@ ARGUS_DEV uint64_t lanemask_lt() { return (1ull << lane_id()) - 1ull; }
 
 ARGUS_DEV uint32_t bit_width64(uint64_t v) { return v ? 64u - (uint32_t)__clzll(v) : 0u; }
 
+// ------------------------------------------------- cross-lane (DPP) helpers
+// gfx9 DPP controls: quad permutations, mirrors inside a row of 16 lanes,
+// shifts inside a row, and broadcasts of a row's lane 15 to the next rows.
+constexpr int kDppQuad1032 = 0xB1;    // quad_perm:[1,0,3,2]
+constexpr int kDppQuad2301 = 0x4E;    // quad_perm:[2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;  // row_half_mirror
+constexpr int kDppMirror = 0x140;      // row_mirror
+constexpr int kDppRowShr = 0x110;      // row_shr:n is kDppRowShr + n
+constexpr int kDppBcast15 = 0x142;     // row_bcast:15
+constexpr int kDppBcast31 = 0x143;     // row_bcast:31
+
+template <int CTRL, int ROWS = 0xF>
+ARGUS_DEV uint32_t dpp32(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, ROWS, 0xF, false);
+}
+
+// Sum over each row of 16 lanes, in every lane of the row.
+ARGUS_DEV uint32_t row_sum32(uint32_t v) {
+  v += dpp32<kDppQuad1032>(v);
+  v += dpp32<kDppQuad2301>(v);
+  v += dpp32<kDppHalfMirror>(v);
+  v += dpp32<kDppMirror>(v);
+  return v;
+}
+ARGUS_DEV uint64_t row_sum64(uint64_t v) {
+  uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+#define ARGUS_ROW_STEP(C)                                              \
+  {                                                                    \
+    const uint64_t o = (uint64_t)dpp32<C>(lo) | ((uint64_t)dpp32<C>(hi) << 32); \
+    const uint64_t r = ((uint64_t)lo | ((uint64_t)hi << 32)) + o;      \
+    lo = (uint32_t)r;                                                  \
+    hi = (uint32_t)(r >> 32);                                          \
+  }
+  ARGUS_ROW_STEP(kDppQuad1032)
+  ARGUS_ROW_STEP(kDppQuad2301)
+  ARGUS_ROW_STEP(kDppHalfMirror)
+  ARGUS_ROW_STEP(kDppMirror)
+#undef ARGUS_ROW_STEP
+  return (uint64_t)lo | ((uint64_t)hi << 32);
+}
+ARGUS_DEV int32_t row_min32(int32_t v) {
+  int32_t o;
+  o = (int32_t)dpp32<kDppQuad1032>((uint32_t)v); v = o < v ? o : v;
+  o = (int32_t)dpp32<kDppQuad2301>((uint32_t)v); v = o < v ? o : v;
+  o = (int32_t)dpp32<kDppHalfMirror>((uint32_t)v); v = o < v ? o : v;
+  o = (int32_t)dpp32<kDppMirror>((uint32_t)v); v = o < v ? o : v;
+  return v;
+}
+// Wave-wide results from per-row results (lanes 0, 16, 32, 48), as scalars.
+ARGUS_DEV uint32_t rows_sum32(uint32_t v) {
+  return __builtin_amdgcn_readlane(v, 0) + __builtin_amdgcn_readlane(v, 16) +
+         __builtin_amdgcn_readlane(v, 32) + __builtin_amdgcn_readlane(v, 48);
+}
+ARGUS_DEV uint64_t rows_sum64(uint64_t v) {
+  const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+  uint64_t r = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    r += (uint64_t)(uint32_t)__builtin_amdgcn_readlane(lo, 16 * q) |
+         ((uint64_t)(uint32_t)__builtin_amdgcn_readlane(hi, 16 * q) << 32);
+  return r;
+}
+ARGUS_DEV int32_t rows_min32(int32_t v) {
+  int32_t a = __builtin_amdgcn_readlane(v, 0), b = __builtin_amdgcn_readlane(v, 16);
+  int32_t c = __builtin_amdgcn_readlane(v, 32), d = __builtin_amdgcn_readlane(v, 48);
+  a = a < b ? a : b;
+  c = c < d ? c : d;
+  return a < c ? a : c;
+}
+
+// Inclusive prefix sum over the 64 lanes of the wave.
+ARGUS_DEV int32_t wave_incl_scan32(int32_t v) {
+  v += (int32_t)dpp32<kDppRowShr + 1>((uint32_t)v);
+  v += (int32_t)dpp32<kDppRowShr + 2>((uint32_t)v);
+  v += (int32_t)dpp32<kDppRowShr + 4>((uint32_t)v);
+  v += (int32_t)dpp32<kDppRowShr + 8>((uint32_t)v);
+  v += (int32_t)dpp32<kDppBcast15, 0xA>((uint32_t)v);
+  v += (int32_t)dpp32<kDppBcast31, 0xC>((uint32_t)v);
+  return v;
+}
+
 // Look-back status words: bits 62..63 hold the state, bits 0..61 the value.
 constexpr uint64_t kFlagAgg = 1ull << 62;
 constexpr uint64_t kFlagIncl = 2ull << 62;
@@ -261,6 +346,7 @@ hipError_t launch_mplan(const RunArgs& a, hipStream_t s);
 hipError_t launch_mseg(const RunArgs& a, int rounds, hipStream_t s);
 hipError_t launch_mpart(const RunArgs& a, int round, hipStream_t s);
 hipError_t launch_merge(const RunArgs& a, int round, hipStream_t s);
+hipError_t launch_merge_sweep(const RunArgs& a, hipStream_t s);
 hipError_t launch_sweep(const RunArgs& a, hipStream_t s);
 hipError_t launch_ov_final(const RunArgs& a, hipStream_t s);
 

@@ -17,11 +17,13 @@
 // neighbouring contexts of one group first differ (no other bit has a pair to
 // merge).  After the last round every group is one run in time order.
 //
-// A round is three launches: segment boundaries (one block), the merge-path
-// split of every output tile (Green, McColl and Bader's merge path: a binary
-// search on the cross diagonal), and the merge of each tile's two input
-// slices in LDS.
-#include "internal.h"
+// A round is two launches after the segment boundaries of all rounds (one
+// block per round): the merge-path split of every output tile (Green, McColl
+// and Bader's merge path: a binary search on the cross diagonal), and the
+// merge of each tile's two input slices in LDS.  The last round does not
+// store what it merges: k_merge_sweep sweeps each merged tile at once (its
+// segments are exactly the groups).
+#include "sweep_common.h"
 
 namespace argus {
 
@@ -69,7 +71,9 @@ __global__ __launch_bounds__(64) void k_mplan(MPlanArgs a) {
   }
   p->m_nctx = (uint32_t)lo;
   p->m_end = lo < n_ctx ? a.ctx_list[lo].y : p->n_valid;
-  p->m_rounds = rounds;
+  // No bit to merge: every group is one context, already in time order; one
+  // round that merges nothing takes each group as a run of its own.
+  p->m_rounds = rounds ? rounds : 1u;
   uint32_t buf = p->rec_final ^ 1u, r = 0;
   for (uint32_t b = 0; b < 32; ++b) {
     if (!((need >> b) & 1u)) continue;
@@ -80,6 +84,14 @@ __global__ __launch_bounds__(64) void k_mplan(MPlanArgs a) {
     m.n_segs = 0;
     m.n_tiles = 0;
     buf ^= 1u;
+  }
+  if (rounds == 0) {
+    MergeRound& m = p->mr[0];
+    m.bit = kSegByGroup;
+    m.src = buf;
+    m.dst = buf ^ 1u;
+    m.n_segs = 0;
+    m.n_tiles = 0;
   }
   p->ev_final = buf;
   p->n_ev = p->m_end;
@@ -134,6 +146,7 @@ struct MSegArgs {
   uint32_t* seg_split;
   uint32_t* seg_tile0;
   uint64_t stride;  // per-round stride of the segment arrays
+  uint32_t shift;
 };
 
 // Segments of every round (block r: round r): maximal runs of contexts with
@@ -152,7 +165,12 @@ __global__ __launch_bounds__(1024) void k_mseg(MSegArgs a) {
   const uint32_t nc = p->m_nctx;
   const uint32_t end = (uint32_t)p->m_end;
   const uint32_t t = threadIdx.x;
-  auto hi_of = [&](uint32_t c) -> uint32_t { return bit >= 31 ? 0u : (c >> (bit + 1)); };
+  // segment key: ctx >> (bit + 1), or the group for a round that merges nothing
+  const bool by_group = bit == kSegByGroup;
+  auto hi_of = [&](uint32_t c) -> uint32_t {
+    if (by_group) return a.shift >= 32 ? 0u : (c >> a.shift);
+    return bit >= 31 ? 0u : (c >> (bit + 1));
+  };
 
   uint32_t carry = 0;
   for (uint32_t base = 0; base < nc; base += 1024) {
@@ -179,7 +197,7 @@ __global__ __launch_bounds__(1024) void k_mseg(MSegArgs a) {
   __threadfence_block();
   __syncthreads();
   // first context of each segment whose bit is 1
-  for (uint32_t j = t; j < nc; j += 1024) {
+  for (uint32_t j = t; j < nc && !by_group; j += 1024) {
     const uint2 e = a.ctx_list[j];
     if (!((e.x >> bit) & 1u)) continue;
     bool first1 = j == 0;
@@ -216,7 +234,7 @@ __global__ __launch_bounds__(1024) void k_mseg(MSegArgs a) {
 
 hipError_t launch_mseg(const RunArgs& a, int rounds, hipStream_t s) {
   MSegArgs m{a.w.plan, a.w.ctx_list, a.w.ctx_seg, a.w.seg_start, a.w.seg_split, a.w.seg_tile0,
-             a.w.ctx_cap + 1};
+             a.w.ctx_cap + 1, a.shift};
   hipLaunchKernelGGL(k_mseg, dim3((uint32_t)(rounds > 0 ? rounds : 1)), dim3(1024), 0, s, m);
   return hipGetLastError();
 }
@@ -242,10 +260,12 @@ __device__ __forceinline__ uint32_t corank(const uint64_t* A, uint32_t la, const
 }
 
 // One merge tile: where its slices of the two runs start, their lengths,
-// and where its output starts (absolute sorted positions).
+// where its output starts, where the two runs end (absolute sorted
+// positions), and whether it is the first tile of its segment.
 struct MergeTask {
-  uint32_t a_pos, na, b_pos, nb, out_pos, pad0, pad1, pad2;
+  uint32_t a_pos, na, b_pos, nb, out_pos, a_end, b_end, first;
 };
+static_assert(sizeof(MergeTask) == 32, "MergeTask layout");
 
 struct MPartArgs {
   const DevPlan* plan;
@@ -296,6 +316,9 @@ __global__ __launch_bounds__(256) void k_mpart(MPartArgs a) {
       tk.b_pos = sp + (d0 - a0);
       tk.nb = (d1 - a1) - (d0 - a0);
       tk.out_pos = s0 + d0;
+      tk.a_end = sp;
+      tk.b_end = s1;
+      tk.first = k == seg_tile0[lo] ? 1u : 0u;
     } else {
       flag_internal_error(a.counters, 256);
     }
@@ -357,7 +380,8 @@ __device__ __forceinline__ void load_task(const uint64_t* src, const MergeTask& 
 // while the current one is merged.
 __global__ __launch_bounds__(kMergeThreads) void k_merge(MergeArgs a) {
   const DevPlan* p = a.plan;
-  if (!p->ev_merge || (uint32_t)a.round >= p->m_rounds) return;
+  // the last round is k_merge_sweep's
+  if (!p->ev_merge || (uint32_t)a.round + 1 >= p->m_rounds) return;
   __shared__ uint64_t s_e[kMergeTile + 1];  // + 1: reads past a run stay inside
   const MergeRound mr = p->mr[a.round];
   const uint64_t n_tiles = mr.n_tiles;
@@ -437,6 +461,628 @@ hipError_t launch_merge(const RunArgs& a, int round, hipStream_t s) {
   if (blocks > resident) blocks = resident;
   hipLaunchKernelGGL(k_merge, dim3((uint32_t)blocks), dim3(kMergeThreads), 0, s, m);
   return hipGetLastError();
+}
+
+
+// ------------------------------------------------- last round and the sweep
+//
+// The last round's segments are the groups, and it is swept tile by tile as
+// it is merged.  A tile cannot know the class counts entering it without
+// waiting for the tiles before it, so it records sums from which its share
+// of U and Q follows once those counts are known (k_ovt_final).  With the
+// tile-local count l (0 before the tile's first event; c = c_in + l) and a
+// bias B (l' = l + B >= 0, a = c_in - B, so c = a + l'):
+//   Q[x][y] (x != y) = sum gap (a_x + l'_x)(a_y + l'_y)
+//                    = S2'[x][y] + a_x S1'[y] + a_y S1'[x] + a_x a_y S0,
+//   Q[x][x]          = sum gap C(a_x + l'_x, 2)
+//                    = S2'[x][x] + a_x S1'[x] + C(a_x, 2) S0,
+// with S0 = sum gap, S1'[x] = sum gap l'_x, S2'[x][y] = sum gap l'_x l'_y,
+// S2'[x][x] = sum gap C(l'_x, 2) (all exact integers, then mod 2^64).  Counts
+// never go below zero, so with m_x the lowest l_x over the tile, class x is
+// active in every gap of the tile when c_in_x + m_x > 0 and exactly where
+// l_x > m_x otherwise; T[x] = sum gap [l_x > m_x] and T2[x][y] = sum gap
+// [l_x > m_x][l_y > m_y] then give U.  A tile spanning 2^32 cycles or more
+// is summed again with 64-bit gaps by a second, rarely busy kernel.
+
+constexpr int32_t kLBias = kMergeTile;  // |l| <= 4096 inside a tile
+
+// Words of one tile record for KC classes: group | first << 32 | wide << 33,
+// then per class (delta | min << 32), S0, S1'[KC], S2'[NP], T[NP] (pairs
+// x <= y in row order; T[x][x] = T[x], T[x][y] = T2[x][y]).
+__host__ __device__ constexpr int tile_rec_words(int kc) { return 2 + 2 * kc + kc * (kc + 1); }
+
+struct MergeSweepArgs {
+  const DevPlan* plan;
+  const uint64_t* ev[2];
+  const MergeTask* task;
+  uint64_t* rec;  // [tiles][tile_rec_words(K)]
+  uint64_t* counters;
+};
+
+// A task of the last round is usable if its slices lie inside their runs and
+// the runs inside the merged range.
+__device__ __forceinline__ bool task_ok_last(const MergeTask& t, uint32_t end) {
+  return task_ok(t, end) && t.a_pos + t.na <= t.a_end && t.a_end <= t.b_end &&
+         t.b_pos + t.nb <= t.b_end && t.b_end <= end;
+}
+
+// The word that follows a tile in merged order (ties: run A first), if its
+// segment continues.
+__device__ __forceinline__ bool tile_next(const uint64_t* src, const MergeTask& t, uint64_t* w) {
+  const uint32_t a1 = t.a_pos + t.na, b1 = t.b_pos + t.nb;
+  const bool ha = a1 < t.a_end, hb = b1 < t.b_end;
+  if (!ha && !hb) return false;
+  const uint64_t ea = ha ? src[a1] : 0ull, eb = hb ? src[b1] : 0ull;
+  *w = (ha && (!hb || mkey(ea) <= mkey(eb))) ? ea : eb;
+  return true;
+}
+
+// Per-thread sums over 8 consecutive merged events e[0..nval) followed by the
+// word `after` (if has_after).  lp: biased local counts l' before the first
+// event; mp: biased tile minima m'.  NARROW (the tile spans less than 2^32
+// cycles): gaps, S0, T and T2 fit 32 bits.  l' < 2^14 either way.
+template <int KC, bool NARROW>
+__device__ __forceinline__ void sweep8(const uint64_t* e, uint32_t nval, uint64_t after,
+                                       bool has_after, const uint32_t (&lp0)[KC],
+                                       const uint32_t (&mp)[KC],
+                                       typename std::conditional<NARROW, uint32_t, uint64_t>::type (&tt)[1 + KC * (KC + 1) / 2],
+                                       uint64_t (&s1)[KC], uint64_t (&s2)[KC * (KC + 1) / 2]) {
+  using UT = typename std::conditional<NARROW, uint32_t, uint64_t>::type;
+  uint32_t l[KC];
+#pragma unroll
+  for (int x = 0; x < KC; ++x) l[x] = lp0[x];
+  uint64_t cur = e[0];
+#pragma unroll 1
+  for (uint32_t j = 0; j < nval; ++j) {
+    const uint32_t code = (uint32_t)(cur & ((1u << kEvCodeBits) - 1u));
+    const uint32_t cls = (code - 1u) >> 1;  // >= KC when code == 0
+    const uint32_t sg = 1u - 2u * ((code - 1u) & 1u);  // +1 BEGIN, -1 END
+#pragma unroll
+    for (int x = 0; x < KC; ++x) l[x] += cls == (uint32_t)x ? sg : 0u;
+    // gap to the next event of the group (none after the last one)
+    const bool inside = j + 1 < nval;
+    const bool has_nx = inside || has_after;
+    const uint64_t nx = inside ? e[j + 1] : after;
+    UT gap;
+    if (NARROW)
+      gap = has_nx ? (UT)((uint32_t)(nx >> kEvCodeBits) - (uint32_t)(cur >> kEvCodeBits)) : (UT)0;
+    else
+      gap = has_nx ? (UT)((nx >> kEvCodeBits) - (cur >> kEvCodeBits)) : (UT)0;
+    // tt: S0, then T[x] (x <= y: T2[x][y], x == y: T[x]) in pair order
+    tt[0] += gap;
+    bool act[KC];
+#pragma unroll
+    for (int x = 0; x < KC; ++x) {
+      act[x] = l[x] > mp[x];
+      s1[x] += (uint64_t)gap * l[x];
+    }
+    int k = 0;
+#pragma unroll
+    for (int x = 0; x < KC; ++x) {
+#pragma unroll
+      for (int y = x; y < KC; ++y, ++k) {
+        const uint32_t w = x != y ? __umul24(l[x], l[y]) : (__umul24(l[x], l[x] - 1u) >> 1);
+        s2[k] += (uint64_t)gap * w;
+        tt[1 + k] += (act[x] && act[y]) ? gap : (UT)0;
+      }
+    }
+    cur = nx;
+  }
+}
+
+// Wave sum of a 64-bit value, result in lane 0.
+__device__ __forceinline__ uint64_t wave_sum64(uint64_t v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_down(v, off);
+  return v;
+}
+
+// LDS of one block of the last round.
+template <int KC>
+struct MsShared {
+  static constexpr int NW = kMergeThreads / 64;
+  static constexpr int NV = 1 + KC + KC * (KC + 1);  // S0, S1', S2', T
+  int32_t wd[NW][KC];
+  int32_t wm[NW][KC];
+  uint64_t next;
+  uint32_t has_next;
+  uint64_t red[NV][NW];
+};
+
+// Merges the tile staged in se (run A then run B) into 8 consecutive outputs
+// per thread and writes them back in merged order.  Ends with every thread
+// past the read of its inputs; the caller synchronises before reading se.
+__device__ __forceinline__ void merge_tile(uint64_t* se, uint32_t na, uint32_t nb, uint32_t t) {
+  const uint32_t cnt = na + nb, d = t * kMergeItems;
+  uint64_t o[kMergeItems];
+#pragma unroll
+  for (int j = 0; j < kMergeItems; ++j) o[j] = 0;
+  if (d < cnt) {
+    const uint64_t* A = se;
+    const uint64_t* B = se + na;
+    uint32_t ia = corank(A, na, B, nb, d), ib = d - ia;
+#pragma unroll
+    for (int j = 0; j < kMergeItems; ++j) {
+      const bool take_a = ia < na && (ib >= nb || mkey(A[ia]) <= mkey(B[ib]));
+      o[j] = take_a ? A[ia] : B[ib < nb ? ib : nb];
+      ia += take_a;
+      ib += !take_a;
+    }
+  }
+  __syncthreads();  // every thread has read its inputs
+#pragma unroll
+  for (int j = 0; j < kMergeItems; ++j)
+    if (d + (uint32_t)j < cnt) se[d + j] = o[j];
+}
+
+// Sums of one merged tile (se, cnt events; ss.next / ss.has_next: the word
+// after it) into its record.  Returns false, with only the record's header
+// written (wide bit set), when !WIDE and the tile spans 2^32 cycles or more.
+template <int KC, bool WIDE>
+__device__ __forceinline__ bool tile_sums(const uint64_t* se, uint32_t cnt, bool first,
+                                          MsShared<KC>& ss, uint64_t* rec, uint32_t es) {
+  constexpr int NP = KC * (KC + 1) / 2;
+  constexpr int NW = MsShared<KC>::NW;
+  constexpr int NV = MsShared<KC>::NV;
+  const uint32_t t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const uint32_t d = t * kMergeItems;
+  const uint32_t nval = d < cnt ? (cnt - d < (uint32_t)kMergeItems ? cnt - d : (uint32_t)kMergeItems) : 0u;
+  const uint64_t first_w = se[0];
+  const bool has_next = ss.has_next != 0;
+  const uint64_t last_w = has_next ? ss.next : se[cnt - 1];
+  const uint64_t g = es >= 64 ? 0ull : (first_w >> es);
+  const uint64_t head = (g & 0xFFFFFFFFull) | ((uint64_t)(first ? 1u : 0u) << 32);
+  if (!WIDE && ((last_w >> kEvCodeBits) - (first_w >> kEvCodeBits)) >= (1ull << 32)) {
+    if (t == 0) rec[0] = head | (1ull << 33);
+    return false;
+  }
+  // ---- class-count deltas of the thread's events, scanned over the block
+  const uint64_t* e = se + d;
+  int32_t dd[KC], inc[KC];
+#pragma unroll
+  for (int x = 0; x < KC; ++x) dd[x] = 0;
+#pragma unroll 2
+  for (uint32_t j = 0; j < nval; ++j) {
+    const uint32_t code = (uint32_t)(e[j] & ((1u << kEvCodeBits) - 1u));
+    const uint32_t cls = (code - 1u) >> 1;
+    const int32_t sg = 1 - 2 * (int32_t)((code - 1u) & 1u);
+#pragma unroll
+    for (int x = 0; x < KC; ++x) dd[x] += cls == (uint32_t)x ? sg : 0;
+  }
+#pragma unroll
+  for (int x = 0; x < KC; ++x) inc[x] = wave_incl_scan32(dd[x]);
+  if (lane == 63) {
+#pragma unroll
+    for (int x = 0; x < KC; ++x) ss.wd[w][x] = inc[x];
+  }
+  __syncthreads();
+  int32_t pre[KC], agg[KC], mn[KC];
+#pragma unroll
+  for (int x = 0; x < KC; ++x) {
+    pre[x] = inc[x] - dd[x];
+    agg[x] = 0;
+  }
+#pragma unroll
+  for (int q = 0; q < NW; ++q) {
+#pragma unroll
+    for (int x = 0; x < KC; ++x) {
+      const int32_t v2 = ss.wd[q][x];
+      pre[x] += q < (int)w ? v2 : 0;
+      agg[x] += v2;
+    }
+  }
+  // ---- tile minima of the local counts (after each event)
+  {
+    int32_t l[KC];
+#pragma unroll
+    for (int x = 0; x < KC; ++x) {
+      l[x] = pre[x];
+      mn[x] = 0x7FFFFFFF;
+    }
+#pragma unroll 2
+    for (uint32_t j = 0; j < nval; ++j) {
+      const uint32_t code = (uint32_t)(e[j] & ((1u << kEvCodeBits) - 1u));
+      const uint32_t cls = (code - 1u) >> 1;
+      const int32_t sg = 1 - 2 * (int32_t)((code - 1u) & 1u);
+#pragma unroll
+      for (int x = 0; x < KC; ++x) {
+        l[x] += cls == (uint32_t)x ? sg : 0;
+        mn[x] = l[x] < mn[x] ? l[x] : mn[x];
+      }
+    }
+#pragma unroll
+    for (int x = 0; x < KC; ++x) {
+      const int32_t m = rows_min32(row_min32(mn[x]));
+      if (lane == 0) ss.wm[w][x] = m;
+    }
+  }
+  __syncthreads();
+  uint32_t lp[KC], mp[KC];
+#pragma unroll
+  for (int x = 0; x < KC; ++x) {
+    int32_t m = 0x7FFFFFFF;
+#pragma unroll
+    for (int q = 0; q < NW; ++q) m = ss.wm[q][x] < m ? ss.wm[q][x] : m;
+    mn[x] = m;
+    lp[x] = (uint32_t)(pre[x] + kLBias);
+    mp[x] = (uint32_t)(m + kLBias);
+  }
+  // ---- sums over this thread's gaps
+  const bool has_after = d + kMergeItems < cnt || has_next;
+  const uint64_t after = d + kMergeItems < cnt ? se[d + kMergeItems] : ss.next;
+  using UT = typename std::conditional<WIDE, uint64_t, uint32_t>::type;
+  UT tt[1 + NP];
+  uint64_t s1[KC], s2[NP];
+#pragma unroll
+  for (int x = 0; x < 1 + NP; ++x) tt[x] = 0;
+#pragma unroll
+  for (int x = 0; x < KC; ++x) s1[x] = 0;
+#pragma unroll
+  for (int x = 0; x < NP; ++x) s2[x] = 0;
+  if (nval) sweep8<KC, !WIDE>(e, nval, after, has_after, lp, mp, tt, s1, s2);
+  // ---- tile totals: waves in registers (rows of 16 lanes, then the four
+  // row results as scalars), then across waves in LDS
+  {
+    int c = 0;
+    // 32-bit sums stay exact per wave in the narrow case: a wave's gaps add
+    // up to less than the tile's span
+    auto put = [&](uint64_t val, bool narrow32) {
+      const uint64_t r = narrow32 ? (uint64_t)rows_sum32(row_sum32((uint32_t)val))
+                                  : rows_sum64(row_sum64(val));
+      if (lane == 0) ss.red[c][w] = r;
+      ++c;
+    };
+    put((uint64_t)tt[0], !WIDE);
+#pragma unroll
+    for (int x = 0; x < KC; ++x) put(s1[x], false);
+#pragma unroll
+    for (int x = 0; x < NP; ++x) put(s2[x], false);
+#pragma unroll
+    for (int x = 0; x < NP; ++x) put((uint64_t)tt[1 + x], !WIDE);
+  }
+  __syncthreads();
+  if (t < (uint32_t)NV) {
+    uint64_t sum = 0;
+#pragma unroll
+    for (int q = 0; q < NW; ++q) sum += ss.red[t][q];
+    rec[1 + KC + t] = sum;
+  } else if (t >= 256 && t < 256u + KC) {
+    const int x = (int)t - 256;
+    rec[1 + x] = (uint64_t)(uint32_t)agg[x] | ((uint64_t)(uint32_t)mn[x] << 32);
+  } else if (t == 384) {
+    rec[0] = head;
+  }
+  return true;
+}
+
+// The last merge round fused with the class-overlap sums.  Each tile of 4096
+// merged events belongs to one group.  Per tile: merge the two input slices
+// in LDS (8 consecutive outputs per thread, written back in merged order),
+// scan the class-count deltas over the block, take the tile minima, and sum
+// S0, S1', S2', T over the tile's gaps into the tile's record with its
+// deltas and minima.  A tile spanning 2^32 cycles or more only gets its
+// record flagged here (k_merge_sweep_wide redoes it).  Tiles are independent
+// (tile = block + k * grid); the loads of one block overlap the work of the
+// other blocks on its compute unit.
+template <int KC, bool WIDE>
+__device__ __forceinline__ void merge_sweep_tiles(const MergeSweepArgs& a) {
+  constexpr int RW = tile_rec_words(KC);
+  const DevPlan* p = a.plan;
+  if (!p->ev_merge || p->m_rounds == 0) return;
+  __shared__ uint64_t s_e[kMergeTile + 1];  // + 1: reads past a run stay inside
+  __shared__ MsShared<KC> ss;
+  const MergeRound mr = p->mr[p->m_rounds - 1];
+  const uint64_t n_tiles = mr.n_tiles;
+  const uint32_t end = (uint32_t)p->m_end;
+  const uint32_t es = p->rec.ts_bits + kEvCodeBits;  // group bits start here
+  const uint64_t* src = a.ev[mr.src];
+  const uint32_t t = threadIdx.x;
+  for (uint64_t k = blockIdx.x; k < n_tiles; k += gridDim.x) {
+    uint64_t* rec = a.rec + k * RW;
+    if (WIDE && !((rec[0] >> 33) & 1u)) continue;
+    const MergeTask tk = a.task[k];
+    if (!task_ok_last(tk, end)) {
+      if (WIDE) continue;  // never flagged
+      // unusable task: a record that starts a segment and adds nothing
+      if (t == 0) flag_internal_error(a.counters, 256);
+      if (t < (uint32_t)RW) rec[t] = t == 0 ? (0xFFFFFFFFull | (1ull << 32)) : 0ull;
+      continue;
+    }
+    uint64_t v[kMergeItems];
+    load_task(src, tk, t, v);
+    uint64_t nx = 0;
+    bool hnx = false;
+    if (t == 0) hnx = tile_next(src, tk, &nx);
+    const uint32_t cnt = tk.na + tk.nb;
+#pragma unroll
+    for (int j = 0; j < kMergeItems; ++j) {
+      const uint32_t i = t + (uint32_t)j * kMergeThreads;
+      if (i < cnt) s_e[i] = v[j];
+    }
+    if (t == 0) {
+      ss.next = nx;
+      ss.has_next = hnx ? 1u : 0u;
+    }
+    __syncthreads();
+    merge_tile(s_e, tk.na, tk.nb, t);
+    __syncthreads();
+    tile_sums<KC, WIDE>(s_e, cnt, tk.first != 0, ss, rec, es);
+    __syncthreads();
+  }
+}
+
+template <int KC>
+__global__ __launch_bounds__(kMergeThreads) void k_merge_sweep(MergeSweepArgs a) {
+  merge_sweep_tiles<KC, false>(a);
+}
+
+// Tiles of the last round flagged as spanning 2^32 cycles or more: merged
+// again and summed with 64-bit gaps.
+template <int KC>
+__global__ __launch_bounds__(kMergeThreads) void k_merge_sweep_wide(MergeSweepArgs a) {
+  merge_sweep_tiles<KC, true>(a);
+}
+
+// ------------------------------------------------------ tile records → rows
+
+struct OvtArgs {
+  const DevPlan* plan;
+  const uint64_t* rec;
+  int64_t* blk;    // [blocks][1 + K]: reset flag, then the block's count deltas
+  uint64_t* ov_u;  // [G][36]
+  uint64_t* ov_q;  // [G][36]
+  uint64_t* counters;
+  uint32_t G;
+};
+
+constexpr int kOvtThreads = 256;
+
+// Per block of 256 tile records: whether a segment starts in it, and the
+// class-count deltas since the last start (or of the whole block).
+template <int KC>
+__global__ __launch_bounds__(kOvtThreads) void k_ovt_agg(OvtArgs a) {
+  constexpr int RW = tile_rec_words(KC);
+  const DevPlan* p = a.plan;
+  if (!p->ev_merge || p->m_rounds == 0) return;
+  const uint64_t n_tiles = p->mr[p->m_rounds - 1].n_tiles;
+  const uint64_t tile = (uint64_t)blockIdx.x * kOvtThreads + threadIdx.x;
+  if ((uint64_t)blockIdx.x * kOvtThreads >= n_tiles) return;
+  __shared__ uint32_t s_last;
+  __shared__ int64_t s_sum[KC];
+  if (threadIdx.x == 0) s_last = 0;
+  if (threadIdx.x < KC) s_sum[threadIdx.x] = 0;
+  __syncthreads();
+  const bool in = tile < n_tiles;
+  const bool first = in && ((a.rec[tile * RW] >> 32) & 1u);
+  if (first) atomicMax(&s_last, threadIdx.x + 1);
+  __syncthreads();
+  const uint32_t last = s_last;  // 1 + index of the last segment start, or 0
+  if (in && threadIdx.x + 1 >= last) {
+#pragma unroll
+    for (int x = 0; x < KC; ++x) {
+      const int32_t dv = (int32_t)(uint32_t)a.rec[tile * RW + 1 + x];
+      if (dv) atomicAdd((unsigned long long*)&s_sum[x], (unsigned long long)(int64_t)dv);
+    }
+  }
+  __syncthreads();
+  int64_t* b = a.blk + (uint64_t)blockIdx.x * (1 + KC);
+  if (threadIdx.x == 0) b[0] = last ? 1 : 0;
+  if (threadIdx.x < KC) b[1 + threadIdx.x] = s_sum[threadIdx.x];
+}
+
+// Counts entering each tile (a segmented scan over the tile records, the
+// carry into a block found by walking back over the block aggregates to the
+// nearest segment start), then each tile's share of U and Q added to its
+// group's rows.
+template <int KC>
+__global__ __launch_bounds__(kOvtThreads) void k_ovt_final(OvtArgs a) {
+  constexpr int KM = KC <= 2 ? 2 : (KC <= 4 ? 4 : 8);  // stride of the pair index
+  constexpr int NP = KC * (KC + 1) / 2;
+  constexpr int RW = tile_rec_words(KC);
+  const DevPlan* p = a.plan;
+  if (!p->ev_merge || p->m_rounds == 0) return;
+  const uint64_t n_tiles = p->mr[p->m_rounds - 1].n_tiles;
+  const uint64_t blk0 = (uint64_t)blockIdx.x * kOvtThreads;
+  if (blk0 >= n_tiles) return;
+  const uint32_t t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const uint64_t tile = blk0 + t;
+  const bool in = tile < n_tiles;
+  __shared__ int64_t s_carry[KC];
+  __shared__ int64_t s_wsum[kOvtThreads / 64][KC];
+  __shared__ uint32_t s_wfirst[kOvtThreads / 64];
+  // ---- carry into this block (wave 0): blocks before it back to a reset
+  if (w == 0) {
+    int64_t acc[KC];
+#pragma unroll
+    for (int x = 0; x < KC; ++x) acc[x] = 0;
+    int64_t top = (int64_t)blockIdx.x - 1;
+    while (top >= 0) {
+      const int64_t bb = top - (int64_t)lane;
+      uint32_t reset = 1;  // before block 0: nothing
+      int64_t val[KC];
+#pragma unroll
+      for (int x = 0; x < KC; ++x) val[x] = 0;
+      if (bb >= 0) {
+        const int64_t* b = a.blk + (uint64_t)bb * (1 + KC);
+        reset = b[0] != 0;
+#pragma unroll
+        for (int x = 0; x < KC; ++x) val[x] = b[1 + x];
+      }
+      const uint64_t mr = __ballot(reset);
+      const int jr = mr ? __ffsll((unsigned long long)mr) - 1 : 64;  // nearest reset
+#pragma unroll
+      for (int x = 0; x < KC; ++x) {
+        int64_t vv = (int)lane <= jr ? val[x] : 0;
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) vv += __shfl_xor(vv, off);
+        acc[x] += vv;
+      }
+      if (jr < 64) break;
+      top -= 64;
+    }
+    if (lane == 0) {
+#pragma unroll
+      for (int x = 0; x < KC; ++x) s_carry[x] = acc[x];
+    }
+  }
+  // ---- segmented exclusive scan of the tile deltas within the block
+  const uint64_t* r = a.rec + tile * RW;
+  const bool first = in && ((r[0] >> 32) & 1u);
+  int32_t dv[KC];
+#pragma unroll
+  for (int x = 0; x < KC; ++x) dv[x] = in ? (int32_t)(uint32_t)r[1 + x] : 0;
+  // inclusive segmented scan in the wave: (reset, sums)
+  uint32_t xr = first ? 1u : 0u;
+  int64_t xs[KC];
+#pragma unroll
+  for (int x = 0; x < KC; ++x) xs[x] = dv[x];
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t yr = __shfl_up(xr, off);
+    int64_t ys[KC];
+#pragma unroll
+    for (int x = 0; x < KC; ++x) ys[x] = __shfl_up(xs[x], off);
+    if ((int)lane >= off && !xr) {
+      xr = yr;
+#pragma unroll
+      for (int x = 0; x < KC; ++x) xs[x] += ys[x];
+    }
+  }
+  if (lane == 63) {
+    s_wfirst[w] = xr;
+#pragma unroll
+    for (int x = 0; x < KC; ++x) s_wsum[w][x] = xs[x];
+  }
+  __syncthreads();
+  // exclusive value entering this tile: fold earlier waves and the carry
+  int64_t cin[KC];
+  {
+    // inclusive minus own (own tile resets: nothing enters from before)
+    bool reset = xr != 0;
+#pragma unroll
+    for (int x = 0; x < KC; ++x) cin[x] = xs[x] - dv[x];
+    if (first) {
+#pragma unroll
+      for (int x = 0; x < KC; ++x) cin[x] = 0;
+    }
+    // a reset inside this wave before (or at) the tile cuts off everything earlier
+    if (!reset) {
+      for (int q = (int)w - 1; q >= 0; --q) {
+#pragma unroll
+        for (int x = 0; x < KC; ++x) cin[x] += s_wsum[q][x];
+        if (s_wfirst[q]) {
+          reset = true;
+          break;
+        }
+      }
+      if (!reset) {
+#pragma unroll
+        for (int x = 0; x < KC; ++x) cin[x] += s_carry[x];
+      }
+    }
+  }
+  // ---- this tile's U and Q
+  uint64_t uu[NP], qq[NP];
+  uint32_t g = 0xFFFFFFFFu;
+  if (in) {
+    g = (uint32_t)r[0];
+    const uint64_t S0 = r[1 + KC];
+    const uint64_t* S1 = r + 2 + KC;
+    const uint64_t* S2 = r + 2 + 2 * KC;
+    const uint64_t* T = r + 2 + 2 * KC + NP;  // pair order; T[x][x] = T[x]
+    bool always[KC];
+    int64_t av[KC];
+#pragma unroll
+    for (int x = 0; x < KC; ++x) {
+      const int32_t m = (int32_t)(uint32_t)(r[1 + x] >> 32);
+      always[x] = cin[x] + m > 0;
+      av[x] = cin[x] - kLBias;
+    }
+    int k = 0;
+#pragma unroll
+    for (int x = 0; x < KC; ++x) {
+#pragma unroll
+      for (int y = x; y < KC; ++y, ++k) {
+        const uint64_t ax = (uint64_t)av[x], ay = (uint64_t)av[y];
+        const uint64_t tx = T[pair_index<KC>(x, x)], ty = T[pair_index<KC>(y, y)];
+        if (x == y) {
+          uu[k] = always[x] ? S0 : tx;
+          const uint64_t cx2 = (uint64_t)((av[x] * (av[x] - 1)) / 2);
+          qq[k] = S2[k] + ax * S1[x] + cx2 * S0;
+        } else {
+          uu[k] = always[x] && always[y] ? S0 : always[x] ? ty : always[y] ? tx : T[k];
+          qq[k] = S2[k] + ax * S1[y] + ay * S1[x] + ax * ay * S0;
+        }
+      }
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < NP; ++k) {
+      uu[k] = 0;
+      qq[k] = 0;
+    }
+  }
+  // whole waves of one group add once; everything else per tile
+  const uint32_t g0 = __shfl(g, 0);
+  const bool uniform = __ballot(g != g0) == 0ull;
+  int k = 0;
+#pragma unroll
+  for (int x = 0; x < KC; ++x) {
+#pragma unroll
+    for (int y = x; y < KC; ++y, ++k) {
+      uint64_t uv = uu[k], qv = qq[k];
+      if (uniform) {
+        uv = wave_sum64(uv);
+        qv = wave_sum64(qv);
+      }
+      if ((!uniform || lane == 0) && g < a.G) {
+        const uint64_t at = (uint64_t)g * kSweepQWords + (uint64_t)pair_index<KM>(x, y);
+        if (uv) atomicAdd((unsigned long long*)&a.ov_u[at], (unsigned long long)uv);
+        if (qv) atomicAdd((unsigned long long*)&a.ov_q[at], (unsigned long long)qv);
+      }
+    }
+  }
+  if (in && g >= a.G && g != 0xFFFFFFFFu) flag_internal_error(a.counters, 256);
+}
+
+#define ARGUS_KC_SWITCH(K, F) \
+  ((K) == 1 ? (const void*)F<1> : (K) == 2 ? (const void*)F<2> : (K) == 3 ? (const void*)F<3> : \
+   (K) == 4 ? (const void*)F<4> : (K) == 5 ? (const void*)F<5> : (K) == 6 ? (const void*)F<6> : \
+   (K) == 7 ? (const void*)F<7> : (const void*)F<8>)
+
+hipError_t launch_merge_sweep(const RunArgs& a, hipStream_t s) {
+  MergeSweepArgs m{};
+  m.plan = a.w.plan;
+  for (int b = 0; b < 2; ++b) m.ev[b] = a.w.key[b];
+  m.task = (const MergeTask*)a.w.part;
+  m.rec = a.w.mslb;
+  m.counters = a.out.d_counters;
+  const void* kern = ARGUS_KC_SWITCH(a.K, k_merge_sweep);
+  uint64_t blocks = a.w.tiles_cap ? a.w.tiles_cap : 1;
+  const uint64_t resident = persistent_blocks(kern, kMergeThreads);
+  if (blocks > resident) blocks = resident;
+  void* args[] = {&m};
+  hipError_t e = hipLaunchKernel(kern, dim3((uint32_t)blocks), dim3(kMergeThreads), args, 0, s);
+  if (e != hipSuccess) return e;
+  const void* wkern = ARGUS_KC_SWITCH(a.K, k_merge_sweep_wide);
+  uint64_t wblocks = a.w.tiles_cap ? a.w.tiles_cap : 1;
+  const uint64_t wres = persistent_blocks(wkern, kMergeThreads);
+  if (wblocks > wres) wblocks = wres;
+  e = hipLaunchKernel(wkern, dim3((uint32_t)wblocks), dim3(kMergeThreads), args, 0, s);
+  if (e != hipSuccess) return e;
+  OvtArgs o{};
+  o.plan = a.w.plan;
+  o.rec = a.w.mslb;
+  o.blk = (int64_t*)a.w.part;  // the merge tasks are no longer needed
+  o.ov_u = a.w.ov_mask;
+  o.ov_q = a.w.ov_q;
+  o.counters = a.out.d_counters;
+  o.G = a.G;
+  const uint64_t ob = ceil_div(a.w.tiles_cap ? a.w.tiles_cap : 1, kOvtThreads);
+  void* oargs[] = {&o};
+  e = hipLaunchKernel(ARGUS_KC_SWITCH(a.K, k_ovt_agg), dim3((uint32_t)ob), dim3(kOvtThreads), oargs, 0, s);
+  if (e != hipSuccess) return e;
+  return hipLaunchKernel(ARGUS_KC_SWITCH(a.K, k_ovt_final), dim3((uint32_t)ob), dim3(kOvtThreads), oargs, 0, s);
 }
 
 }  // namespace argus

@@ -9,14 +9,14 @@
 //             of class B (unordered pairs when A == B), of their intersection.
 // Events (t_begin, +1, class) and (t_end, -1, class) of matched, classified
 // instances are put in (group, time) order beforehand, either by merging the
-// per-context runs of the sorted records (k_merge: one word per record,
-// group | time | code) or by a radix sort of (group, time) keys with a class
-// payload (k_radix).  This kernel
-// scans the per-class active counts c (segmented by group, decoupled
-// look-back across tiles) and, for each gap between consecutive events of a
-// group, adds gap * [c_A > 0 and c_B > 0] to U and gap * c_A * c_B (or
-// gap * c_A (c_A - 1) / 2 for A == B) to Q.  Equal times give zero gaps, so
-// the order among ties does not matter.
+// per-context runs of the sorted records (k_merge.hip, whose last round also
+// sweeps) or, when merging does not apply, by a radix sort of (group, time)
+// keys with a class payload (k_radix).  This kernel sweeps the radix-sorted
+// events: it scans the per-class active counts c (segmented by group,
+// decoupled look-back across tiles) and, for each gap between consecutive
+// events of a group, adds gap * [c_A > 0 and c_B > 0] to U and gap * c_A *
+// c_B (or gap * c_A (c_A - 1) / 2 for A == B) to Q.  Equal times give zero
+// gaps, so the order among ties does not matter.
 #include "sweep_common.h"
 
 namespace argus {
@@ -45,6 +45,7 @@ __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
   constexpr int NP = KM * (KM + 1) / 2;
   constexpr int IT = kSweepItems;
   const DevPlan* P = a.plan;
+  if (P->ev_merge) return;  // merged events are swept by k_merge_sweep
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   __shared__ uint32_t s_tile;
   __shared__ uint64_t s_u[kSweepSlots][NP];
@@ -58,26 +59,20 @@ __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
   const uint64_t tiles = ceil_div(n, kSweepTile);
   const KeySpace ks = P->ev;
   const bool wide = ks.wide != 0;
-  const bool mfmt = P->ev_merge != 0;
   const uint32_t buf = P->ev_final;
   const uint64_t* gk = a.key[buf];
   const uint32_t* gp = a.pay[buf];
   const uint32_t* gc = a.ctxw[buf];
   constexpr uint32_t kNoGroup = 0xFFFFFFFFu;
   // (group, time, class | is_end << 8) of event i; class 0xFF changes no count
-  auto decode = [&](uint64_t raw, uint32_t pay, uint32_t cw, uint32_t* g, uint64_t* t,
+  auto decode = [&](uint64_t k, uint32_t pay, uint32_t cw, uint32_t* g, uint64_t* t,
                     uint32_t* py) {
-    uint64_t k = raw;
-    if (mfmt) {
-      k = raw >> kEvCodeBits;
-      pay = ev_word_pay(raw);
-    }
     *g = wide ? cw : (ks.ts_bits >= 64 ? 0u : (uint32_t)(k >> ks.ts_bits));
     *t = wide ? k : (k & ks.ts_mask);
     *py = pay;
   };
   auto load_one = [&](uint64_t i, uint32_t* g, uint64_t* t, uint32_t* py) {
-    decode(gk[i], mfmt ? 0u : gp[i], wide ? gc[i] : 0u, g, t, py);
+    decode(gk[i], gp[i], wide ? gc[i] : 0u, g, t, py);
   };
 
   for (;;) {
@@ -96,16 +91,7 @@ __global__ __launch_bounds__(kSweepThreads) void k_sweep(SweepArgs a) {
   // ---- this thread's 8 consecutive events, the one before and the one after
   uint32_t g[IT], py[IT];
   uint64_t t[IT];
-  if (p0 + IT <= cnt && mfmt) {
-    const uint4* e4 = (const uint4*)(gk + base + p0);
-#pragma unroll
-    for (int q = 0; q < IT / 2; ++q) {
-      const uint4 v = e4[q];
-      decode((uint64_t)v.x | ((uint64_t)v.y << 32), 0u, 0u, &g[2 * q], &t[2 * q], &py[2 * q]);
-      decode((uint64_t)v.z | ((uint64_t)v.w << 32), 0u, 0u, &g[2 * q + 1], &t[2 * q + 1],
-             &py[2 * q + 1]);
-    }
-  } else if (p0 + IT <= cnt && !wide) {
+  if (p0 + IT <= cnt && !wide) {
     const uint4* k4 = (const uint4*)(gk + base + p0);
     const uint4* q4 = (const uint4*)(gp + base + p0);
     uint32_t pw[IT];

@@ -1,6 +1,6 @@
-// sweep_common.h -- the per-gap accumulation of the class-overlap sweep,
-// shared by the sweep kernel and the last merge round (which sweeps the
-// events it has just merged).
+// sweep_common.h -- the per-gap accumulation of the class-overlap sweep of
+// radix-sorted events, and the layout of the per-group U and Q rows shared
+// with the last merge round (which sweeps the events it has just merged).
 //
 // For each gap between consecutive events of a group, with per-class
 // active counts c (after the earlier event):
@@ -8,6 +8,8 @@
 //   Q[A][B] += gap * c_A * c_B  (A != B),  gap * c_A (c_A - 1) / 2  (A == B),
 // over class pairs A <= B; all arithmetic mod 2^64.
 #pragma once
+
+#include <type_traits>
 
 #include "internal.h"
 
@@ -23,13 +25,6 @@ __host__ __device__ constexpr int pair_index(int a, int b) {
 // a * b mod 2^64 for a 32-bit b
 __device__ __forceinline__ uint64_t mul64x32(uint64_t a, uint32_t b) {
   return (uint64_t)(uint32_t)a * b + ((uint64_t)((uint32_t)(a >> 32) * b) << 32);
-}
-
-// Payload (class | is_end << 8, class 0xFF: no count changes) of a merged
-// event word (code in the low bits: 0 none, else 1 + 2 * class + is_end).
-__device__ __forceinline__ uint32_t ev_word_pay(uint64_t raw) {
-  const uint32_t c = (uint32_t)(raw & ((1u << kEvCodeBits) - 1u));
-  return c ? ((c - 1u) >> 1) | (((c - 1u) & 1u) << 8) : 0xFFu;
 }
 
 // Adds one gap (gap > 0) to the U and Q accumulators of NP = KM (KM + 1) / 2
