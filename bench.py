@@ -73,8 +73,11 @@ def byte_model(name: str, c: dict, plan: dict, R: int, K: int, G: int, flags: in
         if src == 2:  # first pass: raw records / instances
             return (16.0 * n if not ev else 32.0 * nb) + elem * out_n
         return 2.0 * elem * out_n
-    if name == "check_sorted":
-        return 8.0 * nv
+    if name == "tile_sums":
+        # sorted keys and payloads: order check and per-tile depth maps
+        return (12.0 + (4.0 if wide else 0.0)) * nv
+    if name == "tile_sums_full":
+        return (12.0 + (4.0 if wide else 0.0)) * nv if plan["unsorted"] else 0.0
     if name == "ts_hist":
         return 8.0 * nv if plan["unsorted"] else 0.0
     ev_words = K > 0 and plan["rec_ts_bits"] + (max(G - 1, 0)).bit_length() + 5 <= 64

@@ -48,7 +48,7 @@ size_t align_up(size_t v) { return (v + kAlign - 1) & ~(kAlign - 1); }
 // Workspace layout for n records.  Offsets only; the base is added in run.
 struct Layout {
   size_t plan, rec_hist, rec_off, ev_hist, ev_off, tile_ctr;
-  size_t key[2], pay[2], ctxw[2], lb[2], mlb, slb, mslb, tiles, tree;
+  size_t key[2], pay[2], ctxw[2], lb[2], tsum, carry, slb, mslb, tiles, tree;
   size_t pop_ts, pop_reg, pushes, op_parent, op_sum;
   size_t inst, child_sum, hist_key, ov_mask, ov_q;
   size_t push_pos, pop_pos, ctx_list, ctx_seg, seg_start, seg_split, seg_tile0, part;
@@ -80,7 +80,8 @@ Layout make_layout(const argus_attr_config& c, uint64_t n, bool own_instances) {
   L.lb_words = ceil_div(2 * nn, kSortTile) * kRadixBins;
   for (int b = 0; b < 2; ++b) L.lb[b] = take(sizeof(uint64_t) * L.lb_words);
   L.match_tiles = ceil_div(nn, kMatchTile);
-  L.mlb = take(sizeof(uint64_t) * 4 * L.match_tiles);
+  L.tsum = take(sizeof(uint64_t) * L.match_tiles);
+  L.carry = take(sizeof(TileCarry) * L.match_tiles);
   L.slb = take(sizeof(uint64_t) * 8 * ceil_div(nn, kSweepTile));
   L.tiles = take(sizeof(TileDesc) * L.match_tiles);
   uint64_t leaves = 1;
@@ -267,7 +268,8 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
     w.ctxw[b] = (uint32_t*)(base + L.ctxw[b]);
     w.lb[b] = (uint64_t*)(base + L.lb[b]);
   }
-  w.mlb = (uint64_t*)(base + L.mlb);
+  w.tsum = (uint64_t*)(base + L.tsum);
+  w.carry = (TileCarry*)(base + L.carry);
   w.slb = (uint64_t*)(base + L.slb);
   w.mslb = (uint64_t*)(base + L.mslb);
   w.tiles = (TileDesc*)(base + L.tiles);
@@ -341,11 +343,13 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
       "radix_ctx0b", "radix_ctx1b", "radix_ctx2b", "radix_ctx3b"};
   for (int sl = 0; sl < kPhase2Slot; ++sl)
     if (!step(rnames[sl], launch_radix_pass(a, 0, sl, n, s))) return ARGUS_E_HIP;
-  if (!step("check_sorted", launch_check_sorted(a, s))) return ARGUS_E_HIP;
+  if (!step("tile_sums", launch_tsum(a, 0, s))) return ARGUS_E_HIP;
   if (!step("ts_hist", launch_ts_hist(a, s))) return ARGUS_E_HIP;
   if (!step("plan2", launch_plan2(a, s))) return ARGUS_E_HIP;
   for (int sl = kPhase2Slot; sl < kSlots; ++sl)
     if (!step(rnames[sl], launch_radix_pass(a, 0, sl, n, s))) return ARGUS_E_HIP;
+  if (!step("tile_sums_full", launch_tsum(a, 1, s))) return ARGUS_E_HIP;
+  if (!step("tile_scan", launch_mscan(a, s))) return ARGUS_E_HIP;
   if (!step("match", launch_match(a, s))) return ARGUS_E_HIP;
   if (!step("tree", launch_tree(a, s))) return ARGUS_E_HIP;
   if (!step("resolve", launch_resolve(a, s))) return ARGUS_E_HIP;

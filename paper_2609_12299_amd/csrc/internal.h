@@ -146,6 +146,13 @@ struct TileDesc {
   uint32_t pad;
 };
 
+// Entering values of one matching tile, from a scan over the tile sums.
+struct TileCarry {
+  uint32_t s_in;   // depth before the tile's first record
+  uint32_t hpre;   // context starts before the tile
+  uint64_t nbpre;  // BEGINs before the tile
+};
+
 // Device pointers of one run (workspace carved on the host).
 struct Work {
   DevPlan* plan;
@@ -158,7 +165,8 @@ struct Work {
   uint32_t* pay[2];
   uint32_t* ctxw[2];
   uint64_t* lb[2];      // radix look-back status, [tiles][256]
-  uint64_t* mlb;        // matching look-back status, [tiles][4]
+  uint64_t* tsum;       // matching tile sums, [tiles]
+  TileCarry* carry;     // matching tile entering values, [tiles]
   uint64_t* slb;        // sweep look-back status, [tiles][8]
   uint64_t* mslb;       // last merge round tile records, [tiles_cap][2 + 2K + K(K + 1)]
   TileDesc* tiles;      // [match tiles]
@@ -320,6 +328,67 @@ ARGUS_DEV int32_t wave_incl_scan32(int32_t v) {
   return v;
 }
 
+// ------------------------------------------------- clamped depth maps
+// A prefix of the records maps the depth before it to the depth after it:
+// s -> max(c, s + a), or the constant c once a context starts inside.  The
+// identity is {0, 0, 0} on depths >= 0.  All fields fit 32 bits (n < 2^31).
+struct Fn {
+  uint32_t reset;  // 1: output is the constant c (a context starts inside)
+  int32_t a;
+  int32_t c;       // else output is max(c, s + a)
+};
+
+ARGUS_DEV Fn fn_id() { return Fn{0u, 0, 0}; }
+// g after f
+ARGUS_DEV Fn compose(const Fn& f, const Fn& g) {
+  Fn r;
+  r.reset = g.reset | f.reset;
+  r.a = g.reset ? g.a : (f.reset ? 0 : f.a + g.a);
+  r.c = g.reset ? g.c : (f.c + g.a > g.c ? f.c + g.a : g.c);
+  return r;
+}
+ARGUS_DEV int64_t apply(const Fn& f, int64_t s) {
+  if (f.reset) return f.c;
+  return s + f.a > f.c ? s + f.a : f.c;
+}
+template <int CTRL, int ROWS = 0xF>
+ARGUS_DEV Fn dpp_fn(const Fn& f) {
+  return Fn{dpp32<CTRL, ROWS>(f.reset), (int32_t)dpp32<CTRL, ROWS>((uint32_t)f.a),
+            (int32_t)dpp32<CTRL, ROWS>((uint32_t)f.c)};
+}
+ARGUS_DEV Fn shfl_down_fn(const Fn& f, int o) {
+  return Fn{(uint32_t)__shfl_down((int)f.reset, o), __shfl_down(f.a, o), __shfl_down(f.c, o)};
+}
+ARGUS_DEV Fn shfl_fn(const Fn& f, int src) {
+  return Fn{(uint32_t)__shfl((int)f.reset, src), __shfl(f.a, src), __shfl(f.c, src)};
+}
+// Inclusive scan of the maps over the wave (lane order = record order).
+ARGUS_DEV Fn wave_scan_fn(Fn x) {
+  x = compose(dpp_fn<kDppRowShr + 1>(x), x);
+  x = compose(dpp_fn<kDppRowShr + 2>(x), x);
+  x = compose(dpp_fn<kDppRowShr + 4>(x), x);
+  x = compose(dpp_fn<kDppRowShr + 8>(x), x);
+  x = compose(dpp_fn<kDppBcast15, 0xA>(x), x);
+  x = compose(dpp_fn<kDppBcast31, 0xC>(x), x);
+  return x;
+}
+
+// Summary of one matching tile (2048 records) in one word: number of
+// BEGINs (12 bits), c (12 bits), a + 2048 (13 bits), reset (1 bit), number
+// of context starts (12 bits).  BEGIN and start counts travel packed as
+// nb | starts << 16.
+ARGUS_DEV uint64_t pack_tile_sum(const Fn& f, uint32_t nbh) {
+  return ((uint64_t)(nbh >> 16) << 41) | ((uint64_t)f.reset << 40) |
+         ((uint64_t)(uint32_t)(f.a + 2048) << 24) | ((uint64_t)(uint32_t)f.c << 12) |
+         (uint64_t)(nbh & 0xFFFFu);
+}
+ARGUS_DEV void unpack_tile_sum(uint64_t v, Fn* f, uint32_t* nbh) {
+  f->reset = (uint32_t)(v >> 40) & 1u;
+  f->a = (int32_t)((v >> 24) & 0x1FFFull) - 2048;
+  f->c = (int32_t)((v >> 12) & 0xFFFull);
+  *nbh = (uint32_t)(v & 0xFFFull) | ((uint32_t)((v >> 41) & 0xFFFull) << 16);
+}
+
 // Look-back status words: bits 62..63 hold the state, bits 0..61 the value.
 constexpr uint64_t kFlagAgg = 1ull << 62;
 constexpr uint64_t kFlagIncl = 2ull << 62;
@@ -332,7 +401,8 @@ hipError_t launch_ingest(const RunArgs& a, hipStream_t s);
 hipError_t launch_plan(const RunArgs& a, hipStream_t s);
 hipError_t launch_radix_pass(const RunArgs& a, int which /*0 rec, 1 ev*/, int slot,
                              uint64_t max_elems, hipStream_t s);
-hipError_t launch_check_sorted(const RunArgs& a, hipStream_t s);
+hipError_t launch_tsum(const RunArgs& a, int mode, hipStream_t s);
+hipError_t launch_mscan(const RunArgs& a, hipStream_t s);
 hipError_t launch_ts_hist(const RunArgs& a, hipStream_t s);
 hipError_t launch_plan2(const RunArgs& a, hipStream_t s);
 hipError_t launch_match(const RunArgs& a, hipStream_t s);

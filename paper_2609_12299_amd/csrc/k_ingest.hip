@@ -139,7 +139,6 @@ hipError_t launch_init(const RunArgs& a, hipStream_t s) {
   add(w.tile_ctr, sizeof(uint32_t) * kCtrCount, 0);
   // look-back status of the first record pass (its tiles cover every record)
   add(w.lb[0], sizeof(uint64_t) * ceil_div(a.n ? a.n : 1, kSortTile) * kRadixBins, 0);
-  add(w.mlb, sizeof(uint64_t) * 4 * w.match_tiles, 0);
   add(w.slb, sizeof(uint64_t) * 8 * ceil_div(a.n ? a.n : 1, kSweepTile), 0);
   if (a.K > 0) {
     add(w.ov_mask, sizeof(uint64_t) * kMasks * a.G, 0);
@@ -407,46 +406,208 @@ hipError_t launch_plan2(const RunArgs& a, hipStream_t s) {
 
 // ----------------------------------------------------------- sortedness
 
-struct CheckArgs {
+struct TsumArgs {
   DevPlan* plan;
   const uint64_t* key[2];
+  const uint32_t* pay[2];
   const uint32_t* ctxw[2];
+  uint64_t* tsum;  // [match tiles]
+  uint32_t mode;   // 0: after the context passes (check the order too); 1: after the full sort
 };
 
-// After the context-only passes: is the (ctx, ts) order non-decreasing?  If
-// not (some context was out of time order in the input), the full sort runs.
-__global__ __launch_bounds__(256) void k_check_sorted(CheckArgs a) {
+// Per matching tile (2048 consecutive sorted records): the map from the depth
+// before the tile to the depth after it, its BEGINs and its context starts
+// (k_mscan turns these into each tile's entering values, so that k_match
+// needs no look-back).  In mode 0 it also checks that the context-only sort
+// left (ctx, ts) non-decreasing; if not (some context was out of time order
+// in the input) the full sort runs and mode 1 redoes the sums.
+__global__ __launch_bounds__(256) void k_tsum(TsumArgs a) {
   DevPlan* p = a.plan;
-  if (p->force_full) {
+  if (a.mode == 0 && p->force_full) {
     if (blockIdx.x == 0 && threadIdx.x == 0) p->unsorted = 1;
     return;
   }
-  const uint64_t n = p->n_valid;
-  if (n < 2) return;
+  if (a.mode == 1 && !p->unsorted) return;
+  __shared__ Fn s_wfn[4];
+  __shared__ uint32_t s_wnb[4];
+  const uint64_t nv = p->n_valid;
+  const uint64_t tiles = ceil_div(nv, kMatchTile);
   const uint32_t b = p->rec_final;
   const uint64_t* key = a.key[b];
+  const uint32_t* pay = a.pay[b];
   const uint32_t* cw = a.ctxw[b];
-  const bool wide = p->rec.wide != 0;
+  const KeySpace ks = p->rec;
+  const bool wide = ks.wide != 0;
+  const uint32_t tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const uint32_t p0 = tid * kMatchItems;
+  auto ctx_of = [&](uint64_t i, uint64_t k) -> uint32_t {
+    return wide ? cw[i] : (ks.ts_bits >= 64 ? 0u : (uint32_t)(k >> ks.ts_bits));
+  };
   bool bad = false;
-  const uint64_t stride = (uint64_t)gridDim.x * 256;
-  for (uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x; i + 1 < n; i += stride) {
-    const uint64_t k0 = key[i], k1 = key[i + 1];
-    if (!wide) {
-      bad |= k0 > k1;
+  for (uint64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+    const uint64_t base = tile * kMatchTile;
+    const uint32_t cnt = nv - base < (uint64_t)kMatchTile ? (uint32_t)(nv - base) : (uint32_t)kMatchTile;
+    uint64_t k[kMatchItems];
+    uint32_t c[kMatchItems], kind = 0, fv = 0;
+    if (p0 + kMatchItems <= cnt) {
+      const uint4* k4 = (const uint4*)(key + base + p0);
+#pragma unroll
+      for (int q = 0; q < kMatchItems / 2; ++q) {
+        const uint4 v = k4[q];
+        k[2 * q] = (uint64_t)v.x | ((uint64_t)v.y << 32);
+        k[2 * q + 1] = (uint64_t)v.z | ((uint64_t)v.w << 32);
+      }
+      const uint4* p4 = (const uint4*)(pay + base + p0);
+#pragma unroll
+      for (int q = 0; q < kMatchItems / 4; ++q) {
+        const uint4 v = p4[q];
+        kind |= ((v.x >> 16) & 1u) << (4 * q) | ((v.y >> 16) & 1u) << (4 * q + 1) |
+                ((v.z >> 16) & 1u) << (4 * q + 2) | ((v.w >> 16) & 1u) << (4 * q + 3);
+      }
+      fv = 0xFFu;
     } else {
-      const uint32_t c0 = cw[i], c1 = cw[i + 1];
-      bad |= (c0 > c1) || (c0 == c1 && k0 > k1);
+#pragma unroll
+      for (int i = 0; i < kMatchItems; ++i) {
+        const uint32_t q = p0 + i;
+        k[i] = q < cnt ? key[base + q] : 0ull;
+        if (q < cnt) {
+          kind |= ((pay[base + q] >> 16) & 1u) << i;
+          fv |= 1u << i;
+        }
+      }
     }
+#pragma unroll
+    for (int i = 0; i < kMatchItems; ++i) c[i] = ctx_of(base + p0 + i < nv ? base + p0 + i : 0, k[i]);
+    // the record before this thread's first one
+    uint32_t c_prev = (uint32_t)__shfl_up((int)c[kMatchItems - 1], 1);
+    uint64_t k_prev = __shfl_up(k[kMatchItems - 1], 1);
+    bool has_prev = true;
+    if (lane == 0) {
+      const uint64_t pp = base + p0;
+      has_prev = pp > 0 && pp <= nv;
+      if (has_prev) {
+        k_prev = key[pp - 1];
+        c_prev = ctx_of(pp - 1, k_prev);
+      }
+    }
+    Fn f = fn_id();
+    uint32_t nb = 0, nh = 0;
+#pragma unroll
+    for (int i = 0; i < kMatchItems; ++i) {
+      if (!((fv >> i) & 1u)) continue;
+      const bool hp = i > 0 || has_prev;
+      const uint32_t cp = i > 0 ? c[i - 1] : c_prev;
+      const uint64_t kp = i > 0 ? k[i - 1] : k_prev;
+      const bool head = !hp || cp != c[i];
+      if (a.mode == 0 && hp) bad |= wide ? (cp > c[i] || (cp == c[i] && kp > k[i])) : kp > k[i];
+      const bool isb = ((kind >> i) & 1u) == 0;
+      const Fn e = head ? Fn{1u, 0, isb ? 1 : 0} : Fn{0u, isb ? 1 : -1, 0};
+      f = compose(f, e);
+      nb += isb;
+      nh += head;
+    }
+    // tile sums: wave scans, then the four waves in order
+    const Fn x = wave_scan_fn(f);
+    const uint32_t nbx = (uint32_t)wave_incl_scan32((int32_t)(nb | (nh << 16)));
+    if (lane == 63) {
+      s_wfn[w] = x;
+      s_wnb[w] = nbx;
+    }
+    __syncthreads();
+    if (tid == 0) {
+      Fn all = fn_id();
+      uint32_t nball = 0;
+      for (int q = 0; q < 4; ++q) {
+        all = compose(all, s_wfn[q]);
+        nball += s_wnb[q];
+      }
+      a.tsum[tile] = pack_tile_sum(all, nball);
+    }
+    __syncthreads();
   }
-  if (__syncthreads_or(bad) && threadIdx.x == 0) p->unsorted = 1;
+  if (a.mode == 0 && __syncthreads_or(bad) && threadIdx.x == 0) p->unsorted = 1;
 }
 
-hipError_t launch_check_sorted(const RunArgs& a, hipStream_t s) {
-  CheckArgs ca{a.w.plan, {a.w.key[0], a.w.key[1]}, {a.w.ctxw[0], a.w.ctxw[1]}};
-  uint64_t blocks = ceil_div(a.n, 256 * 16);
-  if (blocks > 2048) blocks = 2048;
+hipError_t launch_tsum(const RunArgs& a, int mode, hipStream_t s) {
+  TsumArgs ta{};
+  ta.plan = a.w.plan;
+  for (int b = 0; b < 2; ++b) {
+    ta.key[b] = a.w.key[b];
+    ta.pay[b] = a.w.pay[b];
+    ta.ctxw[b] = a.w.ctxw[b];
+  }
+  ta.tsum = a.w.tsum;
+  ta.mode = (uint32_t)mode;
+  uint64_t blocks = a.w.match_tiles;
+  const uint64_t resident = persistent_blocks((const void*)k_tsum, 256);
+  if (blocks > resident) blocks = resident;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(k_check_sorted, dim3((uint32_t)blocks), dim3(256), 0, s, ca);
+  hipLaunchKernelGGL(k_tsum, dim3((uint32_t)blocks), dim3(256), 0, s, ta);
+  return hipGetLastError();
+}
+
+struct MscanArgs {
+  const DevPlan* plan;
+  const uint64_t* tsum;
+  TileCarry* carry;
+};
+
+// Entering values of every matching tile: an exclusive scan of the tile sums
+// (one block; each thread composes a contiguous run of tiles).
+__global__ __launch_bounds__(1024) void k_mscan(MscanArgs a) {
+  __shared__ Fn s_wfn[16];
+  __shared__ uint32_t s_wnb[16], s_wnh[16];
+  const uint64_t tiles = a.plan->match_tiles;
+  const uint32_t t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const uint64_t per = ceil_div(tiles, 1024);
+  const uint64_t k0 = (uint64_t)t * per, k1 = k0 + per < tiles ? k0 + per : tiles;
+  Fn f = fn_id();
+  uint32_t nb = 0, nh = 0;
+  for (uint64_t k = k0; k < k1; ++k) {
+    Fn g;
+    uint32_t nbh;
+    unpack_tile_sum(a.tsum[k], &g, &nbh);
+    f = compose(f, g);
+    nb += nbh & 0xFFFFu;
+    nh += nbh >> 16;
+  }
+  const Fn x = wave_scan_fn(f);
+  const uint32_t xb = (uint32_t)wave_incl_scan32((int32_t)nb);
+  const uint32_t xh = (uint32_t)wave_incl_scan32((int32_t)nh);
+  if (lane == 63) {
+    s_wfn[w] = x;
+    s_wnb[w] = xb;
+    s_wnh[w] = xh;
+  }
+  Fn ex = Fn{(uint32_t)__shfl_up((int)x.reset, 1), __shfl_up(x.a, 1), __shfl_up(x.c, 1)};
+  if (lane == 0) ex = fn_id();
+  __syncthreads();
+  Fn pre = fn_id();
+  uint64_t pb = xb - nb, ph = xh - nh;
+  for (uint32_t q = 0; q < w; ++q) {
+    pre = compose(pre, s_wfn[q]);
+    pb += s_wnb[q];
+    ph += s_wnh[q];
+  }
+  f = compose(pre, ex);  // map from depth 0 before the data to the depth before tile k0
+  for (uint64_t k = k0; k < k1; ++k) {
+    Fn g;
+    uint32_t nbh;
+    unpack_tile_sum(a.tsum[k], &g, &nbh);
+    TileCarry c;
+    c.s_in = (uint32_t)apply(f, 0);
+    c.hpre = (uint32_t)ph;
+    c.nbpre = pb;
+    a.carry[k] = c;
+    f = compose(f, g);
+    pb += nbh & 0xFFFFu;
+    ph += nbh >> 16;
+  }
+}
+
+hipError_t launch_mscan(const RunArgs& a, hipStream_t s) {
+  MscanArgs m{a.w.plan, a.w.tsum, a.w.carry};
+  hipLaunchKernelGGL(k_mscan, dim3(1), dim3(1024), 0, s, m);
   return hipGetLastError();
 }
 

@@ -15,7 +15,8 @@
 // Both are previous-smaller-value searches, answered here on a min-tree over
 // x held in LDS.  The map s -> max(c, s + a) (or a constant after a context
 // start) composes associatively, so the depth entering each tile comes from
-// a decoupled look-back over tiles.  What a tile cannot resolve locally --
+// a scan over per-tile sums done beforehand (k_tsum, k_mscan), and tiles are
+// processed independently.  What a tile cannot resolve locally --
 // ENDs that pop a level open at the tile start, BEGINs still open at its end,
 // parents opened in an earlier tile -- is summarised per tile and resolved
 // by k_resolve.
@@ -25,63 +26,6 @@
 #include "internal.h"
 
 namespace argus {
-
-struct Fn {
-  uint32_t reset;  // 1: output is the constant c (a context starts inside)
-  int64_t a;
-  int64_t c;       // else output is max(c, s + a)
-};
-
-__device__ __forceinline__ Fn fn_id() { return Fn{0u, 0, 0}; }
-// g after f
-__device__ __forceinline__ Fn compose(const Fn& f, const Fn& g) {
-  if (g.reset) return g;
-  Fn r;
-  r.reset = f.reset;
-  r.a = f.reset ? 0 : f.a + g.a;
-  r.c = f.c + g.a > g.c ? f.c + g.a : g.c;
-  return r;
-}
-__device__ __forceinline__ int64_t apply(const Fn& f, int64_t s) {
-  if (f.reset) return f.c;
-  return s + f.a > f.c ? s + f.a : f.c;
-}
-__device__ __forceinline__ Fn shfl_up_fn(const Fn& f, int o) {
-  Fn r;
-  r.reset = __shfl_up(f.reset, o);
-  r.a = __shfl_up(f.a, o);
-  r.c = __shfl_up(f.c, o);
-  return r;
-}
-
-__device__ __forceinline__ Fn shfl_down_fn(const Fn& f, int o) {
-  Fn r;
-  r.reset = __shfl_down(f.reset, o);
-  r.a = __shfl_down(f.a, o);
-  r.c = __shfl_down(f.c, o);
-  return r;
-}
-__device__ __forceinline__ Fn shfl_fn(const Fn& f, int src) {
-  Fn r;
-  r.reset = __shfl(f.reset, src);
-  r.a = __shfl(f.a, src);
-  r.c = __shfl(f.c, src);
-  return r;
-}
-
-// Tile aggregate in one status word: number of BEGINs (12 bits), c (12
-// bits), a + 2048 (13 bits), reset (1 bit), number of context starts (12
-// bits).  BEGIN and start counts travel packed as nb | starts << 16.
-__device__ __forceinline__ uint64_t pack_agg(const Fn& f, uint32_t nbh) {
-  return kFlagAgg | ((uint64_t)(nbh >> 16) << 41) | ((uint64_t)f.reset << 40) |
-         ((uint64_t)(f.a + 2048) << 24) | ((uint64_t)f.c << 12) | (uint64_t)(nbh & 0xFFFFu);
-}
-__device__ __forceinline__ void unpack_agg(uint64_t v, Fn* f, uint32_t* nbh) {
-  f->reset = (uint32_t)(v >> 40) & 1u;
-  f->a = (int64_t)((v >> 24) & 0x1FFFull) - 2048;
-  f->c = (int64_t)((v >> 12) & 0xFFFull);
-  *nbh = (uint32_t)(v & 0xFFFull) | ((uint32_t)((v >> 41) & 0xFFFull) << 16);
-}
 
 // Min tree over the tile's 2048 leaves with fan-out 8, in LDS.  A leaf is
 // the pair (x + 1, rank | region << 11): the local BEGIN rank and the region
@@ -119,13 +63,9 @@ __device__ __forceinline__ uint32_t leaf_hit8(const uint2* g, uint32_t v) {
 }
 
 // Second word of the last leaf q < 8 * chunk with x + 1 <= v, or kNoHit.
-// g1 holds the chunk's level-1 sibling group (read once per thread).
-__device__ __forceinline__ uint32_t psv_hit(const uint2* leaf, const uint32_t* up,
-                                            const uint32_t (&g1)[8], uint32_t chunk, uint32_t v) {
-  int j = -1;
-#pragma unroll
-  for (int k = 0; k < 8; ++k)
-    if ((uint32_t)k < (chunk & 7u) && g1[k] <= v) j = k;
+__device__ __forceinline__ uint32_t psv_hit(const uint2* leaf, const uint32_t* up, uint32_t chunk,
+                                            uint32_t v) {
+  int j = last_le8(up + kU1 + (chunk & ~7u), chunk & 7u, v);
   int n1;
   if (j >= 0) {
     n1 = (int)(chunk & ~7u) + j;
@@ -154,7 +94,7 @@ struct MatchArgs {
   argus_instance* inst;
   uint64_t* child_sum;
   TileDesc* tiles;
-  uint64_t* mlb;
+  const TileCarry* carry;
   uint64_t* pop_ts;
   uint32_t* pop_reg;
   uint32_t* pushes;
@@ -174,25 +114,30 @@ struct MatchArgs {
 
 constexpr uint32_t kParNone = 0xFFFFFFFFu;
 constexpr uint32_t kParOut = 0xFFFFFFFEu;
+// Child sums of enclosing instances (open when the tile starts) are kept in
+// LDS for the nearest kOcCap levels; deeper ones go to global memory.
+constexpr uint32_t kOcCap = 512;
+constexpr uint32_t kQueueCap = kMatchTile / 4;  // queued searches per wave
 
 __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   const DevPlan* P = a.plan;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const uint32_t tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   constexpr int IT = kMatchItems;
 
   __shared__ uint32_t s_tile;
-  __shared__ uint2 s_leaf[kMatchTile];         // tree leaves, then out-of-tile child sums
-  __shared__ uint32_t s_up[kUpSize];           // upper tree levels
-  __shared__ uint64_t s_tend[kMatchTile];      // t_end of each local BEGIN closed in the tile
-  __shared__ uint64_t s_cs[kMatchTile];        // child sums of each local BEGIN
-  __shared__ uint16_t s_ereg[kMatchTile];      // end region of each local BEGIN (0xFFFF: open)
-  __shared__ uint32_t s_lastctx[kMatchThreads];
+  // tree leaves during the searches; then the child sums of local BEGINs
+  __shared__ uint2 s_leaf[kMatchTile];
+  __shared__ uint32_t s_up[kUpSize];  // upper tree levels
+  // search queues (one per wave) during the searches; then the end time of
+  // each local BEGIN closed in the tile
+  __shared__ uint64_t s_tend[kMatchTile];
+  __shared__ uint16_t s_ereg[kMatchTile];  // end region of each local BEGIN (0xFFFF: open)
+  __shared__ uint64_t s_oc[kOcCap];        // child sums of enclosing instances
   __shared__ Fn s_wfn[4];
   __shared__ uint32_t s_wnb[4];
-  __shared__ uint32_t s_prevctx, s_hasprev;
   __shared__ uint32_t s_first, s_lastp1, s_heads, s_lo, s_sout, s_maxlvl, s_orph;
   __shared__ uint32_t s_sin, s_nbpre_lo, s_nbpre_hi, s_hpre, s_need;
-  uint64_t* s_oc = (uint64_t*)s_leaf;
+  uint64_t* s_cs = (uint64_t*)s_leaf;
 
   const KeySpace ks = P->rec;
   const bool wide = ks.wide != 0;
@@ -214,10 +159,6 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   auto group_of = [&](uint32_t raw_ctx) -> uint32_t {
     return a.shift >= 32 ? 0u : (raw_ctx >> a.shift);
   };
-  // cls: the record's region class, or 0xFF when its events do not count
-  auto ev_code = [&](uint32_t cls, uint32_t is_end) -> uint32_t {
-    return cls < a.K ? 1u + 2u * cls + is_end : 0u;
-  };
 
   for (;;) {
   if (tid == 0) {
@@ -235,87 +176,94 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   if (tile >= P->match_tiles) break;
   const uint64_t base = tile * kMatchTile;
   const uint32_t cnt = nv - base < (uint64_t)kMatchTile ? (uint32_t)(nv - base) : (uint32_t)kMatchTile;
-  const uint32_t p0 = (uint32_t)tid * IT;
+  const uint32_t p0 = tid * IT;
 
   // ---- blocked load: this thread's 8 consecutive records, 16-byte loads
-  uint64_t key[IT];
-  uint32_t pay[IT], ctxr[IT];
-  if (p0 + IT <= cnt) {
-    const uint4* k4 = (const uint4*)(gk + base + p0);
+  uint64_t ts[IT];
+  uint32_t ctxr[IT], reg[IT];
+  uint32_t fb = 0, fv = 0;  // bit i: BEGIN / valid
+  {
+    uint64_t key[IT];
+    uint32_t pay[IT];
+    if (p0 + IT <= cnt) {
+      const uint4* k4 = (const uint4*)(gk + base + p0);
 #pragma unroll
-    for (int q = 0; q < IT / 2; ++q) {
-      const uint4 v = k4[q];
-      key[2 * q] = (uint64_t)v.x | ((uint64_t)v.y << 32);
-      key[2 * q + 1] = (uint64_t)v.z | ((uint64_t)v.w << 32);
-    }
-    const uint4* p4 = (const uint4*)(gp + base + p0);
-#pragma unroll
-    for (int q = 0; q < IT / 4; ++q) {
-      const uint4 v = p4[q];
-      pay[4 * q] = v.x;
-      pay[4 * q + 1] = v.y;
-      pay[4 * q + 2] = v.z;
-      pay[4 * q + 3] = v.w;
-    }
-    if (wide) {
-      const uint4* c4 = (const uint4*)(gc + base + p0);
+      for (int q = 0; q < IT / 2; ++q) {
+        const uint4 v = k4[q];
+        key[2 * q] = (uint64_t)v.x | ((uint64_t)v.y << 32);
+        key[2 * q + 1] = (uint64_t)v.z | ((uint64_t)v.w << 32);
+      }
+      const uint4* p4 = (const uint4*)(gp + base + p0);
 #pragma unroll
       for (int q = 0; q < IT / 4; ++q) {
-        const uint4 v = c4[q];
-        ctxr[4 * q] = v.x;
-        ctxr[4 * q + 1] = v.y;
-        ctxr[4 * q + 2] = v.z;
-        ctxr[4 * q + 3] = v.w;
+        const uint4 v = p4[q];
+        pay[4 * q] = v.x;
+        pay[4 * q + 1] = v.y;
+        pay[4 * q + 2] = v.z;
+        pay[4 * q + 3] = v.w;
+      }
+      if (wide) {
+        const uint4* c4 = (const uint4*)(gc + base + p0);
+#pragma unroll
+        for (int q = 0; q < IT / 4; ++q) {
+          const uint4 v = c4[q];
+          ctxr[4 * q] = v.x;
+          ctxr[4 * q + 1] = v.y;
+          ctxr[4 * q + 2] = v.z;
+          ctxr[4 * q + 3] = v.w;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < IT; ++i) {
+        const uint32_t p = p0 + i;
+        key[i] = p < cnt ? gk[base + p] : 0;
+        pay[i] = p < cnt ? gp[base + p] : 0;
+        if (wide) ctxr[i] = p < cnt ? gc[base + p] : 0;
       }
     }
-  } else {
 #pragma unroll
     for (int i = 0; i < IT; ++i) {
-      const uint32_t p = p0 + i;
-      key[i] = p < cnt ? gk[base + p] : 0;
-      pay[i] = p < cnt ? gp[base + p] : 0;
-      if (wide) ctxr[i] = p < cnt ? gc[base + p] : 0;
+      if (!wide) ctxr[i] = ctx_of_key(key[i]);
+      ts[i] = ks.ts_min + (wide ? key[i] : (key[i] & ks.ts_mask));
+      reg[i] = pay[i] & 0xFFFFu;
+      if (p0 + i < cnt) {
+        fv |= 1u << i;
+        if (((pay[i] >> 16) & 1u) == 0) fb |= 1u << i;
+      }
     }
   }
-  uint64_t ts[IT];
-  uint32_t reg[IT];
-#pragma unroll
-  for (int i = 0; i < IT; ++i) {
-    if (!wide) ctxr[i] = ctx_of_key(key[i]);
-    ts[i] = ks.ts_min + (wide ? key[i] : (key[i] & ks.ts_mask));
-    reg[i] = pay[i] & 0xFFFFu;
-  }
   // Region classes of the records, fetched now so that their latency hides
-  // behind the scan and the look-back.
-  uint32_t cls[IT];
+  // behind the scan and the look-back (packed 8 bits each).
+  uint32_t clsp[2] = {0xFFFFFFFFu, 0xFFFFFFFFu};
+  if (ev_on) {
 #pragma unroll
-  for (int i = 0; i < IT; ++i) {
-    cls[i] = 0xFFu;
-    if (ev_on && p0 + i < cnt && group_of(ctxr[i] + (uint32_t)ks.ctx_min) < a.G)
-      cls[i] = a.region_class[reg[i]];
+    for (int i = 0; i < IT; ++i) {
+      uint32_t c = 0xFFu;
+      if ((fv >> i) & 1u && group_of(ctxr[i] + (uint32_t)ks.ctx_min) < a.G) c = a.region_class[reg[i]];
+      clsp[i >> 2] = (clsp[i >> 2] & ~(0xFFu << (8 * (i & 3)))) | (c << (8 * (i & 3)));
+    }
   }
-  // context of the record before this thread's first one
-  s_lastctx[tid] = ctxr[IT - 1];
-  if (tid == 0) {
-    s_hasprev = base > 0;
-    s_prevctx = base > 0 ? (wide ? gc[base - 1] : ctx_of_key(gk[base - 1])) : 0u;
+  // context of the record before this thread's first one: the previous
+  // lane's last record, or (lane 0) a load of the record before
+  uint32_t prev0 = (uint32_t)__shfl_up((int)ctxr[IT - 1], 1);
+  bool has_prev0 = true;
+  if (lane == 0) {
+    const uint64_t pp = base + p0;
+    has_prev0 = pp > 0;
+    prev0 = pp > 0 ? (wide ? gc[pp - 1] : ctx_of_key(gk[pp - 1])) : 0u;
   }
-  __syncthreads();
-  const bool has_prev0 = tid > 0 || s_hasprev != 0;
-  const uint32_t prev0 = tid > 0 ? s_lastctx[tid - 1] : s_prevctx;
 
-  uint32_t fb = 0, fh = 0, fv = 0;  // bit i: BEGIN / context start / valid
+  uint32_t fh = 0;  // bit i: context start
   Fn f = fn_id();
   uint32_t nb = 0;
   uint32_t first_head = kMatchTile, last_p1 = 0, nheads = 0;
 #pragma unroll
   for (int i = 0; i < IT; ++i) {
     const uint32_t p = p0 + i;
-    if (p < cnt) {
-      const bool isb = ((pay[i] >> 16) & 1u) == 0;
+    if ((fv >> i) & 1u) {
+      const bool isb = (fb >> i) & 1u;
       const bool head = i > 0 ? ctxr[i - 1] != ctxr[i] : (!has_prev0 || prev0 != ctxr[i]);
-      fv |= 1u << i;
-      if (isb) fb |= 1u << i;
       if (head) {
         fh |= 1u << i;
         first_head = p < first_head ? p : first_head;
@@ -335,31 +283,20 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
 
   // ---- block exclusive scan of the per-thread maps, BEGIN counts and
   // context-start counts (packed as nb | starts << 16)
-  Fn x = f;
-  uint32_t nbx = nb | (nheads << 16);
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const Fn y = shfl_up_fn(x, o);
-    const uint32_t ny = __shfl_up(nbx, o);
-    if (lane >= o) {
-      x = compose(y, x);
-      nbx += ny;
-    }
-  }
-  Fn ex = shfl_up_fn(x, 1);
-  uint32_t nbex = __shfl_up(nbx, 1);
-  if (lane == 0) {
-    ex = fn_id();
-    nbex = 0;
-  }
+  const Fn x = wave_scan_fn(f);
+  const uint32_t nbh = nb | (nheads << 16);
+  const uint32_t nbx = (uint32_t)wave_incl_scan32((int32_t)nbh);
   if (lane == 63) {
     s_wfn[w] = x;
     s_wnb[w] = nbx;
   }
+  Fn ex = Fn{(uint32_t)__shfl_up((int)x.reset, 1), __shfl_up(x.a, 1), __shfl_up(x.c, 1)};
+  uint32_t nbex = nbx - nbh;
+  if (lane == 0) ex = fn_id();
   __syncthreads();
   Fn pre = fn_id();
   uint32_t pnb = 0;
-  for (int k = 0; k < w; ++k) {
+  for (uint32_t k = 0; k < w; ++k) {
     pre = compose(pre, s_wfn[k]);
     pnb += s_wnb[k];
   }
@@ -368,91 +305,14 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   const uint32_t tnb = tnbh & 0xFFFFu;  // BEGINs of the tile before this thread
   const uint32_t thd = tnbh >> 16;      // context starts of the tile before this thread
 
-  // ---- decoupled look-back: depth entering the tile, BEGINs before it.
-  // Wave 0 inspects 64 predecessor tiles per round trip (lane j: the j-th
-  // nearest not yet folded in) and folds the aggregates up to the nearest
-  // inclusive value, or up to the nearest tile that has published nothing.
-  if (w == 0) {
-    Fn all = fn_id();
-    uint32_t nball = 0;
-    for (int k = 0; k < 4; ++k) {
-      all = compose(all, s_wfn[k]);
-      nball += s_wnb[k];
-    }
-    uint64_t s_in = 0, nbpre = 0, hpre = 0;
-    uint64_t* lb = a.mlb;
-    if (tile > 0) {
-      if (lane == 0) st_agent(&lb[tile * 4], pack_agg(all, nball));
-      Fn acc = fn_id();
-      uint64_t nb_acc = 0, h_acc = 0;
-      int64_t top = (int64_t)tile - 1;  // nearest tile not yet folded in
-      uint32_t spins = 0;
-      for (;;) {
-        const int64_t tt = top - lane;
-        uint64_t w0 = 0, w1 = 0, w2 = 0, w3 = 0;
-        if (tt >= 0) {
-          w1 = ld_agent(&lb[tt * 4 + 1]);
-          w2 = ld_agent(&lb[tt * 4 + 2]);
-          w3 = ld_agent(&lb[tt * 4 + 3]);
-          w0 = ld_agent(&lb[tt * 4]);
-        }
-        const bool incl = (w1 & ~kValMask) == kFlagIncl && (w2 & ~kValMask) == kFlagIncl &&
-                          (w3 & ~kValMask) == kFlagIncl;
-        const bool agg = (w0 & ~kValMask) == kFlagAgg;
-        const uint64_t mi = __ballot(incl), mn = __ballot(!incl && !agg);
-        const int ji = mi ? __ffsll((unsigned long long)mi) - 1 : 64;
-        const int jn = mn ? __ffsll((unsigned long long)mn) - 1 : 64;
-        const bool done = ji < jn;
-        const int k = done ? ji : jn;  // lanes [0, k) hold aggregates to fold in
-        Fn x = fn_id();
-        uint32_t nx = 0, hx = 0;  // BEGINs, context starts
-        if (lane < k) {
-          uint32_t nbh;
-          unpack_agg(w0, &x, &nbh);
-          nx = nbh & 0xFFFFu;
-          hx = nbh >> 16;
-        }
-        // reduce towards lane 0; a higher lane is an earlier tile
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-          const Fn y = shfl_down_fn(x, o);
-          const uint32_t ny = __shfl_down(nx, o), hy = __shfl_down(hx, o);
-          if (lane + o < 64) {
-            x = compose(y, x);
-            nx += ny;
-            hx += hy;
-          }
-        }
-        acc = compose(shfl_fn(x, 0), acc);
-        nb_acc += (uint32_t)__shfl(nx, 0);
-        h_acc += (uint32_t)__shfl(hx, 0);
-        if (done) {
-          const uint64_t v1 = __shfl(w1, ji), v2 = __shfl(w2, ji), v3 = __shfl(w3, ji);
-          s_in = (uint64_t)apply(acc, (int64_t)(v1 & kValMask));
-          nbpre = (v2 & kValMask) + nb_acc;
-          hpre = (v3 & kValMask) + h_acc;
-          break;
-        }
-        top -= k;
-        if (k == 0) {
-          if (++spins > kMaxSpins) {
-            if (lane == 0) flag_internal_error(a.counters, 8);
-            break;
-          }
-          backoff();
-        }
-      }
-    }
-    if (lane == 0) {
-      const uint64_t s_out = (uint64_t)apply(all, (int64_t)s_in);
-      st_agent(&lb[tile * 4 + 1], kFlagIncl | s_out);
-      st_agent(&lb[tile * 4 + 2], kFlagIncl | (nbpre + (nball & 0xFFFFu)));
-      st_agent(&lb[tile * 4 + 3], kFlagIncl | (hpre + (nball >> 16)));
-      s_sin = (uint32_t)s_in;
-      s_hpre = (uint32_t)hpre;
-      s_nbpre_lo = (uint32_t)nbpre;
-      s_nbpre_hi = (uint32_t)(nbpre >> 32);
-    }
+  // ---- entering values of the tile (depth, BEGINs and context starts
+  // before it), from the scan over the tile sums
+  if (tid == 0) {
+    const TileCarry c = a.carry[tile];
+    s_sin = c.s_in;
+    s_hpre = c.hpre;
+    s_nbpre_lo = (uint32_t)c.nbpre;
+    s_nbpre_hi = (uint32_t)(c.nbpre >> 32);
   }
   __syncthreads();
 
@@ -481,56 +341,52 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
     if (need) atomicOr(&s_need, need);
   }
 
-  // ---- depths (before: sb, after: sa), leaves x + 1 and the lower tree levels
-  uint32_t sb[IT], sa[IT], xp[IT];
-  uint32_t cur = (uint32_t)apply(tfn, (int64_t)s_in);
+  // ---- depths before each record (sb); leaves x + 1 and the lower tree
+  // levels.  The depth after a record is sb + 1 (BEGIN), sb - 1 (END with
+  // sb > 0) or 0 (orphan END).
+  uint32_t sb[IT];
   uint32_t lo = 0xFFFFFFFFu, maxlvl = 0, norph = 0;
-  if (tid == 0 && !first_is_head) lo = s_in;
-#pragma unroll
-  for (int i = 0; i < IT; ++i) {
-    const uint32_t p = p0 + i;
-    sb[i] = 0;
-    sa[i] = 0;
-    xp[i] = 0xFFFFFFFFu;
-    if ((fv >> i) & 1u) {
-      const bool head = (fh >> i) & 1u;
-      const bool isb = (fb >> i) & 1u;
-      const uint32_t before = head ? 0u : cur;
-      uint32_t after;
-      if (isb) {
-        after = before + 1;
-        maxlvl = before > maxlvl ? before : maxlvl;
-      } else if (before == 0) {
-        after = 0;  // orphan END
-        norph++;
-        atomicAdd((unsigned long long*)&a.rstats[(uint64_t)reg[i] * ARGUS_RS_WIDTH + ARGUS_RS_ORPHAN_END], 1ull);
-      } else {
-        after = before - 1;
-      }
-      sb[i] = before;
-      sa[i] = after;
-      xp[i] = head ? 0u : before + 1;  // x + 1, so that a context start is 0
-      if (p < first) lo = after < lo ? after : lo;
-      cur = after;
-      if (p + 1 == cnt) s_sout = after;
-    }
-  }
-  // local BEGIN ranks
-  uint32_t lbr[IT];
   {
-    uint32_t r = tnb;
+    uint32_t cur = (uint32_t)apply(tfn, (int64_t)s_in);
+    if (tid == 0 && !first_is_head) lo = s_in;
+    uint32_t xp[IT];
 #pragma unroll
     for (int i = 0; i < IT; ++i) {
-      lbr[i] = r;
-      r += (fb >> i) & 1u;
+      const uint32_t p = p0 + i;
+      sb[i] = 0;
+      xp[i] = 0xFFFFFFFFu;
+      if ((fv >> i) & 1u) {
+        const bool head = (fh >> i) & 1u;
+        const bool isb = (fb >> i) & 1u;
+        const uint32_t before = head ? 0u : cur;
+        uint32_t after;
+        if (isb) {
+          after = before + 1;
+          maxlvl = before > maxlvl ? before : maxlvl;
+        } else if (before == 0) {
+          after = 0;  // orphan END
+          norph++;
+          atomicAdd((unsigned long long*)&a.rstats[(uint64_t)reg[i] * ARGUS_RS_WIDTH + ARGUS_RS_ORPHAN_END], 1ull);
+        } else {
+          after = before - 1;
+        }
+        sb[i] = before;
+        xp[i] = head ? 0u : before + 1;  // x + 1, so that a context start is 0
+        if (p < first) lo = after < lo ? after : lo;
+        cur = after;
+        if (p + 1 == cnt) s_sout = after;
+      }
     }
-  }
-  {
     uint4* leaf4 = (uint4*)&s_leaf[p0];
+    uint32_t r = tnb;
 #pragma unroll
-    for (int q = 0; q < IT / 2; ++q)
-      leaf4[q] = make_uint4(xp[2 * q], lbr[2 * q] | (reg[2 * q] << 11), xp[2 * q + 1],
-                            lbr[2 * q + 1] | (reg[2 * q + 1] << 11));
+    for (int q = 0; q < IT / 2; ++q) {
+      const uint32_t r0 = r;
+      r += (fb >> (2 * q)) & 1u;
+      const uint32_t r1 = r;
+      r += (fb >> (2 * q + 1)) & 1u;
+      leaf4[q] = make_uint4(xp[2 * q], r0 | (reg[2 * q] << 11), xp[2 * q + 1], r1 | (reg[2 * q + 1] << 11));
+    }
     uint32_t m = xp[0];
 #pragma unroll
     for (int i = 1; i < IT; ++i) m = min(m, xp[i]);
@@ -550,10 +406,7 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   if (lo != 0xFFFFFFFFu) atomicMin(&s_lo, lo);
   if (maxlvl) atomicMax(&s_maxlvl, maxlvl);
   if (norph) atomicAdd(&s_orph, norph);
-  for (int k = tid; k < kMatchTile; k += kMatchThreads) {
-    s_cs[k] = 0;
-    s_ereg[k] = 0xFFFF;
-  }
+  for (uint32_t k = tid; k < (uint32_t)kMatchTile; k += kMatchThreads) s_ereg[k] = 0xFFFF;
   __syncthreads();
   const uint32_t lo_head = first_is_head ? 0u : s_lo;
   const uint32_t sin_eff = first_is_head ? 0u : s_in;
@@ -562,60 +415,92 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   const uint32_t lo_tail = has_head ? 0u : lo_head;
   const uint64_t pool = tile * kMatchTile;
 
-  // ---- searches.  An END at p closing level L needs the last q < p with
-  // x + 1 <= L + 1; a BEGIN at level L >= 1 needs the last q < p with
-  // x + 1 <= L (its parent).  This thread's own records are scanned in
-  // registers first; the tree is climbed from the thread's first record only
-  // when the answer lies further back.
-  uint32_t g1[8];  // level-1 siblings of this thread's chunk
-  {
-    const uint4 ga = *(const uint4*)&s_up[kU1 + (tid & ~7)];
-    const uint4 gb = *(const uint4*)&s_up[kU1 + (tid & ~7) + 4];
-    g1[0] = ga.x; g1[1] = ga.y; g1[2] = ga.z; g1[3] = ga.w;
-    g1[4] = gb.x; g1[5] = gb.y; g1[6] = gb.z; g1[7] = gb.w;
+  // ---- searches.  An END with depth sb before it closes level sb - 1: its
+  // BEGIN is the last q < p with x + 1 <= sb; a BEGIN at level sb >= 1 has
+  // as parent the last q < p with x + 1 <= sb.  This thread's own records
+  // are scanned in registers; the others are queued per wave and answered
+  // on the tree by all lanes of the wave together.
+  uint32_t hit[IT];   // rank | region << 11 of the answer, or kNoHit
+  uint32_t qmask = 0; // bit i: record i asks a question
+  uint32_t pend = 0;  // bit i: answered by the tree
+#pragma unroll
+  for (int i = 0; i < IT; ++i) {
+    hit[i] = kNoHit;
+    const bool headi = (fh >> i) & 1u;
+    if (!((fv >> i) & 1u) || sb[i] == 0) continue;  // top-level BEGIN or orphan END
+    qmask |= 1u << i;
+    const uint32_t v = sb[i];
+    int qi = -1;
+#pragma unroll
+    for (int j = i - 1; j >= 0; --j) {
+      const uint32_t xj = ((fh >> j) & 1u) ? 0u : sb[j] + 1;
+      if (qi < 0 && xj <= v) qi = j;
+    }
+    (void)headi;
+    if (qi >= 0)
+      hit[i] = s_leaf[p0 + qi].y;
+    else
+      pend |= 1u << i;
   }
-  uint32_t par[IT], code[IT];
+  {
+    uint32_t* q = (uint32_t*)(s_tend + w * (kQueueCap / 2));  // kQueueCap u32 entries
+    const uint32_t np = (uint32_t)__popc(pend);
+    const uint32_t off = (uint32_t)wave_incl_scan32((int32_t)np) - np;
+    const uint32_t total = __shfl(off + np, 63);
+    // entries: the query value and the asking thread (v < 2^23 assumed by
+    // the packing; larger depths take the register path below)
+    uint32_t k = off;
+    bool big = false;
+#pragma unroll
+    for (int i = 0; i < IT; ++i) {
+      if (!((pend >> i) & 1u)) continue;
+      big |= sb[i] >= (1u << 23);
+      q[k++] = (sb[i] << 9) | (tid << 1);
+    }
+    const bool any_big = __ballot(big) != 0ull;
+    if (!any_big) {
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      for (uint32_t j = lane; j < total; j += 64) {
+        const uint32_t e = q[j];
+        q[j] = psv_hit(s_leaf, s_up, (e >> 1) & 0xFFu, e >> 9);
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      k = off;
+#pragma unroll
+      for (int i = 0; i < IT; ++i) {
+        if (!((pend >> i) & 1u)) continue;
+        hit[i] = q[k++];
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < IT; ++i)
+        if ((pend >> i) & 1u) hit[i] = psv_hit(s_leaf, s_up, tid, sb[i]);
+    }
+  }
+  __syncthreads();  // the queues are no longer needed: s_tend takes end times
+
+  // ---- what the answers mean
+  uint32_t par[IT];
+  uint32_t mend = 0;  // bit i: END matched to a BEGIN of the same region
 #pragma unroll
   for (int i = 0; i < IT; ++i) {
     par[i] = kParNone;
-    code[i] = 0;
-    if (!((fv >> i) & 1u)) continue;
+    if (!((qmask >> i) & 1u)) continue;
     const bool isb = (fb >> i) & 1u;
-    if (!isb && sb[i] == 0) continue;  // orphan END: no search
-    if (isb && sb[i] == 0) continue;   // top-level BEGIN: no parent
-    const uint32_t v = isb ? sb[i] : sa[i] + 1;
-    int qi = -1;
-#pragma unroll
-    for (int j = i - 1; j >= 0; --j)
-      if (qi < 0 && xp[j] <= v) qi = j;
-    uint32_t qrank, qreg;
-    bool found = qi >= 0;
-    if (found) {
-      // in-thread: rank and region from registers (the hit is always a BEGIN)
-      uint32_t rr = lbr[0], rg = reg[0];
-#pragma unroll
-      for (int j = 0; j < IT; ++j)
-        if (j == qi) {
-          rr = lbr[j];
-          rg = reg[j];
-        }
-      qrank = rr;
-      qreg = rg;
-    } else {
-      const uint32_t h = psv_hit(s_leaf, s_up, g1, (uint32_t)tid, v);
-      found = h != kNoHit;
-      qrank = h & 0x7FFu;
-      qreg = h >> 11;
-    }
+    const bool found = hit[i] != kNoHit;
+    const uint32_t qrank = hit[i] & 0x7FFu, qreg = hit[i] >> 11;
     if (!isb) {
       if (found) {
         s_tend[qrank] = ts[i];
         s_ereg[qrank] = (uint16_t)reg[i];
-        if (ev_on && qreg == reg[i])
-          code[i] = ev_code(cls[i], 1u);
+        if (qreg == reg[i]) mend |= 1u << i;
       } else {
         // pops a level that was open when the tile started
-        const uint32_t L = sa[i];
+        const uint32_t L = sb[i] - 1;
         const uint32_t idx = L - lo_head;
         if (L >= lo_head && idx < (uint32_t)kMatchTile) {
           a.pop_ts[pool + idx] = ts[i];
@@ -629,56 +514,71 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
       par[i] = found ? qrank : kParOut;
     }
   }
-  __syncthreads();
-  for (int k = tid; k < kMatchTile; k += kMatchThreads) s_oc[k] = 0;
+  // child sums of enclosing instances beyond the LDS ones start at zero
+  const uint32_t n_op = (sin_eff > op_lo) ? ((sin_eff - op_lo) < (uint32_t)kMatchTile ? sin_eff - op_lo : (uint32_t)kMatchTile) : 0u;
+  for (uint32_t k = kOcCap + tid; k < n_op; k += kMatchThreads) a.op_sum[pool + k] = 0;
+  __syncthreads();  // the tree is no longer needed: s_leaf takes child sums
+  for (uint32_t k = tid; k < (uint32_t)kMatchTile; k += kMatchThreads) s_cs[k] = 0;
+  for (uint32_t k = tid; k < kOcCap; k += kMatchThreads) s_oc[k] = 0;
+  if (n_op > kOcCap) __threadfence_block();
   __syncthreads();
 
   // ---- instances and child sums
+  uint32_t mbeg = 0;  // bit i: BEGIN matched to an END of the same region
+  {
+    uint32_t r = tnb;
 #pragma unroll
-  for (int i = 0; i < IT; ++i) {
-    const uint32_t p = p0 + i;
-    if (!((fv >> i) & 1u) || !((fb >> i) & 1u)) continue;
-    const uint32_t k = lbr[i];
-    const uint64_t id = nbpre + k;
-    const uint32_t L = sb[i];
-    uint32_t ereg = s_ereg[k];
-    uint64_t t_end = kU64Max;
-    if (ereg != kNoEnd) {
-      t_end = s_tend[k];
-      if (ev_on && ereg == reg[i]) code[i] = ev_code(cls[i], 0u);
-      const uint64_t incl = t_end - ts[i];
-      if (par[i] == kParOut) {
-        const uint32_t oi = (L - 1) - op_lo;
-        if (L >= 1 + op_lo && oi < (uint32_t)kMatchTile)
-          atomicAdd((unsigned long long*)&s_oc[oi], (unsigned long long)incl);
-        else
+    for (int i = 0; i < IT; ++i) {
+      const uint32_t p = p0 + i;
+      if (!((fv >> i) & 1u) || !((fb >> i) & 1u)) continue;
+      const uint32_t k = r++;
+      const uint64_t id = nbpre + k;
+      const uint32_t L = sb[i];
+      uint32_t ereg = s_ereg[k];
+      uint64_t t_end = kU64Max;
+      if (ereg != kNoEnd) {
+        t_end = s_tend[k];
+        if (ereg == reg[i]) mbeg |= 1u << i;
+        const uint64_t incl = t_end - ts[i];
+        if (par[i] == kParOut) {
+          const uint32_t oi = (L - 1) - op_lo;
+          if (L >= 1 + op_lo && oi < (uint32_t)kMatchTile) {
+            if (oi < kOcCap)
+              atomicAdd((unsigned long long*)&s_oc[oi], (unsigned long long)incl);
+            else
+              atomicAdd((unsigned long long*)&a.op_sum[pool + oi], (unsigned long long)incl);
+          } else {
+            flag_internal_error(a.counters, 16);
+          }
+        } else if (par[i] != kParNone) {
+          atomicAdd((unsigned long long*)&s_cs[par[i]], (unsigned long long)incl);
+        }
+      } else if (lastp1 <= p + 1) {
+        // still open when the tile ends, in a context that may continue
+        if (L >= lo_tail && L - lo_tail < (uint32_t)kMatchTile) {
+          a.pushes[pool + (L - lo_tail)] = (uint32_t)id;
+          if (ev_on) a.push_pos[pool + (L - lo_tail)] = (uint32_t)p + (uint32_t)base;
+        } else
           flag_internal_error(a.counters, 16);
-      } else if (par[i] != kParNone) {
-        atomicAdd((unsigned long long*)&s_cs[par[i]], (unsigned long long)incl);
       }
-    } else if (lastp1 <= p + 1) {
-      // still open when the tile ends, in a context that may continue
-      if (L >= lo_tail && L - lo_tail < (uint32_t)kMatchTile) {
-        a.pushes[pool + (L - lo_tail)] = (uint32_t)id;
-        if (ev_on) a.push_pos[pool + (L - lo_tail)] = (uint32_t)p + (uint32_t)base;
-      } else
-        flag_internal_error(a.counters, 16);
+      uint32_t pf;
+      if (par[i] == kParNone) pf = kNoParent;
+      else if (par[i] == kParOut) pf = kParentPending | (uint32_t)tile;
+      else pf = (uint32_t)(nbpre + par[i]);
+      uint4* dst = (uint4*)(a.inst + id);
+      dst[0] = make_uint4((uint32_t)ts[i], (uint32_t)(ts[i] >> 32), (uint32_t)t_end,
+                          (uint32_t)(t_end >> 32));
+      dst[1] = make_uint4(ctxr[i] + (uint32_t)ks.ctx_min, pf, L, reg[i] | (ereg << 16));
     }
-    uint32_t pf;
-    if (par[i] == kParNone) pf = kNoParent;
-    else if (par[i] == kParOut) pf = kParentPending | (uint32_t)tile;
-    else pf = (uint32_t)(nbpre + par[i]);
-    uint4* dst = (uint4*)(a.inst + id);
-    dst[0] = make_uint4((uint32_t)ts[i], (uint32_t)(ts[i] >> 32), (uint32_t)t_end,
-                        (uint32_t)(t_end >> 32));
-    dst[1] = make_uint4(ctxr[i] + (uint32_t)ks.ctx_min, pf, L, reg[i] | (ereg << 16));
   }
   if (ev_on) {
     uint64_t e[IT];
 #pragma unroll
     for (int i = 0; i < IT; ++i) {
       const uint64_t g = group_of(ctxr[i] + (uint32_t)ks.ctx_min);
-      e[i] = (es < 64 ? (g << es) : 0ull) | ((ts[i] - ks.ts_min) << kEvCodeBits) | code[i];
+      const uint32_t c = (clsp[i >> 2] >> (8 * (i & 3))) & 0xFFu;
+      const uint32_t ev = (((mend | mbeg) >> i) & 1u) && c < a.K ? 1u + 2u * c + (((fb >> i) & 1u) ^ 1u) : 0u;
+      e[i] = (es < 64 ? (g << es) : 0ull) | ((ts[i] - ks.ts_min) << kEvCodeBits) | ev;
     }
     if (p0 + IT <= cnt) {
       uint4* e4 = (uint4*)(evo + base + p0);
@@ -697,8 +597,8 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   // ---- per-tile outputs
   const uint32_t tile_nb = (s_wnb[0] + s_wnb[1] + s_wnb[2] + s_wnb[3]) & 0xFFFFu;
   for (uint32_t k = tid; k < tile_nb; k += kMatchThreads) a.child_sum[nbpre + k] = s_cs[k];
-  const uint32_t n_op = (sin_eff > op_lo) ? ((sin_eff - op_lo) < (uint32_t)kMatchTile ? sin_eff - op_lo : (uint32_t)kMatchTile) : 0u;
-  for (uint32_t k = tid; k < n_op; k += kMatchThreads) a.op_sum[pool + k] = s_oc[k];
+  const uint32_t n_oc = n_op < kOcCap ? n_op : kOcCap;
+  for (uint32_t k = tid; k < n_oc; k += kMatchThreads) a.op_sum[pool + k] = s_oc[k];
   if (tid == 0) {
     const uint32_t s_out = cnt ? s_sout : 0u;
     TileDesc d;
@@ -752,7 +652,7 @@ hipError_t launch_match(const RunArgs& a, hipStream_t s) {
   m.inst = a.w.inst;
   m.child_sum = a.w.child_sum;
   m.tiles = a.w.tiles;
-  m.mlb = a.w.mlb;
+  m.carry = a.w.carry;
   m.pop_ts = a.w.pop_ts;
   m.pop_reg = a.w.pop_reg;
   m.pushes = a.w.pushes;
