@@ -48,7 +48,7 @@ size_t align_up(size_t v) { return (v + kAlign - 1) & ~(kAlign - 1); }
 // Workspace layout for n records.  Offsets only; the base is added in run.
 struct Layout {
   size_t plan, rec_hist, rec_off, ev_hist, ev_off, tile_ctr;
-  size_t key[2], pay[2], ctxw[2], lb[2], tsum, carry, slb, mslb, tiles, tree;
+  size_t key[2], pay[2], ctxw[2], lb[2], tsum, carry, bsum, slb, mslb, tiles, tree;
   size_t pop_ts, pop_reg, pushes, op_parent, op_sum;
   size_t inst, child_sum, hist_key, ov_mask, ov_q;
   size_t push_pos, pop_pos, ctx_list, ctx_seg, seg_start, seg_split, seg_tile0, part;
@@ -82,6 +82,7 @@ Layout make_layout(const argus_attr_config& c, uint64_t n, bool own_instances) {
   L.match_tiles = ceil_div(nn, kMatchTile);
   L.tsum = take(sizeof(uint64_t) * L.match_tiles);
   L.carry = take(sizeof(TileCarry) * L.match_tiles);
+  L.bsum = take(sizeof(BlockSum) * kMaxScanBlocks);
   L.slb = take(sizeof(uint64_t) * 8 * ceil_div(nn, kSweepTile));
   L.tiles = take(sizeof(TileDesc) * L.match_tiles);
   uint64_t leaves = 1;
@@ -270,6 +271,7 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
   }
   w.tsum = (uint64_t*)(base + L.tsum);
   w.carry = (TileCarry*)(base + L.carry);
+  w.bsum = (BlockSum*)(base + L.bsum);
   w.slb = (uint64_t*)(base + L.slb);
   w.mslb = (uint64_t*)(base + L.mslb);
   w.tiles = (TileDesc*)(base + L.tiles);

@@ -146,6 +146,23 @@ struct TileDesc {
   uint32_t pad;
 };
 
+// A prefix of the records maps the depth before it to the depth after it:
+// s -> max(c, s + a), or the constant c once a context starts inside.  The
+// identity is {0, 0, 0} on depths >= 0.  All fields fit 32 bits (n < 2^31).
+struct Fn {
+  uint32_t reset;  // 1: output is the constant c (a context starts inside)
+  int32_t a;
+  int32_t c;       // else output is max(c, s + a)
+};
+
+// A run of matching tiles composed (one per block of the tile-sum pass).
+struct BlockSum {
+  Fn f;
+  uint32_t nb;  // BEGINs
+  uint32_t nh;  // context starts
+};
+constexpr uint32_t kMaxScanBlocks = 2048;  // blocks of the tile-sum pass
+
 // Entering values of one matching tile, from a scan over the tile sums.
 struct TileCarry {
   uint32_t s_in;   // depth before the tile's first record
@@ -167,6 +184,7 @@ struct Work {
   uint64_t* lb[2];      // radix look-back status, [tiles][256]
   uint64_t* tsum;       // matching tile sums, [tiles]
   TileCarry* carry;     // matching tile entering values, [tiles]
+  BlockSum* bsum;       // [kMaxScanBlocks]
   uint64_t* slb;        // sweep look-back status, [tiles][8]
   uint64_t* mslb;       // last merge round tile records, [tiles_cap][2 + 2K + K(K + 1)]
   TileDesc* tiles;      // [match tiles]
@@ -329,14 +347,6 @@ ARGUS_DEV int32_t wave_incl_scan32(int32_t v) {
 }
 
 // ------------------------------------------------- clamped depth maps
-// A prefix of the records maps the depth before it to the depth after it:
-// s -> max(c, s + a), or the constant c once a context starts inside.  The
-// identity is {0, 0, 0} on depths >= 0.  All fields fit 32 bits (n < 2^31).
-struct Fn {
-  uint32_t reset;  // 1: output is the constant c (a context starts inside)
-  int32_t a;
-  int32_t c;       // else output is max(c, s + a)
-};
 
 ARGUS_DEV Fn fn_id() { return Fn{0u, 0, 0}; }
 // g after f

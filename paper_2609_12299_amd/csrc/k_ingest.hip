@@ -406,13 +406,17 @@ hipError_t launch_plan2(const RunArgs& a, hipStream_t s) {
 
 // ----------------------------------------------------------- sortedness
 
+// Grid of k_tsum (and of the tile scan, which follows its runs of tiles).
+static uint32_t tsum_blocks(const RunArgs& a);
+
 struct TsumArgs {
   DevPlan* plan;
   const uint64_t* key[2];
   const uint32_t* pay[2];
   const uint32_t* ctxw[2];
-  uint64_t* tsum;  // [match tiles]
-  uint32_t mode;   // 0: after the context passes (check the order too); 1: after the full sort
+  uint64_t* tsum;     // [match tiles]
+  BlockSum* bsum;     // [grid]: each block's run of tiles composed
+  uint32_t mode;      // 0: after the context passes (check the order too); 1: after the full sort
 };
 
 // Per matching tile (2048 consecutive sorted records): the map from the depth
@@ -420,7 +424,8 @@ struct TsumArgs {
 // (k_mscan turns these into each tile's entering values, so that k_match
 // needs no look-back).  In mode 0 it also checks that the context-only sort
 // left (ctx, ts) non-decreasing; if not (some context was out of time order
-// in the input) the full sort runs and mode 1 redoes the sums.
+// in the input) the full sort runs and mode 1 redoes the sums.  Block b takes
+// the b-th contiguous run of tiles and also stores the run composed.
 __global__ __launch_bounds__(256) void k_tsum(TsumArgs a) {
   DevPlan* p = a.plan;
   if (a.mode == 0 && p->force_full) {
@@ -444,7 +449,11 @@ __global__ __launch_bounds__(256) void k_tsum(TsumArgs a) {
     return wide ? cw[i] : (ks.ts_bits >= 64 ? 0u : (uint32_t)(k >> ks.ts_bits));
   };
   bool bad = false;
-  for (uint64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+  const uint64_t per = ceil_div(tiles, gridDim.x);
+  const uint64_t t0 = (uint64_t)blockIdx.x * per, t1 = t0 + per < tiles ? t0 + per : tiles;
+  Fn run = fn_id();
+  uint32_t run_nb = 0, run_nh = 0;
+  for (uint64_t tile = t0; tile < t1; ++tile) {
     const uint64_t base = tile * kMatchTile;
     const uint32_t cnt = nv - base < (uint64_t)kMatchTile ? (uint32_t)(nv - base) : (uint32_t)kMatchTile;
     uint64_t k[kMatchItems];
@@ -522,10 +531,20 @@ __global__ __launch_bounds__(256) void k_tsum(TsumArgs a) {
         nball += s_wnb[q];
       }
       a.tsum[tile] = pack_tile_sum(all, nball);
+      run = compose(run, all);
+      run_nb += nball & 0xFFFFu;
+      run_nh += nball >> 16;
     }
     __syncthreads();
   }
+  if (tid == 0) a.bsum[blockIdx.x] = BlockSum{run, run_nb, run_nh};
   if (a.mode == 0 && __syncthreads_or(bad) && threadIdx.x == 0) p->unsorted = 1;
+}
+
+static uint32_t tsum_blocks(const RunArgs& a) {
+  uint64_t blocks = a.w.match_tiles;
+  if (blocks > kMaxScanBlocks) blocks = kMaxScanBlocks;
+  return blocks < 1 ? 1u : (uint32_t)blocks;
 }
 
 hipError_t launch_tsum(const RunArgs& a, int mode, hipStream_t s) {
@@ -537,39 +556,36 @@ hipError_t launch_tsum(const RunArgs& a, int mode, hipStream_t s) {
     ta.ctxw[b] = a.w.ctxw[b];
   }
   ta.tsum = a.w.tsum;
+  ta.bsum = a.w.bsum;
   ta.mode = (uint32_t)mode;
-  uint64_t blocks = a.w.match_tiles;
-  const uint64_t resident = persistent_blocks((const void*)k_tsum, 256);
-  if (blocks > resident) blocks = resident;
-  if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(k_tsum, dim3((uint32_t)blocks), dim3(256), 0, s, ta);
+  hipLaunchKernelGGL(k_tsum, dim3(tsum_blocks(a)), dim3(256), 0, s, ta);
   return hipGetLastError();
 }
 
 struct MscanArgs {
   const DevPlan* plan;
   const uint64_t* tsum;
+  BlockSum* bsum;  // in: each k_tsum block's run; out (k_mscan_top): what comes before it
   TileCarry* carry;
+  uint32_t nblk;   // k_tsum blocks
 };
 
-// Entering values of every matching tile: an exclusive scan of the tile sums
-// (one block; each thread composes a contiguous run of tiles).
-__global__ __launch_bounds__(1024) void k_mscan(MscanArgs a) {
+// Exclusive scan of the k_tsum block sums (one block; each thread composes
+// a contiguous run of them).  Overwrites each block sum with the composition
+// of everything before that block.
+__global__ __launch_bounds__(1024) void k_mscan_top(MscanArgs a) {
   __shared__ Fn s_wfn[16];
   __shared__ uint32_t s_wnb[16], s_wnh[16];
-  const uint64_t tiles = a.plan->match_tiles;
   const uint32_t t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const uint64_t per = ceil_div(tiles, 1024);
-  const uint64_t k0 = (uint64_t)t * per, k1 = k0 + per < tiles ? k0 + per : tiles;
+  const uint32_t per = (a.nblk + 1023) / 1024;
+  const uint32_t k0 = t * per, k1 = k0 + per < a.nblk ? k0 + per : a.nblk;
   Fn f = fn_id();
   uint32_t nb = 0, nh = 0;
-  for (uint64_t k = k0; k < k1; ++k) {
-    Fn g;
-    uint32_t nbh;
-    unpack_tile_sum(a.tsum[k], &g, &nbh);
-    f = compose(f, g);
-    nb += nbh & 0xFFFFu;
-    nh += nbh >> 16;
+  for (uint32_t k = k0; k < k1; ++k) {
+    const BlockSum b = a.bsum[k];
+    f = compose(f, b.f);
+    nb += b.nb;
+    nh += b.nh;
   }
   const Fn x = wave_scan_fn(f);
   const uint32_t xb = (uint32_t)wave_incl_scan32((int32_t)nb);
@@ -583,31 +599,86 @@ __global__ __launch_bounds__(1024) void k_mscan(MscanArgs a) {
   if (lane == 0) ex = fn_id();
   __syncthreads();
   Fn pre = fn_id();
-  uint64_t pb = xb - nb, ph = xh - nh;
+  uint32_t pb = xb - nb, ph = xh - nh;
   for (uint32_t q = 0; q < w; ++q) {
     pre = compose(pre, s_wfn[q]);
     pb += s_wnb[q];
     ph += s_wnh[q];
   }
-  f = compose(pre, ex);  // map from depth 0 before the data to the depth before tile k0
-  for (uint64_t k = k0; k < k1; ++k) {
-    Fn g;
-    uint32_t nbh;
-    unpack_tile_sum(a.tsum[k], &g, &nbh);
-    TileCarry c;
-    c.s_in = (uint32_t)apply(f, 0);
-    c.hpre = (uint32_t)ph;
-    c.nbpre = pb;
-    a.carry[k] = c;
-    f = compose(f, g);
-    pb += nbh & 0xFFFFu;
-    ph += nbh >> 16;
+  f = compose(pre, ex);
+  for (uint32_t k = k0; k < k1; ++k) {
+    const BlockSum b = a.bsum[k];
+    a.bsum[k] = BlockSum{f, pb, ph};
+    f = compose(f, b.f);
+    pb += b.nb;
+    ph += b.nh;
+  }
+}
+
+// Entering values of every matching tile: block b of k_tsum's grid scans its
+// run of tile sums (256 at a time) after what comes before the run.
+__global__ __launch_bounds__(256) void k_mscan_tiles(MscanArgs a) {
+  __shared__ Fn s_wfn[4];
+  __shared__ uint32_t s_wnb[4], s_wnh[4];
+  const uint64_t tiles = a.plan->match_tiles;
+  const uint64_t per = ceil_div(tiles, gridDim.x);
+  const uint64_t t0 = (uint64_t)blockIdx.x * per, t1 = t0 + per < tiles ? t0 + per : tiles;
+  const uint32_t t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const BlockSum b0 = a.bsum[blockIdx.x];
+  Fn run = b0.f;
+  uint64_t run_nb = b0.nb, run_nh = b0.nh;
+  for (uint64_t c0 = t0; c0 < t1; c0 += 256) {
+    const uint64_t k = c0 + t;
+    Fn g = fn_id();
+    uint32_t nbh = 0;
+    if (k < t1) unpack_tile_sum(a.tsum[k], &g, &nbh);
+    const uint32_t nb = nbh & 0xFFFFu, nh = nbh >> 16;
+    const Fn x = wave_scan_fn(g);
+    const uint32_t xb = (uint32_t)wave_incl_scan32((int32_t)nb);
+    const uint32_t xh = (uint32_t)wave_incl_scan32((int32_t)nh);
+    if (lane == 63) {
+      s_wfn[w] = x;
+      s_wnb[w] = xb;
+      s_wnh[w] = xh;
+    }
+    Fn ex = Fn{(uint32_t)__shfl_up((int)x.reset, 1), __shfl_up(x.a, 1), __shfl_up(x.c, 1)};
+    if (lane == 0) ex = fn_id();
+    __syncthreads();
+    Fn pre = run, all = run;
+    uint64_t pb = run_nb, ph = run_nh, ab = run_nb, ah = run_nh;
+    for (uint32_t q = 0; q < 4; ++q) {
+      if (q < w) {
+        pre = compose(pre, s_wfn[q]);
+        pb += s_wnb[q];
+        ph += s_wnh[q];
+      }
+      all = compose(all, s_wfn[q]);
+      ab += s_wnb[q];
+      ah += s_wnh[q];
+    }
+    pre = compose(pre, ex);
+    pb += xb - nb;
+    ph += xh - nh;
+    if (k < t1) {
+      TileCarry c;
+      c.s_in = (uint32_t)apply(pre, 0);
+      c.hpre = (uint32_t)ph;
+      c.nbpre = pb;
+      a.carry[k] = c;
+    }
+    run = all;
+    run_nb = ab;
+    run_nh = ah;
+    __syncthreads();
   }
 }
 
 hipError_t launch_mscan(const RunArgs& a, hipStream_t s) {
-  MscanArgs m{a.w.plan, a.w.tsum, a.w.carry};
-  hipLaunchKernelGGL(k_mscan, dim3(1), dim3(1024), 0, s, m);
+  MscanArgs m{a.w.plan, a.w.tsum, a.w.bsum, a.w.carry, tsum_blocks(a)};
+  hipLaunchKernelGGL(k_mscan_top, dim3(1), dim3(1024), 0, s, m);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_mscan_tiles, dim3(m.nblk), dim3(256), 0, s, m);
   return hipGetLastError();
 }
 

@@ -105,7 +105,7 @@ struct MatchArgs {
   // overlap events in sorted-record order (merge path)
   uint64_t* ev[2];
   const uint8_t* region_class;
-  uint32_t K, G, shift;
+  uint32_t K, G, shift, R;
   uint32_t* push_pos;
   uint32_t* pop_pos;
   uint2* ctx_list;
@@ -118,13 +118,14 @@ constexpr uint32_t kParOut = 0xFFFFFFFEu;
 // LDS for the nearest kOcCap levels; deeper ones go to global memory.
 constexpr uint32_t kOcCap = 512;
 constexpr uint32_t kQueueCap = kMatchTile / 4;  // queued searches per wave
+constexpr uint32_t kClsLds = 4096;              // region-class tables up to this size live in LDS
 
 __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   const DevPlan* P = a.plan;
   const uint32_t tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   constexpr int IT = kMatchItems;
 
-  __shared__ uint32_t s_tile;
+  __shared__ uint8_t s_cls[kClsLds];  // region classes when R <= kClsLds
   // tree leaves during the searches; then the child sums of local BEGINs
   __shared__ uint2 s_leaf[kMatchTile];
   __shared__ uint32_t s_up[kUpSize];  // upper tree levels
@@ -160,9 +161,62 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
     return a.shift >= 32 ? 0u : (raw_ctx >> a.shift);
   };
 
-  for (;;) {
+  // region classes in LDS when the table is small
+  const bool cls_lds = ev_on && a.R <= kClsLds;
+  if (cls_lds)
+    for (uint32_t r = tid; r < a.R; r += kMatchThreads) s_cls[r] = a.region_class[r];
+
+  // Tiles are independent: tile = block + k * grid, with the next tile's
+  // records loaded while this one is processed.
+  const uint64_t n_tiles = P->match_tiles;
+  const uint32_t p0 = tid * IT;
+  uint64_t tile = blockIdx.x;
+  if (tile >= n_tiles) return;
+  uint64_t nk[IT];
+  uint32_t np[IT], nc[IT];
+  auto issue = [&](uint64_t t) {
+    const uint64_t b = t * kMatchTile;
+    const uint32_t c = nv - b < (uint64_t)kMatchTile ? (uint32_t)(nv - b) : (uint32_t)kMatchTile;
+    if (p0 + IT <= c) {
+      const uint4* k4 = (const uint4*)(gk + b + p0);
+#pragma unroll
+      for (int q = 0; q < IT / 2; ++q) {
+        const uint4 v = k4[q];
+        nk[2 * q] = (uint64_t)v.x | ((uint64_t)v.y << 32);
+        nk[2 * q + 1] = (uint64_t)v.z | ((uint64_t)v.w << 32);
+      }
+      const uint4* p4 = (const uint4*)(gp + b + p0);
+#pragma unroll
+      for (int q = 0; q < IT / 4; ++q) {
+        const uint4 v = p4[q];
+        np[4 * q] = v.x;
+        np[4 * q + 1] = v.y;
+        np[4 * q + 2] = v.z;
+        np[4 * q + 3] = v.w;
+      }
+      if (wide) {
+        const uint4* c4 = (const uint4*)(gc + b + p0);
+#pragma unroll
+        for (int q = 0; q < IT / 4; ++q) {
+          const uint4 v = c4[q];
+          nc[4 * q] = v.x;
+          nc[4 * q + 1] = v.y;
+          nc[4 * q + 2] = v.z;
+          nc[4 * q + 3] = v.w;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < IT; ++i) {
+        const uint32_t q = p0 + i;
+        nk[i] = q < c ? gk[b + q] : 0;
+        np[i] = q < c ? gp[b + q] : 0;
+        if (wide) nc[i] = q < c ? gc[b + q] : 0;
+      }
+    }
+  };
+  issue(tile);
   if (tid == 0) {
-    s_tile = atomicAdd(&a.tile_ctr[kCtrMatch], 1u);
     s_first = kMatchTile;
     s_lastp1 = 0;
     s_heads = 0;
@@ -172,56 +226,26 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
     s_need = 0;
   }
   __syncthreads();
-  const uint64_t tile = s_tile;
-  if (tile >= P->match_tiles) break;
+
+  for (;;) {
   const uint64_t base = tile * kMatchTile;
   const uint32_t cnt = nv - base < (uint64_t)kMatchTile ? (uint32_t)(nv - base) : (uint32_t)kMatchTile;
-  const uint32_t p0 = tid * IT;
+  const uint64_t next = tile + gridDim.x;
 
-  // ---- blocked load: this thread's 8 consecutive records, 16-byte loads
+  // ---- this thread's 8 consecutive records (loaded one tile ahead)
   uint64_t ts[IT];
   uint32_t ctxr[IT], reg[IT];
   uint32_t fb = 0, fv = 0;  // bit i: BEGIN / valid
   {
     uint64_t key[IT];
     uint32_t pay[IT];
-    if (p0 + IT <= cnt) {
-      const uint4* k4 = (const uint4*)(gk + base + p0);
 #pragma unroll
-      for (int q = 0; q < IT / 2; ++q) {
-        const uint4 v = k4[q];
-        key[2 * q] = (uint64_t)v.x | ((uint64_t)v.y << 32);
-        key[2 * q + 1] = (uint64_t)v.z | ((uint64_t)v.w << 32);
-      }
-      const uint4* p4 = (const uint4*)(gp + base + p0);
-#pragma unroll
-      for (int q = 0; q < IT / 4; ++q) {
-        const uint4 v = p4[q];
-        pay[4 * q] = v.x;
-        pay[4 * q + 1] = v.y;
-        pay[4 * q + 2] = v.z;
-        pay[4 * q + 3] = v.w;
-      }
-      if (wide) {
-        const uint4* c4 = (const uint4*)(gc + base + p0);
-#pragma unroll
-        for (int q = 0; q < IT / 4; ++q) {
-          const uint4 v = c4[q];
-          ctxr[4 * q] = v.x;
-          ctxr[4 * q + 1] = v.y;
-          ctxr[4 * q + 2] = v.z;
-          ctxr[4 * q + 3] = v.w;
-        }
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < IT; ++i) {
-        const uint32_t p = p0 + i;
-        key[i] = p < cnt ? gk[base + p] : 0;
-        pay[i] = p < cnt ? gp[base + p] : 0;
-        if (wide) ctxr[i] = p < cnt ? gc[base + p] : 0;
-      }
+    for (int i = 0; i < IT; ++i) {
+      key[i] = nk[i];
+      pay[i] = np[i];
+      ctxr[i] = nc[i];
     }
+    if (next < n_tiles) issue(next);
 #pragma unroll
     for (int i = 0; i < IT; ++i) {
       if (!wide) ctxr[i] = ctx_of_key(key[i]);
@@ -240,7 +264,8 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
 #pragma unroll
     for (int i = 0; i < IT; ++i) {
       uint32_t c = 0xFFu;
-      if ((fv >> i) & 1u && group_of(ctxr[i] + (uint32_t)ks.ctx_min) < a.G) c = a.region_class[reg[i]];
+      if ((fv >> i) & 1u && group_of(ctxr[i] + (uint32_t)ks.ctx_min) < a.G)
+        c = cls_lds ? (uint32_t)s_cls[reg[i]] : (uint32_t)a.region_class[reg[i]];
       clsp[i >> 2] = (clsp[i >> 2] & ~(0xFFu << (8 * (i & 3)))) | (c << (8 * (i & 3)));
     }
   }
@@ -626,8 +651,18 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
     if (s_heads) atomicAdd(&c[ARGUS_C_N_CTX], (unsigned long long)s_heads);
     if (s_maxlvl) atomicMax(&c[ARGUS_C_MAX_LEVEL], (unsigned long long)s_maxlvl);
     if (s_orph) atomicAdd(&c[ARGUS_C_N_ORPHAN_END], (unsigned long long)s_orph);
+    // every thread has read this tile's scalars: reset them for the next
+    s_first = kMatchTile;
+    s_lastp1 = 0;
+    s_heads = 0;
+    s_lo = 0xFFFFFFFFu;
+    s_maxlvl = 0;
+    s_orph = 0;
+    s_need = 0;
   }
   __syncthreads();
+  if (next >= n_tiles) break;
+  tile = next;
   }  // tiles
 }
 
@@ -640,6 +675,7 @@ hipError_t launch_match(const RunArgs& a, hipStream_t s) {
   m.K = a.K;
   m.G = a.G;
   m.shift = a.shift;
+  m.R = a.R;
   m.push_pos = a.w.push_pos;
   m.pop_pos = a.w.pop_pos;
   m.ctx_list = a.w.ctx_list;
