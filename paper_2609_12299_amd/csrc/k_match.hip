@@ -174,8 +174,10 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   if (tile >= n_tiles) return;
   uint64_t nk[IT];
   uint32_t np[IT], nc[IT];
+  uint64_t nprev = 0;  // (lane 0) key or context word of the record before the thread's first
   auto issue = [&](uint64_t t) {
     const uint64_t b = t * kMatchTile;
+    if (lane == 0 && b + p0 > 0 && b + p0 <= nv) nprev = wide ? gc[b + p0 - 1] : gk[b + p0 - 1];
     const uint32_t c = nv - b < (uint64_t)kMatchTile ? (uint32_t)(nv - b) : (uint32_t)kMatchTile;
     if (p0 + IT <= c) {
       const uint4* k4 = (const uint4*)(gk + b + p0);
@@ -236,6 +238,7 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   uint64_t ts[IT];
   uint32_t ctxr[IT], reg[IT];
   uint32_t fb = 0, fv = 0;  // bit i: BEGIN / valid
+  uint64_t prev_raw;
   {
     uint64_t key[IT];
     uint32_t pay[IT];
@@ -245,6 +248,7 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
       pay[i] = np[i];
       ctxr[i] = nc[i];
     }
+    prev_raw = nprev;
     if (next < n_tiles) issue(next);
 #pragma unroll
     for (int i = 0; i < IT; ++i) {
@@ -276,7 +280,7 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   if (lane == 0) {
     const uint64_t pp = base + p0;
     has_prev0 = pp > 0;
-    prev0 = pp > 0 ? (wide ? gc[pp - 1] : ctx_of_key(gk[pp - 1])) : 0u;
+    prev0 = pp > 0 ? (wide ? (uint32_t)prev_raw : ctx_of_key(prev_raw)) : 0u;
   }
 
   uint32_t fh = 0;  // bit i: context start
@@ -487,9 +491,18 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      for (uint32_t j = lane; j < total; j += 64) {
-        const uint32_t e = q[j];
-        q[j] = psv_hit(s_leaf, s_up, (e >> 1) & 0xFFu, e >> 9);
+      // four queries per lane in flight, so that their dependent LDS
+      // reads overlap
+      for (uint32_t j0 = lane; j0 < total; j0 += 256) {
+        uint32_t e[4], h[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) e[u] = j0 + 64u * u < total ? q[j0 + 64u * u] : 0u;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          h[u] = j0 + 64u * u < total ? psv_hit(s_leaf, s_up, (e[u] >> 1) & 0xFFu, e[u] >> 9) : kNoHit;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (j0 + 64u * u < total) q[j0 + 64u * u] = h[u];
       }
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();

@@ -255,3 +255,62 @@ def test_without_instance_outputs(oracle_mod, tracegen_mod):
     log("[gpu] statistics only (instances in the workspace)")
     g = gpu_run(d["records"], p, instances=False)
     assert_parity(g, oracle_run(oracle_mod, d["records"], p, instances=False), instances=False)
+
+
+@pytest.mark.parametrize("depth", [700, 1500])
+def test_enclosing_levels_beyond_lds(oracle_mod, depth):
+    """A tile that starts `depth` levels deep, closes a child of an instance
+    opened in an earlier tile, and then unwinds every level: the child sums
+    of enclosing instances more than 512 levels above the tile's low point
+    take the global-memory path of the matching kernel."""
+    rows, t = [], 0
+    for k in range(depth):
+        rows.append((t, 7, k % 5, 1))
+        t += 1
+    # pairs at the top until the next record starts a matching tile
+    while len(rows) < 2048:
+        rows.append((t, 7, 1, 1))
+        rows.append((t + 3, 7, 1, 2))
+        t += 5
+    rows = rows[:2048]
+    for j in range(6):  # children of the level depth-1 instance, in the new tile
+        rows.append((t, 7, 2, 1))
+        rows.append((t + 7, 7, 2, 2))
+        t += 9
+    for k in reversed(range(depth)):
+        rows.append((t, 7, k % 5, 2))
+        t += 2
+    rec = records_from_rows(rows)
+    p = dict(num_regions=5, num_classes=2, region_class=np.array([0, 1, 0, 1, 0], np.uint8),
+             group_shift=0, num_groups=16)
+    log(f"[gpu] enclosing levels beyond LDS depth={depth}")
+    assert_parity(gpu_run(rec, p), oracle_run(oracle_mod, rec, p))
+
+
+@pytest.mark.parametrize("k", [1, 2, 3, 4, 5, 6, 7, 8])
+@pytest.mark.parametrize("span", ["narrow", "wide"])
+def test_overlap_every_class_count(oracle_mod, k, span):
+    """Class-overlap sums for every number of classes, with groups of several
+    contexts (merged runs), tiles spanning less and more than 2^32 cycles,
+    and unclassified regions."""
+    rng = np.random.default_rng(100 * k + (span == "wide"))
+    R = 12
+    cls = np.array([(r % (k + 1)) if (r % (k + 1)) < k else 0xFF for r in range(R)], np.uint8)
+    rows = []
+    gap_hi = 1 << 34 if span == "wide" else 64
+    for ctx in range(24):
+        t = int(rng.integers(0, 1 << 20))
+        stack = []
+        for _ in range(int(rng.integers(200, 900))):
+            if stack and (len(stack) > 5 or rng.random() < 0.45):
+                rows.append((t, ctx, stack.pop(), 2))
+            else:
+                r = int(rng.integers(0, R))
+                stack.append(r)
+                rows.append((t, ctx, r, 1))
+            t += int(rng.integers(0, gap_hi)) if rng.random() < 0.05 else int(rng.integers(0, 9))
+    rec = records_from_rows(rows)
+    rng.shuffle(rec)
+    p = dict(num_regions=R, num_classes=k, region_class=cls, group_shift=2, num_groups=6)
+    log(f"[gpu] overlap k={k} span={span} n={len(rec)}")
+    assert_parity(gpu_run(rec, p), oracle_run(oracle_mod, rec, p))
