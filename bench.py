@@ -53,7 +53,8 @@ def byte_model(name: str, c: dict, plan: dict, R: int, K: int, G: int, flags: in
     n, nv, nb, nev = c["n"], c["nv"], c["nb"], plan["n_ev"]
     wide = plan["rec_wide"]
     if name == "ingest":
-        return 16.0 * n
+        # records in; runs of one context out (one word per run, a count per chunk)
+        return 16.0 * n + 8.0 * plan.get("n_runs", 0) + 4.0 * (-(-n // 256))
     if name.startswith("radix_") or name.startswith("ev_radix_"):
         ev = name.startswith("ev_")
         slots = plan["ev_slots"] if ev else plan["rec_slots"]
@@ -67,12 +68,21 @@ def byte_model(name: str, c: dict, plan: dict, R: int, K: int, G: int, flags: in
             slot = idx[name[len("radix_"):]]
         if slot >= 16 or not slots[slot]["active"]:
             return 0.0
-        out_n = nev if ev else nv
+        out_n = int(slots[slot]["n_out"])  # records, events, or runs of one context
         elem = 12.0 + (4.0 if (wide and not ev) else 0.0)
         src = int(slots[slot]["src"])
         if src == 2:  # first pass: raw records / instances
             return (16.0 * n if not ev else 32.0 * nb) + elem * out_n
         return 2.0 * elem * out_n
+    runs = plan.get("runs", 0)
+    if name == "runs_base":  # chunk run counts scanned (read twice, written once)
+        return 12.0 * (-(-n // 256)) if runs else 0.0
+    if name == "runs_compact":  # raw runs and counts in; run keys, ids and lengths out
+        return (12.0 * (-(-n // 256)) + 24.0 * plan["n_runs"]) if runs else 0.0
+    if name == "runs_pos":  # run ids and lengths in (twice), positions out
+        return 20.0 * plan["n_runs"] if runs else 0.0
+    if name == "runs_scatter":  # raw records in, packed keys and payloads out
+        return (16.0 * n + 12.0 * nv) if runs else 0.0
     if name == "tile_sums":
         # sorted keys and payloads: order check and per-tile depth maps
         return (12.0 + (4.0 if wide else 0.0)) * nv

@@ -131,9 +131,14 @@ enum {
                                    when each context is already in time order
                                    in the input (results are identical; for
                                    measurement and testing) */
-  ARGUS_FORCE_EVENT_SORT = 8u   /* order the overlap events with a radix sort
+  ARGUS_FORCE_EVENT_SORT = 8u,  /* order the overlap events with a radix sort
                                    of (group, time) even where merging the
                                    per-context runs applies (results are
+                                   identical; for measurement and testing) */
+  ARGUS_FORCE_RECORD_RADIX = 16u /* sort the records by context with radix
+                                   passes over every record even where the
+                                   input holds long runs of one context, which
+                                   are otherwise sorted as runs (results are
                                    identical; for measurement and testing) */
 };
 

@@ -6,7 +6,8 @@ Cross-Layer GPU Performance Measurements around Semantic Regions"
 per-region duration statistics, class overlap and ambiguity counts, computed
 by hand-written HIP kernels for gfx950 behind a C ABI (include/argus_attr.h).
 """
-from .attr import (ABI_VERSION, COUNTER_NAMES, FORCE_EVENT_SORT, FORCE_FULL_SORT, INSTANCE_DTYPE, NUM_COUNTERS,
+from .attr import (ABI_VERSION, COUNTER_NAMES, FORCE_EVENT_SORT, FORCE_FULL_SORT, FORCE_RECORD_RADIX,
+                   INSTANCE_DTYPE, NUM_COUNTERS,
                    OUT_INSTANCE_EXCL, OUT_INSTANCES, RS_WIDTH, ArgusError, RegionAttribution,
                    argus_attr_config, argus_attr_create, argus_attr_destroy,
                    argus_attr_kernel_times, argus_attr_last_error, argus_attr_outputs,
@@ -14,7 +15,8 @@ from .attr import (ABI_VERSION, COUNTER_NAMES, FORCE_EVENT_SORT, FORCE_FULL_SORT
                    load_library, to_host)
 
 __all__ = [
-    "ABI_VERSION", "COUNTER_NAMES", "FORCE_EVENT_SORT", "FORCE_FULL_SORT", "INSTANCE_DTYPE", "NUM_COUNTERS",
+    "ABI_VERSION", "COUNTER_NAMES", "FORCE_EVENT_SORT", "FORCE_FULL_SORT", "FORCE_RECORD_RADIX",
+    "INSTANCE_DTYPE", "NUM_COUNTERS",
     "OUT_INSTANCE_EXCL", "OUT_INSTANCES", "RS_WIDTH", "ArgusError", "RegionAttribution",
     "argus_attr_config", "argus_attr_create", "argus_attr_destroy", "argus_attr_kernel_times",
     "argus_attr_last_error", "argus_attr_outputs", "argus_attr_run", "argus_attr_set_timing",

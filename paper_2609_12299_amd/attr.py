@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libargus_attr.so")
 
 ABI_VERSION = 1
 KIND_BEGIN, KIND_END = 1, 2
-OUT_INSTANCES, OUT_INSTANCE_EXCL, FORCE_FULL_SORT, FORCE_EVENT_SORT = 1, 2, 4, 8
+OUT_INSTANCES, OUT_INSTANCE_EXCL, FORCE_FULL_SORT, FORCE_EVENT_SORT, FORCE_RECORD_RADIX = 1, 2, 4, 8, 16
 NUM_COUNTERS = 32
 RS_WIDTH = 142
 NO_PARENT = 0xFFFFFFFF
@@ -147,7 +147,8 @@ class RegionAttribution:
     def __init__(self, num_regions: int, num_classes: int = 0, region_class=None,
                  group_shift: int = 0, num_groups: int = 0, max_records: int = 1 << 20,
                  instances: bool = True, instance_excl: bool = True,
-                 force_full_sort: bool = False, force_event_sort: bool = False, device=None):
+                 force_full_sort: bool = False, force_event_sort: bool = False,
+                 force_record_radix: bool = False, device=None):
         import torch
         self.torch = torch
         self.device = torch.device(device if device is not None else "cuda")
@@ -161,6 +162,7 @@ class RegionAttribution:
         flags = (OUT_INSTANCES if instances else 0) | (OUT_INSTANCE_EXCL if instance_excl else 0)
         flags |= FORCE_FULL_SORT if force_full_sort else 0
         flags |= FORCE_EVENT_SORT if force_event_sort else 0
+        flags |= FORCE_RECORD_RADIX if force_record_radix else 0
         self.flags = flags
         self.cfg = argus_attr_config(ABI_VERSION, self.R, self.K, int(group_shift),
                                      self.G if self.K else 0, flags, int(max_records), rc_ptr)
@@ -238,7 +240,7 @@ class RegionAttribution:
         t = self.torch
         t.cuda.synchronize(self.device)
         off = ((self._ws.data_ptr() + 255) & ~255) - self._ws.data_ptr()
-        raw = self._ws[off:off + 1712].cpu().numpy()
+        raw = self._ws[off:off + 1728].cpu().numpy()
         slot = np.dtype([("active", "<u4"), ("pos", "<u4"), ("src", "<u4"), ("dst", "<u4"),
                          ("lb", "<u4"), ("n_out", "<u4"), ("n_elems", "<u8"), ("tiles", "<u8")])
         u64 = raw.view(np.uint64)
@@ -249,7 +251,8 @@ class RegionAttribution:
                     n_ev=int(u64[128 // 8]),
                     rec_slots=raw[144:784].view(slot).copy(), ev_slots=raw[784:1424].view(slot).copy(),
                     ev_merge=int(u32[1432 // 4]), merge_rounds=int(u32[1440 // 4]),
-                    merge_end=int(u64[1448 // 8]))
+                    merge_end=int(u64[1448 // 8]), runs=int(u32[1712 // 4]),
+                    n_runs=int(u64[1720 // 8]))
 
     def set_timing(self, on: bool):
         rc = argus_attr_set_timing(self.h, on)

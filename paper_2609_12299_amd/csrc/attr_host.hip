@@ -49,11 +49,12 @@ size_t align_up(size_t v) { return (v + kAlign - 1) & ~(kAlign - 1); }
 struct Layout {
   size_t plan, rec_hist, rec_off, ev_hist, ev_off, tile_ctr;
   size_t key[2], pay[2], ctxw[2], lb[2], tsum, carry, bsum, slb, mslb, tiles, tree;
+  size_t chunk_runs, run_base, run_cnt, run_pos, run_hist, scan_bsum;
   size_t pop_ts, pop_reg, pushes, op_parent, op_sum;
   size_t inst, child_sum, hist_key, ov_mask, ov_q;
   size_t push_pos, pop_pos, ctx_list, ctx_seg, seg_start, seg_split, seg_tile0, part;
   size_t total;
-  uint64_t lb_words, tree_leaves, match_tiles, pool_cap, ctx_cap, tiles_cap;
+  uint64_t lb_words, tree_leaves, match_tiles, pool_cap, ctx_cap, tiles_cap, chunks, run_cap;
 };
 
 Layout make_layout(const argus_attr_config& c, uint64_t n, bool own_instances) {
@@ -83,6 +84,15 @@ Layout make_layout(const argus_attr_config& c, uint64_t n, bool own_instances) {
   L.tsum = take(sizeof(uint64_t) * L.match_tiles);
   L.carry = take(sizeof(TileCarry) * L.match_tiles);
   L.bsum = take(sizeof(BlockSum) * kMaxScanBlocks);
+  // context sort over runs: taken when the runs are at most an eighth of the records
+  L.chunks = ceil_div(nn, kChunk);
+  L.run_cap = nn / 8 + kChunk;
+  L.chunk_runs = take(sizeof(uint32_t) * L.chunks);
+  L.run_base = take(sizeof(uint32_t) * L.chunks);
+  L.run_cnt = take(sizeof(uint32_t) * L.run_cap);
+  L.run_pos = take(sizeof(uint32_t) * L.run_cap);
+  L.run_hist = take(sizeof(uint32_t) * 4 * kRadixBins);
+  L.scan_bsum = take(sizeof(uint64_t) * kMaxScanBlocks);
   L.slb = take(sizeof(uint64_t) * 8 * ceil_div(nn, kSweepTile));
   L.tiles = take(sizeof(TileDesc) * L.match_tiles);
   uint64_t leaves = 1;
@@ -141,7 +151,7 @@ int check_config(const argus_attr_config* c, std::string* why) {
     if (c->num_groups < 1 || c->num_groups > (1u << 20)) { *why = "num_groups must be 1..2^20 when num_classes > 0"; return ARGUS_E_INVAL; }
     if (!c->d_region_class) { *why = "d_region_class is NULL while num_classes > 0"; return ARGUS_E_INVAL; }
   }
-  if (c->flags & ~15u) { *why = "unknown flag bits"; return ARGUS_E_INVAL; }
+  if (c->flags & ~31u) { *why = "unknown flag bits"; return ARGUS_E_INVAL; }
   if (c->max_records >= (1ull << 31)) { *why = "max_records must be < 2^31"; return ARGUS_E_CAPACITY; }
   return ARGUS_OK;
 }
@@ -272,6 +282,14 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
   w.tsum = (uint64_t*)(base + L.tsum);
   w.carry = (TileCarry*)(base + L.carry);
   w.bsum = (BlockSum*)(base + L.bsum);
+  w.chunk_runs = (uint32_t*)(base + L.chunk_runs);
+  w.run_base = (uint32_t*)(base + L.run_base);
+  w.run_cnt = (uint32_t*)(base + L.run_cnt);
+  w.run_pos = (uint32_t*)(base + L.run_pos);
+  w.run_hist = (uint32_t*)(base + L.run_hist);
+  w.scan_bsum = (uint64_t*)(base + L.scan_bsum);
+  w.chunks = L.chunks;
+  w.run_cap = L.run_cap;
   w.slb = (uint64_t*)(base + L.slb);
   w.mslb = (uint64_t*)(base + L.mslb);
   w.tiles = (TileDesc*)(base + L.tiles);
@@ -343,10 +361,17 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
       "radix_ctx0", "radix_ctx1", "radix_ctx2", "radix_ctx3", "radix_ts0", "radix_ts1",
       "radix_ts2", "radix_ts3", "radix_ts4", "radix_ts5", "radix_ts6", "radix_ts7",
       "radix_ctx0b", "radix_ctx1b", "radix_ctx2b", "radix_ctx3b"};
+  // context sort over runs (each launch returns at once on the radix path)
+  if (!step("runs_base", launch_runs_base(a, s))) return ARGUS_E_HIP;
+  if (!step("runs_compact", launch_runs_compact(a, s))) return ARGUS_E_HIP;
+  if (!step("runs_plan", launch_runs_plan(a, s))) return ARGUS_E_HIP;
   for (int sl = 0; sl < kPhase2Slot; ++sl)
     if (!step(rnames[sl], launch_radix_pass(a, 0, sl, n, s))) return ARGUS_E_HIP;
+  if (!step("runs_pos", launch_runs_pos(a, s))) return ARGUS_E_HIP;
+  if (!step("runs_scatter", launch_runs_scatter(a, s))) return ARGUS_E_HIP;
   if (!step("tile_sums", launch_tsum(a, 0, s))) return ARGUS_E_HIP;
   if (!step("ts_hist", launch_ts_hist(a, s))) return ARGUS_E_HIP;
+  if (!step("lb_clear", launch_lb_clear(a, s))) return ARGUS_E_HIP;
   if (!step("plan2", launch_plan2(a, s))) return ARGUS_E_HIP;
   for (int sl = kPhase2Slot; sl < kSlots; ++sl)
     if (!step(rnames[sl], launch_radix_pass(a, 0, sl, n, s))) return ARGUS_E_HIP;

@@ -21,6 +21,7 @@ constexpr int kRadixBins = 256;
 constexpr int kDigitPositions = 12;  // 4 context digits, then 8 timestamp digits
 constexpr int kSlots = 16;           // sort passes planned per sort
 constexpr int kPhase2Slot = 4;       // first slot of the full-sort phase
+constexpr int kChunk = 256;          // input records per chunk of the run detection
 
 constexpr int kMatchThreads = 256;
 constexpr int kMatchItems = 8;
@@ -114,6 +115,10 @@ struct DevPlan {
   uint32_t m_nctx;     // contexts of groups < G (a prefix of the context list)
   uint64_t m_end;      // sorted position where groups >= G start (or n_valid)
   MergeRound mr[kMaxMergeRounds];
+  // context sort over runs of one context in the input
+  uint32_t runs;       // 1: records are sorted as runs (else radix passes over records)
+  uint32_t pad1;
+  uint64_t n_runs;     // runs of one context in the 256-record input chunks
 };
 
 // The Python binding reads the plan back for measurement; keep its layout.
@@ -127,7 +132,8 @@ static_assert(offsetof(DevPlan, ev_merge) == 1432, "DevPlan layout");
 static_assert(offsetof(DevPlan, m_end) == 1448, "DevPlan layout");
 static_assert(sizeof(MergeRound) == 32, "MergeRound layout");
 static_assert(offsetof(DevPlan, mr) == 1456, "DevPlan layout");
-static_assert(sizeof(DevPlan) == 1712, "DevPlan layout");
+static_assert(offsetof(DevPlan, runs) == 1712, "DevPlan layout");
+static_assert(sizeof(DevPlan) == 1728, "DevPlan layout");
 
 // Per-tile summary written by the matching kernel, read by the resolver.
 struct TileDesc {
@@ -185,6 +191,14 @@ struct Work {
   uint64_t* tsum;       // matching tile sums, [tiles]
   TileCarry* carry;     // matching tile entering values, [tiles]
   BlockSum* bsum;       // [kMaxScanBlocks]
+  uint32_t* chunk_runs; // [chunks] runs of one context in each input chunk
+  uint32_t* run_base;   // [chunks] index of each chunk's first run
+  uint32_t* run_cnt;    // [run_cap] valid records of each run
+  uint32_t* run_pos;    // [run_cap] sorted position of each run's first valid record
+  uint32_t* run_hist;   // [4][256] context-digit histograms over runs
+  uint64_t* scan_bsum;  // [kMaxScanBlocks] block sums of the run scans
+  uint64_t chunks;      // ceil(n / kChunk)
+  uint64_t run_cap;     // runs the run path accepts
   uint64_t* slb;        // sweep look-back status, [tiles][8]
   uint64_t* mslb;       // last merge round tile records, [tiles_cap][2 + 2K + K(K + 1)]
   TileDesc* tiles;      // [match tiles]
@@ -412,6 +426,12 @@ hipError_t launch_plan(const RunArgs& a, hipStream_t s);
 hipError_t launch_radix_pass(const RunArgs& a, int which /*0 rec, 1 ev*/, int slot,
                              uint64_t max_elems, hipStream_t s);
 hipError_t launch_tsum(const RunArgs& a, int mode, hipStream_t s);
+hipError_t launch_runs_base(const RunArgs& a, hipStream_t s);
+hipError_t launch_runs_compact(const RunArgs& a, hipStream_t s);
+hipError_t launch_runs_plan(const RunArgs& a, hipStream_t s);
+hipError_t launch_runs_pos(const RunArgs& a, hipStream_t s);
+hipError_t launch_runs_scatter(const RunArgs& a, hipStream_t s);
+hipError_t launch_lb_clear(const RunArgs& a, hipStream_t s);
 hipError_t launch_mscan(const RunArgs& a, hipStream_t s);
 hipError_t launch_ts_hist(const RunArgs& a, hipStream_t s);
 hipError_t launch_plan2(const RunArgs& a, hipStream_t s);

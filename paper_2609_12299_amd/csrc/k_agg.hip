@@ -14,6 +14,7 @@ namespace argus {
 constexpr uint32_t kAggLdsBytes = 96 * 1024;  // per-block statistics budget
 constexpr uint32_t kStatBytes = 6 * 8 + 5 * 4;  // per region
 constexpr uint32_t kHistBytes = 130 * 4;         // per region
+constexpr uint32_t kHistLdsBytes = 152 * 1024;  // per-block budget of the histogram pass (160 KiB of LDS)
 
 __device__ __forceinline__ uint32_t agg_parent(const argus_instance& x, const TileDesc* tiles,
                                                const uint32_t* op_parent) {
@@ -411,8 +412,9 @@ hipError_t launch_hist(const RunArgs& a, hipStream_t s) {
   size_t bytes;
   agg_sizes(a.R, &rl, &hl, &bytes);
   if (hl) return hipSuccess;
-  const uint32_t slice = kAggLdsBytes / kHistBytes;
-  const uint32_t slices = (uint32_t)ceil_div(a.R, slice);
+  // as few slices as fit, of equal size
+  const uint32_t slices = (uint32_t)ceil_div((uint64_t)a.R * kHistBytes, kHistLdsBytes);
+  const uint32_t slice = (uint32_t)ceil_div(a.R, slices);
   HistArgs h{a.w.plan, a.w.hist_key, a.out.d_region_stats, a.R, slice};
   uint64_t blocks = ceil_div(a.n ? a.n : 1, 1024 * 64);
   if (blocks > 256) blocks = 256;

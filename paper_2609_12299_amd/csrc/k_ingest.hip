@@ -79,6 +79,64 @@ __device__ __forceinline__ uint32_t block_excl_scan256(uint32_t v, uint32_t* scr
   return pre + x - v;
 }
 
+// ------------------------------------------------- runs of one context
+// A wave holds one input chunk of 256 records as 4 rows of 64 lanes (record
+// 64 j + lane of the chunk in row j); masks over the chunk have bit
+// p = 64 j + lane in word j.
+static_assert(kChunk == 256, "a chunk is 4 rows of a wave");
+
+// Set bits of m in positions [lo, hi).
+__device__ __forceinline__ uint32_t popc_range(const uint64_t (&m)[4], uint32_t lo, uint32_t hi) {
+  uint32_t c = 0;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const uint32_t a = lo > 64u * r ? lo - 64u * r : 0u;
+    const uint32_t b = hi < 64u * r + 64u ? (hi > 64u * r ? hi - 64u * r : 0u) : 64u;
+    if (a < b) {
+      const uint64_t mk = (b - a == 64 ? ~0ull : ((1ull << (b - a)) - 1ull)) << a;
+      c += (uint32_t)__popcll(m[r] & mk);
+    }
+  }
+  return c;
+}
+// First set bit after position p, or 256.
+__device__ __forceinline__ uint32_t next_set_after(const uint64_t (&m)[4], uint32_t p) {
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    if (64u * r + 63u <= p) continue;
+    uint64_t w = m[r];
+    if (p >= 64u * r) w &= ~0ull << (p - 64u * r) << 1;  // two shifts: p - 64 r may be 63
+    if (w) return 64u * r + (uint32_t)__ffsll((unsigned long long)w) - 1u;
+  }
+  return (uint32_t)kChunk;
+}
+// Last set bit at or before position p (one exists).
+__device__ __forceinline__ uint32_t last_set_upto(const uint64_t (&m)[4], uint32_t p) {
+#pragma unroll
+  for (int r = 3; r >= 0; --r) {
+    if (64u * r > p) continue;
+    uint64_t w = m[r];
+    if (p < 64u * r + 63u) w &= (2ull << (p - 64u * r)) - 1ull;
+    if (w) return 64u * r + 63u - (uint32_t)__clzll(w);
+  }
+  return 0u;
+}
+// Run heads (a record whose predecessor in the chunk has another context,
+// or the chunk's first record) and valid records of the chunk.
+__device__ __forceinline__ void chunk_masks(const uint32_t (&ctx)[4], const bool (&in)[4],
+                                            const bool (&valid)[4], uint64_t (&H)[4],
+                                            uint64_t (&V)[4]) {
+  const uint32_t lane = lane_id();
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    uint32_t prev = (uint32_t)__shfl_up((int)ctx[j], 1);
+    if (lane == 0) prev = j > 0 ? (uint32_t)__builtin_amdgcn_readlane((int)ctx[j > 0 ? j - 1 : 0], 63) : ctx[j];
+    const bool head = in[j] && ((j == 0 && lane == 0) || prev != ctx[j]);
+    H[j] = __ballot(head);
+    V[j] = __ballot(valid[j]);
+  }
+}
+
 // ------------------------------------------------------------------ init
 
 struct Fill {
@@ -137,6 +195,7 @@ hipError_t launch_init(const RunArgs& a, hipStream_t s) {
   add(w.rec_hist, sizeof(uint32_t) * kDigitPositions * kRadixBins, 0);
   add(w.ev_hist, sizeof(uint32_t) * kDigitPositions * kRadixBins, 0);
   add(w.tile_ctr, sizeof(uint32_t) * kCtrCount, 0);
+  add(w.run_hist, sizeof(uint32_t) * 4 * kRadixBins, 0);
   // look-back status of the first record pass (its tiles cover every record)
   add(w.lb[0], sizeof(uint64_t) * ceil_div(a.n ? a.n : 1, kSortTile) * kRadixBins, 0);
   add(w.slb, sizeof(uint64_t) * 8 * ceil_div(a.n ? a.n : 1, kSweepTile), 0);
@@ -168,16 +227,23 @@ struct IngestArgs {
   uint64_t n;
   uint32_t R;
   uint64_t* counters;
-  uint32_t* hist;  // rec_hist: positions 0..3 (raw context digits)
+  uint32_t* hist;        // rec_hist: positions 0..3 (raw context digits)
+  DevPlan* plan;         // n_runs
+  uint64_t* runs_raw;    // [chunk * 256 + j]: context | valid records << 32 of run j
+  uint32_t* chunk_runs;  // [chunk]
 };
 
 // One coalesced 16-byte load per record.  Counts kinds and regions, reduces
 // the timestamp and context ranges of valid records, and builds the 256-bin
 // histograms of the four raw context digits (used by the context passes of
-// the sort).
+// the sort).  Each wave step covers one 256-record chunk, whose runs of one
+// context (and their valid records) are recorded for the context sort over
+// runs.
 __global__ __launch_bounds__(256) void k_ingest(IngestArgs a) {
   __shared__ uint32_t s_hist[4][kRadixBins];
   __shared__ uint64_t s_red[4][8];
+  __shared__ unsigned long long s_runs;
+  if (threadIdx.x == 0) s_runs = 0;
   for (int i = threadIdx.x; i < 4 * kRadixBins; i += 256) (&s_hist[0][0])[i] = 0;
   __syncthreads();
 
@@ -189,12 +255,41 @@ __global__ __launch_bounds__(256) void k_ingest(IngestArgs a) {
   const uint64_t stride = (uint64_t)gridDim.x * 256 * kPer;
   const uint32_t lane = threadIdx.x & 63;
   const uint64_t first = ((uint64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * (64 * kPer);
+  static_assert(kPer * 64 == kChunk, "a wave step is one chunk");
+  uint64_t wave_runs = 0;
   for (uint64_t base = first; base < a.n; base += stride) {
     uint4 r[kPer];
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
       const uint64_t i = base + (uint64_t)j * 64 + lane;
       r[j] = a.rec[i < a.n ? i : a.n - 1];
+    }
+    {
+      // runs of one context in this chunk
+      uint32_t cx[kPer];
+      bool inr[kPer], vl[kPer];
+#pragma unroll
+      for (int j = 0; j < kPer; ++j) {
+        const uint64_t i = base + (uint64_t)j * 64 + lane;
+        const uint32_t kind = (r[j].w >> 16) & 0xFFu;
+        cx[j] = r[j].z;
+        inr[j] = i < a.n;
+        vl[j] = inr[j] && (kind == 1 || kind == 2) && (r[j].w & 0xFFFFu) < a.R;
+      }
+      uint64_t H[4], V[4];
+      chunk_masks(cx, inr, vl, H, V);
+      const uint64_t chunk = base / kChunk;
+#pragma unroll
+      for (int j = 0; j < kPer; ++j) {
+        if (!((H[j] >> lane) & 1ull)) continue;
+        const uint32_t p = 64u * j + lane;
+        const uint32_t li = popc_range(H, 0, p);
+        const uint32_t cnt = popc_range(V, p, next_set_after(H, p));
+        a.runs_raw[chunk * kChunk + li] = (uint64_t)cx[j] | ((uint64_t)cnt << 32);
+      }
+      const uint32_t nr = (uint32_t)(__popcll(H[0]) + __popcll(H[1]) + __popcll(H[2]) + __popcll(H[3]));
+      if (lane == 0) a.chunk_runs[chunk] = nr;
+      wave_runs += nr;
     }
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
@@ -241,6 +336,7 @@ __global__ __launch_bounds__(256) void k_ingest(IngestArgs a) {
   ctx_min = wave_min(ctx_min);
   ctx_max = wave_max(ctx_max);
   const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0 && wave_runs) atomicAdd(&s_runs, (unsigned long long)wave_runs);
   if ((threadIdx.x & 63) == 0) {
     s_red[w][0] = n_valid;
     s_red[w][1] = n_badk;
@@ -268,6 +364,7 @@ __global__ __launch_bounds__(256) void k_ingest(IngestArgs a) {
     if (v[2]) atomicAdd(&c[ARGUS_C_N_BAD_REGION], v[2]);
     if (v[3]) atomicAdd(&c[ARGUS_C_N_BEGIN], v[3]);
     if (v[0] - v[3]) atomicAdd(&c[ARGUS_C_N_END], v[0] - v[3]);
+    if (s_runs) atomicAdd((unsigned long long*)&a.plan->n_runs, s_runs);
     if (v[0]) {
       atomicMin(&c[ARGUS_C_TS_MIN], v[4]);
       atomicMax(&c[ARGUS_C_TS_MAX], v[5]);
@@ -282,7 +379,8 @@ __global__ __launch_bounds__(256) void k_ingest(IngestArgs a) {
 }
 
 hipError_t launch_ingest(const RunArgs& a, hipStream_t s) {
-  IngestArgs ia{(const uint4*)a.rec, a.n, a.R, a.out.d_counters, a.w.rec_hist};
+  IngestArgs ia{(const uint4*)a.rec, a.n, a.R, a.out.d_counters, a.w.rec_hist, a.w.plan,
+                a.w.key[1], a.w.chunk_runs};
   uint64_t blocks = ceil_div(a.n, 256 * 4 * 4);
   if (blocks > 2048) blocks = 2048;
   if (blocks < 1) blocks = 1;
@@ -298,6 +396,8 @@ struct PlanArgs {
   const uint32_t* hist;  // rec_hist
   uint32_t* off;         // rec_off
   uint32_t phase;        // 1: context passes; 2: full sort (if needed)
+  uint32_t force_radix;  // ARGUS_FORCE_RECORD_RADIX
+  uint64_t run_cap;      // runs the run path accepts
 };
 
 __device__ __forceinline__ uint64_t mask_bits(uint32_t bits) {
@@ -331,6 +431,10 @@ __global__ __launch_bounds__(256) void k_plan(PlanArgs a) {
     k.wide = (k.ts_bits + k.ctx_bits > 64) ? 1u : 0u;
     p->rec = k;
     p->match_tiles = ceil_div(n_valid, kMatchTile);
+    // Long runs of one context in the input (per-warp buffers written in
+    // chunks): sort the runs, then place the records, instead of radix
+    // passes over every record.
+    p->runs = (!a.force_radix && !k.wide && n_valid > 0 && p->n_runs <= a.run_cap) ? 1u : 0u;
   }
   // Histogram triviality and exclusive offsets for the positions of this phase.
   const int pos_lo = 0, pos_hi = a.phase == 1 ? 4 : kDigitPositions;
@@ -344,7 +448,12 @@ __global__ __launch_bounds__(256) void k_plan(PlanArgs a) {
   }
   __syncthreads();
   if (t != 0) return;
-  if (a.phase == 1) {
+  if (a.phase == 1 && p->runs) {
+    // the runs are sorted instead (k_runs_plan plans those passes)
+    for (int sl = 0; sl < 4; ++sl) p->rs[sl].active = 0;
+    p->rec_final = 0;
+    p->rec_active = 0;
+  } else if (a.phase == 1) {
     // Context digits only: when every context is already in time order in the
     // input, a stable sort on the context alone gives (ctx, ts, input) order.
     uint32_t nact = 0;
@@ -393,14 +502,345 @@ __global__ __launch_bounds__(256) void k_plan(PlanArgs a) {
 }
 
 hipError_t launch_plan(const RunArgs& a, hipStream_t s) {
-  PlanArgs pa{a.w.plan, a.out.d_counters, a.w.rec_hist, a.w.rec_off, 1};
+  PlanArgs pa{a.w.plan, a.out.d_counters, a.w.rec_hist, a.w.rec_off, 1,
+              (a.flags & ARGUS_FORCE_RECORD_RADIX) ? 1u : 0u, a.w.run_cap};
   hipLaunchKernelGGL(k_plan, dim3(1), dim3(256), 0, s, pa);
   return hipGetLastError();
 }
 
 hipError_t launch_plan2(const RunArgs& a, hipStream_t s) {
-  PlanArgs pa{a.w.plan, a.out.d_counters, a.w.rec_hist, a.w.rec_off, 2};
+  PlanArgs pa{a.w.plan, a.out.d_counters, a.w.rec_hist, a.w.rec_off, 2, 0u, 0ull};
   hipLaunchKernelGGL(k_plan, dim3(1), dim3(256), 0, s, pa);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------- context sort over runs
+//
+// When the input holds long runs of one context (trace buffers written per
+// warp, interleaved in chunks), a stable sort of the records by context is:
+// the runs sorted stably by context (a radix sort over runs, not records),
+// each run's first position an exclusive scan of the run lengths in that
+// order, and every record written to its run's position plus its rank among
+// the run's valid records.  Within a context, runs and the records of a run
+// keep input order, so the result equals the record radix sort's.
+
+// Two-level exclusive scan of run counts: which 0 scans the runs of each
+// chunk (-> index of each chunk's first run), which 1 the valid records of
+// each run in sorted run order (-> each run's first position).
+struct RunScanArgs {
+  DevPlan* plan;
+  uint32_t which;
+  const uint32_t* chunk_runs;
+  uint32_t* run_base;
+  const uint32_t* run_cnt;
+  uint32_t* run_pos;
+  const uint32_t* pay[2];  // sorted run ids
+  uint64_t* bsum;          // [grid]
+};
+
+__device__ __forceinline__ uint64_t rscan_len(const RunScanArgs& a) {
+  return a.which == 0 ? ceil_div(a.plan->n_records, kChunk) : a.plan->n_runs;
+}
+
+__global__ __launch_bounds__(256) void k_rscan_part(RunScanArgs a) {
+  const DevPlan* p = a.plan;
+  if (!p->runs) return;
+  __shared__ uint64_t s_w[4];
+  const uint64_t m = rscan_len(a);
+  const uint64_t per = ceil_div(m, gridDim.x);
+  const uint64_t i0 = (uint64_t)blockIdx.x * per, i1 = i0 + per < m ? i0 + per : m;
+  const uint32_t* ids = a.pay[p->rec_final];
+  uint64_t sum = 0;
+  for (uint64_t i = i0 + threadIdx.x; i < i1; i += 256)
+    sum += a.which == 0 ? a.chunk_runs[i] : a.run_cnt[ids[i]];
+  sum = wave_sum(sum);
+  if ((threadIdx.x & 63) == 0) s_w[threadIdx.x >> 6] = sum;
+  __syncthreads();
+  if (threadIdx.x == 0) a.bsum[blockIdx.x] = s_w[0] + s_w[1] + s_w[2] + s_w[3];
+}
+
+// Exclusive scan of the block sums in place (one block).
+__global__ __launch_bounds__(1024) void k_rscan_top(RunScanArgs a, uint32_t nblk) {
+  if (!a.plan->runs) return;
+  __shared__ uint64_t s_w[16];
+  const uint32_t t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const uint32_t per = (nblk + 1023) / 1024;
+  const uint32_t k0 = t * per, k1 = k0 + per < nblk ? k0 + per : nblk;
+  uint64_t sum = 0;
+  for (uint32_t k = k0; k < k1; ++k) sum += a.bsum[k];
+  uint64_t x = sum;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint64_t y = __shfl_up(x, o);
+    if ((int)lane >= o) x += y;
+  }
+  if (lane == 63) s_w[w] = x;
+  __syncthreads();
+  uint64_t pre = x - sum;
+  for (uint32_t q = 0; q < w; ++q) pre += s_w[q];
+  for (uint32_t k = k0; k < k1; ++k) {
+    const uint64_t v = a.bsum[k];
+    a.bsum[k] = pre;
+    pre += v;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_rscan_apply(RunScanArgs a) {
+  const DevPlan* p = a.plan;
+  if (!p->runs) return;
+  __shared__ uint32_t s_w[4];
+  const uint64_t m = rscan_len(a);
+  const uint64_t per = ceil_div(m, gridDim.x);
+  const uint64_t i0 = (uint64_t)blockIdx.x * per, i1 = i0 + per < m ? i0 + per : m;
+  const uint32_t* ids = a.pay[p->rec_final];
+  const uint32_t t = threadIdx.x, lane = t & 63, w = t >> 6;
+  uint64_t carry = a.bsum[blockIdx.x];
+  for (uint64_t c0 = i0; c0 < i1; c0 += 1024) {
+    uint32_t v[4], sum = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint64_t i = c0 + 4 * t + q;
+      v[q] = i < i1 ? (a.which == 0 ? a.chunk_runs[i] : a.run_cnt[ids[i]]) : 0u;
+      sum += v[q];
+    }
+    const uint32_t x = (uint32_t)wave_incl_scan32((int32_t)sum);
+    if (lane == 63) s_w[w] = x;
+    __syncthreads();
+    uint64_t pre = carry + x - sum;
+    uint64_t all = carry;
+    for (uint32_t q = 0; q < 4; ++q) {
+      if (q < w) pre += s_w[q];
+      all += s_w[q];
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint64_t i = c0 + 4 * t + q;
+      if (i < i1) {
+        if (a.which == 0) a.run_base[i] = (uint32_t)pre;
+        else a.run_pos[ids[i]] = (uint32_t)pre;
+      }
+      pre += v[q];
+    }
+    carry = all;
+    __syncthreads();
+  }
+}
+
+static uint32_t rscan_blocks(uint64_t cap) {
+  uint64_t b = ceil_div(cap ? cap : 1, 4096);
+  if (b > kMaxScanBlocks) b = kMaxScanBlocks;
+  return b < 1 ? 1u : (uint32_t)b;
+}
+
+static hipError_t launch_rscan(const RunArgs& a, uint32_t which, uint64_t cap, hipStream_t s) {
+  RunScanArgs r{};
+  r.plan = a.w.plan;
+  r.which = which;
+  r.chunk_runs = a.w.chunk_runs;
+  r.run_base = a.w.run_base;
+  r.run_cnt = a.w.run_cnt;
+  r.run_pos = a.w.run_pos;
+  for (int b = 0; b < 2; ++b) r.pay[b] = a.w.pay[b];
+  r.bsum = a.w.scan_bsum;
+  const uint32_t nblk = rscan_blocks(cap);
+  hipLaunchKernelGGL(k_rscan_part, dim3(nblk), dim3(256), 0, s, r);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_rscan_top, dim3(1), dim3(1024), 0, s, r, nblk);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_rscan_apply, dim3(nblk), dim3(256), 0, s, r);
+  return hipGetLastError();
+}
+
+hipError_t launch_runs_base(const RunArgs& a, hipStream_t s) { return launch_rscan(a, 0, a.w.chunks, s); }
+hipError_t launch_runs_pos(const RunArgs& a, hipStream_t s) { return launch_rscan(a, 1, a.w.run_cap, s); }
+
+struct RunCompactArgs {
+  DevPlan* plan;
+  const uint64_t* runs_raw;
+  const uint32_t* chunk_runs;
+  const uint32_t* run_base;
+  uint64_t* key;      // key[0]: context offset << ts_bits
+  uint32_t* pay;      // pay[0]: run id
+  uint32_t* run_cnt;
+  uint32_t* run_hist; // [4][256]
+};
+
+// The runs of every chunk, in input order, as sort elements (key: context
+// offset, payload: run id), their lengths, and the context-digit histograms
+// over runs.  A run without valid records sorts as the lowest context.
+__global__ __launch_bounds__(256) void k_runs_compact(RunCompactArgs a) {
+  DevPlan* p = a.plan;
+  if (!p->runs) return;
+  __shared__ uint32_t s_hist[4][kRadixBins];
+  for (int i = threadIdx.x; i < 4 * kRadixBins; i += 256) (&s_hist[0][0])[i] = 0;
+  __syncthreads();
+  const KeySpace ks = p->rec;
+  const uint64_t chunks = ceil_div(p->n_records, kChunk);
+  const uint64_t stride = (uint64_t)gridDim.x * 256;
+  for (uint64_t c = (uint64_t)blockIdx.x * 256 + threadIdx.x; c < chunks; c += stride) {
+    const uint32_t nr = a.chunk_runs[c];
+    const uint32_t rb = a.run_base[c];
+    for (uint32_t j = 0; j < nr && j < (uint32_t)kChunk; ++j) {
+      const uint64_t v = a.runs_raw[c * kChunk + j];
+      const uint32_t cnt = (uint32_t)(v >> 32);
+      const uint64_t rel = cnt ? (uint64_t)((uint32_t)v - (uint32_t)ks.ctx_min) : 0ull;
+      const uint32_t rid = rb + j;
+      a.key[rid] = ks.ts_bits >= 64 ? 0ull : (rel << ks.ts_bits);
+      a.pay[rid] = rid;
+      a.run_cnt[rid] = cnt;
+      const uint32_t ctx = (uint32_t)(ks.ctx_min + rel);
+#pragma unroll
+      for (int d = 0; d < 4; ++d) atomicAdd(&s_hist[d][(ctx >> (8 * d)) & 0xFFu], 1u);
+    }
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < 4 * kRadixBins; i += 256) {
+    const uint32_t h = (&s_hist[0][0])[i];
+    if (h) atomicAdd(&a.run_hist[i], h);
+  }
+}
+
+hipError_t launch_runs_compact(const RunArgs& a, hipStream_t s) {
+  RunCompactArgs r{a.w.plan, a.w.key[1], a.w.chunk_runs, a.w.run_base, a.w.key[0], a.w.pay[0],
+                   a.w.run_cnt, a.w.run_hist};
+  uint64_t blocks = ceil_div(a.w.chunks ? a.w.chunks : 1, 256);
+  if (blocks > 1024) blocks = 1024;
+  hipLaunchKernelGGL(k_runs_compact, dim3((uint32_t)blocks), dim3(256), 0, s, r);
+  return hipGetLastError();
+}
+
+// Plans the context passes over the runs (packed elements in buffer 0).
+__global__ __launch_bounds__(256) void k_runs_plan(DevPlan* p, const uint32_t* hist, uint32_t* off) {
+  __shared__ uint32_t s_scr[4];
+  __shared__ uint32_t s_active[4];
+  if (!p->runs) return;
+  const int t = threadIdx.x;
+  for (int pos = 0; pos < 4; ++pos) {
+    const uint32_t h = hist[pos * kRadixBins + t];
+    const int used = __syncthreads_count(h != 0);
+    uint32_t total;
+    off[pos * kRadixBins + t] = block_excl_scan256(h, s_scr, &total);
+    if (t == 0) s_active[pos] = used > 1 ? 1u : 0u;
+  }
+  __syncthreads();
+  if (t != 0) return;
+  const uint64_t n_runs = p->n_runs;
+  uint32_t j = 0;
+  for (int sl = 0; sl < 4; ++sl) {
+    SlotPlan& sp = p->rs[sl];
+    sp.active = s_active[sl];
+    sp.pos = (uint32_t)sl;
+    if (!sp.active) continue;
+    sp.src = j & 1u;
+    sp.dst = (j & 1u) ^ 1u;
+    sp.lb = j & 1u;
+    sp.n_elems = n_runs;
+    sp.n_out = (uint32_t)n_runs;
+    sp.tiles = ceil_div(n_runs, kSortTile);
+    ++j;
+  }
+  p->rec_final = j & 1u;
+  p->rec_active = j;
+}
+
+hipError_t launch_runs_plan(const RunArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(k_runs_plan, dim3(1), dim3(256), 0, s, a.w.plan, a.w.run_hist, a.w.rec_off);
+  return hipGetLastError();
+}
+
+struct RunScatterArgs {
+  DevPlan* plan;
+  const uint4* rec;
+  uint64_t n;
+  uint32_t R;
+  const uint32_t* run_base;
+  const uint32_t* run_pos;
+  uint64_t* key;  // key[0]
+  uint32_t* pay;  // pay[0]
+  uint64_t* counters;
+};
+
+// Every valid record to its run's position plus its rank among the run's
+// valid records, packed as in the radix path (key (ctx - ctx_min) << ts_bits
+// | (ts - ts_min), payload region | (kind - 1) << 16).  One wave per chunk,
+// as in the ingest.
+__global__ __launch_bounds__(256) void k_runs_scatter(RunScatterArgs a) {
+  DevPlan* p = a.plan;
+  if (!p->runs) return;
+  const KeySpace ks = p->rec;
+  const uint64_t nv = p->n_valid;
+  constexpr int kPer = 4;
+  const uint64_t stride = (uint64_t)gridDim.x * 256 * kPer;
+  const uint32_t lane = threadIdx.x & 63;
+  const uint64_t first = ((uint64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * (64 * kPer);
+  for (uint64_t base = first; base < a.n; base += stride) {
+    uint4 r[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const uint64_t i = base + (uint64_t)j * 64 + lane;
+      r[j] = a.rec[i < a.n ? i : a.n - 1];
+    }
+    const uint64_t chunk = base / kChunk;
+    const uint32_t rb = a.run_base[chunk];
+    uint32_t cx[kPer];
+    bool inr[kPer], vl[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const uint64_t i = base + (uint64_t)j * 64 + lane;
+      const uint32_t kind = (r[j].w >> 16) & 0xFFu;
+      cx[j] = r[j].z;
+      inr[j] = i < a.n;
+      vl[j] = inr[j] && (kind == 1 || kind == 2) && (r[j].w & 0xFFFFu) < a.R;
+    }
+    uint64_t H[4], V[4];
+    chunk_masks(cx, inr, vl, H, V);
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      if (!vl[j]) continue;
+      const uint32_t q = 64u * j + lane;
+      const uint32_t hp = last_set_upto(H, q);
+      const uint32_t li = popc_range(H, 0, hp);
+      const uint64_t out = (uint64_t)a.run_pos[rb + li] + popc_range(V, hp, q);
+      if (out >= nv) {
+        flag_internal_error(a.counters, 1024);
+        continue;
+      }
+      const uint64_t ts = (uint64_t)r[j].x | ((uint64_t)r[j].y << 32);
+      const uint64_t rel = (uint64_t)(cx[j] - (uint32_t)ks.ctx_min);
+      a.key[out] = (ks.ts_bits >= 64 ? 0ull : (rel << ks.ts_bits)) | (ts - ks.ts_min);
+      a.pay[out] = (r[j].w & 0xFFFFu) | ((((r[j].w >> 16) & 0xFFu) - 1u) << 16);
+    }
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) p->rec_final = 0;
+}
+
+hipError_t launch_runs_scatter(const RunArgs& a, hipStream_t s) {
+  RunScatterArgs r{a.w.plan, (const uint4*)a.rec, a.n, a.R, a.w.run_base, a.w.run_pos,
+                   a.w.key[0], a.w.pay[0], a.out.d_counters};
+  uint64_t blocks = ceil_div(a.n, 256 * 4 * 4);
+  if (blocks > 2048) blocks = 2048;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_runs_scatter, dim3((uint32_t)blocks), dim3(256), 0, s, r);
+  return hipGetLastError();
+}
+
+// After the run path the full sort (if needed) starts on a look-back status
+// array that only the shorter run passes have cleared: clear it whole.
+__global__ __launch_bounds__(256) void k_lb_clear(DevPlan* p, uint64_t* lb0, uint64_t* lb1) {
+  if (!p->runs || !p->unsorted) return;
+  uint64_t* lb = (p->rec_active & 1u) ? lb1 : lb0;
+  const uint64_t words = ceil_div(p->n_valid, kSortTile) * kRadixBins;
+  const uint64_t stride = (uint64_t)gridDim.x * 256;
+  for (uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x; i < words; i += stride) lb[i] = 0;
+}
+
+hipError_t launch_lb_clear(const RunArgs& a, hipStream_t s) {
+  uint64_t blocks = ceil_div(ceil_div(a.n ? a.n : 1, kSortTile) * kRadixBins, 256 * 8);
+  if (blocks > 2048) blocks = 2048;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_lb_clear, dim3((uint32_t)blocks), dim3(256), 0, s, a.w.plan, a.w.lb[0], a.w.lb[1]);
   return hipGetLastError();
 }
 

@@ -13,7 +13,8 @@ def log(msg: str) -> None:
 
 
 def gpu_run(rec_u8: np.ndarray, p: dict, force_full: bool = False, instances: bool = True,
-            stream=None, repeat: int = 1, force_event: bool = False, with_plan: bool = False) -> dict:
+            stream=None, repeat: int = 1, force_event: bool = False, with_plan: bool = False,
+            force_radix: bool = False) -> dict:
     import torch
 
     from paper_2609_12299_amd import RegionAttribution, to_host
@@ -21,7 +22,8 @@ def gpu_run(rec_u8: np.ndarray, p: dict, force_full: bool = False, instances: bo
     ra = RegionAttribution(p["num_regions"], p.get("num_classes", 0), p.get("region_class"),
                            p.get("group_shift", 0), p.get("num_groups", 0),
                            max_records=max(n, 1), instances=instances, instance_excl=instances,
-                           force_full_sort=force_full, force_event_sort=force_event)
+                           force_full_sort=force_full, force_event_sort=force_event,
+                           force_record_radix=force_radix)
     rec = torch.from_numpy(np.ascontiguousarray(rec_u8).reshape(-1)).to("cuda")
     outs = []
     for _ in range(repeat):

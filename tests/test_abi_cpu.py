@@ -56,7 +56,7 @@ def cfg(lib, **kw):
     ("num_regions", 65536, -1),
     ("num_classes", 9, -1),
     ("group_shift", 33, -1),
-    ("flags", 16, -1),
+    ("flags", 32, -1),
     ("max_records", 1 << 31, -4),
 ])
 def test_create_rejects_bad_config(lib, field, value, code):

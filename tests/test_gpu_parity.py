@@ -314,3 +314,80 @@ def test_overlap_every_class_count(oracle_mod, k, span):
     p = dict(num_regions=R, num_classes=k, region_class=cls, group_shift=2, num_groups=6)
     log(f"[gpu] overlap k={k} span={span} n={len(rec)}")
     assert_parity(gpu_run(rec, p), oracle_run(oracle_mod, rec, p))
+
+
+def _chunked(rng, n_ctx, per_ctx, chunk, ts_step=7, unsorted=0, bad=0.0, ctx_base=0):
+    """Records of n_ctx contexts interleaved `chunk` at a time (trace buffers
+    written per warp), optionally with `unsorted` records moved back in time
+    and a fraction `bad` of invalid kinds."""
+    rows = []
+    for c in range(n_ctx):
+        t, depth = int(rng.integers(0, 1 << 30)), 0
+        cr = []
+        for _ in range(per_ctx):
+            if depth and rng.random() < 0.5:
+                cr.append((t, ctx_base + c, int(rng.integers(0, 6)), 2))
+                depth -= 1
+            else:
+                cr.append((t, ctx_base + c, int(rng.integers(0, 6)), 1))
+                depth += 1
+            t += int(rng.integers(1, ts_step))
+        for _ in range(unsorted):
+            k = int(rng.integers(1, len(cr)))
+            ts, cx, r, kd = cr[k]
+            cr[k] = (max(0, ts - 50), cx, r, kd)
+        rows.append(cr)
+    out, left = [], True
+    pos = [0] * n_ctx
+    while left:
+        left = False
+        for c in range(n_ctx):
+            take = rows[c][pos[c]:pos[c] + chunk]
+            pos[c] += len(take)
+            out.extend(take)
+            left |= pos[c] < len(rows[c])
+    rec = records_from_rows(out)
+    if bad:
+        mask = rng.random(len(rec)) < bad
+        rec[mask, 14] = 3  # no such kind
+    return rec
+
+
+@pytest.mark.parametrize("radix", [False, True])
+@pytest.mark.parametrize("shape", ["aligned", "ragged", "one_pass_unsorted", "two_pass_unsorted",
+                                   "invalid_inside", "all_invalid_chunks", "short_runs"])
+def test_context_sort_paths(oracle_mod, shape, radix):
+    """The context sort over runs (chunked inputs) and the radix passes over
+    records give identical results, including when the run path is followed
+    by the full sort (with one and with two run passes before it)."""
+    seeds = {"aligned": 1, "ragged": 2, "one_pass_unsorted": 3, "two_pass_unsorted": 4,
+             "invalid_inside": 5, "all_invalid_chunks": 6, "short_runs": 7}
+    rng = np.random.default_rng(seeds[shape])
+    if shape == "aligned":
+        rec = _chunked(rng, 40, 1024, 256)
+    elif shape == "ragged":
+        rec = _chunked(rng, 37, int(rng.integers(300, 900)), 97)
+    elif shape == "one_pass_unsorted":  # contexts < 256: one context digit
+        rec = _chunked(rng, 200, 300, 64, unsorted=3)
+    elif shape == "two_pass_unsorted":  # contexts spread over two digits
+        rec = _chunked(rng, 60, 400, 128, unsorted=2, ctx_base=250)
+    elif shape == "invalid_inside":
+        rec = _chunked(rng, 30, 800, 256, bad=0.02)
+    elif shape == "all_invalid_chunks":
+        rec = _chunked(rng, 30, 800, 256)
+        rec[256:1024, 14] = 0
+        rec[5000:5300, 12] = 0xFF  # bad region (>= R)
+    else:  # runs too short for the run path: the radix passes either way
+        rec = _chunked(rng, 64, 200, 3)
+    p = dict(num_regions=6, num_classes=3, region_class=np.array([0, 1, 2, 0, 1, 0xFF], np.uint8),
+             group_shift=2, num_groups=64)
+    log(f"[gpu] context sort shape={shape} radix={radix} n={len(rec)}")
+    g = gpu_run(rec, p, force_radix=radix, with_plan=True)
+    plan = g.pop("_plan")
+    if radix or shape == "short_runs":
+        assert plan["runs"] == 0
+    else:
+        assert plan["runs"] == 1
+    if "unsorted" in shape:
+        assert plan["unsorted"] == 1
+    assert_parity(g, oracle_run(oracle_mod, rec, p), what=shape)
