@@ -156,7 +156,7 @@ def main() -> int:
     ap.add_argument("--force-full-sort", action="store_true")
     ap.add_argument("--force-event-sort", action="store_true",
                     help="order overlap events with the radix sort instead of merging")
-    ap.add_argument("--cpu-sample", type=int, default=1 << 25)
+    ap.add_argument("--cpu-sample", type=int, default=1 << 27)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernels", action="store_true", help="print per-launch timing to stderr")
     ap.add_argument("--copy-calibrate", action="store_true",
