@@ -51,7 +51,7 @@ struct Layout {
   size_t key[2], pay[2], ctxw[2], lb[2], tsum, carry, bsum, slb, mslb, tiles, tree;
   size_t chunk_runs, run_base, run_cnt, run_pos, run_hist, scan_bsum;
   size_t pop_ts, pop_reg, pushes, op_parent, op_sum;
-  size_t inst, child_sum, hist_key, ov_mask, ov_q;
+  size_t inst, child_sum, hist_key, agg_part, ov_mask, ov_q;
   size_t push_pos, pop_pos, ctx_list, ctx_seg, seg_start, seg_split, seg_tile0, part;
   size_t total;
   uint64_t lb_words, tree_leaves, match_tiles, pool_cap, ctx_cap, tiles_cap, chunks, run_cap;
@@ -108,6 +108,7 @@ Layout make_layout(const argus_attr_config& c, uint64_t n, bool own_instances) {
   L.inst = own_instances ? take(sizeof(argus_instance) * nn) : 0;
   L.child_sum = take(sizeof(uint64_t) * nn);
   L.hist_key = take(sizeof(uint32_t) * nn);
+  L.agg_part = take(sizeof(uint64_t) * agg_part_words(n, c.num_regions));
   const uint64_t G = c.num_classes ? c.num_groups : 0;
   L.ov_mask = take(sizeof(uint64_t) * kMasks * (G ? G : 1));
   L.ov_q = take(sizeof(uint64_t) * kQPairs * (G ? G : 1));
@@ -302,6 +303,7 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
   w.inst = own_inst ? (argus_instance*)(base + L.inst) : out->d_instances;
   w.child_sum = (uint64_t*)(base + L.child_sum);
   w.hist_key = (uint32_t*)(base + L.hist_key);
+  w.agg_part = agg_part_words(n, h->cfg.num_regions) ? (uint64_t*)(base + L.agg_part) : nullptr;
   w.ov_mask = (uint64_t*)(base + L.ov_mask);
   w.ov_q = (uint64_t*)(base + L.ov_q);
   w.push_pos = (uint32_t*)(base + L.push_pos);

@@ -47,6 +47,19 @@ constexpr int kMaxClasses = 8;
 constexpr int kQPairs = kMaxClasses * (kMaxClasses + 1) / 2;  // 36
 constexpr int kMasks = 1 << kMaxClasses;                      // 256
 
+// Payload of a packed record: region | (kind - 1) << 16 | overlap class << 24.
+// The class is 0xFF for a record whose region has none or whose group is not
+// swept (group >= G), so that matching needs no class table.
+constexpr uint32_t kPayClsShift = 24;
+__device__ __forceinline__ uint32_t pack_payload(uint32_t region, uint32_t kind, uint32_t cls) {
+  return region | ((kind - 1u) << 16) | (cls << kPayClsShift);
+}
+// Whether the records of a context take part in the overlap sweep.
+__device__ __forceinline__ bool swept_ctx(uint32_t raw_ctx, uint32_t K, uint32_t G, uint32_t shift) {
+  return K && (shift >= 32 ? 0u : (raw_ctx >> shift)) < G;
+}
+constexpr uint32_t kClsLds = 4096;  // region-class tables up to this size are staged in LDS
+
 constexpr uint32_t kNoParent = 0xFFFFFFFFu;
 constexpr uint32_t kParentPending = 0x80000000u;  // | tile: parent lies in an earlier tile
 constexpr uint16_t kNoEnd = 0xFFFF;
@@ -211,6 +224,7 @@ struct Work {
   argus_instance* inst;
   uint64_t* child_sum;  // [n_begin]
   uint32_t* hist_key;   // [n_begin]
+  uint64_t* agg_part;   // per-block region statistics of k_agg (NULL: flushed atomically)
   uint64_t* ov_mask;    // [G][256]
   uint64_t* ov_q;       // [G][36]
   uint32_t* push_pos;   // sorted position of each pushed BEGIN (pool layout)
@@ -439,6 +453,8 @@ hipError_t launch_match(const RunArgs& a, hipStream_t s);
 hipError_t launch_tree(const RunArgs& a, hipStream_t s);
 hipError_t launch_resolve(const RunArgs& a, hipStream_t s);
 hipError_t launch_agg(const RunArgs& a, hipStream_t s);
+// Words of the per-block statistics buffer of k_agg for n records (0: none).
+uint64_t agg_part_words(uint64_t n, uint32_t R);
 hipError_t launch_hist(const RunArgs& a, hipStream_t s);
 hipError_t launch_ev_plan(const RunArgs& a, hipStream_t s);
 hipError_t launch_ev_clear(const RunArgs& a, hipStream_t s);

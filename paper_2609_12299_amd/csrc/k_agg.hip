@@ -15,6 +15,11 @@ constexpr uint32_t kAggLdsBytes = 96 * 1024;  // per-block statistics budget
 constexpr uint32_t kStatBytes = 6 * 8 + 5 * 4;  // per region
 constexpr uint32_t kHistBytes = 130 * 4;         // per region
 constexpr uint32_t kHistLdsBytes = 152 * 1024;  // per-block budget of the histogram pass (160 KiB of LDS)
+// Region statistics of one block, in this order in the per-block buffer:
+// count, inclusive sum/min/max, exclusive sum/min/max, unclosed, mismatched as
+// begin and as end, self-nested.
+constexpr uint32_t kAggFields = 11;
+constexpr uint64_t kAggPartBytes = 64ull << 20;  // per-block buffer budget
 
 __device__ __forceinline__ uint32_t agg_parent(const argus_instance& x, const TileDesc* tiles,
                                                const uint32_t* op_parent) {
@@ -35,6 +40,7 @@ struct AggArgs {
   const uint32_t* op_parent;
   uint64_t* excl_out;  // NULL unless requested
   uint32_t* hist_key;  // NULL when histograms are done here
+  uint64_t* part;      // [block][kAggFields][R], or NULL: flush with atomics
   uint64_t* counters;
   uint64_t* rstats;
   uint32_t R;
@@ -281,21 +287,40 @@ __global__ __launch_bounds__(512) void k_agg(AggArgs a) {
   if (evk)
     for (uint32_t i = threadIdx.x; i < kDigitPositions * kRadixBins; i += NT)
       if (s_evh[i]) atomicAdd(&a.ev_hist[i], s_evh[i]);
-  for (uint32_t r = threadIdx.x; r < RL; r += NT) {
-    unsigned long long* row = rs + (uint64_t)r * ARGUS_RS_WIDTH;
-    if (s_cnt[r]) {
-      atomicAdd(&row[ARGUS_RS_COUNT], (unsigned long long)s_cnt[r]);
-      atomicAdd(&row[ARGUS_RS_INCL_SUM], (unsigned long long)s_isum[r]);
-      atomicAdd(&row[ARGUS_RS_EXCL_SUM], (unsigned long long)s_esum[r]);
-      atomicMin(&row[ARGUS_RS_INCL_MIN], (unsigned long long)s_imin[r]);
-      atomicMax(&row[ARGUS_RS_INCL_MAX], (unsigned long long)s_imax[r]);
-      atomicMin(&row[ARGUS_RS_EXCL_MIN], (unsigned long long)s_emin[r]);
-      atomicMax(&row[ARGUS_RS_EXCL_MAX], (unsigned long long)s_emax[r]);
+  if (a.part) {
+    // plain stores; k_agg_reduce combines the blocks (many blocks adding
+    // into the same rows with atomics serialise on them)
+    uint64_t* pb = a.part + (uint64_t)blockIdx.x * kAggFields * RL;
+    for (uint32_t r = threadIdx.x; r < RL; r += NT) {
+      pb[0 * RL + r] = s_cnt[r];
+      pb[1 * RL + r] = s_isum[r];
+      pb[2 * RL + r] = s_imin[r];
+      pb[3 * RL + r] = s_imax[r];
+      pb[4 * RL + r] = s_esum[r];
+      pb[5 * RL + r] = s_emin[r];
+      pb[6 * RL + r] = s_emax[r];
+      pb[7 * RL + r] = s_unc[r];
+      pb[8 * RL + r] = s_mab[r];
+      pb[9 * RL + r] = s_mae[r];
+      pb[10 * RL + r] = s_sn[r];
     }
-    if (s_unc[r]) atomicAdd(&row[ARGUS_RS_UNCLOSED], (unsigned long long)s_unc[r]);
-    if (s_mab[r]) atomicAdd(&row[ARGUS_RS_MISM_AS_BEGIN], (unsigned long long)s_mab[r]);
-    if (s_mae[r]) atomicAdd(&row[ARGUS_RS_MISM_AS_END], (unsigned long long)s_mae[r]);
-    if (s_sn[r]) atomicAdd(&row[ARGUS_RS_SELF_NESTED], (unsigned long long)s_sn[r]);
+  } else {
+    for (uint32_t r = threadIdx.x; r < RL; r += NT) {
+      unsigned long long* row = rs + (uint64_t)r * ARGUS_RS_WIDTH;
+      if (s_cnt[r]) {
+        atomicAdd(&row[ARGUS_RS_COUNT], (unsigned long long)s_cnt[r]);
+        atomicAdd(&row[ARGUS_RS_INCL_SUM], (unsigned long long)s_isum[r]);
+        atomicAdd(&row[ARGUS_RS_EXCL_SUM], (unsigned long long)s_esum[r]);
+        atomicMin(&row[ARGUS_RS_INCL_MIN], (unsigned long long)s_imin[r]);
+        atomicMax(&row[ARGUS_RS_INCL_MAX], (unsigned long long)s_imax[r]);
+        atomicMin(&row[ARGUS_RS_EXCL_MIN], (unsigned long long)s_emin[r]);
+        atomicMax(&row[ARGUS_RS_EXCL_MAX], (unsigned long long)s_emax[r]);
+      }
+      if (s_unc[r]) atomicAdd(&row[ARGUS_RS_UNCLOSED], (unsigned long long)s_unc[r]);
+      if (s_mab[r]) atomicAdd(&row[ARGUS_RS_MISM_AS_BEGIN], (unsigned long long)s_mab[r]);
+      if (s_mae[r]) atomicAdd(&row[ARGUS_RS_MISM_AS_END], (unsigned long long)s_mae[r]);
+      if (s_sn[r]) atomicAdd(&row[ARGUS_RS_SELF_NESTED], (unsigned long long)s_sn[r]);
+    }
   }
   if (a.hist_lds) {
     for (uint32_t i = threadIdx.x; i < RL * 130; i += NT) {
@@ -324,6 +349,51 @@ static void agg_sizes(uint32_t R, uint32_t* rl, uint32_t* hist_lds, size_t* byte
   }
 }
 
+static uint64_t agg_grid(uint64_t n) {
+  const uint64_t blocks = ceil_div(n ? n : 1, 512 * 16);
+  return blocks > 512 ? 512 : blocks;
+}
+
+uint64_t agg_part_words(uint64_t n, uint32_t R) {
+  uint32_t rl, hl;
+  size_t bytes;
+  agg_sizes(R, &rl, &hl, &bytes);
+  if (!rl) return 0;
+  const uint64_t words = agg_grid(n) * kAggFields * rl;
+  return words * sizeof(uint64_t) <= kAggPartBytes ? words : 0;
+}
+
+// Combines the per-block statistics of k_agg into the region rows: one
+// thread per (field, region) and run of kAggRun blocks (reads coalesced over
+// regions), then one atomic per thread.
+constexpr uint32_t kAggRun = 32;
+__global__ __launch_bounds__(256) void k_agg_reduce(const uint64_t* part, uint32_t nblk, uint32_t R,
+                                                    uint64_t* rstats) {
+  const uint32_t idx = blockIdx.x * 256 + threadIdx.x;
+  if (idx >= kAggFields * R) return;
+  const uint32_t f = idx / R, r = idx - f * R;
+  const bool is_min = f == 2 || f == 5, is_max = f == 3 || f == 6;
+  const uint32_t b0 = blockIdx.y * kAggRun, b1 = b0 + kAggRun < nblk ? b0 + kAggRun : nblk;
+  uint64_t v = is_min ? kU64Max : 0;
+#pragma unroll 8
+  for (uint32_t b = b0; b < b1; ++b) {
+    const uint64_t x = part[((uint64_t)b * kAggFields + f) * R + r];
+    v = is_min ? (x < v ? x : v) : is_max ? (x > v ? x : v) : v + x;
+  }
+  if (v == (is_min ? kU64Max : 0)) return;
+  constexpr int col[kAggFields] = {ARGUS_RS_COUNT,      ARGUS_RS_INCL_SUM,      ARGUS_RS_INCL_MIN,
+                                   ARGUS_RS_INCL_MAX,   ARGUS_RS_EXCL_SUM,      ARGUS_RS_EXCL_MIN,
+                                   ARGUS_RS_EXCL_MAX,   ARGUS_RS_UNCLOSED,      ARGUS_RS_MISM_AS_BEGIN,
+                                   ARGUS_RS_MISM_AS_END, ARGUS_RS_SELF_NESTED};
+  unsigned long long* dst = (unsigned long long*)(rstats + (uint64_t)r * ARGUS_RS_WIDTH + col[f]);
+  if (is_min)
+    atomicMin(dst, (unsigned long long)v);
+  else if (is_max)
+    atomicMax(dst, (unsigned long long)v);
+  else
+    atomicAdd(dst, (unsigned long long)v);
+}
+
 hipError_t launch_agg(const RunArgs& a, hipStream_t s) {
   uint32_t rl, hl;
   size_t bytes;
@@ -348,11 +418,16 @@ hipError_t launch_agg(const RunArgs& a, hipStream_t s) {
   g.shift = a.shift;
   g.ev_hist = a.w.ev_hist;
   g.wplan = a.w.plan;
-  uint64_t blocks = ceil_div(a.n ? a.n : 1, 512 * 16);
-  if (blocks > 512) blocks = 512;
+  g.part = a.w.agg_part;
+  const uint64_t blocks = agg_grid(a.n);
   if (bytes > 64 * 1024)
     (void)hipFuncSetAttribute((const void*)k_agg, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
   hipLaunchKernelGGL(k_agg, dim3((uint32_t)blocks), dim3(512), bytes, s, g);
+  if (g.part) {
+    const uint32_t threads = kAggFields * rl;
+    hipLaunchKernelGGL(k_agg_reduce, dim3(ceil_div(threads, 256), ceil_div(blocks, kAggRun)), dim3(256), 0, s,
+                       (const uint64_t*)g.part, (uint32_t)blocks, rl, a.out.d_region_stats);
+  }
   return hipGetLastError();
 }
 

@@ -760,15 +760,22 @@ struct RunScatterArgs {
   uint64_t* key;  // key[0]
   uint32_t* pay;  // pay[0]
   uint64_t* counters;
+  const uint8_t* region_class;
+  uint32_t K, G, shift;
 };
 
 // Every valid record to its run's position plus its rank among the run's
 // valid records, packed as in the radix path (key (ctx - ctx_min) << ts_bits
-// | (ts - ts_min), payload region | (kind - 1) << 16).  One wave per chunk,
-// as in the ingest.
+// | (ts - ts_min), payload region | (kind - 1) << 16 | class << 24).  One
+// wave per chunk, as in the ingest.
 __global__ __launch_bounds__(256) void k_runs_scatter(RunScatterArgs a) {
   DevPlan* p = a.plan;
   if (!p->runs) return;
+  __shared__ uint8_t s_cls[kClsLds];
+  const bool cls_lds = a.K && a.R <= kClsLds;
+  if (cls_lds)
+    for (uint32_t r = threadIdx.x; r < a.R; r += 256) s_cls[r] = a.region_class[r];
+  __syncthreads();
   const KeySpace ks = p->rec;
   const uint64_t nv = p->n_valid;
   constexpr int kPer = 4;
@@ -810,7 +817,10 @@ __global__ __launch_bounds__(256) void k_runs_scatter(RunScatterArgs a) {
       const uint64_t ts = (uint64_t)r[j].x | ((uint64_t)r[j].y << 32);
       const uint64_t rel = (uint64_t)(cx[j] - (uint32_t)ks.ctx_min);
       a.key[out] = (ks.ts_bits >= 64 ? 0ull : (rel << ks.ts_bits)) | (ts - ks.ts_min);
-      a.pay[out] = (r[j].w & 0xFFFFu) | ((((r[j].w >> 16) & 0xFFu) - 1u) << 16);
+      const uint32_t region = r[j].w & 0xFFFFu;
+      uint32_t cls = 0xFFu;
+      if (swept_ctx(cx[j], a.K, a.G, a.shift)) cls = cls_lds ? s_cls[region] : a.region_class[region];
+      a.pay[out] = pack_payload(region, (r[j].w >> 16) & 0xFFu, cls);
     }
   }
   if (blockIdx.x == 0 && threadIdx.x == 0) p->rec_final = 0;
@@ -818,7 +828,7 @@ __global__ __launch_bounds__(256) void k_runs_scatter(RunScatterArgs a) {
 
 hipError_t launch_runs_scatter(const RunArgs& a, hipStream_t s) {
   RunScatterArgs r{a.w.plan, (const uint4*)a.rec, a.n, a.R, a.w.run_base, a.w.run_pos,
-                   a.w.key[0], a.w.pay[0], a.out.d_counters};
+                   a.w.key[0], a.w.pay[0], a.out.d_counters, a.region_class, a.K, a.G, a.shift};
   uint64_t blocks = ceil_div(a.n, 256 * 4 * 4);
   if (blocks > 2048) blocks = 2048;
   if (blocks < 1) blocks = 1;

@@ -104,7 +104,6 @@ struct MatchArgs {
   uint32_t* tile_ctr;
   // overlap events in sorted-record order (merge path)
   uint64_t* ev[2];
-  const uint8_t* region_class;
   uint32_t K, G, shift, R;
   uint32_t* push_pos;
   uint32_t* pop_pos;
@@ -118,14 +117,16 @@ constexpr uint32_t kParOut = 0xFFFFFFFEu;
 // LDS for the nearest kOcCap levels; deeper ones go to global memory.
 constexpr uint32_t kOcCap = 512;
 constexpr uint32_t kQueueCap = kMatchTile / 4;  // queued searches per wave
-constexpr uint32_t kClsLds = 4096;              // region-class tables up to this size live in LDS
 
-__global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
+// WIDE: keys hold only the timestamp and contexts come from their own array
+// (one instantiation runs, the other returns at once).
+template <bool WIDE>
+__global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
   const DevPlan* P = a.plan;
+  if ((P->rec.wide != 0) != WIDE) return;
   const uint32_t tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   constexpr int IT = kMatchItems;
 
-  __shared__ uint8_t s_cls[kClsLds];  // region classes when R <= kClsLds
   // tree leaves during the searches; then the child sums of local BEGINs
   __shared__ uint2 s_leaf[kMatchTile];
   __shared__ uint32_t s_up[kUpSize];  // upper tree levels
@@ -141,7 +142,7 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   uint64_t* s_cs = (uint64_t*)s_leaf;
 
   const KeySpace ks = P->rec;
-  const bool wide = ks.wide != 0;
+  constexpr bool wide = WIDE;
   const uint64_t nv = P->n_valid;
   const uint32_t buf = P->rec_final;
   const uint64_t* gk = a.key[buf];
@@ -161,11 +162,6 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
     return a.shift >= 32 ? 0u : (raw_ctx >> a.shift);
   };
 
-  // region classes in LDS when the table is small
-  const bool cls_lds = ev_on && a.R <= kClsLds;
-  if (cls_lds)
-    for (uint32_t r = tid; r < a.R; r += kMatchThreads) s_cls[r] = a.region_class[r];
-
   // Tiles are independent: tile = block + k * grid, with the next tile's
   // records loaded while this one is processed.
   const uint64_t n_tiles = P->match_tiles;
@@ -173,10 +169,12 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   uint64_t tile = blockIdx.x;
   if (tile >= n_tiles) return;
   uint64_t nk[IT];
-  uint32_t np[IT], nc[IT];
+  uint32_t np[IT], nc[WIDE ? IT : 1];
   uint64_t nprev = 0;  // (lane 0) key or context word of the record before the thread's first
+  TileCarry ncarry;  // values entering the tile (a uniform load)
   auto issue = [&](uint64_t t) {
     const uint64_t b = t * kMatchTile;
+    ncarry = a.carry[t];
     if (lane == 0 && b + p0 > 0 && b + p0 <= nv) nprev = wide ? gc[b + p0 - 1] : gk[b + p0 - 1];
     const uint32_t c = nv - b < (uint64_t)kMatchTile ? (uint32_t)(nv - b) : (uint32_t)kMatchTile;
     if (p0 + IT <= c) {
@@ -196,7 +194,7 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
         np[4 * q + 2] = v.z;
         np[4 * q + 3] = v.w;
       }
-      if (wide) {
+      if constexpr (WIDE) {
         const uint4* c4 = (const uint4*)(gc + b + p0);
 #pragma unroll
         for (int q = 0; q < IT / 4; ++q) {
@@ -213,7 +211,7 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
         const uint32_t q = p0 + i;
         nk[i] = q < c ? gk[b + q] : 0;
         np[i] = q < c ? gp[b + q] : 0;
-        if (wide) nc[i] = q < c ? gc[b + q] : 0;
+        if constexpr (WIDE) nc[i] = q < c ? gc[b + q] : 0;
       }
     }
   };
@@ -239,6 +237,8 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   uint32_t ctxr[IT], reg[IT];
   uint32_t fb = 0, fv = 0;  // bit i: BEGIN / valid
   uint64_t prev_raw;
+  // overlap class of each record (8 bits each, 0xFF: none), from the payload
+  uint32_t clsp[2] = {0xFFFFFFFFu, 0xFFFFFFFFu};
   {
     uint64_t key[IT];
     uint32_t pay[IT];
@@ -246,9 +246,17 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
     for (int i = 0; i < IT; ++i) {
       key[i] = nk[i];
       pay[i] = np[i];
-      ctxr[i] = nc[i];
+      ctxr[i] = WIDE ? nc[WIDE ? i : 0] : 0u;
     }
     prev_raw = nprev;
+    if (tid == 0) {
+      // read by every thread after the scan below; the previous tile's reads
+      // of these are behind the barrier that ended it
+      s_sin = ncarry.s_in;
+      s_hpre = ncarry.hpre;
+      s_nbpre_lo = (uint32_t)ncarry.nbpre;
+      s_nbpre_hi = (uint32_t)(ncarry.nbpre >> 32);
+    }
     if (next < n_tiles) issue(next);
 #pragma unroll
     for (int i = 0; i < IT; ++i) {
@@ -258,19 +266,9 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
       if (p0 + i < cnt) {
         fv |= 1u << i;
         if (((pay[i] >> 16) & 1u) == 0) fb |= 1u << i;
+        const uint32_t c = pay[i] >> kPayClsShift;
+        clsp[i >> 2] = (clsp[i >> 2] & ~(0xFFu << (8 * (i & 3)))) | (c << (8 * (i & 3)));
       }
-    }
-  }
-  // Region classes of the records, fetched now so that their latency hides
-  // behind the scan and the look-back (packed 8 bits each).
-  uint32_t clsp[2] = {0xFFFFFFFFu, 0xFFFFFFFFu};
-  if (ev_on) {
-#pragma unroll
-    for (int i = 0; i < IT; ++i) {
-      uint32_t c = 0xFFu;
-      if ((fv >> i) & 1u && group_of(ctxr[i] + (uint32_t)ks.ctx_min) < a.G)
-        c = cls_lds ? (uint32_t)s_cls[reg[i]] : (uint32_t)a.region_class[reg[i]];
-      clsp[i >> 2] = (clsp[i >> 2] & ~(0xFFu << (8 * (i & 3)))) | (c << (8 * (i & 3)));
     }
   }
   // context of the record before this thread's first one: the previous
@@ -336,14 +334,8 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
 
   // ---- entering values of the tile (depth, BEGINs and context starts
   // before it), from the scan over the tile sums
-  if (tid == 0) {
-    const TileCarry c = a.carry[tile];
-    s_sin = c.s_in;
-    s_hpre = c.hpre;
-    s_nbpre_lo = (uint32_t)c.nbpre;
-    s_nbpre_hi = (uint32_t)(c.nbpre >> 32);
-  }
   __syncthreads();
+  const uint32_t tile_nb = (s_wnb[0] + s_wnb[1] + s_wnb[2] + s_wnb[3]) & 0xFFFFu;
 
   const uint32_t s_in = s_sin;
   const uint64_t nbpre = (uint64_t)s_nbpre_lo | ((uint64_t)s_nbpre_hi << 32);
@@ -561,7 +553,7 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
   if (n_op > kOcCap) __threadfence_block();
   __syncthreads();
 
-  // ---- instances and child sums
+  // ---- child sums, open BEGINs and the instances
   uint32_t mbeg = 0;  // bit i: BEGIN matched to an END of the same region
   {
     uint32_t r = tnb;
@@ -572,10 +564,9 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
       const uint32_t k = r++;
       const uint64_t id = nbpre + k;
       const uint32_t L = sb[i];
-      uint32_t ereg = s_ereg[k];
-      uint64_t t_end = kU64Max;
+      const uint32_t ereg = s_ereg[k];
       if (ereg != kNoEnd) {
-        t_end = s_tend[k];
+        const uint64_t t_end = s_tend[k];
         if (ereg == reg[i]) mbeg |= 1u << i;
         const uint64_t incl = t_end - ts[i];
         if (par[i] == kParOut) {
@@ -599,16 +590,25 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
         } else
           flag_internal_error(a.counters, 16);
       }
+      const uint64_t t_end = ereg != kNoEnd ? s_tend[k] : kU64Max;
       uint32_t pf;
       if (par[i] == kParNone) pf = kNoParent;
       else if (par[i] == kParOut) pf = kParentPending | (uint32_t)tile;
       else pf = (uint32_t)(nbpre + par[i]);
+      const uint4 w0 = make_uint4((uint32_t)ts[i], (uint32_t)(ts[i] >> 32), (uint32_t)t_end,
+                                  (uint32_t)(t_end >> 32));
+      const uint4 w1 = make_uint4(ctxr[i] + (uint32_t)ks.ctx_min, pf, L, reg[i] | (ereg << 16));
       uint4* dst = (uint4*)(a.inst + id);
-      dst[0] = make_uint4((uint32_t)ts[i], (uint32_t)(ts[i] >> 32), (uint32_t)t_end,
-                          (uint32_t)(t_end >> 32));
-      dst[1] = make_uint4(ctxr[i] + (uint32_t)ks.ctx_min, pf, L, reg[i] | (ereg << 16));
+      dst[0] = w0;
+      dst[1] = w1;
     }
   }
+  __syncthreads();  // child sums complete
+  for (uint32_t k = tid; k < tile_nb; k += kMatchThreads) a.child_sum[nbpre + k] = s_cs[k];
+  const uint32_t n_oc = n_op < kOcCap ? n_op : kOcCap;
+  for (uint32_t k = tid; k < n_oc; k += kMatchThreads) a.op_sum[pool + k] = s_oc[k];
+
+  // ---- overlap event words
   if (ev_on) {
     uint64_t e[IT];
 #pragma unroll
@@ -630,13 +630,8 @@ __global__ __launch_bounds__(kMatchThreads) void k_match(MatchArgs a) {
         if (p0 + i < cnt) evo[base + p0 + i] = e[i];
     }
   }
-  __syncthreads();
 
   // ---- per-tile outputs
-  const uint32_t tile_nb = (s_wnb[0] + s_wnb[1] + s_wnb[2] + s_wnb[3]) & 0xFFFFu;
-  for (uint32_t k = tid; k < tile_nb; k += kMatchThreads) a.child_sum[nbpre + k] = s_cs[k];
-  const uint32_t n_oc = n_op < kOcCap ? n_op : kOcCap;
-  for (uint32_t k = tid; k < n_oc; k += kMatchThreads) a.op_sum[pool + k] = s_oc[k];
   if (tid == 0) {
     const uint32_t s_out = cnt ? s_sout : 0u;
     TileDesc d;
@@ -684,7 +679,6 @@ hipError_t launch_match(const RunArgs& a, hipStream_t s) {
   m.plan = a.w.plan;
   m.wplan = a.w.plan;
   for (int b = 0; b < 2; ++b) m.ev[b] = a.w.key[b];
-  m.region_class = a.region_class;
   m.K = a.K;
   m.G = a.G;
   m.shift = a.shift;
@@ -710,9 +704,10 @@ hipError_t launch_match(const RunArgs& a, hipStream_t s) {
   m.rstats = a.out.d_region_stats;
   m.tile_ctr = a.w.tile_ctr;
   uint64_t blocks = a.w.match_tiles;
-  const uint64_t resident = persistent_blocks((const void*)k_match, kMatchThreads);
+  const uint64_t resident = persistent_blocks((const void*)k_match<false>, kMatchThreads);
   if (blocks > resident) blocks = resident;
-  hipLaunchKernelGGL(k_match, dim3((uint32_t)blocks), dim3(kMatchThreads), 0, s, m);
+  hipLaunchKernelGGL(k_match<false>, dim3((uint32_t)blocks), dim3(kMatchThreads), 0, s, m);
+  hipLaunchKernelGGL(k_match<true>, dim3((uint32_t)blocks), dim3(kMatchThreads), 0, s, m);
   return hipGetLastError();
 }
 

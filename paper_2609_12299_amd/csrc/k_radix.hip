@@ -127,7 +127,8 @@ __global__ __launch_bounds__(kSortThreads) void k_radix_pass(RadixArgs a) {
       const uint64_t k = wide ? ts_off : ((ks.ts_bits >= 64 ? 0 : (ctx_rel << ks.ts_bits)) | ts_off);
       key[r] = ok ? k : 0;
       cw[r] = ok ? (uint32_t)ctx_rel : 0u;
-      pay[r] = ok ? region | ((kind - 1u) << 16) : 0u;
+      const uint32_t cls = ok && swept_ctx(ctx, a.K, a.G, a.shift) ? a.region_class[region] : 0xFFu;
+      pay[r] = ok ? pack_payload(region, kind, cls) : 0u;
       dig[r] = ok ? digit_of(pos, ctx, ts) : 256u;  // 256: invalid (never written)
     }
   } else {
