@@ -110,17 +110,6 @@ __device__ __forceinline__ uint32_t next_set_after(const uint64_t (&m)[4], uint3
   }
   return (uint32_t)kChunk;
 }
-// Last set bit at or before position p (one exists).
-__device__ __forceinline__ uint32_t last_set_upto(const uint64_t (&m)[4], uint32_t p) {
-#pragma unroll
-  for (int r = 3; r >= 0; --r) {
-    if (64u * r > p) continue;
-    uint64_t w = m[r];
-    if (p < 64u * r + 63u) w &= (2ull << (p - 64u * r)) - 1ull;
-    if (w) return 64u * r + 63u - (uint32_t)__clzll(w);
-  }
-  return 0u;
-}
 // Run heads (a record whose predecessor in the chunk has another context,
 // or the chunk's first record) and valid records of the chunk.
 __device__ __forceinline__ void chunk_masks(const uint32_t (&ctx)[4], const bool (&in)[4],
@@ -238,7 +227,7 @@ struct IngestArgs {
 // histograms of the four raw context digits (used by the context passes of
 // the sort).  Each wave step covers one 256-record chunk, whose runs of one
 // context (and their valid records) are recorded for the context sort over
-// runs.
+// runs; the histograms and the context range are added per run.
 __global__ __launch_bounds__(256) void k_ingest(IngestArgs a) {
   __shared__ uint32_t s_hist[4][kRadixBins];
   __shared__ uint64_t s_red[4][8];
@@ -247,8 +236,10 @@ __global__ __launch_bounds__(256) void k_ingest(IngestArgs a) {
   for (int i = threadIdx.x; i < 4 * kRadixBins; i += 256) (&s_hist[0][0])[i] = 0;
   __syncthreads();
 
+  // Counts are wave-uniform (from ballots); extremes are per lane.
   uint64_t n_valid = 0, n_badk = 0, n_badr = 0, n_begin = 0;
-  uint64_t ts_min = kU64Max, ts_max = 0, ctx_min = kU64Max, ctx_max = 0;
+  uint64_t ts_min = kU64Max, ts_max = 0;
+  uint64_t ctx_min = kU64Max, ctx_max = 0;
   // Each wave takes 4 x 64 consecutive records per step (4 loads in flight
   // per lane); every lane of a wave iterates the same number of times.
   constexpr int kPer = 4;
@@ -264,77 +255,57 @@ __global__ __launch_bounds__(256) void k_ingest(IngestArgs a) {
       const uint64_t i = base + (uint64_t)j * 64 + lane;
       r[j] = a.rec[i < a.n ? i : a.n - 1];
     }
-    {
-      // runs of one context in this chunk
-      uint32_t cx[kPer];
-      bool inr[kPer], vl[kPer];
-#pragma unroll
-      for (int j = 0; j < kPer; ++j) {
-        const uint64_t i = base + (uint64_t)j * 64 + lane;
-        const uint32_t kind = (r[j].w >> 16) & 0xFFu;
-        cx[j] = r[j].z;
-        inr[j] = i < a.n;
-        vl[j] = inr[j] && (kind == 1 || kind == 2) && (r[j].w & 0xFFFFu) < a.R;
-      }
-      uint64_t H[4], V[4];
-      chunk_masks(cx, inr, vl, H, V);
-      const uint64_t chunk = base / kChunk;
-#pragma unroll
-      for (int j = 0; j < kPer; ++j) {
-        if (!((H[j] >> lane) & 1ull)) continue;
-        const uint32_t p = 64u * j + lane;
-        const uint32_t li = popc_range(H, 0, p);
-        const uint32_t cnt = popc_range(V, p, next_set_after(H, p));
-        a.runs_raw[chunk * kChunk + li] = (uint64_t)cx[j] | ((uint64_t)cnt << 32);
-      }
-      const uint32_t nr = (uint32_t)(__popcll(H[0]) + __popcll(H[1]) + __popcll(H[2]) + __popcll(H[3]));
-      if (lane == 0) a.chunk_runs[chunk] = nr;
-      wave_runs += nr;
-    }
+    uint32_t cx[kPer];
+    bool inr[kPer], vl[kPer];
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
       const uint64_t i = base + (uint64_t)j * 64 + lane;
-      const uint64_t ts = (uint64_t)r[j].x | ((uint64_t)r[j].y << 32);
-      const uint32_t ctx = r[j].z;
-      const uint32_t region = r[j].w & 0xFFFFu;
       const uint32_t kind = (r[j].w >> 16) & 0xFFu;
-      const bool in = i < a.n;
+      const uint32_t region = r[j].w & 0xFFFFu;
       const bool kind_ok = kind == 1 || kind == 2;
-      const bool valid = in && kind_ok && region < a.R;
-      n_badk += in && !kind_ok;
-      n_badr += in && kind_ok && region >= a.R;
-      n_valid += valid;
-      n_begin += valid && kind == 1;
-      ts_min = valid && ts < ts_min ? ts : ts_min;
-      ts_max = valid && ts > ts_max ? ts : ts_max;
-      ctx_min = valid && ctx < ctx_min ? ctx : ctx_min;
-      ctx_max = valid && ctx > ctx_max ? ctx : ctx_max;
-      // Context digit histograms.  Trace buffers hold runs of one context,
-      // so a wave whose valid records share a context adds with one atomic
-      // per digit; otherwise lanes with equal digits are found by ballots.
-      const uint64_t vm = __ballot(valid);
-      if (vm == 0) continue;
-      const uint32_t c0 = __shfl(ctx, __ffsll((unsigned long long)vm) - 1);
-      if (__ballot(valid && ctx != c0) == 0) {
-        if (lane == 0) {
-          const uint32_t nv = (uint32_t)__popcll(vm);
+      cx[j] = r[j].z;
+      inr[j] = i < a.n;
+      vl[j] = inr[j] && kind_ok && region < a.R;
+      n_badk += (uint64_t)__popcll(__ballot(inr[j] && !kind_ok));
+      n_badr += (uint64_t)__popcll(__ballot(inr[j] && kind_ok && region >= a.R));
+      n_begin += (uint64_t)__popcll(__ballot(vl[j] && kind == 1));
+      const uint64_t ts = (uint64_t)r[j].x | ((uint64_t)r[j].y << 32);
+      ts_min = vl[j] && ts < ts_min ? ts : ts_min;
+      ts_max = vl[j] && ts > ts_max ? ts : ts_max;
+    }
+    // runs of one context in this chunk
+    uint64_t H[4], V[4];
+    chunk_masks(cx, inr, vl, H, V);
+    const uint64_t chunk = base / kChunk;
+    uint32_t nr = 0, nvc = 0;
 #pragma unroll
-          for (int d = 0; d < 4; ++d) atomicAdd(&s_hist[d][(c0 >> (8 * d)) & 0xFFu], nv);
-        }
-      } else {
+    for (int j = 0; j < kPer; ++j) {
+      nr += (uint32_t)__popcll(H[j]);
+      nvc += (uint32_t)__popcll(V[j]);
+    }
+    n_valid += nvc;
 #pragma unroll
-        for (int d = 0; d < 4; ++d) wave_hist_add(s_hist[d], (ctx >> (8 * d)) & 0xFFu, valid);
+    for (int j = 0; j < kPer; ++j) {
+      if (!((H[j] >> lane) & 1ull)) continue;
+      const uint32_t p = 64u * j + lane;
+      const uint32_t li = popc_range(H, 0, p);
+      const uint32_t cnt = popc_range(V, p, next_set_after(H, p));
+      a.runs_raw[chunk * kChunk + li] = (uint64_t)cx[j] | ((uint64_t)cnt << 32);
+      if (cnt) {
+        // the context range, and the context digit histograms, per run
+        ctx_min = cx[j] < ctx_min ? cx[j] : ctx_min;
+        ctx_max = cx[j] > ctx_max ? cx[j] : ctx_max;
+#pragma unroll
+        for (int d = 0; d < 4; ++d) atomicAdd(&s_hist[d][(cx[j] >> (8 * d)) & 0xFFu], cnt);
       }
     }
+    if (lane == 0) a.chunk_runs[chunk] = nr;
+    wave_runs += nr;
   }
-  n_valid = wave_sum(n_valid);
-  n_badk = wave_sum(n_badk);
-  n_badr = wave_sum(n_badr);
-  n_begin = wave_sum(n_begin);
   ts_min = wave_min(ts_min);
   ts_max = wave_max(ts_max);
-  ctx_min = wave_min(ctx_min);
-  ctx_max = wave_max(ctx_max);
+  const uint64_t cmin = wave_min(ctx_min);
+  const uint64_t cmax = wave_max(ctx_max);
   const int w = threadIdx.x >> 6;
   if ((threadIdx.x & 63) == 0 && wave_runs) atomicAdd(&s_runs, (unsigned long long)wave_runs);
   if ((threadIdx.x & 63) == 0) {
@@ -344,8 +315,8 @@ __global__ __launch_bounds__(256) void k_ingest(IngestArgs a) {
     s_red[w][3] = n_begin;
     s_red[w][4] = ts_min;
     s_red[w][5] = ts_max;
-    s_red[w][6] = ctx_min;
-    s_red[w][7] = ctx_max;
+    s_red[w][6] = cmin;
+    s_red[w][7] = cmax;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -772,6 +743,8 @@ __global__ __launch_bounds__(256) void k_runs_scatter(RunScatterArgs a) {
   DevPlan* p = a.plan;
   if (!p->runs) return;
   __shared__ uint8_t s_cls[kClsLds];
+  __shared__ uint32_t s_roff[4][kChunk];  // per wave: first position of each run minus its head's rank
+  const uint32_t wv = threadIdx.x >> 6;
   const bool cls_lds = a.K && a.R <= kClsLds;
   if (cls_lds)
     for (uint32_t r = threadIdx.x; r < a.R; r += 256) s_cls[r] = a.region_class[r];
@@ -782,15 +755,24 @@ __global__ __launch_bounds__(256) void k_runs_scatter(RunScatterArgs a) {
   const uint64_t stride = (uint64_t)gridDim.x * 256 * kPer;
   const uint32_t lane = threadIdx.x & 63;
   const uint64_t first = ((uint64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * (64 * kPer);
+  // the next chunk's records and run base are loaded while this one is written
+  uint4 nr_[kPer];
+  uint32_t nrb = 0;
+  auto issue = [&](uint64_t b) {
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const uint64_t i = b + (uint64_t)j * 64 + lane;
+      nr_[j] = a.rec[i < a.n ? i : a.n - 1];
+    }
+    nrb = a.run_base[b / kChunk];
+  };
+  if (first < a.n) issue(first);
   for (uint64_t base = first; base < a.n; base += stride) {
     uint4 r[kPer];
 #pragma unroll
-    for (int j = 0; j < kPer; ++j) {
-      const uint64_t i = base + (uint64_t)j * 64 + lane;
-      r[j] = a.rec[i < a.n ? i : a.n - 1];
-    }
-    const uint64_t chunk = base / kChunk;
-    const uint32_t rb = a.run_base[chunk];
+    for (int j = 0; j < kPer; ++j) r[j] = nr_[j];
+    const uint32_t rb = nrb;
+    if (base + stride < a.n) issue(base + stride);
     uint32_t cx[kPer];
     bool inr[kPer], vl[kPer];
 #pragma unroll
@@ -803,13 +785,30 @@ __global__ __launch_bounds__(256) void k_runs_scatter(RunScatterArgs a) {
     }
     uint64_t H[4], V[4];
     chunk_masks(cx, inr, vl, H, V);
+    // Run of each record (heads before it, inclusive) and its rank among the
+    // chunk's valid records; each run head publishes its run's first
+    // position minus its own rank in the wave's LDS slots.
+    uint32_t li[kPer], vr[kPer];
+    uint32_t hb = 0, vb = 0;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const uint32_t hr = hb + (uint32_t)__builtin_amdgcn_mbcnt_hi(
+                                   (uint32_t)(H[j] >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)H[j], 0u));
+      vr[j] = vb + (uint32_t)__builtin_amdgcn_mbcnt_hi(
+                       (uint32_t)(V[j] >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)V[j], 0u));
+      const bool head = (H[j] >> lane) & 1ull;
+      if (head) s_roff[wv][hr] = a.run_pos[rb + hr] - vr[j];
+      li[j] = hr + (head ? 1u : 0u) - 1u;
+      hb += (uint32_t)__popcll(H[j]);
+      vb += (uint32_t)__popcll(V[j]);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
       if (!vl[j]) continue;
-      const uint32_t q = 64u * j + lane;
-      const uint32_t hp = last_set_upto(H, q);
-      const uint32_t li = popc_range(H, 0, hp);
-      const uint64_t out = (uint64_t)a.run_pos[rb + li] + popc_range(V, hp, q);
+      const uint64_t out = (uint64_t)(uint32_t)(s_roff[wv][li[j]] + vr[j]);
       if (out >= nv) {
         flag_internal_error(a.counters, 1024);
         continue;
