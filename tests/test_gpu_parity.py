@@ -391,3 +391,21 @@ def test_context_sort_paths(oracle_mod, shape, radix):
     if "unsorted" in shape:
         assert plan["unsorted"] == 1
     assert_parity(g, oracle_run(oracle_mod, rec, p), what=shape)
+
+
+@pytest.mark.parametrize("R", [1000, 1500, 5000])
+@pytest.mark.parametrize("sort", ["runs", "radix"])
+def test_many_regions(oracle_mod, R, sort):
+    """Region counts on both sides of the statistics' and class tables' LDS
+    limits: per-block partial statistics (1000), statistics in global memory
+    (1500, 5000) and class tables read from global memory (5000), with the
+    histograms in several slices."""
+    rng = np.random.default_rng(R + (sort == "radix"))
+    rec = _chunked(rng, 24, 1500, 256, bad=0.01)
+    regions = rng.integers(0, R + R // 50, size=len(rec))  # a few out of range
+    rec[:, 12] = (regions & 0xFF).astype(np.uint8)
+    rec[:, 13] = (regions >> 8).astype(np.uint8)
+    cls = rng.integers(0, 5, size=R).astype(np.uint8)  # class 4: none (K = 4)
+    p = dict(num_regions=R, num_classes=4, region_class=cls, group_shift=2, num_groups=5)
+    log(f"[gpu] many regions R={R} sort={sort} n={len(rec)}")
+    assert_parity(gpu_run(rec, p, force_radix=sort == "radix"), oracle_run(oracle_mod, rec, p))
