@@ -438,16 +438,24 @@ struct HistArgs {
   const uint32_t* hist_key;
   uint64_t* rstats;
   uint32_t R;
-  uint32_t slice;  // regions per slice
+  uint32_t slice;   // regions per slice
+  uint32_t slices;
+  uint32_t ranges;  // key ranges (a multiple of 8)
 };
 
-// Log2 histograms when they do not fit next to the statistics: each
-// blockIdx.y covers one slice of regions in LDS.
+// Log2 histograms when they do not fit next to the statistics: each block
+// covers one slice of regions in LDS over one range of the keys.  Blocks are
+// numbered so that the slices of one key range are 8 apart: dispatched to
+// the same XCD at about the same time, they read the keys once from HBM and
+// otherwise from that XCD's L2.
 __global__ __launch_bounds__(1024) void k_hist(HistArgs a) {
   extern __shared__ __align__(16) uint8_t smem[];
   constexpr uint32_t NT = 1024;
   uint32_t* s_h = (uint32_t*)smem;
-  const uint32_t r0 = blockIdx.y * a.slice;
+  const uint32_t b = blockIdx.x, grp = b / (8 * a.slices), rem = b % (8 * a.slices);
+  const uint32_t range = grp * 8 + rem % 8, sl = rem / 8;
+  if (range >= a.ranges || sl * a.slice >= a.R) return;
+  const uint32_t r0 = sl * a.slice;
   const uint32_t r1 = r0 + a.slice < a.R ? r0 + a.slice : a.R;
   const uint32_t nr = r1 - r0;
   for (uint32_t i = threadIdx.x; i < nr * 130; i += NT) s_h[i] = 0;
@@ -462,15 +470,15 @@ __global__ __launch_bounds__(1024) void k_hist(HistArgs a) {
   // four keys per load (the key array is 256-byte aligned)
   const uint64_t n4 = nb / 4;
   const uint4* k4 = (const uint4*)a.hist_key;
-  const uint64_t stride = (uint64_t)gridDim.x * NT;
-  for (uint64_t q = (uint64_t)blockIdx.x * NT + threadIdx.x; q < n4; q += stride) {
+  const uint64_t stride = (uint64_t)a.ranges * NT;
+  for (uint64_t q = (uint64_t)range * NT + threadIdx.x; q < n4; q += stride) {
     const uint4 v = k4[q];
     add(v.x);
     add(v.y);
     add(v.z);
     add(v.w);
   }
-  if (blockIdx.x == 0 && threadIdx.x < nb - n4 * 4) add(a.hist_key[n4 * 4 + threadIdx.x]);
+  if (range == 0 && threadIdx.x < nb - n4 * 4) add(a.hist_key[n4 * 4 + threadIdx.x]);
   __syncthreads();
   unsigned long long* rs = (unsigned long long*)a.rstats;
   for (uint32_t i = threadIdx.x; i < nr * 130; i += NT) {
@@ -490,13 +498,13 @@ hipError_t launch_hist(const RunArgs& a, hipStream_t s) {
   // as few slices as fit, of equal size
   const uint32_t slices = (uint32_t)ceil_div((uint64_t)a.R * kHistBytes, kHistLdsBytes);
   const uint32_t slice = (uint32_t)ceil_div(a.R, slices);
-  HistArgs h{a.w.plan, a.w.hist_key, a.out.d_region_stats, a.R, slice};
-  uint64_t blocks = ceil_div(a.n ? a.n : 1, 1024 * 64);
-  if (blocks > 256) blocks = 256;
-  if (blocks < 1) blocks = 1;
+  uint64_t ranges = ceil_div(a.n ? a.n : 1, 1024 * 64);
+  if (ranges > 256) ranges = 256;
+  ranges = ceil_div(ranges, 8) * 8;
+  HistArgs h{a.w.plan, a.w.hist_key, a.out.d_region_stats, a.R, slice, slices, (uint32_t)ranges};
   const size_t hb = (size_t)slice * kHistBytes;
   (void)hipFuncSetAttribute((const void*)k_hist, hipFuncAttributeMaxDynamicSharedMemorySize, (int)hb);
-  hipLaunchKernelGGL(k_hist, dim3((uint32_t)blocks, slices), dim3(1024), hb, s, h);
+  hipLaunchKernelGGL(k_hist, dim3((uint32_t)(ranges * slices)), dim3(1024), hb, s, h);
   return hipGetLastError();
 }
 
