@@ -131,11 +131,11 @@ __global__ __launch_bounds__(512) void k_agg(AggArgs a) {
   }
   uint64_t n_m = 0, n_mm = 0, n_u = 0, n_sn = 0, n_ev = 0, n_skip = 0;
   unsigned long long* rs = (unsigned long long*)a.rstats;
-  // Each wave takes 4 x 64 consecutive instances per step, with their loads
+  // Each wave takes 8 x 64 consecutive instances per step, with their loads
   // (and then the parents' regions) in flight together; every lane of a
   // wave iterates the same number of times (the event histograms use
   // ballots).
-  constexpr int B = 4;
+  constexpr int B = 8;
   const uint32_t lane = threadIdx.x & 63;
   const uint64_t stride = (uint64_t)gridDim.x * NT * B;
   for (uint64_t wb = ((uint64_t)blockIdx.x * (NT / 64) + (threadIdx.x >> 6)) * (64 * B); wb < nb;
@@ -470,8 +470,22 @@ __global__ __launch_bounds__(1024) void k_hist(HistArgs a) {
   // four keys per load (the key array is 256-byte aligned)
   const uint64_t n4 = nb / 4;
   const uint4* k4 = (const uint4*)a.hist_key;
+  // four loads per thread in flight
   const uint64_t stride = (uint64_t)a.ranges * NT;
-  for (uint64_t q = (uint64_t)range * NT + threadIdx.x; q < n4; q += stride) {
+  uint64_t q = (uint64_t)range * NT + threadIdx.x;
+  for (; q + 3 * stride < n4; q += 4 * stride) {
+    uint4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = k4[q + u * stride];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      add(v[u].x);
+      add(v[u].y);
+      add(v[u].z);
+      add(v[u].w);
+    }
+  }
+  for (; q < n4; q += stride) {
     const uint4 v = k4[q];
     add(v.x);
     add(v.y);
