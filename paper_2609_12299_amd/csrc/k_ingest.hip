@@ -248,13 +248,20 @@ __global__ __launch_bounds__(256) void k_ingest(IngestArgs a) {
   const uint64_t first = ((uint64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * (64 * kPer);
   static_assert(kPer * 64 == kChunk, "a wave step is one chunk");
   uint64_t wave_runs = 0;
+  uint4 nr_[kPer];  // the next chunk, loaded while this one is processed
+  auto issue = [&](uint64_t b) {
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const uint64_t i = b + (uint64_t)j * 64 + lane;
+      nr_[j] = a.rec[i < a.n ? i : a.n - 1];
+    }
+  };
+  if (first < a.n) issue(first);
   for (uint64_t base = first; base < a.n; base += stride) {
     uint4 r[kPer];
 #pragma unroll
-    for (int j = 0; j < kPer; ++j) {
-      const uint64_t i = base + (uint64_t)j * 64 + lane;
-      r[j] = a.rec[i < a.n ? i : a.n - 1];
-    }
+    for (int j = 0; j < kPer; ++j) r[j] = nr_[j];
+    if (base + stride < a.n) issue(base + stride);
     uint32_t cx[kPer];
     bool inr[kPer], vl[kPer];
 #pragma unroll

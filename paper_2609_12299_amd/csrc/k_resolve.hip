@@ -145,10 +145,12 @@ __device__ __forceinline__ uint32_t enclosing(const ResolveArgs& a, uint64_t t, 
   return a.pushes[(uint64_t)tp * kMatchTile + (L - d.lo_tail)];
 }
 
-// One wave per tile.
+// Sixteen lanes per tile (a tile has a few open levels at either end), so
+// that a wave keeps four tiles' dependent loads in flight.
+constexpr uint32_t kResolveLanes = 16;
 __global__ __launch_bounds__(256) void k_resolve(ResolveArgs a) {
-  const uint64_t t = (uint64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const uint32_t lane = threadIdx.x & 63;
+  const uint64_t t = (uint64_t)blockIdx.x * (256 / kResolveLanes) + (threadIdx.x / kResolveLanes);
+  const uint32_t lane = threadIdx.x % kResolveLanes;
   if (t >= a.plan->match_tiles) return;
   const TileDesc d = a.tiles[t];
   const uint64_t pool = t * kMatchTile;
@@ -160,7 +162,7 @@ __global__ __launch_bounds__(256) void k_resolve(ResolveArgs a) {
   const uint32_t es = ks.ts_bits + kEvCodeBits;
   uint64_t* evo = a.ev[a.plan->rec_final ^ 1u];
   // BEGINs still open at the end of tile t.
-  for (uint32_t i = lane; i < d.n_push; i += 64) {
+  for (uint32_t i = lane; i < d.n_push; i += kResolveLanes) {
     const uint32_t L = d.lo_tail + i;
     const uint32_t id = a.pushes[pool + i];
     if (id >= nb) {
@@ -201,7 +203,7 @@ __global__ __launch_bounds__(256) void k_resolve(ResolveArgs a) {
     atomicAdd((unsigned long long*)&a.child_sum[pf], (unsigned long long)incl);
   }
   // Instances open when tile t starts that tile t refers to.
-  for (uint32_t i = lane; i < d.n_op; i += 64) {
+  for (uint32_t i = lane; i < d.n_op; i += kResolveLanes) {
     const uint32_t L = d.op_lo + i;
     const uint32_t pid = enclosing(a, t, L);
     a.op_parent[pool + i] = pid;
@@ -221,7 +223,7 @@ hipError_t launch_resolve(const RunArgs& a, hipStream_t s) {
   r.K = a.K;
   r.G = a.G;
   r.shift = a.shift;
-  const uint64_t blocks = ceil_div(a.w.match_tiles, 4);
+  const uint64_t blocks = ceil_div(a.w.match_tiles, 256 / kResolveLanes);
   hipLaunchKernelGGL(k_resolve, dim3((uint32_t)blocks), dim3(256), 0, s, r);
   return hipGetLastError();
 }
