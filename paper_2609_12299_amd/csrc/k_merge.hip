@@ -172,24 +172,36 @@ __global__ __launch_bounds__(1024) void k_mseg(MSegArgs a) {
     return bit >= 31 ? 0u : (c >> (bit + 1));
   };
 
+  // four consecutive contexts per thread, 4096 per block step
   uint32_t carry = 0;
-  for (uint32_t base = 0; base < nc; base += 1024) {
-    const uint32_t j = base + t;
-    bool head = false;
-    uint2 e = make_uint2(0, 0);
-    if (j < nc) {
-      e = a.ctx_list[j];
-      head = j == 0 || hi_of(a.ctx_list[j - 1].x) != hi_of(e.x);
+  for (uint32_t base = 0; base < nc; base += 4096) {
+    const uint32_t j0 = base + 4 * t;
+    bool head[4];
+    uint2 e[4];
+    uint32_t nh = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t j = j0 + q;
+      head[q] = false;
+      e[q] = make_uint2(0, 0);
+      if (j < nc) {
+        e[q] = a.ctx_list[j];
+        head[q] = j == 0 || hi_of(a.ctx_list[j - 1].x) != hi_of(e[q].x);
+      }
+      nh += head[q] ? 1u : 0u;
     }
     uint32_t total;
-    const uint32_t incl = block_incl_scan1024(head ? 1u : 0u, s_w, &total);
-    if (j < nc) {
-      const uint32_t seg = carry + incl - 1;
-      a.ctx_seg[j] = seg;
-      if (head) {
-        a.seg_start[seg] = e.y;
+    uint32_t seg = carry + block_incl_scan1024(nh, s_w, &total) - nh;  // heads before j0
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t j = j0 + q;
+      if (j >= nc) continue;
+      if (head[q]) {
+        a.seg_start[seg] = e[q].y;
         a.seg_split[seg] = kNoSplit;
+        ++seg;
       }
+      a.ctx_seg[j] = seg - 1;
     }
     carry += total;
   }
@@ -209,20 +221,31 @@ __global__ __launch_bounds__(1024) void k_mseg(MSegArgs a) {
   }
   __threadfence_block();
   __syncthreads();
-  // merge tiles per segment, and their prefix
+  // merge tiles per segment, and their prefix (four segments per thread)
   carry = 0;
-  for (uint32_t base = 0; base < n_segs; base += 1024) {
-    const uint32_t sg = base + t;
-    uint32_t tiles = 0;
-    if (sg < n_segs) {
-      const uint32_t s0 = a.seg_start[sg];
-      const uint32_t s1 = sg + 1 < n_segs ? a.seg_start[sg + 1] : end;
-      if (a.seg_split[sg] == kNoSplit) a.seg_split[sg] = s1;
-      tiles = (uint32_t)ceil_div(s1 - s0, kMergeTile);
+  for (uint32_t base = 0; base < n_segs; base += 4096) {
+    const uint32_t g0 = base + 4 * t;
+    uint32_t tiles[4], nt = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t sg = g0 + q;
+      tiles[q] = 0;
+      if (sg < n_segs) {
+        const uint32_t s0 = a.seg_start[sg];
+        const uint32_t s1 = sg + 1 < n_segs ? a.seg_start[sg + 1] : end;
+        if (a.seg_split[sg] == kNoSplit) a.seg_split[sg] = s1;
+        tiles[q] = (uint32_t)ceil_div(s1 - s0, kMergeTile);
+      }
+      nt += tiles[q];
     }
     uint32_t total;
-    const uint32_t incl = block_incl_scan1024(tiles, s_w, &total);
-    if (sg < n_segs) a.seg_tile0[sg] = carry + incl - tiles;
+    uint32_t pre = carry + block_incl_scan1024(nt, s_w, &total) - nt;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t sg = g0 + q;
+      if (sg < n_segs) a.seg_tile0[sg] = pre;
+      pre += tiles[q];
+    }
     carry += total;
   }
   if (t == 0) {
