@@ -282,6 +282,24 @@ __device__ __forceinline__ uint32_t corank(const uint64_t* A, uint32_t la, const
   return lo;
 }
 
+// Merge tiles are staged in LDS with one pad word after every 16, so that
+// threads touching 8 consecutive words each (64 bytes apart) spread over
+// the banks.  lpad maps a tile position to its LDS slot.
+__device__ __forceinline__ uint32_t lpad(uint32_t i) { return i + (i >> 4); }
+constexpr uint32_t kMergeLds = kMergeTile + kMergeTile / 16 + 2;  // + reads just past a run
+
+// corank over runs A = tile[0, na) and B = tile[na, na + nb) staged in LDS.
+__device__ __forceinline__ uint32_t corank_lds(const uint64_t* se, uint32_t na, uint32_t nb,
+                                               uint32_t d) {
+  uint32_t lo = d > nb ? d - nb : 0u, hi = d < na ? d : na;
+  while (lo < hi) {
+    const uint32_t mid = (lo + hi) >> 1;
+    if (mkey(se[lpad(mid)]) <= mkey(se[lpad(na + d - 1 - mid)])) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
 // One merge tile: where its slices of the two runs start, their lengths,
 // where its output starts, where the two runs end (absolute sorted
 // positions), and whether it is the first tile of its segment.
@@ -405,7 +423,7 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(MergeArgs a) {
   const DevPlan* p = a.plan;
   // the last round is k_merge_sweep's
   if (!p->ev_merge || (uint32_t)a.round + 1 >= p->m_rounds) return;
-  __shared__ uint64_t s_e[kMergeTile + 1];  // + 1: reads past a run stay inside
+  __shared__ uint64_t s_e[kMergeLds];
   const MergeRound mr = p->mr[a.round];
   const uint64_t n_tiles = mr.n_tiles;
   const uint32_t end = (uint32_t)p->m_end;
@@ -429,7 +447,7 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(MergeArgs a) {
 #pragma unroll
       for (int j = 0; j < kMergeItems; ++j) {
         const uint32_t i = t + (uint32_t)j * kMergeThreads;
-        if (i < cnt) s_e[i] = v[j];
+        if (i < cnt) s_e[lpad(i)] = v[j];
       }
       __syncthreads();
       // the next tile's inputs, in flight during this merge
@@ -438,13 +456,12 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(MergeArgs a) {
       uint64_t o[kMergeItems];
       const uint32_t d = t * kMergeItems;
       if (d < cnt) {
-        const uint64_t* A = s_e;
-        const uint64_t* B = s_e + na;
-        uint32_t ia = corank(A, na, B, nb, d), ib = d - ia;
+        uint32_t ia = corank_lds(s_e, na, nb, d), ib = d - ia;
 #pragma unroll
         for (int j = 0; j < kMergeItems; ++j) {
-          const bool take_a = ia < na && (ib >= nb || mkey(A[ia]) <= mkey(B[ib]));
-          o[j] = take_a ? A[ia] : B[ib < nb ? ib : nb];
+          const uint64_t va = s_e[lpad(ia)], vb = s_e[lpad(na + (ib < nb ? ib : nb))];
+          const bool take_a = ia < na && (ib >= nb || mkey(va) <= mkey(vb));
+          o[j] = take_a ? va : vb;
           ia += take_a;
           ib += !take_a;
         }
@@ -453,13 +470,13 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(MergeArgs a) {
       if (d < cnt) {
 #pragma unroll
         for (int j = 0; j < kMergeItems; ++j)
-          if (d + j < cnt) s_e[d + j] = o[j];
+          if (d + j < cnt) s_e[lpad(d + j)] = o[j];
       }
       __syncthreads();
 #pragma unroll
       for (int j = 0; j < kMergeItems; ++j) {
         const uint32_t i = t + (uint32_t)j * kMergeThreads;
-        if (i < cnt) dst[tk.out_pos + i] = s_e[i];
+        if (i < cnt) dst[tk.out_pos + i] = s_e[lpad(i)];
       }
       __syncthreads();
       ok = okn;
@@ -540,12 +557,12 @@ __device__ __forceinline__ bool tile_next(const uint64_t* src, const MergeTask& 
   return true;
 }
 
-// Per-thread sums over 8 consecutive merged events e[0..nval) followed by the
-// word `after` (if has_after).  lp: biased local counts l' before the first
+// Per-thread sums over the merged events at tile positions d .. d + nval - 1
+// (staged in se) followed by the word `after` (if has_after).  lp: biased local counts l' before the first
 // event; mp: biased tile minima m'.  NARROW (the tile spans less than 2^32
 // cycles): gaps, S0, T and T2 fit 32 bits.  l' < 2^14 either way.
 template <int KC, bool NARROW>
-__device__ __forceinline__ void sweep8(const uint64_t* e, uint32_t nval, uint64_t after,
+__device__ __forceinline__ void sweep8(const uint64_t* se, uint32_t d, uint32_t nval, uint64_t after,
                                        bool has_after, const uint32_t (&lp0)[KC],
                                        const uint32_t (&mp)[KC],
                                        typename std::conditional<NARROW, uint32_t, uint64_t>::type (&tt)[1 + KC * (KC + 1) / 2],
@@ -554,7 +571,7 @@ __device__ __forceinline__ void sweep8(const uint64_t* e, uint32_t nval, uint64_
   uint32_t l[KC];
 #pragma unroll
   for (int x = 0; x < KC; ++x) l[x] = lp0[x];
-  uint64_t cur = e[0];
+  uint64_t cur = se[lpad(d)];
 #pragma unroll 1
   for (uint32_t j = 0; j < nval; ++j) {
     const uint32_t code = (uint32_t)(cur & ((1u << kEvCodeBits) - 1u));
@@ -565,7 +582,7 @@ __device__ __forceinline__ void sweep8(const uint64_t* e, uint32_t nval, uint64_
     // gap to the next event of the group (none after the last one)
     const bool inside = j + 1 < nval;
     const bool has_nx = inside || has_after;
-    const uint64_t nx = inside ? e[j + 1] : after;
+    const uint64_t nx = inside ? se[lpad(d + j + 1)] : after;
     UT gap;
     if (NARROW)
       gap = has_nx ? (UT)((uint32_t)(nx >> kEvCodeBits) - (uint32_t)(cur >> kEvCodeBits)) : (UT)0;
@@ -621,13 +638,12 @@ __device__ __forceinline__ void merge_tile(uint64_t* se, uint32_t na, uint32_t n
 #pragma unroll
   for (int j = 0; j < kMergeItems; ++j) o[j] = 0;
   if (d < cnt) {
-    const uint64_t* A = se;
-    const uint64_t* B = se + na;
-    uint32_t ia = corank(A, na, B, nb, d), ib = d - ia;
+    uint32_t ia = corank_lds(se, na, nb, d), ib = d - ia;
 #pragma unroll
     for (int j = 0; j < kMergeItems; ++j) {
-      const bool take_a = ia < na && (ib >= nb || mkey(A[ia]) <= mkey(B[ib]));
-      o[j] = take_a ? A[ia] : B[ib < nb ? ib : nb];
+      const uint64_t va = se[lpad(ia)], vb = se[lpad(na + (ib < nb ? ib : nb))];
+      const bool take_a = ia < na && (ib >= nb || mkey(va) <= mkey(vb));
+      o[j] = take_a ? va : vb;
       ia += take_a;
       ib += !take_a;
     }
@@ -635,7 +651,7 @@ __device__ __forceinline__ void merge_tile(uint64_t* se, uint32_t na, uint32_t n
   __syncthreads();  // every thread has read its inputs
 #pragma unroll
   for (int j = 0; j < kMergeItems; ++j)
-    if (d + (uint32_t)j < cnt) se[d + j] = o[j];
+    if (d + (uint32_t)j < cnt) se[lpad(d + j)] = o[j];
 }
 
 // Sums of one merged tile (se, cnt events; ss.next / ss.has_next: the word
@@ -652,7 +668,7 @@ __device__ __forceinline__ bool tile_sums(const uint64_t* se, uint32_t cnt, bool
   const uint32_t nval = d < cnt ? (cnt - d < (uint32_t)kMergeItems ? cnt - d : (uint32_t)kMergeItems) : 0u;
   const uint64_t first_w = se[0];
   const bool has_next = ss.has_next != 0;
-  const uint64_t last_w = has_next ? ss.next : se[cnt - 1];
+  const uint64_t last_w = has_next ? ss.next : se[lpad(cnt - 1)];
   const uint64_t g = es >= 64 ? 0ull : (first_w >> es);
   const uint64_t head = (g & 0xFFFFFFFFull) | ((uint64_t)(first ? 1u : 0u) << 32);
   if (!WIDE && ((last_w >> kEvCodeBits) - (first_w >> kEvCodeBits)) >= (1ull << 32)) {
@@ -660,13 +676,12 @@ __device__ __forceinline__ bool tile_sums(const uint64_t* se, uint32_t cnt, bool
     return false;
   }
   // ---- class-count deltas of the thread's events, scanned over the block
-  const uint64_t* e = se + d;
   int32_t dd[KC], inc[KC];
 #pragma unroll
   for (int x = 0; x < KC; ++x) dd[x] = 0;
 #pragma unroll 2
   for (uint32_t j = 0; j < nval; ++j) {
-    const uint32_t code = (uint32_t)(e[j] & ((1u << kEvCodeBits) - 1u));
+    const uint32_t code = (uint32_t)(se[lpad(d + j)] & ((1u << kEvCodeBits) - 1u));
     const uint32_t cls = (code - 1u) >> 1;
     const int32_t sg = 1 - 2 * (int32_t)((code - 1u) & 1u);
 #pragma unroll
@@ -704,7 +719,7 @@ __device__ __forceinline__ bool tile_sums(const uint64_t* se, uint32_t cnt, bool
     }
 #pragma unroll 2
     for (uint32_t j = 0; j < nval; ++j) {
-      const uint32_t code = (uint32_t)(e[j] & ((1u << kEvCodeBits) - 1u));
+      const uint32_t code = (uint32_t)(se[lpad(d + j)] & ((1u << kEvCodeBits) - 1u));
       const uint32_t cls = (code - 1u) >> 1;
       const int32_t sg = 1 - 2 * (int32_t)((code - 1u) & 1u);
 #pragma unroll
@@ -732,7 +747,7 @@ __device__ __forceinline__ bool tile_sums(const uint64_t* se, uint32_t cnt, bool
   }
   // ---- sums over this thread's gaps
   const bool has_after = d + kMergeItems < cnt || has_next;
-  const uint64_t after = d + kMergeItems < cnt ? se[d + kMergeItems] : ss.next;
+  const uint64_t after = d + kMergeItems < cnt ? se[lpad(d + kMergeItems)] : ss.next;
   using UT = typename std::conditional<WIDE, uint64_t, uint32_t>::type;
   UT tt[1 + NP];
   uint64_t s1[KC], s2[NP];
@@ -742,7 +757,7 @@ __device__ __forceinline__ bool tile_sums(const uint64_t* se, uint32_t cnt, bool
   for (int x = 0; x < KC; ++x) s1[x] = 0;
 #pragma unroll
   for (int x = 0; x < NP; ++x) s2[x] = 0;
-  if (nval) sweep8<KC, !WIDE>(e, nval, after, has_after, lp, mp, tt, s1, s2);
+  if (nval) sweep8<KC, !WIDE>(se, d, nval, after, has_after, lp, mp, tt, s1, s2);
   // ---- tile totals: waves in registers (rows of 16 lanes, then the four
   // row results as scalars), then across waves in LDS
   {
@@ -792,7 +807,7 @@ __device__ __forceinline__ void merge_sweep_tiles(const MergeSweepArgs& a) {
   constexpr int RW = tile_rec_words(KC);
   const DevPlan* p = a.plan;
   if (!p->ev_merge || p->m_rounds == 0) return;
-  __shared__ uint64_t s_e[kMergeTile + 1];  // + 1: reads past a run stay inside
+  __shared__ uint64_t s_e[kMergeLds];
   __shared__ MsShared<KC> ss;
   const MergeRound mr = p->mr[p->m_rounds - 1];
   const uint64_t n_tiles = mr.n_tiles;
@@ -820,7 +835,7 @@ __device__ __forceinline__ void merge_sweep_tiles(const MergeSweepArgs& a) {
 #pragma unroll
     for (int j = 0; j < kMergeItems; ++j) {
       const uint32_t i = t + (uint32_t)j * kMergeThreads;
-      if (i < cnt) s_e[i] = v[j];
+      if (i < cnt) s_e[lpad(i)] = v[j];
     }
     if (t == 0) {
       ss.next = nx;
