@@ -35,6 +35,10 @@ namespace argus {
 // level 3 (4, padded to 8) at 288.  Every group of 8 siblings is 32-byte
 // aligned.
 constexpr int kU1 = 0, kU2 = 256, kU3 = 288, kUpSize = 296;
+// The 8 leaves of each level-1 node are 64 bytes, stored 80 bytes apart so
+// that threads writing or reading their own node hit different banks.
+constexpr int kLeafStride = 10;  // uint2 slots per node
+__device__ __forceinline__ uint32_t leaf_slot(uint32_t p) { return (p >> 3) * kLeafStride + (p & 7u); }
 constexpr uint32_t kNoHit = 0xFFFFFFFFu;
 static_assert(kMatchTile == 2048, "tree levels assume 2048 leaves");
 
@@ -82,7 +86,7 @@ __device__ __forceinline__ uint32_t psv_hit(const uint2* leaf, const uint32_t* u
     }
     n1 = n2 * 8 + last_le8(up + kU1 + n2 * 8, 8u, v);
   }
-  return leaf_hit8(leaf + n1 * 8, v);
+  return leaf_hit8(leaf + n1 * kLeafStride, v);
 }
 
 struct MatchArgs {
@@ -128,7 +132,7 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
   constexpr int IT = kMatchItems;
 
   // tree leaves during the searches; then the child sums of local BEGINs
-  __shared__ uint2 s_leaf[kMatchTile];
+  __shared__ __align__(16) uint2 s_leaf[kMatchTile / 8 * kLeafStride];
   __shared__ uint32_t s_up[kUpSize];  // upper tree levels
   // search queues (one per wave) during the searches; then the end time of
   // each local BEGIN closed in the tile
@@ -398,7 +402,7 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
         if (p + 1 == cnt) s_sout = after;
       }
     }
-    uint4* leaf4 = (uint4*)&s_leaf[p0];
+    uint4* leaf4 = (uint4*)&s_leaf[leaf_slot(p0)];
     uint32_t r = tnb;
 #pragma unroll
     for (int q = 0; q < IT / 2; ++q) {
@@ -459,7 +463,7 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
     }
     (void)headi;
     if (qi >= 0)
-      hit[i] = s_leaf[p0 + qi].y;
+      hit[i] = s_leaf[leaf_slot(p0) + qi].y;
     else
       pend |= 1u << i;
   }
