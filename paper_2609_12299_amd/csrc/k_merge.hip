@@ -815,37 +815,55 @@ __device__ __forceinline__ void merge_sweep_tiles(const MergeSweepArgs& a) {
   const uint32_t es = p->rec.ts_bits + kEvCodeBits;  // group bits start here
   const uint64_t* src = a.ev[mr.src];
   const uint32_t t = threadIdx.x;
-  for (uint64_t k = blockIdx.x; k < n_tiles; k += gridDim.x) {
-    uint64_t* rec = a.rec + k * RW;
-    if (WIDE && !((rec[0] >> 33) & 1u)) continue;
-    const MergeTask tk = a.task[k];
-    if (!task_ok_last(tk, end)) {
-      if (WIDE) continue;  // never flagged
-      // unusable task: a record that starts a segment and adds nothing
-      if (t == 0) flag_internal_error(a.counters, 256);
-      if (t < (uint32_t)RW) rec[t] = t == 0 ? (0xFFFFFFFFull | (1ull << 32)) : 0ull;
-      continue;
+  // WIDE: the block first finds the flagged tiles among kMergeThreads tiles
+  // (one per thread), then processes them in order
+  __shared__ uint32_t s_wide[kMergeThreads];
+  __shared__ uint32_t s_nwide;
+  const uint64_t step = WIDE ? (uint64_t)gridDim.x * kMergeThreads : (uint64_t)gridDim.x;
+  for (uint64_t k0 = WIDE ? (uint64_t)blockIdx.x * kMergeThreads : blockIdx.x; k0 < n_tiles; k0 += step) {
+    uint32_t n_here = 1;
+    if (WIDE) {
+      if (t == 0) s_nwide = 0;
+      __syncthreads();
+      const uint64_t kt = k0 + t;
+      if (kt < n_tiles && ((a.rec[kt * RW] >> 33) & 1u)) s_wide[atomicAdd(&s_nwide, 1u)] = t;
+      __syncthreads();
+      n_here = s_nwide;
+      // the order of the flagged tiles does not matter: each has its own record
     }
-    uint64_t v[kMergeItems];
-    load_task(src, tk, t, v);
-    uint64_t nx = 0;
-    bool hnx = false;
-    if (t == 0) hnx = tile_next(src, tk, &nx);
-    const uint32_t cnt = tk.na + tk.nb;
+    for (uint32_t h = 0; h < n_here; ++h) {
+      const uint64_t k = WIDE ? k0 + s_wide[h] : k0;
+      uint64_t* rec = a.rec + k * RW;
+      const MergeTask tk = a.task[k];
+      if (!task_ok_last(tk, end)) {
+        if (WIDE) continue;  // never flagged
+        // unusable task: a record that starts a segment and adds nothing
+        if (t == 0) flag_internal_error(a.counters, 256);
+        if (t < (uint32_t)RW) rec[t] = t == 0 ? (0xFFFFFFFFull | (1ull << 32)) : 0ull;
+        continue;
+      }
+      uint64_t v[kMergeItems];
+      load_task(src, tk, t, v);
+      uint64_t nx = 0;
+      bool hnx = false;
+      if (t == 0) hnx = tile_next(src, tk, &nx);
+      const uint32_t cnt = tk.na + tk.nb;
 #pragma unroll
-    for (int j = 0; j < kMergeItems; ++j) {
-      const uint32_t i = t + (uint32_t)j * kMergeThreads;
-      if (i < cnt) s_e[lpad(i)] = v[j];
+      for (int j = 0; j < kMergeItems; ++j) {
+        const uint32_t i = t + (uint32_t)j * kMergeThreads;
+        if (i < cnt) s_e[lpad(i)] = v[j];
+      }
+      if (t == 0) {
+        ss.next = nx;
+        ss.has_next = hnx ? 1u : 0u;
+      }
+      __syncthreads();
+      merge_tile(s_e, tk.na, tk.nb, t);
+      __syncthreads();
+      tile_sums<KC, WIDE>(s_e, cnt, tk.first != 0, ss, rec, es);
+      __syncthreads();
     }
-    if (t == 0) {
-      ss.next = nx;
-      ss.has_next = hnx ? 1u : 0u;
-    }
-    __syncthreads();
-    merge_tile(s_e, tk.na, tk.nb, t);
-    __syncthreads();
-    tile_sums<KC, WIDE>(s_e, cnt, tk.first != 0, ss, rec, es);
-    __syncthreads();
+    if (WIDE) __syncthreads();  // s_wide is rewritten for the next tiles
   }
 }
 
