@@ -131,19 +131,20 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
   const uint32_t tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   constexpr int IT = kMatchItems;
 
-  // tree leaves during the searches; then the child sums of local BEGINs
-  __shared__ __align__(16) uint2 s_leaf[kMatchTile / 8 * kLeafStride];
+  __shared__ __align__(16) uint2 s_leaf[kMatchTile / 8 * kLeafStride];  // tree leaves
+  // child sums of local BEGINs; zero between tiles (cleared as they are
+  // written out)
+  __shared__ uint64_t s_cs[kMatchTile];
   __shared__ uint32_t s_up[kUpSize];  // upper tree levels
   // search queues (one per wave) during the searches; then the end time of
   // each local BEGIN closed in the tile
   __shared__ uint64_t s_tend[kMatchTile];
   __shared__ uint16_t s_ereg[kMatchTile];  // end region of each local BEGIN (0xFFFF: open)
-  __shared__ uint64_t s_oc[kOcCap];        // child sums of enclosing instances
+  __shared__ uint64_t s_oc[kOcCap];        // child sums of enclosing instances (zero between tiles)
   __shared__ Fn s_wfn[4];
   __shared__ uint32_t s_wnb[4];
   __shared__ uint32_t s_first, s_lastp1, s_heads, s_lo, s_sout, s_maxlvl, s_orph;
   __shared__ uint32_t s_sin, s_nbpre_lo, s_nbpre_hi, s_hpre, s_need;
-  uint64_t* s_cs = (uint64_t*)s_leaf;
 
   const KeySpace ks = P->rec;
   constexpr bool wide = WIDE;
@@ -220,6 +221,8 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
     }
   };
   issue(tile);
+  for (uint32_t k = tid; k < (uint32_t)kMatchTile; k += kMatchThreads) s_cs[k] = 0;
+  for (uint32_t k = tid; k < kOcCap; k += kMatchThreads) s_oc[k] = 0;
   if (tid == 0) {
     s_first = kMatchTile;
     s_lastp1 = 0;
@@ -551,11 +554,8 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
   // child sums of enclosing instances beyond the LDS ones start at zero
   const uint32_t n_op = (sin_eff > op_lo) ? ((sin_eff - op_lo) < (uint32_t)kMatchTile ? sin_eff - op_lo : (uint32_t)kMatchTile) : 0u;
   for (uint32_t k = kOcCap + tid; k < n_op; k += kMatchThreads) a.op_sum[pool + k] = 0;
-  __syncthreads();  // the tree is no longer needed: s_leaf takes child sums
-  for (uint32_t k = tid; k < (uint32_t)kMatchTile; k += kMatchThreads) s_cs[k] = 0;
-  for (uint32_t k = tid; k < kOcCap; k += kMatchThreads) s_oc[k] = 0;
   if (n_op > kOcCap) __threadfence_block();
-  __syncthreads();
+  __syncthreads();  // end times and end regions of the local BEGINs are complete
 
   // ---- child sums, open BEGINs and the instances
   uint32_t mbeg = 0;  // bit i: BEGIN matched to an END of the same region
@@ -608,9 +608,15 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
     }
   }
   __syncthreads();  // child sums complete
-  for (uint32_t k = tid; k < tile_nb; k += kMatchThreads) a.child_sum[nbpre + k] = s_cs[k];
+  for (uint32_t k = tid; k < tile_nb; k += kMatchThreads) {
+    a.child_sum[nbpre + k] = s_cs[k];
+    s_cs[k] = 0;
+  }
   const uint32_t n_oc = n_op < kOcCap ? n_op : kOcCap;
-  for (uint32_t k = tid; k < n_oc; k += kMatchThreads) a.op_sum[pool + k] = s_oc[k];
+  for (uint32_t k = tid; k < n_oc; k += kMatchThreads) {
+    a.op_sum[pool + k] = s_oc[k];
+    s_oc[k] = 0;
+  }
 
   // ---- overlap event words
   if (ev_on) {
