@@ -163,8 +163,8 @@ def main() -> int:
                     help="also run a plain 1 GiB device copy (reference for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        err("bench.py measures one GPU: this build has no multi-GPU path (the path would shard by "
-            "context group with one all-reduce of the aggregates; see DESIGN.md). Use --gpus 1.")
+        err("bench.py measures one GPU: there is no multi-GPU path (the path would shard by "
+            "context group with one all-reduce of the aggregates). Use --gpus 1.")
         return 2
 
     import torch
