@@ -84,8 +84,12 @@ def byte_model(name: str, c: dict, plan: dict, R: int, K: int, G: int, flags: in
     if name == "runs_scatter":  # raw records in, packed keys and payloads out
         return (16.0 * n + 12.0 * nv) if runs else 0.0
     if name == "tile_sums":
-        # sorted keys and payloads: order check and per-tile depth maps
-        return (12.0 + (4.0 if wide else 0.0)) * nv
+        # sorted keys and payloads: order check and per-tile depth maps (record radix path)
+        return 0.0 if runs else (12.0 + (4.0 if wide else 0.0)) * nv
+    if name == "runs_check":  # each run's count and position, the two keys where it meets the one before
+        return 24.0 * plan["n_runs"] if runs else 0.0
+    if name == "tile_sums_runs":  # sorted payloads (kind and context-start bits)
+        return 4.0 * nv if runs else 0.0
     if name == "tile_sums_full":
         return (12.0 + (4.0 if wide else 0.0)) * nv if plan["unsorted"] else 0.0
     if name == "ts_hist":

@@ -51,6 +51,9 @@ constexpr int kMasks = 1 << kMaxClasses;                      // 256
 // The class is 0xFF for a record whose region has none or whose group is not
 // swept (group >= G), so that matching needs no class table.
 constexpr uint32_t kPayClsShift = 24;
+// Set by the run scatter on the first record of each context (only the tile
+// sums of that path read it).
+constexpr uint32_t kPayStart = 1u << 17;
 __device__ __forceinline__ uint32_t pack_payload(uint32_t region, uint32_t kind, uint32_t cls) {
   return region | ((kind - 1u) << 16) | (cls << kPayClsShift);
 }
@@ -210,6 +213,7 @@ struct Work {
   uint32_t* run_pos;    // [run_cap] sorted position of each run's first valid record
   uint32_t* run_hist;   // [4][256] context-digit histograms over runs
   uint64_t* scan_bsum;  // [kMaxScanBlocks] block sums of the run scans
+  uint8_t* run_head;    // [run_cap] the run starts its context (by run id)
   uint64_t chunks;      // ceil(n / kChunk)
   uint64_t run_cap;     // runs the run path accepts
   uint64_t* slb;        // sweep look-back status, [tiles][8]
@@ -452,6 +456,8 @@ hipError_t launch_plan2(const RunArgs& a, hipStream_t s);
 hipError_t launch_match(const RunArgs& a, hipStream_t s);
 hipError_t launch_tree(const RunArgs& a, hipStream_t s);
 hipError_t launch_resolve(const RunArgs& a, hipStream_t s);
+hipError_t launch_runs_check(const RunArgs& a, hipStream_t s);
+hipError_t launch_tsum_codes(const RunArgs& a, hipStream_t s);
 hipError_t launch_agg(const RunArgs& a, hipStream_t s);
 // Words of the per-block statistics buffer of k_agg for n records (0: none).
 uint64_t agg_part_words(uint64_t n, uint32_t R);

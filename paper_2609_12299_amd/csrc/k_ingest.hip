@@ -516,6 +516,9 @@ struct RunScanArgs {
   uint32_t* run_pos;
   const uint32_t* pay[2];  // sorted run ids
   uint64_t* bsum;          // [grid]
+  // which 1: which runs start their context (for the tile sums)
+  const uint64_t* key[2];  // sorted run keys (context offset << ts_bits)
+  uint8_t* run_head;
 };
 
 __device__ __forceinline__ uint64_t rscan_len(const RunScanArgs& a) {
@@ -596,8 +599,21 @@ __global__ __launch_bounds__(256) void k_rscan_apply(RunScanArgs a) {
     for (int q = 0; q < 4; ++q) {
       const uint64_t i = c0 + 4 * t + q;
       if (i < i1) {
-        if (a.which == 0) a.run_base[i] = (uint32_t)pre;
-        else a.run_pos[ids[i]] = (uint32_t)pre;
+        if (a.which == 0) {
+          a.run_base[i] = (uint32_t)pre;
+        } else {
+          const uint32_t id = ids[i];
+          a.run_pos[id] = (uint32_t)pre;
+          // A run starts its context if it has valid records and the
+          // previous run has another context; runs without valid records
+          // sort as context offset 0, so the runs of offset 0 start it only
+          // at position 0.
+          const uint32_t tb = p->rec.ts_bits;
+          const uint64_t* keys = a.key[p->rec_final];
+          const uint32_t ctx = tb >= 64 ? 0u : (uint32_t)(keys[i] >> tb);
+          const uint32_t prev = i > 0 ? (tb >= 64 ? 0u : (uint32_t)(keys[i - 1] >> tb)) : 0xFFFFFFFFu;
+          a.run_head[id] = v[q] > 0 && (ctx == 0 ? pre == 0 : prev != ctx) ? 1u : 0u;
+        }
       }
       pre += v[q];
     }
@@ -620,8 +636,12 @@ static hipError_t launch_rscan(const RunArgs& a, uint32_t which, uint64_t cap, h
   r.run_base = a.w.run_base;
   r.run_cnt = a.w.run_cnt;
   r.run_pos = a.w.run_pos;
-  for (int b = 0; b < 2; ++b) r.pay[b] = a.w.pay[b];
+  for (int b = 0; b < 2; ++b) {
+    r.pay[b] = a.w.pay[b];
+    r.key[b] = a.w.key[b];
+  }
   r.bsum = a.w.scan_bsum;
+  r.run_head = a.w.run_head;
   const uint32_t nblk = rscan_blocks(cap);
   hipLaunchKernelGGL(k_rscan_part, dim3(nblk), dim3(256), 0, s, r);
   hipError_t e = hipGetLastError();
@@ -742,18 +762,30 @@ struct RunScatterArgs {
   uint64_t* counters;
   const uint8_t* region_class;
   uint32_t K, G, shift;
+  // for the tile sums: which runs start their context
+  const uint32_t* run_cnt;
+  const uint8_t* run_head;
 };
 
 // Every valid record to its run's position plus its rank among the run's
 // valid records, packed as in the radix path (key (ctx - ctx_min) << ts_bits
 // | (ts - ts_min), payload region | (kind - 1) << 16 | class << 24).  One
-// wave per chunk, as in the ingest.
+// wave per chunk, as in the ingest.  For the tile sums it also marks the
+// first record of each context in its payload (kPayStart) and checks that
+// the valid records of a context in the chunk are in time order
+// (k_runs_check checks where runs meet).
 __global__ __launch_bounds__(256) void k_runs_scatter(RunScatterArgs a) {
   DevPlan* p = a.plan;
   if (!p->runs) return;
   __shared__ uint8_t s_cls[kClsLds];
-  __shared__ uint32_t s_roff[4][kChunk];  // per wave: first position of each run minus its head's rank
+  // per wave and run of the chunk: first position minus its head's rank,
+  // first position, valid records | starts its context << 31
+  __shared__ uint32_t s_roff[4][kChunk], s_rpos[4][kChunk], s_rcnt[4][kChunk];
+  // per wave and chunk position: timestamp and context
+  __shared__ uint64_t s_ts[4][kChunk];
+  __shared__ uint32_t s_cx[4][kChunk];
   const uint32_t wv = threadIdx.x >> 6;
+  bool bad = false;
   const bool cls_lds = a.K && a.R <= kClsLds;
   if (cls_lds)
     for (uint32_t r = threadIdx.x; r < a.R; r += 256) s_cls[r] = a.region_class[r];
@@ -796,9 +828,20 @@ __global__ __launch_bounds__(256) void k_runs_scatter(RunScatterArgs a) {
     chunk_masks(cx, inr, vl, H, V);
     // Run of each record (heads before it, inclusive) and its rank among the
     // chunk's valid records; each run head publishes its run's first
-    // position minus its own rank in the wave's LDS slots.
-    uint32_t li[kPer], vr[kPer];
+    // position minus its own rank in the wave's LDS slots.  A chunk whose
+    // in-range records are all valid (the usual case) needs no more LDS:
+    // its order check and run bounds come from neighbouring lanes.
+    uint64_t IR[kPer];
+    bool all_valid = true;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      IR[j] = __ballot(inr[j]);
+      all_valid = all_valid && V[j] == IR[j];
+    }
+    uint32_t li[kPer], vr[kPer], hflag[kPer];
+    int32_t lastv[kPer];  // last valid chunk position in earlier rows (-1: none)
     uint32_t hb = 0, vb = 0;
+    int32_t lv = -1;
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
       const uint32_t hr = hb + (uint32_t)__builtin_amdgcn_mbcnt_hi(
@@ -806,8 +849,23 @@ __global__ __launch_bounds__(256) void k_runs_scatter(RunScatterArgs a) {
       vr[j] = vb + (uint32_t)__builtin_amdgcn_mbcnt_hi(
                        (uint32_t)(V[j] >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)V[j], 0u));
       const bool head = (H[j] >> lane) & 1ull;
-      if (head) s_roff[wv][hr] = a.run_pos[rb + hr] - vr[j];
+      hflag[j] = 0;
+      if (head) {
+        const uint32_t rid = rb + hr, rp = a.run_pos[rid];
+        s_roff[wv][hr] = rp - vr[j];
+        hflag[j] = a.run_head[rid];
+        if (!all_valid) {
+          s_rpos[wv][hr] = rp;
+          s_rcnt[wv][hr] = a.run_cnt[rid] | (hflag[j] << 31);
+        }
+      }
       li[j] = hr + (head ? 1u : 0u) - 1u;
+      if (!all_valid) {
+        s_ts[wv][64 * j + lane] = (uint64_t)r[j].x | ((uint64_t)r[j].y << 32);
+        s_cx[wv][64 * j + lane] = cx[j];
+        lastv[j] = lv;
+        if (V[j]) lv = 64 * j + 63 - (int32_t)__clzll((long long)V[j]);
+      }
       hb += (uint32_t)__popcll(H[j]);
       vb += (uint32_t)__popcll(V[j]);
     }
@@ -816,27 +874,54 @@ __global__ __launch_bounds__(256) void k_runs_scatter(RunScatterArgs a) {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
+      const uint64_t ts = (uint64_t)r[j].x | ((uint64_t)r[j].y << 32);
+      bool first_v = false, starts = false;
+      if (all_valid) {
+        // previous record: the previous lane, or the last lane of the row before
+        uint64_t tp = ((uint64_t)(uint32_t)__shfl_up((int)r[j].y, 1) << 32) | (uint32_t)__shfl_up((int)r[j].x, 1);
+        if (j > 0) {
+          const int jp = j > 0 ? j - 1 : 0;
+          const uint64_t tl = ((uint64_t)(uint32_t)__shfl((int)r[jp].y, 63) << 32) |
+                              (uint32_t)__shfl((int)r[jp].x, 63);
+          if (lane == 0) tp = tl;
+        }
+        const bool h = (H[j] >> lane) & 1ull;
+        if (vl[j] && !h && tp > ts) bad = true;
+        first_v = h;
+        starts = h && hflag[j];
+      }
       if (!vl[j]) continue;
-      const uint64_t out = (uint64_t)(uint32_t)(s_roff[wv][li[j]] + vr[j]);
+      const uint32_t run = li[j];
+      const uint64_t out = (uint64_t)(uint32_t)(s_roff[wv][run] + vr[j]);
       if (out >= nv) {
         flag_internal_error(a.counters, 1024);
         continue;
       }
-      const uint64_t ts = (uint64_t)r[j].x | ((uint64_t)r[j].y << 32);
+      if (!all_valid) {
+        // the previous valid record of the chunk, if it has the same context
+        const uint64_t below = V[j] & ((1ull << lane) - 1ull);
+        const int32_t pv = below ? 64 * j + 63 - (int32_t)__clzll((long long)below) : lastv[j];
+        if (pv >= 0 && s_cx[wv][pv] == cx[j] && s_ts[wv][pv] > ts) bad = true;
+        const uint32_t rpos = s_rpos[wv][run], rc = s_rcnt[wv][run];
+        first_v = (uint32_t)out == rpos;
+        starts = first_v && (rc >> 31);
+      }
       const uint64_t rel = (uint64_t)(cx[j] - (uint32_t)ks.ctx_min);
       a.key[out] = (ks.ts_bits >= 64 ? 0ull : (rel << ks.ts_bits)) | (ts - ks.ts_min);
       const uint32_t region = r[j].w & 0xFFFFu;
       uint32_t cls = 0xFFu;
       if (swept_ctx(cx[j], a.K, a.G, a.shift)) cls = cls_lds ? s_cls[region] : a.region_class[region];
-      a.pay[out] = pack_payload(region, (r[j].w >> 16) & 0xFFu, cls);
+      a.pay[out] = pack_payload(region, (r[j].w >> 16) & 0xFFu, cls) | (starts ? kPayStart : 0u);
     }
   }
+  if (__syncthreads_or(bad) && threadIdx.x == 0) p->unsorted = 1;
   if (blockIdx.x == 0 && threadIdx.x == 0) p->rec_final = 0;
 }
 
 hipError_t launch_runs_scatter(const RunArgs& a, hipStream_t s) {
   RunScatterArgs r{a.w.plan, (const uint4*)a.rec, a.n, a.R, a.w.run_base, a.w.run_pos,
-                   a.w.key[0], a.w.pay[0], a.out.d_counters, a.region_class, a.K, a.G, a.shift};
+                   a.w.key[0], a.w.pay[0], a.out.d_counters, a.region_class, a.K, a.G, a.shift,
+                   a.w.run_cnt, a.w.run_head};
   // 1024 blocks measured fastest: fewer concurrent write streams than with
   // 2048, enough loads in flight unlike 512
   uint64_t blocks = ceil_div(a.n, 256 * 4 * 4);
@@ -888,6 +973,7 @@ struct TsumArgs {
 // the b-th contiguous run of tiles and also stores the run composed.
 __global__ __launch_bounds__(256) void k_tsum(TsumArgs a) {
   DevPlan* p = a.plan;
+  if (a.mode == 0 && p->runs) return;  // k_runs_check and k_tsum_codes instead
   if (a.mode == 0 && p->force_full) {
     if (blockIdx.x == 0 && threadIdx.x == 0) p->unsorted = 1;
     return;
@@ -1019,6 +1105,140 @@ hipError_t launch_tsum(const RunArgs& a, int mode, hipStream_t s) {
   ta.bsum = a.w.bsum;
   ta.mode = (uint32_t)mode;
   hipLaunchKernelGGL(k_tsum, dim3(tsum_blocks(a)), dim3(256), 0, s, ta);
+  return hipGetLastError();
+}
+
+// ------------------------------------------- tile sums after the run scatter
+
+struct RunCheckArgs {
+  DevPlan* plan;
+  const uint32_t* run_cnt;
+  const uint32_t* run_pos;
+  const uint64_t* key;  // sorted keys (key[0])
+};
+
+// The order check where runs meet: the first record of each run against
+// the record before it in sorted order, when both belong to one context.
+// (Inside a chunk the run scatter checks.)
+__global__ __launch_bounds__(256) void k_runs_check(RunCheckArgs a) {
+  DevPlan* p = a.plan;
+  if (!p->runs) return;
+  if (p->force_full) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) p->unsorted = 1;
+    return;
+  }
+  const uint64_t n_runs = p->n_runs;
+  const uint32_t tb = p->rec.ts_bits;
+  bool bad = false;
+  const uint64_t stride = (uint64_t)gridDim.x * 256;
+  for (uint64_t r = (uint64_t)blockIdx.x * 256 + threadIdx.x; r < n_runs; r += stride) {
+    const uint32_t pos = a.run_pos[r];
+    if (a.run_cnt[r] == 0 || pos == 0) continue;
+    const uint64_t k0 = a.key[pos - 1], k1 = a.key[pos];
+    // same context (key bits above ts_bits) and time going back
+    if ((tb >= 64 || (k0 >> tb) == (k1 >> tb)) && k0 > k1) bad = true;
+  }
+  if (__syncthreads_or(bad) && threadIdx.x == 0) p->unsorted = 1;
+}
+
+hipError_t launch_runs_check(const RunArgs& a, hipStream_t s) {
+  RunCheckArgs r{a.w.plan, a.w.run_cnt, a.w.run_pos, a.w.key[0]};
+  uint64_t blocks = ceil_div(a.w.run_cap, 256);
+  if (blocks > 1024) blocks = 1024;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_runs_check, dim3((uint32_t)blocks), dim3(256), 0, s, r);
+  return hipGetLastError();
+}
+
+struct TsumCodeArgs {
+  const DevPlan* plan;
+  const uint32_t* pay;  // payloads of the sorted records (pay[0])
+  uint64_t* tsum;
+  BlockSum* bsum;
+};
+
+// The tile sums of k_tsum (same tiles per block, same outputs) from the
+// payloads the run scatter wrote (kind and context-start bits), without the
+// keys.  One wave per tile, the block's four waves on four consecutive
+// tiles: the wave loads the tile's payloads contiguously, keeps two bits
+// per record in LDS, and each lane then composes 32 consecutive records.
+__global__ __launch_bounds__(256, 8) void k_tsum_codes(TsumCodeArgs a) {
+  const DevPlan* p = a.plan;
+  if (!p->runs) return;
+  __shared__ Fn s_wfn[4];
+  __shared__ uint32_t s_wnb[4];
+  __shared__ __align__(8) uint8_t s_code[4][kMatchTile / 4];  // per wave: 4 records per byte
+  constexpr uint32_t kPerLane = kMatchTile / 64;  // 32
+  const uint64_t nv = p->n_valid;
+  const uint64_t tiles = ceil_div(nv, kMatchTile);
+  const uint32_t tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const uint32_t p0 = lane * kPerLane;
+  const uint64_t per = ceil_div(tiles, gridDim.x);
+  const uint64_t t0 = (uint64_t)blockIdx.x * per, t1 = t0 + per < tiles ? t0 + per : tiles;
+  Fn run = fn_id();
+  uint32_t run_nb = 0, run_nh = 0;
+  auto code_of = [](uint32_t v) -> uint32_t {
+    return (((v >> 16) & 1u) ^ 1u) | ((v & kPayStart) ? 2u : 0u);  // BEGIN | start << 1
+  };
+  for (uint64_t tq = t0; tq < t1; tq += 4) {
+    const uint64_t tile = tq + w;
+    Fn f = fn_id();
+    uint32_t nb = 0, nh = 0;
+    if (tile < t1) {
+      const uint64_t base = tile * kMatchTile;
+      const uint32_t cnt = nv - base < (uint64_t)kMatchTile ? (uint32_t)(nv - base) : (uint32_t)kMatchTile;
+#pragma unroll
+      for (int q = 0; q < (int)kPerLane / 4; ++q) {
+        const uint32_t r0 = (uint32_t)q * 256u + 4u * lane;
+        uint32_t v[4];
+        if (r0 + 4 <= cnt) {
+          const uint4 u = *(const uint4*)(a.pay + base + r0);
+          v[0] = u.x; v[1] = u.y; v[2] = u.z; v[3] = u.w;
+        } else {
+#pragma unroll
+          for (int b = 0; b < 4; ++b) v[b] = r0 + b < cnt ? a.pay[base + r0 + b] : 0u;
+        }
+        s_code[w][r0 >> 2] = (uint8_t)(code_of(v[0]) | code_of(v[1]) << 2 | code_of(v[2]) << 4 |
+                                       code_of(v[3]) << 6);
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      const uint64_t c = *(const uint64_t*)&s_code[w][p0 >> 2];
+#pragma unroll
+      for (int i = 0; i < (int)kPerLane; ++i) {
+        if (p0 + (uint32_t)i >= cnt) break;
+        const uint32_t ci = (uint32_t)(c >> (2 * i)) & 3u;
+        const bool isb = ci & 1u, head = (ci >> 1) & 1u;
+        const Fn e = head ? Fn{1u, 0, isb ? 1 : 0} : Fn{0u, isb ? 1 : -1, 0};
+        f = compose(f, e);
+        nb += isb;
+        nh += head;
+      }
+    }
+    const Fn x = wave_scan_fn(f);
+    const uint32_t nbx = (uint32_t)wave_incl_scan32((int32_t)(nb | (nh << 16)));
+    if (lane == 63) {
+      if (tile < t1) a.tsum[tile] = pack_tile_sum(x, nbx);
+      s_wfn[w] = x;
+      s_wnb[w] = nbx;
+    }
+    __syncthreads();
+    if (tid == 0) {
+      for (int q = 0; q < 4; ++q) {
+        run = compose(run, s_wfn[q]);  // identity for tiles past the run
+        run_nb += s_wnb[q] & 0xFFFFu;
+        run_nh += s_wnb[q] >> 16;
+      }
+    }
+    __syncthreads();
+  }
+  if (tid == 0) a.bsum[blockIdx.x] = BlockSum{run, run_nb, run_nh};
+}
+
+hipError_t launch_tsum_codes(const RunArgs& a, hipStream_t s) {
+  TsumCodeArgs t{a.w.plan, a.w.pay[0], a.w.tsum, a.w.bsum};
+  hipLaunchKernelGGL(k_tsum_codes, dim3(tsum_blocks(a)), dim3(256), 0, s, t);
   return hipGetLastError();
 }
 
