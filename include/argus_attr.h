@@ -217,6 +217,13 @@ const char* argus_attr_last_error(const argus_attr* h);
 int argus_attr_set_timing(argus_attr* h, int enable);
 int argus_attr_kernel_times(argus_attr* h, const char** names, float* ms, int cap);
 
+/* Restricts timing to the launches of one step (a name as reported by
+ * argus_attr_kernel_times, e.g. "match"): while a name is set, every timed
+ * `run` records one event before and one after each launch of that step
+ * only, so that the rest of the run is not slowed by events.  NULL or ""
+ * clears the filter.  Returns ARGUS_OK, or ARGUS_E_INVAL for a NULL handle. */
+int argus_attr_set_timing_filter(argus_attr* h, const char* name);
+
 #ifdef __cplusplus
 }
 #endif

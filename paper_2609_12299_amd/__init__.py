@@ -11,7 +11,8 @@ from .attr import (ABI_VERSION, COUNTER_NAMES, FORCE_EVENT_SORT, FORCE_FULL_SORT
                    OUT_INSTANCE_EXCL, OUT_INSTANCES, RS_WIDTH, ArgusError, RegionAttribution,
                    argus_attr_config, argus_attr_create, argus_attr_destroy,
                    argus_attr_kernel_times, argus_attr_last_error, argus_attr_outputs,
-                   argus_attr_run, argus_attr_set_timing, argus_attr_workspace_bytes,
+                   argus_attr_run, argus_attr_set_timing, argus_attr_set_timing_filter,
+                   argus_attr_workspace_bytes,
                    load_library, to_host)
 
 __all__ = [
@@ -20,5 +21,6 @@ __all__ = [
     "OUT_INSTANCE_EXCL", "OUT_INSTANCES", "RS_WIDTH", "ArgusError", "RegionAttribution",
     "argus_attr_config", "argus_attr_create", "argus_attr_destroy", "argus_attr_kernel_times",
     "argus_attr_last_error", "argus_attr_outputs", "argus_attr_run", "argus_attr_set_timing",
+    "argus_attr_set_timing_filter",
     "argus_attr_workspace_bytes", "load_library", "to_host",
 ]

@@ -82,6 +82,8 @@ def load_library(path: str = LIB_PATH):
     lib.argus_attr_kernel_times.argtypes = [vp, ctypes.POINTER(ctypes.c_char_p),
                                             ctypes.POINTER(ctypes.c_float), i32]
     lib.argus_attr_kernel_times.restype = i32
+    lib.argus_attr_set_timing_filter.argtypes = [vp, ctypes.c_char_p]
+    lib.argus_attr_set_timing_filter.restype = i32
     _lib = lib
     return lib
 
@@ -116,6 +118,10 @@ def argus_attr_last_error(h) -> str:
 
 def argus_attr_set_timing(h, enable: bool) -> int:
     return load_library().argus_attr_set_timing(h, 1 if enable else 0)
+
+
+def argus_attr_set_timing_filter(h, name) -> int:
+    return load_library().argus_attr_set_timing_filter(h, name.encode() if name else None)
 
 
 def argus_attr_kernel_times(h, cap: int = 1 << 16):
@@ -256,6 +262,12 @@ class RegionAttribution:
 
     def set_timing(self, on: bool):
         rc = argus_attr_set_timing(self.h, on)
+        if rc != 0:
+            raise ArgusError(rc, argus_attr_last_error(self.h))
+
+    def set_timing_filter(self, name):
+        """Time only the launches of one step (None: every launch)."""
+        rc = argus_attr_set_timing_filter(self.h, name)
         if rc != 0:
             raise ArgusError(rc, argus_attr_last_error(self.h))
 

@@ -16,10 +16,13 @@ struct argus_attr {
   std::string err;
   int device_checked = -1;  // device ordinal verified to be gfx950
   bool timing = false;
-  // Timing: for every timed run, a start event and one event per launch.
+  std::string filter;  // time only the launches of this step ("": all)
+  // Timing: for every timed run, a start event and one event per launch, or
+  // (filter set) an event before and one after each matching launch.
   struct TimedRun {
     std::vector<hipEvent_t> ev;
     std::vector<const char*> names;
+    bool pairs = false;
   };
   std::vector<TimedRun> runs;
   std::vector<hipEvent_t> pool;  // recycled events
@@ -197,6 +200,12 @@ int argus_attr_set_timing(argus_attr* h, int enable) {
   return ARGUS_OK;
 }
 
+int argus_attr_set_timing_filter(argus_attr* h, const char* name) {
+  if (!h) return ARGUS_E_INVAL;
+  h->filter = name ? name : "";
+  return ARGUS_OK;
+}
+
 int argus_attr_kernel_times(argus_attr* h, const char** names, float* ms, int cap) {
   if (!h) return ARGUS_E_INVAL;
   int total = 0, k = 0;
@@ -204,10 +213,13 @@ int argus_attr_kernel_times(argus_attr* h, const char** names, float* ms, int ca
     if (r.ev.size() < 2) continue;
     if (hipEventSynchronize(r.ev.back()) != hipSuccess)
       return fail(h, ARGUS_E_HIP, "%s", "hipEventSynchronize failed");
-    for (size_t j = 0; j + 1 < r.ev.size(); ++j, ++total) {
+    // launch j spans events (j, j + 1), or (2j, 2j + 1) when recorded in pairs
+    const size_t nl = r.pairs ? r.ev.size() / 2 : r.ev.size() - 1;
+    for (size_t j = 0; j < nl; ++j, ++total) {
       if (k >= cap) continue;
+      const size_t e0 = r.pairs ? 2 * j : j;
       float t = 0;
-      if (hipEventElapsedTime(&t, r.ev[j], r.ev[j + 1]) != hipSuccess)
+      if (hipEventElapsedTime(&t, r.ev[e0], r.ev[e0 + 1]) != hipSuccess)
         return fail(h, ARGUS_E_HIP, "%s", "hipEventElapsedTime failed");
       if (names) names[k] = r.names[j];
       if (ms) ms[k] = t;
@@ -337,68 +349,78 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
   if (h->timing) {
     h->runs.emplace_back();
     tr = &h->runs.back();
-    hipEvent_t e;
-    if (!new_event(&e) || hipEventRecord(e, s) != hipSuccess)
-      return fail(h, ARGUS_E_HIP, "%s", "timing event failed");
-    tr->ev.push_back(e);
+    tr->pairs = !h->filter.empty();
+    if (!tr->pairs) {
+      hipEvent_t e;
+      if (!new_event(&e) || hipEventRecord(e, s) != hipSuccess)
+        return fail(h, ARGUS_E_HIP, "%s", "timing event failed");
+      tr->ev.push_back(e);
+    }
   }
-  auto step = [&](const char* name, hipError_t e) -> bool {
+  auto record = [&]() -> bool {
+    hipEvent_t ev;
+    if (!new_event(&ev) || hipEventRecord(ev, s) != hipSuccess) return false;
+    tr->ev.push_back(ev);
+    return true;
+  };
+  auto step = [&](const char* name, auto&& launch) -> bool {
+    const bool timed = tr && (!tr->pairs || h->filter == name);
+    if (timed && tr->pairs && !record()) return false;  // before the launch
+    hipError_t e = launch();
     if (e == hipSuccess) e = hipGetLastError();
     if (e != hipSuccess) {
       fail(h, ARGUS_E_HIP, "launch failed: %s", name);
       h->err += std::string(" (") + hipGetErrorString(e) + ")";
       return false;
     }
-    if (tr) {
-      hipEvent_t ev;
-      if (!new_event(&ev) || hipEventRecord(ev, s) != hipSuccess) return false;
-      tr->ev.push_back(ev);
+    if (timed) {
+      if (!record()) return false;
       tr->names.push_back(name);
     }
     return true;
   };
 
-  if (!step("init", launch_init(a, s))) return ARGUS_E_HIP;
+  if (!step("init", [&] { return launch_init(a, s); })) return ARGUS_E_HIP;
   if (n == 0) return ARGUS_OK;
-  if (!step("ingest", launch_ingest(a, s))) return ARGUS_E_HIP;
-  if (!step("plan", launch_plan(a, s))) return ARGUS_E_HIP;
+  if (!step("ingest", [&] { return launch_ingest(a, s); })) return ARGUS_E_HIP;
+  if (!step("plan", [&] { return launch_plan(a, s); })) return ARGUS_E_HIP;
   static const char* rnames[kSlots] = {
       "radix_ctx0", "radix_ctx1", "radix_ctx2", "radix_ctx3", "radix_ts0", "radix_ts1",
       "radix_ts2", "radix_ts3", "radix_ts4", "radix_ts5", "radix_ts6", "radix_ts7",
       "radix_ctx0b", "radix_ctx1b", "radix_ctx2b", "radix_ctx3b"};
   // context sort over runs (each launch returns at once on the radix path)
-  if (!step("runs_base", launch_runs_base(a, s))) return ARGUS_E_HIP;
-  if (!step("runs_compact", launch_runs_compact(a, s))) return ARGUS_E_HIP;
-  if (!step("runs_plan", launch_runs_plan(a, s))) return ARGUS_E_HIP;
+  if (!step("runs_base", [&] { return launch_runs_base(a, s); })) return ARGUS_E_HIP;
+  if (!step("runs_compact", [&] { return launch_runs_compact(a, s); })) return ARGUS_E_HIP;
+  if (!step("runs_plan", [&] { return launch_runs_plan(a, s); })) return ARGUS_E_HIP;
   for (int sl = 0; sl < kPhase2Slot; ++sl)
-    if (!step(rnames[sl], launch_radix_pass(a, 0, sl, n, s))) return ARGUS_E_HIP;
-  if (!step("runs_pos", launch_runs_pos(a, s))) return ARGUS_E_HIP;
-  if (!step("runs_scatter", launch_runs_scatter(a, s))) return ARGUS_E_HIP;
-  if (!step("tile_sums", launch_tsum(a, 0, s))) return ARGUS_E_HIP;
-  if (!step("runs_check", launch_runs_check(a, s))) return ARGUS_E_HIP;
-  if (!step("tile_sums_runs", launch_tsum_codes(a, s))) return ARGUS_E_HIP;
-  if (!step("ts_hist", launch_ts_hist(a, s))) return ARGUS_E_HIP;
-  if (!step("lb_clear", launch_lb_clear(a, s))) return ARGUS_E_HIP;
-  if (!step("plan2", launch_plan2(a, s))) return ARGUS_E_HIP;
+    if (!step(rnames[sl], [&] { return launch_radix_pass(a, 0, sl, n, s); })) return ARGUS_E_HIP;
+  if (!step("runs_pos", [&] { return launch_runs_pos(a, s); })) return ARGUS_E_HIP;
+  if (!step("runs_scatter", [&] { return launch_runs_scatter(a, s); })) return ARGUS_E_HIP;
+  if (!step("tile_sums", [&] { return launch_tsum(a, 0, s); })) return ARGUS_E_HIP;
+  if (!step("runs_check", [&] { return launch_runs_check(a, s); })) return ARGUS_E_HIP;
+  if (!step("tile_sums_runs", [&] { return launch_tsum_codes(a, s); })) return ARGUS_E_HIP;
+  if (!step("ts_hist", [&] { return launch_ts_hist(a, s); })) return ARGUS_E_HIP;
+  if (!step("lb_clear", [&] { return launch_lb_clear(a, s); })) return ARGUS_E_HIP;
+  if (!step("plan2", [&] { return launch_plan2(a, s); })) return ARGUS_E_HIP;
   for (int sl = kPhase2Slot; sl < kSlots; ++sl)
-    if (!step(rnames[sl], launch_radix_pass(a, 0, sl, n, s))) return ARGUS_E_HIP;
-  if (!step("tile_sums_full", launch_tsum(a, 1, s))) return ARGUS_E_HIP;
-  if (!step("tile_scan", launch_mscan(a, s))) return ARGUS_E_HIP;
-  if (!step("match", launch_match(a, s))) return ARGUS_E_HIP;
-  if (!step("tree", launch_tree(a, s))) return ARGUS_E_HIP;
-  if (!step("resolve", launch_resolve(a, s))) return ARGUS_E_HIP;
-  if (a.K > 0 && !step("merge_plan", launch_mplan(a, s))) return ARGUS_E_HIP;
-  if (!step("agg", launch_agg(a, s))) return ARGUS_E_HIP;
-  if (!step("hist", launch_hist(a, s))) return ARGUS_E_HIP;
+    if (!step(rnames[sl], [&] { return launch_radix_pass(a, 0, sl, n, s); })) return ARGUS_E_HIP;
+  if (!step("tile_sums_full", [&] { return launch_tsum(a, 1, s); })) return ARGUS_E_HIP;
+  if (!step("tile_scan", [&] { return launch_mscan(a, s); })) return ARGUS_E_HIP;
+  if (!step("match", [&] { return launch_match(a, s); })) return ARGUS_E_HIP;
+  if (!step("tree", [&] { return launch_tree(a, s); })) return ARGUS_E_HIP;
+  if (!step("resolve", [&] { return launch_resolve(a, s); })) return ARGUS_E_HIP;
+  if (a.K > 0 && !step("merge_plan", [&] { return launch_mplan(a, s); })) return ARGUS_E_HIP;
+  if (!step("agg", [&] { return launch_agg(a, s); })) return ARGUS_E_HIP;
+  if (!step("hist", [&] { return launch_hist(a, s); })) return ARGUS_E_HIP;
   if (a.K > 0) {
     static const char* enames[kSlots] = {
         "ev_radix_ts0", "ev_radix_ts1", "ev_radix_ts2", "ev_radix_ts3", "ev_radix_ts4",
         "ev_radix_ts5", "ev_radix_ts6", "ev_radix_ts7", "ev_radix_g0", "ev_radix_g1",
         "ev_radix_g2", "ev_radix_g3", "ev_unused12", "ev_unused13", "ev_unused14", "ev_unused15"};
-    if (!step("ev_plan", launch_ev_plan(a, s))) return ARGUS_E_HIP;
-    if (!step("ev_clear", launch_ev_clear(a, s))) return ARGUS_E_HIP;
+    if (!step("ev_plan", [&] { return launch_ev_plan(a, s); })) return ARGUS_E_HIP;
+    if (!step("ev_clear", [&] { return launch_ev_clear(a, s); })) return ARGUS_E_HIP;
     for (int sl = 0; sl < 12; ++sl)
-      if (!step(enames[sl], launch_radix_pass(a, 1, sl, 2 * n, s))) return ARGUS_E_HIP;
+      if (!step(enames[sl], [&] { return launch_radix_pass(a, 1, sl, 2 * n, s); })) return ARGUS_E_HIP;
     // Merge rounds (device-planned; a round beyond the plan returns at once).
     // The last round is merged and swept by one kernel; there is always at
     // least one round (a group of one context is a run by itself).
@@ -407,14 +429,14 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
         {"mpart4", "merge4"}, {"mpart5", "merge5"}, {"mpart6", "merge6"}, {"mpart7", "merge7"}};
     int rounds = a.shift < (uint32_t)kMaxMergeRounds ? (int)a.shift : kMaxMergeRounds;
     if (rounds < 1) rounds = 1;
-    if (!step("mseg", launch_mseg(a, rounds, s))) return ARGUS_E_HIP;
+    if (!step("mseg", [&] { return launch_mseg(a, rounds, s); })) return ARGUS_E_HIP;
     for (int r = 0; r < rounds; ++r) {
-      if (!step(mnames[r][0], launch_mpart(a, r, s))) return ARGUS_E_HIP;
-      if (r + 1 < rounds && !step(mnames[r][1], launch_merge(a, r, s))) return ARGUS_E_HIP;
+      if (!step(mnames[r][0], [&] { return launch_mpart(a, r, s); })) return ARGUS_E_HIP;
+      if (r + 1 < rounds && !step(mnames[r][1], [&] { return launch_merge(a, r, s); })) return ARGUS_E_HIP;
     }
-    if (!step("merge_sweep", launch_merge_sweep(a, s))) return ARGUS_E_HIP;
-    if (!step("sweep", launch_sweep(a, s))) return ARGUS_E_HIP;
-    if (!step("ov_final", launch_ov_final(a, s))) return ARGUS_E_HIP;
+    if (!step("merge_sweep", [&] { return launch_merge_sweep(a, s); })) return ARGUS_E_HIP;
+    if (!step("sweep", [&] { return launch_sweep(a, s); })) return ARGUS_E_HIP;
+    if (!step("ov_final", [&] { return launch_ov_final(a, s); })) return ARGUS_E_HIP;
   }
   return ARGUS_OK;
 }

@@ -409,3 +409,39 @@ def test_many_regions(oracle_mod, R, sort):
     p = dict(num_regions=R, num_classes=4, region_class=cls, group_shift=2, num_groups=5)
     log(f"[gpu] many regions R={R} sort={sort} n={len(rec)}")
     assert_parity(gpu_run(rec, p, force_radix=sort == "radix"), oracle_run(oracle_mod, rec, p))
+
+
+def test_timing_filter(oracle_mod, tracegen_mod):
+    """Per-launch timing: every launch without a filter, only the named
+    step's launches with one; results unchanged either way."""
+    import torch
+
+    from paper_2609_12299_amd import RegionAttribution, to_host
+    d = tracegen_mod.generate(1, size=1 << 14, threads=2)
+    p = {k: d[k] for k in ("num_regions", "num_classes", "region_class", "group_shift", "num_groups")}
+    rec_u8 = d["records"]
+    n = rec_u8.shape[0]
+    ra = RegionAttribution(p["num_regions"], p["num_classes"], p["region_class"], p["group_shift"],
+                           p["num_groups"], max_records=n, instances=True, instance_excl=True)
+    rec = torch.from_numpy(np.ascontiguousarray(rec_u8).reshape(-1)).to("cuda")
+    log("[gpu] timing filter")
+    try:
+        ra.set_timing(True)
+        ra.run(rec)
+        all_times = ra.kernel_times()
+        names = [k for k, _ in all_times]
+        assert "match" in names and "agg" in names and len(names) > 10
+        assert all(ms >= 0.0 for _, ms in all_times)
+        ra.set_timing_filter("match")
+        out = ra.run(rec)
+        out2 = ra.run(rec)
+        torch.cuda.synchronize()
+        only = ra.kernel_times()
+        assert [k for k, _ in only] == ["match", "match"]
+        assert all(ms > 0.0 for _, ms in only)
+        ra.set_timing_filter(None)
+        ra.set_timing(False)
+        assert_parity(to_host(out), oracle_run(oracle_mod, rec_u8, p), what="filtered timing")
+        assert_parity(to_host(out2), oracle_run(oracle_mod, rec_u8, p), what="filtered timing, second run")
+    finally:
+        ra.close()
