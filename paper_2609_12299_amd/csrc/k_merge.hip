@@ -617,10 +617,18 @@ __device__ __forceinline__ uint64_t wave_sum64(uint64_t v) {
   return v;
 }
 
+// The sums of a tile are taken by its first kMsThreads threads, each over
+// kMsItems consecutive events: fewer, longer sequential runs mean fewer
+// per-thread partial sums to reduce across the block.
+constexpr int kMsThreads = 256;
+constexpr int kMsItems = kMergeTile / kMsThreads;
+static_assert(kMsThreads % 64 == 0 && kMsThreads <= kMergeThreads, "sweep threads");
+static_assert(1 + 8 + 8 * 9 < kMsThreads - 1, "one thread per sum, and one for the header");
+
 // LDS of one block of the last round.
 template <int KC>
 struct MsShared {
-  static constexpr int NW = kMergeThreads / 64;
+  static constexpr int NW = kMsThreads / 64;
   static constexpr int NV = 1 + KC + KC * (KC + 1);  // S0, S1', S2', T
   int32_t wd[NW][KC];
   int32_t wm[NW][KC];
@@ -664,8 +672,9 @@ __device__ __forceinline__ bool tile_sums(const uint64_t* se, uint32_t cnt, bool
   constexpr int NW = MsShared<KC>::NW;
   constexpr int NV = MsShared<KC>::NV;
   const uint32_t t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const uint32_t d = t * kMergeItems;
-  const uint32_t nval = d < cnt ? (cnt - d < (uint32_t)kMergeItems ? cnt - d : (uint32_t)kMergeItems) : 0u;
+  const bool sweeper = t < (uint32_t)kMsThreads;
+  const uint32_t d = t * kMsItems;
+  const uint32_t nval = sweeper && d < cnt ? (cnt - d < (uint32_t)kMsItems ? cnt - d : (uint32_t)kMsItems) : 0u;
   const uint64_t first_w = se[0];
   const bool has_next = ss.has_next != 0;
   const uint64_t last_w = has_next ? ss.next : se[lpad(cnt - 1)];
@@ -675,66 +684,56 @@ __device__ __forceinline__ bool tile_sums(const uint64_t* se, uint32_t cnt, bool
     if (t == 0) rec[0] = head | (1ull << 33);
     return false;
   }
-  // ---- class-count deltas of the thread's events, scanned over the block
-  int32_t dd[KC], inc[KC];
+  // ---- class-count deltas of the thread's events and the lowest running
+  // count after each of them relative to the thread's start, then the
+  // deltas scanned over the block
+  int32_t dd[KC], lmin[KC], pre[KC], agg[KC], mn[KC];
 #pragma unroll
-  for (int x = 0; x < KC; ++x) dd[x] = 0;
+  for (int x = 0; x < KC; ++x) {
+    dd[x] = 0;
+    lmin[x] = 0x7FFFFFFF;
+  }
 #pragma unroll 2
   for (uint32_t j = 0; j < nval; ++j) {
     const uint32_t code = (uint32_t)(se[lpad(d + j)] & ((1u << kEvCodeBits) - 1u));
     const uint32_t cls = (code - 1u) >> 1;
     const int32_t sg = 1 - 2 * (int32_t)((code - 1u) & 1u);
 #pragma unroll
-    for (int x = 0; x < KC; ++x) dd[x] += cls == (uint32_t)x ? sg : 0;
+    for (int x = 0; x < KC; ++x) {
+      dd[x] += cls == (uint32_t)x ? sg : 0;
+      lmin[x] = dd[x] < lmin[x] ? dd[x] : lmin[x];
+    }
   }
+  if (sweeper) {
 #pragma unroll
-  for (int x = 0; x < KC; ++x) inc[x] = wave_incl_scan32(dd[x]);
-  if (lane == 63) {
-#pragma unroll
-    for (int x = 0; x < KC; ++x) ss.wd[w][x] = inc[x];
+    for (int x = 0; x < KC; ++x) {
+      const int32_t inc = wave_incl_scan32(dd[x]);
+      pre[x] = inc - dd[x];
+      if (lane == 63) ss.wd[w][x] = inc;
+    }
   }
   __syncthreads();
-  int32_t pre[KC], agg[KC], mn[KC];
-#pragma unroll
-  for (int x = 0; x < KC; ++x) {
-    pre[x] = inc[x] - dd[x];
-    agg[x] = 0;
-  }
-#pragma unroll
-  for (int q = 0; q < NW; ++q) {
+  if (sweeper) {
+    // ---- tile minima of the local counts (after each event)
 #pragma unroll
     for (int x = 0; x < KC; ++x) {
-      const int32_t v2 = ss.wd[q][x];
-      pre[x] += q < (int)w ? v2 : 0;
-      agg[x] += v2;
-    }
-  }
-  // ---- tile minima of the local counts (after each event)
-  {
-    int32_t l[KC];
+      agg[x] = 0;
 #pragma unroll
-    for (int x = 0; x < KC; ++x) {
-      l[x] = pre[x];
-      mn[x] = 0x7FFFFFFF;
-    }
-#pragma unroll 2
-    for (uint32_t j = 0; j < nval; ++j) {
-      const uint32_t code = (uint32_t)(se[lpad(d + j)] & ((1u << kEvCodeBits) - 1u));
-      const uint32_t cls = (code - 1u) >> 1;
-      const int32_t sg = 1 - 2 * (int32_t)((code - 1u) & 1u);
-#pragma unroll
-      for (int x = 0; x < KC; ++x) {
-        l[x] += cls == (uint32_t)x ? sg : 0;
-        mn[x] = l[x] < mn[x] ? l[x] : mn[x];
+      for (int q = 0; q < NW; ++q) {
+        const int32_t v2 = ss.wd[q][x];
+        pre[x] += q < (int)w ? v2 : 0;
+        agg[x] += v2;
       }
-    }
-#pragma unroll
-    for (int x = 0; x < KC; ++x) {
-      const int32_t m = rows_min32(row_min32(mn[x]));
+      const int32_t m0 = nval ? pre[x] + lmin[x] : 0x7FFFFFFF;
+      const int32_t m = rows_min32(row_min32(m0));
       if (lane == 0) ss.wm[w][x] = m;
     }
   }
   __syncthreads();
+  if (!sweeper) {
+    __syncthreads();
+    return true;
+  }
   uint32_t lp[KC], mp[KC];
 #pragma unroll
   for (int x = 0; x < KC; ++x) {
@@ -746,8 +745,8 @@ __device__ __forceinline__ bool tile_sums(const uint64_t* se, uint32_t cnt, bool
     mp[x] = (uint32_t)(m + kLBias);
   }
   // ---- sums over this thread's gaps
-  const bool has_after = d + kMergeItems < cnt || has_next;
-  const uint64_t after = d + kMergeItems < cnt ? se[lpad(d + kMergeItems)] : ss.next;
+  const bool has_after = d + kMsItems < cnt || has_next;
+  const uint64_t after = d + kMsItems < cnt ? se[lpad(d + kMsItems)] : ss.next;
   using UT = typename std::conditional<WIDE, uint64_t, uint32_t>::type;
   UT tt[1 + NP];
   uint64_t s1[KC], s2[NP];
@@ -784,11 +783,10 @@ __device__ __forceinline__ bool tile_sums(const uint64_t* se, uint32_t cnt, bool
 #pragma unroll
     for (int q = 0; q < NW; ++q) sum += ss.red[t][q];
     rec[1 + KC + t] = sum;
-  } else if (t >= 256 && t < 256u + KC) {
-    const int x = (int)t - 256;
-    rec[1 + x] = (uint64_t)(uint32_t)agg[x] | ((uint64_t)(uint32_t)mn[x] << 32);
-  } else if (t == 384) {
+  } else if (t == (uint32_t)kMsThreads - 1) {
     rec[0] = head;
+#pragma unroll
+    for (int x = 0; x < KC; ++x) rec[1 + x] = (uint64_t)(uint32_t)agg[x] | ((uint64_t)(uint32_t)mn[x] << 32);
   }
   return true;
 }
