@@ -367,6 +367,61 @@ ARGUS_DEV int32_t rows_min32(int32_t v) {
   return a < c ? a : c;
 }
 
+// Wave sums of many 64-bit values at once, by halving: at each of five
+// levels the lanes pair up across a distance (32, 16, 8, 4, 2), each pair of
+// values becomes one whose sum runs over both lanes, and each lane keeps the
+// half selected by its bit of that distance; a last step adds lanes 2k and
+// 2k + 1.  Lane l then holds the total of value bitrev5(l >> 1) (five bits).
+// The distances 32 and 16 use the gfx950 lane-half swaps, the others DPP.
+constexpr int kDppRowRor8 = 0x128;  // row_ror:8 (lane i ^ 8 inside a row)
+ARGUS_DEV uint64_t join64(uint32_t lo, uint32_t hi) { return (uint64_t)lo | ((uint64_t)hi << 32); }
+template <int N, bool HALF32>
+ARGUS_DEV void sums_level_swap(const uint64_t (&a)[N], uint64_t (&o)[(N + 1) / 2]) {
+#pragma unroll
+  for (int k = 0; k < (N + 1) / 2; ++k) {
+    const uint64_t x = a[2 * k], y = 2 * k + 1 < N ? a[2 * k + 1] : 0ull;
+    const uint32_t xl = (uint32_t)x, xh = (uint32_t)(x >> 32), yl = (uint32_t)y, yh = (uint32_t)(y >> 32);
+    if constexpr (HALF32) {
+      // lanes 32..63 of x trade places with lanes 0..31 of y
+      const auto l = __builtin_amdgcn_permlane32_swap(xl, yl, false, false);
+      const auto h = __builtin_amdgcn_permlane32_swap(xh, yh, false, false);
+      o[k] = join64(l[0], h[0]) + join64(l[1], h[1]);
+    } else {
+      // the odd rows of x trade places with the even rows of y
+      const auto l = __builtin_amdgcn_permlane16_swap(xl, yl, false, false);
+      const auto h = __builtin_amdgcn_permlane16_swap(xh, yh, false, false);
+      o[k] = join64(l[0], h[0]) + join64(l[1], h[1]);
+    }
+  }
+}
+template <int N, int CTRL>
+ARGUS_DEV void sums_level_dpp(const uint64_t (&a)[N], uint64_t (&o)[(N + 1) / 2], bool odd) {
+#pragma unroll
+  for (int k = 0; k < (N + 1) / 2; ++k) {
+    const uint64_t x = a[2 * k], y = 2 * k + 1 < N ? a[2 * k + 1] : 0ull;
+    const uint64_t keep = odd ? y : x, send = odd ? x : y;
+    o[k] = keep + join64(dpp32<CTRL>((uint32_t)send), dpp32<CTRL>((uint32_t)(send >> 32)));
+  }
+}
+template <int V>
+ARGUS_DEV uint64_t wave_sums64(const uint64_t (&v)[V], uint32_t* idx) {
+  static_assert(V >= 1 && V <= 32, "at most 32 values");
+  constexpr int N1 = (V + 1) / 2, N2 = (N1 + 1) / 2, N3 = (N2 + 1) / 2, N4 = (N3 + 1) / 2;
+  constexpr int N5 = (N4 + 1) / 2;
+  const uint32_t lane = __lane_id();
+  uint64_t a1[N1], a2[N2], a3[N3], a4[N4], a5[N5];
+  sums_level_swap<V, true>(v, a1);
+  sums_level_swap<N1, false>(a1, a2);
+  sums_level_dpp<N2, kDppRowRor8>(a2, a3, (lane >> 3) & 1u);
+  sums_level_dpp<N3, kDppHalfMirror>(a3, a4, (lane >> 2) & 1u);  // partner 7 - i: bit 2 differs
+  sums_level_dpp<N4, kDppQuad2301>(a4, a5, (lane >> 1) & 1u);
+  uint64_t r = a5[0];
+  r += join64(dpp32<kDppQuad1032>((uint32_t)r), dpp32<kDppQuad1032>((uint32_t)(r >> 32)));
+  *idx = ((lane >> 1) & 1u) << 4 | ((lane >> 2) & 1u) << 3 | ((lane >> 3) & 1u) << 2 |
+         ((lane >> 4) & 1u) << 1 | ((lane >> 5) & 1u);
+  return r;
+}
+
 // Inclusive prefix sum over the 64 lanes of the wave.
 ARGUS_DEV int32_t wave_incl_scan32(int32_t v) {
   v += (int32_t)dpp32<kDppRowShr + 1>((uint32_t)v);

@@ -757,9 +757,22 @@ __device__ __forceinline__ bool tile_sums(const uint64_t* se, uint32_t cnt, bool
 #pragma unroll
   for (int x = 0; x < NP; ++x) s2[x] = 0;
   if (nval) sweep8<KC, !WIDE>(se, d, nval, after, has_after, lp, mp, tt, s1, s2);
-  // ---- tile totals: waves in registers (rows of 16 lanes, then the four
-  // row results as scalars), then across waves in LDS
-  {
+  // ---- tile totals: waves in registers, then across waves in LDS
+  if constexpr (NV <= 32) {
+    uint64_t vals[NV];
+    vals[0] = (uint64_t)tt[0];
+#pragma unroll
+    for (int x = 0; x < KC; ++x) vals[1 + x] = s1[x];
+#pragma unroll
+    for (int x = 0; x < NP; ++x) {
+      vals[1 + KC + x] = s2[x];
+      vals[1 + KC + NP + x] = (uint64_t)tt[1 + x];
+    }
+    uint32_t idx;
+    const uint64_t r = wave_sums64<NV>(vals, &idx);
+    if ((lane & 1u) == 0 && idx < (uint32_t)NV) ss.red[idx][w] = r;
+  } else {
+    // (rows of 16 lanes, then the four row results as scalars)
     int c = 0;
     // 32-bit sums stay exact per wave in the narrow case: a wave's gaps add
     // up to less than the tile's span
