@@ -561,13 +561,18 @@ __device__ __forceinline__ bool tile_next(const uint64_t* src, const MergeTask& 
 // (staged in se) followed by the word `after` (if has_after).  lp: biased local counts l' before the first
 // event; mp: biased tile minima m'.  NARROW (the tile spans less than 2^32
 // cycles): gaps, S0, T and T2 fit 32 bits.  l' < 2^14 either way.
-template <int KC, bool NARROW>
+// BINS (narrow, at most four classes): instead of summing T and T2 per
+// event, each event adds its gap to the thread's bin of the event's set of
+// active classes (1 << KC bins in LDS at hb); T and T2 follow from the bins.
+template <int KC, bool NARROW, bool BINS>
 __device__ __forceinline__ void sweep8(const uint64_t* se, uint32_t d, uint32_t nval, uint64_t after,
                                        bool has_after, const uint32_t (&lp0)[KC],
                                        const uint32_t (&mp)[KC],
                                        typename std::conditional<NARROW, uint32_t, uint64_t>::type (&tt)[1 + KC * (KC + 1) / 2],
-                                       uint64_t (&s1)[KC], uint64_t (&s2)[KC * (KC + 1) / 2]) {
+                                       uint64_t (&s1)[KC], uint64_t (&s2)[KC * (KC + 1) / 2],
+                                       uint32_t* hb) {
   using UT = typename std::conditional<NARROW, uint32_t, uint64_t>::type;
+  static_assert(!BINS || (NARROW && KC <= 4), "bins: narrow tiles, at most four classes");
   uint32_t l[KC];
 #pragma unroll
   for (int x = 0; x < KC; ++x) l[x] = lp0[x];
@@ -603,8 +608,14 @@ __device__ __forceinline__ void sweep8(const uint64_t* se, uint32_t d, uint32_t 
       for (int y = x; y < KC; ++y, ++k) {
         const uint32_t w = x != y ? __umul24(l[x], l[y]) : (__umul24(l[x], l[x] - 1u) >> 1);
         s2[k] += (uint64_t)gap * w;
-        tt[1 + k] += (act[x] && act[y]) ? gap : (UT)0;
+        if constexpr (!BINS) tt[1 + k] += (act[x] && act[y]) ? gap : (UT)0;
       }
+    }
+    if constexpr (BINS) {
+      uint32_t m = 0;
+#pragma unroll
+      for (int x = 0; x < KC; ++x) m |= act[x] ? 1u << x : 0u;
+      atomicAdd(&hb[m], (uint32_t)gap);  // the thread's own bins: no return value needed
     }
     cur = nx;
   }
@@ -635,6 +646,10 @@ struct MsShared {
   uint64_t next;
   uint32_t has_next;
   uint64_t red[NV][NW];
+  // activity bins of each sweeping thread (17 words apart: spread over banks)
+  static constexpr bool BINS = KC <= 4;
+  static constexpr int BW = 17;
+  uint32_t bins[BINS ? kMsThreads * BW : 1];
 };
 
 // Merges the tile staged in se (run A then run B) into 8 consecutive outputs
@@ -756,7 +771,31 @@ __device__ __forceinline__ bool tile_sums(const uint64_t* se, uint32_t cnt, bool
   for (int x = 0; x < KC; ++x) s1[x] = 0;
 #pragma unroll
   for (int x = 0; x < NP; ++x) s2[x] = 0;
-  if (nval) sweep8<KC, !WIDE>(se, d, nval, after, has_after, lp, mp, tt, s1, s2);
+  constexpr bool BINS = !WIDE && MsShared<KC>::BINS;
+  uint32_t* hb = &ss.bins[BINS ? t * MsShared<KC>::BW : 0];
+  if (nval) sweep8<KC, !WIDE, BINS>(se, d, nval, after, has_after, lp, mp, tt, s1, s2, hb);
+  if constexpr (BINS) {
+    // T[x] (pair x, x) and T2[x][y] from the bins, which are cleared for the
+    // next tile
+    uint32_t h[1 << KC];
+#pragma unroll
+    for (int m = 0; m < (1 << KC); ++m) {
+      h[m] = hb[m];
+      hb[m] = 0;
+    }
+    int k = 0;
+#pragma unroll
+    for (int x = 0; x < KC; ++x) {
+#pragma unroll
+      for (int y = x; y < KC; ++y, ++k) {
+        uint32_t v = 0;
+#pragma unroll
+        for (int m = 0; m < (1 << KC); ++m)
+          if (((m >> x) & 1) && ((m >> y) & 1)) v += h[m];
+        tt[1 + k] = v;
+      }
+    }
+  }
   // ---- tile totals: waves in registers, then across waves in LDS
   if constexpr (NV <= 32) {
     uint64_t vals[NV];
@@ -820,6 +859,10 @@ __device__ __forceinline__ void merge_sweep_tiles(const MergeSweepArgs& a) {
   if (!p->ev_merge || p->m_rounds == 0) return;
   __shared__ uint64_t s_e[kMergeLds];
   __shared__ MsShared<KC> ss;
+  if constexpr (!WIDE && MsShared<KC>::BINS) {
+    if (threadIdx.x < (uint32_t)kMsThreads)
+      for (int m = 0; m < MsShared<KC>::BW; ++m) ss.bins[threadIdx.x * MsShared<KC>::BW + m] = 0;
+  }
   const MergeRound mr = p->mr[p->m_rounds - 1];
   const uint64_t n_tiles = mr.n_tiles;
   const uint32_t end = (uint32_t)p->m_end;
