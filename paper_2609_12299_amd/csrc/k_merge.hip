@@ -332,26 +332,40 @@ __global__ __launch_bounds__(256) void k_mpart(MPartArgs a) {
   const uint32_t* seg_start = a.seg_start + off;
   const uint32_t* seg_split = a.seg_split + off;
   const uint32_t* seg_tile0 = a.seg_tile0 + off;
-  for (uint64_t k = (uint64_t)blockIdx.x * 256 + threadIdx.x; k < n_tiles;
-       k += (uint64_t)gridDim.x * 256) {
+  // Lanes take consecutive tiles and every lane of a wave runs the same
+  // iterations: a tile's end split is the next tile's start split, taken
+  // from the next lane when that tile is in the same segment.
+  const uint32_t lane = threadIdx.x & 63;
+  const uint64_t step = (uint64_t)gridDim.x * 256;
+  for (uint64_t k0 = (uint64_t)blockIdx.x * 256 + (threadIdx.x & ~63u); k0 < n_tiles; k0 += step) {
+    const uint64_t k = k0 + lane;
+    const bool in = k < n_tiles;
     // segment of tile k: the last one whose first tile is <= k
     uint32_t lo = 0, hi = n_segs;
-    while (hi - lo > 1) {
+    while (in && hi - lo > 1) {
       const uint32_t mid = (lo + hi) >> 1;
       if (seg_tile0[mid] <= k) lo = mid;
       else hi = mid;
     }
-    const uint32_t s0 = seg_start[lo], sp = seg_split[lo];
-    const uint32_t s1 = lo + 1 < n_segs ? seg_start[lo + 1] : end;
+    const uint32_t s0 = in ? seg_start[lo] : 0u, sp = in ? seg_split[lo] : 0u;
+    const uint32_t s1 = !in ? 0u : lo + 1 < n_segs ? seg_start[lo + 1] : end;
+    const bool ok = in && s0 <= sp && sp <= s1 && s1 <= end;
+    const uint32_t L = s1 - s0, la = sp - s0, lb = s1 - sp;
+    const uint64_t d0w = ok ? (k - seg_tile0[lo]) * (uint64_t)kMergeTile : 0ull;
+    const uint32_t d0 = d0w < L ? (uint32_t)d0w : L;
+    const uint32_t d1 = d0 + kMergeTile < L ? d0 + kMergeTile : L;
+    const uint64_t* A = src + s0;
+    const uint64_t* B = src + sp;
+    const uint32_t a0 = ok ? corank(A, la, B, lb, d0) : 0u;
+    // the next tile starts at d1 in the same segment unless d1 == L
+    const uint32_t a0_next = (uint32_t)__shfl_down((int)a0, 1);
+    const uint32_t lo_next = (uint32_t)__shfl_down((int)lo, 1);
     MergeTask tk{0, 0, 0, 0, 0, 0, 0, 0};
-    if (s0 <= sp && sp <= s1 && s1 <= end) {
-      const uint32_t L = s1 - s0, la = sp - s0, lb = s1 - sp;
-      const uint64_t d0w = (k - seg_tile0[lo]) * (uint64_t)kMergeTile;
-      const uint32_t d0 = d0w < L ? (uint32_t)d0w : L;
-      const uint32_t d1 = d0 + kMergeTile < L ? d0 + kMergeTile : L;
-      const uint64_t* A = src + s0;
-      const uint64_t* B = src + sp;
-      const uint32_t a0 = corank(A, la, B, lb, d0), a1 = corank(A, la, B, lb, d1);
+    if (ok) {
+      uint32_t a1;
+      if (d1 == L) a1 = la;
+      else if (lane < 63 && k + 1 < n_tiles && lo_next == lo) a1 = a0_next;
+      else a1 = corank(A, la, B, lb, d1);
       tk.a_pos = s0 + a0;
       tk.na = a1 - a0;
       tk.b_pos = sp + (d0 - a0);
@@ -360,10 +374,10 @@ __global__ __launch_bounds__(256) void k_mpart(MPartArgs a) {
       tk.a_end = sp;
       tk.b_end = s1;
       tk.first = k == seg_tile0[lo] ? 1u : 0u;
-    } else {
+    } else if (in) {
       flag_internal_error(a.counters, 256);
     }
-    a.task[k] = tk;
+    if (in) a.task[k] = tk;
   }
 }
 

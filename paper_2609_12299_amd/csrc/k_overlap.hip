@@ -443,9 +443,15 @@ struct OvFinalArgs {
   uint32_t K, G, KM;
 };
 
+// The global sums are gathered per block in LDS and added once per block:
+// thousands of groups adding straight into the same few words would
+// serialise on them.
 __global__ __launch_bounds__(256) void k_ov_final(OvFinalArgs a) {
+  __shared__ unsigned long long s_g[2 * 64];
   const uint64_t KK = (uint64_t)a.K * a.K;
   const uint64_t total = (uint64_t)a.G * KK;
+  for (uint32_t i = threadIdx.x; i < 2 * KK; i += 256) s_g[i] = 0;
+  __syncthreads();
   for (uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (uint64_t)gridDim.x * 256) {
     const uint64_t g = i / KK;
     const uint32_t ab = (uint32_t)(i % KK), x = ab / a.K, y = ab % a.K;
@@ -454,16 +460,19 @@ __global__ __launch_bounds__(256) void k_ov_final(OvFinalArgs a) {
     const uint64_t u = a.ov_u[g * kSweepQWords + pi], q = a.ov_q[g * kSweepQWords + pi];
     a.og[g * 2 * KK + ab] = u;
     a.og[g * 2 * KK + KK + ab] = q;
-    if (u) atomicAdd((unsigned long long*)&a.ogl[ab], (unsigned long long)u);
-    if (q) atomicAdd((unsigned long long*)&a.ogl[KK + ab], (unsigned long long)q);
+    if (u) atomicAdd(&s_g[ab], (unsigned long long)u);
+    if (q) atomicAdd(&s_g[KK + ab], (unsigned long long)q);
   }
+  __syncthreads();
+  for (uint32_t i = threadIdx.x; i < 2 * KK; i += 256)
+    if (s_g[i]) atomicAdd((unsigned long long*)&a.ogl[i], s_g[i]);
 }
 
 hipError_t launch_ov_final(const RunArgs& a, hipStream_t s) {
   const uint32_t KM = a.K <= 2 ? 2 : (a.K <= 4 ? 4 : 8);
   OvFinalArgs f{a.w.ov_mask, a.w.ov_q, a.out.d_overlap_group, a.out.d_overlap_global, a.K, a.G, KM};
   uint64_t blocks = ceil_div((uint64_t)a.G * a.K * a.K, 256);
-  if (blocks > 4096) blocks = 4096;
+  if (blocks > 256) blocks = 256;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(k_ov_final, dim3((uint32_t)blocks), dim3(256), 0, s, f);
   return hipGetLastError();
