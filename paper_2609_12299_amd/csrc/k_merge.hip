@@ -1146,6 +1146,41 @@ __global__ __launch_bounds__(kOvtThreads) void k_ovt_final(OvtArgs a) {
       qq[k] = 0;
     }
   }
+  if constexpr (2 * NP <= 32) {
+    // Tiles of one group are adjacent: per group present in the wave, its
+    // lanes' values are summed across the wave and added once.
+    uint64_t pend = __ballot(in && g < a.G);
+    while (pend) {
+      const uint32_t gc = (uint32_t)__shfl((int)g, __ffsll((unsigned long long)pend) - 1);
+      const uint64_t mine = __ballot(g == gc) & pend;
+      pend &= ~mine;
+      const bool take = (mine >> lane) & 1ull;
+      uint64_t vals[2 * NP];
+#pragma unroll
+      for (int k = 0; k < NP; ++k) {
+        vals[k] = take ? uu[k] : 0ull;
+        vals[NP + k] = take ? qq[k] : 0ull;
+      }
+      uint32_t idx;
+      const uint64_t r = wave_sums64<2 * NP>(vals, &idx);
+      if ((lane & 1u) == 0 && idx < 2u * NP && r) {
+        // pair idx % NP in row order, at its place in a group's rows
+        const uint32_t k = idx < (uint32_t)NP ? idx : idx - NP;
+        uint32_t pi = 0;
+        int kk = 0;
+#pragma unroll
+        for (int x = 0; x < KC; ++x) {
+#pragma unroll
+          for (int y = x; y < KC; ++y, ++kk)
+            if ((uint32_t)kk == k) pi = (uint32_t)pair_index<KM>(x, y);
+        }
+        uint64_t* dst = idx < (uint32_t)NP ? a.ov_u : a.ov_q;
+        atomicAdd((unsigned long long*)&dst[(uint64_t)gc * kSweepQWords + pi], (unsigned long long)r);
+      }
+    }
+    if (in && g >= a.G && g != 0xFFFFFFFFu) flag_internal_error(a.counters, 256);
+    return;
+  }
   // whole waves of one group add once; everything else per tile
   const uint32_t g0 = __shfl(g, 0);
   const bool uniform = __ballot(g != g0) == 0ull;
