@@ -824,6 +824,14 @@ __global__ __launch_bounds__(256) void k_runs_scatter(RunScatterArgs a) {
       inr[j] = i < a.n;
       vl[j] = inr[j] && (kind == 1 || kind == 2) && (r[j].w & 0xFFFFu) < a.R;
     }
+    // the positions, context-start flags and sizes of the chunk's first 64
+    // runs, one per lane, in flight while the masks are built
+    const uint64_t n_runs = p->n_runs;
+    const uint32_t prid = rb + lane;
+    const bool pin = prid < n_runs;
+    const uint32_t pre_pos = pin ? a.run_pos[prid] : 0u;
+    const uint32_t pre_head = pin ? a.run_head[prid] : 0u;
+    const uint32_t pre_cnt = pin ? a.run_cnt[prid] : 0u;
     uint64_t H[4], V[4];
     chunk_masks(cx, inr, vl, H, V);
     // Run of each record (heads before it, inclusive) and its rank among the
@@ -849,14 +857,19 @@ __global__ __launch_bounds__(256) void k_runs_scatter(RunScatterArgs a) {
       vr[j] = vb + (uint32_t)__builtin_amdgcn_mbcnt_hi(
                        (uint32_t)(V[j] >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)V[j], 0u));
       const bool head = (H[j] >> lane) & 1ull;
+      const uint32_t sp = (uint32_t)__shfl((int)pre_pos, (int)(hr & 63u));
+      const uint32_t sh = (uint32_t)__shfl((int)pre_head, (int)(hr & 63u));
+      const uint32_t sc = (uint32_t)__shfl((int)pre_cnt, (int)(hr & 63u));
       hflag[j] = 0;
       if (head) {
-        const uint32_t rid = rb + hr, rp = a.run_pos[rid];
+        const uint32_t rid = rb + hr;
+        const bool near = hr < 64u;
+        const uint32_t rp = near ? sp : a.run_pos[rid];
         s_roff[wv][hr] = rp - vr[j];
-        hflag[j] = a.run_head[rid];
+        hflag[j] = near ? sh : a.run_head[rid];
         if (!all_valid) {
           s_rpos[wv][hr] = rp;
-          s_rcnt[wv][hr] = a.run_cnt[rid] | (hflag[j] << 31);
+          s_rcnt[wv][hr] = (near ? sc : a.run_cnt[rid]) | (hflag[j] << 31);
         }
       }
       li[j] = hr + (head ? 1u : 0u) - 1u;
