@@ -77,7 +77,9 @@ __device__ __forceinline__ void whist(uint32_t* hist, uint32_t d, bool valid) {
   if (valid) atomicAdd(&hist[d], 1u);
 }
 
-__global__ __launch_bounds__(512) void k_agg(AggArgs a) {
+// Four waves per SIMD (two blocks per compute unit): the registers and the
+// dynamic LDS of a block are sized for that.
+__global__ __launch_bounds__(512, 4) void k_agg(AggArgs a) {
   extern __shared__ __align__(16) uint8_t smem[];
   const uint32_t RL = a.lds_regions;
   uint64_t* s_isum = (uint64_t*)smem;
@@ -93,7 +95,6 @@ __global__ __launch_bounds__(512) void k_agg(AggArgs a) {
   uint32_t* s_sn = s_mae + RL;
   uint32_t* s_hist = s_sn + RL;  // [RL][130] when hist_lds
   uint32_t* s_evh = s_hist + (a.hist_lds ? RL * 130 : 0);  // [12][256] when K > 0
-  __shared__ uint64_t s_red[8][6];
   constexpr uint32_t NT = 512;
   for (uint32_t r = threadIdx.x; r < RL; r += NT) {
     s_isum[r] = 0;
@@ -131,11 +132,11 @@ __global__ __launch_bounds__(512) void k_agg(AggArgs a) {
   }
   uint64_t n_m = 0, n_mm = 0, n_u = 0, n_sn = 0, n_ev = 0, n_skip = 0;
   unsigned long long* rs = (unsigned long long*)a.rstats;
-  // Each wave takes 8 x 64 consecutive instances per step, with their loads
+  // Each wave takes 4 x 64 consecutive instances per step, with their loads
   // (and then the parents' regions) in flight together; every lane of a
   // wave iterates the same number of times (the event histograms use
   // ballots).
-  constexpr int B = 8;
+  constexpr int B = 4;
   const uint32_t lane = threadIdx.x & 63;
   const uint64_t stride = (uint64_t)gridDim.x * NT * B;
   for (uint64_t wb = ((uint64_t)blockIdx.x * (NT / 64) + (threadIdx.x >> 6)) * (64 * B); wb < nb;
@@ -263,27 +264,7 @@ __global__ __launch_bounds__(512) void k_agg(AggArgs a) {
   n_sn = wsum(n_sn);
   n_ev = wsum(n_ev);
   n_skip = wsum(n_skip);
-  const int w = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) == 0) {
-    s_red[w][0] = n_m;
-    s_red[w][1] = n_mm;
-    s_red[w][2] = n_u;
-    s_red[w][3] = n_sn;
-    s_red[w][4] = n_skip;
-    s_red[w][5] = n_ev;
-  }
-  __syncthreads();
-  if (threadIdx.x < 6) {
-    uint64_t v = 0;
-    for (int q = 0; q < (int)(NT / 64); ++q) v += s_red[q][threadIdx.x];
-    const int idx = threadIdx.x == 0   ? ARGUS_C_N_MATCHED
-                    : threadIdx.x == 1 ? ARGUS_C_N_MISMATCHED
-                    : threadIdx.x == 2 ? ARGUS_C_N_UNCLOSED
-                    : threadIdx.x == 3 ? ARGUS_C_N_SELF_NESTED
-                                       : ARGUS_C_N_OVERLAP_SKIPPED;
-    if (v && threadIdx.x < 5) atomicAdd((unsigned long long*)&a.counters[idx], (unsigned long long)v);
-    if (v && threadIdx.x == 5 && evk) atomicAdd((unsigned long long*)&a.wplan->n_ev, (unsigned long long)v);
-  }
+  __syncthreads();  // every wave's LDS adds are done
   if (evk)
     for (uint32_t i = threadIdx.x; i < kDigitPositions * kRadixBins; i += NT)
       if (s_evh[i]) atomicAdd(&a.ev_hist[i], s_evh[i]);
@@ -330,6 +311,31 @@ __global__ __launch_bounds__(512) void k_agg(AggArgs a) {
         atomicAdd(&rs[(uint64_t)r * ARGUS_RS_WIDTH + ARGUS_RS_HIST_INCL + b], (unsigned long long)h);
       }
     }
+  }
+  // the counters, per block, through the start of the (now read) LDS area
+  // (static LDS would keep two blocks from sharing a compute unit)
+  __syncthreads();
+  uint64_t* s_red = (uint64_t*)smem;  // [8][6]
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    s_red[w * 6 + 0] = n_m;
+    s_red[w * 6 + 1] = n_mm;
+    s_red[w * 6 + 2] = n_u;
+    s_red[w * 6 + 3] = n_sn;
+    s_red[w * 6 + 4] = n_skip;
+    s_red[w * 6 + 5] = n_ev;
+  }
+  __syncthreads();
+  if (threadIdx.x < 6) {
+    uint64_t v = 0;
+    for (int q = 0; q < (int)(NT / 64); ++q) v += s_red[q * 6 + threadIdx.x];
+    const int idx = threadIdx.x == 0   ? ARGUS_C_N_MATCHED
+                    : threadIdx.x == 1 ? ARGUS_C_N_MISMATCHED
+                    : threadIdx.x == 2 ? ARGUS_C_N_UNCLOSED
+                    : threadIdx.x == 3 ? ARGUS_C_N_SELF_NESTED
+                                       : ARGUS_C_N_OVERLAP_SKIPPED;
+    if (v && threadIdx.x < 5) atomicAdd((unsigned long long*)&a.counters[idx], (unsigned long long)v);
+    if (v && threadIdx.x == 5 && evk) atomicAdd((unsigned long long*)&a.wplan->n_ev, (unsigned long long)v);
   }
 }
 
@@ -399,6 +405,7 @@ hipError_t launch_agg(const RunArgs& a, hipStream_t s) {
   size_t bytes;
   agg_sizes(a.R, &rl, &hl, &bytes);
   if (a.K) bytes += sizeof(uint32_t) * kDigitPositions * kRadixBins;
+  if (bytes < 8 * 6 * sizeof(uint64_t)) bytes = 8 * 6 * sizeof(uint64_t);  // the counter sums at the end
   AggArgs g{};
   g.plan = a.w.plan;
   g.inst = a.w.inst;
