@@ -935,10 +935,10 @@ hipError_t launch_runs_scatter(const RunArgs& a, hipStream_t s) {
   RunScatterArgs r{a.w.plan, (const uint4*)a.rec, a.n, a.R, a.w.run_base, a.w.run_pos,
                    a.w.key[0], a.w.pay[0], a.out.d_counters, a.region_class, a.K, a.G, a.shift,
                    a.w.run_cnt, a.w.run_head};
-  // 1024 blocks measured fastest: fewer concurrent write streams than with
-  // 2048, enough loads in flight unlike 512
+  // 1280 blocks, five per compute unit (as many as the LDS holds), measured
+  // fastest: more loads in flight than with 1024 or fewer
   uint64_t blocks = ceil_div(a.n, 256 * 4 * 4);
-  if (blocks > 1024) blocks = 1024;
+  if (blocks > 1280) blocks = 1280;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(k_runs_scatter, dim3((uint32_t)blocks), dim3(256), 0, s, r);
   return hipGetLastError();
