@@ -935,8 +935,10 @@ __device__ __forceinline__ void merge_sweep_tiles(const MergeSweepArgs& a) {
   }
 }
 
+// Up to four classes: six waves per SIMD (three blocks per compute unit; the
+// kernel is ALU bound and the extra waves hide the LDS latency).
 template <int KC>
-__global__ __launch_bounds__(kMergeThreads) void k_merge_sweep(MergeSweepArgs a) {
+__global__ __launch_bounds__(kMergeThreads, KC <= 4 ? 6 : 1) void k_merge_sweep(MergeSweepArgs a) {
   merge_sweep_tiles<KC, false>(a);
 }
 
