@@ -307,10 +307,16 @@ constexpr int kDppMirror = 0x140;      // row_mirror
 constexpr int kDppRowShr = 0x110;      // row_shr:n is kDppRowShr + n
 constexpr int kDppBcast15 = 0x142;     // row_bcast:15
 constexpr int kDppBcast31 = 0x143;     // row_bcast:31
+constexpr int kDppWaveShr1 = 0x138;    // wave_shr:1 (whole wave, one lane up)
 
 template <int CTRL, int ROWS = 0xF>
 ARGUS_DEV uint32_t dpp32(uint32_t v) {
   return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, ROWS, 0xF, false);
+}
+
+// The value of lane i - 1 in lane i, and `first` in lane 0 (one DPP move).
+ARGUS_DEV uint32_t lane_prev(uint32_t v, uint32_t first) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)first, (int)v, kDppWaveShr1, 0xF, 0xF, false);
 }
 
 // Sum over each row of 16 lanes, in every lane of the row.

@@ -118,8 +118,9 @@ __device__ __forceinline__ void chunk_masks(const uint32_t (&ctx)[4], const bool
   const uint32_t lane = lane_id();
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    uint32_t prev = (uint32_t)__shfl_up((int)ctx[j], 1);
-    if (lane == 0) prev = j > 0 ? (uint32_t)__builtin_amdgcn_readlane((int)ctx[j > 0 ? j - 1 : 0], 63) : ctx[j];
+    // previous record: the previous lane, or the last lane of the row before
+    const uint32_t prev =
+        lane_prev(ctx[j], j > 0 ? (uint32_t)__builtin_amdgcn_readlane((int)ctx[j > 0 ? j - 1 : 0], 63) : ctx[j]);
     const bool head = in[j] && ((j == 0 && lane == 0) || prev != ctx[j]);
     H[j] = __ballot(head);
     V[j] = __ballot(valid[j]);
@@ -264,14 +265,14 @@ __global__ __launch_bounds__(256) void k_ingest(IngestArgs a) {
     if (base + stride < a.n) issue(base + stride);
     uint32_t cx[kPer];
     bool inr[kPer], vl[kPer];
+    const uint32_t rem = a.n - base < (uint64_t)kChunk ? (uint32_t)(a.n - base) : (uint32_t)kChunk;
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
-      const uint64_t i = base + (uint64_t)j * 64 + lane;
       const uint32_t kind = (r[j].w >> 16) & 0xFFu;
       const uint32_t region = r[j].w & 0xFFFFu;
       const bool kind_ok = kind == 1 || kind == 2;
       cx[j] = r[j].z;
-      inr[j] = i < a.n;
+      inr[j] = 64u * j + lane < rem;
       vl[j] = inr[j] && kind_ok && region < a.R;
       n_badk += (uint64_t)__popcll(__ballot(inr[j] && !kind_ok));
       n_badr += (uint64_t)__popcll(__ballot(inr[j] && kind_ok && region >= a.R));
@@ -816,12 +817,12 @@ __global__ __launch_bounds__(256) void k_runs_scatter(RunScatterArgs a) {
     if (base + stride < a.n) issue(base + stride);
     uint32_t cx[kPer];
     bool inr[kPer], vl[kPer];
+    const uint32_t rem = a.n - base < (uint64_t)kChunk ? (uint32_t)(a.n - base) : (uint32_t)kChunk;
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
-      const uint64_t i = base + (uint64_t)j * 64 + lane;
       const uint32_t kind = (r[j].w >> 16) & 0xFFu;
       cx[j] = r[j].z;
-      inr[j] = i < a.n;
+      inr[j] = 64u * j + lane < rem;
       vl[j] = inr[j] && (kind == 1 || kind == 2) && (r[j].w & 0xFFFFu) < a.R;
     }
     // the positions, context-start flags and sizes of the chunk's first 64
@@ -891,13 +892,11 @@ __global__ __launch_bounds__(256) void k_runs_scatter(RunScatterArgs a) {
       bool first_v = false, starts = false;
       if (all_valid) {
         // previous record: the previous lane, or the last lane of the row before
-        uint64_t tp = ((uint64_t)(uint32_t)__shfl_up((int)r[j].y, 1) << 32) | (uint32_t)__shfl_up((int)r[j].x, 1);
-        if (j > 0) {
-          const int jp = j > 0 ? j - 1 : 0;
-          const uint64_t tl = ((uint64_t)(uint32_t)__shfl((int)r[jp].y, 63) << 32) |
-                              (uint32_t)__shfl((int)r[jp].x, 63);
-          if (lane == 0) tp = tl;
-        }
+        // (lane 0 of the first row starts a run: its value is not used)
+        const int jp = j > 0 ? j - 1 : 0;
+        const uint32_t fx = (uint32_t)__builtin_amdgcn_readlane((int)r[jp].x, 63);
+        const uint32_t fy = (uint32_t)__builtin_amdgcn_readlane((int)r[jp].y, 63);
+        const uint64_t tp = ((uint64_t)lane_prev(r[j].y, fy) << 32) | lane_prev(r[j].x, fx);
         const bool h = (H[j] >> lane) & 1ull;
         if (vl[j] && !h && tp > ts) bad = true;
         first_v = h;
