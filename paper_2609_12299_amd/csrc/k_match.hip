@@ -340,8 +340,8 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
   const uint32_t thd = tnbh >> 16;      // context starts of the tile before this thread
 
   // ---- entering values of the tile (depth, BEGINs and context starts
-  // before it), from the scan over the tile sums
-  __syncthreads();
+  // before it), from the scan over the tile sums (all written before the
+  // barrier above)
   const uint32_t tile_nb = (s_wnb[0] + s_wnb[1] + s_wnb[2] + s_wnb[3]) & 0xFFFFu;
 
   const uint32_t s_in = s_sin;
