@@ -664,24 +664,23 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
     d.n_op = n_op;
     d.pad = 0;
     a.tiles[tile] = d;
-    unsigned long long* c = (unsigned long long*)a.counters;
-    if (s_need) atomicOr(&a.wplan->m_need, s_need);
-    if (s_heads) atomicAdd(&c[ARGUS_C_N_CTX], (unsigned long long)s_heads);
-    if (s_maxlvl) atomicMax(&c[ARGUS_C_MAX_LEVEL], (unsigned long long)s_maxlvl);
-    if (s_orph) atomicAdd(&c[ARGUS_C_N_ORPHAN_END], (unsigned long long)s_orph);
     // every thread has read this tile's scalars: reset them for the next
+    // (the counts and the merge bits add up over the block's tiles)
     s_first = kMatchTile;
     s_lastp1 = 0;
-    s_heads = 0;
     s_lo = 0xFFFFFFFFu;
-    s_maxlvl = 0;
-    s_orph = 0;
-    s_need = 0;
   }
   __syncthreads();
   if (next >= n_tiles) break;
   tile = next;
   }  // tiles
+  if (tid == 0) {
+    unsigned long long* c = (unsigned long long*)a.counters;
+    if (s_need) atomicOr(&a.wplan->m_need, s_need);
+    if (s_heads) atomicAdd(&c[ARGUS_C_N_CTX], (unsigned long long)s_heads);
+    if (s_maxlvl) atomicMax(&c[ARGUS_C_MAX_LEVEL], (unsigned long long)s_maxlvl);
+    if (s_orph) atomicAdd(&c[ARGUS_C_N_ORPHAN_END], (unsigned long long)s_orph);
+  }
 }
 
 hipError_t launch_match(const RunArgs& a, hipStream_t s) {
