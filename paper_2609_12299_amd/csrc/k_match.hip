@@ -280,7 +280,7 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
   }
   // context of the record before this thread's first one: the previous
   // lane's last record, or (lane 0) a load of the record before
-  uint32_t prev0 = (uint32_t)__shfl_up((int)ctxr[IT - 1], 1);
+  uint32_t prev0 = lane_prev(ctxr[IT - 1], 0u);
   bool has_prev0 = true;
   if (lane == 0) {
     const uint64_t pp = base + p0;
@@ -324,9 +324,11 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
     s_wfn[w] = x;
     s_wnb[w] = nbx;
   }
-  Fn ex = Fn{(uint32_t)__shfl_up((int)x.reset, 1), __shfl_up(x.a, 1), __shfl_up(x.c, 1)};
+  // the previous lane's inclusive map (the identity in lane 0)
+  const Fn id = fn_id();
+  const Fn ex = Fn{lane_prev(x.reset, id.reset), (int32_t)lane_prev((uint32_t)x.a, (uint32_t)id.a),
+                   (int32_t)lane_prev((uint32_t)x.c, (uint32_t)id.c)};
   uint32_t nbex = nbx - nbh;
-  if (lane == 0) ex = fn_id();
   __syncthreads();
   Fn pre = fn_id();
   uint32_t pnb = 0;
@@ -419,13 +421,15 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
 #pragma unroll
     for (int i = 1; i < IT; ++i) m = min(m, xp[i]);
     s_up[kU1 + tid] = m;
-    m = min(m, (uint32_t)__shfl_xor(m, 1));
-    m = min(m, (uint32_t)__shfl_xor(m, 2));
-    m = min(m, (uint32_t)__shfl_xor(m, 4));
+    // minima over 8 lanes (quads, then the mirrored half row), over the row
+    // of 16, then over the wave from the four rows
+    m = min(m, dpp32<kDppQuad1032>(m));
+    m = min(m, dpp32<kDppQuad2301>(m));
+    m = min(m, dpp32<kDppHalfMirror>(m));
     if ((lane & 7) == 0) s_up[kU2 + (tid >> 3)] = m;
-    m = min(m, (uint32_t)__shfl_xor(m, 8));
-    m = min(m, (uint32_t)__shfl_xor(m, 16));
-    m = min(m, (uint32_t)__shfl_xor(m, 32));
+    m = min(m, dpp32<kDppMirror>(m));
+    m = min(min((uint32_t)__builtin_amdgcn_readlane((int)m, 0), (uint32_t)__builtin_amdgcn_readlane((int)m, 16)),
+            min((uint32_t)__builtin_amdgcn_readlane((int)m, 32), (uint32_t)__builtin_amdgcn_readlane((int)m, 48)));
     if (lane == 0) {
       s_up[kU3 + w] = m;
       s_up[kU3 + 4 + w] = 0xFFFFFFFFu;
