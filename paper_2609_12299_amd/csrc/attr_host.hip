@@ -77,7 +77,8 @@ Layout make_layout(const argus_attr_config& c, uint64_t n, bool own_instances) {
   L.ev_off = take(sizeof(uint32_t) * kDigitPositions * kRadixBins);
   L.tile_ctr = take(sizeof(uint32_t) * kCtrCount);
   for (int b = 0; b < 2; ++b) {
-    L.key[b] = take(sizeof(uint64_t) * nn);
+    // key[1] first holds the chunks' run lists: 256 places per chunk
+    L.key[b] = take(sizeof(uint64_t) * ceil_div(nn, kChunk) * kChunk);
     L.pay[b] = take(sizeof(uint32_t) * nn);
     L.ctxw[b] = take(sizeof(uint32_t) * nn);
   }

@@ -268,6 +268,34 @@ enum CtrSlot {
   kCtrCount = 64
 };
 
+// Run lists of the input chunks.  The ingest's waves take chunks g, g + W,
+// g + 2W, ... (W waves); each wave stages its chunks' lists and writes them
+// out in bursts, one wave's after another's: a chunk's list count and place
+// go to the entry at chunk_slot(c) of the chunk table, its runs to the run
+// buffer from 256 * wave_slot0(g) on.  With chunks = q W + r, wave g takes
+// q + (g < r) chunks.
+struct ChunkWaves {
+  uint32_t W;
+  uint64_t q, r;
+};
+__host__ __device__ inline ChunkWaves chunk_waves(uint64_t chunks, uint32_t W) {
+  return ChunkWaves{W, chunks / W, chunks % W};
+}
+__host__ __device__ inline uint64_t wave_slot0(const ChunkWaves& cw, uint64_t g) {
+  return g * cw.q + (g < cw.r ? g : cw.r);
+}
+__host__ __device__ inline uint64_t chunk_slot(const ChunkWaves& cw, uint64_t c) {
+  return wave_slot0(cw, c % cw.W) + c / cw.W;
+}
+// chunk table entry: run count (<= 256) | first run's place in the wave's list << 9
+constexpr uint32_t kChunkCountBits = 9;
+// the ingest's grid for n records (four waves per block)
+__host__ __device__ inline uint32_t ingest_blocks(uint64_t n) {
+  uint64_t blocks = (n + 256 * 4 * 4 - 1) / (256 * 4 * 4);
+  if (blocks > 1024) blocks = 1024;
+  return blocks < 1 ? 1u : (uint32_t)blocks;
+}
+
 // ------------------------------------------------------- device helpers
 #if defined(__HIP_DEVICE_COMPILE__)
 #define ARGUS_DEV __device__ __forceinline__

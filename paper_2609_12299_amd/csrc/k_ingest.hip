@@ -220,8 +220,13 @@ struct IngestArgs {
   uint32_t* hist;        // rec_hist: positions 0..3 (raw context digits)
   DevPlan* plan;         // n_runs
   uint64_t* runs_raw;    // [chunk * 256 + j]: context | valid records << 32 of run j
-  uint32_t* chunk_runs;  // [chunk]
+  uint32_t* chunk_runs;  // [chunk slot]: count | place << kChunkCountBits
 };
+
+// Staged run lists per wave (entries; chunk table words).
+constexpr uint32_t kStageRuns = 512;
+constexpr uint32_t kStageChunks = 256;
+static_assert(kStageRuns >= kChunk, "a chunk's runs fit the stage");
 
 // One coalesced 16-byte load per record.  Counts kinds and regions, reduces
 // the timestamp and context ranges of valid records, and builds the 256-bin
@@ -233,6 +238,8 @@ __global__ __launch_bounds__(256) void k_ingest(IngestArgs a) {
   __shared__ uint32_t s_hist[4][kRadixBins];
   __shared__ uint64_t s_red[4][8];
   __shared__ unsigned long long s_runs;
+  __shared__ uint64_t s_stage[4][kStageRuns];
+  __shared__ uint32_t s_ctab[4][kStageChunks];
   if (threadIdx.x == 0) s_runs = 0;
   for (int i = threadIdx.x; i < 4 * kRadixBins; i += 256) (&s_hist[0][0])[i] = 0;
   __syncthreads();
@@ -249,6 +256,32 @@ __global__ __launch_bounds__(256) void k_ingest(IngestArgs a) {
   const uint64_t first = ((uint64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * (64 * kPer);
   static_assert(kPer * 64 == kChunk, "a wave step is one chunk");
   uint64_t wave_runs = 0;
+  // this wave's run list and chunk table words: staged, then written out
+  const uint32_t wv = threadIdx.x >> 6;
+  const ChunkWaves cw = chunk_waves((a.n + kChunk - 1) / kChunk, gridDim.x * 4);
+  const uint64_t slot0 = wave_slot0(cw, (uint64_t)blockIdx.x * 4 + wv);
+  uint64_t* const list = a.runs_raw + slot0 * kChunk;
+  uint32_t n_out = 0, n_staged = 0;  // runs written out, runs staged
+  uint32_t c_out = 0, c_staged = 0;  // chunk words written out, staged
+  auto wave_sync = [] {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  };
+  auto flush_runs = [&] {
+    wave_sync();
+    for (uint32_t i = lane; i < n_staged; i += 64) list[n_out + i] = s_stage[wv][i];
+    n_out += n_staged;
+    n_staged = 0;
+    wave_sync();
+  };
+  auto flush_chunks = [&] {
+    wave_sync();
+    for (uint32_t i = lane; i < c_staged; i += 64) a.chunk_runs[slot0 + c_out + i] = s_ctab[wv][i];
+    c_out += c_staged;
+    c_staged = 0;
+    wave_sync();
+  };
   uint4 nr_[kPer];  // the next chunk, loaded while this one is processed
   auto issue = [&](uint64_t b) {
 #pragma unroll
@@ -284,7 +317,6 @@ __global__ __launch_bounds__(256) void k_ingest(IngestArgs a) {
     // runs of one context in this chunk
     uint64_t H[4], V[4];
     chunk_masks(cx, inr, vl, H, V);
-    const uint64_t chunk = base / kChunk;
     uint32_t nr = 0, nvc = 0;
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
@@ -292,13 +324,15 @@ __global__ __launch_bounds__(256) void k_ingest(IngestArgs a) {
       nvc += (uint32_t)__popcll(V[j]);
     }
     n_valid += nvc;
+    if (n_staged + nr > kStageRuns) flush_runs();
+    if (c_staged == kStageChunks) flush_chunks();
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
       if (!((H[j] >> lane) & 1ull)) continue;
       const uint32_t p = 64u * j + lane;
       const uint32_t li = popc_range(H, 0, p);
       const uint32_t cnt = popc_range(V, p, next_set_after(H, p));
-      a.runs_raw[chunk * kChunk + li] = (uint64_t)cx[j] | ((uint64_t)cnt << 32);
+      s_stage[wv][n_staged + li] = (uint64_t)cx[j] | ((uint64_t)cnt << 32);
       if (cnt) {
         // the context range, and the context digit histograms, per run
         ctx_min = cx[j] < ctx_min ? cx[j] : ctx_min;
@@ -307,9 +341,13 @@ __global__ __launch_bounds__(256) void k_ingest(IngestArgs a) {
         for (int d = 0; d < 4; ++d) atomicAdd(&s_hist[d][(cx[j] >> (8 * d)) & 0xFFu], cnt);
       }
     }
-    if (lane == 0) a.chunk_runs[chunk] = nr;
+    if (lane == 0) s_ctab[wv][c_staged] = nr | ((n_out + n_staged) << kChunkCountBits);
+    ++c_staged;
+    n_staged += nr;
     wave_runs += nr;
   }
+  if (n_staged) flush_runs();
+  if (c_staged) flush_chunks();
   ts_min = wave_min(ts_min);
   ts_max = wave_max(ts_max);
   const uint64_t cmin = wave_min(ctx_min);
@@ -360,12 +398,9 @@ __global__ __launch_bounds__(256) void k_ingest(IngestArgs a) {
 hipError_t launch_ingest(const RunArgs& a, hipStream_t s) {
   IngestArgs ia{(const uint4*)a.rec, a.n, a.R, a.out.d_counters, a.w.rec_hist, a.w.plan,
                 a.w.key[1], a.w.chunk_runs};
-  // 1024 blocks: four waves per SIMD, each streaming many chunks (measured
-  // faster than more or fewer on the 2^28-record trace)
-  uint64_t blocks = ceil_div(a.n, 256 * 4 * 4);
-  if (blocks > 1024) blocks = 1024;
-  if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(k_ingest, dim3((uint32_t)blocks), dim3(256), 0, s, ia);
+  // up to 1024 blocks: four waves per SIMD, each streaming many chunks
+  // (measured faster than more or fewer on the 2^28-record trace)
+  hipLaunchKernelGGL(k_ingest, dim3(ingest_blocks(a.n)), dim3(256), 0, s, ia);
   return hipGetLastError();
 }
 
@@ -520,7 +555,13 @@ struct RunScanArgs {
   // which 1: which runs start their context (for the tile sums)
   const uint64_t* key[2];  // sorted run keys (context offset << ts_bits)
   uint8_t* run_head;
+  ChunkWaves cw;  // which 0: where each chunk's word is
 };
+
+// which 0: the run count of chunk i (from the ingest's chunk table)
+__device__ __forceinline__ uint32_t rscan_chunk_runs(const RunScanArgs& a, uint64_t i) {
+  return a.chunk_runs[chunk_slot(a.cw, i)] & ((1u << kChunkCountBits) - 1u);
+}
 
 __device__ __forceinline__ uint64_t rscan_len(const RunScanArgs& a) {
   return a.which == 0 ? ceil_div(a.plan->n_records, kChunk) : a.plan->n_runs;
@@ -536,7 +577,7 @@ __global__ __launch_bounds__(256) void k_rscan_part(RunScanArgs a) {
   const uint32_t* ids = a.pay[p->rec_final];
   uint64_t sum = 0;
   for (uint64_t i = i0 + threadIdx.x; i < i1; i += 256)
-    sum += a.which == 0 ? a.chunk_runs[i] : a.run_cnt[ids[i]];
+    sum += a.which == 0 ? rscan_chunk_runs(a, i) : a.run_cnt[ids[i]];
   sum = wave_sum(sum);
   if ((threadIdx.x & 63) == 0) s_w[threadIdx.x >> 6] = sum;
   __syncthreads();
@@ -584,7 +625,7 @@ __global__ __launch_bounds__(256) void k_rscan_apply(RunScanArgs a) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const uint64_t i = c0 + 4 * t + q;
-      v[q] = i < i1 ? (a.which == 0 ? a.chunk_runs[i] : a.run_cnt[ids[i]]) : 0u;
+      v[q] = i < i1 ? (a.which == 0 ? rscan_chunk_runs(a, i) : a.run_cnt[ids[i]]) : 0u;
       sum += v[q];
     }
     const uint32_t x = (uint32_t)wave_incl_scan32((int32_t)sum);
@@ -643,6 +684,7 @@ static hipError_t launch_rscan(const RunArgs& a, uint32_t which, uint64_t cap, h
   }
   r.bsum = a.w.scan_bsum;
   r.run_head = a.w.run_head;
+  r.cw = chunk_waves(a.w.chunks, ingest_blocks(a.n) * 4);
   const uint32_t nblk = rscan_blocks(cap);
   hipLaunchKernelGGL(k_rscan_part, dim3(nblk), dim3(256), 0, s, r);
   hipError_t e = hipGetLastError();
@@ -666,6 +708,7 @@ struct RunCompactArgs {
   uint32_t* pay;      // pay[0]: run id
   uint32_t* run_cnt;
   uint32_t* run_hist; // [4][256]
+  ChunkWaves cw;      // where each chunk's run list is
 };
 
 // The runs of every chunk, in input order, as sort elements (key: context
@@ -681,10 +724,12 @@ __global__ __launch_bounds__(256) void k_runs_compact(RunCompactArgs a) {
   const uint64_t chunks = ceil_div(p->n_records, kChunk);
   const uint64_t stride = (uint64_t)gridDim.x * 256;
   for (uint64_t c = (uint64_t)blockIdx.x * 256 + threadIdx.x; c < chunks; c += stride) {
-    const uint32_t nr = a.chunk_runs[c];
+    const uint32_t cword = a.chunk_runs[chunk_slot(a.cw, c)];
+    const uint32_t nr = cword & ((1u << kChunkCountBits) - 1u);
+    const uint64_t* list = a.runs_raw + wave_slot0(a.cw, c % a.cw.W) * kChunk + (cword >> kChunkCountBits);
     const uint32_t rb = a.run_base[c];
     for (uint32_t j = 0; j < nr && j < (uint32_t)kChunk; ++j) {
-      const uint64_t v = a.runs_raw[c * kChunk + j];
+      const uint64_t v = list[j];
       const uint32_t cnt = (uint32_t)(v >> 32);
       const uint64_t rel = cnt ? (uint64_t)((uint32_t)v - (uint32_t)ks.ctx_min) : 0ull;
       const uint32_t rid = rb + j;
@@ -705,7 +750,7 @@ __global__ __launch_bounds__(256) void k_runs_compact(RunCompactArgs a) {
 
 hipError_t launch_runs_compact(const RunArgs& a, hipStream_t s) {
   RunCompactArgs r{a.w.plan, a.w.key[1], a.w.chunk_runs, a.w.run_base, a.w.key[0], a.w.pay[0],
-                   a.w.run_cnt, a.w.run_hist};
+                   a.w.run_cnt, a.w.run_hist, chunk_waves(a.w.chunks, ingest_blocks(a.n) * 4)};
   uint64_t blocks = ceil_div(a.w.chunks ? a.w.chunks : 1, 256);
   if (blocks > 1024) blocks = 1024;
   hipLaunchKernelGGL(k_runs_compact, dim3((uint32_t)blocks), dim3(256), 0, s, r);
