@@ -53,7 +53,6 @@ struct Layout {
   size_t plan, rec_hist, rec_off, ev_hist, ev_off, tile_ctr;
   size_t key[2], pay[2], ctxw[2], lb[2], tsum, carry, bsum, slb, mslb, tiles, tree;
   size_t chunk_runs, run_base, run_cnt, run_pos, run_hist, scan_bsum;
-  size_t run_head;
   size_t pop_ts, pop_reg, pushes, op_parent, op_sum;
   size_t inst, child_sum, hist_key, agg_part, ov_mask, ov_q;
   size_t push_pos, pop_pos, ctx_list, ctx_seg, seg_start, seg_split, seg_tile0, part;
@@ -98,7 +97,6 @@ Layout make_layout(const argus_attr_config& c, uint64_t n, bool own_instances) {
   L.run_pos = take(sizeof(uint32_t) * L.run_cap);
   L.run_hist = take(sizeof(uint32_t) * 4 * kRadixBins);
   L.scan_bsum = take(sizeof(uint64_t) * kMaxScanBlocks);
-  L.run_head = take(sizeof(uint8_t) * L.run_cap);
   L.slb = take(sizeof(uint64_t) * 8 * ceil_div(nn, kSweepTile));
   L.tiles = take(sizeof(TileDesc) * L.match_tiles);
   uint64_t leaves = 1;
@@ -304,7 +302,6 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
   w.run_pos = (uint32_t*)(base + L.run_pos);
   w.run_hist = (uint32_t*)(base + L.run_hist);
   w.scan_bsum = (uint64_t*)(base + L.scan_bsum);
-  w.run_head = (uint8_t*)(base + L.run_head);
   w.chunks = L.chunks;
   w.run_cap = L.run_cap;
   w.slb = (uint64_t*)(base + L.slb);

@@ -210,10 +210,9 @@ struct Work {
   uint32_t* chunk_runs; // [chunks] runs of one context in each input chunk
   uint32_t* run_base;   // [chunks] index of each chunk's first run
   uint32_t* run_cnt;    // [run_cap] valid records of each run
-  uint32_t* run_pos;    // [run_cap] sorted position of each run's first valid record
+  uint32_t* run_pos;    // [run_cap] sorted position of each run's first valid record | starts its context << 31
   uint32_t* run_hist;   // [4][256] context-digit histograms over runs
   uint64_t* scan_bsum;  // [kMaxScanBlocks] block sums of the run scans
-  uint8_t* run_head;    // [run_cap] the run starts its context (by run id)
   uint64_t chunks;      // ceil(n / kChunk)
   uint64_t run_cap;     // runs the run path accepts
   uint64_t* slb;        // sweep look-back status, [tiles][8]
@@ -289,6 +288,8 @@ __host__ __device__ inline uint64_t chunk_slot(const ChunkWaves& cw, uint64_t c)
 }
 // chunk table entry: run count (<= 256) | first run's place in the wave's list << 9
 constexpr uint32_t kChunkCountBits = 9;
+// run position word (by run id): first sorted position | starts its context << 31
+constexpr uint32_t kRunPosMask = 0x7FFFFFFFu;
 // the ingest's grid for n records (four waves per block)
 __host__ __device__ inline uint32_t ingest_blocks(uint64_t n) {
   uint64_t blocks = (n + 256 * 4 * 4 - 1) / (256 * 4 * 4);

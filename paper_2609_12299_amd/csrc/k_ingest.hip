@@ -552,9 +552,9 @@ struct RunScanArgs {
   uint32_t* run_pos;
   const uint32_t* pay[2];  // sorted run ids
   uint64_t* bsum;          // [grid]
-  // which 1: which runs start their context (for the tile sums)
+  // which 1: which runs start their context (for the tile sums; bit 31 of
+  // run_pos)
   const uint64_t* key[2];  // sorted run keys (context offset << ts_bits)
-  uint8_t* run_head;
   ChunkWaves cw;  // which 0: where each chunk's word is
 };
 
@@ -645,7 +645,6 @@ __global__ __launch_bounds__(256) void k_rscan_apply(RunScanArgs a) {
           a.run_base[i] = (uint32_t)pre;
         } else {
           const uint32_t id = ids[i];
-          a.run_pos[id] = (uint32_t)pre;
           // A run starts its context if it has valid records and the
           // previous run has another context; runs without valid records
           // sort as context offset 0, so the runs of offset 0 start it only
@@ -654,7 +653,8 @@ __global__ __launch_bounds__(256) void k_rscan_apply(RunScanArgs a) {
           const uint64_t* keys = a.key[p->rec_final];
           const uint32_t ctx = tb >= 64 ? 0u : (uint32_t)(keys[i] >> tb);
           const uint32_t prev = i > 0 ? (tb >= 64 ? 0u : (uint32_t)(keys[i - 1] >> tb)) : 0xFFFFFFFFu;
-          a.run_head[id] = v[q] > 0 && (ctx == 0 ? pre == 0 : prev != ctx) ? 1u : 0u;
+          const uint32_t head = v[q] > 0 && (ctx == 0 ? pre == 0 : prev != ctx) ? 1u : 0u;
+          a.run_pos[id] = (uint32_t)pre | (head << 31);
         }
       }
       pre += v[q];
@@ -683,7 +683,6 @@ static hipError_t launch_rscan(const RunArgs& a, uint32_t which, uint64_t cap, h
     r.key[b] = a.w.key[b];
   }
   r.bsum = a.w.scan_bsum;
-  r.run_head = a.w.run_head;
   r.cw = chunk_waves(a.w.chunks, ingest_blocks(a.n) * 4);
   const uint32_t nblk = rscan_blocks(cap);
   hipLaunchKernelGGL(k_rscan_part, dim3(nblk), dim3(256), 0, s, r);
@@ -810,7 +809,6 @@ struct RunScatterArgs {
   uint32_t K, G, shift;
   // for the tile sums: which runs start their context
   const uint32_t* run_cnt;
-  const uint8_t* run_head;
 };
 
 // Every valid record to its run's position plus its rank among the run's
@@ -875,8 +873,8 @@ __global__ __launch_bounds__(256) void k_runs_scatter(RunScatterArgs a) {
     const uint64_t n_runs = p->n_runs;
     const uint32_t prid = rb + lane;
     const bool pin = prid < n_runs;
-    const uint32_t pre_pos = pin ? a.run_pos[prid] : 0u;
-    const uint32_t pre_head = pin ? a.run_head[prid] : 0u;
+    const uint32_t pre_word = pin ? a.run_pos[prid] : 0u;
+    const uint32_t pre_pos = pre_word & kRunPosMask, pre_head = pre_word >> 31;
     const uint32_t pre_cnt = pin ? a.run_cnt[prid] : 0u;
     uint64_t H[4], V[4];
     chunk_masks(cx, inr, vl, H, V);
@@ -910,9 +908,10 @@ __global__ __launch_bounds__(256) void k_runs_scatter(RunScatterArgs a) {
       if (head) {
         const uint32_t rid = rb + hr;
         const bool near = hr < 64u;
-        const uint32_t rp = near ? sp : a.run_pos[rid];
+        const uint32_t far_word = near ? 0u : a.run_pos[rid];
+        const uint32_t rp = near ? sp : (far_word & kRunPosMask);
         s_roff[wv][hr] = rp - vr[j];
-        hflag[j] = near ? sh : a.run_head[rid];
+        hflag[j] = near ? sh : far_word >> 31;
         if (!all_valid) {
           s_rpos[wv][hr] = rp;
           s_rcnt[wv][hr] = (near ? sc : a.run_cnt[rid]) | (hflag[j] << 31);
@@ -978,7 +977,7 @@ __global__ __launch_bounds__(256) void k_runs_scatter(RunScatterArgs a) {
 hipError_t launch_runs_scatter(const RunArgs& a, hipStream_t s) {
   RunScatterArgs r{a.w.plan, (const uint4*)a.rec, a.n, a.R, a.w.run_base, a.w.run_pos,
                    a.w.key[0], a.w.pay[0], a.out.d_counters, a.region_class, a.K, a.G, a.shift,
-                   a.w.run_cnt, a.w.run_head};
+                   a.w.run_cnt};
   // 1280 blocks, five per compute unit (as many as the LDS holds), measured
   // fastest: more loads in flight than with 1024 or fewer
   uint64_t blocks = ceil_div(a.n, 256 * 4 * 4);
@@ -1189,7 +1188,7 @@ __global__ __launch_bounds__(256) void k_runs_check(RunCheckArgs a) {
   bool bad = false;
   const uint64_t stride = (uint64_t)gridDim.x * 256;
   for (uint64_t r = (uint64_t)blockIdx.x * 256 + threadIdx.x; r < n_runs; r += stride) {
-    const uint32_t pos = a.run_pos[r];
+    const uint32_t pos = a.run_pos[r] & kRunPosMask;
     if (a.run_cnt[r] == 0 || pos == 0) continue;
     const uint64_t k0 = a.key[pos - 1], k1 = a.key[pos];
     // same context (key bits above ts_bits) and time going back
