@@ -716,7 +716,7 @@ __device__ __forceinline__ bool tile_sums(const uint64_t* se, uint32_t cnt, bool
   // ---- class-count deltas of the thread's events and the lowest running
   // count after each of them relative to the thread's start, then the
   // deltas scanned over the block
-  int32_t dd[KC], lmin[KC], pre[KC], agg[KC], mn[KC];
+  int32_t dd[KC], lmin[KC], pre[KC];
 #pragma unroll
   for (int x = 0; x < KC; ++x) {
     dd[x] = 0;
@@ -746,13 +746,8 @@ __device__ __forceinline__ bool tile_sums(const uint64_t* se, uint32_t cnt, bool
     // ---- tile minima of the local counts (after each event)
 #pragma unroll
     for (int x = 0; x < KC; ++x) {
-      agg[x] = 0;
 #pragma unroll
-      for (int q = 0; q < NW; ++q) {
-        const int32_t v2 = ss.wd[q][x];
-        pre[x] += q < (int)w ? v2 : 0;
-        agg[x] += v2;
-      }
+      for (int q = 0; q < NW; ++q) pre[x] += q < (int)w ? ss.wd[q][x] : 0;
       const int32_t m0 = nval ? pre[x] + lmin[x] : 0x7FFFFFFF;
       const int32_t m = rows_min32(row_min32(m0));
       if (lane == 0) ss.wm[w][x] = m;
@@ -769,7 +764,6 @@ __device__ __forceinline__ bool tile_sums(const uint64_t* se, uint32_t cnt, bool
     int32_t m = 0x7FFFFFFF;
 #pragma unroll
     for (int q = 0; q < NW; ++q) m = ss.wm[q][x] < m ? ss.wm[q][x] : m;
-    mn[x] = m;
     lp[x] = (uint32_t)(pre[x] + kLBias);
     mp[x] = (uint32_t)(m + kLBias);
   }
@@ -850,9 +844,19 @@ __device__ __forceinline__ bool tile_sums(const uint64_t* se, uint32_t cnt, bool
     for (int q = 0; q < NW; ++q) sum += ss.red[t][q];
     rec[1 + KC + t] = sum;
   } else if (t == (uint32_t)kMsThreads - 1) {
+    // the tile's count changes and minima, again from the per-wave values
+    // (not kept in registers over the sweep)
     rec[0] = head;
 #pragma unroll
-    for (int x = 0; x < KC; ++x) rec[1 + x] = (uint64_t)(uint32_t)agg[x] | ((uint64_t)(uint32_t)mn[x] << 32);
+    for (int x = 0; x < KC; ++x) {
+      int32_t agg = 0, mn = 0x7FFFFFFF;
+#pragma unroll
+      for (int q = 0; q < NW; ++q) {
+        agg += ss.wd[q][x];
+        mn = ss.wm[q][x] < mn ? ss.wm[q][x] : mn;
+      }
+      rec[1 + x] = (uint64_t)(uint32_t)agg | ((uint64_t)(uint32_t)mn << 32);
+    }
   }
   return true;
 }
