@@ -85,31 +85,6 @@ __device__ __forceinline__ uint32_t block_excl_scan256(uint32_t v, uint32_t* scr
 // p = 64 j + lane in word j.
 static_assert(kChunk == 256, "a chunk is 4 rows of a wave");
 
-// Set bits of m in positions [lo, hi).
-__device__ __forceinline__ uint32_t popc_range(const uint64_t (&m)[4], uint32_t lo, uint32_t hi) {
-  uint32_t c = 0;
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const uint32_t a = lo > 64u * r ? lo - 64u * r : 0u;
-    const uint32_t b = hi < 64u * r + 64u ? (hi > 64u * r ? hi - 64u * r : 0u) : 64u;
-    if (a < b) {
-      const uint64_t mk = (b - a == 64 ? ~0ull : ((1ull << (b - a)) - 1ull)) << a;
-      c += (uint32_t)__popcll(m[r] & mk);
-    }
-  }
-  return c;
-}
-// First set bit after position p, or 256.
-__device__ __forceinline__ uint32_t next_set_after(const uint64_t (&m)[4], uint32_t p) {
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    if (64u * r + 63u <= p) continue;
-    uint64_t w = m[r];
-    if (p >= 64u * r) w &= ~0ull << (p - 64u * r) << 1;  // two shifts: p - 64 r may be 63
-    if (w) return 64u * r + (uint32_t)__ffsll((unsigned long long)w) - 1u;
-  }
-  return (uint32_t)kChunk;
-}
 // Run heads (a record whose predecessor in the chunk has another context,
 // or the chunk's first record) and valid records of the chunk.
 __device__ __forceinline__ void chunk_masks(const uint32_t (&ctx)[4], const bool (&in)[4],
@@ -326,12 +301,44 @@ __global__ __launch_bounds__(256) void k_ingest(IngestArgs a) {
     n_valid += nvc;
     if (n_staged + nr > kStageRuns) flush_runs();
     if (c_staged == kStageChunks) flush_chunks();
+    // per row (wave-uniform): heads and valid records before it, and the
+    // valid records before the first head of the rows after it (all of the
+    // chunk's if none)
+    uint32_t hbase[kPer], vbase[kPer], vnext[kPer];
+    {
+      uint32_t hb = 0, vb = 0;
+#pragma unroll
+      for (int j = 0; j < kPer; ++j) {
+        hbase[j] = hb;
+        vbase[j] = vb;
+        hb += (uint32_t)__popcll(H[j]);
+        vb += (uint32_t)__popcll(V[j]);
+      }
+      uint32_t vn = vb;
+#pragma unroll
+      for (int j = kPer - 1; j >= 0; --j) {
+        vnext[j] = vn;
+        if (H[j]) {
+          const uint32_t b = (uint32_t)__ffsll((unsigned long long)H[j]) - 1u;
+          vn = vbase[j] + (uint32_t)__popcll(V[j] & ((1ull << b) - 1ull));
+        }
+      }
+    }
 #pragma unroll
     for (int j = 0; j < kPer; ++j) {
       if (!((H[j] >> lane) & 1ull)) continue;
-      const uint32_t p = 64u * j + lane;
-      const uint32_t li = popc_range(H, 0, p);
-      const uint32_t cnt = popc_range(V, p, next_set_after(H, p));
+      const uint32_t li = hbase[j] + __builtin_amdgcn_mbcnt_hi((uint32_t)(H[j] >> 32),
+                                                                __builtin_amdgcn_mbcnt_lo((uint32_t)H[j], 0u));
+      const uint32_t vp = vbase[j] + __builtin_amdgcn_mbcnt_hi((uint32_t)(V[j] >> 32),
+                                                                __builtin_amdgcn_mbcnt_lo((uint32_t)V[j], 0u));
+      // the next head in this row (two shifts: lane + 1 may be 64)
+      const uint64_t later = H[j] & ((~0ull << lane) << 1);
+      uint32_t vq = vnext[j];
+      if (later) {
+        const uint32_t b = (uint32_t)__ffsll((unsigned long long)later) - 1u;
+        vq = vbase[j] + (uint32_t)__popcll(V[j] & ((1ull << b) - 1ull));
+      }
+      const uint32_t cnt = vq - vp;
       s_stage[wv][n_staged + li] = (uint64_t)cx[j] | ((uint64_t)cnt << 32);
       if (cnt) {
         // the context range, and the context digit histograms, per run
