@@ -16,7 +16,7 @@ from __future__ import annotations
 import numpy as np
 import pytest
 
-from golden_util import RS_FIELDS, RS_HIST_EXCL, RS_HIST_INCL
+from golden_util import RECORD_DTYPE, RS_FIELDS, RS_HIST_EXCL, RS_HIST_INCL
 from gpu_util import assert_parity, gpu_run, log, oracle_run
 
 pytestmark = pytest.mark.gpu
@@ -87,6 +87,36 @@ def _region_stats_from_instances(inst: np.ndarray, excl: np.ndarray, R: int) -> 
     selfn = idx[inst["region_id"][par[idx]] == inst["region_id"][idx]]
     out["self_nested"] = np.bincount(inst["region_id"][selfn].astype(np.int64), minlength=R).astype(np.uint64)
     return out
+
+
+def test_run_lists_in_several_bursts(oracle_mod):
+    """2^25 records of 4096 contexts interleaved 8 at a time: 32 runs per
+    256-record chunk, so every ingest wave stages more runs than its buffer
+    holds and writes its run list out in several bursts, while the context
+    sort over runs is still taken.  Compared whole with the oracle."""
+    rng = np.random.default_rng(25)
+    C, per, step = 4096, 8192, 8
+    n = C * per
+    # per context, groups of four: BEGIN r1, BEGIN r2, END r2, END r1
+    r1 = rng.integers(0, 6, size=(C, per // 4))
+    r2 = rng.integers(0, 6, size=(C, per // 4))
+    region = np.stack([r1, r2, r2, r1], axis=2).reshape(C, per)
+    kind = np.tile(np.array([1, 1, 2, 2], np.uint8), per // 4)[None, :].repeat(C, axis=0)
+    ts = np.cumsum(rng.integers(1, 50, size=(C, per), dtype=np.uint64), axis=1, dtype=np.uint64)
+    ts += rng.integers(0, 1 << 30, size=(C, 1), dtype=np.uint64)
+    ctx = np.arange(C, dtype=np.uint32)[:, None].repeat(per, axis=1)
+    rec = np.zeros((C, per), RECORD_DTYPE)
+    rec["ts"], rec["ctx_key"], rec["region_id"], rec["kind"] = ts, ctx, region, kind
+    # interleave the contexts `step` records at a time (trace buffers per warp)
+    rec = rec.reshape(C, per // step, step).transpose(1, 0, 2).reshape(n)
+    rec_u8 = rec.view(np.uint8).reshape(n, 16)
+    p = dict(num_regions=6, num_classes=2, region_class=np.array([0, 1, 0, 1, 0xFF, 0], np.uint8),
+             group_shift=4, num_groups=C >> 4)
+    log(f"[gpu] staged run lists: n={n}, {256 // step} runs per chunk")
+    g = gpu_run(rec_u8, p, with_plan=True)
+    plan = g.pop("_plan")
+    assert plan["runs"] == 1 and plan["unsorted"] == 0
+    assert_parity(g, oracle_run(oracle_mod, rec_u8, p), what="staged run lists")
 
 
 def test_full_size_large_trace_sampled(oracle_mod, tracegen_mod):
