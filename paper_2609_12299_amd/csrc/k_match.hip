@@ -455,24 +455,28 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
   uint32_t hit[IT];   // rank | region << 11 of the answer, or kNoHit
   uint32_t qmask = 0; // bit i: record i asks a question
   uint32_t pend = 0;  // bit i: answered by the tree
+  // Inside the thread both answers are the BEGIN on top of the thread's own
+  // stack of open BEGINs (a bit mask over its records; a context start
+  // empties it): the last earlier record at depth sb - 1 is the BEGIN that
+  // opened that level, and no later record went below it.
+  uint32_t open = 0;
 #pragma unroll
   for (int i = 0; i < IT; ++i) {
     hit[i] = kNoHit;
-    const bool headi = (fh >> i) & 1u;
-    if (!((fv >> i) & 1u) || sb[i] == 0) continue;  // top-level BEGIN or orphan END
-    qmask |= 1u << i;
-    const uint32_t v = sb[i];
-    int qi = -1;
-#pragma unroll
-    for (int j = i - 1; j >= 0; --j) {
-      const uint32_t xj = ((fh >> j) & 1u) ? 0u : sb[j] + 1;
-      if (qi < 0 && xj <= v) qi = j;
+    if (!((fv >> i) & 1u)) continue;
+    if ((fh >> i) & 1u) open = 0;
+    const bool isb = (fb >> i) & 1u;
+    if (sb[i] != 0) {  // not a top-level BEGIN or an orphan END
+      qmask |= 1u << i;
+      if (open) {
+        const uint32_t qi = 31u - (uint32_t)__clz(open);
+        hit[i] = s_leaf[leaf_slot(p0) + qi].y;
+        if (!isb) open &= ~(1u << qi);
+      } else {
+        pend |= 1u << i;
+      }
     }
-    (void)headi;
-    if (qi >= 0)
-      hit[i] = s_leaf[leaf_slot(p0) + qi].y;
-    else
-      pend |= 1u << i;
+    if (isb) open |= 1u << i;
   }
   {
     uint32_t* q = (uint32_t*)(s_tend + w * (kQueueCap / 2));  // kQueueCap u32 entries
