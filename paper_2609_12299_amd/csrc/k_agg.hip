@@ -477,15 +477,15 @@ __global__ __launch_bounds__(1024) void k_hist(HistArgs a) {
   // four keys per load (the key array is 256-byte aligned)
   const uint64_t n4 = nb / 4;
   const uint4* k4 = (const uint4*)a.hist_key;
-  // four loads per thread in flight
+  // eight loads per thread in flight
   const uint64_t stride = (uint64_t)a.ranges * NT;
   uint64_t q = (uint64_t)range * NT + threadIdx.x;
-  for (; q + 3 * stride < n4; q += 4 * stride) {
-    uint4 v[4];
+  for (; q + 7 * stride < n4; q += 8 * stride) {
+    uint4 v[8];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) v[u] = k4[q + u * stride];
+    for (int u = 0; u < 8; ++u) v[u] = k4[q + u * stride];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < 8; ++u) {
       add(v[u].x);
       add(v[u].y);
       add(v[u].z);
