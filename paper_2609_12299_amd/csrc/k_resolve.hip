@@ -145,9 +145,9 @@ __device__ __forceinline__ uint32_t enclosing(const ResolveArgs& a, uint64_t t, 
   return a.pushes[(uint64_t)tp * kMatchTile + (L - d.lo_tail)];
 }
 
-// Sixteen lanes per tile (a tile has a few open levels at either end), so
-// that a wave keeps four tiles' dependent loads in flight.
-constexpr uint32_t kResolveLanes = 16;
+// Eight lanes per tile (a tile has a few open levels at either end), so
+// that a wave keeps eight tiles' dependent loads in flight.
+constexpr uint32_t kResolveLanes = 8;
 __global__ __launch_bounds__(256) void k_resolve(ResolveArgs a) {
   const uint64_t t = (uint64_t)blockIdx.x * (256 / kResolveLanes) + (threadIdx.x / kResolveLanes);
   const uint32_t lane = threadIdx.x % kResolveLanes;
