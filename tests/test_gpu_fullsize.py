@@ -3,20 +3,17 @@ times (instances and exclusive times written, default sort path).
 
 * The four smaller workloads (2^16 .. 2^26 records) are compared whole with
   the oracle, bit for bit.
-* The 2^28-record trace (4 GiB) is run whole on the GPU.  Its outputs are
-  checked (a) on sampled context groups -- the largest groups and a seeded
-  random choice -- against the oracle run on just those groups' records: the
-  instances, their exclusive times and the groups' overlap matrices must be
-  identical; and (b) through properties that hold at any size: counter
-  identities, per-region statistics recomputed from the instance array, and
-  the global overlap as the sum over groups.
+* The 2^28-record trace (4 GiB) is run whole on the GPU and compared whole
+  with the oracle, bit for bit, after cheap checks of properties that hold at
+  any size (counter identities, per-region statistics recomputed from the
+  instance array).
 """
 from __future__ import annotations
 
 import numpy as np
 import pytest
 
-from golden_util import RECORD_DTYPE, RS_FIELDS, RS_HIST_EXCL, RS_HIST_INCL
+from golden_util import RECORD_DTYPE, RS_FIELDS
 from gpu_util import assert_parity, gpu_run, log, oracle_run
 
 pytestmark = pytest.mark.gpu
@@ -119,84 +116,36 @@ def test_run_lists_in_several_bursts(oracle_mod):
     assert_parity(g, oracle_run(oracle_mod, rec_u8, p), what="staged run lists")
 
 
-def test_full_size_large_trace_sampled(oracle_mod, tracegen_mod):
+@pytest.mark.timeout(900)
+def test_full_size_large_trace_whole(oracle_mod, tracegen_mod):
+    """The 2^28-record trace (4 GiB, 1 % malformed markers, stack levels near
+    10^3) run whole on the GPU and compared whole with the oracle: every
+    counter, region statistic, overlap row, instance and exclusive time."""
     d = tracegen_mod.generate(5, threads=16)
     p = _params(d)
     rec = d["records"]
     n = len(rec)
-    R, K, G, shift = p["num_regions"], p["num_classes"], p["num_groups"], p["group_shift"]
+    R = p["num_regions"]
     log(f"[gpu] full-size large trace: n={n}")
     g = gpu_run(rec, p)
     c = g["counters"].astype(np.uint64)
     assert int(c[31]) == 0, f"internal error flag {int(c[31])}"
     inst, excl = g["instances"], g["instance_excl"]
-
-    # ---- (b) properties at full size
-    log("[gpu] full-size large trace: properties")
-    rv = rec.view(np.uint8).reshape(n, 16)
-    kind = rv[:, 14]
-    region = rv[:, 12].astype(np.uint32) | (rv[:, 13].astype(np.uint32) << 8)
-    ctx = np.ascontiguousarray(rv[:, 8:12]).view(np.uint32).reshape(n)
-    bad_kind = (kind != 1) & (kind != 2)
-    bad_region = ~bad_kind & (region >= R)
-    valid = ~bad_kind & ~bad_region
-    assert int(c[0]) == n
-    assert int(c[2]) == int(bad_kind.sum()) and int(c[3]) == int(bad_region.sum())
-    assert int(c[1]) == int(valid.sum())
-    assert int(c[4]) == int((valid & (kind == 1)).sum()) and int(c[5]) == int((valid & (kind == 2)).sum())
-    assert len(inst) == int(c[4])
-    assert int(c[9]) + int(c[10]) + int(c[11]) == int(c[4])  # matched + mismatched + unclosed = begins
-    # every END is either an orphan or closes exactly one instance
+    log(f"[gpu] full-size large trace: max_level={int(c[14])}, mismatched={int(c[10])}; "
+        "properties")
+    # properties that hold at any size, checked first because they are cheap
+    assert int(c[0]) == n and len(inst) == int(c[4])
+    assert int(c[9]) + int(c[10]) + int(c[11]) == int(c[4])  # matched + mismatched + unclosed
     closed = inst["end_region_id"] != NO_END
-    assert int(c[12]) + int(closed.sum()) == int(c[5])
-    vctx = ctx[valid]
-    assert int(c[8]) == len(np.unique(vctx))
-    assert int(c[16]) == int(vctx.min()) and int(c[17]) == int(vctx.max())
-    ts = np.ascontiguousarray(rv[:, 0:8]).view(np.uint64).reshape(n)[valid]
-    assert int(c[6]) == int(ts.min()) and int(c[7]) == int(ts.max())
-    assert int(c[14]) == int(inst["level"].max())
-    # instances sorted by (ctx, t_begin); durations and exclusive times sane
-    assert np.all(np.diff(inst["ctx_key"].astype(np.int64)) >= 0)
-    same = inst["ctx_key"][1:] == inst["ctx_key"][:-1]
-    assert np.all(inst["t_begin"][1:][same] >= inst["t_begin"][:-1][same])
-    assert np.all(inst["t_end"][closed] >= inst["t_begin"][closed])
+    assert int(c[12]) + int(closed.sum()) == int(c[5])  # orphans + closed = ENDs
     assert np.all(excl[closed] <= (inst["t_end"][closed] - inst["t_begin"][closed]))
-    assert np.all(excl[~closed] == 0)
     rs = g["region_stats"].reshape(R, -1)
     ref = _region_stats_from_instances(inst, excl, R)
     for name, col in RS_FIELDS.items():
-        if name == "orphan_end":
-            continue  # needs the records, not the instances
-        np.testing.assert_array_equal(rs[:, col], ref[name], err_msg=f"region stats {name}")
-    np.testing.assert_array_equal(rs[:, RS_HIST_INCL:RS_HIST_INCL + 65], ref["hist_incl"])
-    np.testing.assert_array_equal(rs[:, RS_HIST_EXCL:RS_HIST_EXCL + 65], ref["hist_excl"])
-    assert int(c[9]) == int(ref["count"].sum())
-    ov = g["overlap_group"].reshape(G, 2 * K * K)
-    np.testing.assert_array_equal(ov.sum(axis=0, dtype=np.uint64), g["overlap_global"].reshape(-1))
-
-    # ---- (a) sampled groups against the oracle
-    grp = ctx >> np.uint32(shift) if shift < 32 else np.zeros(n, np.uint32)
-    sizes = np.bincount(grp.astype(np.int64), minlength=G)
-    rng = np.random.default_rng(12299)
-    largest = np.argsort(-sizes[:G], kind="stable")[:3]
-    rest = np.setdiff1d(np.arange(G), largest)
-    pick = np.concatenate([largest, rng.choice(rest, size=29, replace=False)])
-    sel = np.isin(grp, pick)
-    sub = np.ascontiguousarray(rec[sel])
-    log(f"[gpu] full-size large trace: oracle on {len(pick)} groups, {len(sub)} records")
-    o = oracle_run(oracle_mod, sub, p)
-    oi = o["instances"]
-    keep = np.isin(inst["ctx_key"] >> np.uint32(shift), pick)
-    gi = inst[keep]
-    assert len(gi) == len(oi), f"{len(gi)} sampled instances vs {len(oi)}"
-    for f in ("t_begin", "t_end", "ctx_key", "level", "region_id", "end_region_id"):
-        np.testing.assert_array_equal(gi[f], oi[f], err_msg=f"sampled instances: {f}")
-    gid = np.nonzero(keep)[0]
-    remap = np.full(len(inst), NO_PARENT, np.int64)
-    remap[gid] = np.arange(len(gid))
-    gp = gi["parent"].astype(np.int64)
-    gp_sub = np.where(gp == NO_PARENT, NO_PARENT, remap[np.minimum(gp, len(inst) - 1)])
-    np.testing.assert_array_equal(gp_sub, oi["parent"].astype(np.int64), err_msg="sampled parents")
-    np.testing.assert_array_equal(excl[keep], o["instance_excl"], err_msg="sampled exclusive times")
-    og = o["overlap_group"].reshape(G, 2 * K * K)
-    np.testing.assert_array_equal(ov[pick], og[pick], err_msg="sampled group overlap")
+        if name != "orphan_end":
+            np.testing.assert_array_equal(rs[:, col], ref[name], err_msg=f"region stats {name}")
+    del ref
+    log("[gpu] full-size large trace: oracle on the whole trace")
+    o = oracle_run(oracle_mod, rec, p)
+    log(f"[gpu] full-size large trace: oracle max_level={int(o['counters'][14])}; comparing")
+    assert_parity(g, o, what="full cfg5")

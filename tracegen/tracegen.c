@@ -289,17 +289,18 @@ static void gen_c4(emitter* e, rng_t* r, uint64_t m, uint32_t warp, uint64_t bas
 
 /* C5: bounded walk, depth <= 8, 1024 regions (child != parent), gaps
  * 1 + Exp(200), base 2^39 + U[0, 2^30); `ins` malformed markers inserted at
- * uniformly chosen positions: a duplicate of the preceding BEGIN (placed
- * right after it) when the preceding record is a BEGIN and a fair coin says
- * so, otherwise an END of a uniformly random region. */
+ * uniformly chosen positions, each kind by a fair coin: a duplicate BEGIN
+ * that repeats the region of the last BEGIN written in this context, or an
+ * END of a uniformly random region.  The two kinds are equally frequent, so
+ * the excess of the clamped stack depth over the well-formed depth is a
+ * reflected random walk and reaches levels near 10^3 in the hot contexts. */
 static void gen_c5(emitter* e, rng_t* r, uint64_t m, uint64_t ins) {
   uint64_t t = (1ull << 39) + rng_below(r, 1ull << 30);
   const uint64_t w = m - ins; /* well-formed records */
   uint64_t wdone = 0, ins_left = ins;
   int d = 0;
   uint16_t reg[9];
-  int prev_begin = 0;
-  uint16_t prev_region = 0;
+  uint16_t last_begin = (uint16_t)rng_below(r, 1024);
   for (uint64_t i = 0; i < m; ++i) {
     const uint64_t slots_left = m - i;
     if (i > 0) t += gap_exp(r, 200.0);
@@ -309,13 +310,12 @@ static void gen_c5(emitter* e, rng_t* r, uint64_t m, uint64_t ins) {
       x->ts = t;
       x->ctx = e->ctx;
       x->pad = 0;
-      if (prev_begin && rng_unit(r) < 0.5) {
+      if (rng_unit(r) < 0.5) {
         x->kind = 1;
-        x->region = prev_region;
+        x->region = last_begin;
       } else {
         x->kind = 2;
         x->region = (uint16_t)rng_below(r, 1024);
-        prev_begin = 0;
       }
       continue;
     }
@@ -334,13 +334,11 @@ static void gen_c5(emitter* e, rng_t* r, uint64_t m, uint64_t ins) {
       reg[d++] = g;
       x->kind = 1;
       x->region = g;
-      prev_begin = 1;
-      prev_region = g;
+      last_begin = g;
     } else {
       --d;
       x->kind = 2;
       x->region = reg[d];
-      prev_begin = 0;
     }
     wdone++;
   }
