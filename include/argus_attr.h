@@ -200,6 +200,29 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n_reco
                    void* d_workspace, size_t workspace_bytes,
                    const argus_attr_outputs* out, void* stream);
 
+/* ------------------------------------------------ allocation-free variant */
+/* Size of the library's built-in workspace: one array of this many bytes per
+ * GPU the library runs on, held until the process ends. */
+#define ARGUS_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * computation as argus_attr_run, with the same arguments except the
+ * workspace, which is the library's built-in array on the current device
+ * instead.  It calls no allocating routine.  Outputs and records are the
+ * caller's, as for argus_attr_run.
+ *
+ * Limit: returns ARGUS_E_CAPACITY (before any GPU call, with a message in
+ * argus_attr_last_error) when argus_attr_workspace_bytes(h, n_records)
+ * exceeds ARGUS_NOALLOC_SCRATCH_BYTES -- for example about 2^19 records with
+ * num_classes == 0, or 2^16 records with 4 classes over 2048 groups.
+ * Every call on one GPU uses that GPU's one array, whatever the handle:
+ * calls that overlap in time on one GPU (on different streams, or from
+ * different threads) race and give undefined results.  Calls in order on
+ * one stream are safe; each call initialises what it reads. */
+int argus_attr_run_noalloc(argus_attr* h, const argus_record* d_records, uint64_t n_records,
+                           const argus_attr_outputs* out, void* stream);
+
 /* Destroy a handle; NULL is a no-op. */
 void argus_attr_destroy(argus_attr* h);
 

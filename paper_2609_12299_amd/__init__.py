@@ -6,21 +6,22 @@ Cross-Layer GPU Performance Measurements around Semantic Regions"
 per-region duration statistics, class overlap and ambiguity counts, computed
 by hand-written HIP kernels for gfx950 behind a C ABI (include/argus_attr.h).
 """
-from .attr import (ABI_VERSION, COUNTER_NAMES, FORCE_EVENT_SORT, FORCE_FULL_SORT, FORCE_RECORD_RADIX,
+from .attr import (ABI_VERSION, COUNTER_NAMES, NOALLOC_SCRATCH_BYTES, FORCE_EVENT_SORT, FORCE_FULL_SORT, FORCE_RECORD_RADIX,
                    INSTANCE_DTYPE, NUM_COUNTERS,
                    OUT_INSTANCE_EXCL, OUT_INSTANCES, RS_WIDTH, ArgusError, RegionAttribution,
                    argus_attr_config, argus_attr_create, argus_attr_destroy,
                    argus_attr_kernel_times, argus_attr_last_error, argus_attr_outputs,
-                   argus_attr_run, argus_attr_set_timing, argus_attr_set_timing_filter,
+                   argus_attr_run, argus_attr_run_noalloc, argus_attr_set_timing, argus_attr_set_timing_filter,
                    argus_attr_workspace_bytes,
                    load_library, to_host)
 
 __all__ = [
-    "ABI_VERSION", "COUNTER_NAMES", "FORCE_EVENT_SORT", "FORCE_FULL_SORT", "FORCE_RECORD_RADIX",
+    "ABI_VERSION", "COUNTER_NAMES", "NOALLOC_SCRATCH_BYTES", "FORCE_EVENT_SORT", "FORCE_FULL_SORT", "FORCE_RECORD_RADIX",
     "INSTANCE_DTYPE", "NUM_COUNTERS",
     "OUT_INSTANCE_EXCL", "OUT_INSTANCES", "RS_WIDTH", "ArgusError", "RegionAttribution",
     "argus_attr_config", "argus_attr_create", "argus_attr_destroy", "argus_attr_kernel_times",
-    "argus_attr_last_error", "argus_attr_outputs", "argus_attr_run", "argus_attr_set_timing",
+    "argus_attr_last_error", "argus_attr_outputs", "argus_attr_run", "argus_attr_run_noalloc",
+    "argus_attr_set_timing",
     "argus_attr_set_timing_filter",
     "argus_attr_workspace_bytes", "load_library", "to_host",
 ]

@@ -17,6 +17,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libargus_attr.so")
 
 ABI_VERSION = 1
+NOALLOC_SCRATCH_BYTES = 64 << 20  # ARGUS_NOALLOC_SCRATCH_BYTES
 KIND_BEGIN, KIND_END = 1, 2
 OUT_INSTANCES, OUT_INSTANCE_EXCL, FORCE_FULL_SORT, FORCE_EVENT_SORT, FORCE_RECORD_RADIX = 1, 2, 4, 8, 16
 NUM_COUNTERS = 32
@@ -73,6 +74,8 @@ def load_library(path: str = LIB_PATH):
     lib.argus_attr_run.argtypes = [vp, vp, u64, vp, ctypes.c_size_t,
                                    ctypes.POINTER(argus_attr_outputs), vp]
     lib.argus_attr_run.restype = i32
+    lib.argus_attr_run_noalloc.argtypes = [vp, vp, u64, ctypes.POINTER(argus_attr_outputs), vp]
+    lib.argus_attr_run_noalloc.restype = i32
     lib.argus_attr_destroy.argtypes = [vp]
     lib.argus_attr_destroy.restype = None
     lib.argus_attr_last_error.argtypes = [vp]
@@ -105,6 +108,13 @@ def argus_attr_run(h, d_records: int, n_records: int, d_workspace: int, workspac
                    out: argus_attr_outputs, stream: int) -> int:
     return load_library().argus_attr_run(h, d_records, n_records, d_workspace, workspace_bytes,
                                          ctypes.byref(out), stream)
+
+
+def argus_attr_run_noalloc(h, d_records: int, n_records: int, out: argus_attr_outputs,
+                           stream: int) -> int:
+    return load_library().argus_attr_run_noalloc(h, d_records, n_records,
+                                                 ctypes.byref(out) if out is not None else None,
+                                                 stream)
 
 
 def argus_attr_destroy(h) -> None:
@@ -216,6 +226,14 @@ class RegionAttribution:
         aligned = (base + 255) & ~255
         return aligned, need
 
+    def _outputs(self, out: dict) -> argus_attr_outputs:
+        return argus_attr_outputs(
+            out["counters"].data_ptr(), out["region_stats"].data_ptr(),
+            out["overlap_group"].data_ptr() if self.K else None,
+            out["overlap_global"].data_ptr() if self.K else None,
+            out["instances"].data_ptr() if "instances" in out else None,
+            out["instance_excl"].data_ptr() if "instance_excl" in out else None)
+
     def run(self, records, out: dict | None = None, stream=None) -> dict:
         """Enqueue on `stream` (default: the current torch stream); returns the
         output tensors (valid once the stream has completed)."""
@@ -224,15 +242,21 @@ class RegionAttribution:
         if out is None:
             out = self.alloc(n)
         ws, ws_bytes = self.workspace(n)
-        o = argus_attr_outputs(
-            out["counters"].data_ptr(), out["region_stats"].data_ptr(),
-            out["overlap_group"].data_ptr() if self.K else None,
-            out["overlap_global"].data_ptr() if self.K else None,
-            out["instances"].data_ptr() if "instances" in out else None,
-            out["instance_excl"].data_ptr() if "instance_excl" in out else None)
         s = stream if stream is not None else t.cuda.current_stream(self.device)
-        rc = argus_attr_run(self.h, records.data_ptr() if n else None, n, ws, ws_bytes, o,
-                            s.cuda_stream)
+        rc = argus_attr_run(self.h, records.data_ptr() if n else None, n, ws, ws_bytes,
+                            self._outputs(out), s.cuda_stream)
+        if rc != 0:
+            raise ArgusError(rc, argus_attr_last_error(self.h))
+        return out
+
+    def run_noalloc(self, records, out: dict, stream=None) -> dict:
+        """argus_attr_run_noalloc: the same run with the library's built-in
+        workspace (no workspace tensor); `out` must be preallocated."""
+        t = self.torch
+        n = records.numel() * records.element_size() // 16
+        s = stream if stream is not None else t.cuda.current_stream(self.device)
+        rc = argus_attr_run_noalloc(self.h, records.data_ptr() if n else None, n,
+                                    self._outputs(out), s.cuda_stream)
         if rc != 0:
             raise ArgusError(rc, argus_attr_last_error(self.h))
         return out

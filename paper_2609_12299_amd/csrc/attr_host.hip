@@ -4,6 +4,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -231,11 +232,13 @@ int argus_attr_kernel_times(argus_attr* h, const char** names, float* ms, int ca
   return total;
 }
 
-int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
-                   void* d_workspace, size_t workspace_bytes,
-                   const argus_attr_outputs* out, void* stream_v) {
-  if (!h) return ARGUS_E_INVAL;
-  h->err.clear();
+}  // extern "C"
+
+namespace {
+
+// Argument checks shared by both run entry points (no GPU call).
+int check_run_args(argus_attr* h, const argus_record* d_records, uint64_t n,
+                   const argus_attr_outputs* out) {
   const argus_attr_config& c = h->cfg;
   if (!out) return fail(h, ARGUS_E_INVAL, "%s", "outputs is NULL");
   if (n > c.max_records) return fail(h, ARGUS_E_CAPACITY, "%s", "n_records exceeds max_records");
@@ -249,14 +252,11 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
   if ((c.flags & ARGUS_OUT_INSTANCE_EXCL) && !out->d_instance_excl)
     return fail(h, ARGUS_E_INVAL, "%s", "ARGUS_OUT_INSTANCE_EXCL set but d_instance_excl is NULL");
   if (((uintptr_t)d_records & 15) != 0) return fail(h, ARGUS_E_ALIGN, "%s", "records must be 16-byte aligned");
-  if (!d_workspace) return fail(h, ARGUS_E_INVAL, "%s", "d_workspace is NULL");
-  if (((uintptr_t)d_workspace & (kAlign - 1)) != 0)
-    return fail(h, ARGUS_E_ALIGN, "%s", "workspace must be 256-byte aligned");
-  const bool own_inst = !(c.flags & ARGUS_OUT_INSTANCES);
-  const Layout L = make_layout(c, n, own_inst);
-  if (workspace_bytes < L.total) return fail(h, ARGUS_E_CAPACITY, "%s", "workspace too small");
+  return ARGUS_OK;
+}
 
-  // Device check (lazily, once per device).
+// The current device, checked (once per device and handle) to be gfx950.
+int current_device(argus_attr* h, int* dev_out) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return fail(h, ARGUS_E_HIP, "%s", "hipGetDevice failed");
   if (h->device_checked != dev) {
@@ -267,9 +267,18 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
       return fail(h, ARGUS_E_DEVICE, "device is %s, this library is built for gfx950", prop.gcnArchName);
     h->device_checked = dev;
   }
+  *dev_out = dev;
+  return ARGUS_OK;
+}
 
+// Enqueue every step of one run on `stream_v`, with the workspace at `base`
+// (256-byte aligned, at least make_layout(...).total bytes).
+int enqueue_run(argus_attr* h, const argus_record* d_records, uint64_t n, char* base,
+                const argus_attr_outputs* out, void* stream_v) {
+  const argus_attr_config& c = h->cfg;
+  const bool own_inst = !(c.flags & ARGUS_OUT_INSTANCES);
+  const Layout L = make_layout(c, n, own_inst);
   hipStream_t s = (hipStream_t)stream_v;
-  char* base = (char*)d_workspace;
   RunArgs a{};
   a.rec = d_records;
   a.n = n;
@@ -437,6 +446,85 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
     if (!step("ov_final", [&] { return launch_ov_final(a, s); })) return ARGUS_E_HIP;
   }
   return ARGUS_OK;
+}
+
+// Built-in workspace of the allocation-free entry point: one copy per device,
+// held until the process ends.  Host code never uses the array's name as a
+// device address (on the host it names a stand-in); it uses the address that
+// hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) unsigned char scratch[ARGUS_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on device `dev` (the current device), looked
+// up on the first call for that device.
+int scratch_on_device(argus_attr* h, int dev, char** out) {
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(h, ARGUS_E_DEVICE, "%s", "device ordinal beyond the built-in workspace table");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) {
+      fail(h, ARGUS_E_HIP, "%s", "hipGetSymbolAddress of the built-in workspace failed");
+      if (e != hipSuccess) h->err += std::string(" (") + hipGetErrorString(e) + ")";
+      return ARGUS_E_HIP;
+    }
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = (char*)g_scratch_ptr[dev];
+  return ARGUS_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n,
+                   void* d_workspace, size_t workspace_bytes,
+                   const argus_attr_outputs* out, void* stream_v) {
+  if (!h) return ARGUS_E_INVAL;
+  h->err.clear();
+  int rc = check_run_args(h, d_records, n, out);
+  if (rc != ARGUS_OK) return rc;
+  if (!d_workspace) return fail(h, ARGUS_E_INVAL, "%s", "d_workspace is NULL");
+  if (((uintptr_t)d_workspace & (kAlign - 1)) != 0)
+    return fail(h, ARGUS_E_ALIGN, "%s", "workspace must be 256-byte aligned");
+  const bool own_inst = !(h->cfg.flags & ARGUS_OUT_INSTANCES);
+  if (workspace_bytes < make_layout(h->cfg, n, own_inst).total)
+    return fail(h, ARGUS_E_CAPACITY, "%s", "workspace too small");
+  int dev = 0;
+  rc = current_device(h, &dev);
+  if (rc != ARGUS_OK) return rc;
+  return enqueue_run(h, d_records, n, (char*)d_workspace, out, stream_v);
+}
+
+int argus_attr_run_noalloc(argus_attr* h, const argus_record* d_records, uint64_t n,
+                           const argus_attr_outputs* out, void* stream_v) {
+  if (!h) return ARGUS_E_INVAL;
+  h->err.clear();
+  int rc = check_run_args(h, d_records, n, out);
+  if (rc != ARGUS_OK) return rc;
+  const bool own_inst = !(h->cfg.flags & ARGUS_OUT_INSTANCES);
+  const size_t need = make_layout(h->cfg, n, own_inst).total;
+  if (need > (size_t)ARGUS_NOALLOC_SCRATCH_BYTES) {
+    char buf[256];
+    snprintf(buf, sizeof buf,
+             "n_records needs %zu bytes of workspace; the built-in workspace holds %zu "
+             "(use argus_attr_run with a caller workspace)",
+             need, (size_t)ARGUS_NOALLOC_SCRATCH_BYTES);
+    h->err = buf;
+    return ARGUS_E_CAPACITY;
+  }
+  int dev = 0;
+  rc = current_device(h, &dev);
+  if (rc != ARGUS_OK) return rc;
+  char* base = nullptr;
+  rc = scratch_on_device(h, dev, &base);
+  if (rc != ARGUS_OK) return rc;
+  return enqueue_run(h, d_records, n, base, out, stream_v);
 }
 
 }  // extern "C"

@@ -131,3 +131,33 @@ def test_product_path_does_not_touch_the_oracle():
             if f.endswith((".py", ".hip", ".h", ".cpp")):
                 text = open(os.path.join(dirpath, f)).read()
                 assert "oracle" not in text.lower(), f"{f} mentions the oracle"
+
+
+def test_noalloc_argument_errors_before_any_gpu_call(lib):
+    """The allocation-free entry point checks its arguments, and that the
+    run fits its built-in workspace, before making any HIP call."""
+    rc, h = lib.argus_attr_create(cfg(lib, flags=1))
+    assert rc == 0
+    try:
+        fake = 0x100000  # never dereferenced: every case fails its checks first
+        full = lib.argus_attr_outputs(fake, fake, None, None, fake, None)
+        no_inst = lib.argus_attr_outputs(fake, fake, None, None, None, None)
+        f = lib.argus_attr_run_noalloc
+        assert f(None, fake, 64, full, None) == -1
+        assert f(h, fake, (1 << 20) + 1, full, None) == -4
+        assert f(h, None, 64, full, None) == -1
+        assert f(h, fake, 64, None, None) == -1
+        assert f(h, fake, 64, no_inst, None) == -1
+        assert f(h, fake + 8, 64, full, None) == -3
+        # 2^20 records need more workspace than the built-in array holds
+        assert lib.argus_attr_workspace_bytes(h, 1 << 20) > lib.NOALLOC_SCRATCH_BYTES
+        assert f(h, fake, 1 << 20, full, None) == -4
+        assert "built-in workspace" in lib.argus_attr_last_error(h)
+    finally:
+        lib.argus_attr_destroy(h)
+
+
+def test_noalloc_scratch_size_matches_header(lib):
+    src = open(HEADER).read()
+    m = re.search(r"#define ARGUS_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", src)
+    assert m and int(m.group(1)) << int(m.group(2)) == lib.NOALLOC_SCRATCH_BYTES
