@@ -16,8 +16,8 @@ launch / its average launch time vs 8 TB/s HBM; the launch times come from HIP
 events recorded on the run's stream around that kernel only, during the timed
 steps), a per-launch breakdown from instrumented steps before the timed ones
 (an event after every launch), the whole pipeline's algorithmic bytes per
-record and GB/s, and the CPU oracle timed on a bounded sample of the same
-trace (1 core).
+record and GB/s, practical HBM ceilings (copy, fill, read) measured in the same
+process, and the CPU oracle timed on the same trace (1 core).
 """
 from __future__ import annotations
 
@@ -109,7 +109,9 @@ def byte_model(name: str, c: dict, plan: dict, R: int, K: int, G: int, flags: in
     if name == "agg":
         return 40.0 * nb + (8.0 * nb if flags & 2 else 0.0) + (4.0 * nb if R > 167 else 0.0)
     if name == "hist":
-        return 4.0 * nb * max(1, -(-R // 189)) if R > 167 else 0.0
+        # the histogram keys are read from HBM once; the region slices of one
+        # key range re-read them from the L2 of the XCD that holds them
+        return 4.0 * nb if R > 167 else 0.0
     if name == "ev_hist":
         return 32.0 * nb
     if name == "sweep":
@@ -121,9 +123,10 @@ def byte_model(name: str, c: dict, plan: dict, R: int, K: int, G: int, flags: in
     return 0.0
 
 
-def traffic_for(kernel: str):
+def traffic_for(kernel: str, n_begin: int):
     """HBM bytes per launch measured by rocprofv3 counters, if the committed
-    measurement is for the current source of that kernel."""
+    measurement is for the current source of that kernel and for this trace
+    (same number of BEGIN records)."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
@@ -133,24 +136,69 @@ def traffic_for(kernel: str):
             return None
         src = os.path.join(ROOT, "paper_2609_12299_amd", "csrc", rec["source"])
         sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
-        if sha != rec["source_sha256"]:
+        if sha != rec["source_sha256"] or int(rec.get("n_begin", -1)) != n_begin:
             return None
         return float(rec["bytes_per_launch"])
     except Exception:  # noqa: BLE001
         return None
 
 
-def cpu_baseline(records: np.ndarray, d: dict, sample: int) -> dict:
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(records: np.ndarray, d: dict, sample: int, params: dict) -> dict:
+    """The oracle, single-threaded, on the first `sample` records of the same
+    trace the GPU runs (all of them by default)."""
     import oracle
-    sub = np.ascontiguousarray(records[:sample])
+    sub = records if sample >= len(records) else np.ascontiguousarray(records[:sample])
     t0 = time.perf_counter()
-    oracle.run(sub, d["num_regions"], d["num_classes"], d["region_class"], d["group_shift"],
-               d["num_groups"], instances=True)
+    oracle.run(sub, params["num_regions"], params["num_classes"], params["region_class"],
+               params["group_shift"], params["num_groups"], instances=True)
     t = time.perf_counter() - t0
+    what = ("all records of the trace the GPU runs" if sample >= len(records)
+            else f"first {sample} records ({sample * 16 >> 20} MiB) of the trace the GPU runs")
     return {"value": sample / t, "unit": "records/s", "cores": 1, "kind": "oracle",
-            "seconds": round(t, 3),
-            "sample": f"first {sample} records ({sample * 16 >> 20} MiB) of the same trace, "
-                      "single-threaded C++ oracle (validate, stable sort, stack replay, sums, sweep)"}
+            "seconds": round(t, 3), "host_cpus": os.cpu_count(), "cpu_model": cpu_model(),
+            "sample": f"{what}; single-threaded C++ oracle (validate, stable sort, stack replay, "
+                      "sums, sweep) on 1 of the host's cores"}
+
+
+def hbm_ceiling(dev, nbytes: int = 4 << 30, reps: int = 5) -> dict:
+    """Practical HBM ceilings on this GPU: a plain device copy (read + write),
+    a fill (write only) and a read-only reduction over `nbytes`, timed with
+    events on the current stream (torch's own kernels)."""
+    import torch
+    src = torch.empty(nbytes // 8, dtype=torch.int64, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    res = {}
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps * 1e-3
+
+    res["copy_gbs"] = round(2 * nbytes / timed(lambda: dst.copy_(src)) / 1e9, 1)
+    res["fill_gbs"] = round(nbytes / timed(lambda: dst.fill_(3)) / 1e9, 1)
+    res["read_gbs"] = round(nbytes / timed(lambda: src.sum()) / 1e9, 1)
+    res["bytes"] = nbytes
+    res["how"] = "torch copy_ (read+write), fill_ and sum of an int64 tensor, HIP events"
+    del src, dst
+    torch.cuda.empty_cache()
+    return res
 
 
 def main() -> int:
@@ -162,7 +210,14 @@ def main() -> int:
     ap.add_argument("--force-full-sort", action="store_true")
     ap.add_argument("--force-event-sort", action="store_true",
                     help="order overlap events with the radix sort instead of merging")
-    ap.add_argument("--cpu-sample", type=int, default=1 << 27)
+    ap.add_argument("--no-overlap", action="store_true",
+                    help="run without the class-overlap step (num_classes = 0)")
+    ap.add_argument("--graph", action="store_true",
+                    help="also time the run captured once in a HIP graph and replayed")
+    ap.add_argument("--no-ceiling", action="store_true",
+                    help="skip the copy / fill / read ceiling measurement")
+    ap.add_argument("--cpu-sample", type=int, default=0,
+                    help="records the oracle runs on (0: all records of the trace)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernels", action="store_true", help="print per-launch timing to stderr")
     ap.add_argument("--profile-steps", type=int, default=3,
@@ -187,11 +242,16 @@ def main() -> int:
     d = tracegen.generate(args.config, threads=int(os.environ.get("OMP_NUM_THREADS", "16")))
     rec_np = d["records"]
     n = rec_np.shape[0]
+    params = {k: d[k] for k in ("num_regions", "num_classes", "region_class", "group_shift",
+                                "num_groups")}
+    if args.no_overlap:
+        params.update(num_classes=0, region_class=None, num_groups=0)
     err(f"generated config {args.config}: {n} records in {time.perf_counter() - t0:.1f}s")
     rec = torch.from_numpy(rec_np.reshape(-1)).to(dev)
     torch.cuda.synchronize()
-    ra = RegionAttribution(d["num_regions"], d["num_classes"], d["region_class"], d["group_shift"],
-                           d["num_groups"], max_records=n, instances=True, instance_excl=True,
+    ra = RegionAttribution(params["num_regions"], params["num_classes"], params["region_class"],
+                           params["group_shift"], params["num_groups"], max_records=n,
+                           instances=True, instance_excl=True,
                            force_full_sort=args.force_full_sort,
                            force_event_sort=args.force_event_sort, device=dev)
     out = ra.alloc(n)
@@ -241,16 +301,34 @@ def main() -> int:
     assert len(dom_times) == args.steps, f"expected {args.steps} timed launches of {dom}"
     avg[dom] = float(np.mean(dom_times))
 
+    graph = None
+    if args.graph:
+        # the same run captured once and replayed: host launch work leaves the step
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            ra.run(rec, out)
+        g.replay()
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for _ in range(args.steps):
+            g.replay()
+        torch.cuda.synchronize()
+        gms = (time.perf_counter() - t1) * 1e3 / args.steps
+        graph = {"ms_per_step": round(gms, 4), "records_per_s": n / (gms * 1e-3)}
+        gcnt = out["counters"].cpu().numpy()
+        assert np.array_equal(gcnt, cnt), "graph replay changed the counters"
+        del g
+
     c = dict(n=n, nv=int(cnt[1]), nb=int(cnt[4]))
     flags = ra.flags
-    R, K, G = d["num_regions"], d["num_classes"], d["num_groups"]
+    R, K, G = params["num_regions"], params["num_classes"], params["num_groups"]
     bytes_per = {k: byte_model(k, c, plan, R, K, G, flags) for k in avg}
     step_ms = elapsed * 1e3 / args.steps
     total_bytes = sum(bytes_per.values())
     achieved = bytes_per[dom] / (avg[dom] * 1e-3) / 1e9
     roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1),
                 "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                "traffic": traffic_for(dom), "avg_launch_ms": round(avg[dom], 4),
+                "traffic": traffic_for(dom, c["nb"]), "avg_launch_ms": round(avg[dom], 4),
                 "bytes_per_launch": bytes_per[dom]}
     if args.kernels:
         for k in sorted(avg, key=lambda k: -avg[k]):
@@ -274,10 +352,15 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "u64",
         "data": "synthetic",
-        "config": {"workload": WORKLOADS[args.config], "records": n, "record_bytes": 16,
+        "config": {"workload": WORKLOADS[args.config] + ("; overlap step off" if args.no_overlap else ""),
+                   "records": n, "record_bytes": 16,
                    "contexts": int(d["blocks"]) * int(d["warps"]), "regions": R, "classes": K,
-                   "groups": G, "force_full_sort": bool(args.force_full_sort),
+                   "groups": G, "overlap_step": K > 0,
+                   "force_full_sort": bool(args.force_full_sort),
                    "force_event_sort": bool(args.force_event_sort)},
+        "trace": {"valid": c["nv"], "begins": c["nb"], "matched": int(cnt[9]),
+                  "mismatched": int(cnt[10]), "unclosed": int(cnt[11]), "orphan_ends": int(cnt[12]),
+                  "max_level": int(cnt[14])},
         "pipeline": {"bytes_per_record": round(total_bytes / n, 2),
                      "achieved_gbs": round(total_bytes / (step_ms * 1e-3) / 1e9, 1),
                      "frac_of_peak": round(total_bytes / (step_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
@@ -289,10 +372,14 @@ def main() -> int:
         "kernels_ms": {k: round(v, 4) for k, v in sorted(avg.items(), key=lambda kv: -kv[1])
                        if v >= 0.01},
     }
+    if graph is not None:
+        result["graph"] = graph
+    if not args.no_ceiling:
+        result["hbm_ceiling"] = hbm_ceiling(dev)
     if not args.no_cpu_baseline:
-        sample = min(args.cpu_sample, n)
+        sample = min(args.cpu_sample, n) if args.cpu_sample > 0 else n
         err(f"cpu baseline: oracle on {sample} records ...")
-        result["cpu_baseline"] = cpu_baseline(rec_np, d, sample)
+        result["cpu_baseline"] = cpu_baseline(rec_np, d, sample, params)
     print(json.dumps(result), flush=True)
     ra.close()
     return 0

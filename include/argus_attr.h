@@ -2,13 +2,13 @@
  * argus_attr.h -- region attribution over begin/end marker traces on one
  * MI355X (gfx950) GPU.  C ABI, version 1, little-endian.
  *
- * What the library computes (the paper's Section 3.2: code regions are
- * delimited by begin(id)/end(id) transitions; temporal traces recover
- * region-labelled intervals; each warp keeps a nested region-context stack
- * and the innermost active region owns the work.  Section 3.3: the duration
- * signal is read from a reference region trace.  Section 3.5: observed fields
- * and explicit attribution ambiguity.  Section 4.3: compute/communication
- * overlap.):
+ * What the library computes.  It follows the paper's Section 3.2 (regions
+ * are named by their begin and end markers; a time-ordered trace of those
+ * markers yields the intervals of each region; one stack of open regions per
+ * warp decides which region is innermost at any moment), Section 3.3 (a
+ * region's duration comes from its marker trace), Section 3.5 (directly
+ * observed fields, with ambiguity reported rather than hidden) and Section
+ * 4.3 (overlap of compute and communication regions):
  *
  *   1. Validate each record: kind must be BEGIN (1) or END (2) (else
  *      "bad kind"), then region_id must be < num_regions (else "bad region").

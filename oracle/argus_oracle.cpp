@@ -139,9 +139,9 @@ extern "C" int argus_oracle_run(const void* records_v, uint64_t n,
     return a.ts < b.ts;
   });
 
-  // ---- Step 3: per-context nested stack.  (Section 3.2: transitions are
-  // updates to a nested region-context stack for each warp; a begin pushes,
-  // an end closes the innermost active region.)
+  // ---- Step 3: per-context nested stack.  (Section 3.2: every warp keeps
+  // its own stack of open regions; a BEGIN pushes one and an END closes the
+  // one opened most recently.)
   // Readings: an END pops the top of the stack whatever its region
   // ("region-blind"); the pair is MATCHED if the regions agree and
   // MISMATCHED otherwise.  An END on an empty stack is an orphan and leaves

@@ -38,6 +38,27 @@ INSTANCE_DTYPE = np.dtype([
 ])
 
 
+# Fields of the device-side plan (struct DevPlan in csrc/internal.h) read back
+# for measurement: name -> (byte offset, type).  internal.h asserts the same
+# offsets, and a test checks that the two agree.
+PLAN_BYTES = 1728
+PLAN_FIELDS = {
+    "n_records": (0, "<u8"), "n_valid": (8, "<u8"), "n_begin": (16, "<u8"),
+    "rec_ts_bits": (48, "<u4"), "rec_ctx_bits": (52, "<u4"), "rec_wide": (56, "<u4"),
+    "unsorted": (104, "<u4"), "n_ev": (128, "<u8"), "rec_slots": (144, "slots"),
+    "ev_slots": (784, "slots"), "ev_merge": (1432, "<u4"), "merge_rounds": (1440, "<u4"),
+    "merge_end": (1448, "<u8"), "runs": (1712, "<u4"), "n_runs": (1720, "<u8"),
+}
+# C names of the fields above, as internal.h spells them
+PLAN_C_NAMES = {
+    "rec_ts_bits": "rec.ts_bits", "rec_ctx_bits": "rec.ctx_bits", "rec_wide": "rec.wide",
+    "rec_slots": "rs", "ev_slots": "es", "merge_rounds": "m_rounds", "merge_end": "m_end",
+}
+_SLOT = np.dtype([("active", "<u4"), ("pos", "<u4"), ("src", "<u4"), ("dst", "<u4"),
+                  ("lb", "<u4"), ("n_out", "<u4"), ("n_elems", "<u8"), ("tiles", "<u8")])
+assert _SLOT.itemsize == 40
+
+
 class argus_attr_config(ctypes.Structure):
     _fields_ = [("abi_version", ctypes.c_uint32), ("num_regions", ctypes.c_uint32),
                 ("num_classes", ctypes.c_uint32), ("group_shift", ctypes.c_uint32),
@@ -270,19 +291,14 @@ class RegionAttribution:
         t = self.torch
         t.cuda.synchronize(self.device)
         off = ((self._ws.data_ptr() + 255) & ~255) - self._ws.data_ptr()
-        raw = self._ws[off:off + 1728].cpu().numpy()
-        slot = np.dtype([("active", "<u4"), ("pos", "<u4"), ("src", "<u4"), ("dst", "<u4"),
-                         ("lb", "<u4"), ("n_out", "<u4"), ("n_elems", "<u8"), ("tiles", "<u8")])
-        u64 = raw.view(np.uint64)
-        u32 = raw.view(np.uint32)
-        return dict(n_records=int(u64[0]), n_valid=int(u64[1]), n_begin=int(u64[2]),
-                    rec_ts_bits=int(u32[48 // 4]), rec_ctx_bits=int(u32[52 // 4]),
-                    rec_wide=int(u32[56 // 4]), unsorted=int(u32[104 // 4]),
-                    n_ev=int(u64[128 // 8]),
-                    rec_slots=raw[144:784].view(slot).copy(), ev_slots=raw[784:1424].view(slot).copy(),
-                    ev_merge=int(u32[1432 // 4]), merge_rounds=int(u32[1440 // 4]),
-                    merge_end=int(u64[1448 // 8]), runs=int(u32[1712 // 4]),
-                    n_runs=int(u64[1720 // 8]))
+        raw = self._ws[off:off + PLAN_BYTES].cpu().numpy()
+        res = {}
+        for name, (at, dt) in PLAN_FIELDS.items():
+            if dt == "slots":
+                res[name] = raw[at:at + 16 * _SLOT.itemsize].view(_SLOT).copy()
+            else:
+                res[name] = int(raw[at:at + np.dtype(dt).itemsize].view(dt)[0])
+        return res
 
     def set_timing(self, on: bool):
         rc = argus_attr_set_timing(self.h, on)

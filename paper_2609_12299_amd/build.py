@@ -64,6 +64,52 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+def resources() -> str:
+    """Per-kernel register, scratch, occupancy and LDS use as the compiler
+    reports them for gfx950 (device-only compile of every source)."""
+    import re
+    import tempfile
+    rows = []
+    keys = ("VGPRs", "AGPRs", "TotalSGPRs", "ScratchSize [bytes/lane]", "Occupancy [waves/SIMD]",
+            "LDS Size [bytes/block]", "VGPRs Spill")
+    with tempfile.TemporaryDirectory() as tmp:
+        for src in SOURCES:
+            cmd = [hipcc(), *flags(), "--offload-device-only", "-c", os.path.join(CSRC, src),
+                   "-o", os.path.join(tmp, src + ".o"), "-Rpass-analysis=kernel-resource-usage"]
+            r = subprocess.run(cmd, capture_output=True, text=True)
+            if r.returncode != 0:
+                raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr}")
+            cur = None
+            for line in r.stderr.splitlines():
+                m = re.search(r"remark:\s+Function Name: (\S+)", line)
+                if m:
+                    cur = {"kernel": m.group(1), "file": src}
+                    rows.append(cur)
+                    continue
+                for k in keys:
+                    m = re.search(r"remark:\s+" + re.escape(k) + r": (\d+) ", line)
+                    if m and cur is not None:
+                        cur[k] = int(m.group(1))
+    names = [r["kernel"] for r in rows]
+    filt = shutil.which("c++filt") or shutil.which("llvm-cxxfilt")
+    if filt and names:
+        out = subprocess.run([filt], input="\n".join(names), capture_output=True, text=True).stdout
+        for r, d in zip(rows, out.splitlines()):
+            r["kernel"] = d.split("(")[0]
+    head = f"{'kernel':48s} {'file':14s} VGPR AGPR SGPR spill scratch waves/SIMD   LDS B"
+    lines = [head]
+    for r in rows:
+        lines.append(f"{r['kernel'][:48]:48s} {r['file']:14s} {r.get('VGPRs', 0):4d} "
+                     f"{r.get('AGPRs', 0):4d} {r.get('TotalSGPRs', 0):4d} {r.get('VGPRs Spill', 0):5d} "
+                     f"{r.get('ScratchSize [bytes/lane]', 0):7d} "
+                     f"{r.get('Occupancy [waves/SIMD]', 0):10d} "
+                     f"{r.get('LDS Size [bytes/block]', 0):7d}")
+    return "\n".join(lines)
+
+
 if __name__ == "__main__":
-    build(verbose=True)
+    if len(sys.argv) > 1 and sys.argv[1] == "--resources":
+        print(resources())
+    else:
+        build(verbose=True)
     sys.exit(0)

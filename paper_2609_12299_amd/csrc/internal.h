@@ -137,18 +137,27 @@ struct DevPlan {
   uint64_t n_runs;     // runs of one context in the 256-record input chunks
 };
 
-// The Python binding reads the plan back for measurement; keep its layout.
+// The Python binding reads the plan back for measurement (PLAN_FIELDS in
+// attr.py, checked against these lines by a test): keep its layout.
 static_assert(sizeof(KeySpace) == 40, "KeySpace layout");
 static_assert(sizeof(SlotPlan) == 40, "SlotPlan layout");
+static_assert(sizeof(MergeRound) == 32, "MergeRound layout");
+static_assert(offsetof(DevPlan, n_records) == 0, "DevPlan layout");
+static_assert(offsetof(DevPlan, n_valid) == 8, "DevPlan layout");
+static_assert(offsetof(DevPlan, n_begin) == 16, "DevPlan layout");
+static_assert(offsetof(DevPlan, rec.ts_bits) == 48, "DevPlan layout");
+static_assert(offsetof(DevPlan, rec.ctx_bits) == 52, "DevPlan layout");
+static_assert(offsetof(DevPlan, rec.wide) == 56, "DevPlan layout");
 static_assert(offsetof(DevPlan, unsorted) == 104, "DevPlan layout");
 static_assert(offsetof(DevPlan, n_ev) == 128, "DevPlan layout");
 static_assert(offsetof(DevPlan, rs) == 144, "DevPlan layout");
 static_assert(offsetof(DevPlan, es) == 784, "DevPlan layout");
 static_assert(offsetof(DevPlan, ev_merge) == 1432, "DevPlan layout");
+static_assert(offsetof(DevPlan, m_rounds) == 1440, "DevPlan layout");
 static_assert(offsetof(DevPlan, m_end) == 1448, "DevPlan layout");
-static_assert(sizeof(MergeRound) == 32, "MergeRound layout");
 static_assert(offsetof(DevPlan, mr) == 1456, "DevPlan layout");
 static_assert(offsetof(DevPlan, runs) == 1712, "DevPlan layout");
+static_assert(offsetof(DevPlan, n_runs) == 1720, "DevPlan layout");
 static_assert(sizeof(DevPlan) == 1728, "DevPlan layout");
 
 // Per-tile summary written by the matching kernel, read by the resolver.

@@ -39,16 +39,15 @@ __global__ __launch_bounds__(256) void k_tree_lo(TreeArgs a) {
     a.tree[a.leaves + t] = v;
   }
   __syncthreads();
-  // local heap: node j (1 <= j < sub) covers global node (leaves + first) / sub ... ;
-  // global index of local node j at depth d is (a.leaves / sub) * ... computed below.
+  // A heap over this block's `sub` leaves in LDS (node j has children 2j and
+  // 2j + 1; leaves at sub..2sub-1).  Its level of `width` nodes is part of the
+  // global level of width * gridDim.x nodes, at this block's offset.
   for (uint64_t width = sub / 2; width >= 1; width >>= 1) {
     for (uint64_t k = threadIdx.x; k < width; k += 256) {
       const uint64_t node = width + k;
       const int64_t l = s[2 * node], r = s[2 * node + 1];
       const int64_t m = l < r ? l : r;
       s[node] = m;
-      // global node: level with `width` local nodes corresponds to global
-      // level with width * gridDim.x nodes; offset by this block's share.
       const uint64_t gwidth = width * gridDim.x;
       a.tree[gwidth + (uint64_t)blockIdx.x * width + k] = m;
     }

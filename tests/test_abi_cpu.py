@@ -161,3 +161,15 @@ def test_noalloc_scratch_size_matches_header(lib):
     src = open(HEADER).read()
     m = re.search(r"#define ARGUS_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", src)
     assert m and int(m.group(1)) << int(m.group(2)) == lib.NOALLOC_SCRATCH_BYTES
+
+
+def test_plan_fields_match_internal_layout(lib):
+    """The plan fields the binding reads back sit where internal.h asserts them."""
+    src = open(os.path.join(ROOT, "paper_2609_12299_amd", "csrc", "internal.h")).read()
+    asserted = {m.group(1): int(m.group(2)) for m in
+                re.finditer(r"static_assert\(offsetof\(DevPlan, ([a-z_.]+)\) == (\d+)", src)}
+    size = re.search(r"static_assert\(sizeof\(DevPlan\) == (\d+)", src)
+    assert size and int(size.group(1)) == lib.PLAN_BYTES
+    for name, (off, _) in lib.PLAN_FIELDS.items():
+        cname = lib.PLAN_C_NAMES.get(name, name)
+        assert asserted.get(cname) == off, f"{name} ({cname}): binding {off}, header {asserted.get(cname)}"
