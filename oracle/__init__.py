@@ -15,7 +15,7 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SRC = os.path.join(_HERE, "argus_oracle.cpp")
+_SRCS = [os.path.join(_HERE, "argus_oracle.cpp"), os.path.join(_HERE, "argus_oracle_samples.cpp")]
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 NUM_COUNTERS = 32
@@ -41,8 +41,10 @@ def build(force: bool = True) -> str:
     """Compile the oracle with g++ (single-threaded, -O2)."""
     if force or not os.path.exists(_LIB):
         tmp = _LIB + ".tmp"
-        subprocess.check_call(["g++", "-O2", "-std=c++17", "-Wall", "-shared", "-fPIC",
-                               _SRC, "-o", tmp])
+        # no fused multiply-adds: every product is rounded on its own, as the
+        # attribution arithmetic defines
+        subprocess.check_call(["g++", "-O2", "-std=c++17", "-Wall", "-ffp-contract=off",
+                               "-shared", "-fPIC", *_SRCS, "-o", tmp])
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -58,6 +60,11 @@ def _open(path: str):
                   ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint32,
                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64]
+    g = lib.argus_oracle_samples
+    g.restype = ctypes.c_int
+    g.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p, ctypes.c_uint64,
+                  ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
+                  ctypes.c_void_p] + [ctypes.c_void_p] * 8
     return lib
 
 
@@ -79,6 +86,9 @@ class OracleLib:
 
     def run(self, *args, **kw):
         return run(*args, _lib=self._lib, **kw)
+
+    def samples(self, *args, **kw):
+        return samples(*args, _lib=self._lib, **kw)
 
 
 def _ptr(a):
@@ -133,3 +143,44 @@ def run(records: np.ndarray, num_regions: int, num_classes: int = 0, region_clas
 
 def counters_dict(counters: np.ndarray) -> dict:
     return {name: int(counters[i]) for i, name in enumerate(COUNTER_NAMES)}
+
+
+S_COUNTER_NAMES = ["n_samples", "n_bad_pc", "w_total", "w_attributed", "w_unattributed",
+                   "w_inner_unmatched", "n_pairs"]
+SAMPLE_DTYPE = np.dtype([("ts", "<u8"), ("ctx_key", "<u4"), ("pc", "<u4")])
+assert SAMPLE_DTYPE.itemsize == 16
+
+
+def samples(instances: np.ndarray, samples_: np.ndarray, num_regions: int, num_pcs: int,
+            weights=None, metrics=None, _lib=None) -> dict:
+    """PC-sample attribution on host arrays (Section 3.5's alpha, m_hat, H).
+
+    instances: INSTANCE_DTYPE [n] in canonical order; samples_: SAMPLE_DTYPE
+    [S] (or any 16-byte-itemsize array); weights: u32 [S] or None (1 each);
+    metrics: f64 [M, P] or None.  Returns counters [8] u64, n [P, R] u64,
+    alpha [P, R] f64, pc_total [P] u64, pc_owners [P] u32, entropy [P] f64,
+    region_total [R] u64 and mhat [M, R] f64.
+    """
+    inst = np.ascontiguousarray(instances)
+    smp = np.ascontiguousarray(samples_)
+    assert inst.nbytes % 32 == 0 and smp.nbytes % 16 == 0
+    ni, ns = inst.nbytes // 32, smp.nbytes // 16
+    R, P = int(num_regions), int(num_pcs)
+    w = None if weights is None else np.ascontiguousarray(weights, dtype=np.uint32)
+    assert w is None or w.shape == (ns,)
+    m = None if metrics is None else np.ascontiguousarray(metrics, dtype=np.float64).reshape(-1, P)
+    M = 0 if m is None else m.shape[0]
+    out = dict(counters=np.zeros(8, np.uint64), n=np.zeros((P, R), np.uint64),
+               alpha=np.zeros((P, R), np.float64), pc_total=np.zeros(P, np.uint64),
+               pc_owners=np.zeros(P, np.uint32), entropy=np.zeros(P, np.float64),
+               region_total=np.zeros(R, np.uint64), mhat=np.zeros((M, R), np.float64))
+    lib = _lib if _lib is not None else _load()
+    rc = lib.argus_oracle_samples(_ptr(inst) if ni else None, ni, _ptr(smp) if ns else None, ns,
+                                  _ptr(w), R, P, M, _ptr(m) if M else None,
+                                  _ptr(out["counters"]), _ptr(out["n"]), _ptr(out["alpha"]),
+                                  _ptr(out["pc_total"]), _ptr(out["pc_owners"]),
+                                  _ptr(out["entropy"]), _ptr(out["region_total"]),
+                                  _ptr(out["mhat"]) if M else None)
+    if rc != 0:
+        raise ValueError(f"argus_oracle_samples failed with {rc}")
+    return out

@@ -102,6 +102,54 @@ int argus_oracle_run(const void* records, uint64_t n, uint32_t num_regions,
                      void* instances, uint64_t* instance_excl,
                      uint64_t inst_cap);
 
+/* ------------------------------------------------------------------------
+ * PC-sample attribution (Section 3.2: the innermost active region of the
+ * executing warp receives each execution count; Section 3.5: count-weighted
+ * lifting of PC-keyed metrics into regions, with association entropy as
+ * ambiguity metadata).
+ *
+ *   sample (16 B): u64 ts @0, u32 ctx_key @8, u32 pc @12.
+ *
+ *   instances      n_inst instances in canonical order (as argus_oracle_run
+ *                  writes them).
+ *   samples        n_samples samples; weights [n_samples] executions per
+ *                  sample, or NULL for 1 each.
+ *   num_regions    R; num_pcs P (a sample with pc >= P is counted as bad and
+ *                  takes no further part); num_metrics M; metrics [M * P]
+ *                  (metric k of pc p at k * P + p), may be NULL iff M == 0.
+ * Outputs (all required except alpha and mhat when M == 0):
+ *   counters       [ORC_S_NUM_COUNTERS]
+ *   n_rp           [P * R]  n(r, p) at p * R + r
+ *   alpha          [P * R]  alpha(r, p) = n(r, p) / T(p), 0 where n == 0; or NULL
+ *   pc_total       [P]      T(p) = sum over r of n(r, p)
+ *   pc_owners      [P]      regions r with n(r, p) > 0
+ *   entropy        [P]      H(p) = -sum over r with n > 0 of alpha log alpha
+ *                           (natural log; 0 when T(p) == 0)
+ *   region_total   [R]      sum over p of n(r, p)
+ *   mhat           [M * R]  sum over p with n(r, p) > 0 of alpha(r, p) m(p),
+ *                           in increasing p; or NULL when M == 0
+ * Returns 0, or -1 for bad arguments. */
+enum {
+  ORC_S_N_SAMPLES = 0,       /* sample records */
+  ORC_S_N_BAD_PC = 1,        /* samples with pc >= P */
+  ORC_S_W_TOTAL = 2,         /* weight of the samples with a valid pc */
+  ORC_S_W_ATTRIBUTED = 3,    /* weight given to a matched instance */
+  ORC_S_W_UNATTRIBUTED = 4,  /* weight with no matched active instance */
+  ORC_S_W_INNER_UNMATCHED = 5, /* attributed weight whose innermost active
+                                  instance was mismatched or unclosed */
+  ORC_S_N_PAIRS = 6,         /* (r, p) with n(r, p) > 0 */
+  ORC_S_NUM_COUNTERS = 8
+};
+
+int argus_oracle_samples(const void* instances, uint64_t n_inst,
+                         const void* samples, uint64_t n_samples,
+                         const uint32_t* weights, uint32_t num_regions,
+                         uint32_t num_pcs, uint32_t num_metrics,
+                         const double* metrics, uint64_t* counters,
+                         uint64_t* n_rp, double* alpha, uint64_t* pc_total,
+                         uint32_t* pc_owners, double* entropy,
+                         uint64_t* region_total, double* mhat);
+
 #ifdef __cplusplus
 }
 #endif

@@ -1,10 +1,11 @@
 """The pins must catch plausible mistakes in the oracle.
 
-Each mutant is a one-line textual change to a COPY of oracle/argus_oracle.cpp
-(a dropped term, a wrong sign, index or comparison), compiled into a temporary
-library.  The pin checks (hand-built traces, the depth-scan derivation, the
-brute-force overlap, generator ground truth and invariants) are run against
-it and at least one of them must fail.  The real oracle is never modified.
+Each mutant is a one-line textual change to a COPY of one oracle source
+(a dropped term, a wrong sign, index or comparison), compiled with the other
+source into a temporary library.  The pin checks (hand-built traces, the
+depth-scan derivation, the brute-force overlap and owner searches, closed
+forms and invariants) are run against it and at least one of them must fail.
+The real oracle is never modified.
 """
 from __future__ import annotations
 
@@ -21,6 +22,27 @@ from test_oracle_pins import brute_force_overlap, check_invariants, scan_derivat
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "argus_oracle.cpp")
+SRC_S = os.path.join(ROOT, "oracle", "argus_oracle_samples.cpp")
+
+# one-line mutants of the sample attribution (argus_oracle_samples.cpp)
+MUTANTS_S = {
+    "end_inclusive": ("ends[ei].first <= t; ++ei)", "ends[ei].first < t; ++ei)"),
+    "begin_exclusive": ("begins[bi].first <= t; ++bi)", "begins[bi].first < t; ++bi)"),
+    "owner_not_required_matched": ("if (is_matched(inst[a->second])) {", "if (true) {"),
+    "outermost_owner": ("for (auto a = active.rbegin(); a != active.rend(); ++a) {",
+                        "for (auto a = active.begin(); a != active.end(); ++a) {"),
+    "weights_ignored": ("const uint64_t w = weights ? weights[i] : 1;", "const uint64_t w = 1;"),
+    "owner_parent_region": ("n_rp[uint64_t(smp[i].pc) * R + inst[owner].region] += w;",
+                            "n_rp[uint64_t(smp[i].pc) * R + inst[inst[owner].parent == 0xFFFFFFFFu"
+                            " ? owner : inst[owner].parent].region] += w;"),
+    "entropy_sign": ("if (row[r] > 0) h -= a * std::log(a);", "if (row[r] > 0) h += a * std::log(a);"),
+    "alpha_over_owners": ("const double a = row[r] > 0 ? double(row[r]) / double(T) : 0.0;",
+                          "const double a = row[r] > 0 ? double(row[r]) / double(owners) : 0.0;"),
+    "mhat_unweighted": ("const double term = a * metrics[k * P + p];",
+                        "const double term = metrics[k * P + p];"),
+    "bad_pc_not_counted": ("counters[ORC_S_N_BAD_PC] += 1;", "counters[ORC_S_N_BAD_PC] += 0;"),
+    "ctx_ignored": ("auto it = inst_of.find(kv.first);", "auto it = inst_of.begin();"),
+}
 
 MUTANTS = {
     "parent_dropped": ("x.parent = stack.empty() ? kNone : stack.back();", "x.parent = kNone;"),
@@ -104,6 +126,26 @@ def run_pins(orc) -> list[str]:
     return failures
 
 
+def run_sample_pins(orc) -> list[str]:
+    """The sample-attribution pins of test_oracle_samples against `orc`."""
+    import test_oracle_samples as ts
+    failures = []
+    checks = [("hand_nested", lambda: ts.test_hand_nested_shared_helper(orc)),
+              ("hand_mismatched", lambda: ts.test_hand_mismatched_innermost(orc)),
+              ("hand_unclosed", lambda: ts.test_hand_unclosed_and_zero_length(orc)),
+              ("hand_weights", lambda: ts.test_hand_weights_contexts_and_bad_pcs(orc)),
+              ("entropy_closed_forms", lambda: ts.test_entropy_closed_forms(orc))]
+    checks += [(f"brute_force_owner_{k}", (lambda k=k: ts.test_brute_force_owner(orc, k)))
+               for k in range(40)]
+    checks += [(f"invariants_{k}", (lambda k=k: ts.test_invariants(orc, k))) for k in range(10)]
+    for name, fn in checks:
+        try:
+            fn()
+        except Exception:  # noqa: BLE001 - any failure kills the mutant
+            failures.append(name)
+    return failures
+
+
 @pytest.fixture(scope="module")
 def mutant_dir(tmp_path_factory):
     return tmp_path_factory.mktemp("oracle_mutants")
@@ -111,19 +153,32 @@ def mutant_dir(tmp_path_factory):
 
 def test_unmutated_oracle_passes_all_pins(oracle_mod):
     assert run_pins(oracle_mod) == []
+    assert run_sample_pins(oracle_mod) == []
+
+
+def _build_mutant(mutant_dir, name, target, old, new):
+    src = open(target).read()
+    assert src.count(old) == 1, f"mutation site for {name} not unique"
+    path = os.path.join(str(mutant_dir), f"{name}.cpp")
+    with open(path, "w") as f:
+        f.write(src.replace(old, new))
+    other = SRC_S if target == SRC else SRC
+    inc = os.path.join(ROOT, "oracle")
+    lib = os.path.join(str(mutant_dir), f"lib{name}.so")
+    subprocess.check_call(["g++", "-O1", "-std=c++17", "-ffp-contract=off", "-shared", "-fPIC",
+                           "-I", inc, path, other, "-o", lib])
+    return lib
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
 def test_mutant_is_caught(oracle_mod, mutant_dir, name):
     old, new = MUTANTS[name]
-    src = open(SRC).read()
-    assert src.count(old) == 1, f"mutation site for {name} not unique"
-    path = os.path.join(str(mutant_dir), f"{name}.cpp")
-    with open(path, "w") as f:
-        f.write(src.replace(old, new))
-    inc = os.path.join(ROOT, "oracle")
-    lib = os.path.join(str(mutant_dir), f"lib{name}.so")
-    subprocess.check_call(["g++", "-O1", "-std=c++17", "-shared", "-fPIC", "-I", inc, path,
-                           "-o", lib])
-    orc = oracle_mod.OracleLib(lib)
+    orc = oracle_mod.OracleLib(_build_mutant(mutant_dir, name, SRC, old, new))
     assert run_pins(orc), f"mutant {name} survived every pin"
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS_S))
+def test_sample_mutant_is_caught(oracle_mod, mutant_dir, name):
+    old, new = MUTANTS_S[name]
+    orc = oracle_mod.OracleLib(_build_mutant(mutant_dir, name, SRC_S, old, new))
+    assert run_sample_pins(orc), f"mutant {name} survived every pin"
