@@ -223,6 +223,86 @@ int argus_attr_run(argus_attr* h, const argus_record* d_records, uint64_t n_reco
 int argus_attr_run_noalloc(argus_attr* h, const argus_record* d_records, uint64_t n_records,
                            const argus_attr_outputs* out, void* stream);
 
+/* ------------------------------------------------ PC-sample attribution */
+/* Lifting of PC-keyed measurements into region space (the paper's Section
+ * 3.2: a mapping run replays each warp's stack of open regions, and every
+ * execution of the instruction at a PC counts for the region innermost at
+ * that moment; Section 3.5: count-weighted attribution with association
+ * entropy as ambiguity metadata).  Works on the instance array that
+ * argus_attr_run wrote.
+ *
+ * One sample is one or more executions of the instruction with index `pc`
+ * (0 <= pc < num_pcs) at time `ts` in context `ctx_key`.  Its owner is the
+ * innermost MATCHED instance of that context active at ts (t_begin <= ts <
+ * t_end; an unclosed instance is active from t_begin on and never owns).
+ * Then, with n(r, p) the executions of p owned by region r and
+ * T(p) = sum over r of n(r, p):
+ *   alpha(r, p) = n(r, p) / T(p)              (0 where n(r, p) == 0)
+ *   H(p)        = - sum over r with n(r, p) > 0 of alpha log alpha  (natural log)
+ *   m_hat(r)    = sum over p with n(r, p) > 0 of alpha(r, p) * m(p)
+ * in IEEE double: each alpha is one correctly rounded division; m_hat adds
+ * the rounded products one at a time in increasing p (so the result is
+ * reproducible bit for bit); H is summed in an unspecified order and
+ * carries the error of the device logarithm (a few ulp per term). */
+typedef struct argus_sample {
+  uint64_t ts;      /* cycles of the context's clock, as in the records */
+  uint32_t ctx_key;
+  uint32_t pc;      /* instruction index, < num_pcs (else counted as bad) */
+} argus_sample;     /* 16 bytes, 16-byte aligned */
+
+enum {
+  ARGUS_S_N_SAMPLES = 0,         /* sample records */
+  ARGUS_S_N_BAD_PC = 1,          /* samples with pc >= num_pcs (no further part) */
+  ARGUS_S_W_TOTAL = 2,           /* executions (weights) of the other samples */
+  ARGUS_S_W_ATTRIBUTED = 3,      /* executions given to a matched instance */
+  ARGUS_S_W_UNATTRIBUTED = 4,    /* executions with no matched active instance */
+  ARGUS_S_W_INNER_UNMATCHED = 5, /* attributed executions whose innermost active
+                                    instance was mismatched or unclosed */
+  ARGUS_S_N_PAIRS = 6,           /* (r, p) with n(r, p) > 0 */
+  ARGUS_S_W_BAD_INSTANCE = 7,    /* executions whose owner has region_id >= num_regions
+                                    (instances of another configuration); not counted
+                                    anywhere else; 0 for instances of a run with this R */
+  ARGUS_S_NUM_COUNTERS = 8
+};
+
+typedef struct argus_samples_config {
+  uint32_t abi_version; /* ARGUS_ATTR_ABI_VERSION */
+  uint32_t num_regions; /* R, 1..65535: the R of the run that wrote the instances */
+  uint32_t num_pcs;     /* P, 1..2^24, with P * R <= 2^31 */
+  uint32_t num_metrics; /* M, 0..64: PC-keyed additive metrics to lift */
+} argus_samples_config;
+
+/* All pointers are device memory, caller-owned, 16-byte aligned where they
+ * hold 16-byte elements. */
+typedef struct argus_samples_io {
+  const argus_instance* d_instances; /* canonical order, as argus_attr_run writes it */
+  const uint64_t* d_n_instances;     /* device scalar: instances in the array, e.g.
+                                        &d_counters[ARGUS_C_N_BEGIN] of that run (read on
+                                        the device, so no host synchronisation) */
+  uint64_t max_instances;            /* capacity of d_instances; at most this many are read */
+  const argus_sample* d_samples;     /* [n_samples] */
+  uint64_t n_samples;
+  const uint32_t* d_weights;         /* [n_samples] executions per sample; NULL: 1 each */
+  const double* d_metrics;           /* [M][P] m(p); may be NULL iff M == 0 */
+  uint64_t* d_counters;              /* out [ARGUS_S_NUM_COUNTERS] */
+  uint64_t* d_n;                     /* out [P][R] n(r, p) */
+  double* d_alpha;                   /* out [P][R] alpha(r, p) */
+  uint64_t* d_pc_total;              /* out [P] T(p) */
+  uint32_t* d_pc_owners;             /* out [P] regions with n(r, p) > 0 */
+  double* d_entropy;                 /* out [P] H(p); 0 when T(p) == 0 */
+  uint64_t* d_region_total;          /* out [R] sum over p of n(r, p) */
+  double* d_mhat;                    /* out [M][R] m_hat(r); may be NULL iff M == 0 */
+} argus_samples_io;
+
+/* Enqueue the attribution on `stream` and return without synchronising;
+ * every output is initialised on the stream and valid once it completes.
+ * Allocates nothing.  Argument errors (ARGUS_E_INVAL, ARGUS_E_ABI,
+ * ARGUS_E_ALIGN, ARGUS_E_CAPACITY) are returned before any GPU call;
+ * ARGUS_E_DEVICE if the current device is not gfx950, ARGUS_E_HIP if a
+ * launch fails. */
+int argus_attr_samples(const argus_samples_config* cfg, const argus_samples_io* io,
+                       void* stream);
+
 /* Destroy a handle; NULL is a no-op. */
 void argus_attr_destroy(argus_attr* h);
 

@@ -3,25 +3,27 @@
 The data-parallel core of the evidence join of "Argus: Orchestrating
 Cross-Layer GPU Performance Measurements around Semantic Regions"
 (arxiv 2609.12299): marker records become region instances with nesting,
-per-region duration statistics, class overlap and ambiguity counts, computed
-by hand-written HIP kernels for gfx950 behind a C ABI (include/argus_attr.h).
+per-region duration statistics, class overlap and ambiguity counts, and PC
+samples are attributed to those instances, computed by hand-written HIP
+kernels for gfx950 behind a C ABI (include/argus_attr.h).
 """
-from .attr import (ABI_VERSION, COUNTER_NAMES, NOALLOC_SCRATCH_BYTES, FORCE_EVENT_SORT, FORCE_FULL_SORT, FORCE_RECORD_RADIX,
-                   INSTANCE_DTYPE, NUM_COUNTERS,
-                   OUT_INSTANCE_EXCL, OUT_INSTANCES, RS_WIDTH, ArgusError, RegionAttribution,
-                   argus_attr_config, argus_attr_create, argus_attr_destroy,
-                   argus_attr_kernel_times, argus_attr_last_error, argus_attr_outputs,
-                   argus_attr_run, argus_attr_run_noalloc, argus_attr_set_timing, argus_attr_set_timing_filter,
-                   argus_attr_workspace_bytes,
-                   load_library, to_host)
+from .attr import (ABI_VERSION, COUNTER_NAMES, FORCE_EVENT_SORT, FORCE_FULL_SORT,
+                   FORCE_RECORD_RADIX, INSTANCE_DTYPE, NOALLOC_SCRATCH_BYTES, NUM_COUNTERS,
+                   OUT_INSTANCE_EXCL, OUT_INSTANCES, RS_WIDTH, S_COUNTER_NAMES, SAMPLE_DTYPE,
+                   ArgusError, RegionAttribution, argus_attr_config, argus_attr_create,
+                   argus_attr_destroy, argus_attr_kernel_times, argus_attr_last_error,
+                   argus_attr_outputs, argus_attr_run, argus_attr_run_noalloc,
+                   argus_attr_samples, argus_attr_set_timing, argus_attr_set_timing_filter,
+                   argus_attr_workspace_bytes, argus_samples_config, argus_samples_io,
+                   attribute_samples, load_library, to_host)
 
 __all__ = [
-    "ABI_VERSION", "COUNTER_NAMES", "NOALLOC_SCRATCH_BYTES", "FORCE_EVENT_SORT", "FORCE_FULL_SORT", "FORCE_RECORD_RADIX",
-    "INSTANCE_DTYPE", "NUM_COUNTERS",
-    "OUT_INSTANCE_EXCL", "OUT_INSTANCES", "RS_WIDTH", "ArgusError", "RegionAttribution",
-    "argus_attr_config", "argus_attr_create", "argus_attr_destroy", "argus_attr_kernel_times",
-    "argus_attr_last_error", "argus_attr_outputs", "argus_attr_run", "argus_attr_run_noalloc",
-    "argus_attr_set_timing",
-    "argus_attr_set_timing_filter",
-    "argus_attr_workspace_bytes", "load_library", "to_host",
+    "ABI_VERSION", "COUNTER_NAMES", "FORCE_EVENT_SORT", "FORCE_FULL_SORT", "FORCE_RECORD_RADIX",
+    "INSTANCE_DTYPE", "NOALLOC_SCRATCH_BYTES", "NUM_COUNTERS", "OUT_INSTANCE_EXCL",
+    "OUT_INSTANCES", "RS_WIDTH", "S_COUNTER_NAMES", "SAMPLE_DTYPE", "ArgusError",
+    "RegionAttribution", "argus_attr_config", "argus_attr_create", "argus_attr_destroy",
+    "argus_attr_kernel_times", "argus_attr_last_error", "argus_attr_outputs", "argus_attr_run",
+    "argus_attr_run_noalloc", "argus_attr_samples", "argus_attr_set_timing",
+    "argus_attr_set_timing_filter", "argus_attr_workspace_bytes", "argus_samples_config",
+    "argus_samples_io", "attribute_samples", "load_library", "to_host",
 ]

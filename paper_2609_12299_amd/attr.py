@@ -72,7 +72,30 @@ class argus_attr_outputs(ctypes.Structure):
                 ("d_instances", ctypes.c_void_p), ("d_instance_excl", ctypes.c_void_p)]
 
 
+class argus_samples_config(ctypes.Structure):
+    _fields_ = [("abi_version", ctypes.c_uint32), ("num_regions", ctypes.c_uint32),
+                ("num_pcs", ctypes.c_uint32), ("num_metrics", ctypes.c_uint32)]
+
+
+class argus_samples_io(ctypes.Structure):
+    _fields_ = [("d_instances", ctypes.c_void_p), ("d_n_instances", ctypes.c_void_p),
+                ("max_instances", ctypes.c_uint64), ("d_samples", ctypes.c_void_p),
+                ("n_samples", ctypes.c_uint64), ("d_weights", ctypes.c_void_p),
+                ("d_metrics", ctypes.c_void_p), ("d_counters", ctypes.c_void_p),
+                ("d_n", ctypes.c_void_p), ("d_alpha", ctypes.c_void_p),
+                ("d_pc_total", ctypes.c_void_p), ("d_pc_owners", ctypes.c_void_p),
+                ("d_entropy", ctypes.c_void_p), ("d_region_total", ctypes.c_void_p),
+                ("d_mhat", ctypes.c_void_p)]
+
+
+S_NUM_COUNTERS = 8
+S_COUNTER_NAMES = ["n_samples", "n_bad_pc", "w_total", "w_attributed", "w_unattributed",
+                   "w_inner_unmatched", "n_pairs", "w_bad_instance"]
+SAMPLE_DTYPE = np.dtype([("ts", "<u8"), ("ctx_key", "<u4"), ("pc", "<u4")])
+
 assert ctypes.sizeof(argus_attr_config) == 40
+assert ctypes.sizeof(argus_samples_config) == 16
+assert ctypes.sizeof(argus_samples_io) == 120
 assert ctypes.sizeof(argus_attr_outputs) == 48
 
 _lib = None
@@ -97,6 +120,9 @@ def load_library(path: str = LIB_PATH):
     lib.argus_attr_run.restype = i32
     lib.argus_attr_run_noalloc.argtypes = [vp, vp, u64, ctypes.POINTER(argus_attr_outputs), vp]
     lib.argus_attr_run_noalloc.restype = i32
+    lib.argus_attr_samples.argtypes = [ctypes.POINTER(argus_samples_config),
+                                       ctypes.POINTER(argus_samples_io), vp]
+    lib.argus_attr_samples.restype = i32
     lib.argus_attr_destroy.argtypes = [vp]
     lib.argus_attr_destroy.restype = None
     lib.argus_attr_last_error.argtypes = [vp]
@@ -136,6 +162,50 @@ def argus_attr_run_noalloc(h, d_records: int, n_records: int, out: argus_attr_ou
     return load_library().argus_attr_run_noalloc(h, d_records, n_records,
                                                  ctypes.byref(out) if out is not None else None,
                                                  stream)
+
+
+def argus_attr_samples(cfg: argus_samples_config, io: argus_samples_io, stream: int) -> int:
+    return load_library().argus_attr_samples(ctypes.byref(cfg) if cfg is not None else None,
+                                             ctypes.byref(io) if io is not None else None, stream)
+
+
+def attribute_samples(instances, n_instances, samples, num_regions: int, num_pcs: int,
+                      weights=None, metrics=None, stream=None) -> dict:
+    """argus_attr_samples on torch CUDA tensors.
+
+    instances: the instance tensor argus_attr_run wrote (uint8 [cap, 32]);
+    n_instances: a 1-element uint64 CUDA tensor holding the instance count
+    (e.g. counters[4:5] of that run); samples: uint8 [S, 16] (or any 16-byte
+    records); weights: uint32 [S] or None; metrics: float64 [M, P] or None.
+    Returns the output tensors (valid once the stream has completed)."""
+    import torch
+    dev = samples.device
+    R, P = int(num_regions), int(num_pcs)
+    M = 0 if metrics is None else int(metrics.shape[0])
+    ns = samples.numel() * samples.element_size() // 16
+    cap = instances.numel() * instances.element_size() // 32
+    out = dict(counters=torch.empty(S_NUM_COUNTERS, dtype=torch.uint64, device=dev),
+               n=torch.empty((P, R), dtype=torch.uint64, device=dev),
+               alpha=torch.empty((P, R), dtype=torch.float64, device=dev),
+               pc_total=torch.empty(P, dtype=torch.uint64, device=dev),
+               pc_owners=torch.empty(P, dtype=torch.uint32, device=dev),
+               entropy=torch.empty(P, dtype=torch.float64, device=dev),
+               region_total=torch.empty(R, dtype=torch.uint64, device=dev),
+               mhat=torch.empty((M, R), dtype=torch.float64, device=dev))
+    cfg = argus_samples_config(ABI_VERSION, R, P, M)
+    io = argus_samples_io(instances.data_ptr() if cap else None, n_instances.data_ptr(), cap,
+                          samples.data_ptr() if ns else None, ns,
+                          weights.data_ptr() if weights is not None else None,
+                          metrics.data_ptr() if M else None,
+                          out["counters"].data_ptr(), out["n"].data_ptr(),
+                          out["alpha"].data_ptr(), out["pc_total"].data_ptr(),
+                          out["pc_owners"].data_ptr(), out["entropy"].data_ptr(),
+                          out["region_total"].data_ptr(), out["mhat"].data_ptr() if M else None)
+    s = stream if stream is not None else torch.cuda.current_stream(dev)
+    rc = argus_attr_samples(cfg, io, s.cuda_stream)
+    if rc != 0:
+        raise ArgusError(rc, "argus_attr_samples rejected its arguments")
+    return out
 
 
 def argus_attr_destroy(h) -> None:

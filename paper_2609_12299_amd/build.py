@@ -16,7 +16,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libargus_attr.so")
 SOURCES = ["attr_host.hip", "k_ingest.hip", "k_radix.hip", "k_match.hip", "k_resolve.hip", "k_merge.hip",
-           "k_agg.hip", "k_overlap.hip"]
+           "k_agg.hip", "k_overlap.hip", "k_samples.hip"]
 ARCH = "gfx950"
 
 
@@ -40,9 +40,13 @@ def flags() -> list[str]:
     ]
 
 
+# per-source flags: the sample attribution rounds every product on its own
+FILE_FLAGS = {"k_samples.hip": ["-ffp-contract=off"]}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc(), *flags(), "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [hipcc(), *flags(), *FILE_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr}")
@@ -74,7 +78,8 @@ def resources() -> str:
             "LDS Size [bytes/block]", "VGPRs Spill")
     with tempfile.TemporaryDirectory() as tmp:
         for src in SOURCES:
-            cmd = [hipcc(), *flags(), "--offload-device-only", "-c", os.path.join(CSRC, src),
+            cmd = [hipcc(), *flags(), *FILE_FLAGS.get(src, []), "--offload-device-only", "-c",
+                   os.path.join(CSRC, src),
                    "-o", os.path.join(tmp, src + ".o"), "-Rpass-analysis=kernel-resource-usage"]
             r = subprocess.run(cmd, capture_output=True, text=True)
             if r.returncode != 0:

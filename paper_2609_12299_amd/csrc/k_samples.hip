@@ -1,0 +1,304 @@
+// k_samples.hip -- PC samples attributed to region instances, and PC-keyed
+// metrics lifted into regions.
+//
+// The paper's Section 3.2 maps PC-keyed evidence to regions with a separate
+// mapping run: each warp's region transitions are replayed as a stack of
+// open regions, and an execution of the instruction at PC p counts for the
+// region that is innermost at that moment.  Section 3.5 turns the counts
+// n(r, p) into weights alpha(r, p) = n(r, p) / sum_r' n(r', p), lifts an
+// additive metric as m_hat(r) = sum_p alpha(r, p) m(p) and reports the
+// association entropy H(p) = -sum_r alpha log alpha.
+//
+// Here the stacks are already resolved: argus_attr_run wrote every instance
+// with its interval, level and parent, in (context, begin time) order.  So
+// the instances active at time t in a context are exactly the ancestors (or
+// self) of the last instance of that context that began at or before t
+// which have not ended by t: one binary search and a short walk up the
+// parent links give a sample's owner, the innermost matched active
+// instance.  The counts go to a dense [P][R] table with 64-bit atomics
+// (integer, so the order of the adds does not matter).  Per PC one wave
+// forms T(p), alpha, the owner count and H(p); per region one thread adds
+// alpha * m(p) in increasing p with separately rounded products: a fixed
+// rounding order, so m_hat is reproducible bit for bit.
+#include <string.h>
+
+#include <mutex>
+
+#include "internal.h"
+
+// Every product is rounded before it is added: hipcc would otherwise fuse
+// a * b + c into one fused multiply-add, which rounds once (the file is
+// also built with -ffp-contract=off).
+#pragma clang fp contract(off)
+
+namespace argus {
+
+struct SampArgs {
+  const argus_instance* inst;
+  const uint64_t* n_inst;
+  uint64_t max_inst;
+  const uint4* smp;
+  uint64_t ns;
+  const uint32_t* w;
+  const double* metrics;
+  uint32_t R, P, M;
+  uint64_t* counters;
+  uint64_t* n;
+  double* alpha;
+  uint64_t* pc_total;
+  uint32_t* owners;
+  double* entropy;
+  uint64_t* region_total;
+  double* mhat;
+};
+
+constexpr int kSampThreads = 256;
+
+// Zero the count table and the counters (a fill kernel: no memset node when
+// the caller captures the launch in a graph).
+__global__ __launch_bounds__(kSampThreads) void k_s_clear(SampArgs a) {
+  const uint64_t total = (uint64_t)a.P * a.R;
+  const uint64_t stride = (uint64_t)gridDim.x * kSampThreads;
+  for (uint64_t i = (uint64_t)blockIdx.x * kSampThreads + threadIdx.x; i < total; i += stride)
+    a.n[i] = 0;
+  if (blockIdx.x == 0 && threadIdx.x < ARGUS_S_NUM_COUNTERS) a.counters[threadIdx.x] = 0;
+}
+
+// Sum of a per-thread u64 over the block, added to *dst by one thread.
+__device__ __forceinline__ void block_add(uint64_t v, uint64_t* dst, uint64_t* s_part) {
+  v = row_sum64(v);
+  v = rows_sum64(v);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) s_part[w] = v;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint64_t t = 0;
+    for (int k = 0; k < kSampThreads / 64; ++k) t += s_part[k];
+    if (t) atomicAdd((unsigned long long*)dst, (unsigned long long)t);
+  }
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(kSampThreads) void k_s_join(SampArgs a) {
+  __shared__ uint64_t s_part[kSampThreads / 64];
+  const uint64_t avail = *a.n_inst;
+  const uint64_t ni = avail < a.max_inst ? avail : a.max_inst;
+  const uint4* inst = reinterpret_cast<const uint4*>(a.inst);  // two uint4 per instance
+  uint64_t bad = 0, wt = 0, watt = 0, wun = 0, winner = 0, wbadi = 0;
+  const uint64_t stride = (uint64_t)gridDim.x * kSampThreads;
+  for (uint64_t i = (uint64_t)blockIdx.x * kSampThreads + threadIdx.x; i < a.ns; i += stride) {
+    const uint4 s = a.smp[i];
+    const uint64_t ts = (uint64_t)s.x | ((uint64_t)s.y << 32);
+    const uint32_t ctx = s.z, pc = s.w;
+    const uint64_t w = a.w ? (uint64_t)a.w[i] : 1ull;
+    if (pc >= a.P) {
+      bad += 1;
+      continue;
+    }
+    wt += w;
+    // First instance whose (context, begin time) exceeds (ctx, ts).
+    uint64_t lo = 0, hi = ni;
+    while (lo < hi) {
+      const uint64_t mid = (lo + hi) >> 1;
+      const uint4 h0 = inst[2 * mid];      // t_begin, t_end
+      const uint32_t c = inst[2 * mid + 1].x;  // ctx_key
+      const uint64_t tb = (uint64_t)h0.x | ((uint64_t)h0.y << 32);
+      const bool gt = c > ctx || (c == ctx && tb > ts);
+      if (gt) hi = mid;
+      else lo = mid + 1;
+    }
+    // Walk up from the last instance that began at or before ts: the active
+    // ones are its ancestors (or itself) that have not ended by ts; the
+    // first matched one among them is the owner.
+    int64_t owner_region = -1;
+    bool inner = false;
+    uint64_t x = lo;  // one past the candidate
+    while (x > 0) {
+      const uint64_t y = x - 1;
+      const uint4 h0 = inst[2 * y];
+      const uint4 h1 = inst[2 * y + 1];  // ctx, parent, level, region | end_region << 16
+      if (h1.x != ctx) break;
+      const uint64_t t_end = (uint64_t)h0.z | ((uint64_t)h0.w << 32);
+      const uint32_t reg = h1.w & 0xFFFFu, ereg = h1.w >> 16;
+      const bool closed = ereg != kNoEnd;
+      if (!closed || ts < t_end) {
+        if (closed && ereg == reg) {
+          owner_region = reg < a.R ? (int64_t)reg : -2;  // -2: not an instance of this R
+          break;
+        }
+        inner = true;
+      }
+      // parents precede their children; anything else ends the walk
+      if (h1.y >= y) break;
+      x = (uint64_t)h1.y + 1;
+    }
+    if (owner_region < 0) {
+      if (owner_region == -2) wbadi += w;
+      else wun += w;
+      continue;
+    }
+    watt += w;
+    if (inner) winner += w;
+    atomicAdd((unsigned long long*)&a.n[(uint64_t)pc * a.R + (uint64_t)owner_region],
+              (unsigned long long)w);
+  }
+  block_add(bad, &a.counters[ARGUS_S_N_BAD_PC], s_part);
+  block_add(wt, &a.counters[ARGUS_S_W_TOTAL], s_part);
+  block_add(watt, &a.counters[ARGUS_S_W_ATTRIBUTED], s_part);
+  block_add(wun, &a.counters[ARGUS_S_W_UNATTRIBUTED], s_part);
+  block_add(winner, &a.counters[ARGUS_S_W_INNER_UNMATCHED], s_part);
+  block_add(wbadi, &a.counters[ARGUS_S_W_BAD_INSTANCE], s_part);
+  if (blockIdx.x == 0 && threadIdx.x == 0) a.counters[ARGUS_S_N_SAMPLES] = a.ns;
+}
+
+// One wave per PC: T(p), the owners, alpha (one rounded division each) and
+// H(p) (per-lane sums, then a fixed butterfly over the wave).
+__global__ __launch_bounds__(kSampThreads) void k_s_pc(SampArgs a) {
+  const uint64_t wave = ((uint64_t)blockIdx.x * kSampThreads + threadIdx.x) >> 6;
+  const uint64_t nwaves = (uint64_t)gridDim.x * (kSampThreads / 64);
+  const uint32_t lane = threadIdx.x & 63;
+  uint64_t pairs = 0;
+  for (uint64_t p = wave; p < a.P; p += nwaves) {
+    const uint64_t* row = a.n + p * a.R;
+    uint64_t t = 0;
+    uint32_t own = 0;
+    for (uint32_t r = lane; r < a.R; r += 64) {
+      const uint64_t v = row[r];
+      t += v;
+      own += v != 0;
+    }
+    t = rows_sum64(row_sum64(t));
+    own = rows_sum32(row_sum32(own));
+    const double td = (double)t;
+    double h = 0.0;
+    double* arow = a.alpha + p * a.R;
+    for (uint32_t r = lane; r < a.R; r += 64) {
+      const uint64_t v = row[r];
+      double al = 0.0;
+      if (v) {
+        al = (double)v / td;
+        const double t_h = al * log(al);
+        h = h - t_h;
+      }
+      arow[r] = al;
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) h = h + __shfl_xor(h, off);
+    if (lane == 0) {
+      a.pc_total[p] = t;
+      a.owners[p] = own;
+      a.entropy[p] = h;
+    }
+    pairs += own;
+  }
+  if (lane == 0 && pairs)
+    atomicAdd((unsigned long long*)&a.counters[ARGUS_S_N_PAIRS], (unsigned long long)pairs);
+}
+
+// One thread per region: its total count, and each lifted metric as the
+// products alpha(r, p) * m(p), each rounded, added one at a time in
+// increasing p over the p that region r owns a share of.
+__global__ __launch_bounds__(kSampThreads) void k_s_region(SampArgs a) {
+  const uint64_t r = (uint64_t)blockIdx.x * kSampThreads + threadIdx.x;
+  if (r >= a.R) return;
+  uint64_t tot = 0;
+  for (uint64_t p = 0; p < a.P; ++p) tot += a.n[p * a.R + r];
+  a.region_total[r] = tot;
+  for (uint32_t k = 0; k < a.M; ++k) {
+    const double* m = a.metrics + (uint64_t)k * a.P;
+    double acc = 0.0;
+#pragma unroll 8
+    for (uint64_t p = 0; p < a.P; ++p) {
+      const uint64_t v = a.n[p * a.R + r];
+      const double prod = a.alpha[p * a.R + r] * m[p];
+      if (v) acc = acc + prod;
+    }
+    a.mhat[(uint64_t)k * a.R + r] = acc;
+  }
+}
+
+}  // namespace argus
+
+using namespace argus;
+
+namespace {
+
+std::mutex g_dev_mu;
+int g_dev_ok[64] = {};  // 1: device checked to be gfx950
+
+int check_device() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return ARGUS_E_HIP;
+  if (dev < 0 || dev >= 64) return ARGUS_E_DEVICE;
+  std::lock_guard<std::mutex> lock(g_dev_mu);
+  if (!g_dev_ok[dev]) {
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return ARGUS_E_HIP;
+    if (strncmp(prop.gcnArchName, "gfx950", 6) != 0) return ARGUS_E_DEVICE;
+    g_dev_ok[dev] = 1;
+  }
+  return ARGUS_OK;
+}
+
+bool aligned(const void* p, uintptr_t to) { return ((uintptr_t)p & (to - 1)) == 0; }
+
+uint32_t grid_for(uint64_t items, uint64_t per_block, uint32_t cap) {
+  uint64_t g = (items + per_block - 1) / per_block;
+  if (g > cap) g = cap;
+  return g < 1 ? 1u : (uint32_t)g;
+}
+
+}  // namespace
+
+extern "C" int argus_attr_samples(const argus_samples_config* cfg, const argus_samples_io* io,
+                                  void* stream_v) {
+  if (!cfg || !io) return ARGUS_E_INVAL;
+  if (cfg->abi_version != ARGUS_ATTR_ABI_VERSION) return ARGUS_E_ABI;
+  const uint64_t R = cfg->num_regions, P = cfg->num_pcs, M = cfg->num_metrics;
+  if (R < 1 || R > 65535 || P < 1 || P > (1u << 24) || M > 64) return ARGUS_E_INVAL;
+  if (P * R > (1ull << 31)) return ARGUS_E_CAPACITY;
+  if (!io->d_n_instances || (io->max_instances > 0 && !io->d_instances)) return ARGUS_E_INVAL;
+  if (io->n_samples > 0 && !io->d_samples) return ARGUS_E_INVAL;
+  if (!io->d_counters || !io->d_n || !io->d_alpha || !io->d_pc_total || !io->d_pc_owners ||
+      !io->d_entropy || !io->d_region_total)
+    return ARGUS_E_INVAL;
+  if (M > 0 && (!io->d_metrics || !io->d_mhat)) return ARGUS_E_INVAL;
+  if (!aligned(io->d_instances, 16) || !aligned(io->d_samples, 16) ||
+      !aligned(io->d_n_instances, 8) || !aligned(io->d_weights, 4) ||
+      !aligned(io->d_metrics, 8) || !aligned(io->d_counters, 8) || !aligned(io->d_n, 8) ||
+      !aligned(io->d_alpha, 8) || !aligned(io->d_pc_total, 8) || !aligned(io->d_pc_owners, 4) ||
+      !aligned(io->d_entropy, 8) || !aligned(io->d_region_total, 8) || !aligned(io->d_mhat, 8))
+    return ARGUS_E_ALIGN;
+  const int dc = check_device();
+  if (dc != ARGUS_OK) return dc;
+
+  SampArgs a{};
+  a.inst = io->d_instances;
+  a.n_inst = io->d_n_instances;
+  a.max_inst = io->max_instances;
+  a.smp = reinterpret_cast<const uint4*>(io->d_samples);
+  a.ns = io->n_samples;
+  a.w = io->d_weights;
+  a.metrics = io->d_metrics;
+  a.R = (uint32_t)R;
+  a.P = (uint32_t)P;
+  a.M = (uint32_t)M;
+  a.counters = io->d_counters;
+  a.n = io->d_n;
+  a.alpha = io->d_alpha;
+  a.pc_total = io->d_pc_total;
+  a.owners = io->d_pc_owners;
+  a.entropy = io->d_entropy;
+  a.region_total = io->d_region_total;
+  a.mhat = io->d_mhat;
+  hipStream_t s = (hipStream_t)stream_v;
+  hipLaunchKernelGGL(k_s_clear, dim3(grid_for(P * R, kSampThreads, 4096)), dim3(kSampThreads), 0,
+                     s, a);
+  hipLaunchKernelGGL(k_s_join, dim3(grid_for(a.ns, kSampThreads, 4096)), dim3(kSampThreads), 0, s,
+                     a);
+  hipLaunchKernelGGL(k_s_pc, dim3(grid_for(P, kSampThreads / 64, 4096)), dim3(kSampThreads), 0,
+                     s, a);
+  hipLaunchKernelGGL(k_s_region, dim3(grid_for(R, kSampThreads, 4096)), dim3(kSampThreads), 0,
+                     s, a);
+  return hipGetLastError() == hipSuccess ? ARGUS_OK : ARGUS_E_HIP;
+}

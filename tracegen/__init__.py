@@ -138,3 +138,40 @@ def make_records(rows) -> np.ndarray:
     for i, (ts, ctx, region, kind) in enumerate(rows):
         a[i] = (ts, ctx, region, kind, 0)
     return a.view(np.uint8).reshape(len(rows), 16)
+
+
+SAMPLE_DTYPE = np.dtype([("ts", "<u8"), ("ctx_key", "<u4"), ("pc", "<u4")])
+
+
+def pc_samples(records: np.ndarray, n_samples: int, num_pcs: int, num_regions: int,
+               seed: int = 0, shared_pcs: int = 64, p_shared: float = 0.2,
+               max_offset: int = 400) -> np.ndarray:
+    """Synthetic PC samples shaped like a sampling run over the same kernel.
+
+    Each sample copies the context and the time (plus U[0, max_offset)) of
+    a random marker record, so samples follow the trace's layout and fall
+    inside, between and after regions.  Its PC is drawn from a block of PCs
+    tied to that marker's region id (the code of the region), or, with
+    probability p_shared, from `shared_pcs` helper PCs used by every region
+    (the shared helpers and epilogues that make ownership ambiguous).  About
+    1 in 1000 samples gets pc = num_pcs (out of range).  No attribution is
+    computed here.  Returns SAMPLE_DTYPE [n_samples] in the records' order.
+    """
+    rng = np.random.default_rng(seed)
+    rec = as_records(records)
+    n = len(rec)
+    idx = np.sort(rng.integers(0, n, size=n_samples)) if n else np.zeros(0, np.int64)
+    out = np.zeros(n_samples, SAMPLE_DTYPE)
+    if n == 0:
+        return out
+    out["ts"] = rec["ts"][idx] + rng.integers(0, max_offset, size=n_samples).astype(np.uint64)
+    out["ctx_key"] = rec["ctx_key"][idx]
+    block = max(1, (num_pcs - shared_pcs) // max(1, num_regions))
+    reg = rec["region_id"][idx].astype(np.int64) % max(1, num_regions)
+    own = shared_pcs + reg * block + rng.integers(0, block, size=n_samples)
+    shared = rng.random(n_samples) < p_shared
+    pc = np.where(shared, rng.integers(0, shared_pcs, size=n_samples), own)
+    pc = np.minimum(pc, num_pcs - 1)
+    pc[rng.random(n_samples) < 0.001] = num_pcs
+    out["pc"] = pc.astype(np.uint32)
+    return out
