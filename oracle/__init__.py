@@ -15,7 +15,8 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SRCS = [os.path.join(_HERE, "argus_oracle.cpp"), os.path.join(_HERE, "argus_oracle_samples.cpp")]
+_SRCS = [os.path.join(_HERE, f) for f in
+         ("argus_oracle.cpp", "argus_oracle_samples.cpp", "argus_oracle_scope.cpp")]
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 NUM_COUNTERS = 32
@@ -65,6 +66,11 @@ def _open(path: str):
     g.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p, ctypes.c_uint64,
                   ctypes.c_void_p, ctypes.c_uint32, ctypes.c_uint32, ctypes.c_uint32,
                   ctypes.c_void_p] + [ctypes.c_void_p] * 8
+    h = lib.argus_oracle_scope
+    h.restype = ctypes.c_int
+    h.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32,
+                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                  ctypes.c_void_p]
     return lib
 
 
@@ -89,6 +95,9 @@ class OracleLib:
 
     def samples(self, *args, **kw):
         return samples(*args, _lib=self._lib, **kw)
+
+    def scope(self, *args, **kw):
+        return scope(*args, _lib=self._lib, **kw)
 
 
 def _ptr(a):
@@ -183,4 +192,42 @@ def samples(instances: np.ndarray, samples_: np.ndarray, num_regions: int, num_p
                                   _ptr(out["mhat"]) if M else None)
     if rc != 0:
         raise ValueError(f"argus_oracle_samples failed with {rc}")
+    return out
+
+
+SC_COUNTER_NAMES = ["n_instances", "n_in_scope", "n_matched", "n_mismatched", "n_unclosed",
+                    "n_self_nested", "n_iterations"]
+ALL_SCOPE = dict(role_mask=0, role_lo=0, role_hi=0, group_shift=32, group_lo=0, group_hi=0,
+                 iter_lo=0, iter_hi=0xFFFFFFFF)
+
+
+class _Scope(ctypes.Structure):
+    _fields_ = [(k, ctypes.c_uint32) for k in ("role_mask", "role_lo", "role_hi", "group_shift",
+                                               "group_lo", "group_hi", "iter_lo", "iter_hi")]
+
+
+def scope(instances: np.ndarray, excl: np.ndarray, num_regions: int, region_mask=None,
+          _lib=None, **kw) -> dict:
+    """Iteration ordinals and scoped per-region statistics on host arrays.
+
+    Scope fields (keyword arguments) default to "everything": role_mask,
+    role_lo, role_hi, group_shift, group_lo, group_hi, iter_lo, iter_hi.
+    Returns ordinal [n] u32, stats [R, 142] u64 and counters [8] u64."""
+    inst = np.ascontiguousarray(instances)
+    ex = np.ascontiguousarray(excl, dtype=np.uint64)
+    n = inst.nbytes // 32
+    assert ex.shape == (n,)
+    f = dict(ALL_SCOPE)
+    f.update(kw)
+    sc = _Scope(**{k: int(v) for k, v in f.items()})
+    R = int(num_regions)
+    mask = None if region_mask is None else np.ascontiguousarray(region_mask, dtype=np.uint8)
+    out = dict(ordinal=np.zeros(n, np.uint32), stats=np.zeros((R, RS_WIDTH), np.uint64),
+               counters=np.zeros(8, np.uint64))
+    lib = _lib if _lib is not None else _load()
+    rc = lib.argus_oracle_scope(_ptr(inst) if n else None, _ptr(ex) if n else None, n, R,
+                                ctypes.byref(sc), _ptr(mask), _ptr(out["ordinal"]),
+                                _ptr(out["stats"]), _ptr(out["counters"]))
+    if rc != 0:
+        raise ValueError(f"argus_oracle_scope failed with {rc}")
     return out

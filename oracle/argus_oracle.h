@@ -150,6 +150,46 @@ int argus_oracle_samples(const void* instances, uint64_t n_inst,
                          uint32_t* pc_owners, double* entropy,
                          uint64_t* region_total, double* mhat);
 
+/* ------------------------------------------------------------------------
+ * Scopes and iteration ordinals (Section 3.2: a scope selects dynamic
+ * executions of a region -- by warp role, iteration window or SM subset;
+ * Section 3.3: probes are specialised per iteration).
+ *
+ * ordinal[x] = number of instances y < x (canonical order) of the same
+ * context whose BEGIN region equals x's: the 0-based iteration of region
+ * x in its context.  Instance x is in scope when
+ *   (ctx & role_mask) in [role_lo, role_hi],
+ *   (ctx >> group_shift, 0 if group_shift >= 32) in [group_lo, group_hi],
+ *   ordinal[x] in [iter_lo, iter_hi], and
+ *   region_mask == NULL or region_mask[region] != 0.
+ * stats [R * ORC_RS_WIDTH]: the per-region statistics of argus_oracle_run
+ * over the in-scope instances only (orphan_end stays 0: orphans are no
+ * instances; mism_as_end is counted by the END region of an in-scope
+ * mismatched instance; self_nested when the parent, in scope or not, has
+ * the same region).
+ * counters [ORC_SC_NUM_COUNTERS].  excl [n_inst] exclusive durations. */
+typedef struct {
+  uint32_t role_mask, role_lo, role_hi;
+  uint32_t group_shift, group_lo, group_hi;
+  uint32_t iter_lo, iter_hi;
+} orc_scope;
+
+enum {
+  ORC_SC_N_INSTANCES = 0,
+  ORC_SC_N_IN_SCOPE = 1,
+  ORC_SC_N_MATCHED = 2,
+  ORC_SC_N_MISMATCHED = 3,
+  ORC_SC_N_UNCLOSED = 4,
+  ORC_SC_N_SELF_NESTED = 5,
+  ORC_SC_N_ITERATIONS = 6, /* 1 + the largest ordinal (0 without instances) */
+  ORC_SC_NUM_COUNTERS = 8
+};
+
+int argus_oracle_scope(const void* instances, const uint64_t* excl, uint64_t n_inst,
+                       uint32_t num_regions, const orc_scope* scope,
+                       const uint8_t* region_mask, uint32_t* ordinal,
+                       uint64_t* stats, uint64_t* counters);
+
 #ifdef __cplusplus
 }
 #endif

@@ -23,6 +23,24 @@ from test_oracle_pins import brute_force_overlap, check_invariants, scan_derivat
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "argus_oracle.cpp")
 SRC_S = os.path.join(ROOT, "oracle", "argus_oracle_samples.cpp")
+SRC_C = os.path.join(ROOT, "oracle", "argus_oracle_scope.cpp")
+SOURCES = (SRC, SRC_S, SRC_C)
+
+# one-line mutants of the scopes and ordinals (argus_oracle_scope.cpp)
+MUTANTS_C = {
+    "ordinal_off_by_one": ("    ordinal[x] = c;\n", "    ordinal[x] = c + 1;\n"),
+    "ordinal_per_context_only": ("seen[{inst[x].ctx, inst[x].region}]", "seen[{inst[x].ctx, 0}]"),
+    "window_exclusive": ("in_range(ordinal[x], sc->iter_lo, sc->iter_hi)",
+                         "in_range(ordinal[x] + 1, sc->iter_lo, sc->iter_hi)"),
+    "role_unmasked": ("in_range(a.ctx & sc->role_mask, sc->role_lo, sc->role_hi)",
+                      "in_range(a.ctx, sc->role_lo, sc->role_hi)"),
+    "group_shift_ignored": ("(a.ctx >> sc->group_shift);", "(a.ctx);"),
+    "mism_end_by_begin": ("stats[uint64_t(a.end_region) * ORC_RS_WIDTH + ORC_RS_MISM_AS_END] += 1;",
+                          "stats[uint64_t(a.region) * ORC_RS_WIDTH + ORC_RS_MISM_AS_END] += 1;"),
+    "excl_min_from_incl": ("row[ORC_RS_EXCL_MIN] = std::min(row[ORC_RS_EXCL_MIN], e);",
+                           "row[ORC_RS_EXCL_MIN] = std::min(row[ORC_RS_EXCL_MIN], d);"),
+    "region_mask_ignored": ("(!region_mask || region_mask[a.region] != 0)", "true"),
+}
 
 # one-line mutants of the sample attribution (argus_oracle_samples.cpp)
 MUTANTS_S = {
@@ -151,9 +169,29 @@ def mutant_dir(tmp_path_factory):
     return tmp_path_factory.mktemp("oracle_mutants")
 
 
+def run_scope_pins(orc) -> list[str]:
+    """The scope and ordinal pins of test_oracle_scope against `orc`."""
+    import test_oracle_scope as tc
+    failures = []
+    checks = [("hand_ordinals", lambda: tc.test_hand_ordinals_and_window(orc)),
+              ("hand_role_group_mask", lambda: tc.test_hand_role_group_and_region_mask(orc)),
+              ("hand_malformed", lambda: tc.test_hand_malformed_in_scope(orc))]
+    checks += [(f"brute_force_ordinal_{k}", (lambda k=k: tc.test_brute_force_ordinal(orc, k)))
+               for k in range(30)]
+    checks += [(f"partitions_{k}", (lambda k=k: tc.test_all_scope_and_partitions(orc, k)))
+               for k in range(12)]
+    for name, fn in checks:
+        try:
+            fn()
+        except Exception:  # noqa: BLE001 - any failure kills the mutant
+            failures.append(name)
+    return failures
+
+
 def test_unmutated_oracle_passes_all_pins(oracle_mod):
     assert run_pins(oracle_mod) == []
     assert run_sample_pins(oracle_mod) == []
+    assert run_scope_pins(oracle_mod) == []
 
 
 def _build_mutant(mutant_dir, name, target, old, new):
@@ -162,11 +200,11 @@ def _build_mutant(mutant_dir, name, target, old, new):
     path = os.path.join(str(mutant_dir), f"{name}.cpp")
     with open(path, "w") as f:
         f.write(src.replace(old, new))
-    other = SRC_S if target == SRC else SRC
+    others = [x for x in SOURCES if x != target]
     inc = os.path.join(ROOT, "oracle")
     lib = os.path.join(str(mutant_dir), f"lib{name}.so")
     subprocess.check_call(["g++", "-O1", "-std=c++17", "-ffp-contract=off", "-shared", "-fPIC",
-                           "-I", inc, path, other, "-o", lib])
+                           "-I", inc, path, *others, "-o", lib])
     return lib
 
 
@@ -182,3 +220,10 @@ def test_sample_mutant_is_caught(oracle_mod, mutant_dir, name):
     old, new = MUTANTS_S[name]
     orc = oracle_mod.OracleLib(_build_mutant(mutant_dir, name, SRC_S, old, new))
     assert run_sample_pins(orc), f"mutant {name} survived every pin"
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS_C))
+def test_scope_mutant_is_caught(oracle_mod, mutant_dir, name):
+    old, new = MUTANTS_C[name]
+    orc = oracle_mod.OracleLib(_build_mutant(mutant_dir, name, SRC_C, old, new))
+    assert run_scope_pins(orc), f"mutant {name} survived every pin"
