@@ -303,6 +303,69 @@ typedef struct argus_samples_io {
 int argus_attr_samples(const argus_samples_config* cfg, const argus_samples_io* io,
                        void* stream);
 
+/* ------------------------------------------ scopes and iteration ordinals */
+/* Section 3.2 of the paper separates a region (the code) from its scope:
+ * which dynamic executions are reported -- a warp role, an iteration window
+ * or a subset of SMs; Section 3.3 specialises probes to one iteration of a
+ * loop region.  Works on the instance array (and exclusive durations) that
+ * argus_attr_run wrote.
+ *
+ * ordinal[x] = the number of instances before x (canonical order) of the
+ * same context with the same BEGIN region: the 0-based iteration of that
+ * region in its context (every status counts).  Instance x is in scope when
+ *   (ctx_key & role_mask) in [role_lo, role_hi]            (warp role)
+ *   (ctx_key >> group_shift; 0 if group_shift >= 32) in [group_lo, group_hi]
+ *                                                          (SM subset)
+ *   ordinal[x] in [iter_lo, iter_hi]                       (iteration window)
+ *   d_region_mask == NULL or d_region_mask[region_id] != 0 (region set)
+ * Scoped statistics use the ARGUS_RS_* layout over the in-scope instances:
+ * matched ones give count, sums, min/max and histograms; unclosed and
+ * mismatched (by BEGIN region, and by END region for mism_as_end) ones are
+ * counted; self_nested when the parent (in scope or not) has the same region;
+ * orphan_end is 0 (orphan ENDs are no instances).  All integers. */
+typedef struct argus_scope {
+  uint32_t role_mask, role_lo, role_hi;
+  uint32_t group_shift, group_lo, group_hi;
+  uint32_t iter_lo, iter_hi;
+} argus_scope; /* everything: {0, 0, 0, 32, 0, 0, 0, 0xFFFFFFFF} */
+
+enum {
+  ARGUS_SC_N_INSTANCES = 0,
+  ARGUS_SC_N_IN_SCOPE = 1,
+  ARGUS_SC_N_MATCHED = 2,
+  ARGUS_SC_N_MISMATCHED = 3,
+  ARGUS_SC_N_UNCLOSED = 4,
+  ARGUS_SC_N_SELF_NESTED = 5,
+  ARGUS_SC_N_ITERATIONS = 6, /* 1 + the largest ordinal; 0 without instances */
+  ARGUS_SC_NUM_COUNTERS = 8  /* 7 is zero */
+};
+
+typedef struct argus_scope_config {
+  uint32_t abi_version; /* ARGUS_ATTR_ABI_VERSION */
+  uint32_t num_regions; /* R of the run that wrote the instances */
+  argus_scope scope;
+} argus_scope_config;
+
+typedef struct argus_scope_io {
+  const argus_instance* d_instances; /* canonical order (16-byte aligned) */
+  const uint64_t* d_instance_excl;   /* exclusive durations, as argus_attr_run writes them */
+  const uint64_t* d_n_instances;     /* device scalar, e.g. &d_counters[ARGUS_C_N_BEGIN] */
+  uint64_t max_instances;            /* capacity of the instance arrays, < 2^31 */
+  const uint8_t* d_region_mask;      /* [R] or NULL */
+  uint32_t* d_ordinal;               /* out [max_instances]; the first n are written */
+  uint64_t* d_stats;                 /* out [R][ARGUS_RS_WIDTH] */
+  uint64_t* d_counters;              /* out [ARGUS_SC_NUM_COUNTERS] */
+} argus_scope_io;
+
+/* Device workspace argus_attr_scope needs for up to max_instances instances
+ * (256-byte aligned); 0 if max_instances >= 2^31. */
+size_t argus_attr_scope_workspace_bytes(uint64_t max_instances);
+
+/* Enqueue ordinals and scoped statistics on `stream` without synchronising.
+ * Allocates nothing; argument errors are returned before any GPU call. */
+int argus_attr_scope(const argus_scope_config* cfg, const argus_scope_io* io,
+                     void* d_workspace, size_t workspace_bytes, void* stream);
+
 /* Destroy a handle; NULL is a no-op. */
 void argus_attr_destroy(argus_attr* h);
 

@@ -15,7 +15,9 @@ from .attr import (ABI_VERSION, COUNTER_NAMES, FORCE_EVENT_SORT, FORCE_FULL_SORT
                    argus_attr_outputs, argus_attr_run, argus_attr_run_noalloc,
                    argus_attr_samples, argus_attr_set_timing, argus_attr_set_timing_filter,
                    argus_attr_workspace_bytes, argus_samples_config, argus_samples_io,
-                   attribute_samples, load_library, to_host)
+                   argus_attr_scope, argus_attr_scope_workspace_bytes, argus_scope,
+                   argus_scope_config, argus_scope_io, attribute_samples, load_library,
+                   scope_statistics, to_host)
 
 __all__ = [
     "ABI_VERSION", "COUNTER_NAMES", "FORCE_EVENT_SORT", "FORCE_FULL_SORT", "FORCE_RECORD_RADIX",
@@ -25,5 +27,7 @@ __all__ = [
     "argus_attr_kernel_times", "argus_attr_last_error", "argus_attr_outputs", "argus_attr_run",
     "argus_attr_run_noalloc", "argus_attr_samples", "argus_attr_set_timing",
     "argus_attr_set_timing_filter", "argus_attr_workspace_bytes", "argus_samples_config",
-    "argus_samples_io", "attribute_samples", "load_library", "to_host",
+    "argus_samples_io", "attribute_samples", "load_library", "to_host", "argus_attr_scope",
+    "argus_attr_scope_workspace_bytes", "argus_scope", "argus_scope_config", "argus_scope_io",
+    "scope_statistics",
 ]

@@ -88,6 +88,28 @@ class argus_samples_io(ctypes.Structure):
                 ("d_mhat", ctypes.c_void_p)]
 
 
+class argus_scope(ctypes.Structure):
+    _fields_ = [(k, ctypes.c_uint32) for k in ("role_mask", "role_lo", "role_hi", "group_shift",
+                                               "group_lo", "group_hi", "iter_lo", "iter_hi")]
+
+
+class argus_scope_config(ctypes.Structure):
+    _fields_ = [("abi_version", ctypes.c_uint32), ("num_regions", ctypes.c_uint32),
+                ("scope", argus_scope)]
+
+
+class argus_scope_io(ctypes.Structure):
+    _fields_ = [("d_instances", ctypes.c_void_p), ("d_instance_excl", ctypes.c_void_p),
+                ("d_n_instances", ctypes.c_void_p), ("max_instances", ctypes.c_uint64),
+                ("d_region_mask", ctypes.c_void_p), ("d_ordinal", ctypes.c_void_p),
+                ("d_stats", ctypes.c_void_p), ("d_counters", ctypes.c_void_p)]
+
+
+ALL_SCOPE = dict(role_mask=0, role_lo=0, role_hi=0, group_shift=32, group_lo=0, group_hi=0,
+                 iter_lo=0, iter_hi=0xFFFFFFFF)
+SC_NUM_COUNTERS = 8
+SC_COUNTER_NAMES = ["n_instances", "n_in_scope", "n_matched", "n_mismatched", "n_unclosed",
+                    "n_self_nested", "n_iterations"]
 S_NUM_COUNTERS = 8
 S_COUNTER_NAMES = ["n_samples", "n_bad_pc", "w_total", "w_attributed", "w_unattributed",
                    "w_inner_unmatched", "n_pairs", "w_bad_instance"]
@@ -96,6 +118,8 @@ SAMPLE_DTYPE = np.dtype([("ts", "<u8"), ("ctx_key", "<u4"), ("pc", "<u4")])
 assert ctypes.sizeof(argus_attr_config) == 40
 assert ctypes.sizeof(argus_samples_config) == 16
 assert ctypes.sizeof(argus_samples_io) == 120
+assert ctypes.sizeof(argus_scope_config) == 40
+assert ctypes.sizeof(argus_scope_io) == 64
 assert ctypes.sizeof(argus_attr_outputs) == 48
 
 _lib = None
@@ -123,6 +147,11 @@ def load_library(path: str = LIB_PATH):
     lib.argus_attr_samples.argtypes = [ctypes.POINTER(argus_samples_config),
                                        ctypes.POINTER(argus_samples_io), vp]
     lib.argus_attr_samples.restype = i32
+    lib.argus_attr_scope_workspace_bytes.argtypes = [u64]
+    lib.argus_attr_scope_workspace_bytes.restype = ctypes.c_size_t
+    lib.argus_attr_scope.argtypes = [ctypes.POINTER(argus_scope_config),
+                                     ctypes.POINTER(argus_scope_io), vp, ctypes.c_size_t, vp]
+    lib.argus_attr_scope.restype = i32
     lib.argus_attr_destroy.argtypes = [vp]
     lib.argus_attr_destroy.restype = None
     lib.argus_attr_last_error.argtypes = [vp]
@@ -205,6 +234,50 @@ def attribute_samples(instances, n_instances, samples, num_regions: int, num_pcs
     rc = argus_attr_samples(cfg, io, s.cuda_stream)
     if rc != 0:
         raise ArgusError(rc, "argus_attr_samples rejected its arguments")
+    return out
+
+
+def argus_attr_scope_workspace_bytes(max_instances: int) -> int:
+    return load_library().argus_attr_scope_workspace_bytes(max_instances)
+
+
+def argus_attr_scope(cfg: argus_scope_config, io: argus_scope_io, d_workspace: int,
+                     workspace_bytes: int, stream: int) -> int:
+    return load_library().argus_attr_scope(ctypes.byref(cfg) if cfg is not None else None,
+                                           ctypes.byref(io) if io is not None else None,
+                                           d_workspace, workspace_bytes, stream)
+
+
+def scope_statistics(instances, instance_excl, n_instances, num_regions: int, region_mask=None,
+                     stream=None, **scope) -> dict:
+    """argus_attr_scope on torch CUDA tensors: the instance and exclusive-time
+    tensors argus_attr_run wrote, `n_instances` a 1-element uint64 CUDA
+    tensor (e.g. counters[4:5]); scope fields as keyword arguments (default:
+    everything).  Returns ordinal [cap] u32 (the first n valid), stats
+    [R, 142] u64 and counters [8] u64 (valid once the stream completes)."""
+    import torch
+    dev = instances.device
+    cap = instances.numel() * instances.element_size() // 32
+    R = int(num_regions)
+    f = dict(ALL_SCOPE)
+    f.update(scope)
+    cfg = argus_scope_config(ABI_VERSION, R, argus_scope(**{k: int(v) for k, v in f.items()}))
+    out = dict(ordinal=torch.empty(max(cap, 1), dtype=torch.uint32, device=dev),
+               stats=torch.empty((R, RS_WIDTH), dtype=torch.uint64, device=dev),
+               counters=torch.empty(SC_NUM_COUNTERS, dtype=torch.uint64, device=dev))
+    need = argus_attr_scope_workspace_bytes(cap)
+    ws = torch.empty(need + 256, dtype=torch.uint8, device=dev)
+    ws_ptr = (ws.data_ptr() + 255) & ~255
+    io = argus_scope_io(instances.data_ptr() if cap else None,
+                        instance_excl.data_ptr() if cap else None, n_instances.data_ptr(), cap,
+                        region_mask.data_ptr() if region_mask is not None else None,
+                        out["ordinal"].data_ptr(), out["stats"].data_ptr(),
+                        out["counters"].data_ptr())
+    s = stream if stream is not None else torch.cuda.current_stream(dev)
+    rc = argus_attr_scope(cfg, io, ws_ptr, need, s.cuda_stream)
+    if rc != 0:
+        raise ArgusError(rc, "argus_attr_scope rejected its arguments")
+    out["_workspace"] = ws  # keeps the workspace alive until the caller drops the result
     return out
 
 
