@@ -16,7 +16,8 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRCS = [os.path.join(_HERE, f) for f in
-         ("argus_oracle.cpp", "argus_oracle_samples.cpp", "argus_oracle_scope.cpp")]
+         ("argus_oracle.cpp", "argus_oracle_samples.cpp", "argus_oracle_scope.cpp",
+          "argus_oracle_probes.cpp")]
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 NUM_COUNTERS = 32
@@ -71,6 +72,11 @@ def _open(path: str):
     h.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32,
                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                   ctypes.c_void_p]
+    q = lib.argus_oracle_probes
+    q.restype = ctypes.c_int
+    q.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_void_p,
+                  ctypes.c_uint64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                  ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p]
     return lib
 
 
@@ -98,6 +104,9 @@ class OracleLib:
 
     def scope(self, *args, **kw):
         return scope(*args, _lib=self._lib, **kw)
+
+    def probes(self, *args, **kw):
+        return probes(*args, _lib=self._lib, **kw)
 
 
 def _ptr(a):
@@ -230,4 +239,37 @@ def scope(instances: np.ndarray, excl: np.ndarray, num_regions: int, region_mask
                                 _ptr(out["stats"]), _ptr(out["counters"]))
     if rc != 0:
         raise ValueError(f"argus_oracle_scope failed with {rc}")
+    return out
+
+
+PROBE_DTYPE = np.dtype([("t_start", "<u8"), ("t_end", "<u8"), ("ctx_key", "<u4"),
+                        ("iteration", "<u4"), ("op_region", "<u2"), ("pad0", "<u2"),
+                        ("pad1", "<u4")])
+assert PROBE_DTYPE.itemsize == 32
+PG_COLUMNS = ["instance", "count", "sum", "issue", "p0", "p20", "p40", "p60", "p80", "p100"]
+PR_COUNTER_NAMES = ["n_probes", "n_bad", "n_joined", "n_unjoined", "n_groups"]
+
+
+def probes(instances: np.ndarray, num_regions: int, probes_: np.ndarray, _lib=None) -> dict:
+    """Join probe intervals (PROBE_DTYPE) to reference instances and
+    summarise their latency per joined instance.  Returns ref [n] u32,
+    completion [n] u64, groups [G, 10] u64 (columns PG_COLUMNS), mean [G]
+    f64 and counters [8] u64."""
+    inst = np.ascontiguousarray(instances)
+    pr = np.ascontiguousarray(probes_)
+    ni, npr = inst.nbytes // 32, pr.nbytes // 32
+    cap = max(npr, 1)
+    out = dict(ref=np.zeros(npr, np.uint32), completion=np.zeros(npr, np.uint64),
+               groups=np.zeros((cap, 10), np.uint64), mean=np.zeros(cap, np.float64),
+               counters=np.zeros(8, np.uint64))
+    lib = _lib if _lib is not None else _load()
+    rc = lib.argus_oracle_probes(_ptr(inst) if ni else None, ni, int(num_regions),
+                                 _ptr(pr) if npr else None, npr, _ptr(out["ref"]),
+                                 _ptr(out["completion"]), _ptr(out["groups"]), _ptr(out["mean"]),
+                                 cap, _ptr(out["counters"]))
+    if rc != 0:
+        raise ValueError(f"argus_oracle_probes failed with {rc}")
+    g = int(out["counters"][4])
+    out["groups"] = out["groups"][:g]
+    out["mean"] = out["mean"][:g]
     return out

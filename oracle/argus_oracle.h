@@ -190,6 +190,47 @@ int argus_oracle_scope(const void* instances, const uint64_t* excl, uint64_t n_i
                        const uint8_t* region_mask, uint32_t* ordinal,
                        uint64_t* stats, uint64_t* counters);
 
+/* ------------------------------------------------------------------------
+ * Probe <-> reference join (Section 3.3: a forced-completion probe measures
+ * the exposed latency of one asynchronous operation at one iteration; the
+ * interval is joined to the same operation in the same iteration of the
+ * reference trace through stable identity and scope, never by timestamp;
+ * Section 3.5: exact joins by scope coordinates; Appendix B: mean and the
+ * 0/20/40/60/80th percentiles of the exposed latency).
+ *
+ *   probe (32 B): u64 t_start @0, u64 t_end @8, u32 ctx_key @16,
+ *                 u32 iteration @20, u16 op_region @24, u16 pad, u32 pad.
+ *
+ * A probe is bad when t_end < t_start or op_region >= R.  Otherwise it joins
+ * the reference instance of its context with BEGIN region op_region whose
+ * iteration ordinal (see argus_oracle_scope) equals its iteration; no such
+ * instance: unjoined.  Latency = t_end - t_start.
+ * Per probe: ref [n_probes] (instance index or 0xFFFFFFFF) and completion
+ * [n_probes] = t_begin of the reference instance + latency (UINT64_MAX if
+ * not joined).
+ * Groups: one per reference instance with joined probes, in increasing
+ * instance index; group columns [ORC_PG_WIDTH] u64 each: instance, count,
+ * latency sum, t_issue (the instance's t_begin), p0 (min), p20, p40, p60,
+ * p80, p100 (max), where p_q is the k-th smallest latency with
+ * k = max(1, ceil(q * count / 100)); mean [groups] = (double)sum /
+ * (double)count.
+ * counters [ORC_PR_NUM_COUNTERS].  Returns 0, -1 bad arguments, -2 if the
+ * groups exceed group_cap. */
+enum {
+  ORC_PG_INSTANCE = 0, ORC_PG_COUNT = 1, ORC_PG_SUM = 2, ORC_PG_ISSUE = 3, ORC_PG_P0 = 4,
+  ORC_PG_P20 = 5, ORC_PG_P40 = 6, ORC_PG_P60 = 7, ORC_PG_P80 = 8, ORC_PG_P100 = 9,
+  ORC_PG_WIDTH = 10
+};
+enum {
+  ORC_PR_N_PROBES = 0, ORC_PR_N_BAD = 1, ORC_PR_N_JOINED = 2, ORC_PR_N_UNJOINED = 3,
+  ORC_PR_N_GROUPS = 4, ORC_PR_NUM_COUNTERS = 8
+};
+
+int argus_oracle_probes(const void* instances, uint64_t n_inst, uint32_t num_regions,
+                        const void* probes, uint64_t n_probes, uint32_t* ref,
+                        uint64_t* completion, uint64_t* groups, double* mean,
+                        uint64_t group_cap, uint64_t* counters);
+
 #ifdef __cplusplus
 }
 #endif

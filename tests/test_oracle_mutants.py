@@ -24,7 +24,26 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "argus_oracle.cpp")
 SRC_S = os.path.join(ROOT, "oracle", "argus_oracle_samples.cpp")
 SRC_C = os.path.join(ROOT, "oracle", "argus_oracle_scope.cpp")
-SOURCES = (SRC, SRC_S, SRC_C)
+SRC_P = os.path.join(ROOT, "oracle", "argus_oracle_probes.cpp")
+SOURCES = (SRC, SRC_S, SRC_C, SRC_P)
+
+# one-line mutants of the probe join (argus_oracle_probes.cpp)
+MUTANTS_P = {
+    "join_first_iteration": ("const uint32_t x = it->second[p.iteration];",
+                             "const uint32_t x = it->second[0];"),
+    "rank_floor": ("uint64_t rank = (uint64_t(q[k]) * n + 99) / 100;",
+                   "uint64_t rank = (uint64_t(q[k]) * n) / 100;"),
+    "end_before_start_accepted": ("if (p.t_end < p.t_start || p.op_region >= num_regions) {",
+                                  "if (p.op_region >= num_regions) {"),
+    "completion_from_end": ("completion[j] = inst[x].t_begin + lat;",
+                            "completion[j] = inst[x].t_end + lat;"),
+    "mean_truncated": ("mean[g] = double(sum) / double(n);", "mean[g] = double(sum / n);"),
+    "latencies_unsorted": ("std::sort(v.begin(), v.end());", "(void)0;"),
+    "join_ignores_context": ("auto it = by_key.find({p.ctx, p.op_region});",
+                             "auto it = by_key.find({0u, p.op_region});"),
+    "iteration_off_by_one": ("p.iteration >= it->second.size()",
+                             "p.iteration + 1 >= it->second.size()"),
+}
 
 # one-line mutants of the scopes and ordinals (argus_oracle_scope.cpp)
 MUTANTS_C = {
@@ -188,10 +207,26 @@ def run_scope_pins(orc) -> list[str]:
     return failures
 
 
+def run_probe_pins(orc) -> list[str]:
+    """The probe join pins of test_oracle_probes against `orc`."""
+    import test_oracle_probes as tp
+    failures = []
+    checks = [("hand_join", lambda: tp.test_hand_percentiles_and_join(orc)),
+              ("hand_small", lambda: tp.test_hand_small_counts(orc))]
+    checks += [(f"brute_force_{k}", (lambda k=k: tp.test_brute_force(orc, k))) for k in range(25)]
+    for name, fn in checks:
+        try:
+            fn()
+        except Exception:  # noqa: BLE001 - any failure kills the mutant
+            failures.append(name)
+    return failures
+
+
 def test_unmutated_oracle_passes_all_pins(oracle_mod):
     assert run_pins(oracle_mod) == []
     assert run_sample_pins(oracle_mod) == []
     assert run_scope_pins(oracle_mod) == []
+    assert run_probe_pins(oracle_mod) == []
 
 
 def _build_mutant(mutant_dir, name, target, old, new):
@@ -227,3 +262,10 @@ def test_scope_mutant_is_caught(oracle_mod, mutant_dir, name):
     old, new = MUTANTS_C[name]
     orc = oracle_mod.OracleLib(_build_mutant(mutant_dir, name, SRC_C, old, new))
     assert run_scope_pins(orc), f"mutant {name} survived every pin"
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS_P))
+def test_probe_mutant_is_caught(oracle_mod, mutant_dir, name):
+    old, new = MUTANTS_P[name]
+    orc = oracle_mod.OracleLib(_build_mutant(mutant_dir, name, SRC_P, old, new))
+    assert run_probe_pins(orc), f"mutant {name} survived every pin"
