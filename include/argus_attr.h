@@ -366,6 +366,75 @@ size_t argus_attr_scope_workspace_bytes(uint64_t max_instances);
 int argus_attr_scope(const argus_scope_config* cfg, const argus_scope_io* io,
                      void* d_workspace, size_t workspace_bytes, void* stream);
 
+/* ----------------------------------------- probe <-> reference exact join */
+/* Section 3.3 of the paper: a forced-completion probe measures the exposed
+ * latency of one asynchronous operation at one selected iteration (the
+ * interval from its issue to its forced completion); that interval is
+ * joined to the same operation's issue in the same iteration of the
+ * reference trace through the operation's stable id and the dynamic scope,
+ * never by comparing timestamps across runs (Section 3.5).  Appendix B
+ * reports the mean and the 0th/20th/40th/60th/80th percentiles per
+ * operation and iteration.
+ *
+ * A probe is bad when t_end < t_start or op_region >= num_regions.
+ * Otherwise it joins the reference instance of its context whose BEGIN
+ * region is op_region and whose iteration ordinal (as argus_attr_scope
+ * defines it) equals `iteration`; with no such instance it is unjoined.
+ * Latency = t_end - t_start.  Per probe: d_ref = the joined instance index
+ * (0xFFFFFFFF if none) and d_completion = that instance's t_begin + latency
+ * (UINT64_MAX if none).  One group per reference instance with joined
+ * probes, in increasing instance index: ARGUS_PG_* columns, where p_q is the
+ * k-th smallest latency with k = max(1, ceil(q * count / 100)) (nearest
+ * rank; p0 = minimum, p100 = maximum), and d_mean = (double)sum /
+ * (double)count (one correctly rounded division).  All else is integer. */
+typedef struct argus_probe {
+  uint64_t t_start, t_end; /* the probe run's clock */
+  uint32_t ctx_key;
+  uint32_t iteration;      /* iteration ordinal of the operation's region */
+  uint16_t op_region;      /* region id of the operation in the reference */
+  uint16_t pad0;
+  uint32_t pad1;
+} argus_probe;             /* 32 bytes, 16-byte aligned */
+
+enum {
+  ARGUS_PG_INSTANCE = 0, ARGUS_PG_COUNT = 1, ARGUS_PG_SUM = 2, ARGUS_PG_ISSUE = 3,
+  ARGUS_PG_P0 = 4, ARGUS_PG_P20 = 5, ARGUS_PG_P40 = 6, ARGUS_PG_P60 = 7, ARGUS_PG_P80 = 8,
+  ARGUS_PG_P100 = 9, ARGUS_PG_WIDTH = 10
+};
+enum {
+  ARGUS_PR_N_PROBES = 0, ARGUS_PR_N_BAD = 1, ARGUS_PR_N_JOINED = 2, ARGUS_PR_N_UNJOINED = 3,
+  ARGUS_PR_N_GROUPS = 4, ARGUS_PR_NUM_COUNTERS = 8 /* 5..7 are zero */
+};
+
+typedef struct argus_probes_config {
+  uint32_t abi_version; /* ARGUS_ATTR_ABI_VERSION */
+  uint32_t num_regions; /* R of the run that wrote the reference instances */
+} argus_probes_config;
+
+typedef struct argus_probes_io {
+  const argus_instance* d_instances; /* reference, canonical order (16-byte aligned) */
+  const uint64_t* d_n_instances;     /* device scalar, e.g. &d_counters[ARGUS_C_N_BEGIN] */
+  uint64_t max_instances;            /* capacity of d_instances, < 2^31 */
+  const argus_probe* d_probes;       /* [n_probes] */
+  uint64_t n_probes;                 /* < 2^31 */
+  uint32_t* d_ref;                   /* out [n_probes] */
+  uint64_t* d_completion;            /* out [n_probes] */
+  uint64_t* d_groups;                /* out [n_probes][ARGUS_PG_WIDTH]; the first
+                                        counters[ARGUS_PR_N_GROUPS] rows are written */
+  double* d_mean;                    /* out [n_probes], as many as the groups */
+  uint64_t* d_counters;              /* out [ARGUS_PR_NUM_COUNTERS] */
+} argus_probes_io;
+
+/* Device workspace argus_attr_probes needs (256-byte aligned); 0 if either
+ * size is >= 2^31. */
+size_t argus_attr_probes_workspace_bytes(uint64_t max_instances, uint64_t n_probes);
+
+/* Enqueue the join and the per-group summaries on `stream` without
+ * synchronising.  Allocates nothing; argument errors are returned before
+ * any GPU call. */
+int argus_attr_probes(const argus_probes_config* cfg, const argus_probes_io* io,
+                      void* d_workspace, size_t workspace_bytes, void* stream);
+
 /* Destroy a handle; NULL is a no-op. */
 void argus_attr_destroy(argus_attr* h);
 

@@ -17,7 +17,9 @@ from .attr import (ABI_VERSION, COUNTER_NAMES, FORCE_EVENT_SORT, FORCE_FULL_SORT
                    argus_attr_workspace_bytes, argus_samples_config, argus_samples_io,
                    argus_attr_scope, argus_attr_scope_workspace_bytes, argus_scope,
                    argus_scope_config, argus_scope_io, attribute_samples, load_library,
-                   scope_statistics, to_host)
+                   scope_statistics, to_host, PROBE_DTYPE, argus_attr_probes,
+                   argus_attr_probes_workspace_bytes, argus_probes_config, argus_probes_io,
+                   join_probes)
 
 __all__ = [
     "ABI_VERSION", "COUNTER_NAMES", "FORCE_EVENT_SORT", "FORCE_FULL_SORT", "FORCE_RECORD_RADIX",
@@ -29,5 +31,6 @@ __all__ = [
     "argus_attr_set_timing_filter", "argus_attr_workspace_bytes", "argus_samples_config",
     "argus_samples_io", "attribute_samples", "load_library", "to_host", "argus_attr_scope",
     "argus_attr_scope_workspace_bytes", "argus_scope", "argus_scope_config", "argus_scope_io",
-    "scope_statistics",
+    "scope_statistics", "PROBE_DTYPE", "argus_attr_probes", "argus_attr_probes_workspace_bytes",
+    "argus_probes_config", "argus_probes_io", "join_probes",
 ]

@@ -105,6 +105,25 @@ class argus_scope_io(ctypes.Structure):
                 ("d_stats", ctypes.c_void_p), ("d_counters", ctypes.c_void_p)]
 
 
+class argus_probes_config(ctypes.Structure):
+    _fields_ = [("abi_version", ctypes.c_uint32), ("num_regions", ctypes.c_uint32)]
+
+
+class argus_probes_io(ctypes.Structure):
+    _fields_ = [("d_instances", ctypes.c_void_p), ("d_n_instances", ctypes.c_void_p),
+                ("max_instances", ctypes.c_uint64), ("d_probes", ctypes.c_void_p),
+                ("n_probes", ctypes.c_uint64), ("d_ref", ctypes.c_void_p),
+                ("d_completion", ctypes.c_void_p), ("d_groups", ctypes.c_void_p),
+                ("d_mean", ctypes.c_void_p), ("d_counters", ctypes.c_void_p)]
+
+
+PROBE_DTYPE = np.dtype([("t_start", "<u8"), ("t_end", "<u8"), ("ctx_key", "<u4"),
+                        ("iteration", "<u4"), ("op_region", "<u2"), ("pad0", "<u2"),
+                        ("pad1", "<u4")])
+PG_COLUMNS = ["instance", "count", "sum", "issue", "p0", "p20", "p40", "p60", "p80", "p100"]
+PR_NUM_COUNTERS = 8
+PR_COUNTER_NAMES = ["n_probes", "n_bad", "n_joined", "n_unjoined", "n_groups"]
+
 ALL_SCOPE = dict(role_mask=0, role_lo=0, role_hi=0, group_shift=32, group_lo=0, group_hi=0,
                  iter_lo=0, iter_hi=0xFFFFFFFF)
 SC_NUM_COUNTERS = 8
@@ -120,6 +139,9 @@ assert ctypes.sizeof(argus_samples_config) == 16
 assert ctypes.sizeof(argus_samples_io) == 120
 assert ctypes.sizeof(argus_scope_config) == 40
 assert ctypes.sizeof(argus_scope_io) == 64
+assert ctypes.sizeof(argus_probes_config) == 8
+assert ctypes.sizeof(argus_probes_io) == 80
+assert PROBE_DTYPE.itemsize == 32
 assert ctypes.sizeof(argus_attr_outputs) == 48
 
 _lib = None
@@ -152,6 +174,11 @@ def load_library(path: str = LIB_PATH):
     lib.argus_attr_scope.argtypes = [ctypes.POINTER(argus_scope_config),
                                      ctypes.POINTER(argus_scope_io), vp, ctypes.c_size_t, vp]
     lib.argus_attr_scope.restype = i32
+    lib.argus_attr_probes_workspace_bytes.argtypes = [u64, u64]
+    lib.argus_attr_probes_workspace_bytes.restype = ctypes.c_size_t
+    lib.argus_attr_probes.argtypes = [ctypes.POINTER(argus_probes_config),
+                                      ctypes.POINTER(argus_probes_io), vp, ctypes.c_size_t, vp]
+    lib.argus_attr_probes.restype = i32
     lib.argus_attr_destroy.argtypes = [vp]
     lib.argus_attr_destroy.restype = None
     lib.argus_attr_last_error.argtypes = [vp]
@@ -278,6 +305,48 @@ def scope_statistics(instances, instance_excl, n_instances, num_regions: int, re
     if rc != 0:
         raise ArgusError(rc, "argus_attr_scope rejected its arguments")
     out["_workspace"] = ws  # keeps the workspace alive until the caller drops the result
+    return out
+
+
+def argus_attr_probes_workspace_bytes(max_instances: int, n_probes: int) -> int:
+    return load_library().argus_attr_probes_workspace_bytes(max_instances, n_probes)
+
+
+def argus_attr_probes(cfg: argus_probes_config, io: argus_probes_io, d_workspace: int,
+                      workspace_bytes: int, stream: int) -> int:
+    return load_library().argus_attr_probes(ctypes.byref(cfg) if cfg is not None else None,
+                                            ctypes.byref(io) if io is not None else None,
+                                            d_workspace, workspace_bytes, stream)
+
+
+def join_probes(instances, n_instances, probes, num_regions: int, stream=None) -> dict:
+    """argus_attr_probes on torch CUDA tensors: the reference instance tensor
+    argus_attr_run wrote, `n_instances` a 1-element uint64 CUDA tensor
+    (e.g. counters[4:5]) and the probes (uint8 [P, 32] or any 32-byte
+    records).  Returns ref [P] u32, completion [P] u64, groups [P, 10] u64,
+    mean [P] f64 (the first counters[4] groups valid) and counters [8] u64."""
+    import torch
+    dev = probes.device
+    cap = instances.numel() * instances.element_size() // 32
+    npr = probes.numel() * probes.element_size() // 32
+    out = dict(ref=torch.empty(max(npr, 1), dtype=torch.uint32, device=dev),
+               completion=torch.empty(max(npr, 1), dtype=torch.uint64, device=dev),
+               groups=torch.empty((max(npr, 1), 10), dtype=torch.uint64, device=dev),
+               mean=torch.empty(max(npr, 1), dtype=torch.float64, device=dev),
+               counters=torch.empty(PR_NUM_COUNTERS, dtype=torch.uint64, device=dev))
+    need = argus_attr_probes_workspace_bytes(cap, npr)
+    ws = torch.empty(need + 256, dtype=torch.uint8, device=dev)
+    ws_ptr = (ws.data_ptr() + 255) & ~255
+    cfg = argus_probes_config(ABI_VERSION, int(num_regions))
+    io = argus_probes_io(instances.data_ptr() if cap else None, n_instances.data_ptr(), cap,
+                         probes.data_ptr() if npr else None, npr, out["ref"].data_ptr(),
+                         out["completion"].data_ptr(), out["groups"].data_ptr(),
+                         out["mean"].data_ptr(), out["counters"].data_ptr())
+    s = stream if stream is not None else torch.cuda.current_stream(dev)
+    rc = argus_attr_probes(cfg, io, ws_ptr, need, s.cuda_stream)
+    if rc != 0:
+        raise ArgusError(rc, "argus_attr_probes rejected its arguments")
+    out["_workspace"] = ws
     return out
 
 

@@ -20,6 +20,7 @@
 // the scoped statistics are taken in canonical order with global atomics.
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
 
 #include "internal.h"
@@ -31,60 +32,46 @@ constexpr int kScRounds = 16;
 constexpr uint32_t kScTile = kScThreads * kScRounds;  // 4096 elements
 constexpr uint32_t kScScanBlock = 4096;                // entries per scan block
 
-struct ScopeArgs {
-  const argus_instance* inst;
-  const uint64_t* excl;
-  const uint64_t* n_inst;
-  uint64_t max_inst;
-  uint32_t R;
-  argus_scope sc;
-  const uint8_t* region_mask;
-  uint32_t* ordinal;
-  uint64_t* stats;
-  uint64_t* counters;
-  // workspace
-  uint32_t* key[2];
-  uint64_t* val[2];  // ctx << 32 | canonical index
-  uint32_t* hist;    // [256][tiles_max], digit-major
-  uint32_t* bsum;    // scan block sums
+// A stable LSD radix sort over 8-bit digits of 16-byte elements (two u64
+// words, ping-pong buffers).  The first pass may read the instance array
+// instead (word a = BEGIN region, word b = context << 32 | index).
+struct SortBufs {
+  uint64_t* a[2];
+  uint64_t* b[2];
+  uint32_t* hist;  // [256][tiles_max], digit-major
+  uint32_t* bsum;  // scan block sums
   uint64_t tiles_max;
+  const uint64_t* count_ptr;  // device element count (clamped to count_max), or NULL
+  uint64_t count_max;
+  const argus_instance* inst;  // source of the SRC_INST passes
 };
+enum { kSrcBuf = 0, kSrcInst = 1 };
 
-__device__ __forceinline__ uint64_t sc_count(const ScopeArgs& a) {
-  const uint64_t v = *a.n_inst;
-  return v < a.max_inst ? v : a.max_inst;
+__device__ __forceinline__ uint64_t sb_count(const SortBufs& s) {
+  if (!s.count_ptr) return s.count_max;
+  const uint64_t v = *s.count_ptr;
+  return v < s.count_max ? v : s.count_max;
 }
 
-// Element e of pass `pass` (source: the instances for pass 0, else the
-// buffer the previous pass wrote).
-__device__ __forceinline__ void sc_load(const ScopeArgs& a, int pass, uint64_t e, uint32_t* key,
-                                        uint64_t* val) {
-  if (pass == 0) {
-    const uint4 h1 = reinterpret_cast<const uint4*>(a.inst)[2 * e + 1];
-    *key = h1.w & 0xFFFFu;
-    *val = ((uint64_t)h1.x << 32) | e;
+template <int SRC>
+__device__ __forceinline__ void sb_load(const SortBufs& s, int in, uint64_t e, uint64_t* a,
+                                        uint64_t* b) {
+  if (SRC == kSrcInst) {
+    const uint4 h1 = reinterpret_cast<const uint4*>(s.inst)[2 * e + 1];
+    *a = h1.w & 0xFFFFu;
+    *b = ((uint64_t)h1.x << 32) | e;
   } else {
-    *key = a.key[(pass - 1) & 1][e];
-    *val = a.val[(pass - 1) & 1][e];
+    *a = s.a[in][e];
+    *b = s.b[in][e];
   }
-}
-
-// Fill kernel for the outputs that are accumulated.
-__global__ __launch_bounds__(kScThreads) void k_sc_init(ScopeArgs a) {
-  const uint64_t total = (uint64_t)a.R * ARGUS_RS_WIDTH;
-  for (uint64_t i = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; i < total;
-       i += (uint64_t)gridDim.x * kScThreads) {
-    const uint32_t col = (uint32_t)(i % ARGUS_RS_WIDTH);
-    a.stats[i] = (col == ARGUS_RS_INCL_MIN || col == ARGUS_RS_EXCL_MIN) ? kU64Max : 0ull;
-  }
-  if (blockIdx.x == 0 && threadIdx.x < ARGUS_SC_NUM_COUNTERS) a.counters[threadIdx.x] = 0;
 }
 
 // Per tile: counts of each digit, written digit-major (zeros for tiles past
 // the element count, so that the scan sees a complete table).
-__global__ __launch_bounds__(kScThreads) void k_sc_hist(ScopeArgs a, int pass) {
+template <int SRC>
+__global__ __launch_bounds__(kScThreads) void k_sort_hist(SortBufs s, int in, int word, int shift) {
   __shared__ uint32_t s_cnt[256];
-  const uint64_t n = sc_count(a);
+  const uint64_t n = sb_count(s);
   const uint64_t tile = blockIdx.x;
   s_cnt[threadIdx.x] = 0;
   __syncthreads();
@@ -92,85 +79,77 @@ __global__ __launch_bounds__(kScThreads) void k_sc_hist(ScopeArgs a, int pass) {
   for (uint32_t j = 0; j < kScRounds; ++j) {
     const uint64_t e = base + (uint64_t)j * kScThreads + threadIdx.x;
     if (e < n) {
-      uint32_t key;
-      uint64_t val;
-      sc_load(a, pass, e, &key, &val);
-      atomicAdd(&s_cnt[(key >> (8 * pass)) & 0xFFu], 1u);
+      uint64_t a, b;
+      sb_load<SRC>(s, in, e, &a, &b);
+      atomicAdd(&s_cnt[((word ? b : a) >> shift) & 0xFFu], 1u);
     }
   }
   __syncthreads();
-  a.hist[(uint64_t)threadIdx.x * a.tiles_max + tile] = s_cnt[threadIdx.x];
+  s.hist[(uint64_t)threadIdx.x * s.tiles_max + tile] = s_cnt[threadIdx.x];
 }
 
-// Exclusive scan of the digit-major table, in three launches: block sums,
-// their scan (one block), then each block's scan plus its base.
-__global__ __launch_bounds__(kScThreads) void k_sc_scan_sums(ScopeArgs a) {
+// Exclusive scan of a u32 array in three launches: block sums, their scan
+// (one block), then each block's scan plus its base.
+__global__ __launch_bounds__(kScThreads) void k_scan_sums(uint32_t* data, uint64_t total,
+                                                          uint32_t* bsum) {
   __shared__ uint32_t s_part[kScThreads / 64];
-  const uint64_t total = 256ull * a.tiles_max;
   const uint64_t base = (uint64_t)blockIdx.x * kScScanBlock;
-  uint32_t s = 0;
+  uint32_t v = 0;
   for (uint32_t j = threadIdx.x; j < kScScanBlock; j += kScThreads)
-    if (base + j < total) s += a.hist[base + j];
-  s = rows_sum32(row_sum32(s));
-  if ((threadIdx.x & 63) == 0) s_part[threadIdx.x >> 6] = s;
+    if (base + j < total) v += data[base + j];
+  v = rows_sum32(row_sum32(v));
+  if ((threadIdx.x & 63) == 0) s_part[threadIdx.x >> 6] = v;
   __syncthreads();
-  if (threadIdx.x == 0) a.bsum[blockIdx.x] = s_part[0] + s_part[1] + s_part[2] + s_part[3];
+  if (threadIdx.x == 0) bsum[blockIdx.x] = s_part[0] + s_part[1] + s_part[2] + s_part[3];
 }
 
-__global__ __launch_bounds__(1024) void k_sc_scan_top(ScopeArgs a, uint32_t blocks) {
+// Exclusive scan of v over the block; *carry (LDS) holds the running total
+// across calls.  Every thread of the block must call it.
+template <int NT>
+__device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* s_w, uint32_t* carry) {
+  const uint32_t lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  uint32_t x = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const uint32_t y = __shfl_up(x, d);
+    if (lane >= (uint32_t)d) x += y;
+  }
+  if (lane == 63) s_w[w] = x;
+  __syncthreads();
+  uint32_t wpre = 0;
+  for (uint32_t k = 0; k < w; ++k) wpre += s_w[k];
+  const uint32_t c = *carry;
+  __syncthreads();
+  if (threadIdx.x == NT - 1) *carry = c + wpre + x;
+  __syncthreads();
+  return c + wpre + x - v;
+}
+
+__global__ __launch_bounds__(1024) void k_scan_top(uint32_t* bsum, uint32_t blocks) {
   __shared__ uint32_t s_carry;
   __shared__ uint32_t s_w[16];
   if (threadIdx.x == 0) s_carry = 0;
   __syncthreads();
   for (uint32_t b0 = 0; b0 < blocks; b0 += 1024) {
     const uint32_t b = b0 + threadIdx.x;
-    const uint32_t v = b < blocks ? a.bsum[b] : 0u;
-    // inclusive scan over the block of 1024 values
-    uint32_t x = v;
-    const uint32_t lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-      const uint32_t y = __shfl_up(x, d);
-      if (lane >= (uint32_t)d) x += y;
-    }
-    if (lane == 63) s_w[w] = x;
-    __syncthreads();
-    uint32_t wpre = 0;
-    for (uint32_t k = 0; k < w; ++k) wpre += s_w[k];
-    const uint32_t carry = s_carry;
-    if (b < blocks) a.bsum[b] = carry + wpre + x - v;  // exclusive
-    __syncthreads();
-    if (threadIdx.x == 1023) s_carry = carry + wpre + x;
-    __syncthreads();
+    const uint32_t v = b < blocks ? bsum[b] : 0u;
+    const uint32_t ex = block_excl_scan<1024>(v, s_w, &s_carry);
+    if (b < blocks) bsum[b] = ex;
   }
 }
 
-__global__ __launch_bounds__(kScThreads) void k_sc_scan_apply(ScopeArgs a) {
+__global__ __launch_bounds__(kScThreads) void k_scan_apply(uint32_t* data, uint64_t total,
+                                                           const uint32_t* bsum) {
   __shared__ uint32_t s_w[kScThreads / 64];
   __shared__ uint32_t s_carry;
-  const uint64_t total = 256ull * a.tiles_max;
   const uint64_t base = (uint64_t)blockIdx.x * kScScanBlock;
-  if (threadIdx.x == 0) s_carry = a.bsum[blockIdx.x];
+  if (threadIdx.x == 0) s_carry = bsum[blockIdx.x];
   __syncthreads();
-  const uint32_t lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   for (uint32_t j0 = 0; j0 < kScScanBlock; j0 += kScThreads) {
     const uint64_t i = base + j0 + threadIdx.x;
-    const uint32_t v = i < total ? a.hist[i] : 0u;
-    uint32_t x = v;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-      const uint32_t y = __shfl_up(x, d);
-      if (lane >= (uint32_t)d) x += y;
-    }
-    if (lane == 63) s_w[w] = x;
-    __syncthreads();
-    uint32_t wpre = 0;
-    for (uint32_t k = 0; k < w; ++k) wpre += s_w[k];
-    const uint32_t carry = s_carry;
-    if (i < total) a.hist[i] = carry + wpre + x - v;
-    __syncthreads();
-    if (threadIdx.x == kScThreads - 1) s_carry = carry + wpre + x;
-    __syncthreads();
+    const uint32_t v = i < total ? data[i] : 0u;
+    const uint32_t ex = block_excl_scan<kScThreads>(v, s_w, &s_carry);
+    if (i < total) data[i] = ex;
   }
 }
 
@@ -178,33 +157,34 @@ __global__ __launch_bounds__(kScThreads) void k_sc_scan_apply(ScopeArgs a) {
 // the lanes that share its digit with eight ballots; per-wave digit counts
 // in LDS give the wave's offset within the round, and a running count per
 // digit carries the tile's earlier rounds.
-__global__ __launch_bounds__(kScThreads) void k_sc_scatter(ScopeArgs a, int pass) {
+template <int SRC>
+__global__ __launch_bounds__(kScThreads) void k_sort_scatter(SortBufs s, int in, int out, int word,
+                                                             int shift) {
   __shared__ uint32_t s_wcnt[4][256];
   __shared__ uint32_t s_run[256];
   __shared__ uint32_t s_base[256];
-  const uint64_t n = sc_count(a);
+  const uint64_t n = sb_count(s);
   const uint64_t tile = blockIdx.x;
   const uint32_t tid = threadIdx.x, w = tid >> 6;
   s_run[tid] = 0;
-  s_base[tid] = a.hist[(uint64_t)tid * a.tiles_max + tile];
+  s_base[tid] = s.hist[(uint64_t)tid * s.tiles_max + tile];
   const uint64_t lt = lanemask_lt();
-  uint32_t* dk = a.key[pass & 1];
-  uint64_t* dv = a.val[pass & 1];
+  uint64_t* da = s.a[out];
+  uint64_t* db = s.b[out];
   for (uint32_t j = 0; j < kScRounds; ++j) {
     const uint64_t e = tile * kScTile + (uint64_t)j * kScThreads + tid;
     const bool valid = e < n;
-    uint32_t key = 0;
-    uint64_t val = 0;
-    if (valid) sc_load(a, pass, e, &key, &val);
-    const uint32_t d = (key >> (8 * pass)) & 0xFFu;
+    uint64_t a = 0, b = 0;
+    if (valid) sb_load<SRC>(s, in, e, &a, &b);
+    const uint32_t d = (uint32_t)(((word ? b : a) >> shift) & 0xFFu);
 #pragma unroll
     for (int q = 0; q < 4; ++q) s_wcnt[q][tid] = 0;
     __syncthreads();
     uint64_t peers = __ballot(valid);
 #pragma unroll
-    for (int b = 0; b < 8; ++b) {
-      const uint64_t bal = __ballot((d >> b) & 1u);
-      peers &= ((d >> b) & 1u) ? bal : ~bal;
+    for (int bit = 0; bit < 8; ++bit) {
+      const uint64_t bal = __ballot((d >> bit) & 1u);
+      peers &= ((d >> bit) & 1u) ? bal : ~bal;
     }
     const uint32_t rank = (uint32_t)__popcll(peers & lt);
     if (valid && rank == 0) s_wcnt[w][d] = (uint32_t)__popcll(peers);
@@ -223,34 +203,58 @@ __global__ __launch_bounds__(kScThreads) void k_sc_scatter(ScopeArgs a, int pass
     __syncthreads();
     if (valid) {
       const uint64_t dst = (uint64_t)s_base[d] + s_wcnt[w][d] + rank;
-      dk[dst] = key;
-      dv[dst] = val;
+      da[dst] = a;
+      db[dst] = b;
     }
     __syncthreads();
   }
 }
 
-// First position in the sorted (key, context) sequence [0, hi] that equals
-// (key, ctx): the start of that run.
-__device__ __forceinline__ uint64_t sc_run_start(const uint32_t* k, const uint64_t* v,
-                                                 uint64_t hi, uint32_t key, uint32_t ctx) {
+// First position in [0, hi) of the sorted (a, b >> 32) sequence that is not
+// less than (key, ctx).
+__device__ __forceinline__ uint64_t sb_lower(const uint64_t* ka, const uint64_t* kb, uint64_t hi,
+                                             uint64_t key, uint32_t ctx) {
   uint64_t lo = 0;
   while (lo < hi) {
     const uint64_t mid = (lo + hi) >> 1;
-    const uint32_t km = k[mid], cm = (uint32_t)(v[mid] >> 32);
-    const bool less = km < key || (km == key && cm < ctx);
+    const uint64_t am = ka[mid];
+    const uint32_t cm = (uint32_t)(kb[mid] >> 32);
+    const bool less = am < key || (am == key && cm < ctx);
     if (less) lo = mid + 1;
     else hi = mid;
   }
   return lo;
 }
 
+struct ScopeArgs {
+  const argus_instance* inst;
+  const uint64_t* excl;
+  uint32_t R;
+  argus_scope sc;
+  const uint8_t* region_mask;
+  uint32_t* ordinal;
+  uint64_t* stats;
+  uint64_t* counters;
+  SortBufs s;  // count = the instances
+};
+
+// Fill kernel for the outputs that are accumulated.
+__global__ __launch_bounds__(kScThreads) void k_sc_init(ScopeArgs a) {
+  const uint64_t total = (uint64_t)a.R * ARGUS_RS_WIDTH;
+  for (uint64_t i = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; i < total;
+       i += (uint64_t)gridDim.x * kScThreads) {
+    const uint32_t col = (uint32_t)(i % ARGUS_RS_WIDTH);
+    a.stats[i] = (col == ARGUS_RS_INCL_MIN || col == ARGUS_RS_EXCL_MIN) ? kU64Max : 0ull;
+  }
+  if (blockIdx.x == 0 && threadIdx.x < ARGUS_SC_NUM_COUNTERS) a.counters[threadIdx.x] = 0;
+}
+
 // Ordinal of each sorted element: its distance from the start of its
 // (region, context) run, scattered to canonical order.
 __global__ __launch_bounds__(kScThreads) void k_sc_ordinal(ScopeArgs a, int buf) {
-  const uint64_t n = sc_count(a);
-  const uint32_t* k = a.key[buf];
-  const uint64_t* v = a.val[buf];
+  const uint64_t n = sb_count(a.s);
+  const uint64_t* ka = a.s.a[buf];
+  const uint64_t* kb = a.s.b[buf];
   const uint32_t lane = threadIdx.x & 63;
   uint32_t best = 0;
   const uint64_t nwaves = (uint64_t)gridDim.x * (kScThreads / 64);
@@ -258,14 +262,15 @@ __global__ __launch_bounds__(kScThreads) void k_sc_ordinal(ScopeArgs a, int buf)
        wv * 64 < n; wv += nwaves) {
     const uint64_t e0 = wv * 64, e = e0 + lane;
     const bool valid = e < n;
-    uint32_t key = 0, ctx = 0, idx = 0;
+    uint64_t key = 0;
+    uint32_t ctx = 0, idx = 0;
     bool head = false;
     if (valid) {
-      key = k[e];
-      const uint64_t vv = v[e];
+      key = ka[e];
+      const uint64_t vv = kb[e];
       ctx = (uint32_t)(vv >> 32);
       idx = (uint32_t)vv;
-      head = e == 0 || k[e - 1] != key || (uint32_t)(v[e - 1] >> 32) != ctx;
+      head = e == 0 || ka[e - 1] != key || (uint32_t)(kb[e - 1] >> 32) != ctx;
     }
     // start of the run: the last head at or before this lane, else the run
     // that was open when the wave began (one binary search for the wave)
@@ -276,9 +281,10 @@ __global__ __launch_bounds__(kScThreads) void k_sc_ordinal(ScopeArgs a, int buf)
       if (lane >= (uint32_t)d && o > h) h = o;
     }
     if (__ballot(valid && h < 0)) {
-      const uint32_t k0 = __shfl(key, 0), c0 = __shfl(ctx, 0);
+      const uint64_t k0 = __shfl(key, 0);
+      const uint32_t c0 = __shfl(ctx, 0);
       uint64_t s0 = 0;
-      if (lane == 0) s0 = sc_run_start(k, v, e0, k0, c0);
+      if (lane == 0) s0 = sb_lower(ka, kb, e0, k0, c0);
       s0 = __shfl(s0, 0);
       if (h < 0) h = (int64_t)s0;
     }
@@ -304,7 +310,7 @@ __device__ __forceinline__ bool in_range32(uint64_t v, uint32_t lo, uint32_t hi)
 
 // Scoped statistics in canonical order.
 __global__ __launch_bounds__(kScThreads) void k_sc_stats(ScopeArgs a) {
-  const uint64_t n = sc_count(a);
+  const uint64_t n = sb_count(a.s);
   const uint4* inst = reinterpret_cast<const uint4*>(a.inst);
   uint32_t c_in = 0, c_m = 0, c_mm = 0, c_u = 0, c_s = 0;
   for (uint64_t x = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; x < n;
@@ -363,6 +369,136 @@ __global__ __launch_bounds__(kScThreads) void k_sc_stats(ScopeArgs a) {
   if (blockIdx.x == 0 && threadIdx.x == 0) a.counters[ARGUS_SC_N_INSTANCES] = n;
 }
 
+// ------------------------------------------------ probe <-> reference join
+// Section 3.3: a probe's interval (the exposed latency of one operation at
+// one iteration) is joined to the same operation's issue in the same
+// iteration of the reference trace, by identity and scope rather than by
+// timestamp.  The reference instances sorted by (region, context) give, for
+// (operation region, context), a run in which the iteration-th element is
+// the joined instance.  Joined probes are then sorted by (instance,
+// latency), so each group is a run in latency order and its nearest-rank
+// percentiles are read off by position.
+
+struct ProbeArgs {
+  const argus_instance* inst;
+  const uint4* probes;  // two uint4 per 32-byte probe
+  uint64_t np;
+  uint32_t R;
+  uint64_t none;        // instance code of a probe that joined nothing (= max instances)
+  SortBufs ref;         // the reference sorted by (region, context)
+  int ref_buf;
+  SortBufs pb;          // the probes sorted by (instance, latency)
+  uint32_t* ref_out;
+  uint64_t* completion;
+  uint32_t* flags;      // group heads, then their exclusive scan
+  uint64_t* groups;     // [np][ARGUS_PG_WIDTH]
+  double* mean;
+  uint64_t* counters;
+};
+
+__global__ void k_pr_init(ProbeArgs a) {
+  if (threadIdx.x < ARGUS_PR_NUM_COUNTERS) a.counters[threadIdx.x] = 0;
+}
+
+__global__ __launch_bounds__(kScThreads) void k_pr_join(ProbeArgs a) {
+  const uint64_t nref = sb_count(a.ref);
+  const uint64_t* ra = a.ref.a[a.ref_buf];
+  const uint64_t* rb = a.ref.b[a.ref_buf];
+  uint32_t bad = 0, joined = 0, unjoined = 0;
+  for (uint64_t j = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; j < a.np;
+       j += (uint64_t)gridDim.x * kScThreads) {
+    const uint4 h0 = a.probes[2 * j], h1 = a.probes[2 * j + 1];
+    const uint64_t ts = (uint64_t)h0.x | ((uint64_t)h0.y << 32);
+    const uint64_t te = (uint64_t)h0.z | ((uint64_t)h0.w << 32);
+    const uint32_t ctx = h1.x, it = h1.y, op = h1.z & 0xFFFFu;
+    uint64_t code = a.none, lat = 0, done = kU64Max;
+    if (te < ts || op >= a.R) {
+      bad += 1;
+    } else {
+      const uint64_t tgt = sb_lower(ra, rb, nref, op, ctx) + it;
+      if (tgt < nref && ra[tgt] == op && (uint32_t)(rb[tgt] >> 32) == ctx) {
+        const uint32_t x = (uint32_t)rb[tgt];
+        lat = te - ts;
+        const uint4 ib = reinterpret_cast<const uint4*>(a.inst)[2 * (uint64_t)x];
+        done = ((uint64_t)ib.x | ((uint64_t)ib.y << 32)) + lat;
+        code = x;
+        joined += 1;
+      } else {
+        unjoined += 1;
+      }
+    }
+    a.ref_out[j] = code == a.none ? 0xFFFFFFFFu : (uint32_t)code;
+    a.completion[j] = done;
+    a.pb.a[0][j] = lat;
+    a.pb.b[0][j] = (code << 32) | j;
+  }
+  const uint32_t lane = threadIdx.x & 63;
+  const uint32_t v[3] = {bad, joined, unjoined};
+  const int slot[3] = {ARGUS_PR_N_BAD, ARGUS_PR_N_JOINED, ARGUS_PR_N_UNJOINED};
+#pragma unroll
+  for (int q = 0; q < 3; ++q) {
+    const uint32_t t = rows_sum32(row_sum32(v[q]));
+    if (lane == 0 && t) atomicAdd((unsigned long long*)&a.counters[slot[q]], (unsigned long long)t);
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) a.counters[ARGUS_PR_N_PROBES] = a.np;
+}
+
+__device__ __forceinline__ bool pr_head(const uint64_t* b, uint64_t k, uint64_t none) {
+  const uint64_t r = b[k] >> 32;
+  return r != none && (k == 0 || (b[k - 1] >> 32) != r);
+}
+
+__global__ __launch_bounds__(kScThreads) void k_pr_heads(ProbeArgs a, int buf) {
+  const uint64_t* b = a.pb.b[buf];
+  uint32_t heads = 0;
+  for (uint64_t k = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; k < a.np;
+       k += (uint64_t)gridDim.x * kScThreads) {
+    const uint32_t h = pr_head(b, k, a.none) ? 1u : 0u;
+    a.flags[k] = h;
+    heads += h;
+  }
+  const uint32_t t = rows_sum32(row_sum32(heads));
+  if ((threadIdx.x & 63) == 0 && t)
+    atomicAdd((unsigned long long*)&a.counters[ARGUS_PR_N_GROUPS], (unsigned long long)t);
+}
+
+// One thread per group head: the group's count, sum, issue time, mean and
+// nearest-rank percentiles (its latencies are in increasing order).
+__global__ __launch_bounds__(kScThreads) void k_pr_groups(ProbeArgs a, int buf) {
+  const uint64_t* la = a.pb.a[buf];
+  const uint64_t* b = a.pb.b[buf];
+  for (uint64_t k = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; k < a.np;
+       k += (uint64_t)gridDim.x * kScThreads) {
+    if (!pr_head(b, k, a.none)) continue;
+    const uint64_t r = b[k] >> 32;
+    // end of the run: first position whose instance code exceeds r
+    uint64_t lo = k + 1, hi = a.np;
+    while (lo < hi) {
+      const uint64_t mid = (lo + hi) >> 1;
+      if ((b[mid] >> 32) > r) hi = mid;
+      else lo = mid + 1;
+    }
+    const uint64_t cnt = lo - k;
+    uint64_t sum = 0;
+    for (uint64_t i = k; i < lo; ++i) sum += la[i];
+    const uint64_t g = a.flags[k];
+    uint64_t* row = a.groups + g * ARGUS_PG_WIDTH;
+    row[ARGUS_PG_INSTANCE] = r;
+    row[ARGUS_PG_COUNT] = cnt;
+    row[ARGUS_PG_SUM] = sum;
+    const uint4 ib = reinterpret_cast<const uint4*>(a.inst)[2 * r];
+    row[ARGUS_PG_ISSUE] = (uint64_t)ib.x | ((uint64_t)ib.y << 32);
+    const uint32_t q[6] = {0, 20, 40, 60, 80, 100};
+#pragma unroll
+    for (int t = 0; t < 6; ++t) {
+      uint64_t rank = ((uint64_t)q[t] * cnt + 99) / 100;
+      if (rank < 1) rank = 1;
+      row[ARGUS_PG_P0 + t] = la[k + rank - 1];
+    }
+    a.mean[g] = (double)sum / (double)cnt;
+  }
+}
+
 }  // namespace argus
 
 using namespace argus;
@@ -372,30 +508,115 @@ namespace {
 constexpr size_t kScAlign = 256;
 size_t sc_align(size_t v) { return (v + kScAlign - 1) & ~(kScAlign - 1); }
 
-struct ScLayout {
-  size_t key[2], val[2], hist, bsum, total;
-  uint64_t tiles, scan_blocks;
-};
-
-ScLayout sc_layout(uint64_t max_inst) {
-  ScLayout L{};
-  const uint64_t m = max_inst ? max_inst : 1;
-  L.tiles = (m + kScTile - 1) / kScTile;
-  L.scan_blocks = (256ull * L.tiles + kScScanBlock - 1) / kScScanBlock;
+struct Carver {
   size_t o = 0;
-  auto take = [&](size_t b) {
+  size_t take(size_t b) {
     const size_t at = o;
     o = sc_align(o + (b ? b : 1));
     return at;
-  };
-  for (int b = 0; b < 2; ++b) {
-    L.key[b] = take(sizeof(uint32_t) * m);
-    L.val[b] = take(sizeof(uint64_t) * m);
   }
-  L.hist = take(sizeof(uint32_t) * 256 * L.tiles);
-  L.bsum = take(sizeof(uint32_t) * L.scan_blocks);
-  L.total = o;
+};
+
+uint64_t tiles_for(uint64_t n) { return ((n ? n : 1) + kScTile - 1) / kScTile; }
+uint64_t scan_blocks_for(uint64_t entries) { return (entries + kScScanBlock - 1) / kScScanBlock; }
+
+// Workspace of one 16-byte-element sort of up to m elements (its buffers);
+// the digit table and scan sums are shared and sized by the caller.
+struct SortLayout {
+  size_t a[2], b[2];
+};
+SortLayout carve_sort(Carver& c, uint64_t m) {
+  SortLayout L{};
+  const uint64_t mm = m ? m : 1;
+  for (int k = 0; k < 2; ++k) {
+    L.a[k] = c.take(sizeof(uint64_t) * mm);
+    L.b[k] = c.take(sizeof(uint64_t) * mm);
+  }
   return L;
+}
+
+struct ScLayout {
+  SortLayout ref;
+  size_t hist, bsum, total;
+};
+ScLayout sc_layout(uint64_t max_inst) {
+  Carver c;
+  ScLayout L{};
+  L.ref = carve_sort(c, max_inst);
+  L.hist = c.take(sizeof(uint32_t) * 256 * tiles_for(max_inst));
+  L.bsum = c.take(sizeof(uint32_t) * scan_blocks_for(256 * tiles_for(max_inst)));
+  L.total = c.o;
+  return L;
+}
+
+struct PrLayout {
+  SortLayout ref, pr;
+  size_t hist, bsum, flags, total;
+};
+PrLayout pr_layout(uint64_t max_inst, uint64_t np) {
+  Carver c;
+  PrLayout L{};
+  L.ref = carve_sort(c, max_inst);
+  L.pr = carve_sort(c, np);
+  const uint64_t tiles = std::max(tiles_for(max_inst), tiles_for(np));
+  L.hist = c.take(sizeof(uint32_t) * 256 * tiles);
+  const uint64_t sb = std::max(scan_blocks_for(256 * tiles), scan_blocks_for(np));
+  L.bsum = c.take(sizeof(uint32_t) * sb);
+  L.flags = c.take(sizeof(uint32_t) * (np ? np : 1));
+  L.total = c.o;
+  return L;
+}
+
+SortBufs make_bufs(char* base, const SortLayout& L, size_t hist, size_t bsum, uint64_t count_max,
+                   const uint64_t* count_ptr, const argus_instance* inst) {
+  SortBufs s{};
+  for (int k = 0; k < 2; ++k) {
+    s.a[k] = (uint64_t*)(base + L.a[k]);
+    s.b[k] = (uint64_t*)(base + L.b[k]);
+  }
+  s.hist = (uint32_t*)(base + hist);
+  s.bsum = (uint32_t*)(base + bsum);
+  s.tiles_max = tiles_for(count_max);
+  s.count_ptr = count_ptr;
+  s.count_max = count_max;
+  s.inst = inst;
+  return s;
+}
+
+void scan_u32(uint32_t* data, uint64_t total, uint32_t* bsum, hipStream_t st) {
+  const uint32_t blocks = (uint32_t)scan_blocks_for(total ? total : 1);
+  hipLaunchKernelGGL(k_scan_sums, dim3(blocks), dim3(kScThreads), 0, st, data, total, bsum);
+  hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(1024), 0, st, bsum, blocks);
+  hipLaunchKernelGGL(k_scan_apply, dim3(blocks), dim3(kScThreads), 0, st, data, total, bsum);
+}
+
+// One stable pass on digit (word, shift), reading buffer `in` (or the
+// instances) and writing buffer `out`.
+void sort_pass(const SortBufs& s, bool from_inst, int in, int out, int word, int shift,
+               hipStream_t st) {
+  const uint32_t tiles = (uint32_t)s.tiles_max;
+  if (from_inst)
+    hipLaunchKernelGGL(k_sort_hist<kSrcInst>, dim3(tiles), dim3(kScThreads), 0, st, s, in, word,
+                       shift);
+  else
+    hipLaunchKernelGGL(k_sort_hist<kSrcBuf>, dim3(tiles), dim3(kScThreads), 0, st, s, in, word,
+                       shift);
+  scan_u32(s.hist, 256ull * s.tiles_max, s.bsum, st);
+  if (from_inst)
+    hipLaunchKernelGGL(k_sort_scatter<kSrcInst>, dim3(tiles), dim3(kScThreads), 0, st, s, in, out,
+                       word, shift);
+  else
+    hipLaunchKernelGGL(k_sort_scatter<kSrcBuf>, dim3(tiles), dim3(kScThreads), 0, st, s, in, out,
+                       word, shift);
+}
+
+// The instances sorted by (BEGIN region, context), canonical order kept
+// within; returns the buffer holding the result.
+int sort_reference(const SortBufs& s, uint32_t R, hipStream_t st) {
+  sort_pass(s, true, 0, 0, 0, 0, st);
+  if (R <= 256) return 0;
+  sort_pass(s, false, 0, 1, 0, 8, st);
+  return 1;
 }
 
 std::mutex g_sc_mu;
@@ -421,6 +642,8 @@ uint32_t sc_grid(uint64_t items, uint64_t per_block, uint32_t cap) {
   return g < 1 ? 1u : (uint32_t)g;
 }
 
+bool misaligned(const void* p, uintptr_t to) { return ((uintptr_t)p & (to - 1)) != 0; }
+
 }  // namespace
 
 extern "C" size_t argus_attr_scope_workspace_bytes(uint64_t max_instances) {
@@ -438,10 +661,10 @@ extern "C" int argus_attr_scope(const argus_scope_config* cfg, const argus_scope
     return ARGUS_E_INVAL;
   if (io->max_instances > 0 && (!io->d_instances || !io->d_instance_excl)) return ARGUS_E_INVAL;
   if (!d_workspace) return ARGUS_E_INVAL;
-  if (((uintptr_t)io->d_instances & 15) || ((uintptr_t)io->d_instance_excl & 7) ||
-      ((uintptr_t)io->d_n_instances & 7) || ((uintptr_t)io->d_ordinal & 3) ||
-      ((uintptr_t)io->d_stats & 7) || ((uintptr_t)io->d_counters & 7) ||
-      ((uintptr_t)d_workspace & (kScAlign - 1)))
+  if (misaligned(io->d_instances, 16) || misaligned(io->d_instance_excl, 8) ||
+      misaligned(io->d_n_instances, 8) || misaligned(io->d_ordinal, 4) ||
+      misaligned(io->d_stats, 8) || misaligned(io->d_counters, 8) ||
+      misaligned(d_workspace, kScAlign))
     return ARGUS_E_ALIGN;
   const ScLayout L = sc_layout(io->max_instances);
   if (workspace_bytes < L.total) return ARGUS_E_CAPACITY;
@@ -452,36 +675,87 @@ extern "C" int argus_attr_scope(const argus_scope_config* cfg, const argus_scope
   ScopeArgs a{};
   a.inst = io->d_instances;
   a.excl = io->d_instance_excl;
-  a.n_inst = io->d_n_instances;
-  a.max_inst = io->max_instances;
   a.R = cfg->num_regions;
   a.sc = cfg->scope;
   a.region_mask = io->d_region_mask;
   a.ordinal = io->d_ordinal;
   a.stats = io->d_stats;
   a.counters = io->d_counters;
-  for (int b = 0; b < 2; ++b) {
-    a.key[b] = (uint32_t*)(base + L.key[b]);
-    a.val[b] = (uint64_t*)(base + L.val[b]);
-  }
-  a.hist = (uint32_t*)(base + L.hist);
-  a.bsum = (uint32_t*)(base + L.bsum);
-  a.tiles_max = L.tiles;
-  hipStream_t s = (hipStream_t)stream_v;
-  const uint32_t tiles = (uint32_t)L.tiles;
-  const int passes = cfg->num_regions > 256 ? 2 : 1;
+  a.s = make_bufs(base, L.ref, L.hist, L.bsum, io->max_instances, io->d_n_instances,
+                  io->d_instances);
+  hipStream_t st = (hipStream_t)stream_v;
   hipLaunchKernelGGL(k_sc_init, dim3(sc_grid((uint64_t)a.R * ARGUS_RS_WIDTH, kScThreads, 1024)),
-                     dim3(kScThreads), 0, s, a);
-  for (int p = 0; p < passes; ++p) {
-    hipLaunchKernelGGL(k_sc_hist, dim3(tiles), dim3(kScThreads), 0, s, a, p);
-    hipLaunchKernelGGL(k_sc_scan_sums, dim3((uint32_t)L.scan_blocks), dim3(kScThreads), 0, s, a);
-    hipLaunchKernelGGL(k_sc_scan_top, dim3(1), dim3(1024), 0, s, a, (uint32_t)L.scan_blocks);
-    hipLaunchKernelGGL(k_sc_scan_apply, dim3((uint32_t)L.scan_blocks), dim3(kScThreads), 0, s, a);
-    hipLaunchKernelGGL(k_sc_scatter, dim3(tiles), dim3(kScThreads), 0, s, a, p);
-  }
+                     dim3(kScThreads), 0, st, a);
+  const int buf = sort_reference(a.s, a.R, st);
   hipLaunchKernelGGL(k_sc_ordinal, dim3(sc_grid(io->max_instances, kScThreads, 4096)),
-                     dim3(kScThreads), 0, s, a, (passes - 1) & 1);
+                     dim3(kScThreads), 0, st, a, buf);
   hipLaunchKernelGGL(k_sc_stats, dim3(sc_grid(io->max_instances, kScThreads, 4096)),
-                     dim3(kScThreads), 0, s, a);
+                     dim3(kScThreads), 0, st, a);
+  return hipGetLastError() == hipSuccess ? ARGUS_OK : ARGUS_E_HIP;
+}
+
+extern "C" size_t argus_attr_probes_workspace_bytes(uint64_t max_instances, uint64_t n_probes) {
+  if (max_instances >= (1ull << 31) || n_probes >= (1ull << 31)) return 0;
+  return pr_layout(max_instances, n_probes).total;
+}
+
+extern "C" int argus_attr_probes(const argus_probes_config* cfg, const argus_probes_io* io,
+                                 void* d_workspace, size_t workspace_bytes, void* stream_v) {
+  if (!cfg || !io) return ARGUS_E_INVAL;
+  if (cfg->abi_version != ARGUS_ATTR_ABI_VERSION) return ARGUS_E_ABI;
+  if (cfg->num_regions < 1 || cfg->num_regions > 65535) return ARGUS_E_INVAL;
+  if (io->max_instances >= (1ull << 31) || io->n_probes >= (1ull << 31)) return ARGUS_E_CAPACITY;
+  if (!io->d_n_instances || !io->d_counters) return ARGUS_E_INVAL;
+  if (io->max_instances > 0 && !io->d_instances) return ARGUS_E_INVAL;
+  if (io->n_probes > 0 && (!io->d_probes || !io->d_ref || !io->d_completion || !io->d_groups ||
+                           !io->d_mean))
+    return ARGUS_E_INVAL;
+  if (!d_workspace) return ARGUS_E_INVAL;
+  if (misaligned(io->d_instances, 16) || misaligned(io->d_probes, 16) ||
+      misaligned(io->d_n_instances, 8) || misaligned(io->d_ref, 4) ||
+      misaligned(io->d_completion, 8) || misaligned(io->d_groups, 8) ||
+      misaligned(io->d_mean, 8) || misaligned(io->d_counters, 8) ||
+      misaligned(d_workspace, kScAlign))
+    return ARGUS_E_ALIGN;
+  const PrLayout L = pr_layout(io->max_instances, io->n_probes);
+  if (workspace_bytes < L.total) return ARGUS_E_CAPACITY;
+  const int dc = sc_check_device();
+  if (dc != ARGUS_OK) return dc;
+
+  char* base = (char*)d_workspace;
+  ProbeArgs a{};
+  a.inst = io->d_instances;
+  a.probes = reinterpret_cast<const uint4*>(io->d_probes);
+  a.np = io->n_probes;
+  a.R = cfg->num_regions;
+  a.none = io->max_instances;
+  a.ref = make_bufs(base, L.ref, L.hist, L.bsum, io->max_instances, io->d_n_instances,
+                    io->d_instances);
+  a.pb = make_bufs(base, L.pr, L.hist, L.bsum, io->n_probes, nullptr, io->d_instances);
+  a.ref_out = io->d_ref;
+  a.completion = io->d_completion;
+  a.flags = (uint32_t*)(base + L.flags);
+  a.groups = io->d_groups;
+  a.mean = io->d_mean;
+  a.counters = io->d_counters;
+  hipStream_t st = (hipStream_t)stream_v;
+  hipLaunchKernelGGL(k_pr_init, dim3(1), dim3(64), 0, st, a);
+  if (a.np > 0) {
+    a.ref_buf = sort_reference(a.ref, a.R, st);
+    hipLaunchKernelGGL(k_pr_join, dim3(sc_grid(a.np, kScThreads, 4096)), dim3(kScThreads), 0, st,
+                       a);
+    // (instance, latency) order: the latency's eight bytes, then the
+    // instance code's bytes (stable LSD)
+    int in = 0;
+    for (int byte = 0; byte < 8; ++byte, in ^= 1) sort_pass(a.pb, false, in, in ^ 1, 0, 8 * byte, st);
+    const uint32_t code_bits = 64u - (uint32_t)__builtin_clzll(a.none | 1ull);
+    for (uint32_t byte = 0; 8 * byte < code_bits; ++byte, in ^= 1)
+      sort_pass(a.pb, false, in, in ^ 1, 1, 32 + 8 * (int)byte, st);
+    hipLaunchKernelGGL(k_pr_heads, dim3(sc_grid(a.np, kScThreads, 4096)), dim3(kScThreads), 0, st,
+                       a, in);
+    scan_u32(a.flags, a.np, a.pb.bsum, st);
+    hipLaunchKernelGGL(k_pr_groups, dim3(sc_grid(a.np, kScThreads, 4096)), dim3(kScThreads), 0,
+                       st, a, in);
+  }
   return hipGetLastError() == hipSuccess ? ARGUS_OK : ARGUS_E_HIP;
 }

@@ -175,3 +175,38 @@ def pc_samples(records: np.ndarray, n_samples: int, num_pcs: int, num_regions: i
     pc[rng.random(n_samples) < 0.001] = num_pcs
     out["pc"] = pc.astype(np.uint32)
     return out
+
+
+PROBE_DTYPE = np.dtype([("t_start", "<u8"), ("t_end", "<u8"), ("ctx_key", "<u4"),
+                        ("iteration", "<u4"), ("op_region", "<u2"), ("pad0", "<u2"),
+                        ("pad1", "<u4")])
+
+
+def probes_for(ops, n_ctx: int, iterations: int, repeats: int, seed: int = 0,
+               mu: float = 6.5, sigma: float = 0.7, p_missing: float = 0.01) -> np.ndarray:
+    """Synthetic forced-completion probe intervals: for every context in
+    [0, n_ctx), operation region in `ops` and iteration in [0, iterations),
+    `repeats` probe runs each measure one interval whose length is
+    LogNormal(mu, sigma) cycles, on a clock of their own (start times
+    unrelated to the reference trace).  A fraction p_missing asks for an
+    iteration beyond `iterations` (nothing to join).  No join is computed
+    here.  Returns PROBE_DTYPE records in (repeat, context, op, iteration)
+    order."""
+    rng = np.random.default_rng(seed)
+    ops = np.asarray(ops, np.uint16)
+    c, o, i = np.meshgrid(np.arange(n_ctx), np.arange(len(ops)), np.arange(iterations),
+                          indexing="ij")
+    base = np.stack([c.ravel(), o.ravel(), i.ravel()], axis=1)
+    n = len(base) * repeats
+    out = np.zeros(n, PROBE_DTYPE)
+    rows = np.tile(base, (repeats, 1))
+    out["ctx_key"] = rows[:, 0]
+    out["op_region"] = ops[rows[:, 1]]
+    it = rows[:, 2].astype(np.uint32)
+    miss = rng.random(n) < p_missing
+    it[miss] += np.uint32(iterations)
+    out["iteration"] = it
+    out["t_start"] = rng.integers(0, 1 << 40, size=n).astype(np.uint64)
+    lat = np.maximum(1, np.round(rng.lognormal(mu, sigma, size=n))).astype(np.uint64)
+    out["t_end"] = out["t_start"] + lat
+    return out
