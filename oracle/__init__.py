@@ -17,7 +17,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRCS = [os.path.join(_HERE, f) for f in
          ("argus_oracle.cpp", "argus_oracle_samples.cpp", "argus_oracle_scope.cpp",
-          "argus_oracle_probes.cpp")]
+          "argus_oracle_probes.cpp", "argus_oracle_handoffs.cpp")]
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 NUM_COUNTERS = 32
@@ -77,6 +77,10 @@ def _open(path: str):
     q.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_void_p,
                   ctypes.c_uint64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                   ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p]
+    hh = lib.argus_oracle_handoffs
+    hh.restype = ctypes.c_int
+    hh.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint32, ctypes.c_uint32,
+                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     return lib
 
 
@@ -107,6 +111,9 @@ class OracleLib:
 
     def probes(self, *args, **kw):
         return probes(*args, _lib=self._lib, **kw)
+
+    def handoffs(self, *args, **kw):
+        return handoffs(*args, _lib=self._lib, **kw)
 
 
 def _ptr(a):
@@ -272,4 +279,25 @@ def probes(instances: np.ndarray, num_regions: int, probes_: np.ndarray, _lib=No
     g = int(out["counters"][4])
     out["groups"] = out["groups"][:g]
     out["mean"] = out["mean"][:g]
+    return out
+
+
+PH_COUNTER_NAMES = ["n_at_level", "n_gaps", "gap_sum"]
+
+
+def handoffs(instances: np.ndarray, num_regions: int, level: int = 0, _lib=None) -> dict:
+    """Gaps between successive level-`level` siblings.  Returns pairs
+    [R, R, 4] u64 (count, sum, min, max), hist [65] u64, parent_gap [n] u64
+    and counters [8] u64."""
+    inst = np.ascontiguousarray(instances)
+    n = inst.nbytes // 32
+    R = int(num_regions)
+    out = dict(pairs=np.zeros((R, R, 4), np.uint64), hist=np.zeros(65, np.uint64),
+               parent_gap=np.zeros(n, np.uint64), counters=np.zeros(8, np.uint64))
+    lib = _lib if _lib is not None else _load()
+    rc = lib.argus_oracle_handoffs(_ptr(inst) if n else None, n, R, int(level), _ptr(out["pairs"]),
+                                   _ptr(out["hist"]), _ptr(out["parent_gap"]) if n else None,
+                                   _ptr(out["counters"]))
+    if rc != 0:
+        raise ValueError(f"argus_oracle_handoffs failed with {rc}")
     return out

@@ -231,6 +231,31 @@ int argus_oracle_probes(const void* instances, uint64_t n_inst, uint32_t num_reg
                         uint64_t* completion, uint64_t* groups, double* mean,
                         uint64_t group_cap, uint64_t* counters);
 
+/* ------------------------------------------------------------------------
+ * Phase handoffs (Section 4.2: in a persistent kernel the time spent in the
+ * intervals between successive cooperative phases is a measured quantity
+ * of its own; Section 2 names a phase handoff as a region a developer can
+ * change).
+ *
+ * At level L, two instances x and y of one context are successive phases
+ * when y is the next instance after x with the same parent and level L
+ * (for L = 0: the next top-level instance of the context).  For closed x:
+ * gap = t_begin(y) - t_end(x) (an unclosed x has no successor: everything
+ * after it in its context is nested inside it).
+ *   pairs [R * R * 4]: for (region(x), region(y)) count, gap sum (mod 2^64),
+ *                      min (UINT64_MAX if none), max
+ *   hist [65]: gaps by bit width
+ *   parent_gap [n_inst] or NULL: per parent instance, the sum of the gaps
+ *                      between its successive level-L children (L >= 1)
+ *   counters [ORC_PH_NUM_COUNTERS] */
+enum {
+  ORC_PH_N_AT_LEVEL = 0, ORC_PH_N_GAPS = 1, ORC_PH_GAP_SUM = 2, ORC_PH_NUM_COUNTERS = 8
+};
+
+int argus_oracle_handoffs(const void* instances, uint64_t n_inst, uint32_t num_regions,
+                          uint32_t level, uint64_t* pairs, uint64_t* hist, uint64_t* parent_gap,
+                          uint64_t* counters);
+
 #ifdef __cplusplus
 }
 #endif

@@ -25,7 +25,22 @@ SRC = os.path.join(ROOT, "oracle", "argus_oracle.cpp")
 SRC_S = os.path.join(ROOT, "oracle", "argus_oracle_samples.cpp")
 SRC_C = os.path.join(ROOT, "oracle", "argus_oracle_scope.cpp")
 SRC_P = os.path.join(ROOT, "oracle", "argus_oracle_probes.cpp")
-SOURCES = (SRC, SRC_S, SRC_C, SRC_P)
+SRC_H = os.path.join(ROOT, "oracle", "argus_oracle_handoffs.cpp")
+SOURCES = (SRC, SRC_S, SRC_C, SRC_P, SRC_H)
+
+# one-line mutants of the phase handoffs (argus_oracle_handoffs.cpp)
+MUTANTS_H = {
+    "parent_ignored": ("const std::pair<uint32_t, uint32_t> key{b.ctx, b.parent};",
+                       "const std::pair<uint32_t, uint32_t> key{b.ctx, 0u};"),
+    "gap_from_begin": ("const uint64_t gap = b.t_begin - a.t_end;",
+                       "const uint64_t gap = b.t_begin - a.t_begin;"),
+    "level_off_by_one": ("if (b.level != level) continue;", "if (b.level != level + 1) continue;"),
+    "gap_to_child": ("parent_gap[b.parent] += gap;", "parent_gap[y] += gap;"),
+    "min_sentinel_zero": ("pairs[4 * i + 2] = ~uint64_t(0);", "pairs[4 * i + 2] = 0;"),
+    "first_child_kept": ("    last[key] = y;\n", "    if (it == last.end()) last[key] = y;\n"),
+    "pair_transposed": ("pairs + 4 * (uint64_t(a.region) * R + b.region)",
+                        "pairs + 4 * (uint64_t(b.region) * R + a.region)"),
+}
 
 # one-line mutants of the probe join (argus_oracle_probes.cpp)
 MUTANTS_P = {
@@ -222,11 +237,30 @@ def run_probe_pins(orc) -> list[str]:
     return failures
 
 
+def run_handoff_pins(orc) -> list[str]:
+    """The handoff pins of test_oracle_handoffs against `orc`."""
+    import test_oracle_handoffs as th
+    failures = []
+    checks = [("hand_top", lambda: th.test_hand_top_level(orc)),
+              ("hand_steps", lambda: th.test_hand_steps(orc)),
+              ("hand_malformed", lambda: th.test_hand_malformed_phases(orc))]
+    checks += [(f"brute_force_{k}", (lambda k=k: th.test_brute_force(orc, k))) for k in range(24)]
+    checks += [(f"conservation_{k}", (lambda k=k: th.test_time_conservation(orc, k)))
+               for k in range(10)]
+    for name, fn in checks:
+        try:
+            fn()
+        except Exception:  # noqa: BLE001 - any failure kills the mutant
+            failures.append(name)
+    return failures
+
+
 def test_unmutated_oracle_passes_all_pins(oracle_mod):
     assert run_pins(oracle_mod) == []
     assert run_sample_pins(oracle_mod) == []
     assert run_scope_pins(oracle_mod) == []
     assert run_probe_pins(oracle_mod) == []
+    assert run_handoff_pins(oracle_mod) == []
 
 
 def _build_mutant(mutant_dir, name, target, old, new):
@@ -269,3 +303,10 @@ def test_probe_mutant_is_caught(oracle_mod, mutant_dir, name):
     old, new = MUTANTS_P[name]
     orc = oracle_mod.OracleLib(_build_mutant(mutant_dir, name, SRC_P, old, new))
     assert run_probe_pins(orc), f"mutant {name} survived every pin"
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS_H))
+def test_handoff_mutant_is_caught(oracle_mod, mutant_dir, name):
+    old, new = MUTANTS_H[name]
+    orc = oracle_mod.OracleLib(_build_mutant(mutant_dir, name, SRC_H, old, new))
+    assert run_handoff_pins(orc), f"mutant {name} survived every pin"
