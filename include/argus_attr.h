@@ -173,7 +173,8 @@ enum {
   ARGUS_E_ALIGN = -3,    /* records not 16-B aligned or workspace not 256-B aligned */
   ARGUS_E_CAPACITY = -4, /* n_records > max_records, or workspace too small */
   ARGUS_E_DEVICE = -5,   /* current device is not gfx950 */
-  ARGUS_E_HIP = -6       /* a HIP call failed; see argus_attr_last_error */
+  ARGUS_E_HIP = -6,      /* a HIP call failed; see argus_attr_last_error */
+  ARGUS_E_IO = -7        /* a file could not be written (trace export) */
 };
 
 typedef struct argus_attr argus_attr; /* opaque host-side handle */
@@ -434,6 +435,77 @@ size_t argus_attr_probes_workspace_bytes(uint64_t max_instances, uint64_t n_prob
  * any GPU call. */
 int argus_attr_probes(const argus_probes_config* cfg, const argus_probes_io* io,
                       void* d_workspace, size_t workspace_bytes, void* stream);
+
+/* ---------------------------------------------------------- phase handoffs */
+/* Section 4.2 of the paper measures, on the reference trace of a persistent
+ * kernel, the time spent in the intervals between successive cooperative
+ * phases.  Here the phases are the instances of one nesting level L: y
+ * follows x when y is the next level-L instance after x with the same parent
+ * (for L = 0, the next top-level instance of the same context).  For such a
+ * pair (x closed): gap = t_begin(y) - t_end(x).  An unclosed x has no
+ * successor (what follows it is nested inside it).  Integers throughout. */
+enum {
+  ARGUS_HO_N_AT_LEVEL = 0, /* instances at level L */
+  ARGUS_HO_N_GAPS = 1,     /* successive pairs measured */
+  ARGUS_HO_GAP_SUM = 2,    /* their gaps, summed mod 2^64 */
+  ARGUS_HO_NUM_COUNTERS = 8
+};
+
+typedef struct argus_handoffs_config {
+  uint32_t abi_version; /* ARGUS_ATTR_ABI_VERSION */
+  uint32_t num_regions; /* R, 1..4096 (the pair table is R x R) */
+  uint32_t level;       /* L */
+  uint32_t pad;
+} argus_handoffs_config;
+
+typedef struct argus_handoffs_io {
+  const argus_instance* d_instances; /* canonical order (16-byte aligned) */
+  const uint64_t* d_n_instances;     /* device scalar, e.g. &d_counters[ARGUS_C_N_BEGIN] */
+  uint64_t max_instances;            /* capacity, < 2^31 */
+  uint64_t* d_pairs;                 /* out [R][R][4]: for (region(x), region(y)): count,
+                                        gap sum, min (UINT64_MAX if none), max */
+  uint64_t* d_hist;                  /* out [65]: gaps by bit width */
+  uint64_t* d_parent_gap;            /* out [max_instances] or NULL: per parent instance,
+                                        the sum of the gaps between its successive level-L
+                                        children (the handoff time of one step) */
+  uint64_t* d_counters;              /* out [ARGUS_HO_NUM_COUNTERS] */
+} argus_handoffs_io;
+
+/* Device workspace argus_attr_handoffs needs (256-byte aligned). */
+size_t argus_attr_handoffs_workspace_bytes(uint64_t max_instances);
+
+/* Enqueue the handoff statistics on `stream` without synchronising.
+ * Allocates nothing; argument errors are returned before any GPU call. */
+int argus_attr_handoffs(const argus_handoffs_config* cfg, const argus_handoffs_io* io,
+                        void* d_workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------- Chrome-trace export */
+/* Writes the JSON of Chrome Trace Viewer for region instances and probe
+ * summaries, with the lane layout of the paper's Appendix B: a process per
+ * group of contexts (ctx_key >> group_shift; an SM or a block); per
+ * context, one lane per nesting level of its reference instances (levels
+ * >= 7 share lane 7), then for each operation region with probe groups in
+ * that context a lane with the mean exposed latency (a slice from the
+ * operation's issue in the reference trace, as long as the mean) and a lane
+ * with the 80th, 60th, 40th, 20th and 0th percentile bands (slices from the
+ * issue, each nested in the previous).  Timestamps are cycles divided by
+ * cycles_per_us (microseconds, as the format requires).  Host memory; no
+ * GPU call.  Returns ARGUS_OK, ARGUS_E_INVAL for bad arguments (a group
+ * naming an instance >= n_instances included) or ARGUS_E_IO. */
+enum { ARGUS_TRACE_UNMATCHED = 1u }; /* also draw mismatched pairs */
+
+typedef struct argus_trace_options {
+  double cycles_per_us;            /* > 0 */
+  uint32_t group_shift;            /* 0..32 */
+  uint32_t flags;                  /* ARGUS_TRACE_* */
+  const char* const* region_names; /* [num_regions] or NULL ("r<id>") */
+  uint32_t num_regions;            /* 1..65535 */
+  uint32_t pad;
+} argus_trace_options;
+
+int argus_attr_chrome_trace(const argus_instance* h_instances, uint64_t n_instances,
+                            const uint64_t* h_groups, const double* h_mean, uint64_t n_groups,
+                            const argus_trace_options* opt, const char* path);
 
 /* Destroy a handle; NULL is a no-op. */
 void argus_attr_destroy(argus_attr* h);

@@ -19,7 +19,9 @@ from .attr import (ABI_VERSION, COUNTER_NAMES, FORCE_EVENT_SORT, FORCE_FULL_SORT
                    argus_scope_config, argus_scope_io, attribute_samples, load_library,
                    scope_statistics, to_host, PROBE_DTYPE, argus_attr_probes,
                    argus_attr_probes_workspace_bytes, argus_probes_config, argus_probes_io,
-                   join_probes)
+                   join_probes, argus_attr_handoffs, argus_attr_handoffs_workspace_bytes,
+                   argus_handoffs_config, argus_handoffs_io, phase_handoffs,
+                   argus_attr_chrome_trace, argus_trace_options)
 
 __all__ = [
     "ABI_VERSION", "COUNTER_NAMES", "FORCE_EVENT_SORT", "FORCE_FULL_SORT", "FORCE_RECORD_RADIX",
@@ -32,5 +34,7 @@ __all__ = [
     "argus_samples_io", "attribute_samples", "load_library", "to_host", "argus_attr_scope",
     "argus_attr_scope_workspace_bytes", "argus_scope", "argus_scope_config", "argus_scope_io",
     "scope_statistics", "PROBE_DTYPE", "argus_attr_probes", "argus_attr_probes_workspace_bytes",
-    "argus_probes_config", "argus_probes_io", "join_probes",
+    "argus_probes_config", "argus_probes_io", "join_probes", "argus_attr_handoffs",
+    "argus_attr_handoffs_workspace_bytes", "argus_handoffs_config", "argus_handoffs_io",
+    "phase_handoffs", "argus_attr_chrome_trace", "argus_trace_options",
 ]

@@ -25,7 +25,7 @@ RS_WIDTH = 142
 NO_PARENT = 0xFFFFFFFF
 UNCLOSED = 0xFFFF
 ERRORS = {0: "OK", -1: "ARGUS_E_INVAL", -2: "ARGUS_E_ABI", -3: "ARGUS_E_ALIGN",
-          -4: "ARGUS_E_CAPACITY", -5: "ARGUS_E_DEVICE", -6: "ARGUS_E_HIP"}
+          -4: "ARGUS_E_CAPACITY", -5: "ARGUS_E_DEVICE", -6: "ARGUS_E_HIP", -7: "ARGUS_E_IO"}
 COUNTER_NAMES = [
     "n_records", "n_valid", "n_bad_kind", "n_bad_region", "n_begin", "n_end",
     "ts_min", "ts_max", "n_ctx", "n_matched", "n_mismatched", "n_unclosed",
@@ -124,6 +124,29 @@ PG_COLUMNS = ["instance", "count", "sum", "issue", "p0", "p20", "p40", "p60", "p
 PR_NUM_COUNTERS = 8
 PR_COUNTER_NAMES = ["n_probes", "n_bad", "n_joined", "n_unjoined", "n_groups"]
 
+class argus_handoffs_config(ctypes.Structure):
+    _fields_ = [("abi_version", ctypes.c_uint32), ("num_regions", ctypes.c_uint32),
+                ("level", ctypes.c_uint32), ("pad", ctypes.c_uint32)]
+
+
+class argus_handoffs_io(ctypes.Structure):
+    _fields_ = [("d_instances", ctypes.c_void_p), ("d_n_instances", ctypes.c_void_p),
+                ("max_instances", ctypes.c_uint64), ("d_pairs", ctypes.c_void_p),
+                ("d_hist", ctypes.c_void_p), ("d_parent_gap", ctypes.c_void_p),
+                ("d_counters", ctypes.c_void_p)]
+
+
+HO_NUM_COUNTERS = 8
+HO_COUNTER_NAMES = ["n_at_level", "n_gaps", "gap_sum"]
+
+class argus_trace_options(ctypes.Structure):
+    _fields_ = [("cycles_per_us", ctypes.c_double), ("group_shift", ctypes.c_uint32),
+                ("flags", ctypes.c_uint32), ("region_names", ctypes.POINTER(ctypes.c_char_p)),
+                ("num_regions", ctypes.c_uint32), ("pad", ctypes.c_uint32)]
+
+
+TRACE_UNMATCHED = 1
+
 ALL_SCOPE = dict(role_mask=0, role_lo=0, role_hi=0, group_shift=32, group_lo=0, group_hi=0,
                  iter_lo=0, iter_hi=0xFFFFFFFF)
 SC_NUM_COUNTERS = 8
@@ -142,6 +165,9 @@ assert ctypes.sizeof(argus_scope_io) == 64
 assert ctypes.sizeof(argus_probes_config) == 8
 assert ctypes.sizeof(argus_probes_io) == 80
 assert PROBE_DTYPE.itemsize == 32
+assert ctypes.sizeof(argus_handoffs_config) == 16
+assert ctypes.sizeof(argus_handoffs_io) == 56
+assert ctypes.sizeof(argus_trace_options) == 32
 assert ctypes.sizeof(argus_attr_outputs) == 48
 
 _lib = None
@@ -179,6 +205,14 @@ def load_library(path: str = LIB_PATH):
     lib.argus_attr_probes.argtypes = [ctypes.POINTER(argus_probes_config),
                                       ctypes.POINTER(argus_probes_io), vp, ctypes.c_size_t, vp]
     lib.argus_attr_probes.restype = i32
+    lib.argus_attr_handoffs_workspace_bytes.argtypes = [u64]
+    lib.argus_attr_handoffs_workspace_bytes.restype = ctypes.c_size_t
+    lib.argus_attr_handoffs.argtypes = [ctypes.POINTER(argus_handoffs_config),
+                                        ctypes.POINTER(argus_handoffs_io), vp, ctypes.c_size_t, vp]
+    lib.argus_attr_handoffs.restype = i32
+    lib.argus_attr_chrome_trace.argtypes = [vp, u64, vp, vp, u64,
+                                            ctypes.POINTER(argus_trace_options), ctypes.c_char_p]
+    lib.argus_attr_chrome_trace.restype = i32
     lib.argus_attr_destroy.argtypes = [vp]
     lib.argus_attr_destroy.restype = None
     lib.argus_attr_last_error.argtypes = [vp]
@@ -348,6 +382,70 @@ def join_probes(instances, n_instances, probes, num_regions: int, stream=None) -
         raise ArgusError(rc, "argus_attr_probes rejected its arguments")
     out["_workspace"] = ws
     return out
+
+
+def argus_attr_handoffs_workspace_bytes(max_instances: int) -> int:
+    return load_library().argus_attr_handoffs_workspace_bytes(max_instances)
+
+
+def argus_attr_handoffs(cfg: argus_handoffs_config, io: argus_handoffs_io, d_workspace: int,
+                        workspace_bytes: int, stream: int) -> int:
+    return load_library().argus_attr_handoffs(ctypes.byref(cfg) if cfg is not None else None,
+                                              ctypes.byref(io) if io is not None else None,
+                                              d_workspace, workspace_bytes, stream)
+
+
+def phase_handoffs(instances, n_instances, num_regions: int, level: int = 0,
+                   parent_gap: bool = True, stream=None) -> dict:
+    """argus_attr_handoffs on torch CUDA tensors (the instance tensor
+    argus_attr_run wrote and a 1-element uint64 CUDA tensor with the instance
+    count).  Returns pairs [R, R, 4] u64, hist [65] u64, parent_gap [cap]
+    u64 (if asked) and counters [8] u64."""
+    import torch
+    dev = instances.device
+    cap = instances.numel() * instances.element_size() // 32
+    R = int(num_regions)
+    out = dict(pairs=torch.empty((R, R, 4), dtype=torch.uint64, device=dev),
+               hist=torch.empty(65, dtype=torch.uint64, device=dev),
+               counters=torch.empty(HO_NUM_COUNTERS, dtype=torch.uint64, device=dev))
+    if parent_gap:
+        out["parent_gap"] = torch.empty(max(cap, 1), dtype=torch.uint64, device=dev)
+    need = argus_attr_handoffs_workspace_bytes(cap)
+    ws = torch.empty(need + 256, dtype=torch.uint8, device=dev)
+    ws_ptr = (ws.data_ptr() + 255) & ~255
+    cfg = argus_handoffs_config(ABI_VERSION, R, int(level), 0)
+    io = argus_handoffs_io(instances.data_ptr() if cap else None, n_instances.data_ptr(), cap,
+                           out["pairs"].data_ptr(), out["hist"].data_ptr(),
+                           out["parent_gap"].data_ptr() if parent_gap else None,
+                           out["counters"].data_ptr())
+    s = stream if stream is not None else torch.cuda.current_stream(dev)
+    rc = argus_attr_handoffs(cfg, io, ws_ptr, need, s.cuda_stream)
+    if rc != 0:
+        raise ArgusError(rc, "argus_attr_handoffs rejected its arguments")
+    out["_workspace"] = ws
+    return out
+
+
+def argus_attr_chrome_trace(instances: np.ndarray, path: str, num_regions: int,
+                            cycles_per_us: float, group_shift: int = 0, groups=None, mean=None,
+                            region_names=None, unmatched: bool = False) -> int:
+    """Write the Chrome-trace JSON of host instances (INSTANCE_DTYPE) and,
+    optionally, probe groups (u64 [G, 10]) with their means (f64 [G])."""
+    inst = np.ascontiguousarray(instances)
+    n = inst.nbytes // 32
+    g = None if groups is None else np.ascontiguousarray(groups, dtype=np.uint64).reshape(-1, 10)
+    m = None if mean is None else np.ascontiguousarray(mean, dtype=np.float64)
+    ng = 0 if g is None else g.shape[0]
+    names = None
+    if region_names is not None:
+        names = (ctypes.c_char_p * len(region_names))(*[x.encode() for x in region_names])
+    opt = argus_trace_options(float(cycles_per_us), int(group_shift),
+                              TRACE_UNMATCHED if unmatched else 0,
+                              ctypes.cast(names, ctypes.POINTER(ctypes.c_char_p)) if names else None,
+                              int(num_regions), 0)
+    return load_library().argus_attr_chrome_trace(
+        inst.ctypes.data if n else None, n, g.ctypes.data if ng else None,
+        m.ctypes.data if ng else None, ng, ctypes.byref(opt), path.encode())
 
 
 def argus_attr_destroy(h) -> None:

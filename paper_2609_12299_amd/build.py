@@ -16,7 +16,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libargus_attr.so")
 SOURCES = ["attr_host.hip", "k_ingest.hip", "k_radix.hip", "k_match.hip", "k_resolve.hip", "k_merge.hip",
-           "k_agg.hip", "k_overlap.hip", "k_samples.hip", "k_scope.hip"]
+           "k_agg.hip", "k_overlap.hip", "k_samples.hip", "k_scope.hip", "trace_export.hip"]
 ARCH = "gfx950"
 
 

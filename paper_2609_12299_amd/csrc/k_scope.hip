@@ -499,6 +499,105 @@ __global__ __launch_bounds__(kScThreads) void k_pr_groups(ProbeArgs a, int buf) 
   }
 }
 
+// ------------------------------------------------------------ phase handoffs
+// Section 4.2: the time between successive cooperative phases of a
+// persistent kernel is a quantity of its own.  Phases are the instances of
+// one level L; y follows x when it is the next level-L child of the same
+// parent (for L = 0, the next top-level instance of the context).  Between
+// two such siblings lie only descendants of the first, so after compacting
+// the instances of level <= L (in canonical order), a phase's predecessor is
+// simply the element before it, when that one has level L, the same context
+// and the same parent.
+
+struct HandoffArgs {
+  const argus_instance* inst;
+  const uint64_t* n_inst;
+  uint64_t max_inst;
+  uint32_t R, L;
+  uint32_t* flags;  // level <= L, then their exclusive scan
+  uint32_t* comp;   // compacted instance indices
+  uint32_t* bsum;
+  uint64_t* pairs;  // [R][R][4]: count, sum, min, max
+  uint64_t* hist;   // [65]
+  uint64_t* parent_gap;  // [max_inst] or NULL
+  uint64_t* counters;
+};
+
+__device__ __forceinline__ uint64_t ho_count(const HandoffArgs& a) {
+  const uint64_t v = *a.n_inst;
+  return v < a.max_inst ? v : a.max_inst;
+}
+
+__global__ __launch_bounds__(kScThreads) void k_ho_init(HandoffArgs a) {
+  const uint64_t stride = (uint64_t)gridDim.x * kScThreads;
+  const uint64_t first = (uint64_t)blockIdx.x * kScThreads + threadIdx.x;
+  const uint64_t np = (uint64_t)a.R * a.R * 4;
+  for (uint64_t i = first; i < np; i += stride) a.pairs[i] = (i & 3) == 2 ? kU64Max : 0ull;
+  if (a.parent_gap)
+    for (uint64_t i = first; i < a.max_inst; i += stride) a.parent_gap[i] = 0;
+  if (first < 65) a.hist[first] = 0;
+  if (first < ARGUS_HO_NUM_COUNTERS) a.counters[first] = 0;
+}
+
+__global__ __launch_bounds__(kScThreads) void k_ho_flags(HandoffArgs a) {
+  const uint64_t n = ho_count(a);
+  const uint4* inst = reinterpret_cast<const uint4*>(a.inst);
+  uint32_t at = 0;
+  for (uint64_t x = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; x < n;
+       x += (uint64_t)gridDim.x * kScThreads) {
+    const uint32_t lvl = inst[2 * x + 1].z;
+    a.flags[x] = lvl <= a.L ? 1u : 0u;
+    at += lvl == a.L;
+  }
+  const uint32_t t = rows_sum32(row_sum32(at));
+  if ((threadIdx.x & 63) == 0 && t)
+    atomicAdd((unsigned long long*)&a.counters[ARGUS_HO_N_AT_LEVEL], (unsigned long long)t);
+}
+
+__global__ __launch_bounds__(kScThreads) void k_ho_compact(HandoffArgs a) {
+  const uint64_t n = ho_count(a);
+  const uint4* inst = reinterpret_cast<const uint4*>(a.inst);
+  for (uint64_t x = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; x < n;
+       x += (uint64_t)gridDim.x * kScThreads)
+    if (inst[2 * x + 1].z <= a.L) a.comp[a.flags[x]] = (uint32_t)x;
+}
+
+__global__ __launch_bounds__(kScThreads) void k_ho_pairs(HandoffArgs a) {
+  const uint64_t n = ho_count(a);
+  if (n == 0) return;
+  const uint4* inst = reinterpret_cast<const uint4*>(a.inst);
+  const uint64_t m = a.flags[n - 1] + (inst[2 * (n - 1) + 1].z <= a.L ? 1u : 0u);
+  uint64_t gaps = 0, gsum = 0;
+  for (uint64_t k = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; k + 1 < m;
+       k += (uint64_t)gridDim.x * kScThreads) {
+    const uint64_t x = a.comp[k], y = a.comp[k + 1];
+    const uint4 ya = inst[2 * y], yb = inst[2 * y + 1];
+    if (yb.z != a.L) continue;
+    const uint4 xa = inst[2 * x], xb = inst[2 * x + 1];
+    if (xb.z != a.L || xb.x != yb.x || xb.y != yb.y) continue;  // level, context, parent
+    const uint32_t rx = xb.w & 0xFFFFu, ry = yb.w & 0xFFFFu;
+    if ((xb.w >> 16) == kNoEnd || rx >= a.R || ry >= a.R) continue;
+    const uint64_t te = (uint64_t)xa.z | ((uint64_t)xa.w << 32);
+    const uint64_t tb = (uint64_t)ya.x | ((uint64_t)ya.y << 32);
+    const uint64_t gap = tb - te;
+    unsigned long long* row = (unsigned long long*)(a.pairs + 4 * ((uint64_t)rx * a.R + ry));
+    atomicAdd(&row[0], 1ull);
+    atomicAdd(&row[1], (unsigned long long)gap);
+    atomicMin(&row[2], (unsigned long long)gap);
+    atomicMax(&row[3], (unsigned long long)gap);
+    atomicAdd((unsigned long long*)&a.hist[bit_width64(gap)], 1ull);
+    if (a.parent_gap && yb.y != kNoParent && yb.y < n)
+      atomicAdd((unsigned long long*)&a.parent_gap[yb.y], (unsigned long long)gap);
+    gaps += 1;
+    gsum += gap;
+  }
+  const uint64_t g1 = rows_sum64(row_sum64(gaps)), g2 = rows_sum64(row_sum64(gsum));
+  if ((threadIdx.x & 63) == 0) {
+    if (g1) atomicAdd((unsigned long long*)&a.counters[ARGUS_HO_N_GAPS], (unsigned long long)g1);
+    if (g2) atomicAdd((unsigned long long*)&a.counters[ARGUS_HO_GAP_SUM], (unsigned long long)g2);
+  }
+}
+
 }  // namespace argus
 
 using namespace argus;
@@ -756,6 +855,65 @@ extern "C" int argus_attr_probes(const argus_probes_config* cfg, const argus_pro
     scan_u32(a.flags, a.np, a.pb.bsum, st);
     hipLaunchKernelGGL(k_pr_groups, dim3(sc_grid(a.np, kScThreads, 4096)), dim3(kScThreads), 0,
                        st, a, in);
+  }
+  return hipGetLastError() == hipSuccess ? ARGUS_OK : ARGUS_E_HIP;
+}
+
+extern "C" size_t argus_attr_handoffs_workspace_bytes(uint64_t max_instances) {
+  if (max_instances >= (1ull << 31)) return 0;
+  Carver c;
+  const uint64_t m = max_instances ? max_instances : 1;
+  c.take(sizeof(uint32_t) * m);
+  c.take(sizeof(uint32_t) * m);
+  c.take(sizeof(uint32_t) * scan_blocks_for(m));
+  return c.o;
+}
+
+extern "C" int argus_attr_handoffs(const argus_handoffs_config* cfg, const argus_handoffs_io* io,
+                                   void* d_workspace, size_t workspace_bytes, void* stream_v) {
+  if (!cfg || !io) return ARGUS_E_INVAL;
+  if (cfg->abi_version != ARGUS_ATTR_ABI_VERSION) return ARGUS_E_ABI;
+  if (cfg->num_regions < 1 || cfg->num_regions > 4096) return ARGUS_E_INVAL;
+  if (io->max_instances >= (1ull << 31)) return ARGUS_E_CAPACITY;
+  if (!io->d_n_instances || !io->d_pairs || !io->d_hist || !io->d_counters) return ARGUS_E_INVAL;
+  if (io->max_instances > 0 && !io->d_instances) return ARGUS_E_INVAL;
+  if (!d_workspace) return ARGUS_E_INVAL;
+  if (misaligned(io->d_instances, 16) || misaligned(io->d_n_instances, 8) ||
+      misaligned(io->d_pairs, 8) || misaligned(io->d_hist, 8) ||
+      misaligned(io->d_parent_gap, 8) || misaligned(io->d_counters, 8) ||
+      misaligned(d_workspace, kScAlign))
+    return ARGUS_E_ALIGN;
+  if (workspace_bytes < argus_attr_handoffs_workspace_bytes(io->max_instances))
+    return ARGUS_E_CAPACITY;
+  const int dc = sc_check_device();
+  if (dc != ARGUS_OK) return dc;
+
+  Carver c;
+  const uint64_t m = io->max_instances ? io->max_instances : 1;
+  char* base = (char*)d_workspace;
+  HandoffArgs a{};
+  a.inst = io->d_instances;
+  a.n_inst = io->d_n_instances;
+  a.max_inst = io->max_instances;
+  a.R = cfg->num_regions;
+  a.L = cfg->level;
+  a.flags = (uint32_t*)(base + c.take(sizeof(uint32_t) * m));
+  a.comp = (uint32_t*)(base + c.take(sizeof(uint32_t) * m));
+  a.bsum = (uint32_t*)(base + c.take(sizeof(uint32_t) * scan_blocks_for(m)));
+  a.pairs = io->d_pairs;
+  a.hist = io->d_hist;
+  a.parent_gap = io->d_parent_gap;
+  a.counters = io->d_counters;
+  hipStream_t st = (hipStream_t)stream_v;
+  const uint64_t init_items = std::max<uint64_t>((uint64_t)a.R * a.R * 4, io->max_instances);
+  hipLaunchKernelGGL(k_ho_init, dim3(sc_grid(std::max<uint64_t>(init_items, 65), kScThreads, 4096)),
+                     dim3(kScThreads), 0, st, a);
+  if (io->max_instances > 0) {
+    const uint32_t g = sc_grid(io->max_instances, kScThreads, 4096);
+    hipLaunchKernelGGL(k_ho_flags, dim3(g), dim3(kScThreads), 0, st, a);
+    scan_u32(a.flags, io->max_instances, a.bsum, st);
+    hipLaunchKernelGGL(k_ho_compact, dim3(g), dim3(kScThreads), 0, st, a);
+    hipLaunchKernelGGL(k_ho_pairs, dim3(g), dim3(kScThreads), 0, st, a);
   }
   return hipGetLastError() == hipSuccess ? ARGUS_OK : ARGUS_E_HIP;
 }
