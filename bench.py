@@ -201,12 +201,111 @@ def hbm_ceiling(dev, nbytes: int = 4 << 30, reps: int = 5) -> dict:
     return res
 
 
+PART_DEFAULT_CONFIG = {"samples": 3, "scope": 5, "probes": 2, "handoffs": 3}
+
+
+def bench_part(args, d: dict, rec_np: np.ndarray, dev) -> dict:
+    """One of the steps that work on the instances of a run: PC-sample
+    attribution, scoped statistics with iteration ordinals, the probe join,
+    or the phase handoffs.  The run itself is done once, untimed; `value`
+    is units per second of the timed calls (HIP events on the stream), with
+    an algorithmic-byte model of the whole call."""
+    import torch
+
+    import tracegen
+    from paper_2609_12299_amd import (RegionAttribution, attribute_samples, join_probes,
+                                      phase_handoffs, scope_statistics)
+    n = rec_np.shape[0]
+    R = d["num_regions"]
+    rec = torch.from_numpy(rec_np.reshape(-1)).to(dev)
+    ra = RegionAttribution(R, d["num_classes"], d["region_class"], d["group_shift"],
+                           d["num_groups"], max_records=n, device=dev)
+    out = ra.run(rec)
+    torch.cuda.synchronize()
+    nb = int(out["counters"][4].item())
+    inst, cnt = out["instances"], out["counters"][4:5]
+    part = args.part
+    if part == "samples":
+        S, P = args.samples, args.pcs
+        smp_np = tracegen.pc_samples(rec_np, S, P, R, seed=1)
+        smp = torch.from_numpy(smp_np.view(np.uint8).reshape(-1)).to(dev)
+        met = torch.from_numpy(np.stack([np.arange(P, dtype=np.float64) % 97, np.ones(P)])).to(dev)
+
+        def call():
+            return attribute_samples(inst, cnt, smp, R, P, metrics=met)
+        units, unit_name = S, "samples"
+        # each sample, its owner instance and a count update; the [P][R] table
+        # cleared, read twice, alpha written and read (2 metrics)
+        per_call = 56.0 * S + 8.0 * P * R * 6
+        what = (f"{S} PC samples over {P} PCs (2 metrics) on the instances of the "
+                f"{WORKLOADS[args.config]}")
+    elif part == "scope":
+        def call():
+            return scope_statistics(inst, out["instance_excl"], cnt, R, iter_lo=0, iter_hi=15)
+        units, unit_name = nb, "instances"
+        passes = 2 if R > 256 else 1
+        per_call = nb * (48.0 * passes + 20.0 + 44.0)
+        what = f"iterations 0..15 of every region, on the instances of the {WORKLOADS[args.config]}"
+    elif part == "probes":
+        pr_np = tracegen.probes_for([1, 2, 7], d["blocks"] * d["warps"], 16, 5, seed=9)
+        pr = torch.from_numpy(pr_np.view(np.uint8).reshape(-1)).to(dev)
+
+        def call():
+            return join_probes(inst, cnt, pr, R)
+        units, unit_name = len(pr_np), "probes"
+        code_passes = (max(nb, 1).bit_length() + 7) // 8
+        per_call = (nb * 48.0 * (2 if R > 256 else 1)
+                    + len(pr_np) * (64.0 + 32.0 + 48.0 * (8 + code_passes)))
+        what = (f"{len(pr_np)} probes (3 operations x 16 iterations x 5 repeats per warp) joined "
+                f"to the {WORKLOADS[args.config]}")
+    elif part == "handoffs":
+        def call():
+            return phase_handoffs(inst, cnt, R, level=1)
+        units, unit_name = nb, "instances"
+        per_call = nb * 120.0
+        what = f"level-1 phases (operators within token steps) of the {WORKLOADS[args.config]}"
+    else:
+        raise ValueError(part)
+    keep = [call() for _ in range(max(args.warmup, 1))]
+    torch.cuda.synchronize()
+    del keep
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    res = []
+    e0.record()
+    for _ in range(args.steps):
+        res.append(call())
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    del res
+    ra.close()
+    gbs = per_call / (ms * 1e-3) / 1e9
+    return {
+        "metric": f"{unit_name} per second ({part})", "value": units / (ms * 1e-3),
+        "unit": f"{unit_name}/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f64" if part == "samples" else "u64",
+        "data": "synthetic", "config": {"workload": what, "records": n, "instances": nb,
+                                        "units": units, "regions": R},
+        "roofline": {"bound": "hbm", "kernel": f"whole {part} call", "achieved": round(gbs, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                     "traffic": None, "bytes_per_launch": per_call},
+    }
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=5, choices=sorted(WORKLOADS))
+    ap.add_argument("--config", type=int, default=0, choices=[0] + sorted(WORKLOADS),
+                    help="workload (default: 5 for the run, the part's own otherwise)")
+    ap.add_argument("--part", default="attr", choices=["attr", "samples", "scope", "probes",
+                                                       "handoffs"],
+                    help="attr: the whole attribution run (the headline); the others time one "
+                         "step on the instances of a run")
+    ap.add_argument("--samples", type=int, default=1 << 24, help="PC samples (--part samples)")
+    ap.add_argument("--pcs", type=int, default=65536, help="PCs (--part samples)")
     ap.add_argument("--force-full-sort", action="store_true")
     ap.add_argument("--force-event-sort", action="store_true",
                     help="order overlap events with the radix sort instead of merging")
@@ -238,10 +337,16 @@ def main() -> int:
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
 
+    if args.config == 0:
+        args.config = 5 if args.part == "attr" else PART_DEFAULT_CONFIG[args.part]
     t0 = time.perf_counter()
     d = tracegen.generate(args.config, threads=int(os.environ.get("OMP_NUM_THREADS", "16")))
     rec_np = d["records"]
     n = rec_np.shape[0]
+    if args.part != "attr":
+        err(f"generated config {args.config}: {n} records in {time.perf_counter() - t0:.1f}s")
+        print(json.dumps(bench_part(args, d, rec_np, dev)), flush=True)
+        return 0
     params = {k: d[k] for k in ("num_regions", "num_classes", "region_class", "group_shift",
                                 "num_groups")}
     if args.no_overlap:

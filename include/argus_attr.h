@@ -471,8 +471,9 @@ typedef struct argus_handoffs_io {
   uint64_t* d_counters;              /* out [ARGUS_HO_NUM_COUNTERS] */
 } argus_handoffs_io;
 
-/* Device workspace argus_attr_handoffs needs (256-byte aligned). */
-size_t argus_attr_handoffs_workspace_bytes(uint64_t max_instances);
+/* Device workspace argus_attr_handoffs needs (256-byte aligned); 0 for
+ * max_instances >= 2^31 or num_regions outside 1..4096. */
+size_t argus_attr_handoffs_workspace_bytes(uint64_t max_instances, uint32_t num_regions);
 
 /* Enqueue the handoff statistics on `stream` without synchronising.
  * Allocates nothing; argument errors are returned before any GPU call. */

@@ -205,7 +205,7 @@ def load_library(path: str = LIB_PATH):
     lib.argus_attr_probes.argtypes = [ctypes.POINTER(argus_probes_config),
                                       ctypes.POINTER(argus_probes_io), vp, ctypes.c_size_t, vp]
     lib.argus_attr_probes.restype = i32
-    lib.argus_attr_handoffs_workspace_bytes.argtypes = [u64]
+    lib.argus_attr_handoffs_workspace_bytes.argtypes = [u64, ctypes.c_uint32]
     lib.argus_attr_handoffs_workspace_bytes.restype = ctypes.c_size_t
     lib.argus_attr_handoffs.argtypes = [ctypes.POINTER(argus_handoffs_config),
                                         ctypes.POINTER(argus_handoffs_io), vp, ctypes.c_size_t, vp]
@@ -384,8 +384,8 @@ def join_probes(instances, n_instances, probes, num_regions: int, stream=None) -
     return out
 
 
-def argus_attr_handoffs_workspace_bytes(max_instances: int) -> int:
-    return load_library().argus_attr_handoffs_workspace_bytes(max_instances)
+def argus_attr_handoffs_workspace_bytes(max_instances: int, num_regions: int) -> int:
+    return load_library().argus_attr_handoffs_workspace_bytes(max_instances, num_regions)
 
 
 def argus_attr_handoffs(cfg: argus_handoffs_config, io: argus_handoffs_io, d_workspace: int,
@@ -410,7 +410,7 @@ def phase_handoffs(instances, n_instances, num_regions: int, level: int = 0,
                counters=torch.empty(HO_NUM_COUNTERS, dtype=torch.uint64, device=dev))
     if parent_gap:
         out["parent_gap"] = torch.empty(max(cap, 1), dtype=torch.uint64, device=dev)
-    need = argus_attr_handoffs_workspace_bytes(cap)
+    need = argus_attr_handoffs_workspace_bytes(cap, R)
     ws = torch.empty(need + 256, dtype=torch.uint8, device=dev)
     ws_ptr = (ws.data_ptr() + 255) & ~255
     cfg = argus_handoffs_config(ABI_VERSION, R, int(level), 0)

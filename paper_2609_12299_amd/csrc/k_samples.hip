@@ -17,7 +17,7 @@
 // parent links give a sample's owner, the innermost matched active
 // instance.  The counts go to a dense [P][R] table with 64-bit atomics
 // (integer, so the order of the adds does not matter).  Per PC one wave
-// forms T(p), alpha, the owner count and H(p); per region one thread adds
+// forms T(p), alpha, the owner count and H(p); per region one wave adds
 // alpha * m(p) in increasing p with separately rounded products: a fixed
 // rounding order, so m_hat is reproducible bit for bit.
 #include <string.h>
@@ -195,25 +195,45 @@ __global__ __launch_bounds__(kSampThreads) void k_s_pc(SampArgs a) {
     atomicAdd((unsigned long long*)&a.counters[ARGUS_S_N_PAIRS], (unsigned long long)pairs);
 }
 
-// One thread per region: its total count, and each lifted metric as the
+// One wave per region: its total count, and each lifted metric as the
 // products alpha(r, p) * m(p), each rounded, added one at a time in
-// increasing p over the p that region r owns a share of.
+// increasing p over the p that region r owns a share of.  The wave reads 64
+// PCs at a time, forms their products in parallel, and then adds the
+// non-zero ones in lane order (increasing p), so the additions happen in
+// exactly the sequential order while the zeros cost nothing.
+__device__ __forceinline__ double readlane_f64(double v, int lane) {
+  const uint64_t b = __double_as_longlong(v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)b, lane);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), lane);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
 __global__ __launch_bounds__(kSampThreads) void k_s_region(SampArgs a) {
-  const uint64_t r = (uint64_t)blockIdx.x * kSampThreads + threadIdx.x;
-  if (r >= a.R) return;
+  const uint64_t r = ((uint64_t)blockIdx.x * kSampThreads + threadIdx.x) >> 6;
+  if (r >= a.R) return;  // whole waves leave together
+  const uint32_t lane = threadIdx.x & 63;
   uint64_t tot = 0;
-  for (uint64_t p = 0; p < a.P; ++p) tot += a.n[p * a.R + r];
-  a.region_total[r] = tot;
+  for (uint64_t p0 = 0; p0 < a.P; p0 += 64) {
+    const uint64_t p = p0 + lane;
+    tot += p < a.P ? a.n[p * a.R + r] : 0ull;
+  }
+  tot = rows_sum64(row_sum64(tot));
+  if (lane == 0) a.region_total[r] = tot;
   for (uint32_t k = 0; k < a.M; ++k) {
     const double* m = a.metrics + (uint64_t)k * a.P;
     double acc = 0.0;
-#pragma unroll 8
-    for (uint64_t p = 0; p < a.P; ++p) {
-      const uint64_t v = a.n[p * a.R + r];
-      const double prod = a.alpha[p * a.R + r] * m[p];
-      if (v) acc = acc + prod;
+    for (uint64_t p0 = 0; p0 < a.P; p0 += 64) {
+      const uint64_t p = p0 + lane;
+      const uint64_t v = p < a.P ? a.n[p * a.R + r] : 0ull;
+      const double prod = v ? a.alpha[p * a.R + r] * m[p] : 0.0;
+      uint64_t nz = __ballot(v != 0);
+      while (nz) {
+        const int b = __builtin_ctzll(nz);
+        nz &= nz - 1;
+        acc = acc + readlane_f64(prod, b);
+      }
     }
-    a.mhat[(uint64_t)k * a.R + r] = acc;
+    if (lane == 0) a.mhat[(uint64_t)k * a.R + r] = acc;
   }
 }
 
@@ -298,7 +318,7 @@ extern "C" int argus_attr_samples(const argus_samples_config* cfg, const argus_s
                      a);
   hipLaunchKernelGGL(k_s_pc, dim3(grid_for(P, kSampThreads / 64, 4096)), dim3(kSampThreads), 0,
                      s, a);
-  hipLaunchKernelGGL(k_s_region, dim3(grid_for(R, kSampThreads, 4096)), dim3(kSampThreads), 0,
-                     s, a);
+  hipLaunchKernelGGL(k_s_region, dim3(grid_for(R, kSampThreads / 64, 65536)), dim3(kSampThreads),
+                     0, s, a);
   return hipGetLastError() == hipSuccess ? ARGUS_OK : ARGUS_E_HIP;
 }

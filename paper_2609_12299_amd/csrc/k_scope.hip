@@ -308,13 +308,34 @@ __device__ __forceinline__ bool in_range32(uint64_t v, uint32_t lo, uint32_t hi)
   return lo <= v && v <= hi;
 }
 
-// Scoped statistics in canonical order.
-__global__ __launch_bounds__(kScThreads) void k_sc_stats(ScopeArgs a) {
+// Scoped statistics in canonical order.  With LDS_ROWS, each block keeps
+// the twelve scalar columns of every region in LDS (LDS atomics), and adds
+// them to the output once at the end; the histograms always go straight to
+// the output with global atomics.  Without, every column does.
+constexpr uint32_t kScLdsRegions = 1024;  // 12 x 8 B x 1024 = 96 KiB of LDS
+constexpr int kScStatThreads = 1024;
+constexpr int kScCols = 12;               // ARGUS_RS_COUNT .. ARGUS_RS_SELF_NESTED
+
+template <bool LDS_ROWS>
+__global__ __launch_bounds__(kScStatThreads) void k_sc_stats(ScopeArgs a) {
+  extern __shared__ __align__(16) uint8_t sc_smem[];
+  unsigned long long* srow = reinterpret_cast<unsigned long long*>(sc_smem);
   const uint64_t n = sb_count(a.s);
   const uint4* inst = reinterpret_cast<const uint4*>(a.inst);
+  if (LDS_ROWS) {
+    for (uint32_t i = threadIdx.x; i < a.R * kScCols; i += kScStatThreads) {
+      const uint32_t col = i % kScCols;
+      srow[i] = (col == ARGUS_RS_INCL_MIN || col == ARGUS_RS_EXCL_MIN) ? ~0ull : 0ull;
+    }
+    __syncthreads();
+  }
+  auto col_ptr = [&](uint32_t reg, uint32_t col) -> unsigned long long* {
+    return LDS_ROWS ? &srow[(uint64_t)reg * kScCols + col]
+                    : (unsigned long long*)(a.stats + (uint64_t)reg * ARGUS_RS_WIDTH + col);
+  };
   uint32_t c_in = 0, c_m = 0, c_mm = 0, c_u = 0, c_s = 0;
-  for (uint64_t x = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; x < n;
-       x += (uint64_t)gridDim.x * kScThreads) {
+  for (uint64_t x = (uint64_t)blockIdx.x * kScStatThreads + threadIdx.x; x < n;
+       x += (uint64_t)gridDim.x * kScStatThreads) {
     const uint4 h0 = inst[2 * x], h1 = inst[2 * x + 1];
     const uint32_t ctx = h1.x, reg = h1.w & 0xFFFFu, ereg = h1.w >> 16;
     const uint64_t group = a.sc.group_shift >= 32 ? 0ull : (uint64_t)(ctx >> a.sc.group_shift);
@@ -324,37 +345,50 @@ __global__ __launch_bounds__(kScThreads) void k_sc_stats(ScopeArgs a) {
                     (!a.region_mask || a.region_mask[reg] != 0);
     if (!in) continue;
     c_in += 1;
-    unsigned long long* row = (unsigned long long*)(a.stats + (uint64_t)reg * ARGUS_RS_WIDTH);
     if (ereg == kNoEnd) {
       c_u += 1;
-      atomicAdd(&row[ARGUS_RS_UNCLOSED], 1ull);
+      atomicAdd(col_ptr(reg, ARGUS_RS_UNCLOSED), 1ull);
       continue;
     }
     if (ereg != reg) {
       c_mm += 1;
-      atomicAdd(&row[ARGUS_RS_MISM_AS_BEGIN], 1ull);
-      if (ereg < a.R)
-        atomicAdd((unsigned long long*)(a.stats + (uint64_t)ereg * ARGUS_RS_WIDTH +
-                                        ARGUS_RS_MISM_AS_END), 1ull);
+      atomicAdd(col_ptr(reg, ARGUS_RS_MISM_AS_BEGIN), 1ull);
+      if (ereg < a.R) atomicAdd(col_ptr(ereg, ARGUS_RS_MISM_AS_END), 1ull);
       continue;
     }
     c_m += 1;
     const uint64_t tb = (uint64_t)h0.x | ((uint64_t)h0.y << 32);
     const uint64_t te = (uint64_t)h0.z | ((uint64_t)h0.w << 32);
     const uint64_t d = te - tb, ex = a.excl[x];
-    atomicAdd(&row[ARGUS_RS_COUNT], 1ull);
-    atomicAdd(&row[ARGUS_RS_INCL_SUM], (unsigned long long)d);
-    atomicAdd(&row[ARGUS_RS_EXCL_SUM], (unsigned long long)ex);
-    atomicMin(&row[ARGUS_RS_INCL_MIN], (unsigned long long)d);
-    atomicMax(&row[ARGUS_RS_INCL_MAX], (unsigned long long)d);
-    atomicMin(&row[ARGUS_RS_EXCL_MIN], (unsigned long long)ex);
-    atomicMax(&row[ARGUS_RS_EXCL_MAX], (unsigned long long)ex);
-    atomicAdd(&row[ARGUS_RS_HIST_INCL + bit_width64(d)], 1ull);
-    atomicAdd(&row[ARGUS_RS_HIST_EXCL + bit_width64(ex)], 1ull);
+    atomicAdd(col_ptr(reg, ARGUS_RS_COUNT), 1ull);
+    atomicAdd(col_ptr(reg, ARGUS_RS_INCL_SUM), (unsigned long long)d);
+    atomicAdd(col_ptr(reg, ARGUS_RS_EXCL_SUM), (unsigned long long)ex);
+    atomicMin(col_ptr(reg, ARGUS_RS_INCL_MIN), (unsigned long long)d);
+    atomicMax(col_ptr(reg, ARGUS_RS_INCL_MAX), (unsigned long long)d);
+    atomicMin(col_ptr(reg, ARGUS_RS_EXCL_MIN), (unsigned long long)ex);
+    atomicMax(col_ptr(reg, ARGUS_RS_EXCL_MAX), (unsigned long long)ex);
+    unsigned long long* grow = (unsigned long long*)(a.stats + (uint64_t)reg * ARGUS_RS_WIDTH);
+    atomicAdd(&grow[ARGUS_RS_HIST_INCL + bit_width64(d)], 1ull);
+    atomicAdd(&grow[ARGUS_RS_HIST_EXCL + bit_width64(ex)], 1ull);
     const uint32_t par = h1.y;
     if (par != kNoParent && par < n && (inst[2 * (uint64_t)par + 1].w & 0xFFFFu) == reg) {
       c_s += 1;
-      atomicAdd(&row[ARGUS_RS_SELF_NESTED], 1ull);
+      atomicAdd(col_ptr(reg, ARGUS_RS_SELF_NESTED), 1ull);
+    }
+  }
+  if (LDS_ROWS) {
+    __syncthreads();
+    for (uint32_t i = threadIdx.x; i < a.R * kScCols; i += kScStatThreads) {
+      const uint32_t col = i % kScCols, reg = i / kScCols;
+      const unsigned long long v = srow[i];
+      unsigned long long* g = (unsigned long long*)(a.stats + (uint64_t)reg * ARGUS_RS_WIDTH + col);
+      if (col == ARGUS_RS_INCL_MIN || col == ARGUS_RS_EXCL_MIN) {
+        if (v != ~0ull) atomicMin(g, v);
+      } else if (col == ARGUS_RS_INCL_MAX || col == ARGUS_RS_EXCL_MAX) {
+        if (v) atomicMax(g, v);
+      } else if (v) {
+        atomicAdd(g, v);
+      }
     }
   }
   const uint32_t lane = threadIdx.x & 63;
@@ -517,7 +551,9 @@ struct HandoffArgs {
   uint32_t* flags;  // level <= L, then their exclusive scan
   uint32_t* comp;   // compacted instance indices
   uint32_t* bsum;
-  uint64_t* pairs;  // [R][R][4]: count, sum, min, max
+  uint64_t* pairs;  // [R][R][4]: count, sum, min, max (the output)
+  uint64_t* rep;    // [copies][R][R][4]: per-copy accumulators in the workspace
+  uint32_t copies;  // blocks b add into copy b % copies (fewer same-address atomics)
   uint64_t* hist;   // [65]
   uint64_t* parent_gap;  // [max_inst] or NULL
   uint64_t* counters;
@@ -531,8 +567,8 @@ __device__ __forceinline__ uint64_t ho_count(const HandoffArgs& a) {
 __global__ __launch_bounds__(kScThreads) void k_ho_init(HandoffArgs a) {
   const uint64_t stride = (uint64_t)gridDim.x * kScThreads;
   const uint64_t first = (uint64_t)blockIdx.x * kScThreads + threadIdx.x;
-  const uint64_t np = (uint64_t)a.R * a.R * 4;
-  for (uint64_t i = first; i < np; i += stride) a.pairs[i] = (i & 3) == 2 ? kU64Max : 0ull;
+  const uint64_t np = (uint64_t)a.R * a.R * 4 * a.copies;
+  for (uint64_t i = first; i < np; i += stride) a.rep[i] = (i & 3) == 2 ? kU64Max : 0ull;
   if (a.parent_gap)
     for (uint64_t i = first; i < a.max_inst; i += stride) a.parent_gap[i] = 0;
   if (first < 65) a.hist[first] = 0;
@@ -562,11 +598,17 @@ __global__ __launch_bounds__(kScThreads) void k_ho_compact(HandoffArgs a) {
     if (inst[2 * x + 1].z <= a.L) a.comp[a.flags[x]] = (uint32_t)x;
 }
 
+// Successive pairs: count and sum added, min and max only when they would
+// change (a plain read first), into this block's copy of the table; the
+// histogram in LDS, added once per block.
 __global__ __launch_bounds__(kScThreads) void k_ho_pairs(HandoffArgs a) {
+  __shared__ unsigned long long s_hist[65];
+  for (int i = threadIdx.x; i < 65; i += kScThreads) s_hist[i] = 0;
+  __syncthreads();
   const uint64_t n = ho_count(a);
-  if (n == 0) return;
   const uint4* inst = reinterpret_cast<const uint4*>(a.inst);
-  const uint64_t m = a.flags[n - 1] + (inst[2 * (n - 1) + 1].z <= a.L ? 1u : 0u);
+  const uint64_t m = n ? a.flags[n - 1] + (inst[2 * (n - 1) + 1].z <= a.L ? 1u : 0u) : 0;
+  uint64_t* table = a.rep + (uint64_t)(blockIdx.x % a.copies) * a.R * a.R * 4;
   uint64_t gaps = 0, gsum = 0;
   for (uint64_t k = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; k + 1 < m;
        k += (uint64_t)gridDim.x * kScThreads) {
@@ -580,12 +622,14 @@ __global__ __launch_bounds__(kScThreads) void k_ho_pairs(HandoffArgs a) {
     const uint64_t te = (uint64_t)xa.z | ((uint64_t)xa.w << 32);
     const uint64_t tb = (uint64_t)ya.x | ((uint64_t)ya.y << 32);
     const uint64_t gap = tb - te;
-    unsigned long long* row = (unsigned long long*)(a.pairs + 4 * ((uint64_t)rx * a.R + ry));
+    unsigned long long* row = (unsigned long long*)(table + 4 * ((uint64_t)rx * a.R + ry));
     atomicAdd(&row[0], 1ull);
     atomicAdd(&row[1], (unsigned long long)gap);
-    atomicMin(&row[2], (unsigned long long)gap);
-    atomicMax(&row[3], (unsigned long long)gap);
-    atomicAdd((unsigned long long*)&a.hist[bit_width64(gap)], 1ull);
+    if (gap < __hip_atomic_load(&row[2], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+      atomicMin(&row[2], (unsigned long long)gap);
+    if (gap > __hip_atomic_load(&row[3], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+      atomicMax(&row[3], (unsigned long long)gap);
+    atomicAdd(&s_hist[bit_width64(gap)], 1ull);
     if (a.parent_gap && yb.y != kNoParent && yb.y < n)
       atomicAdd((unsigned long long*)&a.parent_gap[yb.y], (unsigned long long)gap);
     gaps += 1;
@@ -595,6 +639,31 @@ __global__ __launch_bounds__(kScThreads) void k_ho_pairs(HandoffArgs a) {
   if ((threadIdx.x & 63) == 0) {
     if (g1) atomicAdd((unsigned long long*)&a.counters[ARGUS_HO_N_GAPS], (unsigned long long)g1);
     if (g2) atomicAdd((unsigned long long*)&a.counters[ARGUS_HO_GAP_SUM], (unsigned long long)g2);
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < 65; i += kScThreads)
+    if (s_hist[i]) atomicAdd((unsigned long long*)&a.hist[i], s_hist[i]);
+}
+
+// The copies combined into the output table.
+__global__ __launch_bounds__(kScThreads) void k_ho_combine(HandoffArgs a) {
+  const uint64_t np = (uint64_t)a.R * a.R;
+  const uint64_t csz = np * 4;
+  for (uint64_t i = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; i < np;
+       i += (uint64_t)gridDim.x * kScThreads) {
+    uint64_t c = 0, sum = 0, mn = kU64Max, mx = 0;
+    for (uint32_t k = 0; k < a.copies; ++k) {
+      const uint64_t* e = a.rep + k * csz + 4 * i;
+      c += e[0];
+      sum += e[1];
+      mn = e[2] < mn ? e[2] : mn;
+      mx = e[3] > mx ? e[3] : mx;
+    }
+    uint64_t* o = a.pairs + 4 * i;
+    o[0] = c;
+    o[1] = sum;
+    o[2] = mn;
+    o[3] = mx;
   }
 }
 
@@ -788,8 +857,20 @@ extern "C" int argus_attr_scope(const argus_scope_config* cfg, const argus_scope
   const int buf = sort_reference(a.s, a.R, st);
   hipLaunchKernelGGL(k_sc_ordinal, dim3(sc_grid(io->max_instances, kScThreads, 4096)),
                      dim3(kScThreads), 0, st, a, buf);
-  hipLaunchKernelGGL(k_sc_stats, dim3(sc_grid(io->max_instances, kScThreads, 4096)),
-                     dim3(kScThreads), 0, st, a);
+  if (a.R <= kScLdsRegions) {
+    const size_t lds = (size_t)a.R * kScCols * sizeof(uint64_t);
+    (void)hipFuncSetAttribute((const void*)k_sc_stats<true>,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    // one block per compute unit: each flushes its rows once
+    hipLaunchKernelGGL(k_sc_stats<true>,
+                       dim3((uint32_t)std::min<uint64_t>(persistent_blocks((const void*)k_sc_stats<true>,
+                                                                           kScStatThreads),
+                                                         sc_grid(io->max_instances, kScStatThreads, 4096))),
+                       dim3(kScStatThreads), lds, st, a);
+  } else {
+    hipLaunchKernelGGL(k_sc_stats<false>, dim3(sc_grid(io->max_instances, kScStatThreads, 4096)),
+                       dim3(kScStatThreads), 0, st, a);
+  }
   return hipGetLastError() == hipSuccess ? ARGUS_OK : ARGUS_E_HIP;
 }
 
@@ -859,14 +940,37 @@ extern "C" int argus_attr_probes(const argus_probes_config* cfg, const argus_pro
   return hipGetLastError() == hipSuccess ? ARGUS_OK : ARGUS_E_HIP;
 }
 
-extern "C" size_t argus_attr_handoffs_workspace_bytes(uint64_t max_instances) {
-  if (max_instances >= (1ull << 31)) return 0;
+namespace {
+
+// Copies of the pair table: up to 8, within 256 MiB.
+uint32_t ho_copies(uint32_t R) {
+  const uint64_t table = (uint64_t)R * R * 4 * sizeof(uint64_t);
+  uint64_t c = (256ull << 20) / table;
+  if (c > 8) c = 8;
+  return c < 1 ? 1u : (uint32_t)c;
+}
+
+struct HoLayout {
+  size_t flags, comp, bsum, rep, total;
+};
+HoLayout ho_layout(uint64_t max_instances, uint32_t R) {
   Carver c;
+  HoLayout L{};
   const uint64_t m = max_instances ? max_instances : 1;
-  c.take(sizeof(uint32_t) * m);
-  c.take(sizeof(uint32_t) * m);
-  c.take(sizeof(uint32_t) * scan_blocks_for(m));
-  return c.o;
+  L.flags = c.take(sizeof(uint32_t) * m);
+  L.comp = c.take(sizeof(uint32_t) * m);
+  L.bsum = c.take(sizeof(uint32_t) * scan_blocks_for(m));
+  L.rep = c.take(sizeof(uint64_t) * 4 * (uint64_t)R * R * ho_copies(R));
+  L.total = c.o;
+  return L;
+}
+
+}  // namespace
+
+extern "C" size_t argus_attr_handoffs_workspace_bytes(uint64_t max_instances,
+                                                      uint32_t num_regions) {
+  if (max_instances >= (1ull << 31) || num_regions < 1 || num_regions > 4096) return 0;
+  return ho_layout(max_instances, num_regions).total;
 }
 
 extern "C" int argus_attr_handoffs(const argus_handoffs_config* cfg, const argus_handoffs_io* io,
@@ -883,13 +987,11 @@ extern "C" int argus_attr_handoffs(const argus_handoffs_config* cfg, const argus
       misaligned(io->d_parent_gap, 8) || misaligned(io->d_counters, 8) ||
       misaligned(d_workspace, kScAlign))
     return ARGUS_E_ALIGN;
-  if (workspace_bytes < argus_attr_handoffs_workspace_bytes(io->max_instances))
-    return ARGUS_E_CAPACITY;
+  const HoLayout HL = ho_layout(io->max_instances, cfg->num_regions);
+  if (workspace_bytes < HL.total) return ARGUS_E_CAPACITY;
   const int dc = sc_check_device();
   if (dc != ARGUS_OK) return dc;
 
-  Carver c;
-  const uint64_t m = io->max_instances ? io->max_instances : 1;
   char* base = (char*)d_workspace;
   HandoffArgs a{};
   a.inst = io->d_instances;
@@ -897,15 +999,18 @@ extern "C" int argus_attr_handoffs(const argus_handoffs_config* cfg, const argus
   a.max_inst = io->max_instances;
   a.R = cfg->num_regions;
   a.L = cfg->level;
-  a.flags = (uint32_t*)(base + c.take(sizeof(uint32_t) * m));
-  a.comp = (uint32_t*)(base + c.take(sizeof(uint32_t) * m));
-  a.bsum = (uint32_t*)(base + c.take(sizeof(uint32_t) * scan_blocks_for(m)));
+  a.flags = (uint32_t*)(base + HL.flags);
+  a.comp = (uint32_t*)(base + HL.comp);
+  a.bsum = (uint32_t*)(base + HL.bsum);
+  a.rep = (uint64_t*)(base + HL.rep);
+  a.copies = ho_copies(cfg->num_regions);
   a.pairs = io->d_pairs;
   a.hist = io->d_hist;
   a.parent_gap = io->d_parent_gap;
   a.counters = io->d_counters;
   hipStream_t st = (hipStream_t)stream_v;
-  const uint64_t init_items = std::max<uint64_t>((uint64_t)a.R * a.R * 4, io->max_instances);
+  const uint64_t init_items =
+      std::max<uint64_t>((uint64_t)a.R * a.R * 4 * a.copies, io->max_instances);
   hipLaunchKernelGGL(k_ho_init, dim3(sc_grid(std::max<uint64_t>(init_items, 65), kScThreads, 4096)),
                      dim3(kScThreads), 0, st, a);
   if (io->max_instances > 0) {
@@ -915,5 +1020,7 @@ extern "C" int argus_attr_handoffs(const argus_handoffs_config* cfg, const argus
     hipLaunchKernelGGL(k_ho_compact, dim3(g), dim3(kScThreads), 0, st, a);
     hipLaunchKernelGGL(k_ho_pairs, dim3(g), dim3(kScThreads), 0, st, a);
   }
+  hipLaunchKernelGGL(k_ho_combine, dim3(sc_grid((uint64_t)a.R * a.R, kScThreads, 4096)),
+                     dim3(kScThreads), 0, st, a);
   return hipGetLastError() == hipSuccess ? ARGUS_OK : ARGUS_E_HIP;
 }
