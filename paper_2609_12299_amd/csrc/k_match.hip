@@ -125,7 +125,7 @@ constexpr uint32_t kQueueCap = kMatchTile / 4;  // queued searches per wave
 // WIDE: keys hold only the timestamp and contexts come from their own array
 // (one instantiation runs, the other returns at once).
 template <bool WIDE>
-__global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
+__global__ __launch_bounds__(kMatchThreads, 3) void k_match(MatchArgs a) {
   const DevPlan* P = a.plan;
   if ((P->rec.wide != 0) != WIDE) return;
   const uint32_t tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -134,8 +134,10 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
   __shared__ __align__(16) uint2 s_leaf[kMatchTile / 8 * kLeafStride];  // tree leaves
   // child sums of local BEGINs; zero between tiles (cleared as they are
   // written out)
-  __shared__ uint64_t s_cs[kMatchTile];
   __shared__ uint32_t s_up[kUpSize];  // upper tree levels
+  // child sums of local BEGINs share the leaves' LDS: the tree is dead once
+  // the searches are answered
+  uint64_t* const s_cs = reinterpret_cast<uint64_t*>(s_leaf);
   // search queues (one per wave) during the searches; then the end time of
   // each local BEGIN closed in the tile
   __shared__ uint64_t s_tend[kMatchTile];
@@ -220,8 +222,6 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
       }
     }
   };
-  issue(tile);
-  for (uint32_t k = tid; k < (uint32_t)kMatchTile; k += kMatchThreads) s_cs[k] = 0;
   for (uint32_t k = tid; k < kOcCap; k += kMatchThreads) s_oc[k] = 0;
   if (tid == 0) {
     s_first = kMatchTile;
@@ -235,13 +235,18 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
   __syncthreads();
 
   for (;;) {
+  issue(tile);
   const uint64_t base = tile * kMatchTile;
   const uint32_t cnt = nv - base < (uint64_t)kMatchTile ? (uint32_t)(nv - base) : (uint32_t)kMatchTile;
   const uint64_t next = tile + gridDim.x;
 
   // ---- this thread's 8 consecutive records (loaded one tile ahead)
-  uint64_t ts[IT];
-  uint32_t ctxr[IT], reg[IT];
+  // the sort key of each record: its timestamp and context are recomputed
+  // from it where needed (fewer live registers)
+  uint64_t kk[IT];
+  uint32_t ctxw[WIDE ? IT : 1], reg[IT];
+  auto TS = [&](int i) -> uint64_t { return ks.ts_min + (wide ? kk[i] : (kk[i] & ks.ts_mask)); };
+  auto CTX = [&](int i) -> uint32_t { return wide ? ctxw[WIDE ? i : 0] : ctx_of_key(kk[i]); };
   uint32_t fb = 0, fv = 0;  // bit i: BEGIN / valid
   uint64_t prev_raw;
   // overlap class of each record (8 bits each, 0xFF: none), from the payload
@@ -253,7 +258,7 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
     for (int i = 0; i < IT; ++i) {
       key[i] = nk[i];
       pay[i] = np[i];
-      ctxr[i] = WIDE ? nc[WIDE ? i : 0] : 0u;
+      if constexpr (WIDE) ctxw[WIDE ? i : 0] = nc[WIDE ? i : 0];
     }
     prev_raw = nprev;
     if (tid == 0) {
@@ -264,11 +269,9 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
       s_nbpre_lo = (uint32_t)ncarry.nbpre;
       s_nbpre_hi = (uint32_t)(ncarry.nbpre >> 32);
     }
-    if (next < n_tiles) issue(next);
 #pragma unroll
     for (int i = 0; i < IT; ++i) {
-      if (!wide) ctxr[i] = ctx_of_key(key[i]);
-      ts[i] = ks.ts_min + (wide ? key[i] : (key[i] & ks.ts_mask));
+      kk[i] = key[i];
       reg[i] = pay[i] & 0xFFFFu;
       if (p0 + i < cnt) {
         fv |= 1u << i;
@@ -280,7 +283,7 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
   }
   // context of the record before this thread's first one: the previous
   // lane's last record, or (lane 0) a load of the record before
-  uint32_t prev0 = lane_prev(ctxr[IT - 1], 0u);
+  uint32_t prev0 = lane_prev(CTX(IT - 1), 0u);
   bool has_prev0 = true;
   if (lane == 0) {
     const uint64_t pp = base + p0;
@@ -297,7 +300,7 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
     const uint32_t p = p0 + i;
     if ((fv >> i) & 1u) {
       const bool isb = (fb >> i) & 1u;
-      const bool head = i > 0 ? ctxr[i - 1] != ctxr[i] : (!has_prev0 || prev0 != ctxr[i]);
+      const bool head = i > 0 ? CTX(i - 1) != CTX(i) : (!has_prev0 || prev0 != CTX(i));
       if (head) {
         fh |= 1u << i;
         first_head = p < first_head ? p : first_head;
@@ -359,11 +362,11 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
 #pragma unroll
     for (int i = 0; i < IT; ++i) {
       if (!((fh >> i) & 1u)) continue;
-      const uint32_t c1 = ctxr[i] + (uint32_t)ks.ctx_min;
+      const uint32_t c1 = CTX(i) + (uint32_t)ks.ctx_min;
       if (ord < a.ctx_cap) a.ctx_list[ord] = make_uint2(c1, (uint32_t)(base + p0 + i));
       ++ord;
       if (i > 0 || has_prev0) {
-        const uint32_t c0 = (i > 0 ? ctxr[i - 1] : prev0) + (uint32_t)ks.ctx_min;
+        const uint32_t c0 = (i > 0 ? CTX(i - 1) : prev0) + (uint32_t)ks.ctx_min;
         const uint32_t hb = 31u - (uint32_t)__clz(c0 ^ c1);
         if (hb < a.shift && group_of(c1) < a.G) need |= 1u << hb;
       }
@@ -527,6 +530,7 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
     }
   }
   __syncthreads();  // the queues are no longer needed: s_tend takes end times
+  for (uint32_t k = tid; k < tile_nb; k += kMatchThreads) s_cs[k] = 0;
 
   // ---- what the answers mean
   uint32_t par[IT];
@@ -540,7 +544,7 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
     const uint32_t qrank = hit[i] & 0x7FFu, qreg = hit[i] >> 11;
     if (!isb) {
       if (found) {
-        s_tend[qrank] = ts[i];
+        s_tend[qrank] = TS(i);
         s_ereg[qrank] = (uint16_t)reg[i];
         if (qreg == reg[i]) mend |= 1u << i;
       } else {
@@ -548,7 +552,7 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
         const uint32_t L = sb[i] - 1;
         const uint32_t idx = L - lo_head;
         if (L >= lo_head && idx < (uint32_t)kMatchTile) {
-          a.pop_ts[pool + idx] = ts[i];
+          a.pop_ts[pool + idx] = TS(i);
           a.pop_reg[pool + idx] = reg[i];
           if (ev_on) a.pop_pos[pool + idx] = (uint32_t)(base + p0 + i);
         } else {
@@ -580,7 +584,7 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
       if (ereg != kNoEnd) {
         const uint64_t t_end = s_tend[k];
         if (ereg == reg[i]) mbeg |= 1u << i;
-        const uint64_t incl = t_end - ts[i];
+        const uint64_t incl = t_end - TS(i);
         if (par[i] == kParOut) {
           const uint32_t oi = (L - 1) - op_lo;
           if (L >= 1 + op_lo && oi < (uint32_t)kMatchTile) {
@@ -607,9 +611,10 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
       if (par[i] == kParNone) pf = kNoParent;
       else if (par[i] == kParOut) pf = kParentPending | (uint32_t)tile;
       else pf = (uint32_t)(nbpre + par[i]);
-      const uint4 w0 = make_uint4((uint32_t)ts[i], (uint32_t)(ts[i] >> 32), (uint32_t)t_end,
+      const uint64_t tb = TS(i);
+      const uint4 w0 = make_uint4((uint32_t)tb, (uint32_t)(tb >> 32), (uint32_t)t_end,
                                   (uint32_t)(t_end >> 32));
-      const uint4 w1 = make_uint4(ctxr[i] + (uint32_t)ks.ctx_min, pf, L, reg[i] | (ereg << 16));
+      const uint4 w1 = make_uint4(CTX(i) + (uint32_t)ks.ctx_min, pf, L, reg[i] | (ereg << 16));
       uint4* dst = (uint4*)(a.inst + id);
       dst[0] = w0;
       dst[1] = w1;
@@ -618,7 +623,6 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
   __syncthreads();  // child sums complete
   for (uint32_t k = tid; k < tile_nb; k += kMatchThreads) {
     a.child_sum[nbpre + k] = s_cs[k];
-    s_cs[k] = 0;
   }
   const uint32_t n_oc = n_op < kOcCap ? n_op : kOcCap;
   for (uint32_t k = tid; k < n_oc; k += kMatchThreads) {
@@ -631,10 +635,10 @@ __global__ __launch_bounds__(kMatchThreads, 2) void k_match(MatchArgs a) {
     uint64_t e[IT];
 #pragma unroll
     for (int i = 0; i < IT; ++i) {
-      const uint64_t g = group_of(ctxr[i] + (uint32_t)ks.ctx_min);
+      const uint64_t g = group_of(CTX(i) + (uint32_t)ks.ctx_min);
       const uint32_t c = (clsp[i >> 2] >> (8 * (i & 3))) & 0xFFu;
       const uint32_t ev = (((mend | mbeg) >> i) & 1u) && c < a.K ? 1u + 2u * c + (((fb >> i) & 1u) ^ 1u) : 0u;
-      e[i] = (es < 64 ? (g << es) : 0ull) | ((ts[i] - ks.ts_min) << kEvCodeBits) | ev;
+      e[i] = (es < 64 ? (g << es) : 0ull) | ((TS(i) - ks.ts_min) << kEvCodeBits) | ev;
     }
     if (p0 + IT <= cnt) {
       uint4* e4 = (uint4*)(evo + base + p0);
