@@ -56,7 +56,7 @@ struct Layout {
   size_t chunk_runs, run_base, run_cnt, run_pos, run_hist, scan_bsum;
   size_t pop_ts, pop_reg, pushes, op_parent, op_sum;
   size_t inst, child_sum, hist_key, agg_part, ov_mask, ov_q;
-  size_t push_pos, pop_pos, ctx_list, ctx_seg, seg_start, seg_split, seg_tile0, part;
+  size_t push_pos, pop_pos, ctx_list, ctx_seg, seg_run, seg_tile0, seg_samp0, part;
   size_t total;
   uint64_t lb_words, tree_leaves, match_tiles, pool_cap, ctx_cap, tiles_cap, chunks, run_cap;
 };
@@ -120,17 +120,19 @@ Layout make_layout(const argus_attr_config& c, uint64_t n, bool own_instances) {
   // merge path of the overlap events
   const bool ev = c.num_classes > 0;
   L.ctx_cap = ev ? (nn < kCtxCap ? nn : kCtxCap) : 0;
-  L.tiles_cap = ev ? ceil_div(nn, kMergeTile) + L.ctx_cap : 0;
+  // a segment of L events takes at most ceil(L / 4096) tiles in a two-way
+  // pass and (L / 256 + 4) / 12 + 1 in a four-way one
+  L.tiles_cap = ev ? ceil_div(nn, kSampStride * kSampPerTile) + L.ctx_cap + ceil_div(L.ctx_cap, 2) : 0;
   L.push_pos = take(ev ? sizeof(uint32_t) * L.pool_cap : 0);
   L.pop_pos = take(ev ? sizeof(uint32_t) * L.pool_cap : 0);
   L.ctx_list = take(sizeof(uint2) * L.ctx_cap);
-  // segment arrays of every merge round, ctx_cap + 1 entries per round
-  const uint64_t segs = ev ? kMaxMergeRounds * (L.ctx_cap + 1) : 0;
+  // segment arrays of every merge pass, ctx_cap + 1 entries per pass
+  const uint64_t segs = ev ? kMaxMergePasses * (L.ctx_cap + 1) : 0;
   L.ctx_seg = take(sizeof(uint32_t) * segs);
-  L.seg_start = take(sizeof(uint32_t) * segs);
-  L.seg_split = take(sizeof(uint32_t) * segs);
+  L.seg_run = take(sizeof(uint4) * segs);
   L.seg_tile0 = take(sizeof(uint32_t) * segs);
-  L.part = take(32 * L.tiles_cap);
+  L.seg_samp0 = take(sizeof(uint32_t) * segs);
+  L.part = take(48 * L.tiles_cap);
   // tile records of the last merge round (2 + 2K + K(K + 1) words each)
   const uint64_t kc = c.num_classes;
   L.mslb = take(sizeof(uint64_t) * (2 + 2 * kc + kc * (kc + 1)) * L.tiles_cap);
@@ -332,9 +334,9 @@ int enqueue_run(argus_attr* h, const argus_record* d_records, uint64_t n, char* 
   w.pop_pos = (uint32_t*)(base + L.pop_pos);
   w.ctx_list = (uint2*)(base + L.ctx_list);
   w.ctx_seg = (uint32_t*)(base + L.ctx_seg);
-  w.seg_start = (uint32_t*)(base + L.seg_start);
-  w.seg_split = (uint32_t*)(base + L.seg_split);
+  w.seg_run = (uint4*)(base + L.seg_run);
   w.seg_tile0 = (uint32_t*)(base + L.seg_tile0);
+  w.seg_samp0 = (uint32_t*)(base + L.seg_samp0);
   w.part = (uint32_t*)(base + L.part);
   w.ctx_cap = L.ctx_cap;
   w.tiles_cap = L.tiles_cap;
@@ -428,13 +430,14 @@ int enqueue_run(argus_attr* h, const argus_record* d_records, uint64_t n, char* 
     if (!step("ev_clear", [&] { return launch_ev_clear(a, s); })) return ARGUS_E_HIP;
     for (int sl = 0; sl < 12; ++sl)
       if (!step(enames[sl], [&] { return launch_radix_pass(a, 1, sl, 2 * n, s); })) return ARGUS_E_HIP;
-    // Merge rounds (device-planned; a round beyond the plan returns at once).
-    // The last round is merged and swept by one kernel; there is always at
-    // least one round (a group of one context is a run by itself).
-    static const char* mnames[kMaxMergeRounds][2] = {
-        {"mpart0", "merge0"}, {"mpart1", "merge1"}, {"mpart2", "merge2"}, {"mpart3", "merge3"},
-        {"mpart4", "merge4"}, {"mpart5", "merge5"}, {"mpart6", "merge6"}, {"mpart7", "merge7"}};
-    int rounds = a.shift < (uint32_t)kMaxMergeRounds ? (int)a.shift : kMaxMergeRounds;
+    // Merge passes (device-planned; a pass beyond the plan returns at once).
+    // Bits are merged two per pass; the last pass is merged and swept by one
+    // kernel; there is always at least one pass (a group of one context is a
+    // run by itself).
+    static const char* mnames[kMaxMergePasses][2] = {
+        {"mpart0", "merge0"}, {"mpart1", "merge1"}, {"mpart2", "merge2"}, {"mpart3", "merge3"}};
+    const int bits = a.shift < (uint32_t)kMaxMergeRounds ? (int)a.shift : kMaxMergeRounds;
+    int rounds = (bits + 1) / 2;
     if (rounds < 1) rounds = 1;
     if (!step("mseg", [&] { return launch_mseg(a, rounds, s); })) return ARGUS_E_HIP;
     for (int r = 0; r < rounds; ++r) {

@@ -36,7 +36,16 @@ constexpr int kSweepSlots = 8;  // groups of one tile aggregated in LDS
 constexpr int kMergeThreads = 512;
 constexpr int kMergeItems = 8;
 constexpr int kMergeTile = kMergeThreads * kMergeItems;  // 4096 events
-constexpr int kMaxMergeRounds = 8;
+constexpr int kMaxMergeRounds = 8;   // context bits merged (two per pass at most)
+constexpr int kMaxMergePasses = 4;   // merge passes: pairs of bits, then a single one
+// Four-way passes cut each segment at every 12th of its samples in merged
+// order, a sample being every 255th event of a run: a tile then holds at
+// most (12 + 4) * 255 - 4 events, which leaves room for the second pair of
+// runs to start at a multiple of 8 in LDS.
+constexpr uint32_t kSampStride = 255;
+constexpr uint32_t kSampPerTile = 12;
+static_assert((kSampPerTile + 4) * kSampStride - 4 + 7 <= (uint32_t)kMergeTile, "four-way tile bound");
+constexpr uint32_t kNoBit = 0xFFFFFFFFu;  // second bit of a two-way pass
 // Bit of a round that merges nothing: every group holds one context, so the
 // last (only) round takes each group as one run (segments = groups).
 constexpr uint32_t kSegByGroup = 0xFFFFFFFFu;
@@ -96,10 +105,10 @@ struct SlotPlan {
 };
 
 struct MergeRound {
-  uint32_t bit;  // context bit merged in this round
-  uint32_t src;  // event buffer read (0/1)
-  uint32_t dst;  // event buffer written
-  uint32_t pad;
+  uint32_t bit;   // (lower) context bit merged in this pass
+  uint32_t src;   // event buffer read (0/1)
+  uint32_t dst;   // event buffer written
+  uint32_t bit2;  // upper bit of a four-way pass, kNoBit for a two-way one
   uint64_t n_segs;
   uint64_t n_tiles;
 };
@@ -127,7 +136,7 @@ struct DevPlan {
   // overlap events ordered by merging per-context runs
   uint32_t ev_merge;   // 1: merge path chosen (else the event radix sort)
   uint32_t m_need;     // bit b: two contexts of one group first differ in bit b
-  uint32_t m_rounds;   // merge rounds (set bits of m_need)
+  uint32_t m_rounds;   // merge passes (set bits of m_need, taken in pairs)
   uint32_t m_nctx;     // contexts of groups < G (a prefix of the context list)
   uint64_t m_end;      // sorted position where groups >= G start (or n_valid)
   MergeRound mr[kMaxMergeRounds];
@@ -242,11 +251,11 @@ struct Work {
   uint32_t* push_pos;   // sorted position of each pushed BEGIN (pool layout)
   uint32_t* pop_pos;    // sorted position of each popping END (pool layout)
   uint2* ctx_list;      // [ctx_cap] (context key, first sorted position)
-  uint32_t* ctx_seg;    // [rounds][ctx_cap + 1] segment of each context
-  uint32_t* seg_start;  // [rounds][ctx_cap + 1]
-  uint32_t* seg_split;  // [rounds][ctx_cap + 1]
-  uint32_t* seg_tile0;  // [rounds][ctx_cap + 1] first merge tile of each segment
-  uint32_t* part;       // [tiles_cap] merge tasks, 32 B each (k_merge.hip)
+  uint32_t* ctx_seg;    // [passes][ctx_cap + 1] segment of each context
+  uint4* seg_run;       // [passes][ctx_cap + 1] starts of the segment's four runs
+  uint32_t* seg_tile0;  // [passes][ctx_cap + 1] first merge tile of each segment
+  uint32_t* seg_samp0;  // [passes][ctx_cap + 1] first sample of each segment (four-way)
+  uint32_t* part;       // [tiles_cap] merge tasks, 48 B each (k_merge.hip)
   uint64_t ctx_cap;
   uint64_t tiles_cap;
   uint64_t lb_words;    // capacity of each lb array in words

@@ -11,17 +11,23 @@
 // only splits a gap), and the runs of the contexts of each group are merged.
 //
 // Contexts of one group (ctx >> shift) are adjacent in the sorted records.
-// Round b merges, for every prefix ctx >> (b + 1), the run of its contexts
-// whose bit b is 0 with the run of those whose bit b is 1; rounds go over
-// the bits b in increasing order, and only over bits in which two
-// neighbouring contexts of one group first differ (no other bit has a pair to
-// merge).  After the last round every group is one run in time order.
+// Merging over bit b takes, for every prefix ctx >> (b + 1), the run of its
+// contexts whose bit b is 0 and the run of those whose bit b is 1; bits go in
+// increasing order, and only bits in which two neighbouring contexts of one
+// group first differ are merged (no other bit has a pair to merge).  A pass
+// merges two such bits at once: four runs per prefix ctx >> (upper bit + 1),
+// in the order of the two bits read as a number, which is the order two
+// passes of one bit each would give.  After the last pass every group is one
+// run in time order.
 //
-// A round is two launches after the segment boundaries of all rounds (one
-// block per round): the merge-path split of every output tile (Green, McColl
-// and Bader's merge path: a binary search on the cross diagonal), and the
-// merge of each tile's two input slices in LDS.  The last round does not
-// store what it merges: k_merge_sweep sweeps each merged tile at once (its
+// A pass is two launches after the segment boundaries of all passes (one
+// block per pass): the splits of every output tile, then the merge of each
+// tile's input slices in LDS (two stages for four runs: the pairs, then
+// their results).  A two-way pass splits at every 4096th output (Green,
+// McColl and Bader's merge path: a binary search on the cross diagonal); a
+// four-way pass ranks every 255th event of each run among the others and
+// cuts at every 12th of them in merged order.  The last pass does not store
+// what it merges: k_merge_sweep sweeps each merged tile at once (its
 // segments are exactly the groups).
 #include "sweep_common.h"
 
@@ -41,9 +47,10 @@ struct MPlanArgs {
   uint64_t ctx_cap;
 };
 
-// Chooses between merging and the event radix sort, and plans the rounds.
+// Chooses between merging and the event radix sort, and plans the passes.
 // Merging applies when the event word (group, timestamp offset, code) fits
-// 64 bits, the context list is complete, and the rounds are few enough.
+// 64 bits, the context list is complete, and the bits to merge are few
+// enough.
 __global__ __launch_bounds__(64) void k_mplan(MPlanArgs a) {
   if (threadIdx.x != 0) return;
   DevPlan* p = a.plan;
@@ -55,44 +62,48 @@ __global__ __launch_bounds__(64) void k_mplan(MPlanArgs a) {
   const uint64_t n_ctx = a.counters[ARGUS_C_N_CTX];
   if (n_ctx > a.ctx_cap) return;
   const uint32_t need = p->m_need;
-  const uint32_t rounds = (uint32_t)__popc(need);
-  // A round moves 8 + 8 bytes per event, a radix pass 12 + 12 plus its
-  // look-back traffic: merging wins up to about twice as many rounds.
+  const uint32_t bits = (uint32_t)__popc(need);
+  // Merging one bit moves 8 + 8 bytes per event, a radix pass 12 + 12 plus
+  // its look-back traffic: merging wins up to about twice as many bits (and
+  // more, two bits sharing a pass).
   const uint32_t radix_passes = (g_bits + ks.ts_bits + 7) / 8;
-  if (rounds > a.max_rounds || rounds > 2 * radix_passes) return;
+  if (bits > a.max_rounds || bits > 2 * radix_passes) return;
   // contexts of groups < G form a prefix of the (sorted) context list
   uint64_t lo = 0, hi = n_ctx;
   while (lo < hi) {
     const uint64_t mid = (lo + hi) / 2;
     const uint32_t c = a.ctx_list[mid].x;
-    const uint64_t g = a.shift >= 32 ? 0u : (c >> a.shift);
+    const uint64_t g = a.shift >= 32 ? 0 : (c >> a.shift);
     if (g < a.G) lo = mid + 1;
     else hi = mid;
   }
   p->m_nctx = (uint32_t)lo;
   p->m_end = lo < n_ctx ? a.ctx_list[lo].y : p->n_valid;
   // No bit to merge: every group is one context, already in time order; one
-  // round that merges nothing takes each group as a run of its own.
-  p->m_rounds = rounds ? rounds : 1u;
-  uint32_t buf = p->rec_final ^ 1u, r = 0;
-  for (uint32_t b = 0; b < 32; ++b) {
-    if (!((need >> b) & 1u)) continue;
+  // pass that merges nothing takes each group as a run of its own.
+  p->m_rounds = bits ? (bits + 1) / 2 : 1u;
+  uint32_t buf = p->rec_final ^ 1u, r = 0, pending = kNoBit;
+  auto emit = [&](uint32_t b, uint32_t b2) {
     MergeRound& m = p->mr[r++];
     m.bit = b;
+    m.bit2 = b2;
     m.src = buf;
     m.dst = buf ^ 1u;
     m.n_segs = 0;
     m.n_tiles = 0;
     buf ^= 1u;
+  };
+  for (uint32_t b = 0; b < 32; ++b) {
+    if (!((need >> b) & 1u)) continue;
+    if (pending == kNoBit) {
+      pending = b;
+    } else {
+      emit(pending, b);
+      pending = kNoBit;
+    }
   }
-  if (rounds == 0) {
-    MergeRound& m = p->mr[0];
-    m.bit = kSegByGroup;
-    m.src = buf;
-    m.dst = buf ^ 1u;
-    m.n_segs = 0;
-    m.n_tiles = 0;
-  }
+  if (pending != kNoBit) emit(pending, kNoBit);
+  if (bits == 0) emit(kSegByGroup, kNoBit);
   p->ev_final = buf;
   p->n_ev = p->m_end;
   KeySpace ek = ks;
@@ -142,37 +153,56 @@ struct MSegArgs {
   DevPlan* plan;
   const uint2* ctx_list;
   uint32_t* ctx_seg;
-  uint32_t* seg_start;
-  uint32_t* seg_split;
+  uint4* seg_run;
   uint32_t* seg_tile0;
-  uint64_t stride;  // per-round stride of the segment arrays
+  uint32_t* seg_samp0;
+  uint64_t* counters;
+  uint64_t stride;  // per-pass stride of the segment arrays
   uint32_t shift;
 };
 
-// Segments of every round (block r: round r): maximal runs of contexts with
-// equal ctx >> (bit + 1); the split is where bit `bit` becomes 1.  They
-// depend on the context list only, so all rounds are planned at once.
+// Samples of a run of len events: every kSampStride-th, from its first.
+__device__ __forceinline__ uint32_t run_samples(uint32_t len) {
+  return (len + kSampStride - 1) / kSampStride;
+}
+
+// Segments of every pass (block r: pass r): maximal runs of contexts with
+// equal ctx >> (top + 1), top being the pass's upper bit.  The class of a
+// context is the pass's bits read as a number (upper bit high).  Contexts of
+// one segment come in class order: two of them first differ in one of the
+// pass's bits, or in a bit an earlier pass merged (then they share a class
+// and a run already).  So a segment is four runs in a row (two in a two-way
+// pass), run q starting at the first context of class >= q.  The segments
+// depend on the context list only, so all passes are planned at once.
 __global__ __launch_bounds__(1024) void k_mseg(MSegArgs a) {
   DevPlan* p = a.plan;
   const int round = blockIdx.x;
   if (!p->ev_merge || (uint32_t)round >= p->m_rounds) return;
-  a.ctx_seg += round * a.stride;
-  a.seg_start += round * a.stride;
-  a.seg_split += round * a.stride;
-  a.seg_tile0 += round * a.stride;
+  const uint64_t off = (uint64_t)round * a.stride;
+  uint32_t* ctx_seg = a.ctx_seg + off;
+  uint4* seg_run = a.seg_run + off;
+  uint32_t* seg_tile0 = a.seg_tile0 + off;
+  uint32_t* seg_samp0 = a.seg_samp0 + off;
   __shared__ uint32_t s_w[16];
-  const uint32_t bit = p->mr[round].bit;
+  const MergeRound mr = p->mr[round];
+  const bool by_group = mr.bit == kSegByGroup;
+  const bool four = !by_group && mr.bit2 != kNoBit;
+  const uint32_t top = four ? mr.bit2 : mr.bit;
   const uint32_t nc = p->m_nctx;
   const uint32_t end = (uint32_t)p->m_end;
   const uint32_t t = threadIdx.x;
-  // segment key: ctx >> (bit + 1), or the group for a round that merges nothing
-  const bool by_group = bit == kSegByGroup;
+  // segment key: ctx >> (top + 1), or the group for a pass that merges nothing
   auto hi_of = [&](uint32_t c) -> uint32_t {
     if (by_group) return a.shift >= 32 ? 0u : (c >> a.shift);
-    return bit >= 31 ? 0u : (c >> (bit + 1));
+    return top >= 31 ? 0u : (c >> (top + 1));
+  };
+  auto cls_of = [&](uint32_t c) -> uint32_t {
+    if (by_group) return 0u;
+    const uint32_t lo = (c >> mr.bit) & 1u;
+    return four ? ((((c >> mr.bit2) & 1u) << 1) | lo) : lo;
   };
 
-  // four consecutive contexts per thread, 4096 per block step
+  // ---- segment heads: four consecutive contexts per thread, 4096 per block step
   uint32_t carry = 0;
   for (uint32_t base = 0; base < nc; base += 4096) {
     const uint32_t j0 = base + 4 * t;
@@ -197,67 +227,93 @@ __global__ __launch_bounds__(1024) void k_mseg(MSegArgs a) {
       const uint32_t j = j0 + q;
       if (j >= nc) continue;
       if (head[q]) {
-        a.seg_start[seg] = e[q].y;
-        a.seg_split[seg] = kNoSplit;
+        seg_run[seg] = make_uint4(e[q].y, kNoSplit, kNoSplit, kNoSplit);
         ++seg;
       }
-      a.ctx_seg[j] = seg - 1;
+      ctx_seg[j] = seg - 1;
     }
     carry += total;
   }
   const uint32_t n_segs = carry;
   __threadfence_block();
   __syncthreads();
-  // first context of each segment whose bit is 1
+  // ---- run starts: runs q of (class before, class] start at a context
   for (uint32_t j = t; j < nc && !by_group; j += 1024) {
     const uint2 e = a.ctx_list[j];
-    if (!((e.x >> bit) & 1u)) continue;
-    bool first1 = j == 0;
-    if (!first1) {
+    const uint32_t c = cls_of(e.x);
+    if (c == 0) continue;
+    uint32_t pc = 0;  // class of the context before it in the segment (0 at a head)
+    if (j > 0) {
       const uint32_t c0 = a.ctx_list[j - 1].x;
-      first1 = hi_of(c0) != hi_of(e.x) || !((c0 >> bit) & 1u);
+      if (hi_of(c0) == hi_of(e.x)) pc = cls_of(c0);
     }
-    if (first1) a.seg_split[a.ctx_seg[j]] = e.y;
+    if (pc > c) flag_internal_error(a.counters, 256);
+    uint32_t* r = reinterpret_cast<uint32_t*>(&seg_run[ctx_seg[j]]);
+    for (uint32_t q = pc + 1; q <= c && q < 4; ++q) r[q] = e.y;
   }
   __threadfence_block();
   __syncthreads();
-  // merge tiles per segment, and their prefix (four segments per thread)
+  // ---- empty runs start where the next one does; tiles and samples per
+  // segment, and their prefixes (four segments per thread)
   carry = 0;
+  uint32_t carry_s = 0;
   for (uint32_t base = 0; base < n_segs; base += 4096) {
     const uint32_t g0 = base + 4 * t;
-    uint32_t tiles[4], nt = 0;
+    uint32_t tiles[4], samp[4], nt = 0, nsm = 0;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const uint32_t sg = g0 + q;
       tiles[q] = 0;
+      samp[q] = 0;
       if (sg < n_segs) {
-        const uint32_t s0 = a.seg_start[sg];
-        const uint32_t s1 = sg + 1 < n_segs ? a.seg_start[sg + 1] : end;
-        if (a.seg_split[sg] == kNoSplit) a.seg_split[sg] = s1;
-        tiles[q] = (uint32_t)ceil_div(s1 - s0, kMergeTile);
+        uint32_t* r = reinterpret_cast<uint32_t*>(&seg_run[sg]);
+        const uint32_t s0 = r[0];
+        const uint32_t s1 = sg + 1 < n_segs ? reinterpret_cast<const uint32_t*>(&seg_run[sg + 1])[0] : end;
+        uint32_t st3 = r[3], st2 = r[2], st1 = r[1];
+        st3 = st3 == kNoSplit ? s1 : st3;
+        st2 = st2 == kNoSplit ? st3 : st2;
+        st1 = st1 == kNoSplit ? st2 : st1;
+        r[1] = st1;
+        r[2] = st2;
+        r[3] = st3;
+        if (four) {
+          samp[q] = run_samples(st1 - s0) + run_samples(st2 - st1) + run_samples(st3 - st2) +
+                    run_samples(s1 - st3);
+          tiles[q] = (samp[q] + kSampPerTile - 1) / kSampPerTile;
+        } else {
+          tiles[q] = (uint32_t)ceil_div(s1 - s0, kMergeTile);
+        }
       }
       nt += tiles[q];
+      nsm += samp[q];
     }
-    uint32_t total;
+    uint32_t total, total_s;
     uint32_t pre = carry + block_incl_scan1024(nt, s_w, &total) - nt;
+    uint32_t pre_s = carry_s + block_incl_scan1024(nsm, s_w, &total_s) - nsm;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const uint32_t sg = g0 + q;
-      if (sg < n_segs) a.seg_tile0[sg] = pre;
+      if (sg < n_segs) {
+        seg_tile0[sg] = pre;
+        seg_samp0[sg] = pre_s;
+      }
       pre += tiles[q];
+      pre_s += samp[q];
     }
     carry += total;
+    carry_s += total_s;
   }
   if (t == 0) {
-    a.seg_tile0[n_segs] = carry;
+    seg_tile0[n_segs] = carry;
+    seg_samp0[n_segs] = carry_s;
     p->mr[round].n_segs = n_segs;
     p->mr[round].n_tiles = carry;
   }
 }
 
 hipError_t launch_mseg(const RunArgs& a, int rounds, hipStream_t s) {
-  MSegArgs m{a.w.plan, a.w.ctx_list, a.w.ctx_seg, a.w.seg_start, a.w.seg_split, a.w.seg_tile0,
-             a.w.ctx_cap + 1, a.shift};
+  MSegArgs m{a.w.plan, a.w.ctx_list, a.w.ctx_seg, a.w.seg_run, a.w.seg_tile0, a.w.seg_samp0,
+             a.out.d_counters, a.w.ctx_cap + 1, a.shift};
   hipLaunchKernelGGL(k_mseg, dim3((uint32_t)(rounds > 0 ? rounds : 1)), dim3(1024), 0, s, m);
   return hipGetLastError();
 }
@@ -288,38 +344,86 @@ __device__ __forceinline__ uint32_t corank(const uint64_t* A, uint32_t la, const
 __device__ __forceinline__ uint32_t lpad(uint32_t i) { return i + (i >> 4); }
 constexpr uint32_t kMergeLds = kMergeTile + kMergeTile / 16 + 2;  // + reads just past a run
 
-// corank over runs A = tile[0, na) and B = tile[na, na + nb) staged in LDS.
-__device__ __forceinline__ uint32_t corank_lds(const uint64_t* se, uint32_t na, uint32_t nb,
-                                               uint32_t d) {
-  uint32_t lo = d > nb ? d - nb : 0u, hi = d < na ? d : na;
+// corank over the runs P = tile slots [op, op + lp) and Q = [oq, oq + lq)
+// staged in LDS.
+__device__ __forceinline__ uint32_t corank_lds(const uint64_t* se, uint32_t op, uint32_t lp,
+                                               uint32_t oq, uint32_t lq, uint32_t d) {
+  uint32_t lo = d > lq ? d - lq : 0u, hi = d < lp ? d : lp;
   while (lo < hi) {
     const uint32_t mid = (lo + hi) >> 1;
-    if (mkey(se[lpad(mid)]) <= mkey(se[lpad(na + d - 1 - mid)])) lo = mid + 1;
+    if (mkey(se[lpad(op + mid)]) <= mkey(se[lpad(oq + d - 1 - mid)])) lo = mid + 1;
     else hi = mid;
   }
   return lo;
 }
 
-// One merge tile: where its slices of the two runs start, their lengths,
-// where its output starts, where the two runs end (absolute sorted
-// positions), and whether it is the first tile of its segment.
+// One merge tile: where its slice of each of the four runs of its segment
+// starts (absolute sorted positions; a two-way pass leaves the last two
+// empty), where its output starts, whether it is the first tile of its
+// segment, and where the four runs end.  A slice ends where the next tile's
+// starts when that tile is in the same segment, else at its run's end.
 struct MergeTask {
-  uint32_t a_pos, na, b_pos, nb, out_pos, a_end, b_end, first;
+  uint32_t pos[4];
+  uint32_t out_pos, first, pad0, pad1;
+  uint32_t end[4];
 };
-static_assert(sizeof(MergeTask) == 32, "MergeTask layout");
+static_assert(sizeof(MergeTask) == 48, "MergeTask layout");
+
+__device__ __forceinline__ void store_task(MergeTask* dst, const uint32_t (&pos)[4], uint32_t out_pos,
+                                           bool first, const uint32_t (&end)[4]) {
+  uint4* d = reinterpret_cast<uint4*>(dst);
+  d[0] = make_uint4(pos[0], pos[1], pos[2], pos[3]);
+  d[1] = make_uint4(out_pos, first ? 1u : 0u, 0u, 0u);
+  d[2] = make_uint4(end[0], end[1], end[2], end[3]);
+}
 
 struct MPartArgs {
   const DevPlan* plan;
   const uint64_t* ev[2];
-  const uint32_t* seg_start;
-  const uint32_t* seg_split;
+  const uint4* seg_run;
   const uint32_t* seg_tile0;
+  const uint32_t* seg_samp0;
   MergeTask* task;
   uint64_t* counters;
   int round;
   uint64_t stride;
 };
 
+// Events of run R (length L) that come before the event of key `key` in
+// merged order: those of key <= key when R is an earlier run (le), else
+// those of key < key.  Counted over R's samples only (the samples before
+// it), then exactly, knowing the sample count `cnt`: the answer lies in
+// ((cnt - 1) * stride, cnt * stride].
+__device__ __forceinline__ bool before(uint64_t e, uint64_t key, bool le) {
+  return le ? mkey(e) <= key : mkey(e) < key;
+}
+__device__ __forceinline__ uint32_t samples_before(const uint64_t* R, uint32_t ns, uint64_t key,
+                                                   bool le) {
+  uint32_t lo = 0, hi = ns;
+  while (lo < hi) {
+    const uint32_t mid = (lo + hi) >> 1;
+    if (before(R[(uint64_t)mid * kSampStride], key, le)) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+__device__ __forceinline__ uint32_t events_before(const uint64_t* R, uint32_t L, uint32_t cnt,
+                                                  uint64_t key, bool le) {
+  if (cnt == 0) return 0;
+  uint32_t lo = (cnt - 1) * kSampStride + 1, hi = cnt * kSampStride < L ? cnt * kSampStride : L;
+  while (lo < hi) {
+    const uint32_t mid = (lo + hi) >> 1;
+    if (before(R[mid], key, le)) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
+// Two-way pass: one thread per tile; the tile's start is the merge-path
+// split at its first output.  Four-way pass: one thread per sample; its rank
+// in merged order is its index in its run plus the samples of the other runs
+// before it, and a sample of rank 12 j starts tile j of its segment, whose
+// slices start where the events of each run before it end.
 __global__ __launch_bounds__(256) void k_mpart(MPartArgs a) {
   const DevPlan* p = a.plan;
   if (!p->ev_merge || (uint32_t)a.round >= p->m_rounds) return;
@@ -329,55 +433,103 @@ __global__ __launch_bounds__(256) void k_mpart(MPartArgs a) {
   const uint32_t end = (uint32_t)p->m_end;
   const uint64_t* src = a.ev[mr.src];
   const uint64_t off = (uint64_t)a.round * a.stride;
-  const uint32_t* seg_start = a.seg_start + off;
-  const uint32_t* seg_split = a.seg_split + off;
+  const uint4* seg_run = a.seg_run + off;
   const uint32_t* seg_tile0 = a.seg_tile0 + off;
-  // Lanes take consecutive tiles and every lane of a wave runs the same
-  // iterations: a tile's end split is the next tile's start split, taken
-  // from the next lane when that tile is in the same segment.
-  const uint32_t lane = threadIdx.x & 63;
   const uint64_t step = (uint64_t)gridDim.x * 256;
-  for (uint64_t k0 = (uint64_t)blockIdx.x * 256 + (threadIdx.x & ~63u); k0 < n_tiles; k0 += step) {
-    const uint64_t k = k0 + lane;
-    const bool in = k < n_tiles;
-    // segment of tile k: the last one whose first tile is <= k
+  const uint64_t gid = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+  const bool four = mr.bit != kSegByGroup && mr.bit2 != kNoBit;
+  if (!four) {
+    for (uint64_t k = gid; k < n_tiles; k += step) {
+      // segment of tile k: the last one whose first tile is <= k
+      uint32_t lo = 0, hi = n_segs;
+      while (hi - lo > 1) {
+        const uint32_t mid = (lo + hi) >> 1;
+        if (seg_tile0[mid] <= k) lo = mid;
+        else hi = mid;
+      }
+      const uint4 R = seg_run[lo];
+      const uint32_t s0 = R.x, sp = R.y;
+      const uint32_t s1 = lo + 1 < n_segs ? seg_run[lo + 1].x : end;
+      const uint32_t L = s1 - s0, la = sp - s0, lb = s1 - sp;
+      const uint64_t d0w = (k - seg_tile0[lo]) * (uint64_t)kMergeTile;
+      if (!(s0 <= sp && sp <= s1 && s1 <= end && R.z == s1 && R.w == s1 && d0w < L)) {
+        flag_internal_error(a.counters, 256);
+        const uint32_t z[4] = {end, end, end, end};
+        store_task(a.task + k, z, end, true, z);
+        continue;
+      }
+      const uint32_t d0 = (uint32_t)d0w;
+      const uint32_t a0 = corank(src + s0, la, src + sp, lb, d0);
+      const uint32_t pos[4] = {s0 + a0, sp + (d0 - a0), s1, s1};
+      const uint32_t ends[4] = {sp, s1, s1, s1};
+      store_task(a.task + k, pos, s0 + d0, k == seg_tile0[lo], ends);
+    }
+    return;
+  }
+  const uint32_t* samp0 = a.seg_samp0 + off;
+  const uint32_t total = n_segs ? samp0[n_segs] : 0u;
+  for (uint64_t u = gid; u < total; u += step) {
     uint32_t lo = 0, hi = n_segs;
-    while (in && hi - lo > 1) {
+    while (hi - lo > 1) {
       const uint32_t mid = (lo + hi) >> 1;
-      if (seg_tile0[mid] <= k) lo = mid;
+      if (samp0[mid] <= u) lo = mid;
       else hi = mid;
     }
-    const uint32_t s0 = in ? seg_start[lo] : 0u, sp = in ? seg_split[lo] : 0u;
-    const uint32_t s1 = !in ? 0u : lo + 1 < n_segs ? seg_start[lo + 1] : end;
-    const bool ok = in && s0 <= sp && sp <= s1 && s1 <= end;
-    const uint32_t L = s1 - s0, la = sp - s0, lb = s1 - sp;
-    const uint64_t d0w = ok ? (k - seg_tile0[lo]) * (uint64_t)kMergeTile : 0ull;
-    const uint32_t d0 = d0w < L ? (uint32_t)d0w : L;
-    const uint32_t d1 = d0 + kMergeTile < L ? d0 + kMergeTile : L;
-    const uint64_t* A = src + s0;
-    const uint64_t* B = src + sp;
-    const uint32_t a0 = ok ? corank(A, la, B, lb, d0) : 0u;
-    // the next tile starts at d1 in the same segment unless d1 == L
-    const uint32_t a0_next = (uint32_t)__shfl_down((int)a0, 1);
-    const uint32_t lo_next = (uint32_t)__shfl_down((int)lo, 1);
-    MergeTask tk{0, 0, 0, 0, 0, 0, 0, 0};
-    if (ok) {
-      uint32_t a1;
-      if (d1 == L) a1 = la;
-      else if (lane < 63 && k + 1 < n_tiles && lo_next == lo) a1 = a0_next;
-      else a1 = corank(A, la, B, lb, d1);
-      tk.a_pos = s0 + a0;
-      tk.na = a1 - a0;
-      tk.b_pos = sp + (d0 - a0);
-      tk.nb = (d1 - a1) - (d0 - a0);
-      tk.out_pos = s0 + d0;
-      tk.a_end = sp;
-      tk.b_end = s1;
-      tk.first = k == seg_tile0[lo] ? 1u : 0u;
-    } else if (in) {
-      flag_internal_error(a.counters, 256);
+    const uint4 R = seg_run[lo];
+    const uint32_t st[5] = {R.x, R.y, R.z, R.w, lo + 1 < n_segs ? seg_run[lo + 1].x : end};
+    bool ok = st[4] <= end;
+    uint32_t len[4], ns[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      ok = ok && st[q] <= st[q + 1];
+      len[q] = st[q + 1] - st[q];
+      ns[q] = run_samples(len[q]);
     }
-    if (in) a.task[k] = tk;
+    // this sample: run q, index k in it
+    uint32_t rem = (uint32_t)(u - samp0[lo]), q = 0;
+#pragma unroll
+    for (int x = 0; x < 3; ++x) {
+      if (q == (uint32_t)x && rem >= ns[x]) {
+        rem -= ns[x];
+        q = x + 1;
+      }
+    }
+    uint32_t sq = st[0], nq = ns[0];
+#pragma unroll
+    for (int x = 1; x < 4; ++x) {
+      sq = q == (uint32_t)x ? st[x] : sq;
+      nq = q == (uint32_t)x ? ns[x] : nq;
+    }
+    const uint32_t tile0 = seg_tile0[lo], tiles = seg_tile0[lo + 1] - tile0;
+    ok = ok && rem < nq;
+    if (!ok) {
+      flag_internal_error(a.counters, 256);
+      continue;
+    }
+    const uint32_t k = rem * kSampStride;
+    const uint64_t key = mkey(src[sq + k]);
+    uint32_t cnt[4], rho = rem;
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      cnt[x] = 0;
+      if ((uint32_t)x != q && ns[x]) cnt[x] = samples_before(src + st[x], ns[x], key, (uint32_t)x < q);
+      rho += cnt[x];
+    }
+    if (rho % kSampPerTile) continue;
+    const uint32_t j = rho / kSampPerTile;
+    if (j >= tiles || tile0 + (uint64_t)j >= n_tiles) {
+      flag_internal_error(a.counters, 256);
+      continue;
+    }
+    uint32_t pos[4], out = st[0];
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      const uint32_t r = (uint32_t)x == q ? k : events_before(src + st[x], len[x], cnt[x], key, (uint32_t)x < q);
+      pos[x] = st[x] + r;
+      out += r;
+    }
+    const uint32_t ends[4] = {st[1], st[2], st[3], st[4]};
+    store_task(a.task + tile0 + j, pos, out, j == 0, ends);
   }
 }
 
@@ -385,21 +537,170 @@ hipError_t launch_mpart(const RunArgs& a, int round, hipStream_t s) {
   MPartArgs m{};
   m.plan = a.w.plan;
   for (int b = 0; b < 2; ++b) m.ev[b] = a.w.key[b];
-  m.seg_start = a.w.seg_start;
-  m.seg_split = a.w.seg_split;
+  m.seg_run = a.w.seg_run;
   m.seg_tile0 = a.w.seg_tile0;
+  m.seg_samp0 = a.w.seg_samp0;
   m.task = (MergeTask*)a.w.part;
   m.counters = a.out.d_counters;
   m.round = round;
   m.stride = a.w.ctx_cap + 1;
-  uint64_t blocks = ceil_div(a.w.tiles_cap, 256);
-  if (blocks > 1024) blocks = 1024;
-  if (blocks < 1) blocks = 1;
+  // one thread per sample of a four-way pass at most
+  const uint64_t work = a.w.tiles_cap * kSampPerTile;
+  uint64_t blocks = ceil_div(work ? work : 1, 256);
+  if (blocks > 2048) blocks = 2048;
   hipLaunchKernelGGL(k_mpart, dim3((uint32_t)blocks), dim3(256), 0, s, m);
   return hipGetLastError();
 }
 
 // ----------------------------------------------------------------- merge
+
+// A tile as the merge kernels take it: the slices of the four runs (start,
+// length), where the runs end, the output start, the event count and
+// whether it starts its segment.
+struct Tile {
+  uint32_t pos[4], n[4], end[4];
+  uint32_t out_pos, cnt, first;
+};
+
+// Reads tile k (and the start of tile k + 1).  False if its slices or output
+// do not lie inside the merged range, or it holds no event or more than its
+// LDS staging takes.
+__device__ __forceinline__ bool tile_of(const MergeTask* task, uint64_t k, uint64_t n_tiles,
+                                        uint32_t m_end, Tile& tl) {
+  const uint4* tp = reinterpret_cast<const uint4*>(task + k);
+  const uint4 p = tp[0], h = tp[1], e = tp[2];
+  uint4 np = e;
+  if (k + 1 < n_tiles) {
+    const uint4* tq = reinterpret_cast<const uint4*>(task + k + 1);
+    const uint4 qp = tq[0], qh = tq[1];
+    if (!qh.y) np = qp;
+  }
+  const uint32_t ps[4] = {p.x, p.y, p.z, p.w}, es[4] = {e.x, e.y, e.z, e.w};
+  const uint32_t ns[4] = {np.x, np.y, np.z, np.w};
+  bool ok = true;
+  uint32_t cnt = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    ok = ok && ps[q] <= ns[q] && ns[q] <= es[q] && es[q] <= m_end;
+    tl.pos[q] = ps[q];
+    tl.end[q] = es[q];
+    tl.n[q] = ns[q] - ps[q];
+    cnt += tl.n[q];
+  }
+  tl.out_pos = h.x;
+  tl.first = h.y;
+  tl.cnt = cnt;
+  // staged with the second pair from the next multiple of 8 on (stage_tile)
+  const uint32_t span = ((tl.n[0] + tl.n[1] + 7u) & ~7u) + tl.n[2] + tl.n[3];
+  return ok && cnt > 0 && span <= (uint32_t)kMergeTile && h.x <= m_end && cnt <= m_end - h.x;
+}
+
+// Loads this thread's share of a tile's inputs, the four slices one after
+// the other (element t + 512 j; past the end: the last element again, never
+// stored).
+__device__ __forceinline__ void load_tile(const uint64_t* src, const Tile& tl, uint32_t t,
+                                          uint64_t* v) {
+  const uint32_t c1 = tl.n[0], c2 = c1 + tl.n[1], c3 = c2 + tl.n[2], cnt = tl.cnt;
+#pragma unroll
+  for (int j = 0; j < kMergeItems; ++j) {
+    const uint32_t i0 = t + (uint32_t)j * kMergeThreads;
+    const uint32_t i = i0 < cnt ? i0 : cnt - 1;
+    const uint32_t at = i < c1 ? tl.pos[0] + i
+                        : i < c2 ? tl.pos[1] + (i - c1)
+                        : i < c3 ? tl.pos[2] + (i - c2)
+                                 : tl.pos[3] + (i - c3);
+    v[j] = src[at];
+  }
+}
+
+// LDS slot of the second pair of runs (C, D) of a tile: the first multiple
+// of 8 at or after the end of the first pair (A, B), so that no thread's 8
+// outputs of the first stage span both pairs.
+__device__ __forceinline__ uint32_t pair2_slot(const Tile& tl) {
+  return (tl.n[0] + tl.n[1] + 7u) & ~7u;
+}
+
+// Stores a thread's share of the inputs in LDS: A | B, then C | D from
+// pair2_slot on.
+__device__ __forceinline__ void stage_tile(uint64_t* se, const uint64_t* v, const Tile& tl,
+                                           uint32_t t) {
+  const uint32_t nx = tl.n[0] + tl.n[1], gap = pair2_slot(tl) - nx;
+#pragma unroll
+  for (int j = 0; j < kMergeItems; ++j) {
+    const uint32_t i = t + (uint32_t)j * kMergeThreads;
+    if (i < tl.cnt) se[lpad(i < nx ? i : i + gap)] = v[j];
+  }
+}
+
+// Merges the runs P = slots [0, na) and Q = [oq, oq + nb) (oq >= na) staged
+// in se into 8 consecutive outputs per thread, written back in merged order
+// to slots [0, na + nb).  Ends with every thread past the read of its
+// inputs; the caller synchronises before reading se.
+__device__ __forceinline__ void merge_tile(uint64_t* se, uint32_t na, uint32_t oq, uint32_t nb,
+                                           uint32_t t) {
+  const uint32_t cnt = na + nb, d = t * kMergeItems;
+  uint64_t o[kMergeItems];
+#pragma unroll
+  for (int j = 0; j < kMergeItems; ++j) o[j] = 0;
+  if (d < cnt) {
+    uint32_t ia = corank_lds(se, 0, na, oq, nb, d), ib = d - ia;
+#pragma unroll
+    for (int j = 0; j < kMergeItems; ++j) {
+      const uint64_t va = se[lpad(ia)], vb = se[lpad(oq + (ib < nb ? ib : nb))];
+      const bool take_a = ia < na && (ib >= nb || mkey(va) <= mkey(vb));
+      o[j] = take_a ? va : vb;
+      ia += take_a;
+      ib += !take_a;
+    }
+  }
+  __syncthreads();  // every thread has read its inputs
+#pragma unroll
+  for (int j = 0; j < kMergeItems; ++j)
+    if (d + (uint32_t)j < cnt) se[lpad(d + j)] = o[j];
+}
+
+// First stage of a four-run tile staged by stage_tile: A with B and C with
+// D, in place (8 consecutive outputs per thread, each thread in one pair).
+// Ends like merge_tile.
+__device__ __forceinline__ void merge_pairs(uint64_t* se, const Tile& tl, uint32_t t) {
+  const uint32_t y0 = pair2_slot(tl), d = t * kMergeItems;
+  const bool second = d >= y0;
+  const uint32_t o0 = second ? y0 : 0u, lp = second ? tl.n[2] : tl.n[0];
+  const uint32_t lq = second ? tl.n[3] : tl.n[1], dd = d - o0, lim = lp + lq;
+  uint64_t o[kMergeItems];
+#pragma unroll
+  for (int j = 0; j < kMergeItems; ++j) o[j] = 0;
+  if (dd < lim) {
+    uint32_t ip = corank_lds(se, o0, lp, o0 + lp, lq, dd), iq = dd - ip;
+#pragma unroll
+    for (int j = 0; j < kMergeItems; ++j) {
+      const uint64_t va = se[lpad(o0 + ip)], vb = se[lpad(o0 + lp + (iq < lq ? iq : lq))];
+      const bool take_p = ip < lp && (iq >= lq || mkey(va) <= mkey(vb));
+      o[j] = take_p ? va : vb;
+      ip += take_p;
+      iq += !take_p;
+    }
+  }
+  __syncthreads();  // every thread has read its inputs
+#pragma unroll
+  for (int j = 0; j < kMergeItems; ++j)
+    if (dd + (uint32_t)j < lim) se[lpad(d + j)] = o[j];
+}
+
+// Both stages on a staged tile (each only where it has two non-empty runs to
+// merge; the decision is the same for the whole block), leaving the merged
+// tile in slots [0, cnt).  Ends synchronised.
+__device__ __forceinline__ void merge_staged(uint64_t* se, const Tile& tl, uint32_t t) {
+  const uint32_t nx = tl.n[0] + tl.n[1], ny = tl.n[2] + tl.n[3];
+  if ((tl.n[0] && tl.n[1]) || (tl.n[2] && tl.n[3])) {
+    merge_pairs(se, tl, t);
+    __syncthreads();
+  }
+  if (nx && ny) {
+    merge_tile(se, nx, pair2_slot(tl), ny, t);
+    __syncthreads();
+  }
+}
 
 struct MergeArgs {
   const DevPlan* plan;
@@ -409,33 +710,14 @@ struct MergeArgs {
   int round;
 };
 
-// A task is usable if its slices and output lie inside the merged range.
-__device__ __forceinline__ bool task_ok(const MergeTask& t, uint32_t end) {
-  return t.na + t.nb <= (uint32_t)kMergeTile && t.na + t.nb > 0 && t.a_pos + t.na <= end &&
-         t.b_pos + t.nb <= end && t.out_pos + t.na + t.nb <= end;
-}
-
-// Loads this thread's share of a tile's inputs (element t + 512 j; past the
-// end: the last element again, never stored).
-__device__ __forceinline__ void load_task(const uint64_t* src, const MergeTask& tk, uint32_t t,
-                                          uint64_t* v) {
-  const uint32_t cnt = tk.na + tk.nb;
-#pragma unroll
-  for (int j = 0; j < kMergeItems; ++j) {
-    const uint32_t i0 = t + (uint32_t)j * kMergeThreads;
-    const uint32_t i = i0 < cnt ? i0 : cnt - 1;
-    v[j] = i < tk.na ? src[tk.a_pos + i] : src[tk.b_pos + (i - tk.na)];
-  }
-}
-
 // Static tiles (tile = block + k * grid; there is no dependency between
-// tiles).  Each tile's two input slices go through LDS; each thread finds
-// its own split and merges 8 outputs, which are staged in LDS again so that
-// the stores are contiguous.  The next tile's task and inputs are loaded
-// while the current one is merged.
+// tiles).  Each tile's input slices go through LDS; each thread finds its
+// own split and merges 8 outputs per stage, which are staged in LDS again so
+// that the stores are contiguous.  The next tile's task and inputs are
+// loaded while the current one is merged.
 __global__ __launch_bounds__(kMergeThreads) void k_merge(MergeArgs a) {
   const DevPlan* p = a.plan;
-  // the last round is k_merge_sweep's
+  // the last pass is k_merge_sweep's
   if (!p->ev_merge || (uint32_t)a.round + 1 >= p->m_rounds) return;
   __shared__ uint64_t s_e[kMergeLds];
   const MergeRound mr = p->mr[a.round];
@@ -446,60 +728,33 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(MergeArgs a) {
   const uint32_t t = threadIdx.x;
   uint64_t k = blockIdx.x;
   if (k >= n_tiles) return;
-  MergeTask tk = a.task[k];
-  bool ok = task_ok(tk, end);
+  Tile tk;
+  bool ok = tile_of(a.task, k, n_tiles, end, tk);
   uint64_t v[kMergeItems];
-  if (ok) load_task(src, tk, t, v);
+  if (ok) load_tile(src, tk, t, v);
   for (; k < n_tiles; k += gridDim.x) {
     const uint64_t kn = k + gridDim.x;
-    MergeTask tn{0, 0, 0, 0, 0, 0, 0, 0};
-    if (kn < n_tiles) tn = a.task[kn];
+    Tile tn;
+    const bool okn = kn < n_tiles && tile_of(a.task, kn, n_tiles, end, tn);
     if (!ok) {
       if (t == 0) flag_internal_error(a.counters, 256);
     } else {
-      const uint32_t na = tk.na, nb = tk.nb, cnt = na + nb;
-#pragma unroll
-      for (int j = 0; j < kMergeItems; ++j) {
-        const uint32_t i = t + (uint32_t)j * kMergeThreads;
-        if (i < cnt) s_e[lpad(i)] = v[j];
-      }
+      const uint32_t cnt = tk.cnt;
+      stage_tile(s_e, v, tk, t);
       __syncthreads();
       // the next tile's inputs, in flight during this merge
-      const bool okn = kn < n_tiles && task_ok(tn, end);
-      if (okn) load_task(src, tn, t, v);
-      uint64_t o[kMergeItems];
-      const uint32_t d = t * kMergeItems;
-      if (d < cnt) {
-        uint32_t ia = corank_lds(s_e, na, nb, d), ib = d - ia;
-#pragma unroll
-        for (int j = 0; j < kMergeItems; ++j) {
-          const uint64_t va = s_e[lpad(ia)], vb = s_e[lpad(na + (ib < nb ? ib : nb))];
-          const bool take_a = ia < na && (ib >= nb || mkey(va) <= mkey(vb));
-          o[j] = take_a ? va : vb;
-          ia += take_a;
-          ib += !take_a;
-        }
-      }
-      __syncthreads();
-      if (d < cnt) {
-#pragma unroll
-        for (int j = 0; j < kMergeItems; ++j)
-          if (d + j < cnt) s_e[lpad(d + j)] = o[j];
-      }
-      __syncthreads();
+      if (okn) load_tile(src, tn, t, v);
+      merge_staged(s_e, tk, t);
 #pragma unroll
       for (int j = 0; j < kMergeItems; ++j) {
         const uint32_t i = t + (uint32_t)j * kMergeThreads;
         if (i < cnt) dst[tk.out_pos + i] = s_e[lpad(i)];
       }
       __syncthreads();
-      ok = okn;
     }
+    if (!ok && okn) load_tile(src, tn, t, v);
     tk = tn;
-    if (kn < n_tiles && !ok && task_ok(tn, end)) {
-      ok = true;
-      load_task(src, tn, t, v);
-    }
+    ok = okn;
   }
 }
 
@@ -517,10 +772,9 @@ hipError_t launch_merge(const RunArgs& a, int round, hipStream_t s) {
   return hipGetLastError();
 }
 
-
-// ------------------------------------------------- last round and the sweep
+// -------------------------------------------------- last pass and the sweep
 //
-// The last round's segments are the groups, and it is swept tile by tile as
+// The last pass's segments are the groups, and it is swept tile by tile as
 // it is merged.  A tile cannot know the class counts entering it without
 // waiting for the tiles before it, so it records sums from which its share
 // of U and Q follows once those counts are known (k_ovt_final).  With the
@@ -553,22 +807,22 @@ struct MergeSweepArgs {
   uint64_t* counters;
 };
 
-// A task of the last round is usable if its slices lie inside their runs and
-// the runs inside the merged range.
-__device__ __forceinline__ bool task_ok_last(const MergeTask& t, uint32_t end) {
-  return task_ok(t, end) && t.a_pos + t.na <= t.a_end && t.a_end <= t.b_end &&
-         t.b_pos + t.nb <= t.b_end && t.b_end <= end;
-}
-
-// The word that follows a tile in merged order (ties: run A first), if its
-// segment continues.
-__device__ __forceinline__ bool tile_next(const uint64_t* src, const MergeTask& t, uint64_t* w) {
-  const uint32_t a1 = t.a_pos + t.na, b1 = t.b_pos + t.nb;
-  const bool ha = a1 < t.a_end, hb = b1 < t.b_end;
-  if (!ha && !hb) return false;
-  const uint64_t ea = ha ? src[a1] : 0ull, eb = hb ? src[b1] : 0ull;
-  *w = (ha && (!hb || mkey(ea) <= mkey(eb))) ? ea : eb;
-  return true;
+// The word that follows a tile in merged order (ties: the earlier run), if
+// its segment continues.
+__device__ __forceinline__ bool tile_next(const uint64_t* src, const Tile& t, uint64_t* w) {
+  bool has = false;
+  uint64_t best = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t at = t.pos[q] + t.n[q];
+    if (at < t.end[q]) {
+      const uint64_t e = src[at];
+      if (!has || mkey(e) < mkey(best)) best = e;
+      has = true;
+    }
+  }
+  *w = best;
+  return has;
 }
 
 // Per-thread sums over the merged events at tile positions d .. d + nval - 1
@@ -650,7 +904,7 @@ constexpr int kMsItems = kMergeTile / kMsThreads;
 static_assert(kMsThreads % 64 == 0 && kMsThreads <= kMergeThreads, "sweep threads");
 static_assert(1 + 8 + 8 * 9 < kMsThreads - 1, "one thread per sum, and one for the header");
 
-// LDS of one block of the last round.
+// LDS of one block of the last pass.
 template <int KC>
 struct MsShared {
   static constexpr int NW = kMsThreads / 64;
@@ -665,31 +919,6 @@ struct MsShared {
   static constexpr int BW = 17;
   uint32_t bins[BINS ? kMsThreads * BW : 1];
 };
-
-// Merges the tile staged in se (run A then run B) into 8 consecutive outputs
-// per thread and writes them back in merged order.  Ends with every thread
-// past the read of its inputs; the caller synchronises before reading se.
-__device__ __forceinline__ void merge_tile(uint64_t* se, uint32_t na, uint32_t nb, uint32_t t) {
-  const uint32_t cnt = na + nb, d = t * kMergeItems;
-  uint64_t o[kMergeItems];
-#pragma unroll
-  for (int j = 0; j < kMergeItems; ++j) o[j] = 0;
-  if (d < cnt) {
-    uint32_t ia = corank_lds(se, na, nb, d), ib = d - ia;
-#pragma unroll
-    for (int j = 0; j < kMergeItems; ++j) {
-      const uint64_t va = se[lpad(ia)], vb = se[lpad(na + (ib < nb ? ib : nb))];
-      const bool take_a = ia < na && (ib >= nb || mkey(va) <= mkey(vb));
-      o[j] = take_a ? va : vb;
-      ia += take_a;
-      ib += !take_a;
-    }
-  }
-  __syncthreads();  // every thread has read its inputs
-#pragma unroll
-  for (int j = 0; j < kMergeItems; ++j)
-    if (d + (uint32_t)j < cnt) se[lpad(d + j)] = o[j];
-}
 
 // Sums of one merged tile (se, cnt events; ss.next / ss.has_next: the word
 // after it) into its record.  Returns false, with only the record's header
@@ -861,9 +1090,10 @@ __device__ __forceinline__ bool tile_sums(const uint64_t* se, uint32_t cnt, bool
   return true;
 }
 
-// The last merge round fused with the class-overlap sums.  Each tile of 4096
-// merged events belongs to one group.  Per tile: merge the two input slices
-// in LDS (8 consecutive outputs per thread, written back in merged order),
+// The last merge pass fused with the class-overlap sums.  Each tile of at
+// most 4096 merged events belongs to one group.  Per tile: merge the input
+// slices in LDS (8 consecutive outputs per thread and stage, written back in
+// merged order),
 // scan the class-count deltas over the block, take the tile minima, and sum
 // S0, S1', S2', T over the tile's gaps into the tile's record with its
 // deltas and minima.  A tile spanning 2^32 cycles or more only gets its
@@ -906,8 +1136,8 @@ __device__ __forceinline__ void merge_sweep_tiles(const MergeSweepArgs& a) {
     for (uint32_t h = 0; h < n_here; ++h) {
       const uint64_t k = WIDE ? k0 + s_wide[h] : k0;
       uint64_t* rec = a.rec + k * RW;
-      const MergeTask tk = a.task[k];
-      if (!task_ok_last(tk, end)) {
+      Tile tk;
+      if (!tile_of(a.task, k, n_tiles, end, tk)) {
         if (WIDE) continue;  // never flagged
         // unusable task: a record that starts a segment and adds nothing
         if (t == 0) flag_internal_error(a.counters, 256);
@@ -915,23 +1145,18 @@ __device__ __forceinline__ void merge_sweep_tiles(const MergeSweepArgs& a) {
         continue;
       }
       uint64_t v[kMergeItems];
-      load_task(src, tk, t, v);
+      load_tile(src, tk, t, v);
       uint64_t nx = 0;
       bool hnx = false;
       if (t == 0) hnx = tile_next(src, tk, &nx);
-      const uint32_t cnt = tk.na + tk.nb;
-#pragma unroll
-      for (int j = 0; j < kMergeItems; ++j) {
-        const uint32_t i = t + (uint32_t)j * kMergeThreads;
-        if (i < cnt) s_e[lpad(i)] = v[j];
-      }
+      const uint32_t cnt = tk.cnt;
+      stage_tile(s_e, v, tk, t);
       if (t == 0) {
         ss.next = nx;
         ss.has_next = hnx ? 1u : 0u;
       }
       __syncthreads();
-      merge_tile(s_e, tk.na, tk.nb, t);
-      __syncthreads();
+      merge_staged(s_e, tk, t);
       tile_sums<KC, WIDE>(s_e, cnt, tk.first != 0, ss, rec, es);
       __syncthreads();
     }
@@ -946,7 +1171,7 @@ __global__ __launch_bounds__(kMergeThreads, KC <= 4 ? 6 : 1) void k_merge_sweep(
   merge_sweep_tiles<KC, false>(a);
 }
 
-// Tiles of the last round flagged as spanning 2^32 cycles or more: merged
+// Tiles of the last pass flagged as spanning 2^32 cycles or more: merged
 // again and summed with 64-bit gaps.
 template <int KC>
 __global__ __launch_bounds__(kMergeThreads) void k_merge_sweep_wide(MergeSweepArgs a) {

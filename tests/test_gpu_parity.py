@@ -106,7 +106,8 @@ def test_merge_many_small_contexts(oracle_mod, shift, G):
 
 def test_merge_skewed_contexts(oracle_mod):
     """One group: a context spanning many merge tiles next to contexts of a
-    few records, and eight merge rounds (contexts differ in bits 0..7)."""
+    few records, and eight context bits (0..7) merged in four four-way
+    passes."""
     rng = np.random.default_rng(77)
     sizes = [(0, 40000), (1, 2), (2, 4), (4, 30000), (8, 6), (16, 9000), (32, 2), (64, 12),
              (128, 5000)]
@@ -115,7 +116,42 @@ def test_merge_skewed_contexts(oracle_mod):
              group_shift=32, num_groups=1)
     log(f"[gpu] merge: skewed contexts n={len(rec)}")
     g = gpu_run(rec, p, with_plan=True)
-    assert g["_plan"]["ev_merge"] == 1 and g["_plan"]["merge_rounds"] == 8
+    assert g["_plan"]["ev_merge"] == 1 and g["_plan"]["merge_rounds"] == 4
+    assert_parity(g, oracle_run(oracle_mod, rec, p))
+
+
+@pytest.mark.parametrize("case", ["odd_bits", "empty_runs", "five_bits", "ties"])
+def test_merge_four_way(oracle_mod, case):
+    """Four-way passes: three context bits (a four-way pass, then a two-way
+    last pass), segments of a four-way pass with empty runs in the middle
+    and at the end (classes 0 and 3 only; 0 and 1 only), five bits (two
+    stored four-way passes), and runs of equal timestamps across the four
+    runs of a segment, each over several tiles."""
+    rng = np.random.default_rng(["odd_bits", "empty_runs", "five_bits", "ties"].index(case) + 101)
+    spread, passes = 1 << 36, None
+    if case == "odd_bits":
+        sizes = [(0, 9000), (1, 3000), (2, 700), (3, 12000), (4, 5), (5, 2), (6, 8000), (7, 40)]
+        shift, passes = 3, 2
+    elif case == "empty_runs":
+        # bits 0 and 1 in one pass: segment {0, 1} has runs 2, 3 empty,
+        # segment {4, 7} runs 1, 2; bit 2 in the last pass
+        sizes = [(c + 8 * g, 2 * int(rng.integers(1, 4500))) for g in range(3) for c in (0, 1, 4, 7)]
+        shift, passes = 3, 2
+    elif case == "five_bits":
+        sizes = [(c, 2 * int(rng.integers(1, 2000))) for c in range(32) if rng.random() < 0.8]
+        sizes[len(sizes) // 2] = (sizes[len(sizes) // 2][0], 30000)
+        shift, passes = 5, 3
+    else:
+        sizes = [(c, 6000) for c in range(4)] + [(c, 3000) for c in range(4, 16)]
+        spread, shift, passes = 300, 4, 2
+    rec = _nested_contexts(rng, sizes, 6, spread)
+    p = dict(num_regions=6, num_classes=3, region_class=np.array([0, 1, 2, 1, 0, 9], np.uint8),
+             group_shift=shift, num_groups=1 << (12 - shift) if shift < 12 else 1)
+    log(f"[gpu] merge four-way: {case} n={len(rec)}")
+    g = gpu_run(rec, p, with_plan=True)
+    assert g["_plan"]["ev_merge"] == 1
+    if passes is not None:
+        assert g["_plan"]["merge_rounds"] == passes
     assert_parity(g, oracle_run(oracle_mod, rec, p))
 
 

@@ -266,12 +266,15 @@ def test_unmutated_oracle_passes_all_pins(oracle_mod):
 def _build_mutant(mutant_dir, name, target, old, new):
     src = open(target).read()
     assert src.count(old) == 1, f"mutation site for {name} not unique"
-    path = os.path.join(str(mutant_dir), f"{name}.cpp")
+    # one file per (source, mutant): names repeat across sources, and a second
+    # dlopen of a path already loaded returns the first library
+    tag = f"{os.path.splitext(os.path.basename(target))[0]}_{name}"
+    path = os.path.join(str(mutant_dir), f"{tag}.cpp")
     with open(path, "w") as f:
         f.write(src.replace(old, new))
     others = [x for x in SOURCES if x != target]
     inc = os.path.join(ROOT, "oracle")
-    lib = os.path.join(str(mutant_dir), f"lib{name}.so")
+    lib = os.path.join(str(mutant_dir), f"lib{tag}.so")
     subprocess.check_call(["g++", "-O1", "-std=c++17", "-ffp-contract=off", "-shared", "-fPIC",
                            "-I", inc, path, *others, "-o", lib])
     return lib
