@@ -56,7 +56,7 @@ struct Layout {
   size_t chunk_runs, run_base, run_cnt, run_pos, run_hist, scan_bsum;
   size_t pop_ts, pop_reg, pushes, op_parent, op_sum;
   size_t inst, child_sum, hist_key, agg_part, ov_mask, ov_q;
-  size_t push_pos, pop_pos, ctx_list, ctx_seg, seg_run, seg_tile0, seg_samp0, part;
+  size_t push_pos, pop_pos, ctx_list, seg_run, seg_tile0, seg_samp0, part;
   size_t total;
   uint64_t lb_words, tree_leaves, match_tiles, pool_cap, ctx_cap, tiles_cap, chunks, run_cap;
 };
@@ -121,14 +121,13 @@ Layout make_layout(const argus_attr_config& c, uint64_t n, bool own_instances) {
   const bool ev = c.num_classes > 0;
   L.ctx_cap = ev ? (nn < kCtxCap ? nn : kCtxCap) : 0;
   // a segment of L events takes at most ceil(L / 4096) tiles in a two-way
-  // pass and (L / 256 + 4) / 12 + 1 in a four-way one
+  // pass and (L / 127 + 4) / 28 + 1 in a four-way one
   L.tiles_cap = ev ? ceil_div(nn, kSampStride * kSampPerTile) + L.ctx_cap + ceil_div(L.ctx_cap, 2) : 0;
   L.push_pos = take(ev ? sizeof(uint32_t) * L.pool_cap : 0);
   L.pop_pos = take(ev ? sizeof(uint32_t) * L.pool_cap : 0);
   L.ctx_list = take(sizeof(uint2) * L.ctx_cap);
   // segment arrays of every merge pass, ctx_cap + 1 entries per pass
   const uint64_t segs = ev ? kMaxMergePasses * (L.ctx_cap + 1) : 0;
-  L.ctx_seg = take(sizeof(uint32_t) * segs);
   L.seg_run = take(sizeof(uint4) * segs);
   L.seg_tile0 = take(sizeof(uint32_t) * segs);
   L.seg_samp0 = take(sizeof(uint32_t) * segs);
@@ -333,7 +332,6 @@ int enqueue_run(argus_attr* h, const argus_record* d_records, uint64_t n, char* 
   w.push_pos = (uint32_t*)(base + L.push_pos);
   w.pop_pos = (uint32_t*)(base + L.pop_pos);
   w.ctx_list = (uint2*)(base + L.ctx_list);
-  w.ctx_seg = (uint32_t*)(base + L.ctx_seg);
   w.seg_run = (uint4*)(base + L.seg_run);
   w.seg_tile0 = (uint32_t*)(base + L.seg_tile0);
   w.seg_samp0 = (uint32_t*)(base + L.seg_samp0);

@@ -38,12 +38,12 @@ constexpr int kMergeItems = 8;
 constexpr int kMergeTile = kMergeThreads * kMergeItems;  // 4096 events
 constexpr int kMaxMergeRounds = 8;   // context bits merged (two per pass at most)
 constexpr int kMaxMergePasses = 4;   // merge passes: pairs of bits, then a single one
-// Four-way passes cut each segment at every 12th of its samples in merged
-// order, a sample being every 255th event of a run: a tile then holds at
-// most (12 + 4) * 255 - 4 events, which leaves room for the second pair of
+// Four-way passes cut each segment at every 28th of its samples in merged
+// order, a sample being every 127th event of a run: a tile then holds at
+// most (28 + 4) * 127 - 4 events, which leaves room for the second pair of
 // runs to start at a multiple of 8 in LDS.
-constexpr uint32_t kSampStride = 255;
-constexpr uint32_t kSampPerTile = 12;
+constexpr uint32_t kSampStride = 127;
+constexpr uint32_t kSampPerTile = 28;
 static_assert((kSampPerTile + 4) * kSampStride - 4 + 7 <= (uint32_t)kMergeTile, "four-way tile bound");
 constexpr uint32_t kNoBit = 0xFFFFFFFFu;  // second bit of a two-way pass
 // Bit of a round that merges nothing: every group holds one context, so the
@@ -251,7 +251,6 @@ struct Work {
   uint32_t* push_pos;   // sorted position of each pushed BEGIN (pool layout)
   uint32_t* pop_pos;    // sorted position of each popping END (pool layout)
   uint2* ctx_list;      // [ctx_cap] (context key, first sorted position)
-  uint32_t* ctx_seg;    // [passes][ctx_cap + 1] segment of each context
   uint4* seg_run;       // [passes][ctx_cap + 1] starts of the segment's four runs
   uint32_t* seg_tile0;  // [passes][ctx_cap + 1] first merge tile of each segment
   uint32_t* seg_samp0;  // [passes][ctx_cap + 1] first sample of each segment (four-way)

@@ -25,8 +25,8 @@
 // tile's input slices in LDS (two stages for four runs: the pairs, then
 // their results).  A two-way pass splits at every 4096th output (Green,
 // McColl and Bader's merge path: a binary search on the cross diagonal); a
-// four-way pass ranks every 255th event of each run among the others and
-// cuts at every 12th of them in merged order.  The last pass does not store
+// four-way pass ranks every 127th event of each run among the others and
+// cuts at every 28th of them in merged order.  The last pass does not store
 // what it merges: k_merge_sweep sweeps each merged tile at once (its
 // segments are exactly the groups).
 #include "sweep_common.h"
@@ -152,7 +152,6 @@ __device__ __forceinline__ uint32_t block_incl_scan1024(uint32_t v, uint32_t* s_
 struct MSegArgs {
   DevPlan* plan;
   const uint2* ctx_list;
-  uint32_t* ctx_seg;
   uint4* seg_run;
   uint32_t* seg_tile0;
   uint32_t* seg_samp0;
@@ -172,14 +171,14 @@ __device__ __forceinline__ uint32_t run_samples(uint32_t len) {
 // one segment come in class order: two of them first differ in one of the
 // pass's bits, or in a bit an earlier pass merged (then they share a class
 // and a run already).  So a segment is four runs in a row (two in a two-way
-// pass), run q starting at the first context of class >= q.  The segments
-// depend on the context list only, so all passes are planned at once.
+// pass), run q starting at the first context of class >= q (at the segment's
+// end when there is none).  The segments depend on the context list only,
+// so all passes are planned at once.
 __global__ __launch_bounds__(1024) void k_mseg(MSegArgs a) {
   DevPlan* p = a.plan;
   const int round = blockIdx.x;
   if (!p->ev_merge || (uint32_t)round >= p->m_rounds) return;
   const uint64_t off = (uint64_t)round * a.stride;
-  uint32_t* ctx_seg = a.ctx_seg + off;
   uint4* seg_run = a.seg_run + off;
   uint32_t* seg_tile0 = a.seg_tile0 + off;
   uint32_t* seg_samp0 = a.seg_samp0 + off;
@@ -202,10 +201,14 @@ __global__ __launch_bounds__(1024) void k_mseg(MSegArgs a) {
     return four ? ((((c >> mr.bit2) & 1u) << 1) | lo) : lo;
   };
 
-  // ---- segment heads: four consecutive contexts per thread, 4096 per block step
+  // ---- segments and run starts: four consecutive contexts per thread, 4096
+  // per block step.  A context starts the runs of the classes after the one
+  // before it in its segment, up to its own; the last context of a segment
+  // starts the runs after its class at the segment's end.
   uint32_t carry = 0;
   for (uint32_t base = 0; base < nc; base += 4096) {
     const uint32_t j0 = base + 4 * t;
+    uint32_t prev = j0 > 0 && j0 - 1 < nc ? a.ctx_list[j0 - 1].x : 0u;
     bool head[4];
     uint2 e[4];
     uint32_t nh = 0;
@@ -216,9 +219,18 @@ __global__ __launch_bounds__(1024) void k_mseg(MSegArgs a) {
       e[q] = make_uint2(0, 0);
       if (j < nc) {
         e[q] = a.ctx_list[j];
-        head[q] = j == 0 || hi_of(a.ctx_list[j - 1].x) != hi_of(e[q].x);
+        head[q] = j == 0 || hi_of(prev) != hi_of(e[q].x);
+        prev = e[q].x;
       }
       nh += head[q] ? 1u : 0u;
+    }
+    // the context after the thread's last one: does it start a segment, where
+    uint32_t nx_start = end;
+    bool nx_head = true;
+    if (j0 + 4 < nc) {
+      const uint2 f = a.ctx_list[j0 + 4];
+      nx_start = f.y;
+      nx_head = hi_of(f.x) != hi_of(e[3].x);
     }
     uint32_t total;
     uint32_t seg = carry + block_incl_scan1024(nh, s_w, &total) - nh;  // heads before j0
@@ -226,35 +238,27 @@ __global__ __launch_bounds__(1024) void k_mseg(MSegArgs a) {
     for (int q = 0; q < 4; ++q) {
       const uint32_t j = j0 + q;
       if (j >= nc) continue;
-      if (head[q]) {
-        seg_run[seg] = make_uint4(e[q].y, kNoSplit, kNoSplit, kNoSplit);
-        ++seg;
+      if (head[q]) ++seg;
+      uint32_t* r = reinterpret_cast<uint32_t*>(&seg_run[seg - 1]);
+      const uint32_t c = cls_of(e[q].x);
+      const uint32_t pc = head[q] ? 0u : cls_of(q > 0 ? e[q - 1].x : a.ctx_list[j - 1].x);
+      if (head[q]) r[0] = e[q].y;
+      if (pc > c) flag_internal_error(a.counters, 256);
+      for (uint32_t x = pc + 1; x <= c && x < 4; ++x) r[x] = e[q].y;
+      // last context of its segment
+      const bool tail = q < 3 ? (j + 1 >= nc || head[q + 1]) : nx_head;
+      if (tail) {
+        const uint32_t s1 = q < 3 ? (j + 1 < nc ? e[q + 1].y : end) : nx_start;
+        for (uint32_t x = c + 1; x < 4; ++x) r[x] = s1;
       }
-      ctx_seg[j] = seg - 1;
     }
     carry += total;
   }
   const uint32_t n_segs = carry;
   __threadfence_block();
   __syncthreads();
-  // ---- run starts: runs q of (class before, class] start at a context
-  for (uint32_t j = t; j < nc && !by_group; j += 1024) {
-    const uint2 e = a.ctx_list[j];
-    const uint32_t c = cls_of(e.x);
-    if (c == 0) continue;
-    uint32_t pc = 0;  // class of the context before it in the segment (0 at a head)
-    if (j > 0) {
-      const uint32_t c0 = a.ctx_list[j - 1].x;
-      if (hi_of(c0) == hi_of(e.x)) pc = cls_of(c0);
-    }
-    if (pc > c) flag_internal_error(a.counters, 256);
-    uint32_t* r = reinterpret_cast<uint32_t*>(&seg_run[ctx_seg[j]]);
-    for (uint32_t q = pc + 1; q <= c && q < 4; ++q) r[q] = e.y;
-  }
-  __threadfence_block();
-  __syncthreads();
-  // ---- empty runs start where the next one does; tiles and samples per
-  // segment, and their prefixes (four segments per thread)
+  // ---- tiles and samples per segment, and their prefixes (four segments per
+  // thread)
   carry = 0;
   uint32_t carry_s = 0;
   for (uint32_t base = 0; base < n_segs; base += 4096) {
@@ -266,22 +270,14 @@ __global__ __launch_bounds__(1024) void k_mseg(MSegArgs a) {
       tiles[q] = 0;
       samp[q] = 0;
       if (sg < n_segs) {
-        uint32_t* r = reinterpret_cast<uint32_t*>(&seg_run[sg]);
-        const uint32_t s0 = r[0];
-        const uint32_t s1 = sg + 1 < n_segs ? reinterpret_cast<const uint32_t*>(&seg_run[sg + 1])[0] : end;
-        uint32_t st3 = r[3], st2 = r[2], st1 = r[1];
-        st3 = st3 == kNoSplit ? s1 : st3;
-        st2 = st2 == kNoSplit ? st3 : st2;
-        st1 = st1 == kNoSplit ? st2 : st1;
-        r[1] = st1;
-        r[2] = st2;
-        r[3] = st3;
+        const uint4 r = seg_run[sg];
+        const uint32_t s1 = sg + 1 < n_segs ? seg_run[sg + 1].x : end;
         if (four) {
-          samp[q] = run_samples(st1 - s0) + run_samples(st2 - st1) + run_samples(st3 - st2) +
-                    run_samples(s1 - st3);
+          samp[q] = run_samples(r.y - r.x) + run_samples(r.z - r.y) + run_samples(r.w - r.z) +
+                    run_samples(s1 - r.w);
           tiles[q] = (samp[q] + kSampPerTile - 1) / kSampPerTile;
         } else {
-          tiles[q] = (uint32_t)ceil_div(s1 - s0, kMergeTile);
+          tiles[q] = (uint32_t)ceil_div(s1 - r.x, kMergeTile);
         }
       }
       nt += tiles[q];
@@ -312,7 +308,7 @@ __global__ __launch_bounds__(1024) void k_mseg(MSegArgs a) {
 }
 
 hipError_t launch_mseg(const RunArgs& a, int rounds, hipStream_t s) {
-  MSegArgs m{a.w.plan, a.w.ctx_list, a.w.ctx_seg, a.w.seg_run, a.w.seg_tile0, a.w.seg_samp0,
+  MSegArgs m{a.w.plan, a.w.ctx_list, a.w.seg_run, a.w.seg_tile0, a.w.seg_samp0,
              a.out.d_counters, a.w.ctx_cap + 1, a.shift};
   hipLaunchKernelGGL(k_mseg, dim3((uint32_t)(rounds > 0 ? rounds : 1)), dim3(1024), 0, s, m);
   return hipGetLastError();
@@ -389,34 +385,54 @@ struct MPartArgs {
   uint64_t stride;
 };
 
-// Events of run R (length L) that come before the event of key `key` in
-// merged order: those of key <= key when R is an earlier run (le), else
-// those of key < key.  Counted over R's samples only (the samples before
-// it), then exactly, knowing the sample count `cnt`: the answer lies in
-// ((cnt - 1) * stride, cnt * stride].
+// Whether event e comes before an event of key `key` in merged order: e's
+// key is <= key when e is from an earlier run (le), else < key.
 __device__ __forceinline__ bool before(uint64_t e, uint64_t key, bool le) {
   return le ? mkey(e) <= key : mkey(e) < key;
 }
-__device__ __forceinline__ uint32_t samples_before(const uint64_t* R, uint32_t ns, uint64_t key,
-                                                   bool le) {
-  uint32_t lo = 0, hi = ns;
-  while (lo < hi) {
-    const uint32_t mid = (lo + hi) >> 1;
-    if (before(R[(uint64_t)mid * kSampStride], key, le)) lo = mid + 1;
-    else hi = mid;
+
+// For each run x, the first index in [lo[x], hi[x]) whose event, at st[x] +
+// index * SCALE, does not come before `key`, left in lo[x].  search4_seq
+// runs the four searches one after the other, each only as long as its own
+// range (the sample ranks: many lanes, often short ranges); search4 runs
+// them in lockstep, their loads in flight together, a finished search
+// loading `safe` (a valid address) instead (the exact ranks of the few
+// samples that start a tile).
+template <uint32_t SCALE>
+__device__ __forceinline__ void search4_seq(const uint64_t* src, const uint32_t (&st)[5], uint32_t q,
+                                            uint64_t key, uint32_t (&lo)[4], const uint32_t (&hi)[4]) {
+#pragma unroll
+  for (int x = 0; x < 4; ++x) {
+    uint32_t l = lo[x], h = hi[x];
+    while (l < h) {
+      const uint32_t mid = (l + h) >> 1;
+      if (before(src[st[x] + mid * SCALE], key, (uint32_t)x < q)) l = mid + 1;
+      else h = mid;
+    }
+    lo[x] = l;
   }
-  return lo;
 }
-__device__ __forceinline__ uint32_t events_before(const uint64_t* R, uint32_t L, uint32_t cnt,
-                                                  uint64_t key, bool le) {
-  if (cnt == 0) return 0;
-  uint32_t lo = (cnt - 1) * kSampStride + 1, hi = cnt * kSampStride < L ? cnt * kSampStride : L;
-  while (lo < hi) {
-    const uint32_t mid = (lo + hi) >> 1;
-    if (before(R[mid], key, le)) lo = mid + 1;
-    else hi = mid;
+
+template <uint32_t SCALE>
+__device__ __forceinline__ void search4(const uint64_t* src, const uint32_t (&st)[5], uint32_t q,
+                                        uint64_t key, uint32_t safe, uint32_t (&lo)[4],
+                                        uint32_t (&hi)[4]) {
+  while (lo[0] < hi[0] || lo[1] < hi[1] || lo[2] < hi[2] || lo[3] < hi[3]) {
+    uint32_t mid[4];
+    uint64_t v[4];
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      mid[x] = (lo[x] + hi[x]) >> 1;
+      v[x] = src[lo[x] < hi[x] ? st[x] + mid[x] * SCALE : safe];
+    }
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      if (lo[x] < hi[x]) {
+        if (before(v[x], key, (uint32_t)x < q)) lo[x] = mid[x] + 1;
+        else hi[x] = mid[x];
+      }
+    }
   }
-  return lo;
 }
 
 // Two-way pass: one thread per tile; the tile's start is the merge-path
@@ -508,25 +524,42 @@ __global__ __launch_bounds__(256) void k_mpart(MPartArgs a) {
     }
     const uint32_t k = rem * kSampStride;
     const uint64_t key = mkey(src[sq + k]);
-    uint32_t cnt[4], rho = rem;
+    // samples of each other run before it
+    uint32_t sl[4], sh[4], rho = rem;
 #pragma unroll
     for (int x = 0; x < 4; ++x) {
-      cnt[x] = 0;
-      if ((uint32_t)x != q && ns[x]) cnt[x] = samples_before(src + st[x], ns[x], key, (uint32_t)x < q);
-      rho += cnt[x];
+      sl[x] = 0;
+      sh[x] = (uint32_t)x == q ? 0u : ns[x];
     }
+    search4_seq<kSampStride>(src, st, q, key, sl, sh);
+#pragma unroll
+    for (int x = 0; x < 4; ++x) rho += sl[x];
     if (rho % kSampPerTile) continue;
     const uint32_t j = rho / kSampPerTile;
     if (j >= tiles || tile0 + (uint64_t)j >= n_tiles) {
       flag_internal_error(a.counters, 256);
       continue;
     }
+    // events of each other run before it: with c samples before it, between
+    // (c - 1) * stride + 1 and c * stride (or the run's end)
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      const uint32_t c = sl[x];
+      if ((uint32_t)x == q) {
+        sl[x] = sh[x] = k;
+      } else if (c == 0) {
+        sh[x] = 0;
+      } else {
+        sl[x] = (c - 1) * kSampStride + 1;
+        sh[x] = c * kSampStride < len[x] ? c * kSampStride : len[x];
+      }
+    }
+    search4<1>(src, st, q, key, sq + k, sl, sh);
     uint32_t pos[4], out = st[0];
 #pragma unroll
     for (int x = 0; x < 4; ++x) {
-      const uint32_t r = (uint32_t)x == q ? k : events_before(src + st[x], len[x], cnt[x], key, (uint32_t)x < q);
-      pos[x] = st[x] + r;
-      out += r;
+      pos[x] = st[x] + sl[x];
+      out += sl[x];
     }
     const uint32_t ends[4] = {st[1], st[2], st[3], st[4]};
     store_task(a.task + tile0 + j, pos, out, j == 0, ends);
