@@ -236,6 +236,12 @@ __global__ __launch_bounds__(kMatchThreads, 3) void k_match(MatchArgs a) {
 
   for (;;) {
   issue(tile);
+  // thread indices opaque per tile: lane-condition masks derived from them
+  // are then computed where used, not held in scalar registers (spilled)
+  // across the tile loop
+  uint32_t tid = threadIdx.x;
+  asm volatile("" : "+v"(tid));
+  const uint32_t lane = tid & 63, w = tid >> 6;
   const uint64_t base = tile * kMatchTile;
   const uint32_t cnt = nv - base < (uint64_t)kMatchTile ? (uint32_t)(nv - base) : (uint32_t)kMatchTile;
   const uint64_t next = tile + gridDim.x;
@@ -281,6 +287,9 @@ __global__ __launch_bounds__(kMatchThreads, 3) void k_match(MatchArgs a) {
       }
     }
   }
+  // the record flags opaque: later tests of them are not tied back to the
+  // compares that made them (whose masks would stay live across the tile)
+  asm volatile("" : "+v"(fv), "+v"(fb));
   // context of the record before this thread's first one: the previous
   // lane's last record, or (lane 0) a load of the record before
   uint32_t prev0 = lane_prev(CTX(IT - 1), 0u);
@@ -312,6 +321,7 @@ __global__ __launch_bounds__(kMatchThreads, 3) void k_match(MatchArgs a) {
       nb += isb;
     }
   }
+  asm volatile("" : "+v"(fh));
   if (nheads) {
     atomicMin(&s_first, first_head);
     atomicMax(&s_lastp1, last_p1);
@@ -649,7 +659,7 @@ __global__ __launch_bounds__(kMatchThreads, 3) void k_match(MatchArgs a) {
     } else {
 #pragma unroll
       for (int i = 0; i < IT; ++i)
-        if (p0 + i < cnt) evo[base + p0 + i] = e[i];
+        if ((fv >> i) & 1u) evo[base + p0 + i] = e[i];
     }
   }
 
