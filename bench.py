@@ -101,13 +101,15 @@ def byte_model(name: str, c: dict, plan: dict, R: int, K: int, G: int, flags: in
         # sorted keys (+ context words) in; instances and one event word per record out
         return (12.0 + (4.0 if wide else 0.0) + (8.0 if ev_words else 0.0)) * nv + 40.0 * nb
     if name.startswith("merge") and name[5:].isdigit():
-        # rounds before the last: read and write one word per event
+        # passes before the last: read and write one word per event
         return 16.0 * plan["merge_end"] if int(name[5:]) + 1 < plan["merge_rounds"] and plan["ev_merge"] else 0.0
     if name == "merge_sweep":
-        # last round: reads one word per event, merges and sweeps without storing
+        # last pass: reads one word per event, merges and sweeps without storing
         return 8.0 * plan["merge_end"] if plan["ev_merge"] else 0.0
     if name == "agg":
-        return 40.0 * nb + (8.0 * nb if flags & 2 else 0.0) + (4.0 * nb if R > 167 else 0.0)
+        # instances and their exclusive times in (the caller's exclusive output
+        # already holds them), histogram keys out when they do not fit in LDS
+        return 40.0 * nb + (4.0 * nb if R > 167 else 0.0)
     if name == "hist":
         # the histogram keys are read from HBM once; the region slices of one
         # key range re-read them from the L2 of the XCD that holds them
@@ -470,7 +472,7 @@ def main() -> int:
                      "achieved_gbs": round(total_bytes / (step_ms * 1e-3) / 1e9, 1),
                      "frac_of_peak": round(total_bytes / (step_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                      "full_sort": bool(plan["unsorted"]),
-                     "events": f"merged in {plan['merge_rounds']} rounds" if plan["ev_merge"] else "radix sort"},
+                     "events": f"merged in {plan['merge_rounds']} passes" if plan["ev_merge"] else "radix sort"},
         "roofline": roofline,
         # per launch; the dominant kernel's from the timed steps, the others
         # from the instrumented steps before them

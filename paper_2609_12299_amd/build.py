@@ -75,7 +75,7 @@ def resources() -> str:
     import tempfile
     rows = []
     keys = ("VGPRs", "AGPRs", "TotalSGPRs", "ScratchSize [bytes/lane]", "Occupancy [waves/SIMD]",
-            "LDS Size [bytes/block]", "VGPRs Spill")
+            "LDS Size [bytes/block]", "VGPRs Spill", "SGPRs Spill")
     with tempfile.TemporaryDirectory() as tmp:
         for src in SOURCES:
             cmd = [hipcc(), *flags(), *FILE_FLAGS.get(src, []), "--offload-device-only", "-c",
@@ -101,11 +101,13 @@ def resources() -> str:
         out = subprocess.run([filt], input="\n".join(names), capture_output=True, text=True).stdout
         for r, d in zip(rows, out.splitlines()):
             r["kernel"] = d.split("(")[0]
-    head = f"{'kernel':48s} {'file':14s} VGPR AGPR SGPR spill scratch waves/SIMD   LDS B"
+    head = (f"{'kernel':48s} {'file':14s} VGPR AGPR SGPR spill sspill scratch waves/SIMD   LDS B"
+            "\n(spill: VGPRs spilled to scratch; sspill: SGPRs spilled to VGPR lanes)")
     lines = [head]
     for r in rows:
         lines.append(f"{r['kernel'][:48]:48s} {r['file']:14s} {r.get('VGPRs', 0):4d} "
                      f"{r.get('AGPRs', 0):4d} {r.get('TotalSGPRs', 0):4d} {r.get('VGPRs Spill', 0):5d} "
+                     f"{r.get('SGPRs Spill', 0):6d} "
                      f"{r.get('ScratchSize [bytes/lane]', 0):7d} "
                      f"{r.get('Occupancy [waves/SIMD]', 0):10d} "
                      f"{r.get('LDS Size [bytes/block]', 0):7d}")

@@ -55,7 +55,7 @@ struct Layout {
   size_t key[2], pay[2], ctxw[2], lb[2], tsum, carry, bsum, slb, mslb, tiles, tree;
   size_t chunk_runs, run_base, run_cnt, run_pos, run_hist, scan_bsum;
   size_t pop_ts, pop_reg, pushes, op_parent, op_sum;
-  size_t inst, child_sum, hist_key, agg_part, ov_mask, ov_q;
+  size_t inst, excl, hist_key, agg_part, ov_mask, ov_q;
   size_t push_pos, pop_pos, ctx_list, seg_run, seg_tile0, seg_samp0, part;
   size_t total;
   uint64_t lb_words, tree_leaves, match_tiles, pool_cap, ctx_cap, tiles_cap, chunks, run_cap;
@@ -111,7 +111,7 @@ Layout make_layout(const argus_attr_config& c, uint64_t n, bool own_instances) {
   L.op_parent = take(sizeof(uint32_t) * L.pool_cap);
   L.op_sum = take(sizeof(uint64_t) * L.pool_cap);
   L.inst = own_instances ? take(sizeof(argus_instance) * nn) : 0;
-  L.child_sum = take(sizeof(uint64_t) * nn);
+  L.excl = take(sizeof(uint64_t) * nn);
   L.hist_key = take(sizeof(uint32_t) * nn);
   L.agg_part = take(sizeof(uint64_t) * agg_part_words(n, c.num_regions));
   const uint64_t G = c.num_classes ? c.num_groups : 0;
@@ -324,7 +324,10 @@ int enqueue_run(argus_attr* h, const argus_record* d_records, uint64_t n, char* 
   w.op_parent = (uint32_t*)(base + L.op_parent);
   w.op_sum = (uint64_t*)(base + L.op_sum);
   w.inst = own_inst ? (argus_instance*)(base + L.inst) : out->d_instances;
-  w.child_sum = (uint64_t*)(base + L.child_sum);
+  // exclusive times are accumulated in place, in the caller's output when
+  // it asks for them
+  w.excl = (h->cfg.flags & ARGUS_OUT_INSTANCE_EXCL) ? out->d_instance_excl
+                                                   : (uint64_t*)(base + L.excl);
   w.hist_key = (uint32_t*)(base + L.hist_key);
   w.agg_part = agg_part_words(n, h->cfg.num_regions) ? (uint64_t*)(base + L.agg_part) : nullptr;
   w.ov_mask = (uint64_t*)(base + L.ov_mask);

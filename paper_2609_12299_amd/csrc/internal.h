@@ -243,7 +243,8 @@ struct Work {
   uint32_t* op_parent;
   uint64_t* op_sum;
   argus_instance* inst;
-  uint64_t* child_sum;  // [n_begin]
+  uint64_t* excl;       // [n_begin] exclusive times, accumulated in place (the caller's
+                        // output when it asks for them)
   uint32_t* hist_key;   // [n_begin]
   uint64_t* agg_part;   // per-block region statistics of k_agg (NULL: flushed atomically)
   uint64_t* ov_mask;    // [G][256]

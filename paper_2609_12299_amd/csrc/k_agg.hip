@@ -35,10 +35,10 @@ __device__ __forceinline__ uint32_t agg_parent(const argus_instance& x, const Ti
 struct AggArgs {
   const DevPlan* plan;
   argus_instance* inst;
-  const uint64_t* child_sum;
+  const uint64_t* excl;  // exclusive times (closed instances), accumulated in place
   const TileDesc* tiles;
   const uint32_t* op_parent;
-  uint64_t* excl_out;  // NULL unless requested
+  uint64_t* excl_out;  // NULL unless requested; then the same buffer as excl
   uint32_t* hist_key;  // NULL when histograms are done here
   uint64_t* part;      // [block][kAggFields][R], or NULL: flush with atomics
   uint64_t* counters;
@@ -150,7 +150,7 @@ __global__ __launch_bounds__(512, 4) void k_agg(AggArgs a) {
       const uint64_t id = wb + (uint64_t)j * 64 + lane;
       const uint64_t ic = id < nb ? id : nb - 1;
       xs[j] = a.inst[ic];
-      cs[j] = a.child_sum[ic];
+      cs[j] = a.excl[ic];
     }
 #pragma unroll
     for (int j = 0; j < B; ++j) {
@@ -177,8 +177,9 @@ __global__ __launch_bounds__(512, 4) void k_agg(AggArgs a) {
     const bool closed = ereg != kNoEnd;
     const bool matched = closed && ereg == region;
     const uint64_t incl = closed ? x.t_end - x.t_begin : 0;
-    const uint64_t excl = closed ? incl - cs[j] : 0;
-    if (a.excl_out) a.excl_out[id] = excl;
+    const uint64_t excl = closed ? cs[j] : 0;
+    // the output holds the closed instances' exclusive times already
+    if (a.excl_out && !closed) a.excl_out[id] = 0;
     uint32_t hk = 0xFFFFFFFFu;
     if (matched) {
       n_m++;
@@ -409,7 +410,7 @@ hipError_t launch_agg(const RunArgs& a, hipStream_t s) {
   AggArgs g{};
   g.plan = a.w.plan;
   g.inst = a.w.inst;
-  g.child_sum = a.w.child_sum;
+  g.excl = a.w.excl;
   g.tiles = a.w.tiles;
   g.op_parent = a.w.op_parent;
   g.excl_out = (a.flags & ARGUS_OUT_INSTANCE_EXCL) ? a.out.d_instance_excl : nullptr;

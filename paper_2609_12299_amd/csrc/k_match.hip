@@ -21,8 +21,11 @@
 // parents opened in an earlier tile -- is summarised per tile and resolved
 // by k_resolve.
 //
-// Exclusive time needs the sum of the inclusive durations of each instance's
-// closed children; children closed inside the tile are summed in LDS.
+// Exclusive time is its inclusive duration less those of its closed
+// children, accumulated in place (mod 2^64): a closed instance adds its
+// duration to its own slot and takes it off its parent's.  Instances of the
+// tile accumulate in LDS; what goes to instances open when the tile starts
+// is kept per enclosing level for k_resolve.
 #include "internal.h"
 
 namespace argus {
@@ -96,7 +99,7 @@ struct MatchArgs {
   const uint32_t* pay[2];
   const uint32_t* ctxw[2];
   argus_instance* inst;
-  uint64_t* child_sum;
+  uint64_t* excl;
   TileDesc* tiles;
   const TileCarry* carry;
   uint64_t* pop_ts;
@@ -117,8 +120,8 @@ struct MatchArgs {
 
 constexpr uint32_t kParNone = 0xFFFFFFFFu;
 constexpr uint32_t kParOut = 0xFFFFFFFEu;
-// Child sums of enclosing instances (open when the tile starts) are kept in
-// LDS for the nearest kOcCap levels; deeper ones go to global memory.
+// What the tile takes off enclosing instances (open when it starts) is kept
+// in LDS for the nearest kOcCap levels; deeper ones go to global memory.
 constexpr uint32_t kOcCap = 512;
 constexpr uint32_t kQueueCap = kMatchTile / 4;  // queued searches per wave
 
@@ -132,17 +135,15 @@ __global__ __launch_bounds__(kMatchThreads, 3) void k_match(MatchArgs a) {
   constexpr int IT = kMatchItems;
 
   __shared__ __align__(16) uint2 s_leaf[kMatchTile / 8 * kLeafStride];  // tree leaves
-  // child sums of local BEGINs; zero between tiles (cleared as they are
-  // written out)
   __shared__ uint32_t s_up[kUpSize];  // upper tree levels
-  // child sums of local BEGINs share the leaves' LDS: the tree is dead once
-  // the searches are answered
+  // exclusive times of the local BEGINs share the leaves' LDS: the tree is
+  // dead once the searches are answered
   uint64_t* const s_cs = reinterpret_cast<uint64_t*>(s_leaf);
   // search queues (one per wave) during the searches; then the end time of
   // each local BEGIN closed in the tile
   __shared__ uint64_t s_tend[kMatchTile];
   __shared__ uint16_t s_ereg[kMatchTile];  // end region of each local BEGIN (0xFFFF: open)
-  __shared__ uint64_t s_oc[kOcCap];        // child sums of enclosing instances (zero between tiles)
+  __shared__ uint64_t s_oc[kOcCap];        // taken off enclosing instances (zero between tiles)
   __shared__ Fn s_wfn[4];
   __shared__ uint32_t s_wnb[4];
   __shared__ uint32_t s_first, s_lastp1, s_heads, s_lo, s_sout, s_maxlvl, s_orph;
@@ -573,13 +574,13 @@ __global__ __launch_bounds__(kMatchThreads, 3) void k_match(MatchArgs a) {
       par[i] = found ? qrank : kParOut;
     }
   }
-  // child sums of enclosing instances beyond the LDS ones start at zero
+  // sums for enclosing instances beyond the LDS ones start at zero
   const uint32_t n_op = (sin_eff > op_lo) ? ((sin_eff - op_lo) < (uint32_t)kMatchTile ? sin_eff - op_lo : (uint32_t)kMatchTile) : 0u;
   for (uint32_t k = kOcCap + tid; k < n_op; k += kMatchThreads) a.op_sum[pool + k] = 0;
   if (n_op > kOcCap) __threadfence_block();
   __syncthreads();  // end times and end regions of the local BEGINs are complete
 
-  // ---- child sums, open BEGINs and the instances
+  // ---- exclusive times, open BEGINs and the instances
   uint32_t mbeg = 0;  // bit i: BEGIN matched to an END of the same region
   {
     uint32_t r = tnb;
@@ -595,18 +596,21 @@ __global__ __launch_bounds__(kMatchThreads, 3) void k_match(MatchArgs a) {
         const uint64_t t_end = s_tend[k];
         if (ereg == reg[i]) mbeg |= 1u << i;
         const uint64_t incl = t_end - TS(i);
+        // its own duration in, its duration out of its parent's
+        atomicAdd((unsigned long long*)&s_cs[k], (unsigned long long)incl);
+        const unsigned long long out = (unsigned long long)(0ull - incl);
         if (par[i] == kParOut) {
           const uint32_t oi = (L - 1) - op_lo;
           if (L >= 1 + op_lo && oi < (uint32_t)kMatchTile) {
             if (oi < kOcCap)
-              atomicAdd((unsigned long long*)&s_oc[oi], (unsigned long long)incl);
+              atomicAdd((unsigned long long*)&s_oc[oi], out);
             else
-              atomicAdd((unsigned long long*)&a.op_sum[pool + oi], (unsigned long long)incl);
+              atomicAdd((unsigned long long*)&a.op_sum[pool + oi], out);
           } else {
             flag_internal_error(a.counters, 16);
           }
         } else if (par[i] != kParNone) {
-          atomicAdd((unsigned long long*)&s_cs[par[i]], (unsigned long long)incl);
+          atomicAdd((unsigned long long*)&s_cs[par[i]], out);
         }
       } else if (lastp1 <= p + 1) {
         // still open when the tile ends, in a context that may continue
@@ -630,9 +634,9 @@ __global__ __launch_bounds__(kMatchThreads, 3) void k_match(MatchArgs a) {
       dst[1] = w1;
     }
   }
-  __syncthreads();  // child sums complete
+  __syncthreads();  // exclusive times of the tile complete
   for (uint32_t k = tid; k < tile_nb; k += kMatchThreads) {
-    a.child_sum[nbpre + k] = s_cs[k];
+    a.excl[nbpre + k] = s_cs[k];
   }
   const uint32_t n_oc = n_op < kOcCap ? n_op : kOcCap;
   for (uint32_t k = tid; k < n_oc; k += kMatchThreads) {
@@ -724,7 +728,7 @@ hipError_t launch_match(const RunArgs& a, hipStream_t s) {
     m.ctxw[b] = a.w.ctxw[b];
   }
   m.inst = a.w.inst;
-  m.child_sum = a.w.child_sum;
+  m.excl = a.w.excl;
   m.tiles = a.w.tiles;
   m.carry = a.w.carry;
   m.pop_ts = a.w.pop_ts;

@@ -4,7 +4,8 @@
 //   * pops: ENDs that close levels [lo_head, s_in) open when t started;
 //   * pushes: BEGINs at levels [lo_tail, s_out) still open when t ends;
 //   * references to enclosing instances at levels [op_lo, s_in) (parents of
-//     BEGINs opened in t, and the durations of their children closed in t).
+//     BEGINs opened in t, and what their children closed in t take off their
+//     exclusive time).
 // With key(t) = -1 if t holds a context start, else the lowest depth seen in
 // t, the END closing a push at level L of tile t is the pop at level L of the
 // first later tile with key <= L (if that tile continues the context and
@@ -123,7 +124,7 @@ struct ResolveArgs {
   uint32_t* op_parent;
   const uint64_t* op_sum;
   argus_instance* inst;
-  uint64_t* child_sum;
+  uint64_t* excl;  // exclusive time of each instance, accumulated in place
   uint64_t* counters;
   // overlap events of pairs matched across tiles (merge path)
   uint64_t* ev[2];
@@ -195,11 +196,13 @@ __global__ __launch_bounds__(256) void k_resolve(ResolveArgs a) {
         }
       }
     }
+    // exclusive times in place: its duration in, and out of its parent's
+    atomicAdd((unsigned long long*)&a.excl[id], (unsigned long long)incl);
     uint32_t pf = x->parent;
     if (pf == kNoParent) continue;
     if (pf & kParentPending) pf = L >= 1 ? enclosing(a, t, L - 1) : kNoParent;
     if (pf == kNoParent || pf >= nb) continue;
-    atomicAdd((unsigned long long*)&a.child_sum[pf], (unsigned long long)incl);
+    atomicAdd((unsigned long long*)&a.excl[pf], (unsigned long long)(0ull - incl));
   }
   // Instances open when tile t starts that tile t refers to.
   for (uint32_t i = lane; i < d.n_op; i += kResolveLanes) {
@@ -207,13 +210,13 @@ __global__ __launch_bounds__(256) void k_resolve(ResolveArgs a) {
     const uint32_t pid = enclosing(a, t, L);
     a.op_parent[pool + i] = pid;
     const uint64_t sum = a.op_sum[pool + i];
-    if (sum && pid < nb) atomicAdd((unsigned long long*)&a.child_sum[pid], (unsigned long long)sum);
+    if (sum && pid < nb) atomicAdd((unsigned long long*)&a.excl[pid], (unsigned long long)sum);
   }
 }
 
 hipError_t launch_resolve(const RunArgs& a, hipStream_t s) {
   ResolveArgs r{a.w.plan, a.w.tiles, a.w.tree, a.w.tree_leaves, a.w.pop_ts, a.w.pop_reg,
-                a.w.pushes, a.w.op_parent, a.w.op_sum, a.w.inst, a.w.child_sum,
+                a.w.pushes, a.w.op_parent, a.w.op_sum, a.w.inst, a.w.excl,
                 a.out.d_counters};
   for (int b = 0; b < 2; ++b) r.ev[b] = a.w.key[b];
   r.push_pos = a.w.push_pos;
