@@ -437,7 +437,7 @@ int enqueue_run(argus_attr* h, const argus_record* d_records, uint64_t n, char* 
     // run by itself).
     static const char* mnames[kMaxMergePasses][2] = {
         {"mpart0", "merge0"}, {"mpart1", "merge1"}, {"mpart2", "merge2"}, {"mpart3", "merge3"}};
-    const int bits = a.shift < (uint32_t)kMaxMergeRounds ? (int)a.shift : kMaxMergeRounds;
+    const int bits = a.shift < (uint32_t)kMaxMergeBits ? (int)a.shift : kMaxMergeBits;
     int rounds = (bits + 1) / 2;
     if (rounds < 1) rounds = 1;
     if (!step("mseg", [&] { return launch_mseg(a, rounds, s); })) return ARGUS_E_HIP;

@@ -36,7 +36,7 @@ constexpr int kSweepSlots = 8;  // groups of one tile aggregated in LDS
 constexpr int kMergeThreads = 512;
 constexpr int kMergeItems = 8;
 constexpr int kMergeTile = kMergeThreads * kMergeItems;  // 4096 events
-constexpr int kMaxMergeRounds = 8;   // context bits merged (two per pass at most)
+constexpr int kMaxMergeBits = 8;   // context bits merged (two per pass at most)
 constexpr int kMaxMergePasses = 4;   // merge passes: pairs of bits, then a single one
 // Four-way passes cut each segment at every 28th of its samples in merged
 // order, a sample being every 127th event of a run: a tile then holds at
@@ -139,7 +139,7 @@ struct DevPlan {
   uint32_t m_rounds;   // merge passes (set bits of m_need, taken in pairs)
   uint32_t m_nctx;     // contexts of groups < G (a prefix of the context list)
   uint64_t m_end;      // sorted position where groups >= G start (or n_valid)
-  MergeRound mr[kMaxMergeRounds];
+  MergeRound mr[kMaxMergeBits];  // one per pass (at most kMaxMergePasses; the size keeps the layout)
   // context sort over runs of one context in the input
   uint32_t runs;       // 1: records are sorted as runs (else radix passes over records)
   uint32_t pad1;

@@ -43,7 +43,7 @@ struct MPlanArgs {
   const uint64_t* counters;
   uint32_t K, G, shift;
   uint32_t force_radix;
-  uint32_t max_rounds;
+  uint32_t max_bits;
   uint64_t ctx_cap;
 };
 
@@ -67,7 +67,7 @@ __global__ __launch_bounds__(64) void k_mplan(MPlanArgs a) {
   // its look-back traffic: merging wins up to about twice as many bits (and
   // more, two bits sharing a pass).
   const uint32_t radix_passes = (g_bits + ks.ts_bits + 7) / 8;
-  if (bits > a.max_rounds || bits > 2 * radix_passes) return;
+  if (bits > a.max_bits || bits > 2 * radix_passes) return;
   // contexts of groups < G form a prefix of the (sorted) context list
   uint64_t lo = 0, hi = n_ctx;
   while (lo < hi) {
@@ -117,7 +117,7 @@ __global__ __launch_bounds__(64) void k_mplan(MPlanArgs a) {
 hipError_t launch_mplan(const RunArgs& a, hipStream_t s) {
   MPlanArgs m{a.w.plan, a.w.ctx_list, a.out.d_counters, a.K, a.G, a.shift,
               (a.flags & ARGUS_FORCE_EVENT_SORT) ? 1u : 0u,
-              a.shift < (uint32_t)kMaxMergeRounds ? a.shift : (uint32_t)kMaxMergeRounds,
+              a.shift < (uint32_t)kMaxMergeBits ? a.shift : (uint32_t)kMaxMergeBits,
               a.w.ctx_cap};
   hipLaunchKernelGGL(k_mplan, dim3(1), dim3(64), 0, s, m);
   return hipGetLastError();
