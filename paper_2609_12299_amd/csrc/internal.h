@@ -570,6 +570,11 @@ hipError_t launch_agg(const RunArgs& a, hipStream_t s);
 // Words of the per-block statistics buffer of k_agg for n records (0: none).
 uint64_t agg_part_words(uint64_t n, uint32_t R);
 hipError_t launch_hist(const RunArgs& a, hipStream_t s);
+// Log2 histograms of instances from their keys (region << 16 | incl bin << 8
+// | excl bin, 0xFFFFFFFF: none), *d_count of them (at most count_max), added
+// into the region rows (k_agg.hip).
+hipError_t launch_hist_keys(const uint32_t* keys, const uint64_t* d_count, uint64_t count_max,
+                            uint64_t* rstats, uint32_t R, hipStream_t s);
 hipError_t launch_ev_plan(const RunArgs& a, hipStream_t s);
 hipError_t launch_ev_clear(const RunArgs& a, hipStream_t s);
 hipError_t launch_mplan(const RunArgs& a, hipStream_t s);

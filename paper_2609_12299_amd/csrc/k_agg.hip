@@ -442,7 +442,8 @@ hipError_t launch_agg(const RunArgs& a, hipStream_t s) {
 // ------------------------------------------------------------ histograms
 
 struct HistArgs {
-  const DevPlan* plan;
+  const uint64_t* count;  // keys (device), at most count_max
+  uint64_t count_max;
   const uint32_t* hist_key;
   uint64_t* rstats;
   uint32_t R;
@@ -468,7 +469,7 @@ __global__ __launch_bounds__(1024) void k_hist(HistArgs a) {
   const uint32_t nr = r1 - r0;
   for (uint32_t i = threadIdx.x; i < nr * 130; i += NT) s_h[i] = 0;
   __syncthreads();
-  const uint64_t nb = a.plan->n_begin;
+  const uint64_t nb = *a.count < a.count_max ? *a.count : a.count_max;
   auto add = [&](uint32_t k) {
     const uint32_t r = k >> 16;
     if (k == 0xFFFFFFFFu || r < r0 || r >= r1) return;
@@ -512,22 +513,27 @@ __global__ __launch_bounds__(1024) void k_hist(HistArgs a) {
   }
 }
 
+hipError_t launch_hist_keys(const uint32_t* keys, const uint64_t* d_count, uint64_t count_max,
+                            uint64_t* rstats, uint32_t R, hipStream_t s) {
+  // as few slices as fit, of equal size
+  const uint32_t slices = (uint32_t)ceil_div((uint64_t)R * kHistBytes, kHistLdsBytes);
+  const uint32_t slice = (uint32_t)ceil_div(R, slices);
+  uint64_t ranges = ceil_div(count_max ? count_max : 1, 1024 * 64);
+  if (ranges > 256) ranges = 256;
+  ranges = ceil_div(ranges, 8) * 8;
+  HistArgs h{d_count, count_max, keys, rstats, R, slice, slices, (uint32_t)ranges};
+  const size_t hb = (size_t)slice * kHistBytes;
+  (void)hipFuncSetAttribute((const void*)k_hist, hipFuncAttributeMaxDynamicSharedMemorySize, (int)hb);
+  hipLaunchKernelGGL(k_hist, dim3((uint32_t)(ranges * slices)), dim3(1024), hb, s, h);
+  return hipGetLastError();
+}
+
 hipError_t launch_hist(const RunArgs& a, hipStream_t s) {
   uint32_t rl, hl;
   size_t bytes;
   agg_sizes(a.R, &rl, &hl, &bytes);
   if (hl) return hipSuccess;
-  // as few slices as fit, of equal size
-  const uint32_t slices = (uint32_t)ceil_div((uint64_t)a.R * kHistBytes, kHistLdsBytes);
-  const uint32_t slice = (uint32_t)ceil_div(a.R, slices);
-  uint64_t ranges = ceil_div(a.n ? a.n : 1, 1024 * 64);
-  if (ranges > 256) ranges = 256;
-  ranges = ceil_div(ranges, 8) * 8;
-  HistArgs h{a.w.plan, a.w.hist_key, a.out.d_region_stats, a.R, slice, slices, (uint32_t)ranges};
-  const size_t hb = (size_t)slice * kHistBytes;
-  (void)hipFuncSetAttribute((const void*)k_hist, hipFuncAttributeMaxDynamicSharedMemorySize, (int)hb);
-  hipLaunchKernelGGL(k_hist, dim3((uint32_t)(ranges * slices)), dim3(1024), hb, s, h);
-  return hipGetLastError();
+  return launch_hist_keys(a.w.hist_key, &a.w.plan->n_begin, a.n, a.out.d_region_stats, a.R, s);
 }
 
 // ------------------------------------------------------- overlap events

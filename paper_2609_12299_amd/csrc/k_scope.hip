@@ -31,6 +31,13 @@ constexpr int kScThreads = 256;
 constexpr int kScRounds = 16;
 constexpr uint32_t kScTile = kScThreads * kScRounds;  // 4096 elements
 constexpr uint32_t kScScanBlock = 4096;                // entries per scan block
+// Ordinals reach their instances in two steps: (index, ordinal) pairs are
+// gathered per bucket of 2^18 consecutive instance indices, then each bucket
+// is written by blocks of one XCD, whose L2 holds the bucket's 1 MiB of
+// output while they write it.
+constexpr uint32_t kOrdBucketBits = 18;
+constexpr uint32_t kOrdMaxBuckets = 1u << (31 - kOrdBucketBits);  // instances < 2^31
+constexpr uint32_t kOrdSlices = 128;                              // blocks per bucket
 
 // A stable LSD radix sort over 8-bit digits of 16-byte elements (two u64
 // words, ping-pong buffers).  The first pass may read the instance array
@@ -153,60 +160,100 @@ __global__ __launch_bounds__(kScThreads) void k_scan_apply(uint32_t* data, uint6
   }
 }
 
-// Stable scatter of one tile: in each round of 256 elements, each wave finds
-// the lanes that share its digit with eight ballots; per-wave digit counts
-// in LDS give the wave's offset within the round, and a running count per
-// digit carries the tile's earlier rounds.
+// Stable scatter of one tile.  Each wave takes 1024 consecutive elements
+// (16 rounds of 64 lanes, all loaded up front) and ranks each among the
+// wave's earlier elements of its digit: eight ballots find the lanes that
+// share it, and per-wave digit counters in LDS carry the earlier rounds
+// (wave barriers only).  One block barrier later the waves' counts give
+// each digit's offset per wave and the tile-local digit starts; the tile is
+// staged in LDS in digit order and written out so that a run of equal
+// digits goes to consecutive addresses.
+constexpr size_t kScStageBytes = 2 * sizeof(uint64_t) * kScTile;  // dynamic LDS of k_sort_scatter
 template <int SRC>
 __global__ __launch_bounds__(kScThreads) void k_sort_scatter(SortBufs s, int in, int out, int word,
                                                              int shift) {
-  __shared__ uint32_t s_wcnt[4][256];
-  __shared__ uint32_t s_run[256];
+  extern __shared__ __align__(16) uint8_t sc_stage[];
+  uint64_t* s_ta = reinterpret_cast<uint64_t*>(sc_stage);
+  uint64_t* s_tb = s_ta + kScTile;
+  __shared__ uint32_t s_wave[4][256];  // per-wave digit counts, then each wave's offset in the digit
   __shared__ uint32_t s_base[256];
+  __shared__ uint32_t s_lstart[256];
+  __shared__ uint32_t s_w[kScThreads / 64];
+  __shared__ uint32_t s_carry;
   const uint64_t n = sb_count(s);
   const uint64_t tile = blockIdx.x;
-  const uint32_t tid = threadIdx.x, w = tid >> 6;
-  s_run[tid] = 0;
-  s_base[tid] = s.hist[(uint64_t)tid * s.tiles_max + tile];
-  const uint64_t lt = lanemask_lt();
-  uint64_t* da = s.a[out];
-  uint64_t* db = s.b[out];
-  for (uint32_t j = 0; j < kScRounds; ++j) {
-    const uint64_t e = tile * kScTile + (uint64_t)j * kScThreads + tid;
-    const bool valid = e < n;
-    uint64_t a = 0, b = 0;
-    if (valid) sb_load<SRC>(s, in, e, &a, &b);
-    const uint32_t d = (uint32_t)(((word ? b : a) >> shift) & 0xFFu);
+  const uint32_t tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) s_wcnt[q][tid] = 0;
-    __syncthreads();
+  for (int q = 0; q < 4; ++q) s_wave[q][tid] = 0;
+  s_base[tid] = s.hist[(uint64_t)tid * s.tiles_max + tile];
+  if (tid == 0) s_carry = 0;
+  uint64_t av[kScRounds], bv[kScRounds];
+  uint32_t dg[kScRounds], rk[kScRounds];
+  const uint64_t e0 = tile * kScTile + (uint64_t)w * (kScRounds * 64) + lane;
+#pragma unroll
+  for (int r = 0; r < kScRounds; ++r) {
+    const uint64_t e = e0 + (uint64_t)r * 64;
+    av[r] = 0;
+    bv[r] = 0;
+    if (e < n) sb_load<SRC>(s, in, e, &av[r], &bv[r]);
+  }
+  __syncthreads();  // counters cleared
+  const uint64_t lt = lanemask_lt();
+#pragma unroll
+  for (int r = 0; r < kScRounds; ++r) {
+    const bool valid = e0 + (uint64_t)r * 64 < n;
+    const uint32_t d = (uint32_t)(((word ? bv[r] : av[r]) >> shift) & 0xFFu);
     uint64_t peers = __ballot(valid);
 #pragma unroll
     for (int bit = 0; bit < 8; ++bit) {
       const uint64_t bal = __ballot((d >> bit) & 1u);
       peers &= ((d >> bit) & 1u) ? bal : ~bal;
     }
-    const uint32_t rank = (uint32_t)__popcll(peers & lt);
-    if (valid && rank == 0) s_wcnt[w][d] = (uint32_t)__popcll(peers);
-    __syncthreads();
-    {
-      // thread tid owns digit tid: wave offsets within the round, in place
-      uint32_t run = s_run[tid];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const uint32_t c = s_wcnt[q][tid];
-        s_wcnt[q][tid] = run;
-        run += c;
-      }
-      s_run[tid] = run;
-    }
-    __syncthreads();
+    uint32_t rank = 0;
     if (valid) {
-      const uint64_t dst = (uint64_t)s_base[d] + s_wcnt[w][d] + rank;
+      const uint32_t old = s_wave[w][d];
+      rank = old + (uint32_t)__popcll(peers & lt);
+      __builtin_amdgcn_wave_barrier();
+      if ((peers >> lane) == 1ull) s_wave[w][d] = old + (uint32_t)__popcll(peers);
+    }
+    __builtin_amdgcn_wave_barrier();
+    dg[r] = valid ? d : 256u;
+    rk[r] = rank;
+  }
+  __syncthreads();
+  // thread tid owns digit tid: the waves' offsets within it, the tile's count
+  // of it, and (scanned) where it starts in the staged tile
+  uint32_t cnt = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t c = s_wave[q][tid];
+    s_wave[q][tid] = cnt;
+    cnt += c;
+  }
+  s_lstart[tid] = block_excl_scan<kScThreads>(cnt, s_w, &s_carry);
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < kScRounds; ++r) {
+    const uint32_t d = dg[r];
+    if (d >= 256u) continue;
+    const uint32_t slot = s_lstart[d] + s_wave[w][d] + rk[r];
+    if (slot < kScTile) {
+      s_ta[slot] = av[r];
+      s_tb[slot] = bv[r];
+    }
+  }
+  __syncthreads();
+  const uint32_t total = s_carry;  // the tile's elements
+  uint64_t* da = s.a[out];
+  uint64_t* db = s.b[out];
+  for (uint32_t i = tid; i < total && i < kScTile; i += kScThreads) {
+    const uint64_t a = s_ta[i], b = s_tb[i];
+    const uint32_t d = (uint32_t)(((word ? b : a) >> shift) & 0xFFu);
+    const uint64_t dst = (uint64_t)s_base[d] + (i - s_lstart[d]);
+    if (dst < n) {
       da[dst] = a;
       db[dst] = b;
     }
-    __syncthreads();
   }
 }
 
@@ -235,7 +282,10 @@ struct ScopeArgs {
   uint32_t* ordinal;
   uint64_t* stats;
   uint64_t* counters;
-  SortBufs s;  // count = the instances
+  SortBufs s;         // count = the instances
+  uint32_t* octr;     // [kOrdMaxBuckets] pairs gathered per bucket so far
+  uint64_t* pairs;    // [count] ordinal << 32 | index, by bucket (a free sort buffer)
+  uint32_t* hkey;     // [count] histogram key of each instance (a free sort buffer)
 };
 
 // Fill kernel for the outputs that are accumulated.
@@ -247,52 +297,141 @@ __global__ __launch_bounds__(kScThreads) void k_sc_init(ScopeArgs a) {
     a.stats[i] = (col == ARGUS_RS_INCL_MIN || col == ARGUS_RS_EXCL_MIN) ? kU64Max : 0ull;
   }
   if (blockIdx.x == 0 && threadIdx.x < ARGUS_SC_NUM_COUNTERS) a.counters[threadIdx.x] = 0;
+  for (uint64_t i = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; i < kOrdMaxBuckets;
+       i += (uint64_t)gridDim.x * kScThreads)
+    a.octr[i] = 0;
+}
+
+// Start of the (key, ctx) run that holds sorted element e, by one wave:
+// lane k probes e - 2^k (one round trip brackets the start), then 64 probes
+// per step narrow the bracket.
+__device__ __forceinline__ uint64_t run_start_wave(const uint64_t* ka, const uint64_t* kb, uint64_t e,
+                                                   uint64_t key, uint32_t ctx) {
+  const uint32_t lane = threadIdx.x & 63;
+  auto same = [&](uint64_t p) { return ka[p] == key && (uint32_t)(kb[p] >> 32) == ctx; };
+  // p = e - 2^lane; "outside" when p < 0 or its element is of another run
+  const bool in = lane < 63 && (1ull << lane) <= e && same(e - (1ull << lane));
+  const uint64_t out = __ballot(!in);
+  const uint32_t j = (uint32_t)__ffsll((unsigned long long)out) - 1;  // first lane outside
+  if (j == 0) return e;  // e - 1 is outside: e starts its run
+  // the start lies in (e - 2^j, e - 2^(j-1)]: the first position whose element is in the run
+  uint64_t lo = (1ull << j) <= e ? e - (1ull << j) + 1 : 0;  // lo .. hi may hold the start
+  uint64_t hi = e - (1ull << (j - 1));
+  while (lo < hi) {
+    const uint64_t span = hi - lo;
+    const uint64_t p = lo + span * lane / 64;
+    const bool ok = same(p);
+    // the smallest probe inside the run bounds the start from above; the
+    // largest probe outside from below
+    const uint64_t ins = __ballot(ok);
+    const uint64_t outs = __ballot(!ok);
+    if (ins) {
+      const uint32_t f = (uint32_t)__ffsll((unsigned long long)ins) - 1;
+      const uint64_t pf = lo + span * f / 64;
+      uint64_t nlo = lo;
+      if (outs & ((1ull << f) - 1ull)) {
+        const uint32_t g = 63u - (uint32_t)__clzll(outs & ((1ull << f) - 1ull));
+        nlo = lo + span * g / 64 + 1;
+      }
+      lo = nlo;
+      hi = pf;
+    } else {
+      lo = lo + span * 63 / 64 + 1;
+    }
+  }
+  return lo;
 }
 
 // Ordinal of each sorted element: its distance from the start of its
-// (region, context) run, scattered to canonical order.
+// (region, context) run.  A block takes 4096 sorted elements (16 rounds of
+// 64 per wave, chunk c = 4 * round + wave).  The start of a run that began
+// before an element's chunk is the last head of the chunks before it, or
+// (before the tile's first head) the start of the run holding the tile's
+// first element.  The (index, ordinal) pairs go to the buckets of their
+// indices, each block reserving its share of a bucket once.
 __global__ __launch_bounds__(kScThreads) void k_sc_ordinal(ScopeArgs a, int buf) {
+  __shared__ uint32_t s_cnt[kOrdMaxBuckets];  // per bucket: count, then global base
+  __shared__ int64_t s_last[4 * kScRounds];   // last head in each chunk, then the run start entering it
+  __shared__ uint64_t s_tstart;
   const uint64_t n = sb_count(a.s);
   const uint64_t* ka = a.s.a[buf];
   const uint64_t* kb = a.s.b[buf];
-  const uint32_t lane = threadIdx.x & 63;
+  const uint32_t tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const uint32_t nbk = (uint32_t)((n + (1ull << kOrdBucketBits) - 1) >> kOrdBucketBits);
   uint32_t best = 0;
-  const uint64_t nwaves = (uint64_t)gridDim.x * (kScThreads / 64);
-  for (uint64_t wv = ((uint64_t)blockIdx.x * kScThreads + threadIdx.x) >> 6;
-       wv * 64 < n; wv += nwaves) {
-    const uint64_t e0 = wv * 64, e = e0 + lane;
-    const bool valid = e < n;
-    uint64_t key = 0;
-    uint32_t ctx = 0, idx = 0;
-    bool head = false;
-    if (valid) {
-      key = ka[e];
-      const uint64_t vv = kb[e];
-      ctx = (uint32_t)(vv >> 32);
-      idx = (uint32_t)vv;
-      head = e == 0 || ka[e - 1] != key || (uint32_t)(kb[e - 1] >> 32) != ctx;
+  for (uint64_t tile = blockIdx.x; tile * kScTile < n; tile += gridDim.x) {
+    const uint64_t t0 = tile * kScTile;
+    for (uint32_t b = tid; b < nbk; b += kScThreads) s_cnt[b] = 0;
+    if (w == 0) {
+      const uint64_t st = run_start_wave(ka, kb, t0, ka[t0], (uint32_t)(kb[t0] >> 32));
+      if (lane == 0) s_tstart = st;
     }
-    // start of the run: the last head at or before this lane, else the run
-    // that was open when the wave began (one binary search for the wave)
-    int64_t h = head ? (int64_t)e : -1;
+    // heads, and the last head at or before each lane within its chunk
+    int64_t h[kScRounds];
+    uint32_t idx[kScRounds];
 #pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-      const int64_t o = __shfl_up(h, d);
-      if (lane >= (uint32_t)d && o > h) h = o;
+    for (int r = 0; r < kScRounds; ++r) {
+      const uint64_t e = t0 + (uint64_t)r * kScThreads + (uint64_t)w * 64 + lane;
+      const bool valid = e < n;
+      bool head = false;
+      idx[r] = 0xFFFFFFFFu;
+      if (valid) {
+        const uint64_t key = ka[e];
+        const uint64_t vv = kb[e];
+        idx[r] = (uint32_t)vv;
+        head = e == 0 || ka[e - 1] != key || (uint32_t)(kb[e - 1] >> 32) != (uint32_t)(vv >> 32);
+      }
+      int64_t x = head ? (int64_t)e : -1;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const int64_t o = __shfl_up(x, d);
+        if (lane >= (uint32_t)d && o > x) x = o;
+      }
+      h[r] = x;
+      if (lane == 63) s_last[4 * r + w] = x;
     }
-    if (__ballot(valid && h < 0)) {
-      const uint64_t k0 = __shfl(key, 0);
-      const uint32_t c0 = __shfl(ctx, 0);
-      uint64_t s0 = 0;
-      if (lane == 0) s0 = sb_lower(ka, kb, e0, k0, c0);
-      s0 = __shfl(s0, 0);
-      if (h < 0) h = (int64_t)s0;
+    __syncthreads();
+    if (tid == 0) {
+      int64_t run = (int64_t)s_tstart;
+      for (uint32_t c = 0; c < 4 * kScRounds; ++c) {
+        const int64_t l = s_last[c];
+        s_last[c] = run;  // the run start entering chunk c
+        if (l >= 0) run = l;
+      }
     }
-    if (valid) {
-      const uint32_t ord = (uint32_t)(e - (uint64_t)h);
-      a.ordinal[idx] = ord;
-      best = best > ord + 1 ? best : ord + 1;
+    __syncthreads();
+    uint64_t pr[kScRounds];
+    uint32_t bk[kScRounds], slot[kScRounds];
+#pragma unroll
+    for (int r = 0; r < kScRounds; ++r) {
+      const uint64_t e = t0 + (uint64_t)r * kScThreads + (uint64_t)w * 64 + lane;
+      bk[r] = 0xFFFFFFFFu;
+      if (e >= n) continue;
+      const int64_t hs = h[r] >= 0 ? h[r] : s_last[4 * r + w];
+      if (idx[r] < n && hs >= 0 && (uint64_t)hs <= e) {
+        const uint32_t ord = (uint32_t)(e - (uint64_t)hs);
+        best = best > ord + 1 ? best : ord + 1;
+        bk[r] = idx[r] >> kOrdBucketBits;
+        slot[r] = atomicAdd(&s_cnt[bk[r]], 1u);
+        pr[r] = ((uint64_t)ord << 32) | idx[r];
+      } else {
+        flag_internal_error(a.counters, 1);
+      }
     }
+    __syncthreads();
+    for (uint32_t b = tid; b < nbk; b += kScThreads) {
+      const uint32_t c = s_cnt[b];
+      if (c) s_cnt[b] = atomicAdd(&a.octr[b], c);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < kScRounds; ++r) {
+      if (bk[r] == 0xFFFFFFFFu) continue;
+      const uint64_t at = ((uint64_t)bk[r] << kOrdBucketBits) + s_cnt[bk[r]] + slot[r];
+      if (at < n) a.pairs[at] = pr[r];
+      else flag_internal_error(a.counters, 1);
+    }
+    __syncthreads();
   }
   // wave maximum, one atomic per wave
 #pragma unroll
@@ -304,14 +443,35 @@ __global__ __launch_bounds__(kScThreads) void k_sc_ordinal(ScopeArgs a, int buf)
     atomicMax((unsigned long long*)&a.counters[ARGUS_SC_N_ITERATIONS], (unsigned long long)best);
 }
 
+// Each bucket's pairs written to their instances: block k serves XCD k % 8
+// (blocks are dispatched to XCDs round-robin), buckets b with b % 8 == k % 8,
+// one of kOrdSlices slices of the bucket each.
+__global__ __launch_bounds__(kScThreads) void k_sc_ord_place(ScopeArgs a) {
+  const uint64_t n = sb_count(a.s);
+  const uint32_t k = blockIdx.x, x = k % 8, j = k / 8;
+  const uint64_t b = x + 8ull * (j / kOrdSlices);
+  const uint32_t sl = j % kOrdSlices;
+  const uint64_t b0 = b << kOrdBucketBits;
+  if (b0 >= n) return;
+  const uint64_t size = n - b0 < (1ull << kOrdBucketBits) ? n - b0 : (1ull << kOrdBucketBits);
+  const uint64_t lo = b0 + size * sl / kOrdSlices, hi = b0 + size * (sl + 1) / kOrdSlices;
+  for (uint64_t i = lo + threadIdx.x; i < hi; i += kScThreads) {
+    const uint64_t pr = a.pairs[i];
+    const uint32_t idx = (uint32_t)pr;
+    if (idx >= b0 && idx < b0 + size) a.ordinal[idx] = (uint32_t)(pr >> 32);
+    else flag_internal_error(a.counters, 1);
+  }
+}
+
 __device__ __forceinline__ bool in_range32(uint64_t v, uint32_t lo, uint32_t hi) {
   return lo <= v && v <= hi;
 }
 
 // Scoped statistics in canonical order.  With LDS_ROWS, each block keeps
 // the twelve scalar columns of every region in LDS (LDS atomics), and adds
-// them to the output once at the end; the histograms always go straight to
-// the output with global atomics.  Without, every column does.
+// them to the output once at the end; without, every column goes straight
+// to the output with global atomics.  The histograms are counted afterwards
+// from one key per instance (k_hist over slices of regions).
 constexpr uint32_t kScLdsRegions = 1024;  // 12 x 8 B x 1024 = 96 KiB of LDS
 constexpr int kScStatThreads = 1024;
 constexpr int kScCols = 12;               // ARGUS_RS_COUNT .. ARGUS_RS_SELF_NESTED
@@ -343,38 +503,38 @@ __global__ __launch_bounds__(kScStatThreads) void k_sc_stats(ScopeArgs a) {
                     in_range32(group, a.sc.group_lo, a.sc.group_hi) &&
                     in_range32(a.ordinal[x], a.sc.iter_lo, a.sc.iter_hi) && reg < a.R &&
                     (!a.region_mask || a.region_mask[reg] != 0);
-    if (!in) continue;
-    c_in += 1;
-    if (ereg == kNoEnd) {
-      c_u += 1;
-      atomicAdd(col_ptr(reg, ARGUS_RS_UNCLOSED), 1ull);
-      continue;
+    // the instance's histogram key (none unless matched and in scope)
+    uint32_t hk = 0xFFFFFFFFu;
+    if (in) {
+      c_in += 1;
+      if (ereg == kNoEnd) {
+        c_u += 1;
+        atomicAdd(col_ptr(reg, ARGUS_RS_UNCLOSED), 1ull);
+      } else if (ereg != reg) {
+        c_mm += 1;
+        atomicAdd(col_ptr(reg, ARGUS_RS_MISM_AS_BEGIN), 1ull);
+        if (ereg < a.R) atomicAdd(col_ptr(ereg, ARGUS_RS_MISM_AS_END), 1ull);
+      } else {
+        c_m += 1;
+        const uint64_t tb = (uint64_t)h0.x | ((uint64_t)h0.y << 32);
+        const uint64_t te = (uint64_t)h0.z | ((uint64_t)h0.w << 32);
+        const uint64_t d = te - tb, ex = a.excl[x];
+        atomicAdd(col_ptr(reg, ARGUS_RS_COUNT), 1ull);
+        atomicAdd(col_ptr(reg, ARGUS_RS_INCL_SUM), (unsigned long long)d);
+        atomicAdd(col_ptr(reg, ARGUS_RS_EXCL_SUM), (unsigned long long)ex);
+        atomicMin(col_ptr(reg, ARGUS_RS_INCL_MIN), (unsigned long long)d);
+        atomicMax(col_ptr(reg, ARGUS_RS_INCL_MAX), (unsigned long long)d);
+        atomicMin(col_ptr(reg, ARGUS_RS_EXCL_MIN), (unsigned long long)ex);
+        atomicMax(col_ptr(reg, ARGUS_RS_EXCL_MAX), (unsigned long long)ex);
+        hk = (reg << 16) | (bit_width64(d) << 8) | bit_width64(ex);
+        const uint32_t par = h1.y;
+        if (par != kNoParent && par < n && (inst[2 * (uint64_t)par + 1].w & 0xFFFFu) == reg) {
+          c_s += 1;
+          atomicAdd(col_ptr(reg, ARGUS_RS_SELF_NESTED), 1ull);
+        }
+      }
     }
-    if (ereg != reg) {
-      c_mm += 1;
-      atomicAdd(col_ptr(reg, ARGUS_RS_MISM_AS_BEGIN), 1ull);
-      if (ereg < a.R) atomicAdd(col_ptr(ereg, ARGUS_RS_MISM_AS_END), 1ull);
-      continue;
-    }
-    c_m += 1;
-    const uint64_t tb = (uint64_t)h0.x | ((uint64_t)h0.y << 32);
-    const uint64_t te = (uint64_t)h0.z | ((uint64_t)h0.w << 32);
-    const uint64_t d = te - tb, ex = a.excl[x];
-    atomicAdd(col_ptr(reg, ARGUS_RS_COUNT), 1ull);
-    atomicAdd(col_ptr(reg, ARGUS_RS_INCL_SUM), (unsigned long long)d);
-    atomicAdd(col_ptr(reg, ARGUS_RS_EXCL_SUM), (unsigned long long)ex);
-    atomicMin(col_ptr(reg, ARGUS_RS_INCL_MIN), (unsigned long long)d);
-    atomicMax(col_ptr(reg, ARGUS_RS_INCL_MAX), (unsigned long long)d);
-    atomicMin(col_ptr(reg, ARGUS_RS_EXCL_MIN), (unsigned long long)ex);
-    atomicMax(col_ptr(reg, ARGUS_RS_EXCL_MAX), (unsigned long long)ex);
-    unsigned long long* grow = (unsigned long long*)(a.stats + (uint64_t)reg * ARGUS_RS_WIDTH);
-    atomicAdd(&grow[ARGUS_RS_HIST_INCL + bit_width64(d)], 1ull);
-    atomicAdd(&grow[ARGUS_RS_HIST_EXCL + bit_width64(ex)], 1ull);
-    const uint32_t par = h1.y;
-    if (par != kNoParent && par < n && (inst[2 * (uint64_t)par + 1].w & 0xFFFFu) == reg) {
-      c_s += 1;
-      atomicAdd(col_ptr(reg, ARGUS_RS_SELF_NESTED), 1ull);
-    }
+    a.hkey[x] = hk;
   }
   if (LDS_ROWS) {
     __syncthreads();
@@ -705,7 +865,7 @@ SortLayout carve_sort(Carver& c, uint64_t m) {
 
 struct ScLayout {
   SortLayout ref;
-  size_t hist, bsum, total;
+  size_t hist, bsum, octr, total;
 };
 ScLayout sc_layout(uint64_t max_inst) {
   Carver c;
@@ -713,6 +873,7 @@ ScLayout sc_layout(uint64_t max_inst) {
   L.ref = carve_sort(c, max_inst);
   L.hist = c.take(sizeof(uint32_t) * 256 * tiles_for(max_inst));
   L.bsum = c.take(sizeof(uint32_t) * scan_blocks_for(256 * tiles_for(max_inst)));
+  L.octr = c.take(sizeof(uint32_t) * kOrdMaxBuckets);
   L.total = c.o;
   return L;
 }
@@ -771,11 +932,11 @@ void sort_pass(const SortBufs& s, bool from_inst, int in, int out, int word, int
                        shift);
   scan_u32(s.hist, 256ull * s.tiles_max, s.bsum, st);
   if (from_inst)
-    hipLaunchKernelGGL(k_sort_scatter<kSrcInst>, dim3(tiles), dim3(kScThreads), 0, st, s, in, out,
-                       word, shift);
+    hipLaunchKernelGGL(k_sort_scatter<kSrcInst>, dim3(tiles), dim3(kScThreads), kScStageBytes, st, s,
+                       in, out, word, shift);
   else
-    hipLaunchKernelGGL(k_sort_scatter<kSrcBuf>, dim3(tiles), dim3(kScThreads), 0, st, s, in, out,
-                       word, shift);
+    hipLaunchKernelGGL(k_sort_scatter<kSrcBuf>, dim3(tiles), dim3(kScThreads), kScStageBytes, st, s,
+                       in, out, word, shift);
 }
 
 // The instances sorted by (BEGIN region, context), canonical order kept
@@ -799,6 +960,11 @@ int sc_check_device() {
     hipDeviceProp_t prop;
     if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return ARGUS_E_HIP;
     if (strncmp(prop.gcnArchName, "gfx950", 6) != 0) return ARGUS_E_DEVICE;
+    // the sort scatter stages a whole tile (64 KiB of dynamic LDS)
+    for (const void* f : {(const void*)k_sort_scatter<kSrcInst>, (const void*)k_sort_scatter<kSrcBuf>})
+      if (hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kScStageBytes) !=
+          hipSuccess)
+        return ARGUS_E_HIP;
     g_sc_dev_ok[dev] = 1;
   }
   return ARGUS_OK;
@@ -851,12 +1017,20 @@ extern "C" int argus_attr_scope(const argus_scope_config* cfg, const argus_scope
   a.counters = io->d_counters;
   a.s = make_bufs(base, L.ref, L.hist, L.bsum, io->max_instances, io->d_n_instances,
                   io->d_instances);
+  a.octr = (uint32_t*)(base + L.octr);
   hipStream_t st = (hipStream_t)stream_v;
   hipLaunchKernelGGL(k_sc_init, dim3(sc_grid((uint64_t)a.R * ARGUS_RS_WIDTH, kScThreads, 1024)),
                      dim3(kScThreads), 0, st, a);
   const int buf = sort_reference(a.s, a.R, st);
-  hipLaunchKernelGGL(k_sc_ordinal, dim3(sc_grid(io->max_instances, kScThreads, 4096)),
+  a.pairs = a.s.a[buf ^ 1];  // free once the sort is done
+  hipLaunchKernelGGL(k_sc_ordinal, dim3(sc_grid(io->max_instances, kScTile, 2048)),
                      dim3(kScThreads), 0, st, a, buf);
+  {
+    const uint64_t nbk = (io->max_instances + (1ull << kOrdBucketBits) - 1) >> kOrdBucketBits;
+    const uint64_t blocks = 8ull * ((nbk + 7) / 8) * kOrdSlices;
+    hipLaunchKernelGGL(k_sc_ord_place, dim3((uint32_t)(blocks ? blocks : 1)), dim3(kScThreads), 0, st, a);
+  }
+  a.hkey = reinterpret_cast<uint32_t*>(a.s.b[buf ^ 1]);  // free once the sort is done
   if (a.R <= kScLdsRegions) {
     const size_t lds = (size_t)a.R * kScCols * sizeof(uint64_t);
     (void)hipFuncSetAttribute((const void*)k_sc_stats<true>,
@@ -871,6 +1045,9 @@ extern "C" int argus_attr_scope(const argus_scope_config* cfg, const argus_scope
     hipLaunchKernelGGL(k_sc_stats<false>, dim3(sc_grid(io->max_instances, kScStatThreads, 4096)),
                        dim3(kScStatThreads), 0, st, a);
   }
+  if (io->max_instances > 0 &&
+      launch_hist_keys(a.hkey, io->d_n_instances, io->max_instances, a.stats, a.R, st) != hipSuccess)
+    return ARGUS_E_HIP;
   return hipGetLastError() == hipSuccess ? ARGUS_OK : ARGUS_E_HIP;
 }
 
