@@ -246,7 +246,10 @@ def bench_part(args, d: dict, rec_np: np.ndarray, dev) -> dict:
             return scope_statistics(inst, out["instance_excl"], cnt, R, iter_lo=0, iter_hi=15)
         units, unit_name = nb, "instances"
         passes = 2 if R > 256 else 1
-        per_call = nb * (48.0 * passes + 20.0 + 44.0)
+        # sort passes; ordinals (sorted element in, pair out; pair in, ordinal
+        # out); statistics (instance, exclusive time, ordinal in, histogram key
+        # out); the histogram pass over the keys
+        per_call = nb * (48.0 * passes + 24.0 + 12.0 + 48.0 + 4.0)
         what = f"iterations 0..15 of every region, on the instances of the {WORKLOADS[args.config]}"
     elif part == "probes":
         pr_np = tracegen.probes_for([1, 2, 7], d["blocks"] * d["warps"], 16, 5, seed=9)
