@@ -195,45 +195,84 @@ __global__ __launch_bounds__(kSampThreads) void k_s_pc(SampArgs a) {
     atomicAdd((unsigned long long*)&a.counters[ARGUS_S_N_PAIRS], (unsigned long long)pairs);
 }
 
-// One wave per region: its total count, and each lifted metric as the
-// products alpha(r, p) * m(p), each rounded, added one at a time in
-// increasing p over the p that region r owns a share of.  The wave reads 64
-// PCs at a time, forms their products in parallel, and then adds the
-// non-zero ones in lane order (increasing p), so the additions happen in
-// exactly the sequential order while the zeros cost nothing.
-__device__ __forceinline__ double readlane_f64(double v, int lane) {
-  const uint64_t b = __double_as_longlong(v);
-  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)b, lane);
-  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), lane);
-  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+// Per region r: its total count (an integer sum, in any order), and each
+// lifted metric as the products alpha(r, p) * m(p), each rounded, added one
+// at a time in increasing p over the p where region r has a count.
+//
+// alpha(r, p) is zero exactly where the count is (a non-zero count over a
+// total below 2^64 is at least 2^-64), and a running sum that starts at +0
+// never becomes -0 under round-to-nearest, so adding +0 for a p without a
+// count leaves the sum unchanged bit for bit.  Each sum can therefore walk
+// all P terms in order, with no selection across lanes: one wave per region
+// and pair of metrics gathers kLiftChunk PCs of the region's column (alpha,
+// the two metrics and, for the first pair, the counts) one chunk ahead,
+// forms the chunk's products in parallel into LDS, and lane k then adds
+// metric k's products in order.  Chunks in which the region has no count are
+// skipped (they would add only +0).
+constexpr uint32_t kLiftMetrics = 2;
+constexpr int kLiftBlocks = 8;                    // 64-PC blocks per chunk
+constexpr uint32_t kLiftChunk = 64 * kLiftBlocks;
+constexpr uint32_t kLiftRow = kLiftChunk + 2;     // metric rows start on different banks
+
+struct LiftChunk {
+  uint64_t n[kLiftBlocks];
+  double al[kLiftBlocks], x0[kLiftBlocks], x1[kLiftBlocks];
+};
+
+__device__ __forceinline__ void lift_load(LiftChunk& c, const SampArgs& a, uint64_t r, uint64_t p0,
+                                          bool totals, const double* m0, const double* m1,
+                                          uint32_t lane) {
+#pragma unroll
+  for (int u = 0; u < kLiftBlocks; ++u) {
+    const uint64_t p = p0 + 64u * u + lane;
+    const bool in = p < a.P;
+    c.n[u] = in && totals ? a.n[p * a.R + r] : 0ull;
+    c.al[u] = in && m0 ? a.alpha[p * a.R + r] : 0.0;
+    c.x0[u] = in && m0 ? m0[p] : 0.0;
+    c.x1[u] = in && m1 ? m1[p] : 0.0;
+  }
 }
 
-__global__ __launch_bounds__(kSampThreads) void k_s_region(SampArgs a) {
-  const uint64_t r = ((uint64_t)blockIdx.x * kSampThreads + threadIdx.x) >> 6;
-  if (r >= a.R) return;  // whole waves leave together
-  const uint32_t lane = threadIdx.x & 63;
+__global__ __launch_bounds__(64) void k_s_region(SampArgs a) {
+  __shared__ double s_prod[kLiftMetrics][kLiftRow];
+  const uint64_t r = blockIdx.x;
+  const uint32_t lane = threadIdx.x;
+  const bool totals = blockIdx.y == 0;
+  const uint32_t k0 = blockIdx.y * kLiftMetrics;
+  const uint32_t mk = a.M > k0 ? (a.M - k0 < kLiftMetrics ? a.M - k0 : kLiftMetrics) : 0u;
+  const double* m0 = mk > 0 ? a.metrics + (uint64_t)k0 * a.P : nullptr;
+  const double* m1 = mk > 1 ? a.metrics + (uint64_t)(k0 + 1) * a.P : nullptr;
+  const double* row = s_prod[lane < kLiftMetrics ? lane : 0];
   uint64_t tot = 0;
-  for (uint64_t p0 = 0; p0 < a.P; p0 += 64) {
-    const uint64_t p = p0 + lane;
-    tot += p < a.P ? a.n[p * a.R + r] : 0ull;
-  }
-  tot = rows_sum64(row_sum64(tot));
-  if (lane == 0) a.region_total[r] = tot;
-  for (uint32_t k = 0; k < a.M; ++k) {
-    const double* m = a.metrics + (uint64_t)k * a.P;
-    double acc = 0.0;
-    for (uint64_t p0 = 0; p0 < a.P; p0 += 64) {
-      const uint64_t p = p0 + lane;
-      const uint64_t v = p < a.P ? a.n[p * a.R + r] : 0ull;
-      const double prod = v ? a.alpha[p * a.R + r] * m[p] : 0.0;
-      uint64_t nz = __ballot(v != 0);
-      while (nz) {
-        const int b = __builtin_ctzll(nz);
-        nz &= nz - 1;
-        acc = acc + readlane_f64(prod, b);
-      }
+  double acc = 0.0;
+  LiftChunk cur, nxt;
+  lift_load(cur, a, r, 0, totals, m0, m1, lane);
+  for (uint64_t p0 = 0; p0 < a.P; p0 += kLiftChunk) {
+    if (p0 + kLiftChunk < a.P) lift_load(nxt, a, r, p0 + kLiftChunk, totals, m0, m1, lane);
+    bool any = false;
+#pragma unroll
+    for (int u = 0; u < kLiftBlocks; ++u) {
+      tot += cur.n[u];
+      any |= cur.al[u] != 0.0;
     }
-    if (lane == 0) a.mhat[(uint64_t)k * a.R + r] = acc;
+    if (mk > 0 && __ballot(any)) {
+#pragma unroll
+      for (int u = 0; u < kLiftBlocks; ++u) {
+        const bool has = cur.al[u] != 0.0;
+        s_prod[0][64 * u + lane] = has ? cur.al[u] * cur.x0[u] : 0.0;
+        s_prod[1][64 * u + lane] = has ? cur.al[u] * cur.x1[u] : 0.0;
+      }
+      __syncthreads();
+#pragma unroll 32
+      for (uint32_t j = 0; j < kLiftChunk; ++j) acc = acc + row[j];
+      __syncthreads();
+    }
+    cur = nxt;
+  }
+  if (lane < mk) a.mhat[(uint64_t)(k0 + lane) * a.R + r] = acc;
+  if (totals) {
+    tot = rows_sum64(row_sum64(tot));
+    if (lane == 0) a.region_total[r] = tot;
   }
 }
 
@@ -318,7 +357,7 @@ extern "C" int argus_attr_samples(const argus_samples_config* cfg, const argus_s
                      a);
   hipLaunchKernelGGL(k_s_pc, dim3(grid_for(P, kSampThreads / 64, 4096)), dim3(kSampThreads), 0,
                      s, a);
-  hipLaunchKernelGGL(k_s_region, dim3(grid_for(R, kSampThreads / 64, 65536)), dim3(kSampThreads),
-                     0, s, a);
+  const uint32_t lift_y = M > 0 ? (uint32_t)((M + kLiftMetrics - 1) / kLiftMetrics) : 1u;
+  hipLaunchKernelGGL(k_s_region, dim3((uint32_t)R, lift_y), dim3(64), 0, s, a);
   return hipGetLastError() == hipSuccess ? ARGUS_OK : ARGUS_E_HIP;
 }
