@@ -245,11 +245,19 @@ def bench_part(args, d: dict, rec_np: np.ndarray, dev) -> dict:
         def call():
             return scope_statistics(inst, out["instance_excl"], cnt, R, iter_lo=0, iter_hi=15)
         units, unit_name = nb, "instances"
-        passes = 2 if R > 256 else 1
-        # sort passes; ordinals (sorted element in, pair out; pair in, ordinal
-        # out); statistics (instance, exclusive time, ordinal in, histogram key
-        # out); the histogram pass over the keys
-        per_call = nb * (48.0 * passes + 24.0 + 12.0 + 48.0 + 4.0)
+        if R <= 4096:
+            # chunk-local ordinals (context and region half of each instance in,
+            # ordinal out); the carry scan over the chunks' counts (R words per
+            # chunk of 4096: written, read, read and written); statistics
+            # (instance, exclusive time, ordinal in and out, histogram key out);
+            # the histogram pass over the keys
+            per_call = nb * (16.0 + 4.0 + 16.0 * R / 4096 + 32.0 + 8.0 + 4.0 + 4.0 + 4.0 + 4.0)
+        else:
+            passes = 2 if R > 256 else 1
+            # sort passes; ordinals (sorted element in, pair out; pair in, ordinal
+            # out); statistics (instance, exclusive time, ordinal in, histogram
+            # key out); the histogram pass over the keys
+            per_call = nb * (48.0 * passes + 24.0 + 12.0 + 48.0 + 4.0)
         what = f"iterations 0..15 of every region, on the instances of the {WORKLOADS[args.config]}"
     elif part == "probes":
         pr_np = tracegen.probes_for([1, 2, 7], d["blocks"] * d["warps"], 16, 5, seed=9)

@@ -338,7 +338,9 @@ enum {
   ARGUS_SC_N_UNCLOSED = 4,
   ARGUS_SC_N_SELF_NESTED = 5,
   ARGUS_SC_N_ITERATIONS = 6, /* 1 + the largest ordinal; 0 without instances */
-  ARGUS_SC_NUM_COUNTERS = 8  /* 7 is zero */
+  ARGUS_SC_INTERNAL = 7,     /* internal-error bits: 0 unless a consistency check in the
+                                library fails (2: an instance's region_id >= num_regions) */
+  ARGUS_SC_NUM_COUNTERS = 8
 };
 
 typedef struct argus_scope_config {

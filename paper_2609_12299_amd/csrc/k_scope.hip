@@ -7,17 +7,22 @@
 // among the instances of its context with the same BEGIN region, in
 // canonical (context, begin time) order.
 //
-// Ordinals: the instance array is already ordered by context, so a stable
-// sort by region alone yields (region, context, canonical) order, in which
-// the instances of one (context, region) form a run; an instance's ordinal
-// is its distance from the start of its run.  The sort is an LSD radix sort
-// over the region's 8-bit digits (one pass for up to 256 regions, else two):
-// per 4096-element tile a digit histogram, one exclusive scan over the
-// digit-major histograms, then a stable scatter that ranks each tile's
-// elements with eight ballots per wave.  Run starts come from a wave
-// max-scan of the run heads, with one binary search per wave for a run that
-// began before it.  The ordinals are scattered back to canonical order and
-// the scoped statistics are taken in canonical order with global atomics.
+// Ordinals: the instance array is already ordered by context, so within any
+// stretch of it a stable sort by region alone yields (region, context,
+// canonical) order, in which the instances of one (context, region) form a
+// run; an instance's ordinal among them is its distance from the start of
+// its run.  Up to kSoMaxRegions regions, this is done per chunk of 4096
+// consecutive instances, in LDS: each chunk's ordinals are exact except for
+// the context that enters it from earlier chunks, whose counts per region
+// (the carry) come from a scan over the chunks' counts of their last
+// context, and are added where the statistics read the ordinals.  With more
+// regions the whole array is sorted: an LSD radix sort over the region's
+// 8-bit digits (per 4096-element tile a digit histogram, one exclusive scan
+// over the digit-major histograms, then a stable scatter that ranks each
+// tile's elements with eight ballots per wave), run starts from a wave
+// max-scan of the run heads with one binary search per wave for a run that
+// began before it, and the ordinals scattered back to canonical order.  The
+// scoped statistics are taken in canonical order.
 #include <string.h>
 
 #include <algorithm>
@@ -273,6 +278,20 @@ __device__ __forceinline__ uint64_t sb_lower(const uint64_t* ka, const uint64_t*
   return lo;
 }
 
+// Scope counters: slot 7 holds internal-error bits (zero unless a
+// consistency check inside the library fails).
+__device__ __forceinline__ void sc_flag(uint64_t* counters, uint64_t code) {
+  atomicOr((unsigned long long*)&counters[ARGUS_SC_INTERNAL], (unsigned long long)code);
+}
+
+// Chunk-local ordinals (up to kSoMaxRegions regions).
+constexpr uint32_t kSoMaxRegions = 4096;
+constexpr uint32_t kSoCont = 1;    // the chunk's last context continues into the next chunk
+constexpr uint32_t kSoWhole = 2;   // the chunk holds one context
+constexpr uint32_t kSoPcont = 4;   // the chunk's first context began in an earlier chunk
+constexpr uint32_t kSoPending = 0x80000000u;  // ordinal still lacks its chunk's carry
+constexpr uint32_t kSoSeg = 256;   // chunks per segment of the carry scan
+
 struct ScopeArgs {
   const argus_instance* inst;
   const uint64_t* excl;
@@ -286,6 +305,13 @@ struct ScopeArgs {
   uint32_t* octr;     // [kOrdMaxBuckets] pairs gathered per bucket so far
   uint64_t* pairs;    // [count] ordinal << 32 | index, by bucket (a free sort buffer)
   uint32_t* hkey;     // [count] histogram key of each instance (a free sort buffer)
+  // chunk-local ordinals
+  uint32_t fast;      // 1: k_so_local wrote the ordinals; k_sc_stats adds the carries
+  uint32_t* tail;     // [chunks][R] counts of the chunk's last context per region, then
+                      // the carry entering each chunk whose first context began earlier
+  uint32_t* cflag;    // [chunks] kSoCont | kSoWhole | kSoPcont
+  uint32_t* segb;     // [segments][R] segment composites, then the carry entering each
+  uint32_t* segm;     // [segments] 1: the segment passes its entering carry on
 };
 
 // Fill kernel for the outputs that are accumulated.
@@ -415,7 +441,7 @@ __global__ __launch_bounds__(kScThreads) void k_sc_ordinal(ScopeArgs a, int buf)
         slot[r] = atomicAdd(&s_cnt[bk[r]], 1u);
         pr[r] = ((uint64_t)ord << 32) | idx[r];
       } else {
-        flag_internal_error(a.counters, 1);
+        sc_flag(a.counters, 1);
       }
     }
     __syncthreads();
@@ -429,7 +455,7 @@ __global__ __launch_bounds__(kScThreads) void k_sc_ordinal(ScopeArgs a, int buf)
       if (bk[r] == 0xFFFFFFFFu) continue;
       const uint64_t at = ((uint64_t)bk[r] << kOrdBucketBits) + s_cnt[bk[r]] + slot[r];
       if (at < n) a.pairs[at] = pr[r];
-      else flag_internal_error(a.counters, 1);
+      else sc_flag(a.counters, 1);
     }
     __syncthreads();
   }
@@ -459,7 +485,232 @@ __global__ __launch_bounds__(kScThreads) void k_sc_ord_place(ScopeArgs a) {
     const uint64_t pr = a.pairs[i];
     const uint32_t idx = (uint32_t)pr;
     if (idx >= b0 && idx < b0 + size) a.ordinal[idx] = (uint32_t)(pr >> 32);
-    else flag_internal_error(a.counters, 1);
+    else sc_flag(a.counters, 1);
+  }
+}
+
+
+// One stable LDS pass of a chunk's keys (region << 12 | element) on the
+// 8-bit digit at `shift`: each wave ranks its 1024 consecutive keys with
+// eight ballots per round of 64, then the digit offsets of the waves come
+// from one block scan.
+__device__ __forceinline__ void so_pass(const uint32_t* src, uint32_t* dst, uint32_t cnt, int shift,
+                                        uint32_t (*s_wave)[256], uint32_t* s_lstart,
+                                        uint32_t* s_w, uint32_t* s_carry) {
+  const uint32_t tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const uint64_t lt = lanemask_lt();
+#pragma unroll
+  for (int q = 0; q < 4; ++q) s_wave[q][tid] = 0;
+  if (tid == 0) *s_carry = 0;
+  __syncthreads();
+  uint32_t key[kScRounds], rk[kScRounds];
+#pragma unroll
+  for (int r = 0; r < kScRounds; ++r) {
+    const uint32_t p = w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
+    const bool valid = p < cnt;
+    key[r] = valid ? src[p] : 0u;
+    const uint32_t d = (key[r] >> shift) & 0xFFu;
+    uint64_t peers = __ballot(valid);
+#pragma unroll
+    for (int bit = 0; bit < 8; ++bit) {
+      const uint64_t bal = __ballot((d >> bit) & 1u);
+      peers &= ((d >> bit) & 1u) ? bal : ~bal;
+    }
+    uint32_t rank = 0xFFFFFFFFu;
+    if (valid) {
+      const uint32_t old = s_wave[w][d];
+      rank = old + (uint32_t)__popcll(peers & lt);
+      __builtin_amdgcn_wave_barrier();
+      if ((peers >> lane) == 1ull) s_wave[w][d] = old + (uint32_t)__popcll(peers);
+    }
+    __builtin_amdgcn_wave_barrier();
+    rk[r] = rank;
+  }
+  __syncthreads();
+  uint32_t c = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t v = s_wave[q][tid];
+    s_wave[q][tid] = c;
+    c += v;
+  }
+  s_lstart[tid] = block_excl_scan<kScThreads>(c, s_w, s_carry);
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < kScRounds; ++r) {
+    if (rk[r] == 0xFFFFFFFFu) continue;
+    const uint32_t d = (key[r] >> shift) & 0xFFu;
+    const uint32_t slot = s_lstart[d] + s_wave[w][d] + rk[r];
+    if (slot < kScTile) dst[slot] = key[r];
+  }
+  __syncthreads();
+}
+
+// Ordinals of one chunk of 4096 consecutive instances, exact except for the
+// context that entered the chunk from earlier ones (those are written with
+// kSoPending and completed in k_sc_stats), and, when the chunk's last
+// context continues into the next chunk, that context's counts per region.
+// The chunk is sorted stably by region in LDS; a (region, context) run's
+// elements then lie together in canonical order, and an element's local
+// ordinal is its distance from its run's start (a wave max-scan of the run
+// heads).
+__global__ __launch_bounds__(kScThreads) void k_so_local(ScopeArgs a) {
+  __shared__ uint32_t s_k[2][kScTile];   // keys in sort order; then local ordinals by element
+  __shared__ uint32_t s_ctx[kScTile];    // context of each element
+  __shared__ uint32_t s_wave[4][256];
+  __shared__ uint32_t s_lstart[256];
+  __shared__ uint32_t s_w[kScThreads / 64];
+  __shared__ uint32_t s_carry;
+  __shared__ int32_t s_wl[kScThreads / 64];
+  __shared__ uint32_t s_flag;
+  const uint64_t n = sb_count(a.s);
+  const uint4* inst = reinterpret_cast<const uint4*>(a.inst);
+  const uint32_t tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const int passes = a.R > 256 ? 2 : 1;
+  for (uint64_t c = blockIdx.x; c * kScTile < n; c += gridDim.x) {
+    const uint64_t base = c * kScTile;
+    const uint32_t cnt = n - base < (uint64_t)kScTile ? (uint32_t)(n - base) : kScTile;
+    bool bad = false;
+#pragma unroll
+    for (int r = 0; r < kScRounds; ++r) {
+      const uint32_t e = w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
+      if (e < cnt) {
+        const uint4 h1 = inst[2 * (base + e) + 1];
+        const uint32_t reg = h1.w & 0xFFFFu;
+        bad |= reg >= a.R;
+        s_ctx[e] = h1.x;
+        s_k[0][e] = (reg << 12) | e;
+      }
+    }
+    if (bad) sc_flag(a.counters, 2);  // regions must lie below num_regions
+    __syncthreads();
+    if (tid == 0) {
+      const uint32_t F = s_ctx[0], L = s_ctx[cnt - 1];
+      uint32_t f = F == L ? kSoWhole : 0u;
+      if (base > 0 && inst[2 * (base - 1) + 1].x == F) f |= kSoPcont;
+      if (base + cnt < n && inst[2 * (base + cnt) + 1].x == L) f |= kSoCont;
+      a.cflag[c] = f;
+      s_flag = f;
+    }
+    int cur = 0;
+    for (int pass = 0; pass < passes; ++pass, cur ^= 1)
+      so_pass(s_k[cur], s_k[cur ^ 1], cnt, 12 + 8 * pass, s_wave, s_lstart, s_w, &s_carry);
+    const uint32_t* sk = s_k[cur];
+    uint32_t* s_ord = s_k[cur ^ 1];  // local ordinal of each element (the other buffer is free)
+    const uint32_t flag = s_flag;
+    const uint32_t L = s_ctx[cnt - 1];
+    uint32_t* tail = a.tail + c * (uint64_t)a.R;
+    if (flag & kSoCont)
+      for (uint32_t r = tid; r < a.R; r += kScThreads) tail[r] = 0;
+    // run heads: a position whose (region, context) differs from the one before
+    auto same_run = [&](uint32_t k0, uint32_t k1) {
+      return (k0 >> 12) == (k1 >> 12) && s_ctx[k0 & 0xFFFu] == s_ctx[k1 & 0xFFFu];
+    };
+    int32_t hm[kScRounds];
+    int32_t run = -1;
+#pragma unroll
+    for (int r = 0; r < kScRounds; ++r) {
+      const uint32_t q = w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
+      const bool head = q < cnt && (q == 0 || !same_run(sk[q - 1], sk[q]));
+      int32_t x = head ? (int32_t)q : -1;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const int32_t o = __shfl_up(x, d);
+        if (lane >= (uint32_t)d && o > x) x = o;
+      }
+      x = x > run ? x : run;
+      run = __shfl(x, 63);
+      hm[r] = x;
+    }
+    if (lane == 0) s_wl[w] = run;
+    __syncthreads();  // the tail cleared, the waves' last heads
+    int32_t enter = -1;
+    for (uint32_t q = 0; q < w; ++q) enter = s_wl[q] > enter ? s_wl[q] : enter;
+#pragma unroll
+    for (int r = 0; r < kScRounds; ++r) {
+      const uint32_t q = w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
+      if (q >= cnt) continue;
+      const uint32_t k = sk[q];
+      const int32_t h = hm[r] > enter ? hm[r] : enter;
+      const uint32_t local = q - (uint32_t)h;
+      s_ord[k & 0xFFFu] = local;
+      // the last element of a run of the last context: its run's count
+      if ((flag & kSoCont) && s_ctx[k & 0xFFFu] == L && (q + 1 == cnt || !same_run(k, sk[q + 1])) &&
+          (k >> 12) < a.R)
+        tail[k >> 12] = local + 1;
+    }
+    __syncthreads();
+    const uint32_t F = s_ctx[0];
+#pragma unroll
+    for (int r = 0; r < kScRounds; ++r) {
+      const uint32_t e = w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
+      if (e >= cnt) continue;
+      const uint32_t local = s_ord[e];
+      const bool pending = (flag & kSoPcont) && s_ctx[e] == F;
+      a.ordinal[base + e] = pending ? (kSoPending | local) : local;
+    }
+    __syncthreads();  // LDS reused by the next chunk
+  }
+}
+
+__device__ __forceinline__ uint64_t so_chunks(uint64_t n) { return (n + kScTile - 1) / kScTile; }
+
+// The carry entering chunk c (per region): x_{c+1} = m_c x_c + b_c, with
+// m_c = 1 when the chunk is one context that continues from the chunk before
+// and into the next, b_c = the chunk's last-context counts when that context
+// continues (else 0); x_0 = 0.  A three-phase scan: the composite of each
+// segment of kSoSeg chunks, a sequential pass over the segments per region,
+// then each segment's carries.
+__global__ __launch_bounds__(kScThreads) void k_so_seg(ScopeArgs a) {
+  const uint64_t chunks = so_chunks(sb_count(a.s));
+  const uint64_t nseg = (chunks + kSoSeg - 1) / kSoSeg;
+  const uint64_t i = (uint64_t)blockIdx.x * kScThreads + threadIdx.x;
+  const uint64_t sg = i / a.R;
+  const uint32_t r = (uint32_t)(i % a.R);
+  if (sg >= nseg) return;
+  uint32_t M = 1, B = 0;
+  const uint64_t c1 = (sg + 1) * kSoSeg < chunks ? (sg + 1) * kSoSeg : chunks;
+  for (uint64_t c = sg * kSoSeg; c < c1; ++c) {
+    const uint32_t f = a.cflag[c];
+    const uint32_t t = (f & kSoCont) ? a.tail[c * a.R + r] : 0u;
+    if ((f & kSoCont) && (f & kSoWhole) && (f & kSoPcont)) {
+      B += t;
+    } else {
+      M = 0;
+      B = t;
+    }
+  }
+  a.segb[sg * a.R + r] = B;
+  if (r == 0) a.segm[sg] = M;
+}
+
+__global__ __launch_bounds__(kScThreads) void k_so_top(ScopeArgs a) {
+  const uint64_t chunks = so_chunks(sb_count(a.s));
+  const uint64_t nseg = (chunks + kSoSeg - 1) / kSoSeg;
+  const uint32_t r = blockIdx.x * kScThreads + threadIdx.x;
+  if (r >= a.R) return;
+  uint32_t X = 0;
+  for (uint64_t sg = 0; sg < nseg; ++sg) {
+    const uint32_t B = a.segb[sg * a.R + r];
+    a.segb[sg * a.R + r] = X;  // the carry entering the segment
+    X = a.segm[sg] ? X + B : B;
+  }
+}
+
+__global__ __launch_bounds__(kScThreads) void k_so_down(ScopeArgs a) {
+  const uint64_t chunks = so_chunks(sb_count(a.s));
+  const uint64_t nseg = (chunks + kSoSeg - 1) / kSoSeg;
+  const uint64_t i = (uint64_t)blockIdx.x * kScThreads + threadIdx.x;
+  const uint64_t sg = i / a.R;
+  const uint32_t r = (uint32_t)(i % a.R);
+  if (sg >= nseg) return;
+  uint32_t x = a.segb[sg * a.R + r];
+  const uint64_t c1 = (sg + 1) * kSoSeg < chunks ? (sg + 1) * kSoSeg : chunks;
+  for (uint64_t c = sg * kSoSeg; c < c1; ++c) {
+    const uint32_t f = a.cflag[c];
+    const uint32_t t = (f & kSoCont) ? a.tail[c * a.R + r] : 0u;
+    if (f & kSoPcont) a.tail[c * a.R + r] = x;  // the carry entering chunk c
+    x = ((f & kSoCont) && (f & kSoWhole) && (f & kSoPcont)) ? x + t : t;
   }
 }
 
@@ -493,15 +744,24 @@ __global__ __launch_bounds__(kScStatThreads) void k_sc_stats(ScopeArgs a) {
     return LDS_ROWS ? &srow[(uint64_t)reg * kScCols + col]
                     : (unsigned long long*)(a.stats + (uint64_t)reg * ARGUS_RS_WIDTH + col);
   };
-  uint32_t c_in = 0, c_m = 0, c_mm = 0, c_u = 0, c_s = 0;
+  uint32_t c_in = 0, c_m = 0, c_mm = 0, c_u = 0, c_s = 0, best = 0;
   for (uint64_t x = (uint64_t)blockIdx.x * kScStatThreads + threadIdx.x; x < n;
        x += (uint64_t)gridDim.x * kScStatThreads) {
     const uint4 h0 = inst[2 * x], h1 = inst[2 * x + 1];
     const uint32_t ctx = h1.x, reg = h1.w & 0xFFFFu, ereg = h1.w >> 16;
+    uint32_t ord = a.ordinal[x];
+    if (a.fast) {
+      // chunk-local ordinals: add the carry of the context entering the chunk
+      if (ord & kSoPending) {
+        ord = (ord & ~kSoPending) + (reg < a.R ? a.tail[(x / kScTile) * a.R + reg] : 0u);
+        a.ordinal[x] = ord;
+      }
+      best = best > ord + 1 ? best : ord + 1;
+    }
     const uint64_t group = a.sc.group_shift >= 32 ? 0ull : (uint64_t)(ctx >> a.sc.group_shift);
     const bool in = in_range32(ctx & a.sc.role_mask, a.sc.role_lo, a.sc.role_hi) &&
                     in_range32(group, a.sc.group_lo, a.sc.group_hi) &&
-                    in_range32(a.ordinal[x], a.sc.iter_lo, a.sc.iter_hi) && reg < a.R &&
+                    in_range32(ord, a.sc.iter_lo, a.sc.iter_hi) && reg < a.R &&
                     (!a.region_mask || a.region_mask[reg] != 0);
     // the instance's histogram key (none unless matched and in scope)
     uint32_t hk = 0xFFFFFFFFu;
@@ -552,6 +812,15 @@ __global__ __launch_bounds__(kScStatThreads) void k_sc_stats(ScopeArgs a) {
     }
   }
   const uint32_t lane = threadIdx.x & 63;
+  if (a.fast) {
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) {
+      const uint32_t o = __shfl_xor(best, d);
+      best = best > o ? best : o;
+    }
+    if (lane == 0 && best)
+      atomicMax((unsigned long long*)&a.counters[ARGUS_SC_N_ITERATIONS], (unsigned long long)best);
+  }
   const uint32_t v[5] = {c_in, c_m, c_mm, c_u, c_s};
   const int slot[5] = {ARGUS_SC_N_IN_SCOPE, ARGUS_SC_N_MATCHED, ARGUS_SC_N_MISMATCHED,
                        ARGUS_SC_N_UNCLOSED, ARGUS_SC_N_SELF_NESTED};
@@ -865,7 +1134,7 @@ SortLayout carve_sort(Carver& c, uint64_t m) {
 
 struct ScLayout {
   SortLayout ref;
-  size_t hist, bsum, octr, total;
+  size_t hist, bsum, octr, tail, cflag, segb, segm, total;
 };
 ScLayout sc_layout(uint64_t max_inst) {
   Carver c;
@@ -874,6 +1143,12 @@ ScLayout sc_layout(uint64_t max_inst) {
   L.hist = c.take(sizeof(uint32_t) * 256 * tiles_for(max_inst));
   L.bsum = c.take(sizeof(uint32_t) * scan_blocks_for(256 * tiles_for(max_inst)));
   L.octr = c.take(sizeof(uint32_t) * kOrdMaxBuckets);
+  // chunk-local ordinals: per chunk (tile) and region up to kSoMaxRegions
+  const uint64_t chunks = tiles_for(max_inst), segs = (chunks + kSoSeg - 1) / kSoSeg;
+  L.tail = c.take(sizeof(uint32_t) * chunks * kSoMaxRegions);
+  L.cflag = c.take(sizeof(uint32_t) * chunks);
+  L.segb = c.take(sizeof(uint32_t) * segs * kSoMaxRegions);
+  L.segm = c.take(sizeof(uint32_t) * segs);
   L.total = c.o;
   return L;
 }
@@ -1018,19 +1293,36 @@ extern "C" int argus_attr_scope(const argus_scope_config* cfg, const argus_scope
   a.s = make_bufs(base, L.ref, L.hist, L.bsum, io->max_instances, io->d_n_instances,
                   io->d_instances);
   a.octr = (uint32_t*)(base + L.octr);
+  a.tail = (uint32_t*)(base + L.tail);
+  a.cflag = (uint32_t*)(base + L.cflag);
+  a.segb = (uint32_t*)(base + L.segb);
+  a.segm = (uint32_t*)(base + L.segm);
+  a.fast = a.R <= kSoMaxRegions ? 1u : 0u;
   hipStream_t st = (hipStream_t)stream_v;
   hipLaunchKernelGGL(k_sc_init, dim3(sc_grid((uint64_t)a.R * ARGUS_RS_WIDTH, kScThreads, 1024)),
                      dim3(kScThreads), 0, st, a);
-  const int buf = sort_reference(a.s, a.R, st);
-  a.pairs = a.s.a[buf ^ 1];  // free once the sort is done
-  hipLaunchKernelGGL(k_sc_ordinal, dim3(sc_grid(io->max_instances, kScTile, 2048)),
-                     dim3(kScThreads), 0, st, a, buf);
-  {
+  if (a.fast) {
+    const uint64_t chunks = tiles_for(io->max_instances);
+    const uint64_t segs = (chunks + kSoSeg - 1) / kSoSeg;
+    hipLaunchKernelGGL(k_so_local, dim3((uint32_t)std::min<uint64_t>(chunks, 8192)), dim3(kScThreads), 0,
+                       st, a);
+    const uint64_t cells = segs * a.R;
+    hipLaunchKernelGGL(k_so_seg, dim3((uint32_t)((cells + kScThreads - 1) / kScThreads)),
+                       dim3(kScThreads), 0, st, a);
+    hipLaunchKernelGGL(k_so_top, dim3((a.R + kScThreads - 1) / kScThreads), dim3(kScThreads), 0, st, a);
+    hipLaunchKernelGGL(k_so_down, dim3((uint32_t)((cells + kScThreads - 1) / kScThreads)),
+                       dim3(kScThreads), 0, st, a);
+    a.hkey = reinterpret_cast<uint32_t*>(a.s.b[1]);  // the sort buffers are free
+  } else {
+    const int buf = sort_reference(a.s, a.R, st);
+    a.pairs = a.s.a[buf ^ 1];  // free once the sort is done
+    hipLaunchKernelGGL(k_sc_ordinal, dim3(sc_grid(io->max_instances, kScTile, 2048)),
+                       dim3(kScThreads), 0, st, a, buf);
     const uint64_t nbk = (io->max_instances + (1ull << kOrdBucketBits) - 1) >> kOrdBucketBits;
     const uint64_t blocks = 8ull * ((nbk + 7) / 8) * kOrdSlices;
     hipLaunchKernelGGL(k_sc_ord_place, dim3((uint32_t)(blocks ? blocks : 1)), dim3(kScThreads), 0, st, a);
+    a.hkey = reinterpret_cast<uint32_t*>(a.s.b[buf ^ 1]);  // free once the sort is done
   }
-  a.hkey = reinterpret_cast<uint32_t*>(a.s.b[buf ^ 1]);  // free once the sort is done
   if (a.R <= kScLdsRegions) {
     const size_t lds = (size_t)a.R * kScCols * sizeof(uint64_t);
     (void)hipFuncSetAttribute((const void*)k_sc_stats<true>,

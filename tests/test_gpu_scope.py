@@ -51,7 +51,13 @@ SCOPES = [dict(), dict(iter_lo=1, iter_hi=3), dict(role_mask=3, role_lo=1, role_
 
 @pytest.mark.parametrize("n,n_ctx,R,tr", [(0, 3, 3, 10), (1, 1, 2, 5), (4095, 5, 7, 3000),
                                           (4097, 9, 300, 4000), (8193, 3, 2, 100),
-                                          (30001, 17, 9, 40000), (100000, 64, 700, 1 << 20)])
+                                          (30001, 17, 9, 40000), (100000, 64, 700, 1 << 20),
+                                          # more than 4096 regions: the whole-array sort path
+                                          (20000, 7, 5000, 30000),
+                                          # three contexts over ~370 chunks of 4096 instances:
+                                          # carries through whole chunks and across segments
+                                          # of 256 chunks
+                                          (3000000, 3, 40, 1 << 22)])
 def test_random_malformed(oracle_mod, n, n_ctx, R, tr):
     rng = np.random.default_rng(n + R)
     rec = random_malformed(rng, n, n_ctx, R, tr)
