@@ -490,57 +490,76 @@ __global__ __launch_bounds__(kScThreads) void k_sc_ord_place(ScopeArgs a) {
 }
 
 
+// Inclusive maximum over the wave (unsigned; lanes past a row edge see 0).
+__device__ __forceinline__ uint32_t wave_incl_max32(uint32_t v) {
+  v = max(v, dpp32<kDppRowShr + 1>(v));
+  v = max(v, dpp32<kDppRowShr + 2>(v));
+  v = max(v, dpp32<kDppRowShr + 4>(v));
+  v = max(v, dpp32<kDppRowShr + 8>(v));
+  v = max(v, dpp32<kDppBcast15, 0xA>(v));
+  v = max(v, dpp32<kDppBcast31, 0xC>(v));
+  return v;
+}
+
 // One stable LDS pass of a chunk's keys (region << 12 | element) on the
-// 8-bit digit at `shift`: each wave ranks its 1024 consecutive keys with
-// eight ballots per round of 64, then the digit offsets of the waves come
-// from one block scan.
+// `bits`-bit digit at `shift`: each wave ranks its 1024 consecutive keys
+// with one ballot per digit bit per round of 64, then the digit offsets of
+// the waves come from one scan over the 256 digits (a wave scan each, the
+// four wave totals through LDS).  `cw` holds this pass's per-wave digit
+// counts (cleared beforehand); `nw` is cleared here for the next pass.
 __device__ __forceinline__ void so_pass(const uint32_t* src, uint32_t* dst, uint32_t cnt, int shift,
-                                        uint32_t (*s_wave)[256], uint32_t* s_lstart,
-                                        uint32_t* s_w, uint32_t* s_carry) {
+                                        int bits, uint32_t (*cw)[256], uint32_t (*nw)[256],
+                                        uint32_t* s_lstart, uint32_t* s_w) {
   const uint32_t tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const uint64_t lt = lanemask_lt();
-#pragma unroll
-  for (int q = 0; q < 4; ++q) s_wave[q][tid] = 0;
-  if (tid == 0) *s_carry = 0;
-  __syncthreads();
+  const uint32_t dmask = (1u << bits) - 1u;
   uint32_t key[kScRounds], rk[kScRounds];
 #pragma unroll
   for (int r = 0; r < kScRounds; ++r) {
     const uint32_t p = w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
     const bool valid = p < cnt;
     key[r] = valid ? src[p] : 0u;
-    const uint32_t d = (key[r] >> shift) & 0xFFu;
+    const uint32_t d = (key[r] >> shift) & dmask;
     uint64_t peers = __ballot(valid);
-#pragma unroll
-    for (int bit = 0; bit < 8; ++bit) {
+#pragma unroll 8
+    for (int bit = 0; bit < bits; ++bit) {
       const uint64_t bal = __ballot((d >> bit) & 1u);
       peers &= ((d >> bit) & 1u) ? bal : ~bal;
     }
     uint32_t rank = 0xFFFFFFFFu;
     if (valid) {
-      const uint32_t old = s_wave[w][d];
+      const uint32_t old = cw[w][d];
       rank = old + (uint32_t)__popcll(peers & lt);
       __builtin_amdgcn_wave_barrier();
-      if ((peers >> lane) == 1ull) s_wave[w][d] = old + (uint32_t)__popcll(peers);
+      if ((peers >> lane) == 1ull) cw[w][d] = old + (uint32_t)__popcll(peers);
     }
     __builtin_amdgcn_wave_barrier();
     rk[r] = rank;
   }
+#pragma unroll
+  for (int q = 0; q < 4; ++q) nw[q][tid] = 0;
   __syncthreads();
+  // thread tid owns digit tid: the waves' offsets within it, then where the
+  // digit starts in the chunk
   uint32_t c = 0;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
-    const uint32_t v = s_wave[q][tid];
-    s_wave[q][tid] = c;
+    const uint32_t v = cw[q][tid];
+    cw[q][tid] = c;
     c += v;
   }
-  s_lstart[tid] = block_excl_scan<kScThreads>(c, s_w, s_carry);
+  const uint32_t inc = (uint32_t)wave_incl_scan32((int32_t)c);
+  if (lane == 63) s_w[w] = inc;
+  __syncthreads();
+  uint32_t pre = 0;
+  for (uint32_t q = 0; q < w; ++q) pre += s_w[q];
+  s_lstart[tid] = pre + inc - c;
   __syncthreads();
 #pragma unroll
   for (int r = 0; r < kScRounds; ++r) {
     if (rk[r] == 0xFFFFFFFFu) continue;
-    const uint32_t d = (key[r] >> shift) & 0xFFu;
-    const uint32_t slot = s_lstart[d] + s_wave[w][d] + rk[r];
+    const uint32_t d = (key[r] >> shift) & dmask;
+    const uint32_t slot = s_lstart[d] + cw[w][d] + rk[r];
     if (slot < kScTile) dst[slot] = key[r];
   }
   __syncthreads();
@@ -556,97 +575,132 @@ __device__ __forceinline__ void so_pass(const uint32_t* src, uint32_t* dst, uint
 // heads).
 __global__ __launch_bounds__(kScThreads) void k_so_local(ScopeArgs a) {
   __shared__ uint32_t s_k[2][kScTile];   // keys in sort order; then local ordinals by element
-  __shared__ uint32_t s_ctx[kScTile];    // context of each element
-  __shared__ uint32_t s_wave[4][256];
+  // each element's context, as the chunk position where that context starts
+  // (contexts are contiguous in canonical order)
+  __shared__ uint16_t s_seg[kScTile];
+  __shared__ uint32_t s_wave[2][4][256];  // per-wave digit counts of the two passes
   __shared__ uint32_t s_lstart[256];
   __shared__ uint32_t s_w[kScThreads / 64];
-  __shared__ uint32_t s_carry;
-  __shared__ int32_t s_wl[kScThreads / 64];
-  __shared__ uint32_t s_flag;
+  __shared__ uint32_t s_wl[kScThreads / 64];
+  __shared__ uint32_t s_flag, s_lctx;
   const uint64_t n = sb_count(a.s);
   const uint4* inst = reinterpret_cast<const uint4*>(a.inst);
   const uint32_t tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
-  const int passes = a.R > 256 ? 2 : 1;
+  // digit widths of the region (12 + region bits of the key)
+  const uint32_t rbits = a.R > 1 ? 32u - (uint32_t)__clz(a.R - 1) : 1u;
+  const int passes = rbits > 8 ? 2 : 1;
+  const int bits0 = rbits > 8 ? 8 : (int)rbits, bits1 = rbits > 8 ? (int)rbits - 8 : 0;
   for (uint64_t c = blockIdx.x; c * kScTile < n; c += gridDim.x) {
     const uint64_t base = c * kScTile;
     const uint32_t cnt = n - base < (uint64_t)kScTile ? (uint32_t)(n - base) : kScTile;
     bool bad = false;
+    uint32_t ctx[kScRounds];
 #pragma unroll
     for (int r = 0; r < kScRounds; ++r) {
       const uint32_t e = w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
+      ctx[r] = 0;
       if (e < cnt) {
         const uint4 h1 = inst[2 * (base + e) + 1];
         const uint32_t reg = h1.w & 0xFFFFu;
         bad |= reg >= a.R;
-        s_ctx[e] = h1.x;
+        ctx[r] = h1.x;
         s_k[0][e] = (reg << 12) | e;
+        if (e + 1 == cnt) s_lctx = h1.x;
       }
     }
     if (bad) sc_flag(a.counters, 2);  // regions must lie below num_regions
+    // context starts: 1 + the last start at or before each element within the
+    // wave (0: the context began before the wave's first element)
+    uint32_t cs[kScRounds];
+    {
+      // the context before the wave's first element
+      uint32_t before = 0xFFFFFFFFu;
+      const uint32_t e0 = w * (kScRounds * 64);
+      if (e0 > 0 && e0 < cnt) before = inst[2 * (base + e0 - 1) + 1].x;
+      uint32_t run = 0;
+#pragma unroll
+      for (int r = 0; r < kScRounds; ++r) {
+        const uint32_t e = w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
+        const uint32_t prev = lane_prev(ctx[r], before);
+        before = (uint32_t)__builtin_amdgcn_readlane((int)ctx[r], 63);
+        const bool head = e < cnt && (e == 0 || prev != ctx[r]);
+        uint32_t x = wave_incl_max32(head ? e + 1 : 0u);
+        x = x > run ? x : run;
+        run = (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
+        cs[r] = x;
+      }
+      if (lane == 0) s_wl[w] = run;
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) s_wave[0][q][tid] = 0;
     __syncthreads();
+    {
+      uint32_t enter = 0;
+      for (uint32_t q = 0; q < w; ++q) enter = s_wl[q] > enter ? s_wl[q] : enter;
+#pragma unroll
+      for (int r = 0; r < kScRounds; ++r) {
+        const uint32_t e = w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
+        if (e < cnt) s_seg[e] = (uint16_t)((cs[r] > enter ? cs[r] : enter) - 1u);
+      }
+    }
     if (tid == 0) {
-      const uint32_t F = s_ctx[0], L = s_ctx[cnt - 1];
+      const uint32_t F = ctx[0], L = s_lctx;
       uint32_t f = F == L ? kSoWhole : 0u;
       if (base > 0 && inst[2 * (base - 1) + 1].x == F) f |= kSoPcont;
       if (base + cnt < n && inst[2 * (base + cnt) + 1].x == L) f |= kSoCont;
       a.cflag[c] = f;
       s_flag = f;
     }
-    int cur = 0;
-    for (int pass = 0; pass < passes; ++pass, cur ^= 1)
-      so_pass(s_k[cur], s_k[cur ^ 1], cnt, 12 + 8 * pass, s_wave, s_lstart, s_w, &s_carry);
+    so_pass(s_k[0], s_k[1], cnt, 12, bits0, s_wave[0], s_wave[1], s_lstart, s_w);
+    if (passes > 1) so_pass(s_k[1], s_k[0], cnt, 20, bits1, s_wave[1], s_wave[0], s_lstart, s_w);
+    const int cur = passes > 1 ? 0 : 1;
     const uint32_t* sk = s_k[cur];
     uint32_t* s_ord = s_k[cur ^ 1];  // local ordinal of each element (the other buffer is free)
     const uint32_t flag = s_flag;
-    const uint32_t L = s_ctx[cnt - 1];
+    const uint32_t L = s_seg[cnt - 1];
     uint32_t* tail = a.tail + c * (uint64_t)a.R;
     if (flag & kSoCont)
       for (uint32_t r = tid; r < a.R; r += kScThreads) tail[r] = 0;
     // run heads: a position whose (region, context) differs from the one before
     auto same_run = [&](uint32_t k0, uint32_t k1) {
-      return (k0 >> 12) == (k1 >> 12) && s_ctx[k0 & 0xFFFu] == s_ctx[k1 & 0xFFFu];
+      return (k0 >> 12) == (k1 >> 12) && s_seg[k0 & 0xFFFu] == s_seg[k1 & 0xFFFu];
     };
-    int32_t hm[kScRounds];
-    int32_t run = -1;
+    uint32_t hm[kScRounds];  // 1 + the last head at or before each position (0: none)
+    uint32_t run = 0;
 #pragma unroll
     for (int r = 0; r < kScRounds; ++r) {
       const uint32_t q = w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
       const bool head = q < cnt && (q == 0 || !same_run(sk[q - 1], sk[q]));
-      int32_t x = head ? (int32_t)q : -1;
-#pragma unroll
-      for (int d = 1; d < 64; d <<= 1) {
-        const int32_t o = __shfl_up(x, d);
-        if (lane >= (uint32_t)d && o > x) x = o;
-      }
+      uint32_t x = wave_incl_max32(head ? q + 1 : 0u);
       x = x > run ? x : run;
-      run = __shfl(x, 63);
+      run = (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
       hm[r] = x;
     }
     if (lane == 0) s_wl[w] = run;
     __syncthreads();  // the tail cleared, the waves' last heads
-    int32_t enter = -1;
+    uint32_t enter = 0;
     for (uint32_t q = 0; q < w; ++q) enter = s_wl[q] > enter ? s_wl[q] : enter;
 #pragma unroll
     for (int r = 0; r < kScRounds; ++r) {
       const uint32_t q = w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
       if (q >= cnt) continue;
       const uint32_t k = sk[q];
-      const int32_t h = hm[r] > enter ? hm[r] : enter;
-      const uint32_t local = q - (uint32_t)h;
+      const uint32_t h = (hm[r] > enter ? hm[r] : enter) - 1u;
+      const uint32_t local = q - h;
       s_ord[k & 0xFFFu] = local;
       // the last element of a run of the last context: its run's count
-      if ((flag & kSoCont) && s_ctx[k & 0xFFFu] == L && (q + 1 == cnt || !same_run(k, sk[q + 1])) &&
+      if ((flag & kSoCont) && s_seg[k & 0xFFFu] == L && (q + 1 == cnt || !same_run(k, sk[q + 1])) &&
           (k >> 12) < a.R)
         tail[k >> 12] = local + 1;
     }
     __syncthreads();
-    const uint32_t F = s_ctx[0];
 #pragma unroll
     for (int r = 0; r < kScRounds; ++r) {
       const uint32_t e = w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
       if (e >= cnt) continue;
       const uint32_t local = s_ord[e];
-      const bool pending = (flag & kSoPcont) && s_ctx[e] == F;
+      // the chunk's first context starts at position 0
+      const bool pending = (flag & kSoPcont) && s_seg[e] == 0;
       a.ordinal[base + e] = pending ? (kSoPending | local) : local;
     }
     __syncthreads();  // LDS reused by the next chunk
@@ -670,14 +724,22 @@ __global__ __launch_bounds__(kScThreads) void k_so_seg(ScopeArgs a) {
   if (sg >= nseg) return;
   uint32_t M = 1, B = 0;
   const uint64_t c1 = (sg + 1) * kSoSeg < chunks ? (sg + 1) * kSoSeg : chunks;
-  for (uint64_t c = sg * kSoSeg; c < c1; ++c) {
-    const uint32_t f = a.cflag[c];
-    const uint32_t t = (f & kSoCont) ? a.tail[c * a.R + r] : 0u;
-    if ((f & kSoCont) && (f & kSoWhole) && (f & kSoPcont)) {
-      B += t;
-    } else {
-      M = 0;
-      B = t;
+  // branch-free steps, eight chunks' loads at a time (a count slot of a chunk
+  // whose last context ends in it holds no count and is not used)
+  for (uint64_t c0 = sg * kSoSeg; c0 < c1; c0 += 8) {
+    uint32_t f[8], t[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint64_t c = c0 + u;
+      f[u] = c < c1 ? a.cflag[c] : kSoCont | kSoWhole | kSoPcont;
+      t[u] = c < c1 ? a.tail[c * a.R + r] : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint32_t tv = (f[u] & kSoCont) ? t[u] : 0u;
+      const bool keep = (f[u] & (kSoCont | kSoWhole | kSoPcont)) == (kSoCont | kSoWhole | kSoPcont);
+      M = keep ? M : 0u;
+      B = keep ? B + tv : tv;
     }
   }
   a.segb[sg * a.R + r] = B;
@@ -706,11 +768,22 @@ __global__ __launch_bounds__(kScThreads) void k_so_down(ScopeArgs a) {
   if (sg >= nseg) return;
   uint32_t x = a.segb[sg * a.R + r];
   const uint64_t c1 = (sg + 1) * kSoSeg < chunks ? (sg + 1) * kSoSeg : chunks;
-  for (uint64_t c = sg * kSoSeg; c < c1; ++c) {
-    const uint32_t f = a.cflag[c];
-    const uint32_t t = (f & kSoCont) ? a.tail[c * a.R + r] : 0u;
-    if (f & kSoPcont) a.tail[c * a.R + r] = x;  // the carry entering chunk c
-    x = ((f & kSoCont) && (f & kSoWhole) && (f & kSoPcont)) ? x + t : t;
+  for (uint64_t c0 = sg * kSoSeg; c0 < c1; c0 += 8) {
+    uint32_t f[8], t[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint64_t c = c0 + u;
+      f[u] = c < c1 ? a.cflag[c] : 0u;
+      t[u] = c < c1 ? a.tail[c * a.R + r] : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const uint64_t c = c0 + u;
+      if (f[u] & kSoPcont) a.tail[c * a.R + r] = x;  // the carry entering chunk c
+      const uint32_t tv = (f[u] & kSoCont) ? t[u] : 0u;
+      const bool keep = (f[u] & (kSoCont | kSoWhole | kSoPcont)) == (kSoCont | kSoWhole | kSoPcont);
+      x = keep ? x + tv : tv;
+    }
   }
 }
 
@@ -1304,8 +1377,10 @@ extern "C" int argus_attr_scope(const argus_scope_config* cfg, const argus_scope
   if (a.fast) {
     const uint64_t chunks = tiles_for(io->max_instances);
     const uint64_t segs = (chunks + kSoSeg - 1) / kSoSeg;
-    hipLaunchKernelGGL(k_so_local, dim3((uint32_t)std::min<uint64_t>(chunks, 8192)), dim3(kScThreads), 0,
-                       st, a);
+    hipLaunchKernelGGL(k_so_local,
+                       dim3((uint32_t)std::min<uint64_t>(chunks, persistent_blocks((const void*)k_so_local,
+                                                                                   kScThreads))),
+                       dim3(kScThreads), 0, st, a);
     const uint64_t cells = segs * a.R;
     hipLaunchKernelGGL(k_so_seg, dim3((uint32_t)((cells + kScThreads - 1) / kScThreads)),
                        dim3(kScThreads), 0, st, a);
