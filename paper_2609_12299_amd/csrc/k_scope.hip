@@ -1100,12 +1100,27 @@ __global__ __launch_bounds__(kScThreads) void k_ho_compact(HandoffArgs a) {
     if (inst[2 * x + 1].z <= a.L) a.comp[a.flags[x]] = (uint32_t)x;
 }
 
-// Successive pairs: count and sum added, min and max only when they would
-// change (a plain read first), into this block's copy of the table; the
-// histogram in LDS, added once per block.
+// Successive pairs, aggregated per block in an LDS hash table of (x region,
+// y region) keys (linear probing, keys claimed with a compare-and-swap):
+// count, sum, min and max by LDS atomics, added once per block into this
+// block's copy of the table (a pair whose key finds no slot goes there
+// directly: count and sum added, min and max only when they would change);
+// the histogram in LDS, added once per block.
+constexpr uint32_t kHoSlots = 1024;
+constexpr int kHoProbes = 8;
+
 __global__ __launch_bounds__(kScThreads) void k_ho_pairs(HandoffArgs a) {
   __shared__ unsigned long long s_hist[65];
+  __shared__ uint32_t s_key[kHoSlots];                // 1 + rx * R + ry; 0: empty
+  __shared__ unsigned long long s_v[4][kHoSlots];      // count, sum, min, max
   for (int i = threadIdx.x; i < 65; i += kScThreads) s_hist[i] = 0;
+  for (uint32_t i = threadIdx.x; i < kHoSlots; i += kScThreads) {
+    s_key[i] = 0;
+    s_v[0][i] = 0;
+    s_v[1][i] = 0;
+    s_v[2][i] = ~0ull;
+    s_v[3][i] = 0;
+  }
   __syncthreads();
   const uint64_t n = ho_count(a);
   const uint4* inst = reinterpret_cast<const uint4*>(a.inst);
@@ -1124,13 +1139,38 @@ __global__ __launch_bounds__(kScThreads) void k_ho_pairs(HandoffArgs a) {
     const uint64_t te = (uint64_t)xa.z | ((uint64_t)xa.w << 32);
     const uint64_t tb = (uint64_t)ya.x | ((uint64_t)ya.y << 32);
     const uint64_t gap = tb - te;
-    unsigned long long* row = (unsigned long long*)(table + 4 * ((uint64_t)rx * a.R + ry));
-    atomicAdd(&row[0], 1ull);
-    atomicAdd(&row[1], (unsigned long long)gap);
-    if (gap < __hip_atomic_load(&row[2], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
-      atomicMin(&row[2], (unsigned long long)gap);
-    if (gap > __hip_atomic_load(&row[3], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
-      atomicMax(&row[3], (unsigned long long)gap);
+    const uint32_t key = 1u + rx * a.R + ry;
+    uint32_t h = (key * 2654435761u) >> 22;  // 10 bits
+    int slot = -1;
+    for (int p = 0; p < kHoProbes; ++p) {
+      const uint32_t cur = __hip_atomic_load(&s_key[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      if (cur == key) {
+        slot = (int)h;
+        break;
+      }
+      if (cur == 0) {
+        const uint32_t prev = atomicCAS(&s_key[h], 0u, key);
+        if (prev == 0u || prev == key) {
+          slot = (int)h;
+          break;
+        }
+      }
+      h = (h + 1) & (kHoSlots - 1);
+    }
+    if (slot >= 0) {
+      atomicAdd(&s_v[0][slot], 1ull);
+      atomicAdd(&s_v[1][slot], (unsigned long long)gap);
+      atomicMin(&s_v[2][slot], (unsigned long long)gap);
+      atomicMax(&s_v[3][slot], (unsigned long long)gap);
+    } else {
+      unsigned long long* row = (unsigned long long*)(table + 4 * ((uint64_t)rx * a.R + ry));
+      atomicAdd(&row[0], 1ull);
+      atomicAdd(&row[1], (unsigned long long)gap);
+      if (gap < __hip_atomic_load(&row[2], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+        atomicMin(&row[2], (unsigned long long)gap);
+      if (gap > __hip_atomic_load(&row[3], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+        atomicMax(&row[3], (unsigned long long)gap);
+    }
     atomicAdd(&s_hist[bit_width64(gap)], 1ull);
     if (a.parent_gap && yb.y != kNoParent && yb.y < n)
       atomicAdd((unsigned long long*)&a.parent_gap[yb.y], (unsigned long long)gap);
@@ -1145,6 +1185,15 @@ __global__ __launch_bounds__(kScThreads) void k_ho_pairs(HandoffArgs a) {
   __syncthreads();
   for (int i = threadIdx.x; i < 65; i += kScThreads)
     if (s_hist[i]) atomicAdd((unsigned long long*)&a.hist[i], s_hist[i]);
+  for (uint32_t i = threadIdx.x; i < kHoSlots; i += kScThreads) {
+    const uint32_t key = s_key[i];
+    if (!key) continue;
+    unsigned long long* row = (unsigned long long*)(table + 4 * (uint64_t)(key - 1u));
+    atomicAdd(&row[0], s_v[0][i]);
+    atomicAdd(&row[1], s_v[1][i]);
+    atomicMin(&row[2], s_v[2][i]);
+    atomicMax(&row[3], s_v[3][i]);
+  }
 }
 
 // The copies combined into the output table.
@@ -1562,7 +1611,11 @@ extern "C" int argus_attr_handoffs(const argus_handoffs_config* cfg, const argus
     hipLaunchKernelGGL(k_ho_flags, dim3(g), dim3(kScThreads), 0, st, a);
     scan_u32(a.flags, io->max_instances, a.bsum, st);
     hipLaunchKernelGGL(k_ho_compact, dim3(g), dim3(kScThreads), 0, st, a);
-    hipLaunchKernelGGL(k_ho_pairs, dim3(g), dim3(kScThreads), 0, st, a);
+    // resident blocks only: each adds its table once
+    hipLaunchKernelGGL(k_ho_pairs,
+                       dim3((uint32_t)std::min<uint64_t>(g, persistent_blocks((const void*)k_ho_pairs,
+                                                                              kScThreads))),
+                       dim3(kScThreads), 0, st, a);
   }
   hipLaunchKernelGGL(k_ho_combine, dim3(sc_grid((uint64_t)a.R * a.R, kScThreads, 4096)),
                      dim3(kScThreads), 0, st, a);
