@@ -2,7 +2,7 @@
 //
 // Stable sorting is how the records of every execution context are put in
 // execution order before the per-context stack is replayed (the paper's
-// Section 3.2 keeps one nested region-context stack per warp); the same
+// Section 3.2 keeps a stack of open regions for each warp); the same
 // pass orders the overlap events by (group, time).
 //
 // One pass, per tile of 4096 elements (4 waves x 16 rounds x 64 lanes):
