@@ -82,7 +82,7 @@ def test_hand_trace(oracle_mod):
     (0, 100, 3, 3, 5, 50), (7, 0, 2, 2, 3, 10), (300, 2000, 4, 5, 7, 200),
     (2049, 5000, 3, 6, 40, 3000), (30001, 70001, 17, 9, 300, 40000),
     (100000, 300000, 64, 40, 1000, 1 << 20),
-    # a P x R table too small to hold the join's key index: plain binary search
+    # many instances over a table of 3 PCs x 2 regions
     (5000, 3000, 3, 2, 3, 4000)])
 def test_random_malformed(oracle_mod, n, ns, n_ctx, R, P, tr):
     rng = np.random.default_rng(n + ns)
