@@ -799,6 +799,7 @@ __device__ __forceinline__ bool in_range32(uint64_t v, uint32_t lo, uint32_t hi)
 constexpr uint32_t kScLdsRegions = 1024;  // 12 x 8 B x 1024 = 96 KiB of LDS
 constexpr int kScStatThreads = 1024;
 constexpr int kScCols = 12;               // ARGUS_RS_COUNT .. ARGUS_RS_SELF_NESTED
+constexpr int kScStatItems = 4;           // instances per thread and step
 
 template <bool LDS_ROWS>
 __global__ __launch_bounds__(kScStatThreads) void k_sc_stats(ScopeArgs a) {
@@ -818,27 +819,56 @@ __global__ __launch_bounds__(kScStatThreads) void k_sc_stats(ScopeArgs a) {
                     : (unsigned long long*)(a.stats + (uint64_t)reg * ARGUS_RS_WIDTH + col);
   };
   uint32_t c_in = 0, c_m = 0, c_mm = 0, c_u = 0, c_s = 0, best = 0;
-  for (uint64_t x = (uint64_t)blockIdx.x * kScStatThreads + threadIdx.x; x < n;
-       x += (uint64_t)gridDim.x * kScStatThreads) {
-    const uint4 h0 = inst[2 * x], h1 = inst[2 * x + 1];
-    const uint32_t ctx = h1.x, reg = h1.w & 0xFFFFu, ereg = h1.w >> 16;
-    uint32_t ord = a.ordinal[x];
-    if (a.fast) {
-      // chunk-local ordinals: add the carry of the context entering the chunk
-      if (ord & kSoPending) {
-        ord = (ord & ~kSoPending) + (reg < a.R ? a.tail[(x / kScTile) * a.R + reg] : 0u);
-        a.ordinal[x] = ord;
-      }
-      best = best > ord + 1 ? best : ord + 1;
+  // kScStatItems instances per thread and step: their instance and ordinal
+  // loads together, then (in scope and matched only) the exclusive times and
+  // parents' regions together
+  const uint64_t step = (uint64_t)gridDim.x * kScStatThreads;
+  for (uint64_t x0 = (uint64_t)blockIdx.x * kScStatThreads + threadIdx.x; x0 < n;
+       x0 += step * kScStatItems) {
+    uint4 h0[kScStatItems], h1[kScStatItems];
+    uint32_t ord[kScStatItems];
+#pragma unroll
+    for (int j = 0; j < kScStatItems; ++j) {
+      const uint64_t x = x0 + j * step;
+      const uint64_t xc = x < n ? x : n - 1;
+      h0[j] = inst[2 * xc];
+      h1[j] = inst[2 * xc + 1];
+      ord[j] = a.ordinal[xc];
     }
-    const uint64_t group = a.sc.group_shift >= 32 ? 0ull : (uint64_t)(ctx >> a.sc.group_shift);
-    const bool in = in_range32(ctx & a.sc.role_mask, a.sc.role_lo, a.sc.role_hi) &&
-                    in_range32(group, a.sc.group_lo, a.sc.group_hi) &&
-                    in_range32(ord, a.sc.iter_lo, a.sc.iter_hi) && reg < a.R &&
-                    (!a.region_mask || a.region_mask[reg] != 0);
+    bool in[kScStatItems];
+    uint64_t exv[kScStatItems];
+    uint32_t preg[kScStatItems];
+#pragma unroll
+    for (int j = 0; j < kScStatItems; ++j) {
+      const uint64_t x = x0 + j * step;
+      const uint32_t ctx = h1[j].x, reg = h1[j].w & 0xFFFFu, ereg = h1[j].w >> 16;
+      if (a.fast && x < n) {
+        // chunk-local ordinal: add the carry of the context entering the chunk
+        if (ord[j] & kSoPending) {
+          ord[j] = (ord[j] & ~kSoPending) + (reg < a.R ? a.tail[(x / kScTile) * a.R + reg] : 0u);
+          a.ordinal[x] = ord[j];
+        }
+        best = best > ord[j] + 1 ? best : ord[j] + 1;
+      }
+      const uint64_t group = a.sc.group_shift >= 32 ? 0ull : (uint64_t)(ctx >> a.sc.group_shift);
+      in[j] = x < n && in_range32(ctx & a.sc.role_mask, a.sc.role_lo, a.sc.role_hi) &&
+              in_range32(group, a.sc.group_lo, a.sc.group_hi) &&
+              in_range32(ord[j], a.sc.iter_lo, a.sc.iter_hi) && reg < a.R &&
+              (!a.region_mask || a.region_mask[reg] != 0);
+      const bool mt = in[j] && ereg == reg;
+      exv[j] = mt ? a.excl[x] : 0ull;
+      const uint32_t par = h1[j].y;
+      preg[j] = mt && par != kNoParent && par < n ? (inst[2 * (uint64_t)par + 1].w & 0xFFFFu)
+                                                  : 0xFFFFFFFFu;
+    }
+#pragma unroll
+    for (int j = 0; j < kScStatItems; ++j) {
+    const uint64_t x = x0 + j * step;
+    if (x >= n) continue;
+    const uint32_t reg = h1[j].w & 0xFFFFu, ereg = h1[j].w >> 16;
     // the instance's histogram key (none unless matched and in scope)
     uint32_t hk = 0xFFFFFFFFu;
-    if (in) {
+    if (in[j]) {
       c_in += 1;
       if (ereg == kNoEnd) {
         c_u += 1;
@@ -849,9 +879,9 @@ __global__ __launch_bounds__(kScStatThreads) void k_sc_stats(ScopeArgs a) {
         if (ereg < a.R) atomicAdd(col_ptr(ereg, ARGUS_RS_MISM_AS_END), 1ull);
       } else {
         c_m += 1;
-        const uint64_t tb = (uint64_t)h0.x | ((uint64_t)h0.y << 32);
-        const uint64_t te = (uint64_t)h0.z | ((uint64_t)h0.w << 32);
-        const uint64_t d = te - tb, ex = a.excl[x];
+        const uint64_t tb = (uint64_t)h0[j].x | ((uint64_t)h0[j].y << 32);
+        const uint64_t te = (uint64_t)h0[j].z | ((uint64_t)h0[j].w << 32);
+        const uint64_t d = te - tb, ex = exv[j];
         atomicAdd(col_ptr(reg, ARGUS_RS_COUNT), 1ull);
         atomicAdd(col_ptr(reg, ARGUS_RS_INCL_SUM), (unsigned long long)d);
         atomicAdd(col_ptr(reg, ARGUS_RS_EXCL_SUM), (unsigned long long)ex);
@@ -860,14 +890,14 @@ __global__ __launch_bounds__(kScStatThreads) void k_sc_stats(ScopeArgs a) {
         atomicMin(col_ptr(reg, ARGUS_RS_EXCL_MIN), (unsigned long long)ex);
         atomicMax(col_ptr(reg, ARGUS_RS_EXCL_MAX), (unsigned long long)ex);
         hk = (reg << 16) | (bit_width64(d) << 8) | bit_width64(ex);
-        const uint32_t par = h1.y;
-        if (par != kNoParent && par < n && (inst[2 * (uint64_t)par + 1].w & 0xFFFFu) == reg) {
+        if (preg[j] == reg) {
           c_s += 1;
           atomicAdd(col_ptr(reg, ARGUS_RS_SELF_NESTED), 1ull);
         }
       }
     }
     a.hkey[x] = hk;
+    }
   }
   if (LDS_ROWS) {
     __syncthreads();
