@@ -47,9 +47,20 @@ constexpr uint32_t kOrdSlices = 128;                              // blocks per 
 // A stable LSD radix sort over 8-bit digits of 16-byte elements (two u64
 // words, ping-pong buffers).  The first pass may read the instance array
 // instead (word a = BEGIN region, word b = context << 32 | index).
+// Device-side state of a sort whose passes on constant digits are skipped:
+// over all elements, the OR and the AND of each word (bits where they
+// differ mark the digits that vary).  The passes go over word a's bytes
+// 0..7, then word b's bytes 4..7, in that order; a pass that runs moves the
+// elements to the other buffer, so the buffer a pass reads is the parity of
+// the passes before it that run.
+struct SortCtl {
+  uint64_t or_a, and_a, or_b, and_b;
+};
+
 struct SortBufs {
   uint64_t* a[2];
   uint64_t* b[2];
+  SortCtl* ctl;    // NULL: every pass runs, buffers as the caller says
   uint32_t* hist;  // [256][tiles_max], digit-major
   uint32_t* bsum;  // scan block sums
   uint64_t tiles_max;
@@ -58,6 +69,28 @@ struct SortBufs {
   const argus_instance* inst;  // source of the SRC_INST passes
 };
 enum { kSrcBuf = 0, kSrcInst = 1 };
+
+// A pass whose digit is the same for every element leaves the order as it
+// is: it is skipped (its kernels return at once and the buffer stays).
+__device__ __forceinline__ bool sb_skip(const SortBufs& s, int word, int shift) {
+  if (!s.ctl) return false;
+  const uint64_t vary = word ? (s.ctl->or_b ^ s.ctl->and_b) : (s.ctl->or_a ^ s.ctl->and_a);
+  return ((vary >> shift) & 0xFFu) == 0;
+}
+// The buffer holding the elements before the pass on (word, shift) (after
+// all passes: word 1, shift 64).
+__device__ __forceinline__ int sb_in(const SortBufs& s, int in, int word, int shift) {
+  if (!s.ctl) return in;
+  const uint64_t va = s.ctl->or_a ^ s.ctl->and_a, vb = s.ctl->or_b ^ s.ctl->and_b;
+  int ran = 0;
+  for (int sh = 0; sh < 64; sh += 8) {
+    if (word == 0 && sh >= shift) break;
+    ran += ((va >> sh) & 0xFFu) != 0;
+  }
+  if (word == 1)
+    for (int sh = 32; sh < shift; sh += 8) ran += ((vb >> sh) & 0xFFu) != 0;
+  return ran & 1;
+}
 
 __device__ __forceinline__ uint64_t sb_count(const SortBufs& s) {
   if (!s.count_ptr) return s.count_max;
@@ -83,6 +116,8 @@ __device__ __forceinline__ void sb_load(const SortBufs& s, int in, uint64_t e, u
 template <int SRC>
 __global__ __launch_bounds__(kScThreads) void k_sort_hist(SortBufs s, int in, int word, int shift) {
   __shared__ uint32_t s_cnt[256];
+  if (sb_skip(s, word, shift)) return;
+  in = sb_in(s, in, word, shift);
   const uint64_t n = sb_count(s);
   const uint64_t tile = blockIdx.x;
   s_cnt[threadIdx.x] = 0;
@@ -165,6 +200,36 @@ __global__ __launch_bounds__(kScThreads) void k_scan_apply(uint32_t* data, uint6
   }
 }
 
+// A small table scanned by one block: staged in LDS with coalesced loads,
+// each of 1024 threads sums a stretch of consecutive entries, one block scan
+// places the stretches, each thread writes its stretch's exclusive prefixes
+// in LDS, and the table goes back with coalesced stores.
+constexpr uint64_t kScSmallMax = 32768;
+__global__ __launch_bounds__(1024) void k_scan_small(uint32_t* data, uint64_t total, SortBufs s,
+                                                     int word, int shift) {
+  __shared__ uint32_t s_d[kScSmallMax];
+  __shared__ uint32_t s_carry;
+  __shared__ uint32_t s_w[16];
+  if (sb_skip(s, word, shift)) return;  // the digit table of a skipped pass
+  const uint32_t t = threadIdx.x, n = (uint32_t)total;
+  for (uint32_t i = t; i < n; i += 1024) s_d[i] = data[i];
+  if (t == 0) s_carry = 0;
+  __syncthreads();
+  const uint32_t per = (n + 1023) / 1024, b = t * per;
+  uint32_t v = 0;
+  for (uint32_t k = 0; k < per; ++k)
+    if (b + k < n) v += s_d[b + k];
+  uint32_t run = block_excl_scan<1024>(v, s_w, &s_carry);
+  for (uint32_t k = 0; k < per; ++k) {
+    if (b + k >= n) break;
+    const uint32_t d = s_d[b + k];
+    s_d[b + k] = run;
+    run += d;
+  }
+  __syncthreads();
+  for (uint32_t i = t; i < n; i += 1024) data[i] = s_d[i];
+}
+
 // Stable scatter of one tile.  Each wave takes 1024 consecutive elements
 // (16 rounds of 64 lanes, all loaded up front) and ranks each among the
 // wave's earlier elements of its digit: eight ballots find the lanes that
@@ -177,6 +242,9 @@ constexpr size_t kScStageBytes = 2 * sizeof(uint64_t) * kScTile;  // dynamic LDS
 template <int SRC>
 __global__ __launch_bounds__(kScThreads) void k_sort_scatter(SortBufs s, int in, int out, int word,
                                                              int shift) {
+  if (sb_skip(s, word, shift)) return;
+  in = sb_in(s, in, word, shift);
+  out = s.ctl ? in ^ 1 : out;
   extern __shared__ __align__(16) uint8_t sc_stage[];
   uint64_t* s_ta = reinterpret_cast<uint64_t*>(sc_stage);
   uint64_t* s_tb = s_ta + kScTile;
@@ -960,10 +1028,12 @@ struct ProbeArgs {
   uint64_t* groups;     // [np][ARGUS_PG_WIDTH]
   double* mean;
   uint64_t* counters;
+  uint64_t* vpart;      // [join blocks][4] each block's ORs and ANDs of the sort words
 };
 
 __global__ void k_pr_init(ProbeArgs a) {
   if (threadIdx.x < ARGUS_PR_NUM_COUNTERS) a.counters[threadIdx.x] = 0;
+
 }
 
 __global__ __launch_bounds__(kScThreads) void k_pr_join(ProbeArgs a) {
@@ -971,6 +1041,8 @@ __global__ __launch_bounds__(kScThreads) void k_pr_join(ProbeArgs a) {
   const uint64_t* ra = a.ref.a[a.ref_buf];
   const uint64_t* rb = a.ref.b[a.ref_buf];
   uint32_t bad = 0, joined = 0, unjoined = 0;
+  // the OR and the AND of the sort words (latency; instance code << 32)
+  uint64_t oa = 0, na = ~0ull, ob = 0, nb2 = ~0ull;
   for (uint64_t j = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; j < a.np;
        j += (uint64_t)gridDim.x * kScThreads) {
     const uint4 h0 = a.probes[2 * j], h1 = a.probes[2 * j + 1];
@@ -997,6 +1069,35 @@ __global__ __launch_bounds__(kScThreads) void k_pr_join(ProbeArgs a) {
     a.completion[j] = done;
     a.pb.a[0][j] = lat;
     a.pb.b[0][j] = (code << 32) | j;
+    oa |= lat;
+    na &= lat;
+    ob |= code << 32;
+    nb2 &= code << 32;
+  }
+  {
+    // the block's OR and AND, combined over the blocks by k_pr_vary
+    __shared__ uint64_t s_v[kScThreads / 64][4];
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1) {
+      oa |= (uint64_t)__shfl_xor((long long)oa, d);
+      na &= (uint64_t)__shfl_xor((long long)na, d);
+      ob |= (uint64_t)__shfl_xor((long long)ob, d);
+      nb2 &= (uint64_t)__shfl_xor((long long)nb2, d);
+    }
+    const uint32_t wv = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+      s_v[wv][0] = oa;
+      s_v[wv][1] = na;
+      s_v[wv][2] = ob;
+      s_v[wv][3] = nb2;
+    }
+    __syncthreads();
+    if (threadIdx.x < 4) {
+      uint64_t v = s_v[0][threadIdx.x];
+      for (int q = 1; q < kScThreads / 64; ++q)
+        v = (threadIdx.x & 1) ? (v & s_v[q][threadIdx.x]) : (v | s_v[q][threadIdx.x]);
+      a.vpart[4 * (uint64_t)blockIdx.x + threadIdx.x] = v;
+    }
   }
   const uint32_t lane = threadIdx.x & 63;
   const uint32_t v[3] = {bad, joined, unjoined};
@@ -1009,12 +1110,42 @@ __global__ __launch_bounds__(kScThreads) void k_pr_join(ProbeArgs a) {
   if (blockIdx.x == 0 && threadIdx.x == 0) a.counters[ARGUS_PR_N_PROBES] = a.np;
 }
 
+// The blocks' ORs and ANDs of the probe sort words into the sort state.
+__global__ __launch_bounds__(1024) void k_pr_vary(ProbeArgs a, uint32_t blocks) {
+  __shared__ uint64_t s_v[16][4];
+  uint64_t v[4] = {0, ~0ull, 0, ~0ull};
+  for (uint32_t b = threadIdx.x; b < blocks; b += 1024)
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      v[k] = (k & 1) ? (v[k] & a.vpart[4 * (uint64_t)b + k]) : (v[k] | a.vpart[4 * (uint64_t)b + k]);
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const uint64_t o = (uint64_t)__shfl_xor((long long)v[k], d);
+      v[k] = (k & 1) ? (v[k] & o) : (v[k] | o);
+    }
+  const uint32_t w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) s_v[w][k] = v[k];
+  __syncthreads();
+  if (threadIdx.x < 4) {
+    const int k = threadIdx.x;
+    uint64_t r = s_v[0][k];
+    for (int q = 1; q < 16; ++q) r = (k & 1) ? (r & s_v[q][k]) : (r | s_v[q][k]);
+    uint64_t* c = reinterpret_cast<uint64_t*>(a.pb.ctl);
+    c[k] = r;  // or_a, and_a, or_b, and_b
+  }
+}
+
 __device__ __forceinline__ bool pr_head(const uint64_t* b, uint64_t k, uint64_t none) {
   const uint64_t r = b[k] >> 32;
   return r != none && (k == 0 || (b[k - 1] >> 32) != r);
 }
 
 __global__ __launch_bounds__(kScThreads) void k_pr_heads(ProbeArgs a, int buf) {
+  buf = sb_in(a.pb, buf, 1, 64);
   const uint64_t* b = a.pb.b[buf];
   uint32_t heads = 0;
   for (uint64_t k = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; k < a.np;
@@ -1031,6 +1162,7 @@ __global__ __launch_bounds__(kScThreads) void k_pr_heads(ProbeArgs a, int buf) {
 // One thread per group head: the group's count, sum, issue time, mean and
 // nearest-rank percentiles (its latencies are in increasing order).
 __global__ __launch_bounds__(kScThreads) void k_pr_groups(ProbeArgs a, int buf) {
+  buf = sb_in(a.pb, buf, 1, 64);
   const uint64_t* la = a.pb.a[buf];
   const uint64_t* b = a.pb.b[buf];
   for (uint64_t k = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; k < a.np;
@@ -1307,7 +1439,7 @@ ScLayout sc_layout(uint64_t max_inst) {
 
 struct PrLayout {
   SortLayout ref, pr;
-  size_t hist, bsum, flags, total;
+  size_t hist, bsum, flags, ctl, vpart, total;
 };
 PrLayout pr_layout(uint64_t max_inst, uint64_t np) {
   Carver c;
@@ -1319,6 +1451,8 @@ PrLayout pr_layout(uint64_t max_inst, uint64_t np) {
   const uint64_t sb = std::max(scan_blocks_for(256 * tiles), scan_blocks_for(np));
   L.bsum = c.take(sizeof(uint32_t) * sb);
   L.flags = c.take(sizeof(uint32_t) * (np ? np : 1));
+  L.ctl = c.take(sizeof(SortCtl));
+  L.vpart = c.take(sizeof(uint64_t) * 4 * 4096);  // the join's blocks (at most 4096)
   L.total = c.o;
   return L;
 }
@@ -1339,7 +1473,14 @@ SortBufs make_bufs(char* base, const SortLayout& L, size_t hist, size_t bsum, ui
   return s;
 }
 
-void scan_u32(uint32_t* data, uint64_t total, uint32_t* bsum, hipStream_t st) {
+void scan_u32(uint32_t* data, uint64_t total, uint32_t* bsum, hipStream_t st,
+              const SortBufs* sk = nullptr, int word = 0, int shift = 0) {
+  if (total <= kScSmallMax) {
+    SortBufs none{};
+    hipLaunchKernelGGL(k_scan_small, dim3(1), dim3(1024), 0, st, data, total, sk ? *sk : none,
+                       word, shift);
+    return;
+  }
   const uint32_t blocks = (uint32_t)scan_blocks_for(total ? total : 1);
   hipLaunchKernelGGL(k_scan_sums, dim3(blocks), dim3(kScThreads), 0, st, data, total, bsum);
   hipLaunchKernelGGL(k_scan_top, dim3(1), dim3(1024), 0, st, bsum, blocks);
@@ -1357,7 +1498,7 @@ void sort_pass(const SortBufs& s, bool from_inst, int in, int out, int word, int
   else
     hipLaunchKernelGGL(k_sort_hist<kSrcBuf>, dim3(tiles), dim3(kScThreads), 0, st, s, in, word,
                        shift);
-  scan_u32(s.hist, 256ull * s.tiles_max, s.bsum, st);
+  scan_u32(s.hist, 256ull * s.tiles_max, s.bsum, st, &s, word, shift);
   if (from_inst)
     hipLaunchKernelGGL(k_sort_scatter<kSrcInst>, dim3(tiles), dim3(kScThreads), kScStageBytes, st, s,
                        in, out, word, shift);
@@ -1535,6 +1676,8 @@ extern "C" int argus_attr_probes(const argus_probes_config* cfg, const argus_pro
   a.ref = make_bufs(base, L.ref, L.hist, L.bsum, io->max_instances, io->d_n_instances,
                     io->d_instances);
   a.pb = make_bufs(base, L.pr, L.hist, L.bsum, io->n_probes, nullptr, io->d_instances);
+  a.pb.ctl = reinterpret_cast<SortCtl*>(base + L.ctl);  // passes on constant digits are skipped
+  a.vpart = reinterpret_cast<uint64_t*>(base + L.vpart);
   a.ref_out = io->d_ref;
   a.completion = io->d_completion;
   a.flags = (uint32_t*)(base + L.flags);
@@ -1545,8 +1688,9 @@ extern "C" int argus_attr_probes(const argus_probes_config* cfg, const argus_pro
   hipLaunchKernelGGL(k_pr_init, dim3(1), dim3(64), 0, st, a);
   if (a.np > 0) {
     a.ref_buf = sort_reference(a.ref, a.R, st);
-    hipLaunchKernelGGL(k_pr_join, dim3(sc_grid(a.np, kScThreads, 4096)), dim3(kScThreads), 0, st,
-                       a);
+    const uint32_t jb = sc_grid(a.np, kScThreads, 4096);
+    hipLaunchKernelGGL(k_pr_join, dim3(jb), dim3(kScThreads), 0, st, a);
+    hipLaunchKernelGGL(k_pr_vary, dim3(1), dim3(1024), 0, st, a, jb);
     // (instance, latency) order: the latency's eight bytes, then the
     // instance code's bytes (stable LSD)
     int in = 0;
