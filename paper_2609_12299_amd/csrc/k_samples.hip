@@ -263,8 +263,23 @@ __global__ __launch_bounds__(64) void k_s_region(SampArgs a) {
         s_prod[1][64 * u + lane] = has ? cur.al[u] * cur.x1[u] : 0.0;
       }
       __syncthreads();
-#pragma unroll 32
-      for (uint32_t j = 0; j < kLiftChunk; ++j) acc = acc + row[j];
+      // in order, 32 products at a time, the next 32 read from LDS while
+      // these are added
+      double b0[32], b1[32];
+#pragma unroll
+      for (int q = 0; q < 32; ++q) b0[q] = row[q];
+      for (uint32_t j = 0; j < kLiftChunk; j += 64) {
+#pragma unroll
+        for (int q = 0; q < 32; ++q) b1[q] = row[j + 32 + q];
+#pragma unroll
+        for (int q = 0; q < 32; ++q) acc = acc + b0[q];
+        if (j + 64 < kLiftChunk) {
+#pragma unroll
+          for (int q = 0; q < 32; ++q) b0[q] = row[j + 64 + q];
+        }
+#pragma unroll
+        for (int q = 0; q < 32; ++q) acc = acc + b1[q];
+      }
       __syncthreads();
     }
     cur = nxt;
