@@ -91,3 +91,28 @@ def test_persistent_gemm_probes(oracle_mod, tracegen_mod):
                     cls=d["region_class"], shift=d["group_shift"], G=d["num_groups"])
     assert int(o["counters"][2]) > 0 and int(o["counters"][4]) > 0
     assert_probe_parity(g, o, "config 2")
+
+
+@pytest.mark.parametrize("spread", ["full", "equal", "byte5"])
+def test_latency_spreads(oracle_mod, spread):
+    """The (instance, latency) sort skips the passes whose byte is the same
+    for every probe: latencies varying in all eight bytes (no pass skipped),
+    all zero (every latency pass skipped), and varying only in bytes 0 and 5
+    (the passes between and after them skipped)."""
+    rng = np.random.default_rng({"full": 1, "equal": 2, "byte5": 3}[spread])
+    rec = random_malformed(rng, 30001, 17, 9, 40000)
+    pr = _probes(rng, 20000, 17, 9, 30)
+    ok = pr["t_end"] >= pr["t_start"]
+    if spread == "full":
+        lat = rng.integers(0, 1 << 62, size=len(pr), dtype=np.uint64)
+        pr["t_start"] = rng.integers(0, 1 << 62, size=len(pr), dtype=np.uint64)
+    elif spread == "equal":
+        # 0, as unjoined and malformed probes have: every latency byte is constant
+        lat = np.zeros(len(pr), np.uint64)
+    else:
+        lat = (rng.integers(0, 256, size=len(pr)).astype(np.uint64) << np.uint64(40)) | np.uint64(3)
+    pr["t_end"] = np.where(ok, pr["t_start"] + lat, pr["t_start"] - np.uint64(1))
+    log(f"[gpu] probes latency spread {spread}")
+    g, o = run_both(oracle_mod, rec, 9, pr)
+    assert int(o["counters"][2]) > 0
+    assert_probe_parity(g, o, f"spread {spread}")
