@@ -266,16 +266,38 @@ def bench_part(args, d: dict, rec_np: np.ndarray, dev) -> dict:
         def call():
             return join_probes(inst, cnt, pr, R)
         units, unit_name = len(pr_np), "probes"
-        code_passes = (max(nb, 1).bit_length() + 7) // 8
-        per_call = (nb * 48.0 * (2 if R > 256 else 1)
-                    + len(pr_np) * (64.0 + 32.0 + 48.0 * (8 + code_passes)))
+
+        def probe_bytes(r):
+            # the reference sort pass(es); the join (probe and reference
+            # instance in, outputs and sort element out); the sort passes the
+            # library runs: those whose byte of the latency or the instance
+            # code is not the same for every probe
+            ref = r["ref"][:len(pr_np)].cpu().numpy().astype(np.uint64)
+            joined = ref != np.uint64(0xFFFFFFFF)
+            lat = np.where(joined, pr_np["t_end"] - pr_np["t_start"], np.uint64(0))
+            # an unjoined probe's code is the instance capacity
+            code = np.where(joined, ref, np.uint64(inst.shape[0]))
+
+            def varying(v, nbytes):
+                if len(v) == 0:
+                    return 0
+                d = np.bitwise_or.reduce(v) ^ np.bitwise_and.reduce(v)
+                return sum(1 for k in range(nbytes) if (int(d) >> (8 * k)) & 0xFF)
+            passes = varying(lat, 8) + varying(code, 4)
+            return (nb * 48.0 * (2 if R > 256 else 1)
+                    + len(pr_np) * (64.0 + 32.0 + 48.0 * passes))
+        per_call = None
         what = (f"{len(pr_np)} probes (3 operations x 16 iterations x 5 repeats per warp) joined "
                 f"to the {WORKLOADS[args.config]}")
     elif part == "handoffs":
         def call():
             return phase_handoffs(inst, cnt, R, level=1)
         units, unit_name = nb, "instances"
-        per_call = nb * 120.0
+        # compaction (level word in, index out for level <= 1); pairs (index
+        # and both instances in, for each level <= 1 instance)
+        lv = inst.view(torch.int32).view(-1, 8)[:nb, 6]
+        m = int(((lv >= 0) & (lv <= 1)).sum().item()) if nb else 0  # levels are below 2^31
+        per_call = nb * 4.0 + m * (4.0 + 4.0 + 64.0)
         what = f"level-1 phases (operators within token steps) of the {WORKLOADS[args.config]}"
     else:
         raise ValueError(part)
@@ -290,6 +312,8 @@ def bench_part(args, d: dict, rec_np: np.ndarray, dev) -> dict:
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / args.steps
+    if per_call is None:
+        per_call = probe_bytes(res[-1])
     del res
     ra.close()
     gbs = per_call / (ms * 1e-3) / 1e9

@@ -450,6 +450,8 @@ enum {
   ARGUS_HO_N_AT_LEVEL = 0, /* instances at level L */
   ARGUS_HO_N_GAPS = 1,     /* successive pairs measured */
   ARGUS_HO_GAP_SUM = 2,    /* their gaps, summed mod 2^64 */
+  ARGUS_HO_INTERNAL = 7,   /* internal-error bits: 0 unless a consistency check in the
+                              library fails */
   ARGUS_HO_NUM_COUNTERS = 8
 };
 

@@ -1212,9 +1212,10 @@ struct HandoffArgs {
   const uint64_t* n_inst;
   uint64_t max_inst;
   uint32_t R, L;
-  uint32_t* flags;  // level <= L, then their exclusive scan
-  uint32_t* comp;   // compacted instance indices
-  uint32_t* bsum;
+  uint32_t* comp;    // instances of level <= L in canonical order
+  uint64_t* status;  // [tiles] look-back words of the compaction (count, flags)
+  uint32_t* tctr;    // tile counter of the compaction
+  uint64_t* mtot;    // instances compacted
   uint64_t* pairs;  // [R][R][4]: count, sum, min, max (the output)
   uint64_t* rep;    // [copies][R][R][4]: per-copy accumulators in the workspace
   uint32_t copies;  // blocks b add into copy b % copies (fewer same-address atomics)
@@ -1237,29 +1238,95 @@ __global__ __launch_bounds__(kScThreads) void k_ho_init(HandoffArgs a) {
     for (uint64_t i = first; i < a.max_inst; i += stride) a.parent_gap[i] = 0;
   if (first < 65) a.hist[first] = 0;
   if (first < ARGUS_HO_NUM_COUNTERS) a.counters[first] = 0;
-}
-
-__global__ __launch_bounds__(kScThreads) void k_ho_flags(HandoffArgs a) {
-  const uint64_t n = ho_count(a);
-  const uint4* inst = reinterpret_cast<const uint4*>(a.inst);
-  uint32_t at = 0;
-  for (uint64_t x = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; x < n;
-       x += (uint64_t)gridDim.x * kScThreads) {
-    const uint32_t lvl = inst[2 * x + 1].z;
-    a.flags[x] = lvl <= a.L ? 1u : 0u;
-    at += lvl == a.L;
+  const uint64_t tiles = (a.max_inst + kScTile - 1) / kScTile;
+  for (uint64_t i = first; i < tiles; i += stride) a.status[i] = 0;
+  if (first == 0) {
+    *a.tctr = 0;
+    *a.mtot = 0;
   }
-  const uint32_t t = rows_sum32(row_sum32(at));
-  if ((threadIdx.x & 63) == 0 && t)
-    atomicAdd((unsigned long long*)&a.counters[ARGUS_HO_N_AT_LEVEL], (unsigned long long)t);
 }
 
+// The instances of level <= L compacted in canonical order, in one pass:
+// blocks take tiles of 4096 instances in order (a counter), count the
+// tile's qualifying instances (a ballot per round of 64, the waves' counts
+// through LDS), publish the count, find the count before the tile by
+// decoupled look-back, and write the indices.  The tile holding the last
+// instance records the total.
 __global__ __launch_bounds__(kScThreads) void k_ho_compact(HandoffArgs a) {
+  __shared__ uint32_t s_tile, s_w[kScThreads / 64];
+  __shared__ uint64_t s_base;
   const uint64_t n = ho_count(a);
-  const uint4* inst = reinterpret_cast<const uint4*>(a.inst);
-  for (uint64_t x = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; x < n;
-       x += (uint64_t)gridDim.x * kScThreads)
-    if (inst[2 * x + 1].z <= a.L) a.comp[a.flags[x]] = (uint32_t)x;
+  const uint64_t T = (n + kScTile - 1) / kScTile;
+  const uint32_t* iw = reinterpret_cast<const uint32_t*>(a.inst);  // 8 words per instance
+  const uint32_t tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const uint64_t lt = lanemask_lt();
+  uint32_t at = 0;
+  for (;;) {
+    if (tid == 0) s_tile = atomicAdd(a.tctr, 1u);
+    __syncthreads();
+    const uint64_t tile = s_tile;
+    if (tile >= T) break;
+    const uint64_t base = tile * kScTile;
+    uint64_t qm[kScRounds];  // ballot of the qualifying lanes of each round
+    uint32_t wc = 0;
+#pragma unroll
+    for (int r = 0; r < kScRounds; ++r) {
+      const uint64_t x = base + w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
+      const bool in = x < n;
+      const uint32_t lvl = in ? iw[8 * x + 6] : 0u;
+      at += in && lvl == a.L;
+      qm[r] = __ballot(in && lvl <= a.L);
+      wc += (uint32_t)__popcll(qm[r]);
+    }
+    if (lane == 0) s_w[w] = wc;
+    __syncthreads();
+    uint32_t wpre = 0, cnt = 0;
+#pragma unroll
+    for (int q = 0; q < kScThreads / 64; ++q) {
+      wpre += q < (int)w ? s_w[q] : 0u;
+      cnt += s_w[q];
+    }
+    if (tid == 0) {
+      uint64_t excl = 0;
+      if (tile == 0) {
+        st_agent(&a.status[0], kFlagIncl | cnt);
+      } else {
+        st_agent(&a.status[tile], kFlagAgg | cnt);
+        int64_t tt = (int64_t)tile - 1;
+        uint32_t spins = 0;
+        while (tt >= 0) {
+          const uint64_t v = ld_agent(&a.status[tt]);
+          const uint64_t f = v & ~kValMask;
+          if (f == 0) {
+            if (++spins > kMaxSpins) {
+              atomicOr((unsigned long long*)&a.counters[ARGUS_HO_INTERNAL], 1ull);
+              break;
+            }
+            backoff();
+            continue;
+          }
+          excl += v & kValMask;
+          if (f == kFlagIncl) break;
+          --tt;
+        }
+        st_agent(&a.status[tile], kFlagIncl | (excl + cnt));
+      }
+      s_base = excl;
+      if (tile == T - 1) *a.mtot = excl + cnt;
+    }
+    __syncthreads();
+    uint64_t o = s_base + wpre;
+#pragma unroll
+    for (int r = 0; r < kScRounds; ++r) {
+      if ((qm[r] >> lane) & 1u)
+        a.comp[o + (uint32_t)__popcll(qm[r] & lt)] =
+            (uint32_t)(base + w * (kScRounds * 64) + (uint32_t)r * 64 + lane);
+      o += (uint32_t)__popcll(qm[r]);
+    }
+  }
+  const uint32_t tot = rows_sum32(row_sum32(at));
+  if (lane == 0 && tot)
+    atomicAdd((unsigned long long*)&a.counters[ARGUS_HO_N_AT_LEVEL], (unsigned long long)tot);
 }
 
 // Successive pairs, aggregated per block in an LDS hash table of (x region,
@@ -1286,7 +1353,7 @@ __global__ __launch_bounds__(kScThreads) void k_ho_pairs(HandoffArgs a) {
   __syncthreads();
   const uint64_t n = ho_count(a);
   const uint4* inst = reinterpret_cast<const uint4*>(a.inst);
-  const uint64_t m = n ? a.flags[n - 1] + (inst[2 * (n - 1) + 1].z <= a.L ? 1u : 0u) : 0;
+  const uint64_t m = *a.mtot;
   uint64_t* table = a.rep + (uint64_t)(blockIdx.x % a.copies) * a.R * a.R * 4;
   uint64_t gaps = 0, gsum = 0;
   for (uint64_t k = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; k + 1 < m;
@@ -1718,15 +1785,16 @@ uint32_t ho_copies(uint32_t R) {
 }
 
 struct HoLayout {
-  size_t flags, comp, bsum, rep, total;
+  size_t comp, status, tctr, mtot, rep, total;
 };
 HoLayout ho_layout(uint64_t max_instances, uint32_t R) {
   Carver c;
   HoLayout L{};
   const uint64_t m = max_instances ? max_instances : 1;
-  L.flags = c.take(sizeof(uint32_t) * m);
   L.comp = c.take(sizeof(uint32_t) * m);
-  L.bsum = c.take(sizeof(uint32_t) * scan_blocks_for(m));
+  L.status = c.take(sizeof(uint64_t) * tiles_for(m));
+  L.tctr = c.take(sizeof(uint32_t));
+  L.mtot = c.take(sizeof(uint64_t));
   L.rep = c.take(sizeof(uint64_t) * 4 * (uint64_t)R * R * ho_copies(R));
   L.total = c.o;
   return L;
@@ -1766,9 +1834,10 @@ extern "C" int argus_attr_handoffs(const argus_handoffs_config* cfg, const argus
   a.max_inst = io->max_instances;
   a.R = cfg->num_regions;
   a.L = cfg->level;
-  a.flags = (uint32_t*)(base + HL.flags);
   a.comp = (uint32_t*)(base + HL.comp);
-  a.bsum = (uint32_t*)(base + HL.bsum);
+  a.status = (uint64_t*)(base + HL.status);
+  a.tctr = (uint32_t*)(base + HL.tctr);
+  a.mtot = (uint64_t*)(base + HL.mtot);
   a.rep = (uint64_t*)(base + HL.rep);
   a.copies = ho_copies(cfg->num_regions);
   a.pairs = io->d_pairs;
@@ -1782,9 +1851,12 @@ extern "C" int argus_attr_handoffs(const argus_handoffs_config* cfg, const argus
                      dim3(kScThreads), 0, st, a);
   if (io->max_instances > 0) {
     const uint32_t g = sc_grid(io->max_instances, kScThreads, 4096);
-    hipLaunchKernelGGL(k_ho_flags, dim3(g), dim3(kScThreads), 0, st, a);
-    scan_u32(a.flags, io->max_instances, a.bsum, st);
-    hipLaunchKernelGGL(k_ho_compact, dim3(g), dim3(kScThreads), 0, st, a);
+    // resident blocks only: they take the tiles in order
+    hipLaunchKernelGGL(k_ho_compact,
+                       dim3((uint32_t)std::min<uint64_t>(tiles_for(io->max_instances),
+                                                         persistent_blocks((const void*)k_ho_compact,
+                                                                           kScThreads))),
+                       dim3(kScThreads), 0, st, a);
     // resident blocks only: each adds its table once
     hipLaunchKernelGGL(k_ho_pairs,
                        dim3((uint32_t)std::min<uint64_t>(g, persistent_blocks((const void*)k_ho_pairs,
