@@ -294,10 +294,11 @@ def bench_part(args, d: dict, rec_np: np.ndarray, dev) -> dict:
             return phase_handoffs(inst, cnt, R, level=1)
         units, unit_name = nb, "instances"
         # compaction (level word in, index out for level <= 1); pairs (index
-        # and both instances in, for each level <= 1 instance)
+        # and both instances in, for each level <= 1 instance); the per-parent
+        # sums (one output word per instance)
         lv = inst.view(torch.int32).view(-1, 8)[:nb, 6]
         m = int(((lv >= 0) & (lv <= 1)).sum().item()) if nb else 0  # levels are below 2^31
-        per_call = nb * 4.0 + m * (4.0 + 4.0 + 64.0)
+        per_call = nb * (4.0 + 8.0) + m * (4.0 + 4.0 + 64.0)
         what = f"level-1 phases (operators within token steps) of the {WORKLOADS[args.config]}"
     else:
         raise ValueError(part)

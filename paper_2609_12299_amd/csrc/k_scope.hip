@@ -1217,8 +1217,9 @@ struct HandoffArgs {
   uint32_t* tctr;    // tile counter of the compaction
   uint64_t* mtot;    // instances compacted
   uint64_t* pairs;  // [R][R][4]: count, sum, min, max (the output)
-  uint64_t* rep;    // [copies][R][R][4]: per-copy accumulators in the workspace
-  uint32_t copies;  // blocks b add into copy b % copies (fewer same-address atomics)
+  uint32_t* dkey;   // [dumps][kHoSlots]: each pair block's hash table keys (0: empty)
+  uint64_t* dval;   // [dumps][kHoSlots][4]: and its count, sum, min, max
+  uint32_t dumps;   // pair blocks launched
   uint64_t* hist;   // [65]
   uint64_t* parent_gap;  // [max_inst] or NULL
   uint64_t* counters;
@@ -1232,8 +1233,8 @@ __device__ __forceinline__ uint64_t ho_count(const HandoffArgs& a) {
 __global__ __launch_bounds__(kScThreads) void k_ho_init(HandoffArgs a) {
   const uint64_t stride = (uint64_t)gridDim.x * kScThreads;
   const uint64_t first = (uint64_t)blockIdx.x * kScThreads + threadIdx.x;
-  const uint64_t np = (uint64_t)a.R * a.R * 4 * a.copies;
-  for (uint64_t i = first; i < np; i += stride) a.rep[i] = (i & 3) == 2 ? kU64Max : 0ull;
+  const uint64_t np = (uint64_t)a.R * a.R * 4;
+  for (uint64_t i = first; i < np; i += stride) a.pairs[i] = (i & 3) == 2 ? kU64Max : 0ull;
   if (a.parent_gap)
     for (uint64_t i = first; i < a.max_inst; i += stride) a.parent_gap[i] = 0;
   if (first < 65) a.hist[first] = 0;
@@ -1330,20 +1331,33 @@ __global__ __launch_bounds__(kScThreads) void k_ho_compact(HandoffArgs a) {
 }
 
 // Successive pairs, aggregated per block in an LDS hash table of (x region,
-// y region) keys (linear probing, keys claimed with a compare-and-swap):
-// count, sum, min and max by LDS atomics, added once per block into this
-// block's copy of the table (a pair whose key finds no slot goes there
-// directly: count and sum added, min and max only when they would change);
-// the histogram in LDS, added once per block.
-constexpr uint32_t kHoSlots = 1024;
-constexpr int kHoProbes = 8;
+// y region) keys (linear probing from the key's home slot, keys claimed with a
+// compare-and-swap): count, sum, min and max by LDS atomics.  At the end each
+// block stores its table, keys and values, into its own dump with plain
+// stores; k_ho_merge adds the dumps up.  A pair whose key finds no slot goes
+// to the output row directly, by global atomics (such a key is never in the
+// table: every insertion of a key probes the same slots from its home).  One
+// block of 1024 threads per compute unit holds 4096 keys in 144 KiB of LDS.
+// The histogram is in LDS, added once per block.  The loop runs in steps of
+// one wave over 64 consecutive pairs, so that the histogram and the
+// per-parent sums are combined across the wave first: one LDS add per
+// distinct bit width and one global add per run of lanes with the same parent
+// (the phases of one parent step are consecutive, so a wave holds one or two
+// parents, where an add per lane would queue 64 atomics on one address).
+constexpr uint32_t kHoSlots = 4096;
+constexpr int kHoProbes = 16;
+constexpr uint32_t kHoThreads = 1024;
+constexpr uint32_t kHoHashShift = 20;  // 32 - log2(kHoSlots)
+constexpr uint32_t kHoMaxDumps = 256;  // pair blocks at most: one per compute unit
 
-__global__ __launch_bounds__(kScThreads) void k_ho_pairs(HandoffArgs a) {
+__device__ __forceinline__ uint32_t ho_hash(uint32_t key) { return key * 2654435761u; }
+
+__global__ __launch_bounds__(kHoThreads) void k_ho_pairs(HandoffArgs a) {
   __shared__ unsigned long long s_hist[65];
   __shared__ uint32_t s_key[kHoSlots];                // 1 + rx * R + ry; 0: empty
   __shared__ unsigned long long s_v[4][kHoSlots];      // count, sum, min, max
-  for (int i = threadIdx.x; i < 65; i += kScThreads) s_hist[i] = 0;
-  for (uint32_t i = threadIdx.x; i < kHoSlots; i += kScThreads) {
+  for (int i = threadIdx.x; i < 65; i += kHoThreads) s_hist[i] = 0;
+  for (uint32_t i = threadIdx.x; i < kHoSlots; i += kHoThreads) {
     s_key[i] = 0;
     s_v[0][i] = 0;
     s_v[1][i] = 0;
@@ -1354,56 +1368,93 @@ __global__ __launch_bounds__(kScThreads) void k_ho_pairs(HandoffArgs a) {
   const uint64_t n = ho_count(a);
   const uint4* inst = reinterpret_cast<const uint4*>(a.inst);
   const uint64_t m = *a.mtot;
-  uint64_t* table = a.rep + (uint64_t)(blockIdx.x % a.copies) * a.R * a.R * 4;
+  const uint32_t lane = threadIdx.x & 63;
   uint64_t gaps = 0, gsum = 0;
-  for (uint64_t k = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; k + 1 < m;
-       k += (uint64_t)gridDim.x * kScThreads) {
-    const uint64_t x = a.comp[k], y = a.comp[k + 1];
-    const uint4 ya = inst[2 * y], yb = inst[2 * y + 1];
-    if (yb.z != a.L) continue;
-    const uint4 xa = inst[2 * x], xb = inst[2 * x + 1];
-    if (xb.z != a.L || xb.x != yb.x || xb.y != yb.y) continue;  // level, context, parent
-    const uint32_t rx = xb.w & 0xFFFFu, ry = yb.w & 0xFFFFu;
-    if ((xb.w >> 16) == kNoEnd || rx >= a.R || ry >= a.R) continue;
-    const uint64_t te = (uint64_t)xa.z | ((uint64_t)xa.w << 32);
-    const uint64_t tb = (uint64_t)ya.x | ((uint64_t)ya.y << 32);
-    const uint64_t gap = tb - te;
-    const uint32_t key = 1u + rx * a.R + ry;
-    uint32_t h = (key * 2654435761u) >> 22;  // 10 bits
-    int slot = -1;
-    for (int p = 0; p < kHoProbes; ++p) {
-      const uint32_t cur = __hip_atomic_load(&s_key[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-      if (cur == key) {
-        slot = (int)h;
-        break;
-      }
-      if (cur == 0) {
-        const uint32_t prev = atomicCAS(&s_key[h], 0u, key);
-        if (prev == 0u || prev == key) {
-          slot = (int)h;
-          break;
+  for (uint64_t k0 = (uint64_t)blockIdx.x * kHoThreads + (threadIdx.x & ~63u); k0 + 1 < m;
+       k0 += (uint64_t)gridDim.x * kHoThreads) {
+    const uint64_t k = k0 + lane;
+    bool ok = k + 1 < m;
+    uint64_t gap = 0;
+    uint32_t par = kNoParent;
+    if (ok) {
+      const uint64_t x = a.comp[k], y = a.comp[k + 1];
+      const uint4 ya = inst[2 * y], yb = inst[2 * y + 1];
+      ok = yb.z == a.L;
+      if (ok) {
+        const uint4 xa = inst[2 * x], xb = inst[2 * x + 1];
+        const uint32_t rx = xb.w & 0xFFFFu, ry = yb.w & 0xFFFFu;
+        ok = xb.z == a.L && xb.x == yb.x && xb.y == yb.y &&  // level, context, parent
+             (xb.w >> 16) != kNoEnd && rx < a.R && ry < a.R;
+        if (ok) {
+          const uint64_t te = (uint64_t)xa.z | ((uint64_t)xa.w << 32);
+          const uint64_t tb = (uint64_t)ya.x | ((uint64_t)ya.y << 32);
+          gap = tb - te;
+          par = yb.y;
+          const uint32_t key = 1u + rx * a.R + ry;
+          uint32_t h = ho_hash(key) >> kHoHashShift;
+          int slot = -1;
+          for (int p = 0; p < kHoProbes; ++p) {
+            const uint32_t cur = __hip_atomic_load(&s_key[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            if (cur == key) {
+              slot = (int)h;
+              break;
+            }
+            if (cur == 0) {
+              const uint32_t prev = atomicCAS(&s_key[h], 0u, key);
+              if (prev == 0u || prev == key) {
+                slot = (int)h;
+                break;
+              }
+            }
+            h = (h + 1) & (kHoSlots - 1);
+          }
+          if (slot >= 0) {
+            atomicAdd(&s_v[0][slot], 1ull);
+            atomicAdd(&s_v[1][slot], (unsigned long long)gap);
+            atomicMin(&s_v[2][slot], (unsigned long long)gap);
+            atomicMax(&s_v[3][slot], (unsigned long long)gap);
+          } else {
+            unsigned long long* row = (unsigned long long*)(a.pairs + 4 * ((uint64_t)rx * a.R + ry));
+            atomicAdd(&row[0], 1ull);
+            atomicAdd(&row[1], (unsigned long long)gap);
+            if (gap < __hip_atomic_load(&row[2], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+              atomicMin(&row[2], (unsigned long long)gap);
+            if (gap > __hip_atomic_load(&row[3], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+              atomicMax(&row[3], (unsigned long long)gap);
+          }
         }
       }
-      h = (h + 1) & (kHoSlots - 1);
     }
-    if (slot >= 0) {
-      atomicAdd(&s_v[0][slot], 1ull);
-      atomicAdd(&s_v[1][slot], (unsigned long long)gap);
-      atomicMin(&s_v[2][slot], (unsigned long long)gap);
-      atomicMax(&s_v[3][slot], (unsigned long long)gap);
-    } else {
-      unsigned long long* row = (unsigned long long*)(table + 4 * ((uint64_t)rx * a.R + ry));
-      atomicAdd(&row[0], 1ull);
-      atomicAdd(&row[1], (unsigned long long)gap);
-      if (gap < __hip_atomic_load(&row[2], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
-        atomicMin(&row[2], (unsigned long long)gap);
-      if (gap > __hip_atomic_load(&row[3], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
-        atomicMax(&row[3], (unsigned long long)gap);
+    // histogram: one leader lane per distinct bit width adds the lanes that share it
+    const uint32_t bin = ok ? bit_width64(gap) : 65u;
+    for (uint64_t pend = __ballot(ok); pend;) {
+      const uint32_t l = (uint32_t)__builtin_ctzll(pend);
+      const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)bin, (int)l);
+      const uint64_t same = __ballot(bin == b);
+      if (lane == l) atomicAdd(&s_hist[b], (unsigned long long)__popcll(same));
+      pend &= ~same;
     }
-    atomicAdd(&s_hist[bit_width64(gap)], 1ull);
-    if (a.parent_gap && yb.y != kNoParent && yb.y < n)
-      atomicAdd((unsigned long long*)&a.parent_gap[yb.y], (unsigned long long)gap);
-    gaps += 1;
+    if (a.parent_gap) {
+      // segmented inclusive scan over runs of equal parents (head flag, sum),
+      // then the last lane of each run adds the run's sum
+      const bool pc = ok && par != kNoParent && par < n;
+      const uint32_t p = pc ? par : kNoParent;
+      uint32_t f = lane_prev(p, ~p) != p;
+      uint64_t v = pc ? gap : 0;
+#pragma unroll
+      for (int d = 1; d < 64; d <<= 1) {
+        const uint64_t vu = __shfl_up(v, d);
+        const uint32_t fu = __shfl_up(f, d);
+        if (lane >= (uint32_t)d) {
+          if (!f) v += vu;
+          f |= fu;
+        }
+      }
+      const uint32_t pn = __shfl_down(p, 1);
+      if (pc && (lane == 63 || pn != p))
+        atomicAdd((unsigned long long*)&a.parent_gap[p], (unsigned long long)v);
+    }
+    gaps += ok ? 1 : 0;
     gsum += gap;
   }
   const uint64_t g1 = rows_sum64(row_sum64(gaps)), g2 = rows_sum64(row_sum64(gsum));
@@ -1412,38 +1463,96 @@ __global__ __launch_bounds__(kScThreads) void k_ho_pairs(HandoffArgs a) {
     if (g2) atomicAdd((unsigned long long*)&a.counters[ARGUS_HO_GAP_SUM], (unsigned long long)g2);
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < 65; i += kScThreads)
+  for (int i = threadIdx.x; i < 65; i += kHoThreads)
     if (s_hist[i]) atomicAdd((unsigned long long*)&a.hist[i], s_hist[i]);
-  for (uint32_t i = threadIdx.x; i < kHoSlots; i += kScThreads) {
+  uint32_t* dk = a.dkey + (uint64_t)blockIdx.x * kHoSlots;
+  ulonglong2* dv = reinterpret_cast<ulonglong2*>(a.dval + (uint64_t)blockIdx.x * kHoSlots * 4);
+  for (uint32_t i = threadIdx.x; i < kHoSlots; i += kHoThreads) {
     const uint32_t key = s_key[i];
-    if (!key) continue;
-    unsigned long long* row = (unsigned long long*)(table + 4 * (uint64_t)(key - 1u));
-    atomicAdd(&row[0], s_v[0][i]);
-    atomicAdd(&row[1], s_v[1][i]);
-    atomicMin(&row[2], s_v[2][i]);
-    atomicMax(&row[3], s_v[3][i]);
+    dk[i] = key;
+    if (key) {
+      dv[2 * i] = make_ulonglong2(s_v[0][i], s_v[1][i]);
+      dv[2 * i + 1] = make_ulonglong2(s_v[2][i], s_v[3][i]);
+    }
   }
 }
 
-// The copies combined into the output table.
-__global__ __launch_bounds__(kScThreads) void k_ho_combine(HandoffArgs a) {
-  const uint64_t np = (uint64_t)a.R * a.R;
-  const uint64_t csz = np * 4;
-  for (uint64_t i = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; i < np;
-       i += (uint64_t)gridDim.x * kScThreads) {
-    uint64_t c = 0, sum = 0, mn = kU64Max, mx = 0;
-    for (uint32_t k = 0; k < a.copies; ++k) {
-      const uint64_t* e = a.rep + k * csz + 4 * i;
-      c += e[0];
-      sum += e[1];
-      mn = e[2] < mn ? e[2] : mn;
-      mx = e[3] > mx ? e[3] : mx;
+// The dumps merged.  Block j owns the keys whose home slot lies in
+// [j kHoSpan, (j + 1) kHoSpan): in every dump such a key sits less than
+// kHoProbes slots after its home, so the block reads that window of each dump
+// (kHoWin lanes per dump, several dumps at a time), adds the entries it owns
+// in an LDS table and then into their output rows, which no other block
+// writes (keys that overflowed there are never in a dump; keys that overflow
+// the merge table are added with atomics).
+constexpr uint32_t kHoSpan = 16;
+constexpr uint32_t kHoWin = 32;  // lanes per dump: kHoSpan + kHoProbes - 1 of them read
+constexpr uint32_t kMgSlots = 1024;
+constexpr int kMgProbes = 16;
+static_assert(kHoSpan + kHoProbes - 1 <= kHoWin && kHoSlots % kHoSpan == 0, "merge window");
+
+__global__ __launch_bounds__(kScThreads) void k_ho_merge(HandoffArgs a) {
+  __shared__ uint32_t s_key[kMgSlots];
+  __shared__ unsigned long long s_v[4][kMgSlots];
+  for (uint32_t i = threadIdx.x; i < kMgSlots; i += kScThreads) {
+    s_key[i] = 0;
+    s_v[0][i] = 0;
+    s_v[1][i] = 0;
+    s_v[2][i] = ~0ull;
+    s_v[3][i] = 0;
+  }
+  __syncthreads();
+  const uint32_t lo = blockIdx.x * kHoSpan;
+  const uint32_t o = threadIdx.x % kHoWin;
+  const uint32_t slot = (lo + o) & (kHoSlots - 1);
+  if (o < kHoSpan + kHoProbes - 1) {
+    for (uint32_t d = threadIdx.x / kHoWin; d < a.dumps; d += kScThreads / kHoWin) {
+      const uint64_t e = (uint64_t)d * kHoSlots + slot;
+      const uint32_t key = a.dkey[e];
+      if (!key) continue;
+      const uint32_t hk = ho_hash(key), home = hk >> kHoHashShift;
+      if (home < lo || home >= lo + kHoSpan) continue;
+      const ulonglong2* v = reinterpret_cast<const ulonglong2*>(a.dval + 4 * e);
+      const ulonglong2 cs = v[0], mm = v[1];
+      uint32_t h = (hk >> 10) & (kMgSlots - 1);  // the bits below the home slot's
+      int at = -1;
+      for (int p = 0; p < kMgProbes; ++p) {
+        const uint32_t cur = __hip_atomic_load(&s_key[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (cur == key) {
+          at = (int)h;
+          break;
+        }
+        if (cur == 0) {
+          const uint32_t prev = atomicCAS(&s_key[h], 0u, key);
+          if (prev == 0u || prev == key) {
+            at = (int)h;
+            break;
+          }
+        }
+        h = (h + 1) & (kMgSlots - 1);
+      }
+      if (at >= 0) {
+        atomicAdd(&s_v[0][at], cs.x);
+        atomicAdd(&s_v[1][at], cs.y);
+        atomicMin(&s_v[2][at], mm.x);
+        atomicMax(&s_v[3][at], mm.y);
+      } else {
+        unsigned long long* row = (unsigned long long*)(a.pairs + 4 * (uint64_t)(key - 1u));
+        atomicAdd(&row[0], cs.x);
+        atomicAdd(&row[1], cs.y);
+        atomicMin(&row[2], mm.x);
+        atomicMax(&row[3], mm.y);
+      }
     }
-    uint64_t* o = a.pairs + 4 * i;
-    o[0] = c;
-    o[1] = sum;
-    o[2] = mn;
-    o[3] = mx;
+  }
+  __syncthreads();
+  for (uint32_t i = threadIdx.x; i < kMgSlots; i += kScThreads) {
+    const uint32_t key = s_key[i];
+    if (!key) continue;
+    uint64_t* row = a.pairs + 4 * (uint64_t)(key - 1u);
+    row[0] += s_v[0][i];
+    row[1] += s_v[1][i];
+    row[2] = s_v[2][i] < row[2] ? s_v[2][i] : row[2];
+    row[3] = s_v[3][i] > row[3] ? s_v[3][i] : row[3];
   }
 }
 
@@ -1776,16 +1885,8 @@ extern "C" int argus_attr_probes(const argus_probes_config* cfg, const argus_pro
 
 namespace {
 
-// Copies of the pair table: up to 8, within 256 MiB.
-uint32_t ho_copies(uint32_t R) {
-  const uint64_t table = (uint64_t)R * R * 4 * sizeof(uint64_t);
-  uint64_t c = (256ull << 20) / table;
-  if (c > 8) c = 8;
-  return c < 1 ? 1u : (uint32_t)c;
-}
-
 struct HoLayout {
-  size_t comp, status, tctr, mtot, rep, total;
+  size_t comp, status, tctr, mtot, dkey, dval, total;
 };
 HoLayout ho_layout(uint64_t max_instances, uint32_t R) {
   Carver c;
@@ -1795,7 +1896,8 @@ HoLayout ho_layout(uint64_t max_instances, uint32_t R) {
   L.status = c.take(sizeof(uint64_t) * tiles_for(m));
   L.tctr = c.take(sizeof(uint32_t));
   L.mtot = c.take(sizeof(uint64_t));
-  L.rep = c.take(sizeof(uint64_t) * 4 * (uint64_t)R * R * ho_copies(R));
+  L.dkey = c.take(sizeof(uint32_t) * (uint64_t)kHoMaxDumps * kHoSlots);
+  L.dval = c.take(sizeof(uint64_t) * 4 * (uint64_t)kHoMaxDumps * kHoSlots);
   L.total = c.o;
   return L;
 }
@@ -1838,15 +1940,15 @@ extern "C" int argus_attr_handoffs(const argus_handoffs_config* cfg, const argus
   a.status = (uint64_t*)(base + HL.status);
   a.tctr = (uint32_t*)(base + HL.tctr);
   a.mtot = (uint64_t*)(base + HL.mtot);
-  a.rep = (uint64_t*)(base + HL.rep);
-  a.copies = ho_copies(cfg->num_regions);
+  a.dkey = (uint32_t*)(base + HL.dkey);
+  a.dval = (uint64_t*)(base + HL.dval);
   a.pairs = io->d_pairs;
   a.hist = io->d_hist;
   a.parent_gap = io->d_parent_gap;
   a.counters = io->d_counters;
   hipStream_t st = (hipStream_t)stream_v;
   const uint64_t init_items =
-      std::max<uint64_t>((uint64_t)a.R * a.R * 4 * a.copies, io->max_instances);
+      std::max<uint64_t>((uint64_t)a.R * a.R * 4, io->max_instances);
   hipLaunchKernelGGL(k_ho_init, dim3(sc_grid(std::max<uint64_t>(init_items, 65), kScThreads, 4096)),
                      dim3(kScThreads), 0, st, a);
   if (io->max_instances > 0) {
@@ -1857,13 +1959,11 @@ extern "C" int argus_attr_handoffs(const argus_handoffs_config* cfg, const argus
                                                          persistent_blocks((const void*)k_ho_compact,
                                                                            kScThreads))),
                        dim3(kScThreads), 0, st, a);
-    // resident blocks only: each adds its table once
-    hipLaunchKernelGGL(k_ho_pairs,
-                       dim3((uint32_t)std::min<uint64_t>(g, persistent_blocks((const void*)k_ho_pairs,
-                                                                              kScThreads))),
-                       dim3(kScThreads), 0, st, a);
+    // resident blocks only (one per compute unit): each stores its table once
+    a.dumps = (uint32_t)std::min<uint64_t>(
+        std::min<uint64_t>(g, persistent_blocks((const void*)k_ho_pairs, kHoThreads)), kHoMaxDumps);
+    hipLaunchKernelGGL(k_ho_pairs, dim3(a.dumps), dim3(kHoThreads), 0, st, a);
+    hipLaunchKernelGGL(k_ho_merge, dim3(kHoSlots / kHoSpan), dim3(kScThreads), 0, st, a);
   }
-  hipLaunchKernelGGL(k_ho_combine, dim3(sc_grid((uint64_t)a.R * a.R, kScThreads, 4096)),
-                     dim3(kScThreads), 0, st, a);
   return hipGetLastError() == hipSuccess ? ARGUS_OK : ARGUS_E_HIP;
 }

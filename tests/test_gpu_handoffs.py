@@ -51,9 +51,10 @@ def test_hand_steps(oracle_mod):
 
 @pytest.mark.parametrize("n,n_ctx,R,tr", [(0, 2, 2, 10), (3, 1, 2, 10), (4097, 5, 7, 3000),
                                           (30001, 17, 40, 40000), (100000, 64, 300, 1 << 20),
-                                          # thousands of distinct region pairs per block: the
-                                          # per-block LDS table fills and pairs go to the global
-                                          # table directly
+                                          # millions of distinct region pairs: every block's LDS
+                                          # table fills and pairs go to the output rows directly,
+                                          # and the keys homed in one merge range across all the
+                                          # tables outnumber the merge table's slots
                                           (8000000, 16, 3000, 1 << 22)])
 def test_random(oracle_mod, n, n_ctx, R, tr):
     rng = np.random.default_rng(n + R + 5)
