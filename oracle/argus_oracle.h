@@ -8,12 +8,12 @@
  * definitions.  The product path never links, loads or calls it, and it
  * shares no header, helper, table or kernel with the GPU library.
  *
- * What it computes follows the paper's Section 3.2 (regions are delimited
- * by begin(id)/end(id) transitions; temporal traces recover region-labelled
- * intervals; a per-warp nested region-context stack decides which region
- * is innermost), Section 3.3 (the duration signal is read from a reference
- * region trace), Section 3.5 (observed fields; reports expose attribution
- * ambiguity) and Section 4.3 (compute/communication overlap).  Where the
+ * What it computes follows the paper's Section 3.2 (BEGIN and END markers
+ * bound a region; pairing them per context gives intervals labelled with
+ * their region; the open regions of a context form a stack whose top is the
+ * innermost one), Section 3.3 (durations come from a traced reference
+ * region), Section 3.5 (the fields a report holds, and how it shows that an
+ * attribution is ambiguous) and Section 4.3 (compute/communication overlap).  Where the
  * paper is silent the readings are the ones listed with each function in
  * argus_oracle.cpp.
  *

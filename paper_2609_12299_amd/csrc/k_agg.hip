@@ -1,8 +1,8 @@
 // k_agg.hip -- per-region observed statistics and ambiguity counts, and the
 // planning of the overlap events.
 //
-// Section 3.5 of the paper: duration is an observed field of a region
-// report, and reports expose attribution ambiguity.  Statistics are taken
+// Section 3.5 of the paper: a region's report holds measured durations and
+// makes ambiguous attributions visible.  Statistics are taken
 // over matched instances; unclosed, mismatched and self-nested instances are
 // counted per region.  Per-block partial results live in LDS and are flushed
 // once per block with global atomics (all integer: the result does not
