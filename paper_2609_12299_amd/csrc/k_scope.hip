@@ -662,18 +662,36 @@ __global__ __launch_bounds__(kScThreads) void k_so_local(ScopeArgs a) {
     const uint64_t base = c * kScTile;
     const uint32_t cnt = n - base < (uint64_t)kScTile ? (uint32_t)(n - base) : kScTile;
     bool bad = false;
-    uint32_t ctx[kScRounds];
+    uint32_t ctx[kScRounds], rw[kScRounds];
+    // all the chunk's loads issued before the first is used (indices clamped
+    // to the chunk's last element, cnt >= 1, instead of a branch per load),
+    // with the contexts just before the wave's first element, before the
+    // chunk and after it
+    const uint32_t e0 = w * (kScRounds * 64);
+    const uint32_t ctx_wprev = inst[2 * (base + (e0 > 0 && e0 < cnt ? e0 - 1 : 0)) + 1].x;
+    const uint32_t ctx_cprev = inst[2 * (base > 0 ? base - 1 : 0) + 1].x;
+    const uint32_t ctx_cnext = inst[2 * (base + cnt < n ? base + cnt : base) + 1].x;
 #pragma unroll
     for (int r = 0; r < kScRounds; ++r) {
       const uint32_t e = w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
-      ctx[r] = 0;
+      const uint4 h1 = inst[2 * (base + (e < cnt ? e : cnt - 1)) + 1];
+      ctx[r] = h1.x;
+      rw[r] = h1.w;
+    }
+    // keep the loaded words in registers (the compiler would otherwise
+    // reload one inside the branch that uses it, after the others)
+#pragma unroll
+    for (int r = 0; r < kScRounds; ++r) asm volatile("" : "+v"(ctx[r]), "+v"(rw[r]));
+#pragma unroll
+    for (int r = 0; r < kScRounds; ++r) {
+      const uint32_t e = w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
       if (e < cnt) {
-        const uint4 h1 = inst[2 * (base + e) + 1];
-        const uint32_t reg = h1.w & 0xFFFFu;
+        const uint32_t reg = rw[r] & 0xFFFFu;
         bad |= reg >= a.R;
-        ctx[r] = h1.x;
         s_k[0][e] = (reg << 12) | e;
-        if (e + 1 == cnt) s_lctx = h1.x;
+        if (e + 1 == cnt) s_lctx = ctx[r];
+      } else {
+        ctx[r] = 0;
       }
     }
     if (bad) sc_flag(a.counters, 2);  // regions must lie below num_regions
@@ -682,9 +700,8 @@ __global__ __launch_bounds__(kScThreads) void k_so_local(ScopeArgs a) {
     uint32_t cs[kScRounds];
     {
       // the context before the wave's first element
-      uint32_t before = 0xFFFFFFFFu;
-      const uint32_t e0 = w * (kScRounds * 64);
-      if (e0 > 0 && e0 < cnt) before = inst[2 * (base + e0 - 1) + 1].x;
+      const uint32_t before0 = e0 > 0 && e0 < cnt ? ctx_wprev : 0xFFFFFFFFu;
+      uint32_t before = before0;
       uint32_t run = 0;
 #pragma unroll
       for (int r = 0; r < kScRounds; ++r) {
@@ -714,8 +731,8 @@ __global__ __launch_bounds__(kScThreads) void k_so_local(ScopeArgs a) {
     if (tid == 0) {
       const uint32_t F = ctx[0], L = s_lctx;
       uint32_t f = F == L ? kSoWhole : 0u;
-      if (base > 0 && inst[2 * (base - 1) + 1].x == F) f |= kSoPcont;
-      if (base + cnt < n && inst[2 * (base + cnt) + 1].x == L) f |= kSoCont;
+      if (base > 0 && ctx_cprev == F) f |= kSoPcont;
+      if (base + cnt < n && ctx_cnext == L) f |= kSoCont;
       a.cflag[c] = f;
       s_flag = f;
     }
@@ -1269,12 +1286,20 @@ __global__ __launch_bounds__(kScThreads) void k_ho_compact(HandoffArgs a) {
     if (tile >= T) break;
     const uint64_t base = tile * kScTile;
     uint64_t qm[kScRounds];  // ballot of the qualifying lanes of each round
+    uint32_t lv[kScRounds];
+    // all the tile's loads issued before the first is used (indices clamped
+    // to the last instance, n >= 1 here, instead of a branch per load)
+#pragma unroll
+    for (int r = 0; r < kScRounds; ++r) {
+      const uint64_t x = base + w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
+      lv[r] = iw[8 * (x < n ? x : n - 1) + 6];
+    }
     uint32_t wc = 0;
 #pragma unroll
     for (int r = 0; r < kScRounds; ++r) {
       const uint64_t x = base + w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
       const bool in = x < n;
-      const uint32_t lvl = in ? iw[8 * x + 6] : 0u;
+      const uint32_t lvl = lv[r];
       at += in && lvl == a.L;
       qm[r] = __ballot(in && lvl <= a.L);
       wc += (uint32_t)__popcll(qm[r]);
