@@ -127,7 +127,8 @@ int argus_oracle_run(const void* records, uint64_t n, uint32_t num_regions,
  *                           (natural log; 0 when T(p) == 0)
  *   region_total   [R]      sum over p of n(r, p)
  *   mhat           [M * R]  sum over p with n(r, p) > 0 of alpha(r, p) m(p),
- *                           in increasing p; or NULL when M == 0
+ *                           in 512 strands (p mod 512, each in increasing
+ *                           p) combined by halving; or NULL when M == 0
  * Returns 0, or -1 for bad arguments. */
 enum {
   ORC_S_N_SAMPLES = 0,       /* sample records */

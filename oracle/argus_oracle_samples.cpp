@@ -25,9 +25,13 @@
 //     and is counted as "inner unmatched" (ambiguity exposed).  With no
 //     matched active instance the weight is unattributed.
 //   * Floating point: IEEE double, each alpha by one division
-//     n(r, p) / T(p); m_hat(r) adds the products alpha(r, p) * m(p) one at a
-//     time in increasing p, over the p with n(r, p) > 0, each product rounded
-//     before the addition; H(p) adds alpha log alpha in increasing r.
+//     n(r, p) / T(p); each product alpha(r, p) * m(p) rounded before it is
+//     added, over the p with n(r, p) > 0.  The paper fixes no order for the
+//     sum over p; m_hat(r) takes it in 512 strands: strand j adds, from +0
+//     and in increasing p, the products with p mod 512 = j; then the strands
+//     are combined by halving, strand j += strand j + h for j < h, with
+//     h = 256, 128, ..., 1, and m_hat(r) is strand 0.  H(p) adds
+//     alpha log alpha in increasing r.
 
 #include "argus_oracle.h"
 
@@ -166,21 +170,26 @@ extern "C" int argus_oracle_samples(const void* instances_v, uint64_t n_inst,
     }
     entropy[p] = h;
   }
-  // Per region: total count and the lifted metrics, summed in increasing p.
+  // Per region: total count and the lifted metrics, summed in the strand
+  // order stated at the top of this file.
+  const uint64_t kStrands = 512;
+  std::vector<double> strand(kStrands);
   for (uint64_t r = 0; r < R; ++r) {
     uint64_t tot = 0;
     for (uint64_t p = 0; p < P; ++p) tot += n_rp[p * R + r];
     region_total[r] = tot;
     for (uint64_t k = 0; k < M; ++k) {
-      double acc = 0.0;
+      std::fill(strand.begin(), strand.end(), 0.0);
       for (uint64_t p = 0; p < P; ++p) {
         const uint64_t n = n_rp[p * R + r];
         if (n == 0) continue;
         const double a = double(n) / double(pc_total[p]);
         const double term = a * metrics[k * P + p];
-        acc = acc + term;
+        strand[p % kStrands] = strand[p % kStrands] + term;
       }
-      mhat[k * R + r] = acc;
+      for (uint64_t h = kStrands / 2; h >= 1; h /= 2)
+        for (uint64_t j = 0; j < h; ++j) strand[j] = strand[j] + strand[j + h];
+      mhat[k * R + r] = strand[0];
     }
   }
   return 0;

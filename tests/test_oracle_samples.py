@@ -195,3 +195,23 @@ def test_invariants(oracle_mod, seed):
     assert np.all(o["entropy"] <= np.log(np.maximum(own, 1)) + 1e-12)
     assert np.all(o["entropy"] >= 0)
     assert int(c[6]) == int((o["n"] > 0).sum())
+
+
+def test_mhat_strand_order(oracle_mod):
+    """The sum over p is taken in 512 strands (p mod 512, each in increasing
+    p) combined by halving.  One region owns PCs 0, 1 and 512 of P = 513,
+    alpha = 1, metric 1e16, 1 and -1e16: strand 0 holds 1e16 + (-1e16) = 0,
+    strand 1 holds 1, so m_hat = 1 exactly; adding in increasing p would lose
+    the 1 to rounding (1e16 + 1 rounds to 1e16) and give 0.  A second metric,
+    1e16, -1e16 and 1 on PCs 0, 256 and 1, checks the halving: its first step
+    pairs strands 0 and 256 (0) before strand 1 joins (1), where pairing
+    neighbours, or adding in increasing p, meets 1e16 + 1 first and gives 0."""
+    inst = _instances(oracle_mod, [(0, 0, 0, B), (100, 0, 0, E)], 1)
+    smp = _samples([(10, 0, 0), (10, 0, 1), (10, 0, 512), (10, 0, 256)])
+    m = np.zeros((2, 513))
+    m[0, 0], m[0, 1], m[0, 512] = 1e16, 1.0, -1e16
+    m[1, 0], m[1, 256], m[1, 1] = 1e16, -1e16, 1.0
+    o = oracle_mod.samples(inst, smp, 1, 513, metrics=m)
+    assert o["alpha"][[0, 1, 256, 512], 0].tolist() == [1.0, 1.0, 1.0, 1.0]
+    assert o["mhat"][0, 0] == 1.0
+    assert o["mhat"][1, 0] == 1.0
