@@ -17,9 +17,10 @@
 // parent links give a sample's owner, the innermost matched active
 // instance.  The counts go to a dense [P][R] table with 64-bit atomics
 // (integer, so the order of the adds does not matter).  Per PC one wave
-// forms T(p), alpha, the owner count and H(p); per region one wave adds
-// alpha * m(p) in increasing p with separately rounded products: a fixed
-// rounding order, so m_hat is reproducible bit for bit.
+// forms T(p), alpha, the owner count and H(p); per region one block adds
+// the separately rounded products alpha * m(p) in a fixed order (512
+// strands by p mod 512, combined by halving), so m_hat is reproducible bit
+// for bit.
 #include <string.h>
 
 #include <mutex>
@@ -196,98 +197,115 @@ __global__ __launch_bounds__(kSampThreads) void k_s_pc(SampArgs a) {
 }
 
 // Per region r: its total count (an integer sum, in any order), and each
-// lifted metric as the products alpha(r, p) * m(p), each rounded, added one
-// at a time in increasing p over the p where region r has a count.
+// lifted metric as the products alpha(r, p) * m(p), each rounded, summed in
+// a fixed order (the paper fixes none): 512 strands, strand j adding from +0
+// and in increasing p the products with p mod 512 = j, then the strands
+// combined by halving, strand j += strand j + h for j < h, h = 256, ..., 1;
+// m_hat(r) is strand 0.  One block of 512 threads per region and pair of
+// metrics: thread j is strand j, with the loads of kLiftRounds values of p
+// issued together; the halving runs through LDS down to 64 strands, then
+// within one wave.
 //
 // alpha(r, p) is zero exactly where the count is (a non-zero count over a
-// total below 2^64 is at least 2^-64), and a running sum that starts at +0
-// never becomes -0 under round-to-nearest, so adding +0 for a p without a
-// count leaves the sum unchanged bit for bit.  Each sum can therefore walk
-// all P terms in order, with no selection across lanes: one wave per region
-// and pair of metrics gathers kLiftChunk PCs of the region's column (alpha,
-// the two metrics and, for the first pair, the counts) one chunk ahead,
-// forms the chunk's products in parallel into LDS, and lane k then adds
-// metric k's products in order.  Chunks in which the region has no count are
-// skipped (they would add only +0).
+// total below 2^64 is at least 2^-64), and a sum that starts at +0 never
+// becomes -0 under round-to-nearest, so a p without a count adds +0 and
+// leaves the strand unchanged bit for bit: strands need no selection of
+// their terms across lanes.
 constexpr uint32_t kLiftMetrics = 2;
-constexpr int kLiftBlocks = 8;                    // 64-PC blocks per chunk
-constexpr uint32_t kLiftChunk = 64 * kLiftBlocks;
-constexpr uint32_t kLiftRow = kLiftChunk + 2;     // metric rows start on different banks
+constexpr uint32_t kLiftStrands = 512;
+constexpr int kLiftRounds = 8;  // values of p per strand and load batch
 
-struct LiftChunk {
-  uint64_t n[kLiftBlocks];
-  double al[kLiftBlocks], x0[kLiftBlocks], x1[kLiftBlocks];
-};
-
-__device__ __forceinline__ void lift_load(LiftChunk& c, const SampArgs& a, uint64_t r, uint64_t p0,
-                                          bool totals, const double* m0, const double* m1,
-                                          uint32_t lane) {
-#pragma unroll
-  for (int u = 0; u < kLiftBlocks; ++u) {
-    const uint64_t p = p0 + 64u * u + lane;
-    const bool in = p < a.P;
-    c.n[u] = in && totals ? a.n[p * a.R + r] : 0ull;
-    c.al[u] = in && m0 ? a.alpha[p * a.R + r] : 0.0;
-    c.x0[u] = in && m0 ? m0[p] : 0.0;
-    c.x1[u] = in && m1 ? m1[p] : 0.0;
-  }
-}
-
-__global__ __launch_bounds__(64) void k_s_region(SampArgs a) {
-  __shared__ double s_prod[kLiftMetrics][kLiftRow];
-  const uint64_t r = blockIdx.x;
-  const uint32_t lane = threadIdx.x;
+__global__ __launch_bounds__(kLiftStrands) void k_s_region(SampArgs a) {
+  __shared__ double s_acc[kLiftMetrics][kLiftStrands];
+  __shared__ uint64_t s_tot[kLiftStrands / 64];
+  // Blocks go to the 8 XCDs round-robin; the regions of one XCD are made
+  // consecutive, so that the column lines they share (8 regions per 64-byte
+  // line of n and alpha) come through that XCD's L2 once.
+  const uint32_t per = (a.R + 7) / 8;
+  const uint64_t r = (uint64_t)(blockIdx.x % 8) * per + blockIdx.x / 8;
+  if (r >= a.R) return;  // the whole block, before any barrier
+  const uint32_t j = threadIdx.x, lane = j & 63, w = j >> 6;
   const bool totals = blockIdx.y == 0;
   const uint32_t k0 = blockIdx.y * kLiftMetrics;
   const uint32_t mk = a.M > k0 ? (a.M - k0 < kLiftMetrics ? a.M - k0 : kLiftMetrics) : 0u;
   const double* m0 = mk > 0 ? a.metrics + (uint64_t)k0 * a.P : nullptr;
   const double* m1 = mk > 1 ? a.metrics + (uint64_t)(k0 + 1) * a.P : nullptr;
-  const double* row = s_prod[lane < kLiftMetrics ? lane : 0];
   uint64_t tot = 0;
-  double acc = 0.0;
-  LiftChunk cur, nxt;
-  lift_load(cur, a, r, 0, totals, m0, m1, lane);
-  for (uint64_t p0 = 0; p0 < a.P; p0 += kLiftChunk) {
-    if (p0 + kLiftChunk < a.P) lift_load(nxt, a, r, p0 + kLiftChunk, totals, m0, m1, lane);
-    bool any = false;
+  double acc0 = 0.0, acc1 = 0.0;
+  for (uint64_t p0 = 0; p0 < a.P; p0 += (uint64_t)kLiftStrands * kLiftRounds) {
+    uint64_t nv[kLiftRounds];
+    double al[kLiftRounds], x0[kLiftRounds], x1[kLiftRounds];
+    // indices clamped to P - 1 (the values of p >= P are dropped below),
+    // each array's loads in one block so that they go out together
+    if (totals) {
 #pragma unroll
-    for (int u = 0; u < kLiftBlocks; ++u) {
-      tot += cur.n[u];
-      any |= cur.al[u] != 0.0;
-    }
-    if (mk > 0 && __ballot(any)) {
-#pragma unroll
-      for (int u = 0; u < kLiftBlocks; ++u) {
-        const bool has = cur.al[u] != 0.0;
-        s_prod[0][64 * u + lane] = has ? cur.al[u] * cur.x0[u] : 0.0;
-        s_prod[1][64 * u + lane] = has ? cur.al[u] * cur.x1[u] : 0.0;
+      for (int u = 0; u < kLiftRounds; ++u) {
+        const uint64_t p = p0 + (uint64_t)kLiftStrands * u + j;
+        nv[u] = a.n[(p < a.P ? p : a.P - 1) * a.R + r];
       }
-      __syncthreads();
-      // in order, 32 products at a time, the next 32 read from LDS while
-      // these are added
-      double b0[32], b1[32];
-#pragma unroll
-      for (int q = 0; q < 32; ++q) b0[q] = row[q];
-      for (uint32_t j = 0; j < kLiftChunk; j += 64) {
-#pragma unroll
-        for (int q = 0; q < 32; ++q) b1[q] = row[j + 32 + q];
-#pragma unroll
-        for (int q = 0; q < 32; ++q) acc = acc + b0[q];
-        if (j + 64 < kLiftChunk) {
-#pragma unroll
-          for (int q = 0; q < 32; ++q) b0[q] = row[j + 64 + q];
-        }
-#pragma unroll
-        for (int q = 0; q < 32; ++q) acc = acc + b1[q];
-      }
-      __syncthreads();
     }
-    cur = nxt;
+    if (m0) {
+#pragma unroll
+      for (int u = 0; u < kLiftRounds; ++u) {
+        const uint64_t p = p0 + (uint64_t)kLiftStrands * u + j;
+        const uint64_t pc = p < a.P ? p : a.P - 1;
+        al[u] = a.alpha[pc * a.R + r];
+        x0[u] = m0[pc];
+      }
+    }
+    if (m1) {
+#pragma unroll
+      for (int u = 0; u < kLiftRounds; ++u) {
+        const uint64_t p = p0 + (uint64_t)kLiftStrands * u + j;
+        x1[u] = m1[p < a.P ? p : a.P - 1];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kLiftRounds; ++u) {
+      const uint64_t p = p0 + (uint64_t)kLiftStrands * u + j;
+      const bool in = p < a.P;
+      if (totals) tot += in ? nv[u] : 0ull;
+      if (m0) {
+        const bool has = in && al[u] != 0.0;
+        acc0 = acc0 + (has ? al[u] * x0[u] : 0.0);
+        if (m1) acc1 = acc1 + (has ? al[u] * x1[u] : 0.0);
+      }
+    }
   }
-  if (lane < mk) a.mhat[(uint64_t)(k0 + lane) * a.R + r] = acc;
+  if (mk > 0) {
+    s_acc[0][j] = acc0;
+    s_acc[1][j] = acc1;
+  }
   if (totals) {
-    tot = rows_sum64(row_sum64(tot));
-    if (lane == 0) a.region_total[r] = tot;
+    const uint64_t t = rows_sum64(row_sum64(tot));
+    if (lane == 0) s_tot[w] = t;
+  }
+  __syncthreads();
+  if (mk > 0) {
+    for (uint32_t h = kLiftStrands / 2; h >= 64; h >>= 1) {
+      if (j < h) {
+        s_acc[0][j] = s_acc[0][j] + s_acc[0][j + h];
+        s_acc[1][j] = s_acc[1][j] + s_acc[1][j + h];
+      }
+      __syncthreads();
+    }
+    if (w == 0) {
+      double v0 = s_acc[0][lane], v1 = s_acc[1][lane];
+#pragma unroll
+      for (int h = 32; h >= 1; h >>= 1) {
+        v0 = v0 + __shfl_down(v0, h);
+        v1 = v1 + __shfl_down(v1, h);
+      }
+      if (lane == 0) {
+        a.mhat[(uint64_t)k0 * a.R + r] = v0;
+        if (mk > 1) a.mhat[(uint64_t)(k0 + 1) * a.R + r] = v1;
+      }
+    }
+  }
+  if (totals && j == 0) {
+    uint64_t t = 0;
+    for (uint32_t q = 0; q < kLiftStrands / 64; ++q) t += s_tot[q];
+    a.region_total[r] = t;
   }
 }
 
@@ -373,6 +391,7 @@ extern "C" int argus_attr_samples(const argus_samples_config* cfg, const argus_s
   hipLaunchKernelGGL(k_s_pc, dim3(grid_for(P, kSampThreads / 64, 4096)), dim3(kSampThreads), 0,
                      s, a);
   const uint32_t lift_y = M > 0 ? (uint32_t)((M + kLiftMetrics - 1) / kLiftMetrics) : 1u;
-  hipLaunchKernelGGL(k_s_region, dim3((uint32_t)R, lift_y), dim3(64), 0, s, a);
+  hipLaunchKernelGGL(k_s_region, dim3(8 * (uint32_t)((R + 7) / 8), lift_y), dim3(kLiftStrands), 0, s,
+                     a);
   return hipGetLastError() == hipSuccess ? ARGUS_OK : ARGUS_E_HIP;
 }
