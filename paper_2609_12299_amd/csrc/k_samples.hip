@@ -87,7 +87,12 @@ __global__ __launch_bounds__(kSampThreads) void k_s_join(SampArgs a) {
   const uint4* inst = reinterpret_cast<const uint4*>(a.inst);  // two uint4 per instance
   uint64_t bad = 0, wt = 0, watt = 0, wun = 0, winner = 0, wbadi = 0;
   const uint64_t stride = (uint64_t)gridDim.x * kSampThreads;
-  for (uint64_t i = (uint64_t)blockIdx.x * kSampThreads + threadIdx.x; i < a.ns; i += stride) {
+  // blocks go to the 8 XCDs round-robin: give each XCD a contiguous eighth
+  // of the block indices (when the grid divides by 8), so that neighbouring
+  // samples, whose searches end in the same lines, share one L2
+  const uint32_t G = gridDim.x;
+  const uint32_t bid = G % 8 == 0 ? (blockIdx.x % 8) * (G / 8) + blockIdx.x / 8 : blockIdx.x;
+  for (uint64_t i = (uint64_t)bid * kSampThreads + threadIdx.x; i < a.ns; i += stride) {
     const uint4 s = a.smp[i];
     const uint64_t ts = (uint64_t)s.x | ((uint64_t)s.y << 32);
     const uint32_t ctx = s.z, pc = s.w;
