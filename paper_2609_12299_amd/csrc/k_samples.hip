@@ -109,7 +109,9 @@ __global__ __launch_bounds__(kSampThreads) void k_s_join(SampArgs a) {
       const uint4 h0 = inst[2 * mid];      // t_begin, t_end
       const uint32_t c = inst[2 * mid + 1].x;  // ctx_key
       const uint64_t tb = (uint64_t)h0.x | ((uint64_t)h0.y << 32);
-      const bool gt = c > ctx || (c == ctx && tb > ts);
+      // bitwise, not short-circuit: t_begin and ctx_key are loaded together,
+      // one round trip per level instead of two
+      const bool gt = (c > ctx) | ((c == ctx) & (tb > ts));
       if (gt) hi = mid;
       else lo = mid + 1;
     }
@@ -123,6 +125,9 @@ __global__ __launch_bounds__(kSampThreads) void k_s_join(SampArgs a) {
       const uint64_t y = x - 1;
       const uint4 h0 = inst[2 * y];
       const uint4 h1 = inst[2 * y + 1];  // ctx, parent, level, region | end_region << 16
+      // every word the step uses loaded before the first test (the compiler
+      // would otherwise load each after the test before it)
+      asm volatile("" ::"v"(h0.z), "v"(h0.w), "v"(h1.x), "v"(h1.y), "v"(h1.w));
       if (h1.x != ctx) break;
       const uint64_t t_end = (uint64_t)h0.z | ((uint64_t)h0.w << 32);
       const uint32_t reg = h1.w & 0xFFFFu, ereg = h1.w >> 16;

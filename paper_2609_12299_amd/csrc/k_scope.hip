@@ -339,7 +339,9 @@ __device__ __forceinline__ uint64_t sb_lower(const uint64_t* ka, const uint64_t*
     const uint64_t mid = (lo + hi) >> 1;
     const uint64_t am = ka[mid];
     const uint32_t cm = (uint32_t)(kb[mid] >> 32);
-    const bool less = am < key || (am == key && cm < ctx);
+    // bitwise, not short-circuit: both words are loaded before either is
+    // compared, one round trip per level instead of two
+    const bool less = (am < key) | ((am == key) & (cm < ctx));
     if (less) lo = mid + 1;
     else hi = mid;
   }
@@ -1071,8 +1073,16 @@ __global__ __launch_bounds__(kScThreads) void k_pr_join(ProbeArgs a) {
       bad += 1;
     } else {
       const uint64_t tgt = sb_lower(ra, rb, nref, op, ctx) + it;
-      if (tgt < nref && ra[tgt] == op && (uint32_t)(rb[tgt] >> 32) == ctx) {
-        const uint32_t x = (uint32_t)rb[tgt];
+      // both words of the target loaded together (index clamped; nref == 0
+      // loads nothing)
+      uint64_t av = ~0ull, bv = 0;
+      if (nref) {
+        const uint64_t tc = tgt < nref ? tgt : nref - 1;
+        av = ra[tc];
+        bv = rb[tc];
+      }
+      if ((tgt < nref) & (av == op) & ((uint32_t)(bv >> 32) == ctx)) {
+        const uint32_t x = (uint32_t)bv;
         lat = te - ts;
         const uint4 ib = reinterpret_cast<const uint4*>(a.inst)[2 * (uint64_t)x];
         done = ((uint64_t)ib.x | ((uint64_t)ib.y << 32)) + lat;
