@@ -152,18 +152,50 @@ __global__ __launch_bounds__(512, 4) void k_agg(AggArgs a) {
       xs[j] = a.inst[ic];
       cs[j] = a.excl[ic];
     }
+    // Parents in earlier tiles (agg_parent's reading), the four instances'
+    // loads issued together at each of two steps: tile bounds, then the
+    // enclosing-instance entry.  A lane without such a parent reads tile 0
+    // and entry 0, which exist whenever the loop runs, and drops the value.
+    uint32_t olo[B], nop[B], opv[B];
+    bool pend[B], inr[B];
 #pragma unroll
     for (int j = 0; j < B; ++j) {
-      par[j] = agg_parent(xs[j], a.tiles, a.op_parent);
+      const uint32_t pf = xs[j].parent;
+      pend[j] = pf != kNoParent && (pf & kParentPending) != 0;
+      const uint64_t t = pend[j] ? (pf & ~kParentPending) : 0;
+      olo[j] = a.tiles[t].op_lo;
+      nop[j] = a.tiles[t].n_op;
+    }
+#pragma unroll
+    for (int j = 0; j < B; ++j) {
+      const uint32_t pf = xs[j].parent;
+      const uint64_t t = pend[j] ? (pf & ~kParentPending) : 0;
+      const uint32_t L = xs[j].level - 1;
+      inr[j] = pend[j] & (xs[j].level != 0) & (L >= olo[j]) & (L - olo[j] < nop[j]);
+      opv[j] = a.op_parent[inr[j] ? t * kMatchTile + (L - olo[j]) : 0];
+    }
+#pragma unroll
+    for (int j = 0; j < B; ++j) {
+      par[j] = !pend[j] ? xs[j].parent : (inr[j] ? opv[j] : kNoParent);
       if (par[j] != kNoParent && par[j] >= nb) {
         flag_internal_error(a.counters, 4);
         par[j] = kNoParent;
       }
     }
+    // the parents' regions and, with overlap events, the instances' classes
+    // (loaded together, before the first is used)
+    uint32_t rcl[B];
 #pragma unroll
     for (int j = 0; j < B; ++j) {
       const bool matched = xs[j].end_region_id != kNoEnd && xs[j].end_region_id == xs[j].region_id;
       preg[j] = (matched && par[j] != kNoParent) ? a.inst[par[j]].region_id : (uint16_t)kNoEnd;
+    }
+    if (a.K) {
+#pragma unroll
+      for (int j = 0; j < B; ++j) {
+        const uint32_t rg = xs[j].region_id;
+        rcl[j] = a.region_class[rg < a.R ? rg : 0u];
+      }
     }
 #pragma unroll
     for (int j = 0; j < B; ++j) {
@@ -184,7 +216,7 @@ __global__ __launch_bounds__(512, 4) void k_agg(AggArgs a) {
     if (matched) {
       n_m++;
       if (a.K) {
-        const uint32_t cls = a.region_class[region];
+        const uint32_t cls = rcl[j];
         if (cls < a.K) {
           eg = a.shift >= 32 ? 0 : (x.ctx_key >> a.shift);
           if (eg < a.G) {
