@@ -1250,19 +1250,28 @@ __global__ __launch_bounds__(256, 8) void k_tsum_codes(TsumCodeArgs a) {
     if (tile < t1) {
       const uint64_t base = tile * kMatchTile;
       const uint32_t cnt = nv - base < (uint64_t)kMatchTile ? (uint32_t)(nv - base) : (uint32_t)kMatchTile;
+      // a full tile (all but the last) loads its payloads in one batch; a
+      // choice per load would make each wait for the one before
+      uint4 u[kPerLane / 4];
+      if (cnt == kMatchTile) {
+#pragma unroll
+        for (int q = 0; q < (int)kPerLane / 4; ++q)
+          u[q] = *(const uint4*)(a.pay + base + (uint32_t)q * 256u + 4u * lane);
+      } else {
+#pragma unroll
+        for (int q = 0; q < (int)kPerLane / 4; ++q) {
+          const uint32_t r0 = (uint32_t)q * 256u + 4u * lane;
+          u[q].x = r0 < cnt ? a.pay[base + r0] : 0u;
+          u[q].y = r0 + 1 < cnt ? a.pay[base + r0 + 1] : 0u;
+          u[q].z = r0 + 2 < cnt ? a.pay[base + r0 + 2] : 0u;
+          u[q].w = r0 + 3 < cnt ? a.pay[base + r0 + 3] : 0u;
+        }
+      }
 #pragma unroll
       for (int q = 0; q < (int)kPerLane / 4; ++q) {
         const uint32_t r0 = (uint32_t)q * 256u + 4u * lane;
-        uint32_t v[4];
-        if (r0 + 4 <= cnt) {
-          const uint4 u = *(const uint4*)(a.pay + base + r0);
-          v[0] = u.x; v[1] = u.y; v[2] = u.z; v[3] = u.w;
-        } else {
-#pragma unroll
-          for (int b = 0; b < 4; ++b) v[b] = r0 + b < cnt ? a.pay[base + r0 + b] : 0u;
-        }
-        s_code[w][r0 >> 2] = (uint8_t)(code_of(v[0]) | code_of(v[1]) << 2 | code_of(v[2]) << 4 |
-                                       code_of(v[3]) << 6);
+        s_code[w][r0 >> 2] = (uint8_t)(code_of(u[q].x) | code_of(u[q].y) << 2 |
+                                       code_of(u[q].z) << 4 | code_of(u[q].w) << 6);
       }
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_wave_barrier();
