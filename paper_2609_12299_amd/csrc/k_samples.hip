@@ -164,6 +164,7 @@ __global__ __launch_bounds__(kSampThreads) void k_s_join(SampArgs a) {
 
 // One wave per PC: T(p), the owners, alpha (one rounded division each) and
 // H(p) (per-lane sums, then a fixed butterfly over the wave).
+constexpr int kPcRegs = 4;  // rows of up to 256 regions held in registers
 __global__ __launch_bounds__(kSampThreads) void k_s_pc(SampArgs a) {
   const uint64_t wave = ((uint64_t)blockIdx.x * kSampThreads + threadIdx.x) >> 6;
   const uint64_t nwaves = (uint64_t)gridDim.x * (kSampThreads / 64);
@@ -171,27 +172,58 @@ __global__ __launch_bounds__(kSampThreads) void k_s_pc(SampArgs a) {
   uint64_t pairs = 0;
   for (uint64_t p = wave; p < a.P; p += nwaves) {
     const uint64_t* row = a.n + p * a.R;
+    double* arow = a.alpha + p * a.R;
     uint64_t t = 0;
     uint32_t own = 0;
-    for (uint32_t r = lane; r < a.R; r += 64) {
-      const uint64_t v = row[r];
-      t += v;
-      own += v != 0;
-    }
-    t = rows_sum64(row_sum64(t));
-    own = rows_sum32(row_sum32(own));
-    const double td = (double)t;
     double h = 0.0;
-    double* arow = a.alpha + p * a.R;
-    for (uint32_t r = lane; r < a.R; r += 64) {
-      const uint64_t v = row[r];
-      double al = 0.0;
-      if (v) {
-        al = (double)v / td;
-        const double t_h = al * log(al);
-        h = h - t_h;
+    if (a.R <= 64 * kPcRegs) {
+      // the row in registers, its loads issued together (indices clamped to
+      // the row), read once for the total, alpha and H
+      uint64_t v[kPcRegs];
+#pragma unroll
+      for (int k = 0; k < kPcRegs; ++k) {
+        const uint32_t r = lane + 64u * k;
+        v[k] = row[r < a.R ? r : a.R - 1];
       }
-      arow[r] = al;
+#pragma unroll
+      for (int k = 0; k < kPcRegs; ++k) {
+        if (lane + 64u * k >= a.R) v[k] = 0;
+        t += v[k];
+        own += v[k] != 0;
+      }
+      t = rows_sum64(row_sum64(t));
+      own = rows_sum32(row_sum32(own));
+      const double td = (double)t;
+#pragma unroll
+      for (int k = 0; k < kPcRegs; ++k) {
+        const uint32_t r = lane + 64u * k;
+        double al = 0.0;
+        if (v[k]) {
+          al = (double)v[k] / td;
+          const double t_h = al * log(al);
+          h = h - t_h;
+        }
+        if (r < a.R) arow[r] = al;
+      }
+    } else {
+      for (uint32_t r = lane; r < a.R; r += 64) {
+        const uint64_t v = row[r];
+        t += v;
+        own += v != 0;
+      }
+      t = rows_sum64(row_sum64(t));
+      own = rows_sum32(row_sum32(own));
+      const double td = (double)t;
+      for (uint32_t r = lane; r < a.R; r += 64) {
+        const uint64_t v = row[r];
+        double al = 0.0;
+        if (v) {
+          al = (double)v / td;
+          const double t_h = al * log(al);
+          h = h - t_h;
+        }
+        arow[r] = al;
+      }
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) h = h + __shfl_xor(h, off);
