@@ -92,39 +92,18 @@ __global__ __launch_bounds__(kSampThreads) void k_s_join(SampArgs a) {
   // samples, whose searches end in the same lines, share one L2
   const uint32_t G = gridDim.x;
   const uint32_t bid = G % 8 == 0 ? (blockIdx.x % 8) * (G / 8) + blockIdx.x / 8 : blockIdx.x;
-  for (uint64_t i = (uint64_t)bid * kSampThreads + threadIdx.x; i < a.ns; i += stride) {
-    const uint4 s = a.smp[i];
-    const uint64_t ts = (uint64_t)s.x | ((uint64_t)s.y << 32);
-    const uint32_t ctx = s.z, pc = s.w;
-    const uint64_t w = a.w ? (uint64_t)a.w[i] : 1ull;
-    if (pc >= a.P) {
-      bad += 1;
-      continue;
-    }
-    wt += w;
-    // First instance whose (context, begin time) exceeds (ctx, ts).
-    uint64_t lo = 0, hi = ni;
-    while (lo < hi) {
-      const uint64_t mid = (lo + hi) >> 1;
-      const uint4 h0 = inst[2 * mid];      // t_begin, t_end
-      const uint32_t c = inst[2 * mid + 1].x;  // ctx_key
-      const uint64_t tb = (uint64_t)h0.x | ((uint64_t)h0.y << 32);
-      // bitwise, not short-circuit: t_begin and ctx_key are loaded together,
-      // one round trip per level instead of two
-      const bool gt = (c > ctx) | ((c == ctx) & (tb > ts));
-      if (gt) hi = mid;
-      else lo = mid + 1;
-    }
-    // Walk up from the last instance that began at or before ts: the active
-    // ones are its ancestors (or itself) that have not ended by ts; the
-    // first matched one among them is the owner.
+  // The owner of one sample from its search result: walk up from the last
+  // instance that began at or before ts; the active ones are its ancestors
+  // (or itself) that have not ended by ts, and the first matched one among
+  // them is the owner.
+  auto finish = [&](uint64_t lo, uint64_t ts, uint32_t ctx, uint32_t pc, uint64_t w) {
     int64_t owner_region = -1;
     bool inner = false;
     uint64_t x = lo;  // one past the candidate
     while (x > 0) {
       const uint64_t y = x - 1;
       const uint4 h0 = inst[2 * y];
-      const uint4 h1 = inst[2 * y + 1];  // ctx, parent, level, region | end_region << 16
+      const uint4 h1 = inst[2 * y + 1];
       // every word the step uses loaded before the first test (the compiler
       // would otherwise load each after the test before it)
       asm volatile("" ::"v"(h0.z), "v"(h0.w), "v"(h1.x), "v"(h1.y), "v"(h1.w));
@@ -146,12 +125,56 @@ __global__ __launch_bounds__(kSampThreads) void k_s_join(SampArgs a) {
     if (owner_region < 0) {
       if (owner_region == -2) wbadi += w;
       else wun += w;
-      continue;
+      return;
     }
     watt += w;
     if (inner) winner += w;
     atomicAdd((unsigned long long*)&a.n[(uint64_t)pc * a.R + (uint64_t)owner_region],
               (unsigned long long)w);
+  };
+  // Two samples per thread (i and i + stride), their searches in lockstep:
+  // each search is a chain of dependent loads, and two chains per lane keep
+  // twice the requests in flight.  The search finds the first instance whose
+  // (context, begin time) exceeds the sample's; the key is compared with
+  // bitwise operators, so that a level's two loads go out together.
+  for (uint64_t i = (uint64_t)bid * kSampThreads + threadIdx.x; i < a.ns; i += 2 * stride) {
+    const uint64_t i1 = i + stride;
+    const bool has1 = i1 < a.ns;
+    const uint4 s0 = a.smp[i], s1 = a.smp[has1 ? i1 : i];
+    const uint64_t ts0 = (uint64_t)s0.x | ((uint64_t)s0.y << 32);
+    const uint64_t ts1 = (uint64_t)s1.x | ((uint64_t)s1.y << 32);
+    const uint32_t ctx0 = s0.z, pc0 = s0.w, ctx1 = s1.z, pc1 = s1.w;
+    const uint64_t w0 = a.w ? (uint64_t)a.w[i] : 1ull;
+    const uint64_t w1 = a.w ? (uint64_t)a.w[has1 ? i1 : i] : 1ull;
+    const bool ok0 = pc0 < a.P, ok1 = has1 && pc1 < a.P;
+    if (ok0) wt += w0;
+    else bad += 1;
+    if (has1) {
+      if (ok1) wt += w1;
+      else bad += 1;
+    }
+    uint64_t lo0 = 0, hi0 = ok0 ? ni : 0, lo1 = 0, hi1 = ok1 ? ni : 0;
+    while ((lo0 < hi0) | (lo1 < hi1)) {
+      const bool a0 = lo0 < hi0, a1 = lo1 < hi1;
+      const uint64_t m0 = (lo0 + hi0) >> 1, m1 = (lo1 + hi1) >> 1;
+      const uint64_t q0 = a0 ? m0 : 0, q1 = a1 ? m1 : 0;  // a finished chain reads instance 0
+      const uint4 g0 = inst[2 * q0], g1 = inst[2 * q1];
+      const uint32_t c0 = inst[2 * q0 + 1].x, c1 = inst[2 * q1 + 1].x;
+      const uint64_t tb0 = (uint64_t)g0.x | ((uint64_t)g0.y << 32);
+      const uint64_t tb1 = (uint64_t)g1.x | ((uint64_t)g1.y << 32);
+      const bool gt0 = (c0 > ctx0) | ((c0 == ctx0) & (tb0 > ts0));
+      const bool gt1 = (c1 > ctx1) | ((c1 == ctx1) & (tb1 > ts1));
+      if (a0) {
+        if (gt0) hi0 = m0;
+        else lo0 = m0 + 1;
+      }
+      if (a1) {
+        if (gt1) hi1 = m1;
+        else lo1 = m1 + 1;
+      }
+    }
+    if (ok0) finish(lo0, ts0, ctx0, pc0, w0);
+    if (ok1) finish(lo1, ts1, ctx1, pc1, w1);
   }
   block_add(bad, &a.counters[ARGUS_S_N_BAD_PC], s_part);
   block_add(wt, &a.counters[ARGUS_S_W_TOTAL], s_part);
