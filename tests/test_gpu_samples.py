@@ -99,6 +99,22 @@ def test_random_malformed(oracle_mod, n, ns, n_ctx, R, P, tr):
     assert_samples_parity(g, o, f"random n={n}")
 
 
+def test_no_metrics_many_pcs(oracle_mod):
+    """No PC metrics (M = 0): counts, alpha, entropy and region totals only,
+    over 5000 PCs (more than one load batch of the 512 lifting strands)."""
+    rng = np.random.default_rng(77)
+    n, n_ctx, R, P, tr, ns = 20000, 8, 7, 5000, 30000, 40000
+    rec = random_malformed(rng, n, n_ctx, R, tr)
+    from paper_2609_12299_amd import SAMPLE_DTYPE
+    smp = np.zeros(ns, SAMPLE_DTYPE)
+    smp["ts"] = rng.integers(0, tr + 5, size=ns)
+    smp["ctx_key"] = rng.integers(0, n_ctx + 1, size=ns)
+    smp["pc"] = rng.integers(0, P, size=ns)
+    log(f"[gpu] samples without metrics: n={n} samples={ns} R={R} P={P}")
+    g, o = run_both(oracle_mod, rec, R, smp, P)
+    assert_samples_parity(g, o, "no metrics")
+
+
 @pytest.mark.parametrize("cfg,blocks,size,ns,P", [(2, 16, 4096, 1 << 18, 4096),
                                                   (3, 16, 8192, 1 << 19, 20000),
                                                   (5, 0, 1 << 20, 1 << 19, 8192)])
