@@ -571,227 +571,115 @@ __device__ __forceinline__ uint32_t wave_incl_max32(uint32_t v) {
   return v;
 }
 
-// One stable LDS pass of a chunk's keys (region << 12 | element) on the
-// `bits`-bit digit at `shift`: each wave ranks its 1024 consecutive keys
-// with one ballot per digit bit per round of 64, then the digit offsets of
-// the waves come from one scan over the 256 digits (a wave scan each, the
-// four wave totals through LDS).  `cw` holds this pass's per-wave digit
-// counts (cleared beforehand); `nw` is cleared here for the next pass.
-__device__ __forceinline__ void so_pass(const uint32_t* src, uint32_t* dst, uint32_t cnt, int shift,
-                                        int bits, uint32_t (*cw)[256], uint32_t (*nw)[256],
-                                        uint32_t* s_lstart, uint32_t* s_w) {
-  const uint32_t tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
-  const uint64_t lt = lanemask_lt();
-  const uint32_t dmask = (1u << bits) - 1u;
-  uint32_t key[kScRounds], rk[kScRounds];
-#pragma unroll
-  for (int r = 0; r < kScRounds; ++r) {
-    const uint32_t p = w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
-    const bool valid = p < cnt;
-    key[r] = valid ? src[p] : 0u;
-    const uint32_t d = (key[r] >> shift) & dmask;
-    uint64_t peers = __ballot(valid);
-#pragma unroll 8
-    for (int bit = 0; bit < bits; ++bit) {
-      const uint64_t bal = __ballot((d >> bit) & 1u);
-      peers &= ((d >> bit) & 1u) ? bal : ~bal;
-    }
-    uint32_t rank = 0xFFFFFFFFu;
-    if (valid) {
-      const uint32_t old = cw[w][d];
-      rank = old + (uint32_t)__popcll(peers & lt);
-      __builtin_amdgcn_wave_barrier();
-      if ((peers >> lane) == 1ull) cw[w][d] = old + (uint32_t)__popcll(peers);
-    }
-    __builtin_amdgcn_wave_barrier();
-    rk[r] = rank;
-  }
-#pragma unroll
-  for (int q = 0; q < 4; ++q) nw[q][tid] = 0;
-  __syncthreads();
-  // thread tid owns digit tid: the waves' offsets within it, then where the
-  // digit starts in the chunk
-  uint32_t c = 0;
-#pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const uint32_t v = cw[q][tid];
-    cw[q][tid] = c;
-    c += v;
-  }
-  const uint32_t inc = (uint32_t)wave_incl_scan32((int32_t)c);
-  if (lane == 63) s_w[w] = inc;
-  __syncthreads();
-  uint32_t pre = 0;
-  for (uint32_t q = 0; q < w; ++q) pre += s_w[q];
-  s_lstart[tid] = pre + inc - c;
-  __syncthreads();
-#pragma unroll
-  for (int r = 0; r < kScRounds; ++r) {
-    if (rk[r] == 0xFFFFFFFFu) continue;
-    const uint32_t d = (key[r] >> shift) & dmask;
-    const uint32_t slot = s_lstart[d] + cw[w][d] + rk[r];
-    if (slot < kScTile) dst[slot] = key[r];
-  }
-  __syncthreads();
-}
-
 // Ordinals of one chunk of 4096 consecutive instances, exact except for the
 // context that entered the chunk from earlier ones (those are written with
 // kSoPending and completed in k_sc_stats), and, when the chunk's last
 // context continues into the next chunk, that context's counts per region.
-// The chunk is sorted stably by region in LDS; a (region, context) run's
-// elements then lie together in canonical order, and an element's local
-// ordinal is its distance from its run's start (a wave max-scan of the run
-// heads).
+// One wave per chunk walks it in order, 64 elements per round.  An element's
+// local ordinal is the count its (context, region) reached before the round,
+// kept per region in the wave's LDS row, plus its rank among the lanes of
+// the round with the same context and region (contexts are contiguous, so
+// the lanes of one context form a range; the region by one ballot per
+// region bit).  A counter keeps the chunk position where its context starts
+// beside the count, so a context that starts inside the chunk counts from
+// zero.  The loads of kSoBatch rounds are issued together.
+constexpr int kSoBatch = 16;
+
 __global__ __launch_bounds__(kScThreads) void k_so_local(ScopeArgs a) {
-  __shared__ uint32_t s_k[2][kScTile];   // keys in sort order; then local ordinals by element
-  // each element's context, as the chunk position where that context starts
-  // (contexts are contiguous in canonical order)
-  __shared__ uint16_t s_seg[kScTile];
-  __shared__ uint32_t s_wave[2][4][256];  // per-wave digit counts of the two passes
-  __shared__ uint32_t s_lstart[256];
-  __shared__ uint32_t s_w[kScThreads / 64];
-  __shared__ uint32_t s_wl[kScThreads / 64];
-  __shared__ uint32_t s_flag, s_lctx;
+  extern __shared__ uint32_t so_cnt[];  // [4 waves][R]: context start << 16 | count
   const uint64_t n = sb_count(a.s);
   const uint4* inst = reinterpret_cast<const uint4*>(a.inst);
-  const uint32_t tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
-  // digit widths of the region (12 + region bits of the key)
+  const uint32_t w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  uint32_t* cr = so_cnt + (uint64_t)w * a.R;
   const uint32_t rbits = a.R > 1 ? 32u - (uint32_t)__clz(a.R - 1) : 1u;
-  const int passes = rbits > 8 ? 2 : 1;
-  const int bits0 = rbits > 8 ? 8 : (int)rbits, bits1 = rbits > 8 ? (int)rbits - 8 : 0;
-  for (uint64_t c = blockIdx.x; c * kScTile < n; c += gridDim.x) {
+  const uint64_t lt = lanemask_lt();
+  const uint64_t above = lane == 63 ? 0ull : (~0ull << (lane + 1));  // lanes after this one
+  const uint64_t chunks = (n + kScTile - 1) / kScTile;
+  bool bad = false;
+  for (uint64_t c = (uint64_t)blockIdx.x * 4 + w; c < chunks; c += (uint64_t)gridDim.x * 4) {
     const uint64_t base = c * kScTile;
     const uint32_t cnt = n - base < (uint64_t)kScTile ? (uint32_t)(n - base) : kScTile;
-    bool bad = false;
-    uint32_t ctx[kScRounds], rw[kScRounds];
-    // all the chunk's loads issued before the first is used (indices clamped
-    // to the chunk's last element, cnt >= 1, instead of a branch per load),
-    // with the contexts just before the wave's first element, before the
-    // chunk and after it
-    const uint32_t e0 = w * (kScRounds * 64);
-    const uint32_t ctx_wprev = inst[2 * (base + (e0 > 0 && e0 < cnt ? e0 - 1 : 0)) + 1].x;
-    const uint32_t ctx_cprev = inst[2 * (base > 0 ? base - 1 : 0) + 1].x;
-    const uint32_t ctx_cnext = inst[2 * (base + cnt < n ? base + cnt : base) + 1].x;
+    // the chunk's first and last contexts and their neighbours outside it
+    const uint32_t F = inst[2 * base + 1].x, L = inst[2 * (base + cnt - 1) + 1].x;
+    const uint32_t ctx_before = inst[2 * (base > 0 ? base - 1 : 0) + 1].x;
+    const uint32_t ctx_after = inst[2 * (base + cnt < n ? base + cnt : base) + 1].x;
+    uint32_t f = F == L ? kSoWhole : 0u;
+    if (base > 0 && ctx_before == F) f |= kSoPcont;
+    if (base + cnt < n && ctx_after == L) f |= kSoCont;
+    if (lane == 0) a.cflag[c] = f;
+    for (uint32_t r = lane; r < a.R; r += 64) cr[r] = 0;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    uint32_t seg1 = 0;  // 1 + the context start of the element before the round
+    uint32_t pctx = F;  // the context of that element (the first element starts one anyway)
+    for (uint32_t b0 = 0; b0 < cnt; b0 += 64u * kSoBatch) {
+      uint32_t cx[kSoBatch], rw[kSoBatch];
 #pragma unroll
-    for (int r = 0; r < kScRounds; ++r) {
-      const uint32_t e = w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
-      const uint4 h1 = inst[2 * (base + (e < cnt ? e : cnt - 1)) + 1];
-      ctx[r] = h1.x;
-      rw[r] = h1.w;
-    }
-    // keep the loaded words in registers (the compiler would otherwise
-    // reload one inside the branch that uses it, after the others)
-#pragma unroll
-    for (int r = 0; r < kScRounds; ++r) asm volatile("" : "+v"(ctx[r]), "+v"(rw[r]));
-#pragma unroll
-    for (int r = 0; r < kScRounds; ++r) {
-      const uint32_t e = w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
-      if (e < cnt) {
-        const uint32_t reg = rw[r] & 0xFFFFu;
-        bad |= reg >= a.R;
-        s_k[0][e] = (reg << 12) | e;
-        if (e + 1 == cnt) s_lctx = ctx[r];
-      } else {
-        ctx[r] = 0;
+      for (int k = 0; k < kSoBatch; ++k) {
+        const uint32_t e = b0 + 64u * k + lane;
+        const uint4 h1 = inst[2 * (base + (e < cnt ? e : cnt - 1)) + 1];
+        cx[k] = h1.x;
+        rw[k] = h1.w;
       }
-    }
-    if (bad) sc_flag(a.counters, 2);  // regions must lie below num_regions
-    // context starts: 1 + the last start at or before each element within the
-    // wave (0: the context began before the wave's first element)
-    uint32_t cs[kScRounds];
-    {
-      // the context before the wave's first element
-      const uint32_t before0 = e0 > 0 && e0 < cnt ? ctx_wprev : 0xFFFFFFFFu;
-      uint32_t before = before0;
-      uint32_t run = 0;
 #pragma unroll
-      for (int r = 0; r < kScRounds; ++r) {
-        const uint32_t e = w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
-        const uint32_t prev = lane_prev(ctx[r], before);
-        before = (uint32_t)__builtin_amdgcn_readlane((int)ctx[r], 63);
-        const bool head = e < cnt && (e == 0 || prev != ctx[r]);
+      for (int k = 0; k < kSoBatch; ++k) {
+        const uint32_t r0 = b0 + 64u * k;  // the round's first element
+        if (r0 >= cnt) break;
+        const uint32_t e = r0 + lane;
+        const bool in = e < cnt;
+        const uint32_t ctx = cx[k], reg = rw[k] & 0xFFFFu;
+        bad |= in && reg >= a.R;
+        const bool ok = in && reg < a.R;
+        const bool head = in && (e == 0 || lane_prev(ctx, pctx) != ctx);
         uint32_t x = wave_incl_max32(head ? e + 1 : 0u);
-        x = x > run ? x : run;
-        run = (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
-        cs[r] = x;
+        x = x > seg1 ? x : seg1;
+        const uint32_t seg = x - 1u;  // where this element's context starts in the chunk
+        seg1 = (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
+        pctx = (uint32_t)__builtin_amdgcn_readlane((int)ctx, 63);
+        // the lanes of this context in the round, then those of this region
+        const uint64_t nxt = __ballot(head) & above;
+        const uint32_t hi = nxt ? (uint32_t)__builtin_ctzll(nxt) : 64u;
+        const uint32_t lo = seg > r0 ? seg - r0 : 0u;
+        uint64_t peers = __ballot(ok) & (hi == 64u ? ~0ull : ((1ull << hi) - 1ull)) & (~0ull << lo);
+        for (uint32_t bit = 0; bit < rbits; ++bit) {
+          const bool set = (reg >> bit) & 1u;
+          const uint64_t bal = __ballot(set);
+          peers &= set ? bal : ~bal;
+        }
+        const uint32_t rc = ok ? reg : 0u;
+        const uint32_t ent = ok ? cr[rc] : 0u;
+        const uint32_t prior = (ent >> 16) == seg ? (ent & 0xFFFFu) : 0u;
+        const uint32_t local = ok ? prior + (uint32_t)__popcll(peers & lt) : 0u;
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        // the last lane of each (context, region) group carries its count on
+        if (ok && (peers >> lane) == 1ull) cr[rc] = (seg << 16) | (prior + (uint32_t)__popcll(peers));
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        if (in) {
+          // the chunk's first context starts at position 0
+          const bool pending = (f & kSoPcont) && seg == 0;
+          a.ordinal[base + e] = pending ? (kSoPending | local) : local;
+        }
       }
-      if (lane == 0) s_wl[w] = run;
     }
-#pragma unroll
-    for (int q = 0; q < 4; ++q) s_wave[0][q][tid] = 0;
-    __syncthreads();
-    {
-      uint32_t enter = 0;
-      for (uint32_t q = 0; q < w; ++q) enter = s_wl[q] > enter ? s_wl[q] : enter;
-#pragma unroll
-      for (int r = 0; r < kScRounds; ++r) {
-        const uint32_t e = w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
-        if (e < cnt) s_seg[e] = (uint16_t)((cs[r] > enter ? cs[r] : enter) - 1u);
+    if (f & kSoCont) {
+      // the last context's counts (its start: the last element's)
+      const uint32_t ls = seg1 - 1u;
+      uint32_t* tail = a.tail + c * (uint64_t)a.R;
+      for (uint32_t r = lane; r < a.R; r += 64) {
+        const uint32_t ent = cr[r];
+        tail[r] = (ent >> 16) == ls ? (ent & 0xFFFFu) : 0u;
       }
     }
-    if (tid == 0) {
-      const uint32_t F = ctx[0], L = s_lctx;
-      uint32_t f = F == L ? kSoWhole : 0u;
-      if (base > 0 && ctx_cprev == F) f |= kSoPcont;
-      if (base + cnt < n && ctx_cnext == L) f |= kSoCont;
-      a.cflag[c] = f;
-      s_flag = f;
-    }
-    so_pass(s_k[0], s_k[1], cnt, 12, bits0, s_wave[0], s_wave[1], s_lstart, s_w);
-    if (passes > 1) so_pass(s_k[1], s_k[0], cnt, 20, bits1, s_wave[1], s_wave[0], s_lstart, s_w);
-    const int cur = passes > 1 ? 0 : 1;
-    const uint32_t* sk = s_k[cur];
-    uint32_t* s_ord = s_k[cur ^ 1];  // local ordinal of each element (the other buffer is free)
-    const uint32_t flag = s_flag;
-    const uint32_t L = s_seg[cnt - 1];
-    uint32_t* tail = a.tail + c * (uint64_t)a.R;
-    if (flag & kSoCont)
-      for (uint32_t r = tid; r < a.R; r += kScThreads) tail[r] = 0;
-    // run heads: a position whose (region, context) differs from the one before
-    auto same_run = [&](uint32_t k0, uint32_t k1) {
-      return (k0 >> 12) == (k1 >> 12) && s_seg[k0 & 0xFFFu] == s_seg[k1 & 0xFFFu];
-    };
-    uint32_t hm[kScRounds];  // 1 + the last head at or before each position (0: none)
-    uint32_t run = 0;
-#pragma unroll
-    for (int r = 0; r < kScRounds; ++r) {
-      const uint32_t q = w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
-      const bool head = q < cnt && (q == 0 || !same_run(sk[q - 1], sk[q]));
-      uint32_t x = wave_incl_max32(head ? q + 1 : 0u);
-      x = x > run ? x : run;
-      run = (uint32_t)__builtin_amdgcn_readlane((int)x, 63);
-      hm[r] = x;
-    }
-    if (lane == 0) s_wl[w] = run;
-    __syncthreads();  // the tail cleared, the waves' last heads
-    uint32_t enter = 0;
-    for (uint32_t q = 0; q < w; ++q) enter = s_wl[q] > enter ? s_wl[q] : enter;
-#pragma unroll
-    for (int r = 0; r < kScRounds; ++r) {
-      const uint32_t q = w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
-      if (q >= cnt) continue;
-      const uint32_t k = sk[q];
-      const uint32_t h = (hm[r] > enter ? hm[r] : enter) - 1u;
-      const uint32_t local = q - h;
-      s_ord[k & 0xFFFu] = local;
-      // the last element of a run of the last context: its run's count
-      if ((flag & kSoCont) && s_seg[k & 0xFFFu] == L && (q + 1 == cnt || !same_run(k, sk[q + 1])) &&
-          (k >> 12) < a.R)
-        tail[k >> 12] = local + 1;
-    }
-    __syncthreads();
-#pragma unroll
-    for (int r = 0; r < kScRounds; ++r) {
-      const uint32_t e = w * (kScRounds * 64) + (uint32_t)r * 64 + lane;
-      if (e >= cnt) continue;
-      const uint32_t local = s_ord[e];
-      // the chunk's first context starts at position 0
-      const bool pending = (flag & kSoPcont) && s_seg[e] == 0;
-      a.ordinal[base + e] = pending ? (kSoPending | local) : local;
-    }
-    __syncthreads();  // LDS reused by the next chunk
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();  // the row is cleared for the next chunk after these reads
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
+  if (__ballot(bad) && lane == 0) sc_flag(a.counters, 2);  // regions must lie below num_regions
 }
 
 __device__ __forceinline__ uint64_t so_chunks(uint64_t n) { return (n + kScTile - 1) / kScTile; }
@@ -1808,10 +1696,16 @@ extern "C" int argus_attr_scope(const argus_scope_config* cfg, const argus_scope
   if (a.fast) {
     const uint64_t chunks = tiles_for(io->max_instances);
     const uint64_t segs = (chunks + kSoSeg - 1) / kSoSeg;
+    // four chunks at a time per block (a wave each), each wave with its row
+    // of R counters
+    const size_t so_lds = (size_t)4 * a.R * sizeof(uint32_t);
+    (void)hipFuncSetAttribute((const void*)k_so_local, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)so_lds);
     hipLaunchKernelGGL(k_so_local,
-                       dim3((uint32_t)std::min<uint64_t>(chunks, persistent_blocks((const void*)k_so_local,
-                                                                                   kScThreads))),
-                       dim3(kScThreads), 0, st, a);
+                       dim3((uint32_t)std::min<uint64_t>((chunks + 3) / 4,
+                                                         persistent_blocks((const void*)k_so_local,
+                                                                           kScThreads))),
+                       dim3(kScThreads), so_lds, st, a);
     const uint64_t cells = segs * a.R;
     hipLaunchKernelGGL(k_so_seg, dim3((uint32_t)((cells + kScThreads - 1) / kScThreads)),
                        dim3(kScThreads), 0, st, a);
