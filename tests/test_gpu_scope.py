@@ -52,6 +52,10 @@ SCOPES = [dict(), dict(iter_lo=1, iter_hi=3), dict(role_mask=3, role_lo=1, role_
 @pytest.mark.parametrize("n,n_ctx,R,tr", [(0, 3, 3, 10), (1, 1, 2, 5), (4095, 5, 7, 3000),
                                           (4097, 9, 300, 4000), (8193, 3, 2, 100),
                                           (30001, 17, 9, 40000), (100000, 64, 700, 1 << 20),
+                                          # 4096 regions: the chunk walk's widest case (a
+                                          # ballot per region bit, 12 of them, and 64 KiB of
+                                          # counters per block)
+                                          (60000, 11, 4096, 80000),
                                           # more than 4096 regions: the whole-array sort path
                                           (20000, 7, 5000, 30000),
                                           # three contexts over ~370 chunks of 4096 instances:
