@@ -625,7 +625,7 @@ __global__ __launch_bounds__(kScThreads) void k_so_local(ScopeArgs a) {
 #pragma unroll
       for (int k = 0; k < kSoBatch; ++k) {
         const uint32_t r0 = b0 + 64u * k;  // the round's first element
-        if (r0 >= cnt) break;
+        if (r0 < cnt) {
         const uint32_t e = r0 + lane;
         const bool in = e < cnt;
         const uint32_t ctx = cx[k], reg = rw[k] & 0xFFFFu;
@@ -663,6 +663,7 @@ __global__ __launch_bounds__(kScThreads) void k_so_local(ScopeArgs a) {
           // the chunk's first context starts at position 0
           const bool pending = (f & kSoPcont) && seg == 0;
           a.ordinal[base + e] = pending ? (kSoPending | local) : local;
+        }
         }
       }
     }
