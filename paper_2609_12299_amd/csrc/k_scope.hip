@@ -1302,10 +1302,13 @@ __global__ __launch_bounds__(kHoThreads) void k_ho_pairs(HandoffArgs a) {
     uint32_t par = kNoParent;
     if (ok) {
       const uint64_t x = a.comp[k], y = a.comp[k + 1];
+      // both instances loaded together (y is at level L for nearly every
+      // pair), not x after y's test
       const uint4 ya = inst[2 * y], yb = inst[2 * y + 1];
+      const uint4 xa = inst[2 * x], xb = inst[2 * x + 1];
+      asm volatile("" ::"v"(yb.z), "v"(xb.z));
       ok = yb.z == a.L;
       if (ok) {
-        const uint4 xa = inst[2 * x], xb = inst[2 * x + 1];
         const uint32_t rx = xb.w & 0xFFFFu, ry = yb.w & 0xFFFFu;
         ok = xb.z == a.L && xb.x == yb.x && xb.y == yb.y &&  // level, context, parent
              (xb.w >> 16) != kNoEnd && rx < a.R && ry < a.R;
