@@ -169,22 +169,25 @@ __global__ __launch_bounds__(256) void k_resolve(ResolveArgs a) {
       flag_internal_error(a.counters, 64);
       continue;
     }
+    // the instance's own fields, in flight during the tree walk
+    argus_instance* x = a.inst + id;
+    const uint64_t t_begin = x->t_begin;
+    const uint32_t xreg = x->region_id, xctx = x->ctx_key, xpar = x->parent;
     const int64_t t2 = first_le(a.tree, a.leaves, t, (int64_t)L);
     if (t2 < 0) continue;  // context ends with the data: unclosed
     const TileDesc d2 = a.tiles[t2];
-    if (L < d2.lo_head || L - d2.lo_head >= d2.n_pop) continue;  // context ended: unclosed
+    // bitwise: both bounds loaded together
+    if ((L < d2.lo_head) | (L - d2.lo_head >= d2.n_pop)) continue;  // context ended: unclosed
     const uint64_t q = (uint64_t)t2 * kMatchTile + (L - d2.lo_head);
     const uint64_t t_end = a.pop_ts[q];
     const uint32_t ereg = a.pop_reg[q];
-    argus_instance* x = a.inst + id;
     x->t_end = t_end;
     x->end_region_id = (uint16_t)ereg;
-    const uint64_t t_begin = x->t_begin;
     const uint64_t incl = t_end - t_begin;
-    if (ev_on && ereg == x->region_id) {
+    if (ev_on && ereg == xreg) {
       // both events of a classified instance of a group < G
       const uint32_t cls = a.region_class[ereg];
-      const uint64_t g = a.shift >= 32 ? 0u : (x->ctx_key >> a.shift);
+      const uint64_t g = a.shift >= 32 ? 0u : (xctx >> a.shift);
       const uint32_t pb = a.push_pos[pool + i], pe = a.pop_pos[q];
       if (cls < a.K && g < a.G) {
         if (pb < nv && pe < nv) {
@@ -198,7 +201,7 @@ __global__ __launch_bounds__(256) void k_resolve(ResolveArgs a) {
     }
     // exclusive times in place: its duration in, and out of its parent's
     atomicAdd((unsigned long long*)&a.excl[id], (unsigned long long)incl);
-    uint32_t pf = x->parent;
+    uint32_t pf = xpar;
     if (pf == kNoParent) continue;
     if (pf & kParentPending) pf = L >= 1 ? enclosing(a, t, L - 1) : kNoParent;
     if (pf == kNoParent || pf >= nb) continue;
