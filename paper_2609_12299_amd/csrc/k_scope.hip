@@ -775,7 +775,7 @@ __device__ __forceinline__ bool in_range32(uint64_t v, uint32_t lo, uint32_t hi)
 constexpr uint32_t kScLdsRegions = 1024;  // 12 x 8 B x 1024 = 96 KiB of LDS
 constexpr int kScStatThreads = 1024;
 constexpr int kScCols = 12;               // ARGUS_RS_COUNT .. ARGUS_RS_SELF_NESTED
-constexpr int kScStatItems = 4;           // instances per thread and step
+constexpr int kScStatItems = 2;           // instances per thread and step
 
 template <bool LDS_ROWS>
 __global__ __launch_bounds__(kScStatThreads) void k_sc_stats(ScopeArgs a) {
@@ -796,20 +796,31 @@ __global__ __launch_bounds__(kScStatThreads) void k_sc_stats(ScopeArgs a) {
   };
   uint32_t c_in = 0, c_m = 0, c_mm = 0, c_u = 0, c_s = 0, best = 0;
   // kScStatItems instances per thread and step: their instance and ordinal
-  // loads together, then (in scope and matched only) the exclusive times and
-  // parents' regions together
+  // loads together, issued one step ahead; then (in scope and matched only)
+  // the exclusive times and parents' regions together
   const uint64_t step = (uint64_t)gridDim.x * kScStatThreads;
-  for (uint64_t x0 = (uint64_t)blockIdx.x * kScStatThreads + threadIdx.x; x0 < n;
-       x0 += step * kScStatItems) {
+  const uint64_t first = (uint64_t)blockIdx.x * kScStatThreads + threadIdx.x;
+  uint4 p0[kScStatItems], p1[kScStatItems];
+  uint32_t pord[kScStatItems];
+  auto issue = [&](uint64_t xs) {
+#pragma unroll
+    for (int j = 0; j < kScStatItems; ++j) {
+      const uint64_t x = xs + j * step;
+      const uint64_t xc = x < n ? x : n - 1;
+      p0[j] = inst[2 * xc];
+      p1[j] = inst[2 * xc + 1];
+      pord[j] = a.ordinal[xc];
+    }
+  };
+  if (first < n) issue(first);
+  for (uint64_t x0 = first; x0 < n; x0 += step * kScStatItems) {
     uint4 h0[kScStatItems], h1[kScStatItems];
     uint32_t ord[kScStatItems];
 #pragma unroll
     for (int j = 0; j < kScStatItems; ++j) {
-      const uint64_t x = x0 + j * step;
-      const uint64_t xc = x < n ? x : n - 1;
-      h0[j] = inst[2 * xc];
-      h1[j] = inst[2 * xc + 1];
-      ord[j] = a.ordinal[xc];
+      h0[j] = p0[j];
+      h1[j] = p1[j];
+      ord[j] = pord[j];
     }
     bool in[kScStatItems];
     uint64_t exv[kScStatItems];
@@ -837,6 +848,9 @@ __global__ __launch_bounds__(kScStatThreads) void k_sc_stats(ScopeArgs a) {
       preg[j] = mt && par != kNoParent && par < n ? (inst[2 * (uint64_t)par + 1].w & 0xFFFFu)
                                                   : 0xFFFFFFFFu;
     }
+    // the next step's loads, issued after this step's dependent loads (a
+    // wait for a load also waits for every load issued before it)
+    if (x0 + step * kScStatItems < n) issue(x0 + step * kScStatItems);
 #pragma unroll
     for (int j = 0; j < kScStatItems; ++j) {
     const uint64_t x = x0 + j * step;
