@@ -132,27 +132,37 @@ __global__ __launch_bounds__(512, 4) void k_agg(AggArgs a) {
   }
   uint64_t n_m = 0, n_mm = 0, n_u = 0, n_sn = 0, n_ev = 0, n_skip = 0;
   unsigned long long* rs = (unsigned long long*)a.rstats;
-  // Each wave takes 4 x 64 consecutive instances per step, with their loads
-  // (and then the parents' regions) in flight together; every lane of a
-  // wave iterates the same number of times (the event histograms use
-  // ballots).
-  constexpr int B = 4;
+  // Each wave takes 2 x 64 consecutive instances per step, with their loads
+  // (and then the parents' regions) in flight together, and the next step's
+  // loads issued before this step's statistics; every lane of a wave
+  // iterates the same number of times (the event histograms use ballots).
+  constexpr int B = 2;
   const uint32_t lane = threadIdx.x & 63;
   const uint64_t stride = (uint64_t)gridDim.x * NT * B;
-  for (uint64_t wb = ((uint64_t)blockIdx.x * (NT / 64) + (threadIdx.x >> 6)) * (64 * B); wb < nb;
-       wb += stride) {
+  const uint64_t wfirst = ((uint64_t)blockIdx.x * (NT / 64) + (threadIdx.x >> 6)) * (64 * B);
+  argus_instance pxs[B];
+  uint64_t pcs[B];
+  auto issue = [&](uint64_t wbs) {
+#pragma unroll
+    for (int j = 0; j < B; ++j) {
+      const uint64_t id = wbs + (uint64_t)j * 64 + lane;
+      const uint64_t ic = id < nb ? id : nb - 1;
+      pxs[j] = a.inst[ic];
+      pcs[j] = a.excl[ic];
+    }
+  };
+  if (wfirst < nb) issue(wfirst);
+  for (uint64_t wb = wfirst; wb < nb; wb += stride) {
     argus_instance xs[B];
     uint64_t cs[B];
     uint32_t par[B];
     uint16_t preg[B];
 #pragma unroll
     for (int j = 0; j < B; ++j) {
-      const uint64_t id = wb + (uint64_t)j * 64 + lane;
-      const uint64_t ic = id < nb ? id : nb - 1;
-      xs[j] = a.inst[ic];
-      cs[j] = a.excl[ic];
+      xs[j] = pxs[j];
+      cs[j] = pcs[j];
     }
-    // Parents in earlier tiles (agg_parent's reading), the four instances'
+    // Parents in earlier tiles (agg_parent's reading), the instances'
     // loads issued together at each of two steps: tile bounds, then the
     // enclosing-instance entry.  A lane without such a parent reads tile 0
     // and entry 0, which exist whenever the loop runs, and drops the value.
@@ -197,6 +207,8 @@ __global__ __launch_bounds__(512, 4) void k_agg(AggArgs a) {
         rcl[j] = a.region_class[rg < a.R ? rg : 0u];
       }
     }
+    // the next step's loads, issued after this step's dependent loads
+    if (wb + stride < nb) issue(wb + stride);
 #pragma unroll
     for (int j = 0; j < B; ++j) {
     const uint64_t id = wb + (uint64_t)j * 64 + lane;
