@@ -330,24 +330,6 @@ __global__ __launch_bounds__(kScThreads) void k_sort_scatter(SortBufs s, int in,
   }
 }
 
-// First position in [0, hi) of the sorted (a, b >> 32) sequence that is not
-// less than (key, ctx).
-__device__ __forceinline__ uint64_t sb_lower(const uint64_t* ka, const uint64_t* kb, uint64_t hi,
-                                             uint64_t key, uint32_t ctx) {
-  uint64_t lo = 0;
-  while (lo < hi) {
-    const uint64_t mid = (lo + hi) >> 1;
-    const uint64_t am = ka[mid];
-    const uint32_t cm = (uint32_t)(kb[mid] >> 32);
-    // bitwise, not short-circuit: both words are loaded before either is
-    // compared, one round trip per level instead of two
-    const bool less = (am < key) | ((am == key) & (cm < ctx));
-    if (less) lo = mid + 1;
-    else hi = mid;
-  }
-  return lo;
-}
-
 // Scope counters: slot 7 holds internal-error bits (zero unless a
 // consistency check inside the library fails).
 __device__ __forceinline__ void sc_flag(uint64_t* counters, uint64_t code) {
@@ -965,17 +947,16 @@ __global__ __launch_bounds__(kScThreads) void k_pr_join(ProbeArgs a) {
   uint32_t bad = 0, joined = 0, unjoined = 0;
   // the OR and the AND of the sort words (latency; instance code << 32)
   uint64_t oa = 0, na = ~0ull, ob = 0, nb2 = ~0ull;
-  for (uint64_t j = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; j < a.np;
-       j += (uint64_t)gridDim.x * kScThreads) {
-    const uint4 h0 = a.probes[2 * j], h1 = a.probes[2 * j + 1];
-    const uint64_t ts = (uint64_t)h0.x | ((uint64_t)h0.y << 32);
-    const uint64_t te = (uint64_t)h0.z | ((uint64_t)h0.w << 32);
-    const uint32_t ctx = h1.x, it = h1.y, op = h1.z & 0xFFFFu;
+  // Two probes per thread (j and j + stride), their reference searches in
+  // lockstep: each search is a chain of dependent loads, and two chains per
+  // lane keep more in flight.
+  const uint64_t stride = (uint64_t)gridDim.x * kScThreads;
+  auto finish = [&](uint64_t j, uint64_t ts, uint64_t te, uint32_t ctx, uint32_t op, bool ok,
+                    uint64_t tgt) {
     uint64_t code = a.none, lat = 0, done = kU64Max;
-    if (te < ts || op >= a.R) {
+    if (!ok) {
       bad += 1;
     } else {
-      const uint64_t tgt = sb_lower(ra, rb, nref, op, ctx) + it;
       // both words of the target loaded together (index clamped; nref == 0
       // loads nothing)
       uint64_t av = ~0ull, bv = 0;
@@ -1003,6 +984,37 @@ __global__ __launch_bounds__(kScThreads) void k_pr_join(ProbeArgs a) {
     na &= lat;
     ob |= code << 32;
     nb2 &= code << 32;
+  };
+  for (uint64_t j = (uint64_t)blockIdx.x * kScThreads + threadIdx.x; j < a.np; j += 2 * stride) {
+    const uint64_t j1 = j + stride;
+    const bool has1 = j1 < a.np;
+    const uint4 g0 = a.probes[2 * j], g1 = a.probes[2 * j + 1];
+    const uint4 q0 = a.probes[2 * (has1 ? j1 : j)], q1 = a.probes[2 * (has1 ? j1 : j) + 1];
+    const uint64_t ts0 = (uint64_t)g0.x | ((uint64_t)g0.y << 32), te0 = (uint64_t)g0.z | ((uint64_t)g0.w << 32);
+    const uint64_t ts1 = (uint64_t)q0.x | ((uint64_t)q0.y << 32), te1 = (uint64_t)q0.z | ((uint64_t)q0.w << 32);
+    const uint32_t ctx0 = g1.x, it0 = g1.y, op0 = g1.z & 0xFFFFu;
+    const uint32_t ctx1 = q1.x, it1 = q1.y, op1 = q1.z & 0xFFFFu;
+    const bool ok0 = !(te0 < ts0 || op0 >= a.R), ok1 = has1 && !(te1 < ts1 || op1 >= a.R);
+    uint64_t lo0 = 0, hi0 = ok0 ? nref : 0, lo1 = 0, hi1 = ok1 ? nref : 0;
+    while ((lo0 < hi0) | (lo1 < hi1)) {
+      const bool c0 = lo0 < hi0, c1 = lo1 < hi1;
+      const uint64_t m0 = (lo0 + hi0) >> 1, m1 = (lo1 + hi1) >> 1;
+      const uint64_t r0 = c0 ? m0 : 0, r1 = c1 ? m1 : 0;  // a finished chain reads element 0
+      const uint64_t am0 = ra[r0], am1 = ra[r1];
+      const uint32_t cm0 = (uint32_t)(rb[r0] >> 32), cm1 = (uint32_t)(rb[r1] >> 32);
+      const bool less0 = (am0 < op0) | ((am0 == op0) & (cm0 < ctx0));
+      const bool less1 = (am1 < op1) | ((am1 == op1) & (cm1 < ctx1));
+      if (c0) {
+        if (less0) lo0 = m0 + 1;
+        else hi0 = m0;
+      }
+      if (c1) {
+        if (less1) lo1 = m1 + 1;
+        else hi1 = m1;
+      }
+    }
+    finish(j, ts0, te0, ctx0, op0, ok0, lo0 + it0);
+    if (has1) finish(j1, ts1, te1, ctx1, op1, ok1, lo1 + it1);
   }
   {
     // the block's OR and AND, combined over the blocks by k_pr_vary
@@ -1811,7 +1823,7 @@ extern "C" int argus_attr_probes(const argus_probes_config* cfg, const argus_pro
   hipLaunchKernelGGL(k_pr_init, dim3(1), dim3(64), 0, st, a);
   if (a.np > 0) {
     a.ref_buf = sort_reference(a.ref, a.R, st);
-    const uint32_t jb = sc_grid(a.np, kScThreads, 4096);
+    const uint32_t jb = sc_grid(a.np, 2 * kScThreads, 4096);  // two probes per thread
     hipLaunchKernelGGL(k_pr_join, dim3(jb), dim3(kScThreads), 0, st, a);
     hipLaunchKernelGGL(k_pr_vary, dim3(1), dim3(1024), 0, st, a, jb);
     // (instance, latency) order: the latency's eight bytes, then the
